@@ -1,0 +1,422 @@
+/*
+ * Oracle for the SLO- and KV-aware query placement of Aladdin
+ * (Nie, Fonseca, Liu: "Aladdin: Joint Placement and Scaling for SLO-Aware LLM
+ * Serving", arXiv 2405.06856).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This is the plain, slow, single-threaded CPU
+ * reference that the GPU library is checked against.  Only the test suite, the
+ * smoke check and the CPU-baseline leg of the benchmark load it; the product
+ * path never does.  It shares no code, header or table with the GPU library.
+ *
+ * Arithmetic: token counts in int64, latencies in IEEE fp64 with the
+ * parenthesisation written below; build with -ffp-contract=off and without
+ * fast-math so every fp64 result is one correctly rounded operation.
+ *
+ * What is computed, per arriving query q = (l_in, l_pred), in arrival order:
+ *
+ *  KV model, Eq. 1 with h = 1, j = 0: a request with input l_in that has
+ *  generated g tokens holds c = l_in + g tokens and will decode r = l_pred - g
+ *  more iterations.  Constraint (e) with the footprint vector w of Sec. 4.2
+ *  (w = [kv(l_in), kv(l_in+1), ..., kv(l_in+l_pred), 0, ...]) means: at future
+ *  iteration t = 0, 1, ... a request holds c + t tokens while t <= r and none
+ *  afterwards.  The worker's KV demand is the element-wise sum of those vectors
+ *  and must stay <= M at every t.
+ *
+ *  Decode constraint (b): Eq. 4 bounds the batch's total context by
+ *  (T_dec - c3 - c2*b)/k2; with the strictness knob gamma the context of a
+ *  request counts as l_in + gamma*l_out, where (reading of Table 1 and the
+ *  gamma explanation) l_out is split into tokens already generated and tokens
+ *  still to come: D = c + gamma*r.  The check is written multiplied out:
+ *      k2 * sum(D)  <=  theta * ((T_dec - c3) - c2*b),   b = batch size.
+ *
+ *  TTFT constraint (c): the prefill of all requests placed on the worker
+ *  during the current heartbeat (plus q) must finish within T_pre:
+ *      (c1 + k1*S1) + k1q*S2 <= T_pre,  S1 = sum l_in, S2 = sum l_in^2.
+ *  (Eq. 2 is the k1q = 0 case.)
+ *
+ *  Algorithm 1: sort workers by capacity_norm = ||(B, sum(D))||_2 from large
+ *  to small and place q on the first worker meeting (b), (c), (e); the
+ *  comparison is done exactly on the integer 2^(2*gs) * capacity_norm^2 with
+ *  gamma = gn / 2^gs, ties to the lowest worker index.  With a fixed worker
+ *  pool, "open a new bin" is a rejection (worker -1, state unchanged).
+ *
+ *  Heartbeat: after every H processed queries (H > 0) every worker runs one
+ *  decode iteration: c += 1, r -= 1, requests with r < 0 leave, and the
+ *  per-heartbeat prefill sums S1, S2 restart at zero.
+ *
+ * Constraint (d) needs decoding-time history that the workloads do not define
+ * and is not evaluated.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <math.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORA_OK 0
+#define ORA_EINVAL -1
+#define ORA_ENOMEM -2
+#define ORA_EOVERFLOW -3
+#define ORA_ECHECK -4
+
+typedef struct {
+    double c1, k1, k1q;
+    double c3, c2, k2;
+    double ttft_slo, decode_slo;
+    double theta;
+    int32_t gamma_num, gamma_log2den;
+} ora_model_t;
+
+typedef struct {
+    int64_t M;          /* KV capacity in tokens */
+    int64_t n, cap;     /* number of requests, allocated length */
+    int64_t *c, *r;     /* current context, remaining iterations; sorted by r descending */
+    int64_t SC, SR;     /* sum of c and sum of r over the requests */
+    int64_t S1, S2;     /* prefill sums of requests placed in this heartbeat */
+} worker_t;
+
+typedef struct {
+    int rc;
+    int feasible, kv_ok, dec_ok, ttft_ok, near_tie;
+    int64_t peak;
+    double lhs, rhs, ttft, tdec;
+    unsigned __int128 key;
+} pair_t;
+
+/* ------------------------------------------------------------------ */
+/* KV peak: max over t >= 0 of sum over requests alive at t of (c + t).
+ * Between two consecutive remaining lengths the alive set is fixed and the sum
+ * grows with t, so the maximum sits at one of the request end points t = r_j.
+ * The requests are visited in descending r; once every request with r >= t
+ * has been added, the running sums give the demand at t.  The optional extra
+ * request (cq, rq) joins at its own end point. */
+#define DEMAND_AT(t) do { int64_t d_ = sumc + cnt * (t); peak = d_ > peak ? d_ : peak; } while (0)
+static int64_t kv_peak(const worker_t* w, int has_q, int64_t cq, int64_t rq)
+{
+    const int64_t n = w->n;
+    const int64_t* c = w->c;
+    const int64_t* r = w->r;
+    int64_t sumc = 0, cnt = 0, peak = 0;
+    int64_t i = 0;
+    if (has_q) {
+        /* requests that end after q */
+        for (; i < n && r[i] > rq; ++i) {
+            sumc += c[i]; cnt += 1;
+            if (i + 1 == n || r[i + 1] != r[i]) DEMAND_AT(r[i]);
+        }
+        /* q's end point, together with every request ending at the same time */
+        for (; i < n && r[i] == rq; ++i) { sumc += c[i]; cnt += 1; }
+        sumc += cq; cnt += 1;
+        DEMAND_AT(rq);
+    }
+    /* requests that end before q */
+    for (; i < n; ++i) {
+        sumc += c[i]; cnt += 1;
+        if (i + 1 == n || r[i + 1] != r[i]) DEMAND_AT(r[i]);
+    }
+    return peak;
+}
+#undef DEMAND_AT
+
+static int near(double x, double y)
+{
+    double m = fmax(fabs(x), fabs(y));
+    return fabs(x - y) <= 1e-9 * m;
+}
+
+/* One (query, worker) evaluation; returns ORA_EOVERFLOW when an integer
+ * quantity leaves the range where its fp64 conversion is exact. */
+static int eval_pair(const worker_t* w, const ora_model_t* m, int64_t lin, int64_t lpred, pair_t* o)
+{
+    const int gs = m->gamma_log2den;
+    const int64_t gn = m->gamma_num;
+    const int64_t SC = w->SC, SR = w->SR;
+    const int64_t B = w->n;
+    const int64_t b = B + 1;
+
+    /* (e) KV capacity */
+    o->peak = kv_peak(w, 1, lin, lpred);
+    o->kv_ok = o->peak <= w->M;
+
+    /* (b) decode: sum(D) = sum(c) + gamma*sum(r), held exactly as DS * 2^-gs */
+    const int64_t DS = SC * ((int64_t)1 << gs) + gn * SR;
+    const int64_t DSq = DS + lin * ((int64_t)1 << gs) + gn * lpred;
+    if (DSq >= ((int64_t)1 << 53)) return ORA_EOVERFLOW;
+    const double sumD = ldexp((double)DSq, -gs);
+    o->lhs = m->k2 * sumD;
+    o->rhs = m->theta * ((m->decode_slo - m->c3) - m->c2 * (double)b);
+    o->dec_ok = o->lhs <= o->rhs;
+
+    /* (c) TTFT of this heartbeat's prefill batch including q */
+    const int64_t S1 = w->S1 + lin;
+    const int64_t S2 = w->S2 + lin * lin;
+    if (S2 >= ((int64_t)1 << 53)) return ORA_EOVERFLOW;
+    o->ttft = (m->c1 + m->k1 * (double)S1) + m->k1q * (double)S2;
+    o->ttft_ok = o->ttft <= m->ttft_slo;
+
+    o->feasible = o->kv_ok && o->dec_ok && o->ttft_ok;
+    o->tdec = (m->c3 + m->c2 * (double)b) + m->k2 * sumD;
+    o->near_tie = near(o->lhs, o->rhs) || near(o->ttft, m->ttft_slo);
+
+    /* rank key of Algorithm 1, before placement */
+    const unsigned __int128 x = (unsigned __int128)(B * ((int64_t)1 << gs));
+    const unsigned __int128 y = (unsigned __int128)(DS < 0 ? -DS : DS);
+    o->key = x * x + y * y;
+    if (o->key >= ((unsigned __int128)1 << 63)) return ORA_EOVERFLOW;
+    return ORA_OK;
+}
+
+/* (key, -index) comparison: does worker a rank strictly before worker b? */
+static int ranks_before(unsigned __int128 ka, int a, unsigned __int128 kb, int b)
+{
+    if (ka != kb) return ka > kb;
+    return a < b;
+}
+
+static unsigned __int128* g_sort_keys;
+static int cmp_rank(const void* pa, const void* pb)
+{
+    int a = *(const int*)pa, b = *(const int*)pb;
+    if (ranks_before(g_sort_keys[a], a, g_sort_keys[b], b)) return -1;
+    if (ranks_before(g_sort_keys[b], b, g_sort_keys[a], a)) return 1;
+    return 0;
+}
+
+static int add_request(worker_t* w, int64_t c, int64_t r)
+{
+    if (w->n == w->cap) {
+        int64_t nc = w->cap ? 2 * w->cap : 16;
+        int64_t* cc = (int64_t*)realloc(w->c, (size_t)nc * sizeof(int64_t));
+        if (!cc) return ORA_ENOMEM;
+        w->c = cc;
+        int64_t* rr = (int64_t*)realloc(w->r, (size_t)nc * sizeof(int64_t));
+        if (!rr) return ORA_ENOMEM;
+        w->r = rr;
+        w->cap = nc;
+    }
+    /* keep r descending: insert after every request with r >= the new one */
+    int64_t pos = w->n;
+    while (pos > 0 && w->r[pos - 1] < r) pos -= 1;
+    memmove(w->c + pos + 1, w->c + pos, (size_t)(w->n - pos) * sizeof(int64_t));
+    memmove(w->r + pos + 1, w->r + pos, (size_t)(w->n - pos) * sizeof(int64_t));
+    w->c[pos] = c;
+    w->r[pos] = r;
+    w->n += 1;
+    w->SC += c;
+    w->SR += r;
+    return ORA_OK;
+}
+
+static void heartbeat(worker_t* w)
+{
+    int64_t keep = 0, SC = 0, SR = 0;
+    for (int64_t i = 0; i < w->n; ++i) {
+        w->c[i] += 1;
+        w->r[i] -= 1;
+        if (w->r[i] >= 0) { keep = i + 1; SC += w->c[i]; SR += w->r[i]; }  /* finished ones form the tail */
+    }
+    w->n = keep;
+    w->SC = SC;
+    w->SR = SR;
+    w->S1 = 0;
+    w->S2 = 0;
+}
+
+static void free_workers(worker_t* ws, int32_t W)
+{
+    if (!ws) return;
+    for (int32_t i = 0; i < W; ++i) { free(ws[i].c); free(ws[i].r); }
+    free(ws);
+}
+
+static int valid_model(const ora_model_t* m)
+{
+    if (!(isfinite(m->c1) && isfinite(m->k1) && isfinite(m->k1q) && isfinite(m->c3) &&
+          isfinite(m->c2) && isfinite(m->k2) && isfinite(m->ttft_slo) && isfinite(m->decode_slo) &&
+          isfinite(m->theta))) return 0;
+    if (m->gamma_log2den < 0 || m->gamma_log2den > 8) return 0;
+    if (m->gamma_num < 0 || m->gamma_num > (1 << m->gamma_log2den)) return 0;
+    return 1;
+}
+
+/*
+ * Place a stream of queries.
+ *   W workers with capacities M[W]; residents in CSR form (res_off[W+1]) with
+ *   input length, predicted output length and tokens generated so far.
+ *   H: heartbeat period in processed queries (0 = none).
+ *   no_commit: evaluate every query against the initial state and commit
+ *   nothing (used to sample a stream in which no query is ever placed).
+ *   check: also run Algorithm 1 literally (sort by rank, first feasible) and
+ *   verify after each commit that the worker's new KV peak equals the
+ *   evaluated one; returns ORA_ECHECK on any disagreement.
+ *   n_threads: threads for the per-worker evaluations of one query (they are
+ *   independent; every reduction over workers stays sequential).
+ * Outputs (any may be NULL): worker per query (-1 = rejected) and diagnostics;
+ * final per-worker batch size, sum(c), sum(r), KV peak, S1, S2.
+ */
+int ora_place(int32_t W, const int64_t* M, const int64_t* res_off,
+              const int32_t* res_lin, const int32_t* res_lpred, const int32_t* res_g,
+              const ora_model_t* model, int32_t Q, const int32_t* q_lin, const int32_t* q_lpred,
+              int32_t H, int32_t no_commit, int32_t check, int32_t n_threads,
+              int32_t* out_worker, int32_t* out_nfeas, int32_t* out_near_tie,
+              int64_t* out_peak_chosen, int64_t* out_excess_min,
+              double* out_ttft_chosen, double* out_tdec_chosen,
+              int64_t* fin_B, int64_t* fin_SC, int64_t* fin_SR, int64_t* fin_peak,
+              int64_t* fin_S1, int64_t* fin_S2)
+{
+    if (W <= 0 || Q < 0 || H < 0 || !model || !valid_model(model)) return ORA_EINVAL;
+    worker_t* ws = (worker_t*)calloc((size_t)W, sizeof(worker_t));
+    pair_t* pr = (pair_t*)calloc((size_t)W, sizeof(pair_t));
+    int* order = (int*)calloc((size_t)W, sizeof(int));
+    unsigned __int128* keys = (unsigned __int128*)calloc((size_t)W, sizeof(unsigned __int128));
+    int rc = ORA_OK;
+    if (!ws || !pr || !order || !keys) { rc = ORA_ENOMEM; goto done; }
+
+    for (int32_t i = 0; i < W; ++i) {
+        ws[i].M = M[i];
+        for (int64_t k = res_off ? res_off[i] : 0; res_off && k < res_off[i + 1]; ++k) {
+            int64_t lin = res_lin[k], lp = res_lpred[k], g = res_g[k];
+            if (lin < 1 || lp < 1 || g < 0 || g >= lp) { rc = ORA_EINVAL; goto done; }
+            rc = add_request(&ws[i], lin + g, lp - g);
+            if (rc) goto done;
+        }
+    }
+
+    int32_t since_hb = 0;
+    for (int32_t q = 0; q < Q; ++q) {
+        const int64_t lin = q_lin[q], lp = q_lpred[q];
+        if (lin < 1 || lp < 1) { rc = ORA_EINVAL; goto done; }
+        int best = -1;
+        int nfeas = 0;
+        int64_t excess_min = INT64_MAX;
+#ifdef _OPENMP
+#pragma omp parallel for num_threads(n_threads > 0 ? n_threads : 1) schedule(static)
+#endif
+        for (int32_t i = 0; i < W; ++i) pr[i].rc = eval_pair(&ws[i], model, lin, lp, &pr[i]);
+        for (int32_t i = 0; i < W; ++i) {
+            if (pr[i].rc) { rc = pr[i].rc; goto done; }
+            nfeas += pr[i].feasible;
+            int64_t ex = pr[i].peak - ws[i].M;
+            if (ex < excess_min) excess_min = ex;
+            /* exhaustive search: highest (key, -index) among feasible workers */
+            if (pr[i].feasible && (best < 0 || ranks_before(pr[i].key, i, pr[best].key, best))) best = i;
+        }
+        if (check) {
+            /* Algorithm 1 as written: sort bins by capacity_norm, first feasible */
+            for (int32_t i = 0; i < W; ++i) { order[i] = i; keys[i] = pr[i].key; }
+            g_sort_keys = keys;
+            qsort(order, (size_t)W, sizeof(int), cmp_rank);
+            int first = -1;
+            for (int32_t k = 0; k < W; ++k) if (pr[order[k]].feasible) { first = order[k]; break; }
+            if (first != best) { rc = ORA_ECHECK; goto done; }
+        }
+        /* near tie: any worker ranked at or above the choice (all, if rejected)
+         * whose decode or TTFT margin is within 1e-9 relative */
+        int nt = 0;
+        for (int32_t i = 0; i < W; ++i) {
+            if (!pr[i].near_tie) continue;
+            if (best < 0 || i == best || ranks_before(pr[i].key, i, pr[best].key, best)) { nt = 1; break; }
+        }
+        if (out_worker) out_worker[q] = best;
+        if (out_nfeas) out_nfeas[q] = nfeas;
+        if (out_near_tie) out_near_tie[q] = nt;
+        if (out_excess_min) out_excess_min[q] = excess_min;
+        if (out_peak_chosen) out_peak_chosen[q] = best >= 0 ? pr[best].peak : 0;
+        if (out_ttft_chosen) out_ttft_chosen[q] = best >= 0 ? pr[best].ttft : 0.0;
+        if (out_tdec_chosen) out_tdec_chosen[q] = best >= 0 ? pr[best].tdec : 0.0;
+
+        if (best >= 0 && !no_commit) {
+            worker_t* w = &ws[best];
+            rc = add_request(w, lin, lp);
+            if (rc) goto done;
+            w->S1 += lin;
+            w->S2 += lin * lin;
+            if (check && kv_peak(w, 0, 0, 0) != pr[best].peak) { rc = ORA_ECHECK; goto done; }
+        }
+        if (H > 0 && !no_commit) {
+            since_hb += 1;
+            if (since_hb == H) {
+                for (int32_t i = 0; i < W; ++i) heartbeat(&ws[i]);
+                since_hb = 0;
+            }
+        }
+    }
+    for (int32_t i = 0; i < W; ++i) {
+        if (fin_B) fin_B[i] = ws[i].n;
+        if (fin_SC) fin_SC[i] = ws[i].SC;
+        if (fin_SR) fin_SR[i] = ws[i].SR;
+        if (fin_peak) fin_peak[i] = kv_peak(&ws[i], 0, 0, 0);
+        if (fin_S1) fin_S1[i] = ws[i].S1;
+        if (fin_S2) fin_S2[i] = ws[i].S2;
+    }
+done:
+    free_workers(ws, W);
+    free(pr);
+    free(order);
+    free(keys);
+    return rc;
+}
+
+typedef struct {
+    int32_t n_workers;
+    int32_t gpus_per_worker;
+    int64_t kv_capacity;
+    ora_model_t model;
+} ora_scenario_t;
+
+/*
+ * Scaling sweep: every scenario starts with empty workers and places the same
+ * query stream on its own (no heartbeat).  Per scenario: number of rejected
+ * queries and the index of the first rejection (-1 if none); optionally the
+ * full placement (out_worker[s*Q + q]).
+ */
+int ora_sweep(int32_t S, const ora_scenario_t* scen, int32_t Q, const int32_t* q_lin,
+              const int32_t* q_lpred, int32_t n_threads, int32_t* out_rejected,
+              int32_t* out_first_reject, int32_t* out_worker)
+{
+    if (S < 0 || Q < 0) return ORA_EINVAL;
+    int rc_all = ORA_OK;
+    /* scenarios are independent; each one is placed sequentially */
+#ifdef _OPENMP
+#pragma omp parallel for num_threads(n_threads > 0 ? n_threads : 1) schedule(dynamic, 1)
+#endif
+    for (int32_t s = 0; s < S; ++s) {
+        const int32_t W = scen[s].n_workers;
+        int64_t* M = (int64_t*)malloc((size_t)(W > 0 ? W : 1) * sizeof(int64_t));
+        int32_t* tmp = (int32_t*)malloc((size_t)(Q > 0 ? Q : 1) * sizeof(int32_t));
+        int rc = (M && tmp) ? ORA_OK : ORA_ENOMEM;
+        int32_t* dst = out_worker ? out_worker + (int64_t)s * Q : tmp;
+        if (rc == ORA_OK) {
+            for (int32_t i = 0; i < W; ++i) M[i] = scen[s].kv_capacity;
+            rc = ora_place(W, M, NULL, NULL, NULL, NULL, &scen[s].model, Q, q_lin, q_lpred, 0, 0, 0, 1,
+                           dst, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL);
+        }
+        if (rc == ORA_OK) {
+            int32_t rej = 0, first = -1;
+            for (int32_t q = 0; q < Q; ++q) if (dst[q] < 0) { if (first < 0) first = q; rej += 1; }
+            out_rejected[s] = rej;
+            out_first_reject[s] = first;
+        } else {
+#ifdef _OPENMP
+#pragma omp critical
+#endif
+            rc_all = rc;
+        }
+        free(M);
+        free(tmp);
+    }
+    return rc_all;
+}
+
+/* KV peak of an explicit request list (c, r), exposed for the unit tests. */
+int64_t ora_kv_peak(int64_t n, const int64_t* c, const int64_t* r)
+{
+    worker_t w;
+    memset(&w, 0, sizeof w);
+    for (int64_t i = 0; i < n; ++i) if (add_request(&w, c[i], r[i])) return -1;
+    int64_t p = kv_peak(&w, 0, 0, 0);
+    free(w.c); free(w.r);
+    return p;
+}

@@ -1,0 +1,163 @@
+"""ctypes front end of the C oracle (test infrastructure only).
+
+The C source (``aladdin_oracle.c``) holds all of the oracle's arithmetic; this
+module only marshals numpy arrays.  It imports nothing from the GPU package
+except the seeded workload generator.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "aladdin_oracle.c")
+LIB = os.path.join(HERE, "liboracle.so")
+
+ORA_OK, ORA_EINVAL, ORA_ENOMEM, ORA_EOVERFLOW, ORA_ECHECK = 0, -1, -2, -3, -4
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (fp64 without contraction or fast-math)."""
+    if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        tmp = LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=gnu11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-fPIC",
+               "-shared", "-Wall", "-Wextra", "-o", tmp, SRC, "-lm"]
+        subprocess.check_call(cmd)
+        os.replace(tmp, LIB)
+    return LIB
+
+
+class OraModel(ctypes.Structure):
+    _fields_ = [("c1", ctypes.c_double), ("k1", ctypes.c_double), ("k1q", ctypes.c_double),
+                ("c3", ctypes.c_double), ("c2", ctypes.c_double), ("k2", ctypes.c_double),
+                ("ttft_slo", ctypes.c_double), ("decode_slo", ctypes.c_double),
+                ("theta", ctypes.c_double), ("gamma_num", ctypes.c_int32),
+                ("gamma_log2den", ctypes.c_int32)]
+
+
+class OraScenario(ctypes.Structure):
+    _fields_ = [("n_workers", ctypes.c_int32), ("gpus_per_worker", ctypes.c_int32),
+                ("kv_capacity", ctypes.c_int64), ("model", OraModel)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        build()
+        L = ctypes.CDLL(LIB)
+        P = ctypes.c_void_p
+        i32, i64 = ctypes.c_int32, ctypes.c_int64
+        L.ora_place.argtypes = [i32, P, P, P, P, P, ctypes.POINTER(OraModel), i32, P, P, i32, i32, i32,
+                                i32, P, P, P, P, P, P, P, P, P, P, P, P, P]
+        L.ora_place.restype = ctypes.c_int
+        L.ora_sweep.argtypes = [i32, P, i32, P, P, i32, P, P, P]
+        L.ora_sweep.restype = ctypes.c_int
+        L.ora_kv_peak.argtypes = [i64, P, P]
+        L.ora_kv_peak.restype = i64
+        _lib = L
+    return _lib
+
+
+def to_model(m) -> OraModel:
+    return OraModel(m.c1, m.k1, m.k1q, m.c3, m.c2, m.k2, m.ttft_slo, m.decode_slo, m.theta,
+                    m.gamma_num, m.gamma_log2den)
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+@dataclass
+class PlaceResult:
+    worker: np.ndarray          # int32 [Q]
+    n_feasible: np.ndarray      # int32 [Q]
+    near_tie: np.ndarray        # int32 [Q]
+    kv_peak_chosen: np.ndarray  # int64 [Q]
+    kv_excess_min: np.ndarray   # int64 [Q]
+    ttft_chosen: np.ndarray     # float64 [Q]
+    tdec_chosen: np.ndarray     # float64 [Q]
+    B: np.ndarray               # int64 [W] final batch size
+    sum_c: np.ndarray
+    sum_r: np.ndarray
+    peak: np.ndarray
+    S1: np.ndarray
+    S2: np.ndarray
+
+
+def place(W, kv_capacity, res_offsets, res_l_in, res_l_pred, res_generated, model, q_l_in, q_l_pred,
+          heartbeat_every=0, no_commit=False, check=False, n_threads=1) -> PlaceResult:
+    L = lib()
+    Q = int(len(q_l_in))
+    c64 = lambda a: np.ascontiguousarray(a, dtype=np.int64)
+    c32 = lambda a: np.ascontiguousarray(a, dtype=np.int32)
+    M = c64(kv_capacity)
+    off = c64(res_offsets) if res_offsets is not None else None
+    rl, rp, rg = (c32(a) if a is not None else None for a in (res_l_in, res_l_pred, res_generated))
+    ql, qp = c32(q_l_in), c32(q_l_pred)
+    out = PlaceResult(*(np.zeros(Q, t) for t in (np.int32, np.int32, np.int32, np.int64, np.int64,
+                                                 np.float64, np.float64)),
+                      *(np.zeros(W, np.int64) for _ in range(6)))
+    m = to_model(model)
+    rc = L.ora_place(W, _ptr(M), _ptr(off), _ptr(rl), _ptr(rp), _ptr(rg), ctypes.byref(m), Q,
+                     _ptr(ql), _ptr(qp), int(heartbeat_every), int(bool(no_commit)), int(bool(check)),
+                     int(n_threads), _ptr(out.worker), _ptr(out.n_feasible), _ptr(out.near_tie),
+                     _ptr(out.kv_peak_chosen), _ptr(out.kv_excess_min), _ptr(out.ttft_chosen),
+                     _ptr(out.tdec_chosen), _ptr(out.B), _ptr(out.sum_c), _ptr(out.sum_r),
+                     _ptr(out.peak), _ptr(out.S1), _ptr(out.S2))
+    if rc != ORA_OK:
+        raise RuntimeError("oracle ora_place failed with code %d" % rc)
+    return out
+
+
+def place_trace(trace, q_slice=slice(None), **kw) -> PlaceResult:
+    """Run the oracle on a workloads.Trace (optionally on a slice of its queries)."""
+    return place(trace.n_workers, trace.kv_capacity, trace.res_offsets, trace.res_l_in,
+                 trace.res_l_pred, trace.res_generated, trace.model, trace.q_l_in[q_slice],
+                 trace.q_l_pred[q_slice], heartbeat_every=kw.pop("heartbeat_every", trace.heartbeat_every),
+                 **kw)
+
+
+def sweep(scenarios, q_l_in, q_l_pred, want_workers=False, n_threads=1):
+    L = lib()
+    S = len(scenarios)
+    Q = int(len(q_l_in))
+    arr = (OraScenario * max(S, 1))()
+    for i, s in enumerate(scenarios):
+        arr[i] = OraScenario(s.n_workers, s.gpus_per_worker, s.kv_capacity, to_model(s.model))
+    rej = np.zeros(S, np.int32)
+    first = np.zeros(S, np.int32)
+    workers = np.zeros(S * Q, np.int32) if want_workers else None
+    ql = np.ascontiguousarray(q_l_in, dtype=np.int32)
+    qp = np.ascontiguousarray(q_l_pred, dtype=np.int32)
+    rc = L.ora_sweep(S, ctypes.cast(arr, ctypes.c_void_p), Q, _ptr(ql), _ptr(qp), int(n_threads), _ptr(rej),
+                     _ptr(first), _ptr(workers))
+    if rc != ORA_OK:
+        raise RuntimeError("oracle ora_sweep failed with code %d" % rc)
+    return rej, first, (workers.reshape(S, Q) if want_workers else None)
+
+
+def kv_peak(c, r) -> int:
+    c = np.ascontiguousarray(c, dtype=np.int64)
+    r = np.ascontiguousarray(r, dtype=np.int64)
+    return int(lib().ora_kv_peak(len(c), _ptr(c), _ptr(r)))
+
+
+def min_gpus(scenarios, rejected):
+    """Smallest total GPU count (n_workers * gpus_per_worker) over scenarios with
+    no rejection; ties go to the lowest scenario index.  Returns (gpus, index)
+    or (None, -1) when every scenario rejects something."""
+    best, idx = None, -1
+    for i, (s, r) in enumerate(zip(scenarios, rejected)):
+        if r == 0:
+            g = s.n_workers * s.gpus_per_worker
+            if best is None or g < best:
+                best, idx = g, i
+    return best, idx

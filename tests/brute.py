@@ -1,0 +1,113 @@
+"""Brute-force placement written straight from the paper's definitions.
+
+Used only to pin the oracle on tiny inputs.  It is deliberately different in
+form from the oracle:
+
+* KV demand uses the explicit footprint vector of constraint (e) (Sec. 4.2):
+  a request contributes [kv(l_in+g), kv(l_in+g+1), ..., kv(l_in+l_pred), 0, ...]
+  from the current iteration on, with kv(x) = x (Eq. 1, h=1, j=0); the worker
+  demand is the element-wise sum and must stay <= M at every element.
+* The decode constraint (b) is checked in the division form of Eq. 4,
+  sum(l_in + gamma*l_out) <= theta * (T_dec - c3 - c2*b) / k2, in exact
+  rational arithmetic on the fp64 coefficient values.
+* The TTFT constraint (c) is Eq. 2 (plus the quadratic term) in exact rationals.
+* Algorithm 1's ranking uses capacity_norm = hypot(B, sum(D)) in fp64, sorted
+  large to small with ties to the lower index, then the first feasible worker.
+* A heartbeat drops the first element of every footprint vector (one decode
+  iteration has run); empty vectors leave.
+"""
+from __future__ import annotations
+
+import math
+from fractions import Fraction
+from typing import List
+
+
+class Req:
+    __slots__ = ("l_in", "l_pred", "g", "new")
+
+    def __init__(self, l_in, l_pred, g=0, new=False):
+        self.l_in, self.l_pred, self.g, self.new = int(l_in), int(l_pred), int(g), bool(new)
+
+    def footprint(self) -> List[int]:
+        return [self.l_in + k for k in range(self.g, self.l_pred + 1)]
+
+
+def demand_peak(vectors: List[List[int]]) -> int:
+    K = max((len(v) for v in vectors), default=0)
+    tot = [0] * K
+    for v in vectors:
+        for k, x in enumerate(v):
+            tot[k] += x
+    return max(tot, default=0)
+
+
+class BruteWorker:
+    def __init__(self, M, reqs=()):
+        self.M = int(M)
+        self.vecs = [r.footprint() for r in reqs]
+        # per request: (context-now, remaining, l_in, is_new)
+        self.meta = [[r.l_in + r.g, r.l_pred - r.g, r.l_in, False] for r in reqs]
+
+    def heartbeat(self):
+        keep_v, keep_m = [], []
+        for v, m in zip(self.vecs, self.meta):
+            v = v[1:]
+            if v:
+                keep_v.append(v)
+                keep_m.append([m[0] + 1, m[1] - 1, m[2], False])
+        self.vecs, self.meta = keep_v, keep_m
+
+    def batch(self):
+        return len(self.vecs)
+
+
+def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0):
+    """Per query a dict: chosen worker (-1 = none), n_feasible, per-worker KV
+    peaks and a flag telling whether any exact latency margin is so small that
+    fp64 rounding could decide it (those queries are not comparable bit for bit)."""
+    gamma = Fraction(model.gamma_num, 2 ** model.gamma_log2den)
+    F = Fraction
+    out = []
+    since = 0
+    for (l_in, l_pred) in queries:
+        q = Req(l_in, l_pred, 0, True)
+        qv = q.footprint()
+        feas, norms, peaks = [], [], []
+        close = False
+        for w in workers:
+            b = w.batch() + 1
+            peak = demand_peak(w.vecs + [qv])
+            kv_ok = peak <= w.M
+            # sum of (l_in + gamma * l_out) with l_out split into generated (counted
+            # fully, it is already in the context) and remaining (weighted by gamma)
+            sumD = sum(F(c) + gamma * F(r) for c, r, _, _ in w.meta) + F(l_in) + gamma * F(l_pred)
+            ld = (F(model.decode_slo) - F(model.c3) - F(model.c2) * b) / F(model.k2)
+            dec_ok = sumD <= F(model.theta) * ld
+            S1 = sum(F(li) for _, _, li, new in w.meta if new) + F(l_in)
+            S2 = sum(F(li) ** 2 for _, _, li, new in w.meta if new) + F(l_in) ** 2
+            ttft = F(model.c1) + F(model.k1) * S1 + F(model.k1q) * S2
+            ttft_ok = ttft <= F(model.ttft_slo)
+            lim = F(model.theta) * ld
+            if abs(lim - sumD) <= F(1, 10 ** 9) * max(abs(lim), abs(sumD)) or \
+               abs(F(model.ttft_slo) - ttft) <= F(1, 10 ** 9) * max(abs(ttft), abs(F(model.ttft_slo))):
+                close = True
+            feas.append(kv_ok and dec_ok and ttft_ok)
+            sumD_now = sum(F(c) + gamma * F(r) for c, r, _, _ in w.meta)
+            norms.append(math.hypot(float(w.batch()), float(sumD_now)))
+            peaks.append(peak)
+        order = sorted(range(len(workers)), key=lambda i: (-norms[i], i))
+        chosen = next((i for i in order if feas[i]), -1)
+        if chosen >= 0:
+            w = workers[chosen]
+            w.vecs.append(qv)
+            w.meta.append([l_in, l_pred, l_in, True])
+        out.append({"worker": chosen, "n_feasible": sum(feas), "peaks": peaks, "norms": norms,
+                    "close": close})
+        if heartbeat_every:
+            since += 1
+            if since == heartbeat_every:
+                for w in workers:
+                    w.heartbeat()
+                since = 0
+    return out

@@ -1,0 +1,254 @@
+"""Pins of the CPU oracle against the paper and against mathematics (no GPU).
+
+Each test checks the oracle against something other than itself: a value the
+paper prints, a closed form, the explicit footprint-vector definition of
+constraint (e), Eq. 3/Eq. 4 evaluated in exact rationals, or Algorithm 1 run
+literally with a floating-point capacity_norm.
+"""
+from __future__ import annotations
+
+import dataclasses
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import ref
+from paper_2405_06856_amd import workloads as wl
+from tests.brute import BruteWorker, Req, brute_place, demand_peak
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+# A model whose latency constraints never bind (only constraint (e) matters).
+FREE = wl.Model(c1=0.0, k1=0.0, k1q=0.0, c3=0.0, c2=0.0, k2=1e-12, ttft_slo=1e9, decode_slo=1e9)
+
+
+def run(W, M, residents, model, queries, H=0, check=True):
+    """residents: list per worker of (l_in, l_pred, g)."""
+    off = np.zeros(W + 1, np.int64)
+    rl, rp, rg = [], [], []
+    for i in range(W):
+        for (a, b, g) in residents[i]:
+            rl.append(a); rp.append(b); rg.append(g)
+        off[i + 1] = len(rl)
+    q = np.array(queries, np.int32).reshape(-1, 2)
+    return ref.place(W, np.full(W, M, np.int64) if np.isscalar(M) else np.asarray(M, np.int64), off,
+                     np.array(rl, np.int32), np.array(rp, np.int32), np.array(rg, np.int32), model,
+                     q[:, 0], q[:, 1], heartbeat_every=H, check=check)
+
+
+# --------------------------------------------------------------------------- paper's worked example
+def test_fig3_worked_example():
+    fx = json.load(open(os.path.join(GOLDEN, "fig3_example.json")))
+    pr, dv = fx["printed"], fx["derived"]
+    LP, LO = tuple(dv["long_prompt"]), tuple(dv["long_output"])
+    kinds = {"long_prompt": LP, "long_output": LO}
+    queries = [kinds[k] for k in pr["arrival_order"]]
+    M = pr["kv_capacity"]
+    # JSQ as described: prompts together, outputs together
+    assert ref.kv_peak([LP[0], LP[0]], [LP[1], LP[1]]) == pr["jsq_peak_each_worker"]
+    assert ref.kv_peak([LO[0], LO[0]], [LO[1], LO[1]]) == pr["jsq_peak_each_worker"]
+    assert pr["jsq_peak_each_worker"] > M
+    # Algorithm 1 with only the KV constraint binding reaches the printed best placement
+    res = run(pr["n_workers"], M, [[], []], FREE, queries)
+    assert list(res.worker) == [0, 0, 1, 1]
+    assert list(res.peak) == [pr["best_peak_each_worker"]] * 2
+    assert all(p <= M for p in res.peak)
+
+
+# --------------------------------------------------------------------------- KV peak
+def test_peak_equals_footprint_vector_sum():
+    rng = np.random.default_rng(11)
+    for _ in range(3000):
+        n = int(rng.integers(0, 7))
+        reqs = [Req(rng.integers(1, 9), rng.integers(1, 9)) for _ in range(n)]
+        for r in reqs:
+            r.g = int(rng.integers(0, r.l_pred))
+        want = demand_peak([r.footprint() for r in reqs])
+        got = ref.kv_peak([r.l_in + r.g for r in reqs], [r.l_pred - r.g for r in reqs])
+        assert got == want
+
+
+def test_lone_request_peak_closed_form():
+    # a lone new request peaks at its last iteration: l_in + l_pred
+    for lin, lp in [(1, 1), (4, 1), (1, 4), (300, 17), (32768, 4096)]:
+        res = run(1, 10 ** 9, [[]], FREE, [(lin, lp)])
+        assert res.kv_peak_chosen[0] == lin + lp
+        assert res.peak[0] == lin + lp
+
+
+def test_peak_ties_and_exact_capacity():
+    # equal remaining lengths: all alive until the common end point
+    assert ref.kv_peak([5, 7, 9], [3, 3, 3]) == (5 + 3) + (7 + 3) + (9 + 3)
+    # capacity exactly reached is allowed (<= M), one more token is not
+    res = run(1, 10, [[]], FREE, [(4, 1), (1, 4)])      # peak 7 after both
+    assert list(res.worker) == [0, 0]
+    res = run(1, 6, [[]], FREE, [(4, 1), (1, 4)])
+    assert list(res.worker) == [0, -1]
+    assert res.kv_excess_min[1] == 7 - 6
+
+
+# --------------------------------------------------------------------------- whole placement vs brute force
+def _random_model(rng):
+    # coefficients chosen so that each constraint binds for some of the tiny cases
+    return wl.Model(c1=float(rng.uniform(0.0, 0.2)), k1=float(rng.uniform(0.005, 0.05)),
+                    k1q=float(rng.choice([0.0, rng.uniform(0.0, 0.005)])),
+                    c3=float(rng.uniform(0.0, 0.1)), c2=float(rng.uniform(0.0, 0.05)),
+                    k2=float(rng.uniform(0.002, 0.02)), ttft_slo=float(rng.uniform(0.3, 1.5)),
+                    decode_slo=float(rng.uniform(0.2, 0.6)), theta=float(rng.choice([1.0, 0.75, 0.5])),
+                    gamma_num=int(rng.integers(0, 3)), gamma_log2den=1)
+
+
+@pytest.mark.parametrize("H", [0, 1, 3])
+def test_placement_matches_bruteforce(H):
+    rng = np.random.default_rng(100 + H)
+    compared = 0
+    for case in range(400):
+        W = int(rng.integers(1, 5))
+        model = _random_model(rng)
+        residents = []
+        for _ in range(W):
+            rs = []
+            for _ in range(int(rng.integers(0, 6))):
+                lp = int(rng.integers(1, 9))
+                rs.append((int(rng.integers(1, 9)), lp, int(rng.integers(0, lp))))
+            residents.append(rs)
+        M = [int(rng.integers(8, 60)) for _ in range(W)]
+        queries = [(int(rng.integers(1, 9)), int(rng.integers(1, 9))) for _ in range(int(rng.integers(1, 12)))]
+        res = run(W, M, residents, model, queries, H=H)
+        bw = [BruteWorker(M[i], [Req(a, b, g) for (a, b, g) in residents[i]]) for i in range(W)]
+        want = brute_place(bw, model, queries, heartbeat_every=H)
+        for k, wq in enumerate(want):
+            if wq["close"]:
+                break  # fp64 rounding may legitimately decide from here on
+            norms = sorted(wq["norms"])
+            if any(0 < b - a <= 1e-12 * b for a, b in zip(norms, norms[1:])):
+                break
+            assert res.worker[k] == wq["worker"], (case, k)
+            assert res.n_feasible[k] == wq["n_feasible"], (case, k)
+            assert res.kv_excess_min[k] == min(p - m for p, m in zip(wq["peaks"], M)), (case, k)
+            if wq["worker"] >= 0:
+                assert res.kv_peak_chosen[k] == wq["peaks"][wq["worker"]]
+            compared += 1
+    assert compared > 1500
+
+
+def test_heartbeat_is_one_iteration_shift():
+    # after one decode iteration the demand seen from the new "now" is the old
+    # demand vector without its first element
+    rng = np.random.default_rng(5)
+    for _ in range(500):
+        rs = []
+        for _ in range(int(rng.integers(1, 7))):
+            lp = int(rng.integers(1, 9))
+            rs.append((int(rng.integers(1, 9)), lp, int(rng.integers(0, lp))))
+        vecs = [Req(a, b, g).footprint() for (a, b, g) in rs]
+        K = max(len(v) for v in vecs)
+        tot = [sum(v[k] if k < len(v) else 0 for v in vecs) for k in range(K)]
+        # one query that fits nowhere (capacity 0) just to trigger the heartbeat
+        res = run(1, 0, [rs], FREE, [(1, 1)], H=1)
+        assert res.worker[0] == -1
+        assert res.peak[0] == max(tot[1:], default=0)
+        assert res.B[0] == sum(1 for v in vecs if len(v) > 1)
+
+
+def test_alg1_sorted_scan_equals_exhaustive_on_workloads():
+    # check=True makes the oracle run Algorithm 1 literally (sort, first
+    # feasible) beside the exhaustive argmax and fail on any difference
+    for name in ("tiny", "medium"):
+        t = wl.make_config(name)
+        ref.place_trace(t, check=True)
+
+
+def test_committed_placements_respect_every_constraint():
+    t = wl.make_config("medium")
+    r = ref.place_trace(t)
+    m = t.model
+    placed = r.worker >= 0
+    assert placed.sum() > 0
+    assert np.all(r.kv_peak_chosen[placed] <= t.kv_capacity[r.worker[placed]])
+    assert np.all(r.ttft_chosen[placed] <= m.ttft_slo)
+    # Eq. 3 form of the decode check at theta = 1: T_d <= T_dec
+    assert m.theta == 1.0
+    assert np.all(r.tdec_chosen[placed] <= m.decode_slo * (1 + 1e-12))
+    # no worker ends above capacity unless its residents already put it there
+    start = ref.place_trace(t, q_slice=slice(0, 0))
+    assert np.all(r.peak <= np.maximum(t.kv_capacity, start.peak))
+    assert np.all(r.peak[start.peak <= t.kv_capacity] <= t.kv_capacity[start.peak <= t.kv_capacity])
+
+
+def test_rejected_queries_leave_state_unchanged():
+    t = wl.make_config("tiny")
+    r = ref.place_trace(t)
+    keep = r.worker >= 0
+    # dropping the rejected queries from the stream changes nothing
+    r2 = ref.place(t.n_workers, t.kv_capacity, t.res_offsets, t.res_l_in, t.res_l_pred, t.res_generated,
+                   t.model, t.q_l_in[keep], t.q_l_pred[keep])
+    assert np.array_equal(r2.worker, r.worker[keep])
+    for f in ("B", "sum_c", "sum_r", "peak", "S1", "S2"):
+        assert np.array_equal(getattr(r2, f), getattr(r, f))
+
+
+def test_monotone_within_heartbeat():
+    # a commit never lowers B, sum(D), S1, S2 or the peak, so a worker that was
+    # infeasible for a query stays infeasible: evaluating a query at the
+    # initial state admits at least as many workers as at any later state
+    t = wl.make_config("medium")
+    at_start = ref.place_trace(t, no_commit=True)
+    seq = ref.place_trace(t)
+    assert np.all(seq.n_feasible <= at_start.n_feasible)
+    assert np.all(seq.kv_excess_min >= at_start.kv_excess_min)
+
+
+def test_decode_margin_exactly_zero_is_feasible_and_near_tie():
+    # k2 * sumD == theta*((T_dec - c3) - c2*b) exactly: lhs <= rhs holds
+    m = dataclasses.replace(FREE, c3=0.0, c2=0.0, k2=0.5, decode_slo=5.0, theta=1.0, gamma_num=0)
+    # sumD = l_in = 10 -> lhs = 5.0 = rhs
+    res = run(1, 10 ** 6, [[]], m, [(10, 3), (1, 1)])
+    assert res.worker[0] == 0 and res.near_tie[0] == 1
+    assert res.worker[1] == -1 and res.near_tie[1] == 0
+
+
+def test_ttft_margin_exactly_zero_is_feasible():
+    m = dataclasses.replace(FREE, c1=0.5, k1=0.25, k1q=0.0, ttft_slo=3.0)
+    res = run(2, 10 ** 6, [[], []], m, [(10, 2), (1, 1)])
+    assert res.worker[0] == 0 and res.ttft_chosen[0] == 3.0 and res.near_tie[0] == 1
+    # the first worker's prefill budget is used up; the second one takes it
+    assert res.worker[1] == 1
+
+
+def test_capacity_norm_ranking_picks_fullest_feasible():
+    # worker 1 holds more context -> ranked first; worker 0 chosen only when 1 is full
+    res = run(2, [100, 30], [[(2, 2, 0)], [(10, 5, 0)]], FREE, [(3, 3), (3, 3), (3, 3)])
+    assert list(res.worker) == [1, 1, 0]
+
+
+def test_sweep_equals_independent_places():
+    s = wl.make_sweep("mini", 9, Q=300, worker_counts=(2, 3, 5), gpu_counts=(1, 2), base_capacity=6000,
+                      model=wl.BASE_MODEL, in_dist=wl.MID_IN, out_dist=wl.MID_OUT, rate=None)
+    rej, first, workers = ref.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True, n_threads=2)
+    for i, sc in enumerate(s.scenarios):
+        r = ref.place(sc.n_workers, np.full(sc.n_workers, sc.kv_capacity, np.int64), None, None, None, None,
+                      sc.model, s.q_l_in, s.q_l_pred)
+        assert np.array_equal(r.worker, workers[i])
+        assert rej[i] == int((r.worker < 0).sum())
+        neg = np.flatnonzero(r.worker < 0)
+        assert first[i] == (int(neg[0]) if len(neg) else -1)
+    assert rej.min() < rej.max()
+
+
+def test_threads_do_not_change_results():
+    t = wl.make_config("medium")
+    a = ref.place_trace(t, n_threads=1)
+    b = ref.place_trace(t, n_threads=4)
+    for f in ("worker", "n_feasible", "near_tie", "kv_peak_chosen", "kv_excess_min", "ttft_chosen",
+              "tdec_chosen", "B", "peak"):
+        assert np.array_equal(getattr(a, f), getattr(b, f))
+
+
+def test_invalid_inputs_rejected():
+    with pytest.raises(RuntimeError):
+        run(1, 10, [[(3, 2, 2)]], FREE, [(1, 1)])   # g must be < l_pred
+    with pytest.raises(RuntimeError):
+        run(1, 10, [[]], FREE, [(0, 1)])            # l_in >= 1
