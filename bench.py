@@ -1,0 +1,180 @@
+"""Benchmark of the placement evaluator on one MI355X.
+
+A step is one pass of the placement path over the large workload (512 workers
+with 512 resident requests each, 65536 arriving queries): every (query, worker)
+pair is evaluated (KV peak, decode and TTFT checks), each query is resolved by
+Algorithm 1 and committed in arrival order, diagnostics included.  Inputs and
+worker state are resident in HBM before the timed region.  The same line also
+reports the scaling sweep (256 cluster configurations x 16384 queries) as
+sweeps per second, the roofline position of the pair-evaluation kernel, and the
+CPU oracle timed on a bounded sample on this host.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
+TILE_LARGE = 65536
+
+
+def algorithmic_bytes_per_pair(residents_per_worker: int) -> int:
+    # the two int32 columns the breakpoint rule depends on (remaining length and
+    # context of every resident) plus five int64 worker aggregates
+    return 8 * residents_per_worker + 40
+
+
+def cpu_baseline(trace, budget_s: float = 12.0, max_q: int = 8192):
+    """The oracle as it stands, one thread, on the first n queries of the stream
+    (n doubled until one run takes at least half the budget)."""
+    from oracle import ref
+    ref.build()
+    n = 256
+    while True:
+        t0 = time.perf_counter()
+        ref.place(trace.n_workers, trace.kv_capacity, trace.res_offsets, trace.res_l_in, trace.res_l_pred,
+                  trace.res_generated, trace.model, trace.q_l_in[:n], trace.q_l_pred[:n], n_threads=1)
+        dt = time.perf_counter() - t0
+        if dt >= budget_s / 2 or n >= max_q:
+            break
+        n = min(max_q, 2 * n)
+    return {"value": n * trace.n_workers / dt, "unit": "pair-evals/s", "cores": 1, "kind": "oracle",
+            "sample": "first %d of %d queries x %d workers of the large workload, single thread, "
+                      "%.1f s" % (n, trace.n_queries, trace.n_workers, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--sweep-steps", type=int, default=3)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-sweep", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the evaluator runs on a single device "
+              "(multi-GPU sharding is a design note, not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2405_06856_amd import aladdin
+    from paper_2405_06856_amd import workloads as wl
+
+    dev = torch.device("cuda", 0)
+    trace = wl.make_config("large")
+    R = int(trace.res_offsets[1] - trace.res_offsets[0])
+    W, Q = trace.n_workers, trace.n_queries
+    pairs = W * Q
+
+    ev = aladdin.Evaluator(0, tile=TILE_LARGE)
+    t_load0 = time.perf_counter()
+    ev.load_trace(trace)
+    load_s = time.perf_counter() - t_load0
+    ql = torch.as_tensor(trace.q_l_in, dtype=torch.int32).to(dev)
+    qp = torch.as_tensor(trace.q_l_pred, dtype=torch.int32).to(dev)
+    before = ev.summary()
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        out, dg = ev.place_device(ql, qp, 0, diag=True)
+    torch.cuda.synchronize()
+    # No query of this stream fits anywhere, so the worker state is the same at
+    # the start of every step (checked below).
+    ev.profiling(True)
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(ev.stream)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        out, dg = ev.place_device(ql, qp, 0, diag=True)
+    stop.record(ev.stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = start.elapsed_time(stop)
+    eval_ms, eval_n = ev.kernel_time("eval")
+    sel_ms, sel_n = ev.kernel_time("select")
+    com_ms, com_n = ev.kernel_time("commit")
+    bld_ms, bld_n = ev.kernel_time("build")
+    ev.profiling(False)
+    placed = int((out >= 0).sum().item())
+    after = ev.summary()
+    assert placed == 0 and all(np.array_equal(before[k], after[k]) for k in before), \
+        "state changed during the large-workload steps"
+
+    ms_per_step = gpu_ms / args.steps
+    value = pairs / (ms_per_step / 1e3)
+    eval_avg_ms = eval_ms / max(eval_n, 1)
+    pairs_per_eval_launch = pairs * args.steps / max(eval_n, 1)
+    achieved = algorithmic_bytes_per_pair(R) * pairs_per_eval_launch / (eval_avg_ms / 1e3) / 1e9
+    traffic = None
+    tfile = os.path.join(ROOT, "profiles", "pair_eval_large_traffic.json")
+    if os.path.exists(tfile):
+        try:
+            traffic = json.load(open(tfile)).get("bytes_per_launch")
+        except Exception:
+            traffic = None
+
+    sweep_info = None
+    if not args.no_sweep:
+        sw = wl.make_config("sweep")
+        sev = aladdin.Evaluator(0, tile=1024)
+        rej, first, _ = sev.sweep(sw.scenarios, sw.q_l_in, sw.q_l_pred)  # warm-up
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.sweep_steps):
+            rej, first, _ = sev.sweep(sw.scenarios, sw.q_l_in, sw.q_l_pred)
+        torch.cuda.synchronize()
+        sweep_s = (time.perf_counter() - t0) / args.sweep_steps
+        gpus, idx = aladdin.smallest_feasible_cluster(sw.scenarios, rej)
+        sweep_info = {"sweeps_per_s": 1.0 / sweep_s, "ms_per_sweep": sweep_s * 1e3,
+                      "scenarios": len(sw.scenarios), "queries": sw.n_queries,
+                      "min_total_gpus": gpus, "min_gpus_scenario": idx}
+        sev.close()
+
+    line = {
+        "metric": "query x worker placement evals/sec (+ scenario sweeps/sec; % of HBM roofline)",
+        "value": value,
+        "unit": "pair-evals/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32/int64 tokens + fp64 latencies",
+        "data": "synthetic",
+        "config": {"workload": "large: 512 workers x 512 resident requests, 65536 queries, KV 262144 tokens, "
+                               "lognormal lengths (input mu 6.5 sigma 1.2 [16,8192], output mu 5.5 sigma 1.0 "
+                               "[8,2048]), diagnostics on",
+                   "pairs_per_step": pairs, "tile": TILE_LARGE, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "k_eval (pair evaluation)", "kernel_avg_ms": eval_avg_ms,
+                     "bytes_per_pair": algorithmic_bytes_per_pair(R)},
+        "kernels_ms_per_step": {"build": bld_ms / args.steps, "eval": eval_ms / args.steps,
+                                "select": sel_ms / args.steps, "commit": com_ms / args.steps},
+        "wall_ms_per_step": wall * 1e3 / args.steps,
+        "load_ms": load_s * 1e3,
+        "sweep": sweep_info,
+    }
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(trace)
+    ev.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,157 @@
+/*
+ * libaladdin -- SLO- and KV-aware query placement evaluator for MI355X (gfx950).
+ *
+ * Implements the request-placement path of Aladdin (Nie, Fonseca, Liu: "Aladdin:
+ * Joint Placement and Scaling for SLO-Aware LLM Serving", arXiv 2405.06856):
+ * every arriving query is evaluated against every serving worker and placed by
+ * the best-fit heuristic (Algorithm 1) in arrival order; the same evaluator runs
+ * over many cluster configurations to find the smallest feasible one.
+ *
+ * Placement rule (per query q = (l_in, l_pred), per worker w):
+ *   - constraint (e), KV capacity (Eq. 1 with h = 1, j = 0; footprint vector w of
+ *     Sec. 4.2): a request that has generated g tokens holds c = l_in + g tokens
+ *     and decodes r = l_pred - g more iterations, holding c + t tokens at future
+ *     iteration t <= r.  The worker's demand with q added must stay <= M at
+ *     every t; it is evaluated at the request end points only.
+ *   - constraint (b), decode SLO (Eq. 3/Eq. 4): with b = batch size + 1 and
+ *     D = c + gamma * r per request,
+ *       k2 * sum(D) <= theta * ((T_dec - c3) - c2 * b).
+ *   - constraint (c), TTFT SLO (Eq. 2 plus a quadratic term): over the requests
+ *     placed on w in the current heartbeat plus q,
+ *       (c1 + k1 * sum(l_in)) + k1q * sum(l_in^2) <= T_pre.
+ *   - Algorithm 1: among workers meeting (b), (c), (e), choose the largest
+ *     capacity_norm = ||(B, sum(D))||_2 before placement (compared exactly as an
+ *     integer), ties to the lowest worker index; none -> rejected (-1).
+ *   - heartbeat: after every H processed queries each worker runs one decode
+ *     iteration (c += 1, r -= 1, finished requests leave) and the TTFT sums of
+ *     constraint (c) restart at zero.
+ * Constraint (d) (prefill preemption slack) is not evaluated.
+ *
+ * Conventions
+ *   - Every array argument except where marked "host" is a DEVICE pointer to
+ *     contiguous memory owned by the caller (e.g. a torch tensor's data_ptr());
+ *     the library never frees caller memory.  Device memory for worker state and
+ *     scratch is allocated by the library inside the handle.
+ *   - All work runs on the stream given to ald_create.  Every call below returns
+ *     after that stream has finished the call's work, so errors are synchronous
+ *     and outputs are ready on return.
+ *   - Return value: ALD_OK (0) or a negative ALD_E* code; ald_last_error() gives
+ *     a message.  On a validation error nothing is written to the outputs and
+ *     the handle's worker state is unchanged.
+ *   - A handle is used by one host thread at a time.
+ *   - Token counts are integers; latencies are IEEE fp64 evaluated with the
+ *     parenthesisation shown above, without fused multiply-add.  Internally the
+ *     per-request KV bookkeeping is 32-bit; ALD_EOVERFLOW is returned when a
+ *     stream could leave that range (capacities above 2^30 tokens, lengths above
+ *     2^24, or a worker state whose demand could pass 2^31).
+ */
+#ifndef ALADDIN_H
+#define ALADDIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ALD_OK 0
+#define ALD_EINVAL (-1)    /* invalid argument or input value */
+#define ALD_EHIP (-2)      /* HIP runtime error (launch, copy, allocation) */
+#define ALD_ESLOTS (-3)    /* a worker ran out of request slots */
+#define ALD_ESTATE (-4)    /* call order: no workers loaded */
+#define ALD_EOVERFLOW (-5) /* a value would leave the exactly representable range */
+
+typedef struct ald_handle* ald_handle_t;
+
+/* Latency / SLO model of one worker type; all fp64 (host struct, copied). */
+typedef struct {
+    double c1, k1, k1q;        /* prefill: T_p = (c1 + k1*S1) + k1q*S2            (Eq. 2) */
+    double c3, c2, k2;         /* decode:  T_d = (c3 + c2*b) + k2*context          (Eq. 3) */
+    double ttft_slo;           /* T_pre, seconds                                   (Table 1) */
+    double decode_slo;         /* T_dec, seconds per output token; must exceed c3  (Eq. 4) */
+    double theta;              /* prediction-error knob of constraint (b), in (0, 1] */
+    int32_t gamma_num;         /* strictness knob gamma = gamma_num / 2^gamma_log2den, */
+    int32_t gamma_log2den;     /*   0 <= gamma <= 1, gamma_log2den in [0, 8]           */
+} ald_model_t;
+
+/* One cluster configuration of a scaling sweep (host struct). */
+typedef struct {
+    int32_t n_workers;         /* >= 1 */
+    int32_t gpus_per_worker;   /* informational, not used by the evaluator */
+    int64_t kv_capacity;       /* tokens per worker, 1 .. 2^30 */
+    ald_model_t model;
+} ald_scenario_t;
+
+/* Per-query diagnostics (40 bytes, device array of Q). */
+typedef struct {
+    int32_t n_feasible;        /* workers meeting (b), (c), (e) for this query */
+    int32_t near_tie;          /* 1 if a worker ranked at or above the choice (every worker
+                                  when rejected) has a decode or TTFT margin within 1e-9
+                                  relative: fp64 rounding could have decided it */
+    int64_t kv_peak_chosen;    /* KV peak of the chosen worker with q added (0 if rejected) */
+    int64_t kv_excess_min;     /* min over all workers of (KV peak with q) - capacity */
+    double ttft_chosen;        /* prefill time of the chosen worker's batch with q (0 if rejected) */
+    double tdec_chosen;        /* (c3 + c2*b) + k2*sum(D) of the chosen worker (0 if rejected) */
+} ald_query_diag_t;
+
+/* Create a handle on HIP device `device`, launching on `hip_stream`
+ * (a hipStream_t, or NULL for the default stream). */
+int ald_create(ald_handle_t* handle, int device, void* hip_stream);
+
+/* Release the handle and all device memory it allocated.  NULL is accepted. */
+int ald_destroy(ald_handle_t handle);
+
+/* Queries evaluated per speculative tile (default 4096, 64 .. 1048576).  The
+ * result never depends on it; only speed does. */
+int ald_set_tile(ald_handle_t handle, int32_t tile_queries);
+
+/* Load W workers with their ongoing requests (Table 1 inputs), replacing any
+ * previous state.  Device arrays: kv_capacity[W]; res_offsets[W+1] (CSR: worker
+ * i owns residents res_offsets[i] .. res_offsets[i+1]-1, res_offsets[0] = 0);
+ * res_l_in, res_l_pred, res_generated [res_offsets[W]] with l_in >= 1,
+ * l_pred >= 1, 0 <= generated < l_pred.  `model` is a host pointer.
+ * slots_per_worker: request slots kept per worker (0 = derive the bound on the
+ * batch size from constraint (b); required when that bound is infinite). */
+int ald_load_workers(ald_handle_t handle, int32_t W, const ald_model_t* model,
+                     const int64_t* kv_capacity, const int64_t* res_offsets,
+                     const int32_t* res_l_in, const int32_t* res_l_pred,
+                     const int32_t* res_generated, int32_t slots_per_worker);
+
+/* Place Q queries (device arrays q_l_in[Q], q_l_pred[Q], values >= 1) in index
+ * (arrival) order on the loaded workers, committing every placement.  Repeated
+ * calls continue the same stream.  heartbeat_every = H > 0: a heartbeat after
+ * every H processed queries (counted across calls); 0: no heartbeat in this
+ * call.  out_worker[Q] (device): chosen worker or -1.  out_diag[Q] (device) or
+ * NULL. */
+int ald_place_stream(ald_handle_t handle, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
+                     int32_t heartbeat_every, int32_t* out_worker, ald_query_diag_t* out_diag);
+
+/* Scaling sweep: S scenarios (host array scen[S]), each starting with empty
+ * workers, each placing the same Q queries (device arrays) with no heartbeat.
+ * Device outputs: out_rejected[S], out_first_reject[S] (-1 if none) and, if not
+ * NULL, out_worker[S*Q] (row s = placement of scenario s).  The handle's loaded
+ * workers are not touched (no ald_load_workers needed). */
+int ald_sweep_scenarios(ald_handle_t handle, int32_t S, const ald_scenario_t* scen, int32_t Q,
+                        const int32_t* q_l_in, const int32_t* q_l_pred, int32_t* out_rejected,
+                        int32_t* out_first_reject, int32_t* out_worker);
+
+/* Current state of every loaded worker (device arrays of W): batch size, sum of
+ * contexts, sum of remaining lengths, KV peak over future iterations. */
+int ald_worker_summary(ald_handle_t handle, int32_t* B, int64_t* sum_c, int64_t* sum_r, int64_t* peak);
+
+/* Kernel timing with HIP events on the handle's stream (off by default).
+ * kind: 0 = state build, 1 = pair evaluation, 2 = per-query selection,
+ * 3 = commit.  Totals accumulate over calls while enabled; enabling resets them. */
+int ald_set_profiling(ald_handle_t handle, int32_t enable);
+int ald_kernel_time(ald_handle_t handle, int32_t kind, double* total_ms, int64_t* launches);
+
+/* Message for the last error on this handle, or for a code. */
+const char* ald_last_error(ald_handle_t handle);
+const char* ald_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ALADDIN_H */

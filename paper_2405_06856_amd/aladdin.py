@@ -1,0 +1,272 @@
+"""Python binding of libaladdin (argument marshalling only).
+
+Every function named ``ald_*`` forwards to the C-ABI entry point of the same
+name declared in ``include/aladdin.h``; device arrays are passed as torch CUDA
+tensors (PyTorch supplies device memory and the stream, nothing else).  All
+placement arithmetic runs in the HIP kernels of ``libaladdin.so``; there is no
+CPU fallback, and importing this module fails when the library is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libaladdin.so")
+
+ALD_OK, ALD_EINVAL, ALD_EHIP, ALD_ESLOTS, ALD_ESTATE, ALD_EOVERFLOW = 0, -1, -2, -3, -4, -5
+
+KERNEL_KINDS = {"build": 0, "eval": 1, "select": 2, "commit": 3}
+
+
+class AladdinError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__("%s (code %d)" % (msg, code))
+        self.code = code
+
+
+class Model(ctypes.Structure):
+    _fields_ = [("c1", ctypes.c_double), ("k1", ctypes.c_double), ("k1q", ctypes.c_double),
+                ("c3", ctypes.c_double), ("c2", ctypes.c_double), ("k2", ctypes.c_double),
+                ("ttft_slo", ctypes.c_double), ("decode_slo", ctypes.c_double),
+                ("theta", ctypes.c_double), ("gamma_num", ctypes.c_int32),
+                ("gamma_log2den", ctypes.c_int32)]
+
+
+class Scenario(ctypes.Structure):
+    _fields_ = [("n_workers", ctypes.c_int32), ("gpus_per_worker", ctypes.c_int32),
+                ("kv_capacity", ctypes.c_int64), ("model", Model)]
+
+
+DIAG_DTYPE = np.dtype([("n_feasible", "<i4"), ("near_tie", "<i4"), ("kv_peak_chosen", "<i8"),
+                       ("kv_excess_min", "<i8"), ("ttft_chosen", "<f8"), ("tdec_chosen", "<f8")])
+assert DIAG_DTYPE.itemsize == 40
+
+SYMBOLS = ("ald_create", "ald_destroy", "ald_set_tile", "ald_load_workers", "ald_place_stream",
+           "ald_sweep_scenarios", "ald_worker_summary", "ald_set_profiling", "ald_kernel_time",
+           "ald_last_error", "ald_strerror")
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libaladdin.so is not built (run __graft_entry__.build()): %s" % LIB_PATH)
+    L = ctypes.CDLL(LIB_PATH)
+    P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    sig = {
+        "ald_create": ([ctypes.POINTER(P), ctypes.c_int, P], ctypes.c_int),
+        "ald_destroy": ([P], ctypes.c_int),
+        "ald_set_tile": ([P, i32], ctypes.c_int),
+        "ald_load_workers": ([P, i32, ctypes.POINTER(Model), P, P, P, P, P, i32], ctypes.c_int),
+        "ald_place_stream": ([P, i32, P, P, i32, P, P], ctypes.c_int),
+        "ald_sweep_scenarios": ([P, i32, P, i32, P, P, P, P, P], ctypes.c_int),
+        "ald_worker_summary": ([P, P, P, P, P], ctypes.c_int),
+        "ald_set_profiling": ([P, i32], ctypes.c_int),
+        "ald_kernel_time": ([P, i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)], ctypes.c_int),
+        "ald_last_error": ([P], ctypes.c_char_p),
+        "ald_strerror": ([ctypes.c_int], ctypes.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = res
+    return L
+
+
+_L = _load()
+
+
+def _check(h, rc: int):
+    if rc != ALD_OK:
+        msg = _L.ald_last_error(h).decode() if h else _L.ald_strerror(rc).decode()
+        raise AladdinError(rc, msg)
+
+
+def _dptr(t) -> Optional[int]:
+    """Device pointer of a contiguous torch CUDA tensor (None passes NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("expected a device (CUDA/HIP) tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return t.data_ptr()
+
+
+# ----------------------------------------------------------------------------- C-ABI mirrors
+def ald_create(device: int = 0, stream: Optional[int] = None) -> ctypes.c_void_p:
+    h = ctypes.c_void_p()
+    rc = _L.ald_create(ctypes.byref(h), int(device), stream)
+    _check(None, rc)
+    return h
+
+
+def ald_destroy(h) -> None:
+    _L.ald_destroy(h)
+
+
+def ald_set_tile(h, tile_queries: int) -> None:
+    _check(h, _L.ald_set_tile(h, int(tile_queries)))
+
+
+def ald_load_workers(h, W: int, model: Model, kv_capacity, res_offsets, res_l_in, res_l_pred, res_generated,
+                     slots_per_worker: int = 0) -> None:
+    _check(h, _L.ald_load_workers(h, int(W), ctypes.byref(model), _dptr(kv_capacity), _dptr(res_offsets),
+                                  _dptr(res_l_in), _dptr(res_l_pred), _dptr(res_generated),
+                                  int(slots_per_worker)))
+
+
+def ald_place_stream(h, Q: int, q_l_in, q_l_pred, heartbeat_every: int, out_worker, out_diag=None) -> None:
+    _check(h, _L.ald_place_stream(h, int(Q), _dptr(q_l_in), _dptr(q_l_pred), int(heartbeat_every),
+                                  _dptr(out_worker), _dptr(out_diag)))
+
+
+def ald_sweep_scenarios(h, S: int, scen, Q: int, q_l_in, q_l_pred, out_rejected, out_first_reject,
+                        out_worker=None) -> None:
+    _check(h, _L.ald_sweep_scenarios(h, int(S), ctypes.cast(scen, ctypes.c_void_p), int(Q), _dptr(q_l_in),
+                                     _dptr(q_l_pred), _dptr(out_rejected), _dptr(out_first_reject),
+                                     _dptr(out_worker)))
+
+
+def ald_worker_summary(h, B, sum_c, sum_r, peak) -> None:
+    _check(h, _L.ald_worker_summary(h, _dptr(B), _dptr(sum_c), _dptr(sum_r), _dptr(peak)))
+
+
+def ald_set_profiling(h, enable: bool) -> None:
+    _check(h, _L.ald_set_profiling(h, int(bool(enable))))
+
+
+def ald_kernel_time(h, kind: int):
+    ms = ctypes.c_double()
+    n = ctypes.c_int64()
+    _check(h, _L.ald_kernel_time(h, int(kind), ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
+
+
+def ald_last_error(h) -> str:
+    return _L.ald_last_error(h).decode()
+
+
+def ald_strerror(code: int) -> str:
+    return _L.ald_strerror(int(code)).decode()
+
+
+# ----------------------------------------------------------------------------- convenience wrapper
+def to_model(m) -> Model:
+    return Model(m.c1, m.k1, m.k1q, m.c3, m.c2, m.k2, m.ttft_slo, m.decode_slo, m.theta, m.gamma_num,
+                 m.gamma_log2den)
+
+
+@dataclass
+class Placement:
+    worker: np.ndarray                 # int32 [Q]
+    diag: Optional[np.ndarray] = None  # DIAG_DTYPE [Q]
+
+
+class Evaluator:
+    """A handle bound to one device and torch's current stream on it."""
+
+    def __init__(self, device: int = 0, tile: Optional[int] = None):
+        import torch
+        self.torch = torch
+        self.device = torch.device("cuda", device)
+        self.stream = torch.cuda.current_stream(self.device)
+        self.h = ald_create(device, self.stream.cuda_stream)
+        if tile is not None:
+            ald_set_tile(self.h, tile)
+        self.W = 0
+
+    def close(self):
+        if self.h is not None:
+            ald_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _dev(self, a, dtype):
+        t = self.torch
+        return t.as_tensor(np.ascontiguousarray(a), dtype=dtype).to(self.device)
+
+    def load(self, W, model, kv_capacity, res_offsets, res_l_in, res_l_pred, res_generated, slots_per_worker=0):
+        t = self.torch
+        self._keep = [self._dev(kv_capacity, t.int64), self._dev(res_offsets, t.int64),
+                      self._dev(res_l_in, t.int32), self._dev(res_l_pred, t.int32),
+                      self._dev(res_generated, t.int32)]
+        ald_load_workers(self.h, W, to_model(model), *self._keep, slots_per_worker=slots_per_worker)
+        self.W = W
+
+    def load_trace(self, trace, slots_per_worker=0):
+        self.load(trace.n_workers, trace.model, trace.kv_capacity, trace.res_offsets, trace.res_l_in,
+                  trace.res_l_pred, trace.res_generated, slots_per_worker)
+
+    def place_device(self, q_l_in, q_l_pred, heartbeat_every=0, diag=True):
+        """Device tensors in, device tensors out (no host copies)."""
+        t = self.torch
+        Q = int(q_l_in.numel())
+        out = t.empty(Q, dtype=t.int32, device=self.device)
+        d = t.empty(Q * DIAG_DTYPE.itemsize, dtype=t.uint8, device=self.device) if diag else None
+        ald_place_stream(self.h, Q, q_l_in, q_l_pred, heartbeat_every, out, d)
+        return out, d
+
+    def place(self, q_l_in, q_l_pred, heartbeat_every=0, diag=True) -> Placement:
+        t = self.torch
+        ql = self._dev(q_l_in, t.int32)
+        qp = self._dev(q_l_pred, t.int32)
+        out, d = self.place_device(ql, qp, heartbeat_every, diag)
+        res = Placement(worker=out.cpu().numpy())
+        if d is not None:
+            res.diag = d.cpu().numpy().view(DIAG_DTYPE)
+        return res
+
+    def summary(self):
+        t = self.torch
+        W = self.W
+        B = t.empty(W, dtype=t.int32, device=self.device)
+        sc = t.empty(W, dtype=t.int64, device=self.device)
+        sr = t.empty(W, dtype=t.int64, device=self.device)
+        pk = t.empty(W, dtype=t.int64, device=self.device)
+        ald_worker_summary(self.h, B, sc, sr, pk)
+        return {"B": B.cpu().numpy(), "sum_c": sc.cpu().numpy(), "sum_r": sr.cpu().numpy(),
+                "peak": pk.cpu().numpy()}
+
+    def sweep(self, scenarios, q_l_in, q_l_pred, want_workers=False):
+        t = self.torch
+        S = len(scenarios)
+        arr = (Scenario * S)()
+        for i, s in enumerate(scenarios):
+            arr[i] = Scenario(s.n_workers, s.gpus_per_worker, s.kv_capacity, to_model(s.model))
+        ql = self._dev(q_l_in, t.int32)
+        qp = self._dev(q_l_pred, t.int32)
+        Q = int(ql.numel())
+        rej = t.empty(S, dtype=t.int32, device=self.device)
+        first = t.empty(S, dtype=t.int32, device=self.device)
+        ow = t.empty(S * Q, dtype=t.int32, device=self.device) if want_workers else None
+        ald_sweep_scenarios(self.h, S, arr, Q, ql, qp, rej, first, ow)
+        return (rej.cpu().numpy(), first.cpu().numpy(),
+                ow.cpu().numpy().reshape(S, Q) if want_workers else None)
+
+    def profiling(self, enable=True):
+        ald_set_profiling(self.h, enable)
+
+    def kernel_time(self, kind: str):
+        return ald_kernel_time(self.h, KERNEL_KINDS[kind])
+
+
+def smallest_feasible_cluster(scenarios, rejected):
+    """Scenario with no rejection and the fewest GPUs (n_workers * gpus_per_worker),
+    lowest index on ties: returns (gpus, index) or (None, -1)."""
+    best, idx = None, -1
+    for i, s in enumerate(scenarios):
+        if int(rejected[i]) != 0:
+            continue
+        g = s.n_workers * s.gpus_per_worker
+        if best is None or g < best:
+            best, idx = g, i
+    return best, idx

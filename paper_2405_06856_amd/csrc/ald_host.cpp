@@ -1,0 +1,660 @@
+// Host side of libaladdin: argument validation, device memory, and the round
+// loop that drives the tile pipeline (build -> eval -> select -> commit) on the
+// caller's HIP stream.  Every entry point returns after its stream work is done.
+#include "../../include/aladdin.h"
+#include "ald_internal.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+using namespace ald;
+
+namespace {
+
+struct Arena {
+    std::vector<void*> allocs;
+    State st{};
+    std::vector<Scen> hscen;
+    std::vector<int32_t> hW;  // workers per scenario
+    int32_t S = 0, NW = 0;
+    int32_t T = 0;            // tile the scratch is laid out for
+    int32_t eval_blocks = 0, sel_blocks = 0, commit_blocks = 0;
+    size_t scratch_bytes = 0;
+    void* scratch = nullptr;
+    Scen* dscen = nullptr;
+
+    ~Arena()
+    {
+        for (void* p : allocs) (void)hipFree(p);
+        if (scratch) (void)hipFree(scratch);
+    }
+};
+
+struct Events {
+    hipEvent_t a, b;
+    int kind;
+};
+
+}  // namespace
+
+struct ald_handle {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    std::string err;
+    int32_t tile = 4096;
+    Arena* main = nullptr;
+    int32_t W = 0;
+    ald_model_t model{};
+    int32_t max_cap = 0;
+    // stream position carried across ald_place_stream calls
+    int32_t tau = 0, hb_index = 0, since_hb = 0, round = 0;
+    int64_t* stats = nullptr;  // device scratch for query statistics
+    int32_t* err_word = nullptr;
+    bool prof = false;
+    std::vector<Events> pending;
+    std::vector<Events> pool;
+    double tot_ms[4] = {0, 0, 0, 0};
+    int64_t launches[4] = {0, 0, 0, 0};
+};
+
+namespace {
+
+int fail(ald_handle* h, int code, const std::string& msg)
+{
+    if (h) h->err = msg;
+    return code;
+}
+
+#define HIPCHK(h, call)                                                                   \
+    do {                                                                                  \
+        hipError_t e_ = (call);                                                           \
+        if (e_ != hipSuccess)                                                             \
+            return fail((h), ALD_EHIP, std::string(#call) + ": " + hipGetErrorString(e_)); \
+    } while (0)
+
+bool finite_model(const ald_model_t& m)
+{
+    const double v[] = {m.c1, m.k1, m.k1q, m.c3, m.c2, m.k2, m.ttft_slo, m.decode_slo, m.theta};
+    for (double x : v)
+        if (!std::isfinite(x)) return false;
+    return true;
+}
+
+// Reasons a model is unusable, or empty.
+std::string check_model(const ald_model_t& m)
+{
+    if (!finite_model(m)) return "model coefficients must be finite";
+    if (!(m.k2 > 0.0)) return "k2 must be > 0";
+    if (!(m.c2 >= 0.0)) return "c2 must be >= 0";
+    if (!(m.decode_slo > m.c3)) return "decode_slo must exceed c3 (Eq. 4)";
+    if (!(m.theta > 0.0 && m.theta <= 1.0)) return "theta must lie in (0, 1]";
+    if (m.gamma_log2den < 0 || m.gamma_log2den > 8) return "gamma_log2den must lie in [0, 8]";
+    if (m.gamma_num < 0 || m.gamma_num > (1 << m.gamma_log2den)) return "gamma must lie in [0, 1]";
+    return "";
+}
+
+// Largest batch size b for which constraint (b) can still hold: a feasible
+// placement needs theta*((T_dec - c3) - c2*b) >= k2*sum(D) > 0.  Evaluated with
+// the same fp64 expression as the kernels.  -1 = unbounded (c2 == 0).
+int64_t batch_bound(const ald_model_t& m)
+{
+    if (m.c2 == 0.0) return -1;
+    auto ok = [&](int64_t b) { return m.theta * ((m.decode_slo - m.c3) - m.c2 * (double)b) > 0.0; };
+    if (!ok(1)) return 0;
+    int64_t lo = 1, hi = (int64_t)1 << 31;
+    while (lo < hi) {
+        int64_t mid = lo + (hi - lo + 1) / 2;
+        if (ok(mid)) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
+Scen make_scen(const ald_model_t& m)
+{
+    Scen s{};
+    s.c1 = m.c1; s.k1 = m.k1; s.k1q = m.k1q;
+    s.c3 = m.c3; s.c2 = m.c2; s.k2 = m.k2;
+    s.ttft = m.ttft_slo; s.tdec = m.decode_slo; s.theta = m.theta;
+    s.gn = m.gamma_num; s.gs = m.gamma_log2den;
+    return s;
+}
+
+template <typename T>
+int dalloc(ald_handle* h, Arena* a, T** p, size_t count)
+{
+    void* q = nullptr;
+    if (count == 0) count = 1;
+    HIPCHK(h, hipMalloc(&q, count * sizeof(T)));
+    a->allocs.push_back(q);
+    *p = (T*)q;
+    return ALD_OK;
+}
+
+// Worker and slot arrays for S scenarios.  caps[w] = request slots of worker w.
+int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std::vector<int32_t>& W,
+               const std::vector<int32_t>& caps, const std::vector<int32_t>& Ms)
+{
+    a->S = (int32_t)scen.size();
+    a->hscen = scen;
+    a->hW = W;
+    int64_t NW = 0;
+    for (int32_t w : W) NW += w;
+    a->NW = (int32_t)NW;
+    std::vector<int64_t> base(NW);
+    int64_t slots = 0;
+    for (int64_t i = 0; i < NW; ++i) {
+        base[i] = slots;
+        slots += (int64_t)caps[i] + 1;
+    }
+    int32_t wb = 0;
+    for (int s = 0; s < a->S; ++s) {
+        a->hscen[s].W = W[s];
+        a->hscen[s].wbase = wb;
+        wb += W[s];
+    }
+    State& st = a->st;
+    int rc = ALD_OK;
+#define A(field, count) if ((rc = dalloc(h, a, &st.field, (size_t)(count))) != ALD_OK) return rc
+    A(slot_base, NW); A(cap, NW); A(n, NW); A(head, NW); A(M, NW); A(S1, NW); A(S2, NW);
+    A(hbs, NW); A(dirty, NW); A(built, NW); A(B, NW); A(DS, NW); A(key, NW); A(peak, NW);
+    A(rhs, NW); A(SC, NW); A(SR, NW);
+    A(e, slots); A(s, slots); A(pme, slots); A(sm, slots); A(ss, slots);
+    Ctl* ctl = nullptr;
+    TileInfo* ti = nullptr;
+    if ((rc = dalloc(h, a, &ctl, a->S)) != ALD_OK) return rc;
+    if ((rc = dalloc(h, a, &ti, a->S)) != ALD_OK) return rc;
+    if ((rc = dalloc(h, a, &a->dscen, a->S)) != ALD_OK) return rc;
+#undef A
+    st.ctl = ctl;
+    st.tinfo = ti;
+    st.scen = a->dscen;
+    st.S = a->S;
+    st.NW = a->NW;
+    HIPCHK(h, hipMemcpyAsync(st.slot_base, base.data(), NW * sizeof(int64_t), hipMemcpyHostToDevice, h->stream));
+    HIPCHK(h, hipMemcpyAsync(st.cap, caps.data(), NW * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
+    HIPCHK(h, hipMemcpyAsync(st.M, Ms.data(), NW * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
+    for (auto* p : {(void*)st.n, (void*)st.head, (void*)st.hbs, (void*)st.dirty, (void*)st.built, (void*)st.B,
+                    (void*)st.peak})
+        HIPCHK(h, hipMemsetAsync(p, 0, NW * sizeof(int32_t), h->stream));
+    for (auto* p : {(void*)st.S1, (void*)st.S2, (void*)st.DS, (void*)st.key, (void*)st.SC, (void*)st.SR,
+                    (void*)st.rhs})
+        HIPCHK(h, hipMemsetAsync(p, 0, NW * sizeof(int64_t), h->stream));
+    return ALD_OK;
+}
+
+// Lay out the tile scratch for tile length T and fill in the grid geometry.
+int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
+{
+    const int32_t nchunks = (T + EVAL_THREADS - 1) / EVAL_THREADS;
+    int64_t NWtot = 0;
+    for (int s = 0; s < a->S; ++s) NWtot += a->hW[s];
+    int32_t wpb = (int32_t)std::max<int64_t>(1, (NWtot * nchunks + target_blocks - 1) / target_blocks);
+    int64_t bits = 0, part = 0, qs = 0;
+    int32_t eb = 0, sb = 0, cb = 0;
+    const int32_t nfin = std::min(64, std::max(1, nchunks / 8));
+    for (int s = 0; s < a->S; ++s) {
+        Scen& sc = a->hscen[s];
+        sc.wpb = std::min(wpb, std::max(1, sc.W));
+        sc.nblk = (sc.W + sc.wpb - 1) / sc.wpb;
+        sc.eval_blk0 = eb;
+        eb += sc.nblk * nchunks;
+        sc.sel_blk0 = sb;
+        sb += nchunks;
+        sc.nfin = nfin;
+        sc.fin_blk0 = cb;
+        cb += 1 + nfin;
+        sc.bits_off = bits;
+        bits += (int64_t)nchunks * (EVAL_THREADS / 64) * sc.W;
+        sc.part_off = part;
+        part += (int64_t)nchunks * EVAL_THREADS * sc.nblk;
+        sc.qsum_off = qs;
+        qs += (int64_t)nchunks * EVAL_THREADS;
+    }
+    a->eval_blocks = eb;
+    a->sel_blocks = sb;
+    a->commit_blocks = cb;
+    a->T = T;
+    const size_t need = (size_t)bits * 16 + (size_t)part * sizeof(int4) + (size_t)qs * sizeof(QSum) + 1024;
+    if (need > a->scratch_bytes) {
+        if (a->scratch) HIPCHK(h, hipFree(a->scratch));
+        a->scratch = nullptr;
+        a->scratch_bytes = 0;
+        HIPCHK(h, hipMalloc(&a->scratch, need));
+        a->scratch_bytes = need;
+    }
+    char* p = (char*)a->scratch;
+    a->st.bits_feas = (uint64_t*)p;
+    p += (size_t)bits * 8;
+    a->st.bits_nt = (uint64_t*)p;
+    p += (size_t)bits * 8;
+    p = (char*)(((uintptr_t)p + 255) & ~(uintptr_t)255);
+    a->st.part = (int4*)p;
+    p += (size_t)part * sizeof(int4);
+    p = (char*)(((uintptr_t)p + 255) & ~(uintptr_t)255);
+    a->st.qsum = (QSum*)p;
+    HIPCHK(h, hipMemcpyAsync(a->dscen, a->hscen.data(), a->S * sizeof(Scen), hipMemcpyHostToDevice, h->stream));
+    return ALD_OK;
+}
+
+hipError_t prof_begin(ald_handle* h, int kind, Events* ev)
+{
+    if (!h->prof) return hipSuccess;
+    if (h->pool.empty()) {
+        Events e;
+        hipError_t r = hipEventCreate(&e.a);
+        if (r != hipSuccess) return r;
+        r = hipEventCreate(&e.b);
+        if (r != hipSuccess) return r;
+        h->pool.push_back(e);
+    }
+    *ev = h->pool.back();
+    h->pool.pop_back();
+    ev->kind = kind;
+    return hipEventRecord(ev->a, h->stream);
+}
+
+hipError_t prof_end(ald_handle* h, Events* ev)
+{
+    if (!h->prof) return hipSuccess;
+    h->pending.push_back(*ev);
+    return hipEventRecord(ev->b, h->stream);
+}
+
+// After a stream sync: fold recorded event pairs into the totals.
+void prof_collect(ald_handle* h)
+{
+    for (Events& e : h->pending) {
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, e.a, e.b) == hipSuccess) {
+            h->tot_ms[e.kind] += ms;
+            h->launches[e.kind] += 1;
+        }
+        h->pool.push_back(e);
+    }
+    h->pending.clear();
+}
+
+#define LAUNCH(h, kind, expr)                         \
+    do {                                              \
+        Events ev_;                                   \
+        HIPCHK(h, prof_begin(h, kind, &ev_));         \
+        HIPCHK(h, (expr));                            \
+        HIPCHK(h, prof_end(h, &ev_));                 \
+    } while (0)
+
+int map_dev_error(ald_handle* h, int32_t code)
+{
+    switch (code) {
+    case DEV_ESLOTS: return fail(h, ALD_ESLOTS, "a worker ran out of request slots (raise slots_per_worker)");
+    case DEV_EOVERFLOW: return fail(h, ALD_EOVERFLOW, "a worker's state left the exactly representable range");
+    case DEV_EINVAL: return fail(h, ALD_EINVAL, "invalid request lengths");
+    default: return fail(h, ALD_EHIP, "device error " + std::to_string(code));
+    }
+}
+
+// Rounds needed to finish every scenario from its control state, if no tile is cut.
+int64_t rounds_needed(const std::vector<Ctl>& c)
+{
+    int64_t most = 0;
+    for (const Ctl& x : c) {
+        if (x.err) continue;
+        int64_t r = 0;
+        int32_t pos = x.start, since = x.since_hb;
+        while (pos < x.Q) {
+            int32_t end = tile_end(pos, x.Q, x.T, x.H, since);
+            since += end - pos;
+            if (x.H > 0 && since >= x.H) since = 0;
+            pos = end;
+            ++r;
+        }
+        most = std::max(most, r);
+    }
+    return most;
+}
+
+// Drive the tile pipeline until every scenario has consumed its queries.
+int run_rounds(ald_handle* h, Arena* a, bool build_every_round)
+{
+    std::vector<Ctl> hc(a->S);
+    HIPCHK(h, hipMemcpyAsync(hc.data(), a->st.ctl, a->S * sizeof(Ctl), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    bool first = true;
+    for (;;) {
+        int64_t need = rounds_needed(hc);
+        if (need == 0) break;
+        for (int64_t r = 0; r < need; ++r) {
+            if (build_every_round || first) LAUNCH(h, 0, launch_build(a->st, h->stream, 0));
+            first = false;
+            LAUNCH(h, 1, launch_eval(a->st, a->eval_blocks, h->stream));
+            LAUNCH(h, 2, launch_select(a->st, a->sel_blocks, h->stream));
+            LAUNCH(h, 3, launch_commit(a->st, a->commit_blocks, h->stream));
+        }
+        HIPCHK(h, hipMemcpyAsync(hc.data(), a->st.ctl, a->S * sizeof(Ctl), hipMemcpyDeviceToHost, h->stream));
+        HIPCHK(h, hipStreamSynchronize(h->stream));
+        prof_collect(h);
+        for (const Ctl& x : hc)
+            if (x.err) return map_dev_error(h, x.err);
+    }
+    return ALD_OK;
+}
+
+int query_stats(ald_handle* h, const int32_t* lin, const int32_t* lpred, int32_t Q, int64_t out[4])
+{
+    HIPCHK(h, hipMemsetAsync(h->stats, 0, 4 * sizeof(int64_t), h->stream));
+    HIPCHK(h, launch_query_stats(lin, lpred, Q, h->stats, h->stream));
+    HIPCHK(h, hipMemcpyAsync(out, h->stats, 4 * sizeof(int64_t), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    if (out[0] != 0) return fail(h, ALD_EINVAL, "query lengths must lie in [1, 2^24]");
+    return ALD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ald_strerror(int code)
+{
+    switch (code) {
+    case ALD_OK: return "ok";
+    case ALD_EINVAL: return "invalid argument";
+    case ALD_EHIP: return "HIP runtime error";
+    case ALD_ESLOTS: return "worker request slots exhausted";
+    case ALD_ESTATE: return "no workers loaded";
+    case ALD_EOVERFLOW: return "value outside the exactly representable range";
+    default: return "unknown error";
+    }
+}
+
+const char* ald_last_error(ald_handle_t h) { return h ? h->err.c_str() : "null handle"; }
+
+int ald_create(ald_handle_t* out, int device, void* hip_stream)
+{
+    if (!out) return ALD_EINVAL;
+    *out = nullptr;
+    int count = 0;
+    if (hipGetDeviceCount(&count) != hipSuccess || count <= 0) return ALD_EHIP;
+    if (device < 0 || device >= count) return ALD_EINVAL;
+    if (hipSetDevice(device) != hipSuccess) return ALD_EHIP;
+    ald_handle* h = new ald_handle();
+    h->device = device;
+    h->stream = (hipStream_t)hip_stream;
+    if (hipMalloc(&h->stats, 4 * sizeof(int64_t)) != hipSuccess ||
+        hipMalloc(&h->err_word, sizeof(int32_t)) != hipSuccess) {
+        if (h->stats) (void)hipFree(h->stats);
+        delete h;
+        return ALD_EHIP;
+    }
+    *out = h;
+    return ALD_OK;
+}
+
+int ald_destroy(ald_handle_t h)
+{
+    if (!h) return ALD_OK;
+    (void)hipSetDevice(h->device);
+    (void)hipStreamSynchronize(h->stream);
+    delete h->main;
+    (void)hipFree(h->stats);
+    (void)hipFree(h->err_word);
+    for (Events& e : h->pool) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
+    for (Events& e : h->pending) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
+    delete h;
+    return ALD_OK;
+}
+
+int ald_set_tile(ald_handle_t h, int32_t tile_queries)
+{
+    if (!h) return ALD_EINVAL;
+    if (tile_queries < 64 || tile_queries > (1 << 20)) return fail(h, ALD_EINVAL, "tile must lie in [64, 2^20]");
+    h->tile = tile_queries;
+    return ALD_OK;
+}
+
+int ald_set_profiling(ald_handle_t h, int32_t enable)
+{
+    if (!h) return ALD_EINVAL;
+    h->prof = enable != 0;
+    if (h->prof) {
+        for (int k = 0; k < 4; ++k) { h->tot_ms[k] = 0; h->launches[k] = 0; }
+    }
+    return ALD_OK;
+}
+
+int ald_kernel_time(ald_handle_t h, int32_t kind, double* total_ms, int64_t* launches)
+{
+    if (!h || kind < 0 || kind > 3) return ALD_EINVAL;
+    if (total_ms) *total_ms = h->tot_ms[kind];
+    if (launches) *launches = h->launches[kind];
+    return ALD_OK;
+}
+
+int ald_load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const int64_t* kv_capacity,
+                     const int64_t* res_offsets, const int32_t* res_l_in, const int32_t* res_l_pred,
+                     const int32_t* res_generated, int32_t slots_per_worker)
+{
+    if (!h) return ALD_EINVAL;
+    HIPCHK(h, hipSetDevice(h->device));
+    if (W <= 0) return fail(h, ALD_EINVAL, "W must be >= 1");
+    if (!model || !kv_capacity || !res_offsets) return fail(h, ALD_EINVAL, "null argument");
+    if (slots_per_worker < 0) return fail(h, ALD_EINVAL, "slots_per_worker must be >= 0");
+    std::string why = check_model(*model);
+    if (!why.empty()) return fail(h, ALD_EINVAL, why);
+    std::vector<int64_t> off(W + 1), cap64(W);
+    HIPCHK(h, hipMemcpyAsync(off.data(), res_offsets, (W + 1) * sizeof(int64_t), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipMemcpyAsync(cap64.data(), kv_capacity, W * sizeof(int64_t), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    if (off[0] != 0) return fail(h, ALD_EINVAL, "res_offsets[0] must be 0");
+    for (int i = 0; i < W; ++i) {
+        if (off[i + 1] < off[i]) return fail(h, ALD_EINVAL, "res_offsets must be non-decreasing");
+        if (cap64[i] < 1) return fail(h, ALD_EINVAL, "kv_capacity must be >= 1");
+        if (cap64[i] > ((int64_t)1 << 30)) return fail(h, ALD_EOVERFLOW, "kv_capacity above 2^30 tokens");
+    }
+    if (off[W] > 0 && (!res_l_in || !res_l_pred || !res_generated)) return fail(h, ALD_EINVAL, "null resident array");
+    int64_t bound = slots_per_worker > 0 ? slots_per_worker : batch_bound(*model);
+    if (bound < 0) return fail(h, ALD_EINVAL, "c2 == 0 leaves the batch size unbounded: pass slots_per_worker");
+    std::vector<int32_t> caps(W), Ms(W);
+    int64_t total = 0;
+    int32_t maxcap = 0;
+    for (int i = 0; i < W; ++i) {
+        const int64_t R = off[i + 1] - off[i];
+        const int64_t c = std::max<int64_t>(R, bound) + 1;
+        if (c > (1 << 24)) return fail(h, ALD_EINVAL, "too many request slots per worker");
+        caps[i] = (int32_t)c;
+        Ms[i] = (int32_t)cap64[i];
+        total += c + 1;
+        maxcap = std::max(maxcap, (int32_t)c);
+    }
+    if (total * 20 > ((int64_t)64 << 30)) return fail(h, ALD_EINVAL, "worker state would exceed 64 GiB");
+
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    delete h->main;
+    h->main = nullptr;
+    Arena* a = new Arena();
+    std::vector<Scen> sc(1, make_scen(*model));
+    int rc = make_arena(h, a, sc, std::vector<int32_t>(1, W), caps, Ms);
+    if (rc == ALD_OK) rc = layout_scratch(h, a, 256, 4096);
+    if (rc != ALD_OK) { delete a; return rc; }
+    a->st.err_word = h->err_word;
+    HIPCHK(h, hipMemsetAsync(h->err_word, 0, sizeof(int32_t), h->stream));
+    HIPCHK(h, launch_ingest(a->st, W, res_offsets, res_l_in, res_l_pred, res_generated, h->stream));
+    int32_t dev_err = 0;
+    HIPCHK(h, hipMemcpyAsync(&dev_err, h->err_word, sizeof(int32_t), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    if (dev_err) {
+        delete a;
+        if (dev_err == DEV_EINVAL) return fail(h, ALD_EINVAL, "resident lengths must satisfy 1 <= l_in, l_pred <= 2^24 and 0 <= generated < l_pred");
+        if (dev_err == DEV_EOVERFLOW) return fail(h, ALD_EOVERFLOW, "a worker's residents exceed 2^30 tokens of future KV demand");
+        return map_dev_error(h, dev_err);
+    }
+    // build the breakpoint summaries once (one pass of the build kernel)
+    Ctl c{};
+    c.Q = 1;
+    c.T = 1;
+    c.rebuild = 1;
+    c.first_rej = INT32_MAX;
+    HIPCHK(h, hipMemcpyAsync(a->st.ctl, &c, sizeof(Ctl), hipMemcpyHostToDevice, h->stream));
+    HIPCHK(h, launch_build(a->st, h->stream, 0));
+    HIPCHK(h, hipMemcpyAsync(&c, a->st.ctl, sizeof(Ctl), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    if (c.err) { delete a; return map_dev_error(h, c.err); }
+    h->main = a;
+    h->W = W;
+    h->model = *model;
+    h->max_cap = maxcap;
+    h->tau = h->hb_index = h->since_hb = h->round = 0;
+    return ALD_OK;
+}
+
+int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
+                     int32_t heartbeat_every, int32_t* out_worker, ald_query_diag_t* out_diag)
+{
+    if (!h) return ALD_EINVAL;
+    HIPCHK(h, hipSetDevice(h->device));
+    if (!h->main) return fail(h, ALD_ESTATE, "ald_load_workers has not been called");
+    if (Q < 0 || heartbeat_every < 0) return fail(h, ALD_EINVAL, "Q and heartbeat_every must be >= 0");
+    if (Q == 0) return ALD_OK;
+    if (!q_l_in || !q_l_pred || !out_worker) return fail(h, ALD_EINVAL, "null argument");
+    int64_t qs[4];
+    int rc = query_stats(h, q_l_in, q_l_pred, Q, qs);
+    if (rc != ALD_OK) return rc;
+    const int32_t H = heartbeat_every;
+    int32_t tau = h->tau, hb = h->hb_index, since = h->since_hb;
+    bool rebuild = false;
+    if (H > 0 && since >= H) {  // a heartbeat already due from an earlier, longer period
+        tau += 1;
+        hb += 1;
+        since = 0;
+        rebuild = true;
+    }
+    const int64_t tau_final = (int64_t)tau + (H > 0 ? (int64_t)Q / H + 2 : 0);
+    if (tau_final >= ((int64_t)1 << 27) || (int64_t)h->max_cap * tau_final >= ((int64_t)1 << 27))
+        return fail(h, ALD_EOVERFLOW, "too many heartbeats for the 32-bit request state");
+    Arena* a = h->main;
+    int32_t T = std::min(h->tile, Q);
+    if (H > 0) T = std::min(T, H);
+    if (T != a->T) {
+        rc = layout_scratch(h, a, T, 4096);
+        if (rc != ALD_OK) return rc;
+    }
+    Ctl c{};
+    c.start = 0;
+    c.Q = Q;
+    c.T = T;
+    c.H = H;
+    c.since_hb = since;
+    c.tau = tau;
+    c.hb_index = hb;
+    c.rebuild = rebuild ? 1 : 0;
+    c.first_rej = INT32_MAX;
+    c.round = h->round;
+    TileInfo ti{};
+    ti.first_pc[0] = ti.first_pc[1] = INT32_MAX;
+    HIPCHK(h, hipMemcpyAsync(a->st.ctl, &c, sizeof(Ctl), hipMemcpyHostToDevice, h->stream));
+    HIPCHK(h, hipMemcpyAsync(a->st.tinfo, &ti, sizeof(TileInfo), hipMemcpyHostToDevice, h->stream));
+    a->st.q_lin = q_l_in;
+    a->st.q_lpred = q_l_pred;
+    a->st.out_worker = out_worker;
+    a->st.out_diag = (Diag*)out_diag;
+    rc = run_rounds(h, a, true);
+    if (rc != ALD_OK) return rc;
+    HIPCHK(h, hipMemcpyAsync(&c, a->st.ctl, sizeof(Ctl), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    h->tau = c.tau;
+    h->hb_index = c.hb_index;
+    h->since_hb = c.since_hb;
+    h->round = c.round;
+    return ALD_OK;
+}
+
+int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, int32_t Q, const int32_t* q_l_in,
+                        const int32_t* q_l_pred, int32_t* out_rejected, int32_t* out_first_reject,
+                        int32_t* out_worker)
+{
+    if (!h) return ALD_EINVAL;
+    HIPCHK(h, hipSetDevice(h->device));
+    if (S <= 0 || Q < 0) return fail(h, ALD_EINVAL, "S must be >= 1 and Q >= 0");
+    if (!scen || !out_rejected || !out_first_reject) return fail(h, ALD_EINVAL, "null argument");
+    if (Q > 0 && (!q_l_in || !q_l_pred)) return fail(h, ALD_EINVAL, "null query array");
+    std::vector<Scen> sc(S);
+    std::vector<int32_t> W(S), caps, Ms;
+    int64_t NW = 0, slots = 0;
+    for (int s = 0; s < S; ++s) {
+        if (scen[s].n_workers < 1) return fail(h, ALD_EINVAL, "scenario with no workers");
+        if (scen[s].kv_capacity < 1) return fail(h, ALD_EINVAL, "kv_capacity must be >= 1");
+        if (scen[s].kv_capacity > ((int64_t)1 << 30)) return fail(h, ALD_EOVERFLOW, "kv_capacity above 2^30 tokens");
+        std::string why = check_model(scen[s].model);
+        if (!why.empty()) return fail(h, ALD_EINVAL, "scenario " + std::to_string(s) + ": " + why);
+        NW += scen[s].n_workers;
+        int64_t b = batch_bound(scen[s].model);
+        int64_t cap = (b < 0 ? (int64_t)Q : std::min<int64_t>(Q, b)) + 1;
+        slots += scen[s].n_workers * (cap + 1);
+    }
+    if (NW > (1 << 30)) return fail(h, ALD_EINVAL, "too many workers");
+    if (slots * 20 > ((int64_t)128 << 30)) return fail(h, ALD_EINVAL, "sweep state would exceed 128 GiB");
+    int64_t qs[4] = {0, 0, 0, 0};
+    if (Q > 0) {
+        int rc = query_stats(h, q_l_in, q_l_pred, Q, qs);
+        if (rc != ALD_OK) return rc;
+    }
+    for (int s = 0; s < S; ++s) {
+        sc[s] = make_scen(scen[s].model);
+        W[s] = scen[s].n_workers;
+        int64_t b = batch_bound(scen[s].model);
+        int32_t cap = (int32_t)((b < 0 ? (int64_t)Q : std::min<int64_t>(Q, b)) + 1);
+        for (int i = 0; i < W[s]; ++i) {
+            caps.push_back(cap);
+            Ms.push_back((int32_t)scen[s].kv_capacity);
+        }
+    }
+    Arena a;
+    int rc = make_arena(h, &a, sc, W, caps, Ms);
+    if (rc != ALD_OK) return rc;
+    const int32_t T = std::max(1, std::min(h->tile, Q));
+    rc = layout_scratch(h, &a, T, 16384);
+    if (rc != ALD_OK) return rc;
+    std::vector<Ctl> c(S);
+    for (int s = 0; s < S; ++s) {
+        c[s] = Ctl{};
+        c[s].Q = Q;
+        c[s].T = T;
+        c[s].rebuild = 1;
+        c[s].first_rej = INT32_MAX;
+    }
+    std::vector<TileInfo> ti(S);
+    for (auto& t : ti) { t = TileInfo{}; t.first_pc[0] = t.first_pc[1] = INT32_MAX; }
+    HIPCHK(h, hipMemcpyAsync(a.st.ctl, c.data(), S * sizeof(Ctl), hipMemcpyHostToDevice, h->stream));
+    HIPCHK(h, hipMemcpyAsync(a.st.tinfo, ti.data(), S * sizeof(TileInfo), hipMemcpyHostToDevice, h->stream));
+    a.st.q_lin = q_l_in;
+    a.st.q_lpred = q_l_pred;
+    a.st.out_worker = out_worker;
+    a.st.out_diag = nullptr;
+    a.st.err_word = h->err_word;
+    for (int s = 0; s < S; ++s) a.hscen[s].out_off = (int64_t)s * Q;
+    HIPCHK(h, hipMemcpyAsync(a.dscen, a.hscen.data(), S * sizeof(Scen), hipMemcpyHostToDevice, h->stream));
+    if (Q > 0) {
+        rc = run_rounds(h, &a, false);
+        if (rc != ALD_OK) return rc;
+    }
+    HIPCHK(h, launch_sweep_outputs(a.st, out_rejected, out_first_reject, h->stream));
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    return ALD_OK;
+}
+
+int ald_worker_summary(ald_handle_t h, int32_t* B, int64_t* sum_c, int64_t* sum_r, int64_t* peak)
+{
+    if (!h) return ALD_EINVAL;
+    HIPCHK(h, hipSetDevice(h->device));
+    if (!h->main) return fail(h, ALD_ESTATE, "ald_load_workers has not been called");
+    if (!B || !sum_c || !sum_r || !peak) return fail(h, ALD_EINVAL, "null argument");
+    // bring every worker's summaries to the current decode iteration first
+    HIPCHK(h, launch_build(h->main->st, h->stream, 1));
+    HIPCHK(h, launch_summary(h->main->st, h->W, B, sum_c, sum_r, peak, h->stream));
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    return ALD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,179 @@
+// Internal layout shared by the HIP kernels and the host side of libaladdin.
+//
+// Worker state (one "scenario" = one pool of workers with one latency model;
+// ald_place_stream uses one scenario, ald_sweep_scenarios many):
+//
+//   Each worker owns a slot range [slot_base, slot_base + cap] of five int32
+//   arrays.  Requests are kept in absolute decode-iteration form so that a
+//   heartbeat (one decode iteration of every worker) only increments tau:
+//       e = r + tau   (iteration at which the request emits its last token)
+//       s = c - tau   (context minus tau; c = s + tau at any tau)
+//   Slots [head, n) hold the live requests sorted by e ascending; slots before
+//   head hold finished requests (e < tau) that are dropped lazily.
+//
+//   With P_k = sum_{j >= k} (s_j + e_k)  (the KV demand at the end point of
+//   request k counted over the requests at or after slot k; it equals the
+//   demand at iteration r_k whenever k is the first of its tie group, and is
+//   below it otherwise), the summaries are
+//       ss[k]  = sum_{j >= k} s_j                     (ss[n] = 0)
+//       pme[k] = max_{head <= j < k} (P_j + e_j)       (pme[head] = NEG)
+//       sm[k]  = max_{j >= k} P_j                     (sm[n] = NEG)
+//   For a query with sq = l_in - tau, eq = l_pred + tau and
+//   l = first live slot with e >= eq, the demand peak with the query added is
+//       max( pme[l] + sq,  sm[l],  ss[l] + (n - l) * eq + sq + eq ).
+//   All of these are tau-free: a heartbeat leaves them valid except that
+//   requests whose e fell below tau must leave the live range.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ald {
+
+constexpr int TOPK = 4;            // feasible candidates kept per query
+constexpr int EVAL_THREADS = 256;  // queries per pair-evaluation block
+constexpr int SEL_THREADS = 256;   // queries per selection block
+constexpr int COMMIT_THREADS = 256;
+constexpr int BUILD_THREADS = 256;
+constexpr int MAX_DIRTY = 64;      // workers changed within one tile before the tile is cut
+constexpr int32_t NEG = INT32_MIN;
+
+// error codes raised on the device (mirrors ALD_E* in aladdin.h)
+constexpr int32_t DEV_EINVAL = -1;
+constexpr int32_t DEV_ESLOTS = -3;
+constexpr int32_t DEV_EOVERFLOW = -5;
+
+struct Scen {
+    double c1, k1, k1q, c3, c2, k2, ttft, tdec, theta;
+    int32_t gn, gs;
+    int32_t W;          // workers in this scenario
+    int32_t wbase;      // first global worker index
+    int32_t wpb;        // workers per pair-evaluation block
+    int32_t nblk;       // worker blocks (ceil(W / wpb))
+    int32_t eval_blk0;  // first pair-evaluation block of this scenario
+    int32_t sel_blk0;   // first selection block
+    int32_t fin_blk0;   // first commit block (1 sequential + nfin finalizers)
+    int32_t nfin;
+    int64_t bits_off;   // uint64 words into bits_feas / bits_nt
+    int64_t part_off;   // int4 entries into part
+    int64_t qsum_off;   // QSum entries into qsum
+    int64_t out_off;    // offset into out_worker
+};
+
+// Per-scenario control block.  Written by the commit kernel's sequential block
+// only; every other kernel only reads it (kernel boundaries order the accesses).
+struct Ctl {
+    int32_t start;      // next query to process
+    int32_t Q;          // queries in this call
+    int32_t T;          // tile length
+    int32_t H;          // heartbeat period (0 = none)
+    int32_t since_hb;   // processed queries since the last heartbeat
+    int32_t tau;        // decode iterations run so far (absolute time offset)
+    int32_t hb_index;   // heartbeat counter (stamps the TTFT sums)
+    int32_t rebuild;    // 1: every worker's summaries must be rebuilt (tau moved)
+    int32_t err;        // first device error (0 = none)
+    int32_t n_rej;      // rejected queries
+    int32_t first_rej;  // first rejected query (INT32_MAX = none)
+    int32_t aborts;     // tiles cut short (statistics)
+    int32_t round;      // rounds run
+    int32_t commits;    // placements made
+    int32_t pad0, pad1;
+};
+
+// Tile description published by the selection kernel for the commit kernel.
+struct TileInfo {
+    int32_t start, end, parity, pad;
+    int32_t first_pc[2];  // first query of the tile with a feasible worker (by round parity)
+};
+
+// Per-query result of the selection kernel (tile-start state).
+struct QSum {
+    uint64_t tkey[TOPK];  // best feasible workers: rank keys, descending
+    int32_t tw[TOPK];     // their indices (-1 = none)
+    uint64_t ntkey;       // best-ranked worker with a near-tie margin
+    int32_t ntw;          // its index (-1 = none)
+    int32_t ntcnt;        // workers with a near-tie margin
+    int32_t nfeas;        // feasible workers
+    int32_t ex1, w1;      // smallest KV excess (ties: highest index first)
+    int32_t ex2, w2;      // second smallest
+    int32_t pad;
+};
+
+// Device mirror of ald_query_diag_t.
+struct Diag {
+    int32_t n_feasible;
+    int32_t near_tie;
+    int64_t kv_peak_chosen;
+    int64_t kv_excess_min;
+    double ttft_chosen;
+    double tdec_chosen;
+};
+
+struct State {
+    // per worker [NW]
+    int64_t* slot_base;
+    int32_t* cap;
+    int32_t* n;
+    int32_t* head;
+    int32_t* M;
+    int64_t* S1;
+    int64_t* S2;
+    int32_t* hbs;      // heartbeat stamp of S1/S2
+    int32_t* dirty;    // round stamp of the last commit
+    int32_t* built;
+    int32_t* B;
+    int64_t* DS;       // 2^gs * sum(c) + gn * sum(r)
+    uint64_t* key;     // (2^gs B)^2 + DS^2
+    int32_t* peak;     // KV peak without a new query
+    double* rhs;       // theta * ((T_dec - c3) - c2 * (B + 1))
+    int64_t* SC;       // sum(c)
+    int64_t* SR;       // sum(r)
+    // per slot
+    int32_t* e;
+    int32_t* s;
+    int32_t* pme;
+    int32_t* sm;
+    int32_t* ss;
+    // per scenario [S]
+    const Scen* scen;
+    Ctl* ctl;
+    TileInfo* tinfo;
+    int32_t S;
+    int32_t NW;
+    // tile scratch
+    uint64_t* bits_feas;
+    uint64_t* bits_nt;
+    int4* part;
+    QSum* qsum;
+    // queries and outputs
+    const int32_t* q_lin;
+    const int32_t* q_lpred;
+    int32_t* out_worker;
+    Diag* out_diag;    // only with S == 1
+    int32_t* err_word; // load-time validation
+};
+
+inline __host__ __device__ int32_t tile_end(int32_t start, int32_t Q, int32_t T, int32_t H, int32_t since_hb) {
+    int64_t end = (int64_t)start + T;
+    if (end > Q) end = Q;
+    if (H > 0) {
+        int64_t hb = (int64_t)start + (H - since_hb);
+        if (hb < end) end = hb;
+    }
+    return (int32_t)end;
+}
+
+// host-side launchers (ald_kernels.hip)
+hipError_t launch_ingest(const State& st, int32_t W, const int64_t* res_off, const int32_t* lin,
+                         const int32_t* lpred, const int32_t* gen, hipStream_t stream);
+hipError_t launch_build(const State& st, hipStream_t stream, int force);
+hipError_t launch_eval(const State& st, int32_t blocks, hipStream_t stream);
+hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream);
+hipError_t launch_commit(const State& st, int32_t blocks, hipStream_t stream);
+hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q, int64_t* stats,
+                              hipStream_t stream);
+hipError_t launch_summary(const State& st, int32_t W, int32_t* B, int64_t* sc, int64_t* sr, int64_t* peak,
+                          hipStream_t stream);
+hipError_t launch_sweep_outputs(const State& st, int32_t* rejected, int32_t* first_reject, hipStream_t stream);
+
+}  // namespace ald

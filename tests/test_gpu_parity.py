@@ -1,0 +1,311 @@
+"""GPU library vs CPU oracle, element by element (needs an MI355X).
+
+Integer outputs (worker choice, feasible counts, KV peaks and excesses, final
+worker sums) must match exactly.  fp64 latencies are computed with the same
+operations in the same order on both sides and are expected bit-identical;
+the contract tolerance is a relative 1e-9 and is what the assertion enforces,
+with any bit difference reported separately.  Queries whose decode or TTFT
+margin lies within that tolerance are flagged by both sides (near_tie) and
+counted separately.
+"""
+from __future__ import annotations
+
+import dataclasses
+import hashlib
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import ref
+from paper_2405_06856_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+FIELDS_INT = ("n_feasible", "near_tie", "kv_peak_chosen", "kv_excess_min")
+FIELDS_FP = ("ttft_chosen", "tdec_chosen")
+RTOL = 1e-9
+
+
+@pytest.fixture(scope="module")
+def aladdin():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2405_06856_amd import aladdin as mod
+    return mod
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def gpu_place(aladdin, trace, tile=4096, diag=True, H=None, chunks=None, slots=0):
+    ev = aladdin.Evaluator(0, tile=tile)
+    ev.load_trace(trace, slots_per_worker=slots)
+    H = trace.heartbeat_every if H is None else H
+    if chunks is None:
+        res = ev.place(trace.q_l_in, trace.q_l_pred, H, diag=diag)
+        worker, dg = res.worker, res.diag
+    else:
+        ws, ds = [], []
+        for a, b in chunks:
+            r = ev.place(trace.q_l_in[a:b], trace.q_l_pred[a:b], H, diag=diag)
+            ws.append(r.worker)
+            ds.append(r.diag)
+        worker = np.concatenate(ws)
+        dg = np.concatenate(ds) if diag else None
+    summ = ev.summary()
+    ev.close()
+    return worker, dg, summ
+
+
+def compare(worker, dg, summ, want, label=""):
+    assert np.array_equal(worker, want.worker), (label, np.flatnonzero(worker != want.worker)[:10])
+    if dg is not None:
+        for f in FIELDS_INT:
+            g = dg[f].astype(np.int64)
+            w = getattr(want, f).astype(np.int64)
+            assert np.array_equal(g, w), (label, f, np.flatnonzero(g != w)[:10])
+        for f in FIELDS_FP:
+            g, w = dg[f], getattr(want, f)
+            assert np.allclose(g, w, rtol=RTOL, atol=0.0), (label, f)
+            nbits = int((g.view(np.int64) != w.view(np.int64)).sum())
+            if nbits:
+                say("%s: %s within 1e-9 but %d values differ in the last bits" % (label, f, nbits))
+    if summ is not None:
+        for f in ("B", "sum_c", "sum_r", "peak"):
+            assert np.array_equal(summ[f].astype(np.int64), getattr(want, f)), (label, f)
+
+
+# ----------------------------------------------------------------------------- small workloads
+@pytest.mark.parametrize("tile", [64, 256, 4096])
+def test_tiny_matches_oracle(aladdin, tile):
+    t = wl.make_config("tiny")
+    say("tiny tile", tile)
+    compare(*gpu_place(aladdin, t, tile=tile), ref.place_trace(t), "tiny/%d" % tile)
+
+
+@pytest.mark.parametrize("tile", [64, 1024, 4096])
+def test_medium_matches_oracle(aladdin, tile):
+    t = wl.make_config("medium")
+    say("medium tile", tile)
+    compare(*gpu_place(aladdin, t, tile=tile), ref.place_trace(t), "medium/%d" % tile)
+
+
+def test_medium_without_diagnostics_same_choices(aladdin):
+    t = wl.make_config("medium")
+    w, d, s = gpu_place(aladdin, t, tile=512, diag=False)
+    assert d is None
+    compare(w, None, s, ref.place_trace(t), "medium/nodiag")
+
+
+def test_stream_continues_across_calls(aladdin):
+    # one stream placed in four calls equals the whole stream at once
+    t = wl.make_trace("chunks", 21, W=24, R=20, Q=1500, kv_capacity=30000, model=wl.BASE_MODEL,
+                      heartbeat_every=37)
+    cuts = [(0, 100), (100, 101), (101, 900), (900, 1500)]
+    compare(*gpu_place(aladdin, t, tile=256, chunks=cuts), ref.place_trace(t), "chunks")
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_ragged_traces(aladdin, seed):
+    rng = np.random.default_rng(1000 + seed)
+    W = int(rng.integers(1, 70))
+    R = rng.integers(0, 60, W)
+    H = int(rng.choice([0, 1, 5, 64, 333]))
+    model = wl.BASE_MODEL.scaled(float(rng.uniform(0.3, 1.2)))
+    model = dataclasses.replace(model, theta=float(rng.choice([1.0, 0.9, 0.5])),
+                                gamma_num=int(rng.integers(0, 3)), gamma_log2den=1)
+    t = wl.make_trace("rand%d" % seed, 2000 + seed, W=W, R=0, Q=int(rng.integers(1, 3000)),
+                      kv_capacity=int(rng.integers(2000, 40000)), model=model, heartbeat_every=H,
+                      R_per_worker=R)
+    tile = int(rng.choice([64, 100, 256, 1000]))
+    say("random seed", seed, "W", W, "Q", t.n_queries, "H", H, "tile", tile)
+    compare(*gpu_place(aladdin, t, tile=tile), ref.place_trace(t), "rand%d" % seed)
+
+
+# ----------------------------------------------------------------------------- adversarial cases
+FREE = wl.Model(c1=0.0, k1=1e-12, k1q=0.0, c3=0.0, c2=1e-3, k2=1e-12, ttft_slo=1e9, decode_slo=1.0)
+
+
+def _trace(W, M, residents, queries, model=FREE, H=0):
+    counts = np.array([len(r) for r in residents], np.int64)
+    off = np.zeros(W + 1, np.int64)
+    off[1:] = np.cumsum(counts)
+    flat = [x for r in residents for x in r] or [(1, 1, 0)]
+    arr = np.array(flat, np.int32).reshape(-1, 3)[: int(counts.sum())]
+    q = np.array(queries, np.int32).reshape(-1, 2)
+    return wl.Trace(name="adv", seed=0, model=model, kv_capacity=np.asarray(M, np.int64) * np.ones(W, np.int64),
+                    res_offsets=off, res_l_in=arr[:, 0].copy(), res_l_pred=arr[:, 1].copy(),
+                    res_generated=arr[:, 2].copy(), q_l_in=q[:, 0].copy(), q_l_pred=q[:, 1].copy(),
+                    arrivals=None, heartbeat_every=H)
+
+
+def test_fig3_example_on_gpu(aladdin):
+    fx = json.load(open(os.path.join(GOLDEN, "fig3_example.json")))
+    LP, LO = fx["derived"]["long_prompt"], fx["derived"]["long_output"]
+    t = _trace(2, fx["printed"]["kv_capacity"], [[], []], [LP, LO, LP, LO])
+    w, d, s = gpu_place(aladdin, t, tile=64)
+    assert list(w) == [0, 0, 1, 1]
+    assert list(s["peak"]) == [fx["printed"]["best_peak_each_worker"]] * 2
+
+
+def test_all_workers_identical_rank_ties(aladdin):
+    # identical workers: ties everywhere, lowest index wins each time
+    res = [[(50, 10, 3), (20, 30, 0)]] * 40
+    q = [(30, 20)] * 300 + [(1, 1)] * 50
+    t = _trace(40, 2000, res, q)
+    compare(*gpu_place(aladdin, t, tile=128), ref.place_trace(t), "ties")
+
+
+def test_peak_exactly_at_capacity(aladdin):
+    # (4,1) then (1,4) gives a peak of exactly 7
+    t = _trace(3, 7, [[], [], []], [(4, 1), (1, 4), (4, 1), (1, 4), (4, 1), (1, 4), (3, 3)])
+    compare(*gpu_place(aladdin, t, tile=64), ref.place_trace(t), "exact-cap")
+
+
+def test_many_commits_to_one_worker_in_one_tile(aladdin):
+    # one roomy worker absorbs hundreds of placements inside a single tile
+    t = _trace(5, [10 ** 6, 50, 50, 50, 50], [[], [], [], [], []], [(3, 2)] * 700)
+    compare(*gpu_place(aladdin, t, tile=1024, slots=800), ref.place_trace(t), "one-worker")
+
+
+def test_no_worker_ever_fits(aladdin):
+    t = _trace(7, 10, [[(5, 5, 0)]] * 7, [(20, 20)] * 333)
+    w, d, s = gpu_place(aladdin, t, tile=64)
+    assert (w == -1).all()
+    compare(w, d, s, ref.place_trace(t), "nothing-fits")
+
+
+def test_single_worker_and_empty_residents(aladdin):
+    t = _trace(1, 5000, [[]], [(int(a), int(b)) for a, b in zip(range(1, 200), range(200, 1, -1))])
+    compare(*gpu_place(aladdin, t, tile=64), ref.place_trace(t), "single")
+
+
+def test_heartbeat_every_query_drains_residents(aladdin):
+    res = [[(10, 3, 1), (5, 2, 0), (7, 9, 8)] for _ in range(9)]
+    q = [(2, 2)] * 400
+    t = _trace(9, 40, res, q, H=1)
+    compare(*gpu_place(aladdin, t, tile=64), ref.place_trace(t), "hb1")
+
+
+def test_near_tie_margins_are_flagged(aladdin):
+    # decode margin exactly zero for the first query
+    m = wl.Model(c1=0.0, k1=0.0, k1q=0.0, c3=0.0, c2=0.0, k2=0.5, ttft_slo=1e9, decode_slo=5.0,
+                 gamma_num=0, gamma_log2den=1)
+    t = _trace(2, 10 ** 6, [[], []], [(10, 3), (1, 1), (9, 1)], model=m)
+    w, d, s = gpu_place(aladdin, t, tile=64, slots=16)
+    want = ref.place_trace(t)
+    compare(w, d, s, want, "near-tie")
+    assert d["near_tie"][0] == 1
+
+
+def test_slots_exhausted_is_reported(aladdin):
+    t = _trace(1, 10 ** 6, [[]], [(3, 2)] * 50)
+    ev = aladdin.Evaluator(0, tile=64)
+    ev.load_trace(t, slots_per_worker=8)
+    with pytest.raises(aladdin.AladdinError) as ei:
+        ev.place(t.q_l_in, t.q_l_pred, 0)
+    assert ei.value.code == aladdin.ALD_ESLOTS
+    ev.close()
+
+
+def test_invalid_inputs_are_rejected(aladdin):
+    t = _trace(2, 100, [[(3, 2, 0)], []], [(1, 1)])
+    ev = aladdin.Evaluator(0, tile=64)
+    bad = dataclasses.replace(t, res_generated=np.array([2], np.int32))  # g must be < l_pred
+    with pytest.raises(aladdin.AladdinError) as ei:
+        ev.load_trace(bad)
+    assert ei.value.code == aladdin.ALD_EINVAL
+    with pytest.raises(aladdin.AladdinError) as ei:
+        ev.place([1], [1], 0)
+    assert ei.value.code == aladdin.ALD_ESTATE
+    ev.load_trace(t)
+    with pytest.raises(aladdin.AladdinError) as ei:
+        ev.place([0], [1], 0)
+    assert ei.value.code == aladdin.ALD_EINVAL
+    bad_model = dataclasses.replace(t, model=dataclasses.replace(FREE, decode_slo=0.0, c3=0.1))
+    with pytest.raises(aladdin.AladdinError):
+        ev.load_trace(bad_model)
+    ev.close()
+
+
+def test_sweep_small_matches_oracle(aladdin):
+    s = wl.make_sweep("mini", 9, Q=700, worker_counts=(2, 3, 5, 16), gpu_counts=(1, 2), base_capacity=6000,
+                      model=wl.BASE_MODEL, in_dist=wl.MID_IN, out_dist=wl.MID_OUT, rate=None)
+    ev = aladdin.Evaluator(0, tile=128)
+    rej, first, workers = ev.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True)
+    ev.close()
+    orej, ofirst, oworkers = ref.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True)
+    assert np.array_equal(workers, oworkers)
+    assert np.array_equal(rej, orej)
+    assert np.array_equal(first, ofirst)
+
+
+def test_repeat_runs_bitwise_identical(aladdin):
+    t = wl.make_config("medium")
+    a = gpu_place(aladdin, t, tile=1024)
+    b = gpu_place(aladdin, t, tile=1024)
+    assert np.array_equal(a[0], b[0])
+    assert a[1].tobytes() == b[1].tobytes()
+
+
+# ----------------------------------------------------------------------------- full-size workloads
+def _digest(a):
+    return hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
+
+
+def _check_golden(name, worker, dg, summ):
+    g = json.load(open(os.path.join(GOLDEN, "%s_oracle.json" % name)))
+    assert int((worker >= 0).sum()) == g["placed"]
+    assert _digest(worker.astype(np.int32)) == g["sha256"]["worker"]
+    casts = {"n_feasible": np.int32, "near_tie": np.int32, "kv_peak_chosen": np.int64,
+             "kv_excess_min": np.int64, "ttft_chosen": np.float64, "tdec_chosen": np.float64}
+    for f, dt in casts.items():
+        assert _digest(dg[f].astype(dt)) == g["sha256"][f], f
+    for f in ("B", "sum_c", "sum_r", "peak"):
+        assert _digest(summ[f].astype(np.int64)) == g["sha256"][f], f
+    smp = g["sample"]
+    idx = np.array(smp["index"])
+    assert np.array_equal(worker[idx], np.array(smp["worker"]))
+    for f in FIELDS_INT:
+        assert np.array_equal(dg[f][idx].astype(np.int64), np.array(smp[f], np.int64)), f
+
+
+def test_large_full_size(aladdin):
+    t = wl.make_config("large")
+    say("large: W=512 R=512 Q=65536")
+    w, d, s = gpu_place(aladdin, t, tile=65536)
+    _check_golden("large", w, d, s)
+    # sampled queries recomputed by the oracle one by one at the initial state
+    # (valid because no query of this stream is ever placed)
+    idx = np.arange(0, t.n_queries, 4099)
+    want = ref.place(t.n_workers, t.kv_capacity, t.res_offsets, t.res_l_in, t.res_l_pred, t.res_generated,
+                     t.model, t.q_l_in[idx], t.q_l_pred[idx], no_commit=True)
+    assert (w == -1).all()
+    for f in FIELDS_INT:
+        assert np.array_equal(d[f][idx].astype(np.int64), getattr(want, f).astype(np.int64)), f
+
+
+def test_long_full_size(aladdin):
+    t = wl.make_config("long")
+    say("long: W=2048 R=1024 Q=131072 heartbeat 100")
+    w, d, s = gpu_place(aladdin, t, tile=4096)
+    _check_golden("long", w, d, s)
+
+
+def test_sweep_full_size(aladdin):
+    s = wl.make_config("sweep")
+    say("sweep: 256 scenarios x 16384 queries")
+    g = json.load(open(os.path.join(GOLDEN, "sweep_oracle.json")))
+    ev = aladdin.Evaluator(0, tile=1024)
+    rej, first, workers = ev.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True)
+    ev.close()
+    assert list(rej) == g["rejected"]
+    assert list(first) == g["first_reject"]
+    assert _digest(workers.astype(np.int32)) == g["sha256"]["worker"]
+    gpus, idx = aladdin.smallest_feasible_cluster(s.scenarios, rej)
+    assert (gpus, idx) == (g["min_gpus"], g["min_gpus_scenario"])
