@@ -84,13 +84,43 @@ __device__ __forceinline__ int lower_bound_i32(const int32_t* a, int lo, int hi,
     return lo;
 }
 
-// Algorithm 1 order: does (ka, a) rank strictly before (kb, b)?  b < 0 = empty.
+// Algorithm 1 order: does (ka, a) rank strictly before (kb, b)?  An index < 0
+// marks an absent entry, which ranks after every present one.
 __device__ __forceinline__ bool ranks_before(uint64_t ka, int a, uint64_t kb, int b)
 {
-    if (b < 0) return a >= 0;
-    if (a < 0) return false;
-    if (ka != kb) return ka > kb;
-    return a < b;
+    const bool better = (ka > kb) | ((ka == kb) & (a < b));
+    return (a >= 0) & ((b < 0) | better);
+}
+
+// Insert candidate (ck, cw) into a best-first list of N entries (cw < 0: no-op).
+// Written as a compare-exchange chain of selects: no divergent branch touches
+// the register-resident list.
+template <int N>
+__device__ __forceinline__ void topk_insert(uint64_t (&key)[N], int32_t (&idx)[N], uint64_t ck, int32_t cw)
+{
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+        const bool sw = ranks_before(ck, cw, key[k], idx[k]);
+        const uint64_t ok = key[k];
+        const int32_t ow = idx[k];
+        key[k] = sw ? ck : ok;
+        idx[k] = sw ? cw : ow;
+        ck = sw ? ok : ck;
+        cw = sw ? ow : cw;
+    }
+}
+
+// Keep the two smallest (excess, index) pairs, ordered by excess ascending and
+// then index descending.  y < 0: no candidate.
+__device__ __forceinline__ void min2_insert(int32_t& ex1, int32_t& w1, int32_t& ex2, int32_t& w2, int32_t x, int32_t y)
+{
+    const bool present = y >= 0;
+    const bool b1 = present & ((w1 < 0) | (x < ex1) | ((x == ex1) & (y > w1)));
+    const bool b2 = present & !b1 & ((w2 < 0) | (x < ex2) | ((x == ex2) & (y > w2)));
+    ex2 = b1 ? ex1 : (b2 ? x : ex2);
+    w2 = b1 ? w1 : (b2 ? y : w2);
+    ex1 = b1 ? x : ex1;
+    w1 = b1 ? y : w1;
 }
 
 __device__ __forceinline__ bool near_tie(double x, double y)
@@ -417,14 +447,7 @@ __global__ __launch_bounds__(EVAL_THREADS) void k_eval(State st)
             st.bits_feas[row + w] = bf;
             st.bits_nt[row + w] = bn;
         }
-        const int32_t ex = (int32_t)(peak - v.M);
-        // ascending excess, ties to the higher index (w grows through the loop)
-        if (ex <= ex1) {
-            ex2 = ex1; w2 = w1;
-            ex1 = ex; w1 = w;
-        } else if (ex <= ex2) {
-            ex2 = ex; w2 = w;
-        }
+        min2_insert(ex1, w1, ex2, w2, (int32_t)(peak - v.M), w);
     }
     if (act) st.part[sc.part_off + (int64_t)(qi - start) * sc.nblk + wb] = make_int4(ex1, w1, ex2, w2);
 }
@@ -464,48 +487,24 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     for (int w = 0; w < sc.W; ++w) {
         const uint64_t fw = st.bits_feas[row + w];
         const uint64_t nw = st.bits_nt[row + w];
-        if ((fw | nw) == 0) continue;
+        if ((fw | nw) == 0) continue;  // wave-uniform
         const uint64_t key = st.key[sc.wbase + w];
-        if ((fw >> lane) & 1) {
-            ++nfeas;
-            // insert (key, w); equal keys keep the earlier (lower) index first
-            if (ranks_before(key, w, tkey[TOPK - 1], tw[TOPK - 1])) {
-                uint64_t ck = key;
-                int32_t cw = w;
-#pragma unroll
-                for (int k = 0; k < TOPK; ++k) {
-                    if (ranks_before(ck, cw, tkey[k], tw[k])) {
-                        const uint64_t tk = tkey[k];
-                        const int32_t tww = tw[k];
-                        tkey[k] = ck; tw[k] = cw;
-                        ck = tk; cw = tww;
-                    }
-                }
-            }
-        }
-        if ((nw >> lane) & 1) {
-            ++ntcnt;
-            if (ranks_before(key, w, ntkey, ntw)) { ntkey = key; ntw = w; }
-        }
+        const bool f = (fw >> lane) & 1;
+        const bool nb = (nw >> lane) & 1;
+        nfeas += f ? 1 : 0;
+        topk_insert<TOPK>(tkey, tw, key, f ? w : -1);
+        ntcnt += nb ? 1 : 0;
+        const bool better = nb & ranks_before(key, w, ntkey, ntw);
+        ntkey = better ? key : ntkey;
+        ntw = better ? w : ntw;
     }
     int32_t ex1 = INT32_MAX, w1 = -1, ex2 = INT32_MAX, w2 = -1;
     const int4* prow = st.part + sc.part_off + (int64_t)(qi - start) * sc.nblk;
-    for (int b = 0; b < sc.nblk && act; ++b) {
-        const int4 p = prow[b];
-        // blocks cover ascending worker ranges; merge keeping (excess asc, index desc)
-        const int32_t ce[2] = {p.x, p.z};
-        const int32_t cw[2] = {p.y, p.w};
-#pragma unroll
-        for (int k = 0; k < 2; ++k) {
-            if (cw[k] < 0) continue;
-            const int32_t x = ce[k], y = cw[k];
-            const bool b1 = x < ex1 || (x == ex1 && y > w1);
-            if (b1) {
-                ex2 = ex1; w2 = w1;
-                ex1 = x; w1 = y;
-            } else if (x < ex2 || (x == ex2 && y > w2)) {
-                ex2 = x; w2 = y;
-            }
+    if (act) {
+        for (int b = 0; b < sc.nblk; ++b) {
+            const int4 p = prow[b];
+            min2_insert(ex1, w1, ex2, w2, p.x, p.y);
+            min2_insert(ex1, w1, ex2, w2, p.z, p.w);
         }
     }
     if (!act) return;
@@ -548,23 +547,20 @@ __device__ Resolved resolve(const State& st, const Scen& sc, const QSum& q, int 
     int32_t bw = -1;
     int32_t nf = q.nfeas;
     if (!want_diag && q.nfeas == 0) return r;  // rejected whatever changed in the tile
-    if (q.nfeas > 0) {
-        const int lim = q.nfeas < TOPK ? q.nfeas : TOPK;
-        for (int k = 0; k < lim; ++k) {
-            const int w = q.tw[k];
-            if (st.dirty[sc.wbase + w] != stamp) {
-                have = true;
-                bk = q.tkey[k];
-                bw = w;
-                break;
-            }
-        }
-        if (!have && q.nfeas > TOPK) { r.abort = 1; return r; }
+    const int lim = q.nfeas < TOPK ? q.nfeas : TOPK;
+#pragma unroll
+    for (int k = 0; k < TOPK; ++k) {
+        const int w = q.tw[k];
+        const bool clean = (k < lim) && (w >= 0) && (st.dirty[sc.wbase + (w >= 0 ? w : 0)] != stamp);
+        const bool take = clean & !have;
+        bk = take ? q.tkey[k] : bk;
+        bw = take ? w : bw;
+        have = have | take;
     }
+    if (!have && q.nfeas > TOPK) { r.abort = 1; return r; }
     const int64_t word = sc.bits_off + (int64_t)((i - start) >> 6) * sc.W;
     const int bit = (i - start) & 63;
     int32_t clean_nt = q.ntcnt;
-    bool dnt = false;
     uint64_t dntk = 0;
     int32_t dntw = -1;
     int64_t chosen_peak = 0;
@@ -574,27 +570,28 @@ __device__ Resolved resolve(const State& st, const Scen& sc, const QSum& q, int 
         const int gw = sc.wbase + d;
         const bool fs = (st.bits_feas[word + d] >> bit) & 1;
         const bool ns = (st.bits_nt[word + d] >> bit) & 1;
-        if (ns) --clean_nt;
+        clean_nt -= ns ? 1 : 0;
         const View v = load_view(st, gw, hb);
         const Latency L = latency(sc, v, lin, lp, v.n - v.head + 1);
-        if (fs) {
-            --nf;
-            if (L.dec_ok && L.ttft_ok) {
-                const int64_t peak = kv_peak_with(v, sq, eq);
-                if (peak <= v.M) {
-                    ++nf;
-                    if (ranks_before(v.key, d, bk, bw)) {
-                        bk = v.key; bw = d; have = true;
-                        chosen_peak = peak; chosen_peak_known = true;
-                    }
-                }
-            }
+        nf -= fs ? 1 : 0;
+        bool feas_now = false;
+        int64_t peak = 0;
+        if (fs && L.dec_ok && L.ttft_ok) {
+            peak = kv_peak_with(v, sq, eq);
+            feas_now = peak <= v.M;
         }
-        if (L.nt) {
-            dnt = true;
-            if (ranks_before(v.key, d, dntk, dntw)) { dntk = v.key; dntw = d; }
-        }
+        nf += feas_now ? 1 : 0;
+        const bool better = feas_now & ranks_before(v.key, d, bk, bw);
+        bk = better ? v.key : bk;
+        bw = better ? d : bw;
+        have = have | better;
+        chosen_peak = better ? peak : chosen_peak;
+        chosen_peak_known = better | (chosen_peak_known & !better);
+        const bool ntb = L.nt & ranks_before(v.key, d, dntk, dntw);
+        dntk = ntb ? v.key : dntk;
+        dntw = ntb ? d : dntw;
     }
+    const bool dnt = dntw >= 0;
     r.w = have ? bw : -1;
     if (!want_diag) return r;
 
