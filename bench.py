@@ -14,6 +14,7 @@ CPU oracle timed on a bounded sample on this host.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -30,6 +31,28 @@ def algorithmic_bytes_per_pair(residents_per_worker: int) -> int:
     # the two int32 columns the breakpoint rule depends on (remaining length and
     # context of every resident) plus five int64 worker aggregates
     return 8 * residents_per_worker + 40
+
+
+def kernel_source_sha256() -> str:
+    h = hashlib.sha256()
+    for p in ("paper_2405_06856_amd/csrc/ald_kernels.hip", "paper_2405_06856_amd/csrc/ald_internal.h"):
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per pair-evaluation launch from the committed counter record,
+    or None when the kernel source changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "pair_eval_large_traffic.json")
+    try:
+        with open(path) as f:
+            doc = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if doc.get("kernel_source_sha256") != kernel_source_sha256():
+        return None
+    return doc.get("bytes_per_launch")
 
 
 def cpu_baseline(trace, budget_s: float = 12.0, max_q: int = 8192):
@@ -51,6 +74,26 @@ def cpu_baseline(trace, budget_s: float = 12.0, max_q: int = 8192):
                       "%.1f s" % (n, trace.n_queries, trace.n_workers, dt)}
 
 
+def time_sweep(steps: int):
+    import torch
+
+    from paper_2405_06856_amd import aladdin
+    from paper_2405_06856_amd import workloads as wl
+    sw = wl.make_config("sweep")
+    sev = aladdin.Evaluator(0, tile=1024)
+    rej, first, _ = sev.sweep(sw.scenarios, sw.q_l_in, sw.q_l_pred)  # warm-up
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        rej, first, _ = sev.sweep(sw.scenarios, sw.q_l_in, sw.q_l_pred)
+    torch.cuda.synchronize()
+    sweep_s = (time.perf_counter() - t0) / steps
+    gpus, idx = aladdin.smallest_feasible_cluster(sw.scenarios, rej)
+    sev.close()
+    return {"sweeps_per_s": 1.0 / sweep_s, "ms_per_sweep": sweep_s * 1e3, "scenarios": len(sw.scenarios),
+            "queries": sw.n_queries, "min_total_gpus": gpus, "min_gpus_scenario": idx}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -59,6 +102,10 @@ def main():
     ap.add_argument("--sweep-steps", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--sweep-only", action="store_true", help="time only the scaling sweep (for profiling)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="also run a plain device-to-device copy of MIB MiB (a reference kernel of known "
+                         "traffic for scaling memory counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the evaluator runs on a single device "
@@ -72,6 +119,17 @@ def main():
     from paper_2405_06856_amd import workloads as wl
 
     dev = torch.device("cuda", 0)
+    if args.sweep_only:
+        print(json.dumps({"sweep": time_sweep(args.sweep_steps)}), flush=True)
+        return
+    if args.calibrate_copy > 0:
+        n = args.calibrate_copy * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     trace = wl.make_config("large")
     R = int(trace.res_offsets[1] - trace.res_offsets[0])
     W, Q = trace.n_workers, trace.n_queries
@@ -118,31 +176,9 @@ def main():
     eval_avg_ms = eval_ms / max(eval_n, 1)
     pairs_per_eval_launch = pairs * args.steps / max(eval_n, 1)
     achieved = algorithmic_bytes_per_pair(R) * pairs_per_eval_launch / (eval_avg_ms / 1e3) / 1e9
-    traffic = None
-    tfile = os.path.join(ROOT, "profiles", "pair_eval_large_traffic.json")
-    if os.path.exists(tfile):
-        try:
-            traffic = json.load(open(tfile)).get("bytes_per_launch")
-        except Exception:
-            traffic = None
+    traffic = measured_traffic() if pairs_per_eval_launch == pairs else None
 
-    sweep_info = None
-    if not args.no_sweep:
-        sw = wl.make_config("sweep")
-        sev = aladdin.Evaluator(0, tile=1024)
-        rej, first, _ = sev.sweep(sw.scenarios, sw.q_l_in, sw.q_l_pred)  # warm-up
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.sweep_steps):
-            rej, first, _ = sev.sweep(sw.scenarios, sw.q_l_in, sw.q_l_pred)
-        torch.cuda.synchronize()
-        sweep_s = (time.perf_counter() - t0) / args.sweep_steps
-        gpus, idx = aladdin.smallest_feasible_cluster(sw.scenarios, rej)
-        sweep_info = {"sweeps_per_s": 1.0 / sweep_s, "ms_per_sweep": sweep_s * 1e3,
-                      "scenarios": len(sw.scenarios), "queries": sw.n_queries,
-                      "min_total_gpus": gpus, "min_gpus_scenario": idx}
-        sev.close()
-
+    sweep_info = None if args.no_sweep else time_sweep(args.sweep_steps)
     line = {
         "metric": "query x worker placement evals/sec (+ scenario sweeps/sec; % of HBM roofline)",
         "value": value,

@@ -52,7 +52,6 @@ struct ald_handle {
     int32_t max_cap = 0;
     // stream position carried across ald_place_stream calls
     int32_t tau = 0, hb_index = 0, since_hb = 0, round = 0;
-    int64_t* stats = nullptr;  // device scratch for query statistics
     int32_t* err_word = nullptr;
     bool prof = false;
     std::vector<Events> pending;
@@ -291,7 +290,7 @@ int map_dev_error(ald_handle* h, int32_t code)
     switch (code) {
     case DEV_ESLOTS: return fail(h, ALD_ESLOTS, "a worker ran out of request slots (raise slots_per_worker)");
     case DEV_EOVERFLOW: return fail(h, ALD_EOVERFLOW, "a worker's state left the exactly representable range");
-    case DEV_EINVAL: return fail(h, ALD_EINVAL, "invalid request lengths");
+    case DEV_EINVAL: return fail(h, ALD_EINVAL, "query lengths must lie in [1, 2^24]");
     default: return fail(h, ALD_EHIP, "device error " + std::to_string(code));
     }
 }
@@ -317,11 +316,10 @@ int64_t rounds_needed(const std::vector<Ctl>& c)
 }
 
 // Drive the tile pipeline until every scenario has consumed its queries.
-int run_rounds(ald_handle* h, Arena* a, bool build_every_round)
+// `hc` holds the control blocks as last written to the device; on return it
+// holds their final device values.
+int run_rounds(ald_handle* h, Arena* a, bool build_every_round, std::vector<Ctl>& hc)
 {
-    std::vector<Ctl> hc(a->S);
-    HIPCHK(h, hipMemcpyAsync(hc.data(), a->st.ctl, a->S * sizeof(Ctl), hipMemcpyDeviceToHost, h->stream));
-    HIPCHK(h, hipStreamSynchronize(h->stream));
     bool first = true;
     for (;;) {
         int64_t need = rounds_needed(hc);
@@ -339,16 +337,6 @@ int run_rounds(ald_handle* h, Arena* a, bool build_every_round)
         for (const Ctl& x : hc)
             if (x.err) return map_dev_error(h, x.err);
     }
-    return ALD_OK;
-}
-
-int query_stats(ald_handle* h, const int32_t* lin, const int32_t* lpred, int32_t Q, int64_t out[4])
-{
-    HIPCHK(h, hipMemsetAsync(h->stats, 0, 4 * sizeof(int64_t), h->stream));
-    HIPCHK(h, launch_query_stats(lin, lpred, Q, h->stats, h->stream));
-    HIPCHK(h, hipMemcpyAsync(out, h->stats, 4 * sizeof(int64_t), hipMemcpyDeviceToHost, h->stream));
-    HIPCHK(h, hipStreamSynchronize(h->stream));
-    if (out[0] != 0) return fail(h, ALD_EINVAL, "query lengths must lie in [1, 2^24]");
     return ALD_OK;
 }
 
@@ -382,9 +370,7 @@ int ald_create(ald_handle_t* out, int device, void* hip_stream)
     ald_handle* h = new ald_handle();
     h->device = device;
     h->stream = (hipStream_t)hip_stream;
-    if (hipMalloc(&h->stats, 4 * sizeof(int64_t)) != hipSuccess ||
-        hipMalloc(&h->err_word, sizeof(int32_t)) != hipSuccess) {
-        if (h->stats) (void)hipFree(h->stats);
+    if (hipMalloc(&h->err_word, sizeof(int32_t)) != hipSuccess) {
         delete h;
         return ALD_EHIP;
     }
@@ -398,7 +384,6 @@ int ald_destroy(ald_handle_t h)
     (void)hipSetDevice(h->device);
     (void)hipStreamSynchronize(h->stream);
     delete h->main;
-    (void)hipFree(h->stats);
     (void)hipFree(h->err_word);
     for (Events& e : h->pool) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
     for (Events& e : h->pending) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
@@ -518,9 +503,7 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
     if (Q < 0 || heartbeat_every < 0) return fail(h, ALD_EINVAL, "Q and heartbeat_every must be >= 0");
     if (Q == 0) return ALD_OK;
     if (!q_l_in || !q_l_pred || !out_worker) return fail(h, ALD_EINVAL, "null argument");
-    int64_t qs[4];
-    int rc = query_stats(h, q_l_in, q_l_pred, Q, qs);
-    if (rc != ALD_OK) return rc;
+    int rc = ALD_OK;
     const int32_t H = heartbeat_every;
     int32_t tau = h->tau, hb = h->hb_index, since = h->since_hb;
     bool rebuild = false;
@@ -555,14 +538,15 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
     ti.first_pc[0] = ti.first_pc[1] = INT32_MAX;
     HIPCHK(h, hipMemcpyAsync(a->st.ctl, &c, sizeof(Ctl), hipMemcpyHostToDevice, h->stream));
     HIPCHK(h, hipMemcpyAsync(a->st.tinfo, &ti, sizeof(TileInfo), hipMemcpyHostToDevice, h->stream));
+    HIPCHK(h, launch_query_stats(q_l_in, q_l_pred, Q, a->st.ctl, 1, h->stream));
     a->st.q_lin = q_l_in;
     a->st.q_lpred = q_l_pred;
     a->st.out_worker = out_worker;
     a->st.out_diag = (Diag*)out_diag;
-    rc = run_rounds(h, a, true);
+    std::vector<Ctl> hc(1, c);
+    rc = run_rounds(h, a, true, hc);
     if (rc != ALD_OK) return rc;
-    HIPCHK(h, hipMemcpyAsync(&c, a->st.ctl, sizeof(Ctl), hipMemcpyDeviceToHost, h->stream));
-    HIPCHK(h, hipStreamSynchronize(h->stream));
+    c = hc[0];
     h->tau = c.tau;
     h->hb_index = c.hb_index;
     h->since_hb = c.since_hb;
@@ -595,11 +579,6 @@ int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, i
     }
     if (NW > (1 << 30)) return fail(h, ALD_EINVAL, "too many workers");
     if (slots * 20 > ((int64_t)128 << 30)) return fail(h, ALD_EINVAL, "sweep state would exceed 128 GiB");
-    int64_t qs[4] = {0, 0, 0, 0};
-    if (Q > 0) {
-        int rc = query_stats(h, q_l_in, q_l_pred, Q, qs);
-        if (rc != ALD_OK) return rc;
-    }
     for (int s = 0; s < S; ++s) {
         sc[s] = make_scen(scen[s].model);
         W[s] = scen[s].n_workers;
@@ -636,7 +615,8 @@ int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, i
     for (int s = 0; s < S; ++s) a.hscen[s].out_off = (int64_t)s * Q;
     HIPCHK(h, hipMemcpyAsync(a.dscen, a.hscen.data(), S * sizeof(Scen), hipMemcpyHostToDevice, h->stream));
     if (Q > 0) {
-        rc = run_rounds(h, &a, false);
+        HIPCHK(h, launch_query_stats(q_l_in, q_l_pred, Q, a.st.ctl, S, h->stream));
+        rc = run_rounds(h, &a, false, c);
         if (rc != ALD_OK) return rc;
     }
     HIPCHK(h, launch_sweep_outputs(a.st, out_rejected, out_first_reject, h->stream));

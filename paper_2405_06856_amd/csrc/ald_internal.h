@@ -170,7 +170,7 @@ hipError_t launch_build(const State& st, hipStream_t stream, int force);
 hipError_t launch_eval(const State& st, int32_t blocks, hipStream_t stream);
 hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream);
 hipError_t launch_commit(const State& st, int32_t blocks, hipStream_t stream);
-hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q, int64_t* stats,
+hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q, Ctl* ctl, int32_t S,
                               hipStream_t stream);
 hipError_t launch_summary(const State& st, int32_t W, int32_t* B, int64_t* sc, int64_t* sr, int64_t* peak,
                           hipStream_t stream);

@@ -855,30 +855,20 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
 }
 
 // ---------------------------------------------------------------------------------------------
-__global__ void k_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q, int64_t* stats)
+// Query validation for one call: any length outside [1, 2^24] sets the error
+// word of every scenario, which makes every later kernel of the call a no-op.
+__global__ __launch_bounds__(256) void k_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q,
+                                                     Ctl* ctl, int32_t S)
 {
-    // stats: [0] bad count, [1] max l_in, [2] max l_pred, [3] max l_in + l_pred
-    int64_t bad = 0, mi = 0, mp = 0, ms = 0;
+    __shared__ int64_t red[4];
+    int64_t bad = 0;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < Q; i += (int64_t)gridDim.x * blockDim.x) {
         const int32_t a = lin[i], p = lpred[i];
-        const bool ok = a >= 1 && p >= 1 && a <= (1 << 24) && p <= (1 << 24);
-        bad += ok ? 0 : 1;
-        mi = a > mi ? a : mi;
-        mp = p > mp ? p : mp;
-        ms = (int64_t)a + p > ms ? (int64_t)a + p : ms;
+        bad += (a >= 1 && p >= 1 && a <= (1 << 24) && p <= (1 << 24)) ? 0 : 1;
     }
-    for (int d = 32; d > 0; d >>= 1) {
-        bad += __shfl_down(bad, d, 64);
-        int64_t o = __shfl_down(mi, d, 64); mi = o > mi ? o : mi;
-        o = __shfl_down(mp, d, 64); mp = o > mp ? o : mp;
-        o = __shfl_down(ms, d, 64); ms = o > ms ? o : ms;
-    }
-    if (lane_id() == 0) {
-        if (bad) atomicAdd((unsigned long long*)&stats[0], (unsigned long long)bad);
-        atomicMax((unsigned long long*)&stats[1], (unsigned long long)mi);
-        atomicMax((unsigned long long*)&stats[2], (unsigned long long)mp);
-        atomicMax((unsigned long long*)&stats[3], (unsigned long long)ms);
-    }
+    bad = block_reduce<256>(bad, 0, OpAdd(), red);
+    if (threadIdx.x == 0 && bad)
+        for (int s = 0; s < S; ++s) atomicCAS(&ctl[s].err, 0, DEV_EINVAL);
 }
 
 __global__ void k_summary(State st, int32_t W, int32_t* B, int64_t* sc, int64_t* sr, int64_t* peak)
@@ -932,13 +922,13 @@ hipError_t launch_commit(const State& st, int32_t blocks, hipStream_t stream)
     return hipGetLastError();
 }
 
-hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q, int64_t* stats,
+hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q, Ctl* ctl, int32_t S,
                               hipStream_t stream)
 {
     int blocks = (Q + 255) / 256;
-    if (blocks > 1024) blocks = 1024;
+    if (blocks > 256) blocks = 256;
     if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL(k_query_stats, dim3(blocks), dim3(256), 0, stream, lin, lpred, Q, stats);
+    hipLaunchKernelGGL(k_query_stats, dim3(blocks), dim3(256), 0, stream, lin, lpred, Q, ctl, S);
     return hipGetLastError();
 }
 
