@@ -159,11 +159,13 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
     int rc = ALD_OK;
 #define A(field, count) if ((rc = dalloc(h, a, &st.field, (size_t)(count))) != ALD_OK) return rc
     A(slot_base, NW); A(cap, NW); A(n, NW); A(head, NW); A(M, NW); A(S1, NW); A(S2, NW);
-    A(hbs, NW); A(dirty, NW); A(built, NW); A(B, NW); A(DS, NW); A(key, NW); A(peak, NW);
+    A(hbs, NW); A(built, NW); A(B, NW); A(DS, NW); A(key, NW); A(peak, NW);
     A(rhs, NW); A(SC, NW); A(SR, NW);
     A(e, slots); A(s, slots); A(pme, slots); A(sm, slots); A(ss, slots);
     Ctl* ctl = nullptr;
     TileInfo* ti = nullptr;
+    if ((rc = dalloc(h, a, &st.dlist, (size_t)a->S * MAX_DIRTY)) != ALD_OK) return rc;
+    if ((rc = dalloc(h, a, &st.dcount, a->S)) != ALD_OK) return rc;
     if ((rc = dalloc(h, a, &ctl, a->S)) != ALD_OK) return rc;
     if ((rc = dalloc(h, a, &ti, a->S)) != ALD_OK) return rc;
     if ((rc = dalloc(h, a, &a->dscen, a->S)) != ALD_OK) return rc;
@@ -176,12 +178,21 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
     HIPCHK(h, hipMemcpyAsync(st.slot_base, base.data(), NW * sizeof(int64_t), hipMemcpyHostToDevice, h->stream));
     HIPCHK(h, hipMemcpyAsync(st.cap, caps.data(), NW * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
     HIPCHK(h, hipMemcpyAsync(st.M, Ms.data(), NW * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
-    for (auto* p : {(void*)st.n, (void*)st.head, (void*)st.hbs, (void*)st.dirty, (void*)st.built, (void*)st.B,
+    for (auto* p : {(void*)st.n, (void*)st.head, (void*)st.hbs, (void*)st.built, (void*)st.B,
                     (void*)st.peak})
         HIPCHK(h, hipMemsetAsync(p, 0, NW * sizeof(int32_t), h->stream));
     for (auto* p : {(void*)st.S1, (void*)st.S2, (void*)st.DS, (void*)st.key, (void*)st.SC, (void*)st.SR,
                     (void*)st.rhs})
         HIPCHK(h, hipMemsetAsync(p, 0, NW * sizeof(int64_t), h->stream));
+    HIPCHK(h, hipMemsetAsync(st.dcount, 0, a->S * sizeof(int32_t), h->stream));
+    // empty workers of a scenario are interchangeable when they share one capacity
+    int64_t w0 = 0;
+    for (int s = 0; s < a->S; ++s) {
+        bool uni = true;
+        for (int32_t i = 1; i < W[s]; ++i) uni = uni && Ms[w0 + i] == Ms[w0];
+        a->hscen[s].uniform_M = uni ? 1 : 0;
+        w0 += W[s];
+    }
     return ALD_OK;
 }
 
@@ -194,7 +205,7 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
     int32_t wpb = (int32_t)std::max<int64_t>(1, (NWtot * nchunks + target_blocks - 1) / target_blocks);
     int64_t bits = 0, part = 0, qs = 0;
     int32_t eb = 0, sb = 0, cb = 0;
-    const int32_t nfin = std::min(64, std::max(1, nchunks / 8));
+    const int32_t nfin = std::min(256, std::max(1, nchunks / 2));
     for (int s = 0; s < a->S; ++s) {
         Scen& sc = a->hscen[s];
         sc.wpb = std::min(wpb, std::max(1, sc.W));
@@ -325,7 +336,9 @@ int run_rounds(ald_handle* h, Arena* a, bool build_every_round, std::vector<Ctl>
         int64_t need = rounds_needed(hc);
         if (need == 0) break;
         for (int64_t r = 0; r < need; ++r) {
-            if (build_every_round || first) LAUNCH(h, 0, launch_build(a->st, h->stream, 0));
+            // full check after a heartbeat can have moved tau; otherwise only the
+            // workers the previous commit touched
+            LAUNCH(h, 0, launch_build(a->st, h->stream, (build_every_round || first) ? 0 : 1));
             first = false;
             LAUNCH(h, 1, launch_eval(a->st, a->eval_blocks, h->stream));
             LAUNCH(h, 2, launch_select(a->st, a->sel_blocks, h->stream));
@@ -447,7 +460,7 @@ int ald_load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const 
     for (int i = 0; i < W; ++i) {
         const int64_t R = off[i + 1] - off[i];
         const int64_t c = std::max<int64_t>(R, bound) + 1;
-        if (c > (1 << 24)) return fail(h, ALD_EINVAL, "too many request slots per worker");
+        if (c > HOT) return fail(h, ALD_EINVAL, "more than " + std::to_string(HOT - 1) + " request slots per worker");
         caps[i] = (int32_t)c;
         Ms[i] = (int32_t)cap64[i];
         total += c + 1;
@@ -544,7 +557,7 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
     a->st.out_worker = out_worker;
     a->st.out_diag = (Diag*)out_diag;
     std::vector<Ctl> hc(1, c);
-    rc = run_rounds(h, a, true, hc);
+    rc = run_rounds(h, a, H > 0, hc);
     if (rc != ALD_OK) return rc;
     c = hc[0];
     h->tau = c.tau;
@@ -575,6 +588,9 @@ int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, i
         NW += scen[s].n_workers;
         int64_t b = batch_bound(scen[s].model);
         int64_t cap = (b < 0 ? (int64_t)Q : std::min<int64_t>(Q, b)) + 1;
+        if (cap > HOT)
+            return fail(h, ALD_EINVAL, "scenario " + std::to_string(s) + " admits more than " + std::to_string(HOT - 1) +
+                                           " requests per worker");
         slots += scen[s].n_workers * (cap + 1);
     }
     if (NW > (1 << 30)) return fail(h, ALD_EINVAL, "too many workers");
@@ -631,7 +647,7 @@ int ald_worker_summary(ald_handle_t h, int32_t* B, int64_t* sum_c, int64_t* sum_
     if (!h->main) return fail(h, ALD_ESTATE, "ald_load_workers has not been called");
     if (!B || !sum_c || !sum_r || !peak) return fail(h, ALD_EINVAL, "null argument");
     // bring every worker's summaries to the current decode iteration first
-    HIPCHK(h, launch_build(h->main->st, h->stream, 1));
+    HIPCHK(h, launch_build(h->main->st, h->stream, 2));
     HIPCHK(h, launch_summary(h->main->st, h->W, B, sum_c, sum_r, peak, h->stream));
     HIPCHK(h, hipStreamSynchronize(h->stream));
     return ALD_OK;

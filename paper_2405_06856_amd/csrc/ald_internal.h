@@ -33,7 +33,8 @@ namespace ald {
 constexpr int TOPK = 4;            // feasible candidates kept per query
 constexpr int EVAL_THREADS = 256;  // queries per pair-evaluation block
 constexpr int SEL_THREADS = 256;   // queries per selection block
-constexpr int COMMIT_THREADS = 256;
+constexpr int COMMIT_THREADS = 64;  // the arrival-order commit runs as one wave
+constexpr int HOT = 8192;          // most request slots per worker (commit keeps one worker in LDS)
 constexpr int BUILD_THREADS = 256;
 constexpr int MAX_DIRTY = 64;      // workers changed within one tile before the tile is cut
 constexpr int32_t NEG = INT32_MIN;
@@ -54,6 +55,8 @@ struct Scen {
     int32_t sel_blk0;   // first selection block
     int32_t fin_blk0;   // first commit block (1 sequential + nfin finalizers)
     int32_t nfin;
+    int32_t uniform_M;  // every worker has the same capacity: empty workers are interchangeable
+    int32_t pad0;
     int64_t bits_off;   // uint64 words into bits_feas / bits_nt
     int64_t part_off;   // int4 entries into part
     int64_t qsum_off;   // QSum entries into qsum
@@ -86,14 +89,18 @@ struct TileInfo {
     int32_t first_pc[2];  // first query of the tile with a feasible worker (by round parity)
 };
 
-// Per-query result of the selection kernel (tile-start state).
+// Per-query result of the selection kernel (tile-start state).  With
+// interchangeable empty workers (uniform capacity), empty workers are not listed
+// one by one: `efeas` says whether an empty worker is feasible (all are alike).
 struct QSum {
-    uint64_t tkey[TOPK];  // best feasible workers: rank keys, descending
+    uint64_t tkey[TOPK];  // best feasible listed workers: rank keys, descending
     int32_t tw[TOPK];     // their indices (-1 = none)
     uint64_t ntkey;       // best-ranked worker with a near-tie margin
     int32_t ntw;          // its index (-1 = none)
     int32_t ntcnt;        // workers with a near-tie margin
-    int32_t nfeas;        // feasible workers
+    int32_t nfeas;        // feasible workers (all kinds)
+    int32_t ncand;        // feasible workers of the listed kind
+    int32_t efeas;        // an empty worker is feasible
     int32_t ex1, w1;      // smallest KV excess (ties: highest index first)
     int32_t ex2, w2;      // second smallest
     int32_t pad;
@@ -119,7 +126,6 @@ struct State {
     int64_t* S1;
     int64_t* S2;
     int32_t* hbs;      // heartbeat stamp of S1/S2
-    int32_t* dirty;    // round stamp of the last commit
     int32_t* built;
     int32_t* B;
     int64_t* DS;       // 2^gs * sum(c) + gn * sum(r)
@@ -138,6 +144,8 @@ struct State {
     const Scen* scen;
     Ctl* ctl;
     TileInfo* tinfo;
+    int32_t* dlist;    // [S * MAX_DIRTY] workers changed in the last tile (global index)
+    int32_t* dcount;   // [S]
     int32_t S;
     int32_t NW;
     // tile scratch
@@ -166,7 +174,9 @@ inline __host__ __device__ int32_t tile_end(int32_t start, int32_t Q, int32_t T,
 // host-side launchers (ald_kernels.hip)
 hipError_t launch_ingest(const State& st, int32_t W, const int64_t* res_off, const int32_t* lin,
                          const int32_t* lpred, const int32_t* gen, hipStream_t stream);
-hipError_t launch_build(const State& st, hipStream_t stream, int force);
+// mode 0: every worker whose summaries are stale; 1: only the workers listed by
+// the last commit; 2: every worker unconditionally
+hipError_t launch_build(const State& st, hipStream_t stream, int mode);
 hipError_t launch_eval(const State& st, int32_t blocks, hipStream_t stream);
 hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream);
 hipError_t launch_commit(const State& st, int32_t blocks, hipStream_t stream);

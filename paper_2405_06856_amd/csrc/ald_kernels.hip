@@ -389,17 +389,25 @@ __global__ __launch_bounds__(BUILD_THREADS) void k_ingest(State st, const int64_
         st.S1[gw] = 0;
         st.S2[gw] = 0;
         st.hbs[gw] = -1;
-        st.dirty[gw] = 0;
     }
 }
 
 // ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(BUILD_THREADS) void k_build(State st, int force)
+__global__ __launch_bounds__(BUILD_THREADS) void k_build(State st, int mode)
 {
-    const int gw = blockIdx.x;
-    const int s = find_scen_by_worker(st, gw);
+    int gw, s;
+    if (mode == 1) {
+        s = blockIdx.x / MAX_DIRTY;
+        const int j = blockIdx.x % MAX_DIRTY;
+        if (s >= st.S || j >= st.dcount[s]) return;
+        gw = st.dlist[s * MAX_DIRTY + j];
+        if (st.built[gw]) return;
+    } else {
+        gw = blockIdx.x;
+        s = find_scen_by_worker(st, gw);
+    }
     const Ctl* c = st.ctl + s;
-    if (!force) {
+    if (mode == 0) {
         if (c->err || c->start >= c->Q) return;
         if (!c->rebuild && st.built[gw]) return;
     }
@@ -481,7 +489,8 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     int32_t tw[TOPK];
 #pragma unroll
     for (int k = 0; k < TOPK; ++k) { tkey[k] = 0; tw[k] = -1; }
-    int32_t nfeas = 0, ntcnt = 0, ntw = -1;
+    int32_t nfeas = 0, ntcnt = 0, ntw = -1, ncand = 0;
+    bool efeas = false;
     uint64_t ntkey = 0;
     const int64_t row = sc.bits_off + (int64_t)((qi - start) >> 6) * sc.W;
     for (int w = 0; w < sc.W; ++w) {
@@ -492,7 +501,12 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
         const bool f = (fw >> lane) & 1;
         const bool nb = (nw >> lane) & 1;
         nfeas += f ? 1 : 0;
-        topk_insert<TOPK>(tkey, tw, key, f ? w : -1);
+        // an empty worker has rank key 0; with uniform capacity all empty
+        // workers are alike and stand in one class
+        const bool cls = sc.uniform_M && key == 0;
+        efeas = efeas | (cls & f);
+        ncand += (f & !cls) ? 1 : 0;
+        topk_insert<TOPK>(tkey, tw, key, (f && !cls) ? w : -1);
         ntcnt += nb ? 1 : 0;
         const bool better = nb & ranks_before(key, w, ntkey, ntw);
         ntkey = better ? key : ntkey;
@@ -515,6 +529,8 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     q.ntw = ntw;
     q.ntcnt = ntcnt;
     q.nfeas = nfeas;
+    q.ncand = ncand;
+    q.efeas = efeas ? 1 : 0;
     q.ex1 = ex1; q.w1 = w1;
     q.ex2 = ex2; q.w2 = w2;
     q.pad = 0;
@@ -523,101 +539,436 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
 }
 
 // ---------------------------------------------------------------------------------------------
-// Commit.
+// Commit.  One wave per scenario walks the tile in arrival order.  Workers
+// committed to earlier in the tile ("dirty") are re-evaluated from their live
+// aggregates, kept in LDS; the worker last committed to keeps its live request
+// columns in LDS.  A commit updates the columns in LDS, writes them through to
+// HBM and only marks the worker's summaries stale: the build kernel of the next
+// round rebuilds them.  Columns this wave wrote are read back only with
+// device-coherent loads after a release fence.
 
-struct Resolved {
-    int32_t w;        // chosen worker (scenario-local), -1 = rejected
-    int32_t abort;    // the tile-start lists cannot decide this query exactly
+constexpr int DBITS_W = 2048;  // dirty bitmap words in LDS: scenarios of up to 65536 workers
+
+// ---- cross-lane primitives of the commit wave (DPP and readlane; no LDS
+// permutes on the sequential path)
+
+__device__ __forceinline__ int32_t rdlane(int32_t v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ uint64_t rdlane64(uint64_t v, int l)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ int64_t rdlane64s(int64_t v, int l) { return (int64_t)rdlane64((uint64_t)v, l); }
+__device__ __forceinline__ double rdlane_f64(double v, int l)
+{
+    return __builtin_bit_cast(double, rdlane64(__builtin_bit_cast(uint64_t, v), l));
+}
+
+// Inclusive scan over the 64 lanes (lane 0 first) with DPP row shifts and row
+// broadcasts; lanes without a source keep the identity.
+template <typename Op>
+__device__ __forceinline__ int32_t wave_incl_scan(int32_t x, int32_t ident, Op op)
+{
+    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x111, 0xf, 0xf, false));  // row_shr:1
+    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x112, 0xf, 0xf, false));  // row_shr:2
+    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x114, 0xf, 0xf, false));  // row_shr:4
+    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x118, 0xf, 0xf, false));  // row_shr:8
+    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x142, 0xa, 0xf, false));  // row_bcast:15
+    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x143, 0xc, 0xf, false));  // row_bcast:31
+    return x;
+}
+struct Add32 {
+    __device__ int32_t operator()(int32_t a, int32_t b) const { return a + b; }
+};
+struct Max32 {
+    __device__ int32_t operator()(int32_t a, int32_t b) const { return a > b ? a : b; }
+};
+__device__ __forceinline__ int32_t wave_sum32(int32_t v) { return rdlane(wave_incl_scan(v, 0, Add32()), 63); }
+__device__ __forceinline__ int32_t wave_max32(int32_t v) { return rdlane(wave_incl_scan(v, INT32_MIN, Max32()), 63); }
+__device__ __forceinline__ int64_t wave_sum64(int64_t v)
+{
+#pragma unroll
+    for (int d = 32; d > 0; d >>= 1) v += __shfl_xor(v, d, 64);
+    return v;
+}
+
+// Lane holding the best (key, index) by Algorithm 1's order among lanes with
+// `valid`, or -1.  A scalar walk over the (few) candidate lanes.
+__device__ __forceinline__ int wave_best_lane(uint64_t key, int32_t w, bool valid)
+{
+    uint64_t m = __ballot(valid);
+    int best = -1;
+    uint64_t bk = 0;
+    int32_t bw = -1;
+    while (m) {
+        const int l = __ffsll((unsigned long long)m) - 1;
+        m &= m - 1;
+        const uint64_t k = rdlane64(key, l);
+        const int32_t ww = rdlane(w, l);
+        if (ranks_before(k, ww, bk, bw)) {
+            best = l;
+            bk = k;
+            bw = ww;
+        }
+    }
+    return best;
+}
+
+// Column element: plain LDS read, or a device-coherent global read of data
+// that this wave may have written earlier in the launch.
+template <bool GLOBAL>
+__device__ __forceinline__ int32_t col(const int32_t* p, int k)
+{
+    if (GLOBAL) return __hip_atomic_load(p + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return p[k];
+}
+
+// KV demand peak with the query added, from a worker's live columns e, s
+// (B entries sorted by e).  All lanes take part; all get the result.  Lane l
+// takes chunk 63 - l, so a prefix over lanes is a suffix over slots.  Every
+// partial sum here is a token count below 2^31 (checked at the boundary).
+template <bool GLOBAL>
+__device__ int64_t wave_kv_peak(const int32_t* e, const int32_t* s, int B, int32_t sq, int32_t eq)
+{
+    const int lane = lane_id();
+    const int CH = (B + 63) >> 6;
+    const int c = 63 - lane;
+    const int k0 = min(B, c * CH);
+    const int k1 = min(B, k0 + CH);
+    int32_t ls = 0;
+    for (int k = k0; k < k1; ++k) ls += col<GLOBAL>(s, k);
+    int64_t run = (int64_t)(wave_incl_scan(ls, 0, Add32()) - ls);  // slots after this chunk
+    int32_t best = INT32_MIN, ssge = 0, cge = 0;
+    for (int k = k1 - 1; k >= k0; --k) {
+        const int32_t ek = col<GLOBAL>(e, k), sk = col<GLOBAL>(s, k);
+        run += sk;  // sum of s over slots >= k
+        const int64_t P = run + (int64_t)(B - k) * ek;
+        const bool before = ek < eq;  // the query is still alive at this end point
+        const int32_t val = (int32_t)(before ? P + sq + ek : P);
+        best = val > best ? val : best;
+        ssge += before ? 0 : sk;
+        cge += before ? 0 : 1;
+    }
+    const int64_t bmax = wave_max32(best);
+    const int64_t own = (int64_t)wave_sum32(ssge) + (int64_t)wave_sum32(cge) * eq + sq + eq;
+    return bmax > own ? bmax : own;
+}
+
+// The same, evaluated by one lane alone.
+template <bool GLOBAL>
+__device__ int64_t lane_kv_peak(const int32_t* e, const int32_t* s, int B, int32_t sq, int32_t eq)
+{
+    int64_t run = 0, best = INT64_MIN, ssge = 0, cge = 0;
+    for (int k = B - 1; k >= 0; --k) {
+        const int32_t ek = col<GLOBAL>(e, k), sk = col<GLOBAL>(s, k);
+        run += sk;
+        const int64_t P = run + (int64_t)(B - k) * ek;
+        const bool before = ek < eq;
+        const int64_t val = before ? P + sq + ek : P;
+        best = val > best ? val : best;
+        ssge += before ? 0 : sk;
+        cge += before ? 0 : 1;
+    }
+    const int64_t own = ssge + cge * eq + sq + eq;
+    return best > own ? best : own;
+}
+
+// A worker committed to earlier in the tile.
+struct DAgg {
+    int32_t w;       // scenario-local index
+    int32_t B, n, head, M, hbs;
+    int32_t empty0;  // it was empty when the tile started
+    int32_t cap;
+    int64_t base;    // first slot
+    int64_t DS, S1, S2, SC, SR;
+    uint64_t key;
+    double rhs;
+};
+
+// Orders LDS traffic between the lanes of the (single-wave) commit block
+// without waiting for outstanding global memory operations.
+__device__ __forceinline__ void wave_sync() { __builtin_amdgcn_wave_barrier(); }
+
+// Bit words of the tile-start feasibility / near-tie masks that cover one
+// 64-query window, cached per dirty worker (one worker per lane).
+struct WinBits {
+    uint64_t f0, f1, n0, n1;
+};
+
+__device__ __forceinline__ WinBits load_win_bits(const State& st, const Scen& sc, int w, int start, int w0, int end)
+{
+    WinBits b;
+    const int64_t g0 = (w0 - start) >> 6;
+    const int64_t row0 = sc.bits_off + g0 * sc.W + w;
+    b.f0 = st.bits_feas[row0];
+    b.n0 = st.bits_nt[row0];
+    const bool two = (int64_t)(end - start) > (g0 + 1) * 64;
+    b.f1 = two ? st.bits_feas[row0 + sc.W] : 0;
+    b.n1 = two ? st.bits_nt[row0 + sc.W] : 0;
+    return b;
+}
+
+// bit of query i (tile offset) in a cached window
+__device__ __forceinline__ bool win_bit(uint64_t lo, uint64_t hi, int start, int w0, int i)
+{
+    const int g = ((i - start) >> 6) - ((w0 - start) >> 6);
+    const uint64_t word = g == 0 ? lo : hi;
+    return (word >> ((i - start) & 63)) & 1;
+}
+
+__device__ __forceinline__ View dagg_view(const DAgg& a, int32_t hb)
+{
+    View v;
+    v.e = v.pme = v.sm = v.ss = nullptr;
+    v.head = a.head;
+    v.n = a.n;
+    v.M = a.M;
+    v.DS = a.DS;
+    const bool cur = a.hbs == hb;
+    v.S1 = cur ? a.S1 : 0;
+    v.S2 = cur ? a.S2 : 0;
+    v.key = a.key;
+    v.rhs = a.rhs;
+    return v;
+}
+
+// Per-launch commit state held in LDS.
+struct CommitLDS {
+    DAgg dag[MAX_DIRTY];
+    uint32_t dbits[DBITS_W];
+    int32_t he[HOT];
+    int32_t hs[HOT];
+};
+
+// Is worker w (scenario-local) dirty in this tile?
+__device__ __forceinline__ bool dirty_w(const CommitLDS& L, int W, int nd, int w)
+{
+    if (W <= DBITS_W * 32) return (L.dbits[w >> 5] >> (w & 31)) & 1u;
+    bool d = false;
+    for (int j = 0; j < nd; ++j) d = d | (L.dag[j].w == w);
+    return d;
+}
+
+// dag entry of a dirty worker (wave-cooperative; -1 if absent)
+__device__ __forceinline__ int dag_slot(const CommitLDS& L, int nd, int w)
+{
+    const int lane = lane_id();
+    const uint64_t m = __ballot(lane < nd && L.dag[lane < nd ? lane : 0].w == w);
+    return m ? __ffsll((unsigned long long)m) - 1 : -1;
+}
+
+// Lowest-index worker at or after `from` that is empty and untouched in this
+// tile (wave-cooperative; -1 if none).  Empty workers have rank key 0.
+__device__ int next_empty_worker(const State& st, const Scen& sc, const CommitLDS& L, int nd, int from)
+{
+    for (int base = from; base < sc.W; base += 64) {
+        const int w = base + lane_id();
+        const bool emp = w < sc.W && st.key[sc.wbase + w] == 0 && !dirty_w(L, sc.W, nd, w);
+        const uint64_t m = __ballot(emp);
+        if (m) return base + __ffsll((unsigned long long)m) - 1;
+    }
+    return -1;
+}
+
+struct QView {  // the committing query's summary, broadcast to the whole wave
+    uint64_t tkey[TOPK];
+    int32_t tw[TOPK];
+    uint64_t ntkey;
+    int32_t ntw, ntcnt, nfeas, ncand, efeas, ex1, w1, ex2, w2;
+};
+
+__device__ __forceinline__ QView broadcast_q(const QSum& q, int p)
+{
+    QView v;
+#pragma unroll
+    for (int k = 0; k < TOPK; ++k) {
+        v.tkey[k] = rdlane64(q.tkey[k], p);
+        v.tw[k] = rdlane(q.tw[k], p);
+    }
+    v.ntkey = rdlane64(q.ntkey, p);
+    v.ntw = rdlane(q.ntw, p);
+    v.ntcnt = rdlane(q.ntcnt, p);
+    v.nfeas = rdlane(q.nfeas, p);
+    v.ncand = rdlane(q.ncand, p);
+    v.efeas = rdlane(q.efeas, p);
+    v.ex1 = rdlane(q.ex1, p);
+    v.w1 = rdlane(q.w1, p);
+    v.ex2 = rdlane(q.ex2, p);
+    v.w2 = rdlane(q.w2, p);
+    return v;
+}
+
+// Diagnostics of a query with no feasible worker at tile start (so none now),
+// decided by its own lane.
+__device__ Diag reject_diag(const State& st, const Scen& sc, const QSum& q, int i, int start, int w0, int32_t lin,
+                            int32_t lp, int32_t tau, int32_t hb, const CommitLDS& L, int nd, int hot,
+                            const WinBits& wb, int* abort)
+{
+    Diag d;
+    d.n_feasible = 0;
+    d.kv_peak_chosen = 0;
+    d.ttft_chosen = 0.0;
+    d.tdec_chosen = 0.0;
+    d.kv_excess_min = 0;
+    d.near_tie = 0;
+    *abort = 0;
+    const int32_t sq = lin - tau, eq = lp + tau;
+    int64_t exmin = q.ex1;
+    if (q.w1 >= 0 && dirty_w(L, sc.W, nd, q.w1)) {
+        if (q.w2 >= 0 && dirty_w(L, sc.W, nd, q.w2)) {
+            *abort = 1;
+            return d;
+        }
+        int j = 0;
+        while (j < nd && L.dag[j].w != q.w1) ++j;
+        const DAgg& a = L.dag[j];
+        const int64_t base = a.base + a.head;
+        const int64_t pk = (j == hot) ? lane_kv_peak<false>(L.he, L.hs, a.B, sq, eq)
+                                      : lane_kv_peak<true>(st.e + base, st.s + base, a.B, sq, eq);
+        const int64_t ex_now = pk - a.M;
+        exmin = q.w2 < 0 ? ex_now : (ex_now < q.ex2 ? ex_now : (int64_t)q.ex2);
+    }
+    d.kv_excess_min = exmin;
+    // near tie over every worker (the query is rejected)
+    int clean_nt = q.ntcnt;
+    bool nt = false;
+    for (int j = 0; j < nd; ++j) {
+        const DAgg& a = L.dag[j];
+        const uint64_t n0 = rdlane64(wb.n0, j), n1 = rdlane64(wb.n1, j);
+        clean_nt -= win_bit(n0, n1, start, w0, i) ? 1 : 0;
+        nt = nt | latency(sc, dagg_view(a, hb), lin, lp, a.B + 1).nt;
+    }
+    nt = nt | (clean_nt > 0);
+    d.near_tie = nt ? 1 : 0;
+    return d;
+}
+
+struct Decision {
+    int32_t w;      // chosen worker, -1 = rejected
+    int32_t abort;  // the tile-start lists cannot decide this query exactly
     Diag d;
 };
 
-// Decide query i (and its diagnostics) at the current state, using the
-// tile-start summary q for workers untouched in this tile and re-evaluating
-// the workers committed to earlier in the tile (dl[0..nd)).
-__device__ Resolved resolve(const State& st, const Scen& sc, const QSum& q, int i, int start,
-                            int32_t lin, int32_t lp, int32_t tau, int32_t hb, int32_t stamp,
-                            const int32_t* dl, int nd, bool want_diag)
+// Decide one query with the whole wave.
+__device__ Decision decide(const State& st, const Scen& sc, const QView& q, int i, int start, int w0, int32_t lin,
+                           int32_t lp, int32_t tau, int32_t hb, const CommitLDS& L, int nd, int hot,
+                           int next_empty, bool want_diag, const WinBits& wb)
 {
-    Resolved r;
-    r.abort = 0;
+    Decision r;
     r.w = -1;
+    r.abort = 0;
+    r.d.n_feasible = 0;
+    r.d.near_tie = 0;
+    r.d.kv_peak_chosen = 0;
+    r.d.kv_excess_min = 0;
+    r.d.ttft_chosen = 0.0;
+    r.d.tdec_chosen = 0.0;
+    const int lane = lane_id();
     const int32_t sq = lin - tau, eq = lp + tau;
+    // best untouched candidate from the tile-start list
     bool have = false;
     uint64_t bk = 0;
     int32_t bw = -1;
-    int32_t nf = q.nfeas;
-    if (!want_diag && q.nfeas == 0) return r;  // rejected whatever changed in the tile
-    const int lim = q.nfeas < TOPK ? q.nfeas : TOPK;
+    const int lim = q.ncand < TOPK ? q.ncand : TOPK;
 #pragma unroll
     for (int k = 0; k < TOPK; ++k) {
         const int w = q.tw[k];
-        const bool clean = (k < lim) && (w >= 0) && (st.dirty[sc.wbase + (w >= 0 ? w : 0)] != stamp);
+        const bool clean = (k < lim) && (w >= 0) && !dirty_w(L, sc.W, nd, w >= 0 ? w : 0);
         const bool take = clean & !have;
         bk = take ? q.tkey[k] : bk;
         bw = take ? w : bw;
         have = have | take;
     }
-    if (!have && q.nfeas > TOPK) { r.abort = 1; return r; }
-    const int64_t word = sc.bits_off + (int64_t)((i - start) >> 6) * sc.W;
-    const int bit = (i - start) & 63;
-    int32_t clean_nt = q.ntcnt;
-    uint64_t dntk = 0;
-    int32_t dntw = -1;
-    int64_t chosen_peak = 0;
-    bool chosen_peak_known = false;
-    for (int j = 0; j < nd; ++j) {
-        const int d = dl[j];
-        const int gw = sc.wbase + d;
-        const bool fs = (st.bits_feas[word + d] >> bit) & 1;
-        const bool ns = (st.bits_nt[word + d] >> bit) & 1;
-        clean_nt -= ns ? 1 : 0;
-        const View v = load_view(st, gw, hb);
-        const Latency L = latency(sc, v, lin, lp, v.n - v.head + 1);
-        nf -= fs ? 1 : 0;
-        bool feas_now = false;
-        int64_t peak = 0;
-        if (fs && L.dec_ok && L.ttft_ok) {
-            peak = kv_peak_with(v, sq, eq);
-            feas_now = peak <= v.M;
-        }
-        nf += feas_now ? 1 : 0;
-        const bool better = feas_now & ranks_before(v.key, d, bk, bw);
-        bk = better ? v.key : bk;
-        bw = better ? d : bw;
-        have = have | better;
-        chosen_peak = better ? peak : chosen_peak;
-        chosen_peak_known = better | (chosen_peak_known & !better);
-        const bool ntb = L.nt & ranks_before(v.key, d, dntk, dntw);
-        dntk = ntb ? v.key : dntk;
-        dntw = ntb ? d : dntw;
+    if (!have && q.ncand > TOPK) {
+        r.abort = 1;
+        return r;
     }
-    const bool dnt = dntw >= 0;
+    if (!have && sc.uniform_M && q.efeas && next_empty >= 0) {
+        have = true;
+        bk = 0;
+        bw = next_empty;
+    }
+    // workers changed earlier in the tile: one per lane
+    const bool valid = lane < nd;
+    DAgg a;
+    a.w = -1;
+    a.B = a.n = a.head = a.M = a.hbs = a.empty0 = a.cap = 0;
+    a.base = 0;
+    a.DS = a.S1 = a.S2 = a.SC = a.SR = 0;
+    a.key = 0;
+    a.rhs = 0.0;
+    if (valid) a = L.dag[lane];
+    bool fs = false, ns = false;
+    Latency Lt;
+    Lt.dec_ok = Lt.ttft_ok = Lt.nt = false;
+    Lt.lhs = Lt.ttft = Lt.tdec = 0.0;
+    if (valid) {
+        fs = (sc.uniform_M && a.empty0) ? (q.efeas != 0) : win_bit(wb.f0, wb.f1, start, w0, i);
+        ns = win_bit(wb.n0, wb.n1, start, w0, i);
+        Lt = latency(sc, dagg_view(a, hb), lin, lp, a.B + 1);
+    }
+    bool unknown = valid && fs && Lt.dec_ok && Lt.ttft_ok;  // KV check still needed
+    bool feas_now = false;
+    int64_t peak_now = 0;
+    // evaluate candidates best-first; without diagnostics stop at the first
+    // feasible one ranked above the current best
+    for (;;) {
+        const bool cand = unknown && (want_diag || ranks_before(a.key, a.w, bk, bw));
+        const int bl = wave_best_lane(a.key, a.w, cand);
+        if (bl < 0) break;
+        const int32_t cB = rdlane(a.B, bl);
+        const int32_t chead = rdlane(a.head, bl);
+        const int32_t cM = rdlane(a.M, bl);
+        const int64_t base = rdlane64s(a.base, bl) + chead;
+        const int64_t pk = (bl == hot) ? wave_kv_peak<false>(L.he, L.hs, cB, sq, eq)
+                                       : wave_kv_peak<true>(st.e + base, st.s + base, cB, sq, eq);
+        const bool ok = pk <= cM;
+        if (lane == bl) {
+            unknown = false;
+            feas_now = ok;
+            peak_now = pk;
+        }
+        if (!want_diag && ok) break;
+    }
+    const bool fdirty = valid && feas_now;
+    const int bl = wave_best_lane(a.key, a.w, fdirty);
+    if (bl >= 0) {
+        const uint64_t dk = rdlane64(a.key, bl);
+        const int32_t dw = rdlane(a.w, bl);
+        if (!have || ranks_before(dk, dw, bk, bw)) {
+            have = true;
+            bk = dk;
+            bw = dw;
+        }
+    }
     r.w = have ? bw : -1;
     if (!want_diag) return r;
 
-    r.d.n_feasible = nf;
-    // smallest KV excess over all workers at the current state
-    int64_t exmin;
-    if (q.w1 >= 0 && st.dirty[sc.wbase + q.w1] == stamp) {
-        const View v = load_view(st, sc.wbase + q.w1, hb);
-        const int64_t ex_now = kv_peak_with(v, sq, eq) - v.M;
-        if (q.w2 < 0) {
-            exmin = ex_now;
-        } else if (st.dirty[sc.wbase + q.w2] != stamp) {
-            exmin = ex_now < q.ex2 ? ex_now : (int64_t)q.ex2;
-        } else {
+    // ---- diagnostics at the current state
+    r.d.n_feasible = q.nfeas - __popcll(__ballot(valid && fs)) + __popcll(__ballot(fdirty));
+    // smallest KV excess
+    int64_t exmin = q.ex1;
+    if (q.w1 >= 0 && dirty_w(L, sc.W, nd, q.w1)) {
+        if (q.w2 >= 0 && dirty_w(L, sc.W, nd, q.w2)) {
             r.abort = 1;
             return r;
         }
-    } else {
-        exmin = q.ex1;
+        const int j = dag_slot(L, nd, q.w1);
+        const int32_t jB = rdlane(a.B, j), jhead = rdlane(a.head, j), jM = rdlane(a.M, j);
+        const int64_t base = rdlane64s(a.base, j) + jhead;
+        const int64_t pk = (j == hot) ? wave_kv_peak<false>(L.he, L.hs, jB, sq, eq)
+                                      : wave_kv_peak<true>(st.e + base, st.s + base, jB, sq, eq);
+        const int64_t ex_now = pk - jM;
+        exmin = q.w2 < 0 ? ex_now : (ex_now < q.ex2 ? ex_now : (int64_t)q.ex2);
     }
     r.d.kv_excess_min = exmin;
-    // near tie among workers ranked at or above the choice (all if rejected)
+    // near tie among workers ranked at or above the choice (all when rejected)
+    const int clean_nt = q.ntcnt - __popcll(__ballot(valid && ns));
     bool nt = false;
     if (clean_nt > 0) {
-        if (q.ntw >= 0 && st.dirty[sc.wbase + q.ntw] != stamp) {
-            if (r.w < 0 || !ranks_before(bk, bw, q.ntkey, q.ntw)) nt = true;
+        if (q.ntw >= 0 && !dirty_w(L, sc.W, nd, q.ntw)) {
+            nt = r.w < 0 || !ranks_before(bk, bw, q.ntkey, q.ntw);
         } else if (r.w < 0) {
             nt = true;
         } else {
@@ -625,88 +976,26 @@ __device__ Resolved resolve(const State& st, const Scen& sc, const QSum& q, int 
             return r;
         }
     }
-    if (dnt && (r.w < 0 || !ranks_before(bk, bw, dntk, dntw))) nt = true;
+    const bool dnt = valid && Lt.nt && (r.w < 0 || !ranks_before(bk, bw, a.key, a.w));
+    nt = nt | (__ballot(dnt) != 0);
     r.d.near_tie = nt ? 1 : 0;
+    // the chosen worker's figures
     if (r.w >= 0) {
-        const View v = load_view(st, sc.wbase + r.w, hb);
-        const Latency L = latency(sc, v, lin, lp, v.n - v.head + 1);
-        r.d.kv_peak_chosen = chosen_peak_known ? chosen_peak : kv_peak_with(v, sq, eq);
-        r.d.ttft_chosen = L.ttft;
-        r.d.tdec_chosen = L.tdec;
-    } else {
-        r.d.kv_peak_chosen = 0;
-        r.d.ttft_chosen = 0.0;
-        r.d.tdec_chosen = 0.0;
+        const int j = dag_slot(L, nd, r.w);
+        if (j >= 0) {
+            r.d.kv_peak_chosen = rdlane64s(peak_now, j);
+            r.d.ttft_chosen = rdlane_f64(Lt.ttft, j);
+            r.d.tdec_chosen = rdlane_f64(Lt.tdec, j);
+        } else {
+            // untouched in this tile: its summaries are current
+            const View v = load_view(st, sc.wbase + r.w, hb);
+            const Latency Lc = latency(sc, v, lin, lp, v.n - v.head + 1);
+            r.d.kv_peak_chosen = kv_peak_with(v, sq, eq);
+            r.d.ttft_chosen = Lc.ttft;
+            r.d.tdec_chosen = Lc.tdec;
+        }
     }
     return r;
-}
-
-// Insert one request into worker gw (whole block) and rebuild its summaries.
-__device__ bool commit_insert(const State& st, const Scen& sc, int gw, int32_t lin, int32_t lp, int32_t tau,
-                              int32_t hb, int32_t* err)
-{
-    constexpr int NT = COMMIT_THREADS;
-    __shared__ int64_t red[NT / 64];
-    const int tid = threadIdx.x;
-    const int64_t base = st.slot_base[gw];
-    int32_t* e = st.e + base;
-    int32_t* s = st.s + base;
-    int32_t* t1 = st.pme + base;  // scratch: summaries are rebuilt right after
-    int32_t* t2 = st.sm + base;
-    int n = st.n[gw];
-    int head = st.head[gw];
-    const int cap = st.cap[gw];
-    if (n >= cap) {
-        if (head == 0) {
-            if (tid == 0) raise_error(err, DEV_ESLOTS);
-            __syncthreads();
-            return false;
-        }
-        for (int k = head + tid; k < n; k += NT) { t1[k] = e[k]; t2[k] = s[k]; }
-        __syncthreads();
-        for (int k = head + tid; k < n; k += NT) { e[k - head] = t1[k]; s[k - head] = t2[k]; }
-        __syncthreads();
-        n -= head;
-        head = 0;
-    }
-    const int32_t eq = lp + tau, sq = lin - tau;
-    int64_t le = 0;
-    for (int k = head + tid; k < n; k += NT) le += (e[k] <= eq) ? 1 : 0;
-    const int u = head + (int)block_reduce<NT>(le, 0, OpAdd(), red);
-    for (int k = u + tid; k < n; k += NT) { t1[k] = e[k]; t2[k] = s[k]; }
-    __syncthreads();
-    for (int k = u + tid; k < n; k += NT) { e[k + 1] = t1[k]; s[k + 1] = t2[k]; }
-    if (tid == 0) {
-        e[u] = eq;
-        s[u] = sq;
-        st.n[gw] = n + 1;
-        st.head[gw] = head;
-        const bool cur = st.hbs[gw] == hb;
-        const int64_t S1 = (cur ? st.S1[gw] : 0) + lin;
-        const int64_t S2 = (cur ? st.S2[gw] : 0) + (int64_t)lin * lin;
-        if (S2 >= ((int64_t)1 << 53)) raise_error(err, DEV_EOVERFLOW);
-        st.S1[gw] = S1;
-        st.S2[gw] = S2;
-        st.hbs[gw] = hb;
-    }
-    __syncthreads();
-    build_worker(st, sc, gw, tau, err);
-    return true;
-}
-
-__device__ __forceinline__ int block_min_int(int v, int* lds)
-{
-    // lds: COMMIT_THREADS/64 ints
-    for (int d = 32; d > 0; d >>= 1) {
-        int o = __shfl_down(v, d, 64);
-        v = o < v ? o : v;
-    }
-    if (lane_id() == 0) lds[wave_id()] = v;
-    __syncthreads();
-    int m = lds[0];
-    for (int j = 1; j < COMMIT_THREADS / 64; ++j) m = lds[j] < m ? lds[j] : m;
-    __syncthreads();
-    return m;
 }
 
 __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
@@ -717,10 +1006,7 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
     const int part = blockIdx.x - sc.fin_blk0;
     const TileInfo ti = st.tinfo[s];
     Ctl* cp = st.ctl + s;
-    const int tid = threadIdx.x;
-    __shared__ int mins[NT / 64];
-    __shared__ int64_t red[NT / 64];
-
+    const int lane = threadIdx.x;
     if (ti.start >= ti.end) return;
     const int32_t start = ti.start, end = ti.end;
     const int32_t fpc = min(ti.first_pc[ti.parity], end);
@@ -729,7 +1015,7 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
         // queries before the first one with any feasible worker: rejected, and
         // no worker of the tile has changed yet when they are decided
         int64_t cnt = 0;
-        for (int i = start + (part - 1) * NT + tid; i < fpc; i += sc.nfin * NT) {
+        for (int i = start + (part - 1) * NT + lane; i < fpc; i += sc.nfin * NT) {
             const QSum& q = st.qsum[sc.qsum_off + (i - start)];
             if (st.out_worker) st.out_worker[sc.out_off + i] = -1;
             if (st.out_diag) {
@@ -744,31 +1030,38 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
             }
             ++cnt;
         }
-        cnt = block_reduce<NT>(cnt, 0, OpAdd(), red);
-        if (tid == 0 && cnt > 0) atomicAdd(&cp->n_rej, (int)cnt);
-        if (tid == 0 && part == 1 && fpc > start) atomicMin(&cp->first_rej, start);
+        cnt = wave_sum64(cnt);
+        if (lane == 0 && cnt > 0) atomicAdd(&cp->n_rej, (int)cnt);
+        if (lane == 0 && part == 1 && fpc > start) atomicMin(&cp->first_rej, start);
         return;
     }
 
-    // ---- sequential block
+    // ---- the sequential wave
     const Ctl c = *cp;
     if (c.err) return;
     const int32_t tau = c.tau, hb = c.hb_index;
-    const int32_t stamp = c.round + 1;
-    __shared__ int32_t dl[MAX_DIRTY];
-    __shared__ int nd;
-    __shared__ int32_t sh_w, sh_lin, sh_lp;
-    if (tid == 0) {
-        nd = 0;
-        cp->rebuild = 0;
-    }
-    __syncthreads();
+    __shared__ CommitLDS L;
+    if (sc.W <= DBITS_W * 32)
+        for (int k = lane; k < (sc.W + 31) / 32; k += NT) L.dbits[k] = 0u;
+    if (lane == 0) cp->rebuild = 0;
+    wave_sync();
     const bool want_diag = st.out_diag != nullptr;
+    int nd = 0;            // dirty workers (wave-uniform)
+    // Column stores go only to the hot worker; they are fenced when another
+    // worker becomes hot, so every non-hot dirty worker's columns can be read
+    // back from HBM (coherently) and the hot one is read from LDS.
+    int hot = -1;          // dag entry whose columns are in L.he / L.hs
+    bool pending = false;  // hot-worker column stores not yet fenced
+    int next_empty = sc.uniform_M ? next_empty_worker(st, sc, L, nd, 0) : -1;
     int pos = fpc;
-    bool cut = false;
-    int commits = 0;
-    while (pos < end) {
-        const int i = pos + tid;
+    bool cut = false, err = false;
+    int commits = 0, nrej = 0, firstrej = INT32_MAX;
+    WinBits wb;
+    wb.f0 = wb.f1 = wb.n0 = wb.n1 = 0;
+    while (pos < end && !cut) {
+        // one window of 64 queries; `cur` is the first undecided lane
+        const int w0 = pos;
+        const int i = w0 + lane;
         const bool act = i < end;
         QSum q;
         int32_t lin = 1, lp = 1;
@@ -779,63 +1072,191 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
         } else {
             q.nfeas = 0;
         }
-        const int p = block_min_int((act && q.nfeas > 0) ? tid : NT, mins);
-        Resolved r;
-        r.abort = 0;
-        r.w = -1;
-        if (act && tid <= p) {
-            r = resolve(st, sc, q, i, start, lin, lp, tau, hb, stamp, dl, nd, want_diag);
-            if (tid < p) r.w = -1;
-        }
-        const int ab = block_min_int((act && tid <= p && r.abort) ? tid : NT, mins);
-        const int lim = min(p, ab);
-        if (act && tid < lim) {
-            if (st.out_worker) st.out_worker[sc.out_off + i] = -1;
-            if (want_diag) st.out_diag[i] = r.d;
-            atomicAdd(&cp->n_rej, 1);
-            atomicMin(&cp->first_rej, i);
-        }
-        if (ab <= p && ab < NT) {
-            pos += ab;
-            cut = true;
-            break;
-        }
-        if (p >= NT) {
-            pos = min(end, pos + NT);
-            continue;
-        }
-        if (tid == p) {
-            sh_w = r.w;
-            sh_lin = lin;
-            sh_lp = lp;
-            if (st.out_worker) st.out_worker[sc.out_off + i] = r.w;
-            if (want_diag) st.out_diag[i] = r.d;
-            if (r.w < 0) {
-                atomicAdd(&cp->n_rej, 1);
-                atomicMin(&cp->first_rej, i);
+        if (lane < nd) wb = load_win_bits(st, sc, L.dag[lane].w, start, w0, end);
+        const uint64_t potm = __ballot(act && q.nfeas > 0);
+        int cur = 0;
+        while (cur < NT && w0 + cur < end) {
+            const uint64_t pm = potm & (~0ull << cur);
+            const int p = pm ? __ffsll((unsigned long long)pm) - 1 : NT;
+            // lanes cur..p-1: rejected whatever happened earlier in the tile
+            Diag dr;
+            int ab = 0;
+            const bool mine = act && lane >= cur && lane < p;
+            if (want_diag && mine) dr = reject_diag(st, sc, q, i, start, w0, lin, lp, tau, hb, L, nd, hot, wb, &ab);
+            const uint64_t am = __ballot(mine && ab);
+            const int abl = am ? __ffsll((unsigned long long)am) - 1 : NT;
+            const int lim = min(p, abl);
+            if (act && lane >= cur && lane < lim) {
+                if (st.out_worker) st.out_worker[sc.out_off + i] = -1;
+                if (want_diag) st.out_diag[i] = dr;
             }
-        }
-        __syncthreads();
-        const int w = sh_w;
-        pos += p + 1;
-        if (w >= 0) {
+            const uint64_t rm = __ballot(act && lane >= cur && lane < lim);
+            nrej += __popcll(rm);
+            if (rm && firstrej == INT32_MAX) firstrej = w0 + __ffsll((unsigned long long)rm) - 1;
+            if (abl < p) {
+                pos = w0 + abl;
+                cut = true;
+                break;
+            }
+            if (p >= NT) {
+                cur = NT;
+                break;
+            }
+            // the query of lane p, decided by the whole wave
+            const int ip = w0 + p;
+            const QView qv = broadcast_q(q, p);
+            const int32_t plin = rdlane(lin, p), plp = rdlane(lp, p);
+            const Decision dc = decide(st, sc, qv, ip, start, w0, plin, plp, tau, hb, L, nd, hot, next_empty,
+                                       want_diag, wb);
+            if (dc.abort) {
+                pos = ip;
+                cut = true;
+                break;
+            }
+            if (lane == 0) {
+                if (st.out_worker) st.out_worker[sc.out_off + ip] = dc.w;
+                if (want_diag) st.out_diag[ip] = dc.d;
+            }
+            cur = p + 1;
+            if (dc.w < 0) {
+                nrej += 1;
+                if (firstrej == INT32_MAX) firstrej = ip;
+                continue;
+            }
+
+            // ---- commit the query to worker w
+            const int w = dc.w;
             const int gw = sc.wbase + w;
-            if (!commit_insert(st, sc, gw, sh_lin, sh_lp, tau, hb, &cp->err)) break;
-            ++commits;
-            if (tid == 0 && st.dirty[gw] != stamp) {
-                st.dirty[gw] = stamp;
-                dl[nd] = w;
-                nd = nd + 1;
+            int j = dag_slot(L, nd, w);
+            if (j < 0) {
+                j = nd;
+                DAgg x;
+                x.w = w;
+                x.n = st.n[gw];
+                x.head = st.head[gw];
+                x.B = st.B[gw];
+                x.M = st.M[gw];
+                x.hbs = st.hbs[gw];
+                x.empty0 = x.B == 0 ? 1 : 0;
+                x.cap = st.cap[gw];
+                x.base = st.slot_base[gw];
+                x.DS = st.DS[gw];
+                x.S1 = st.S1[gw];
+                x.S2 = st.S2[gw];
+                x.SC = st.SC[gw];
+                x.SR = st.SR[gw];
+                x.key = st.key[gw];
+                x.rhs = st.rhs[gw];
+                if (lane == 0) {
+                    L.dag[j] = x;
+                    if (sc.W <= DBITS_W * 32) L.dbits[w >> 5] |= 1u << (w & 31);
+                }
+                if (lane == j) wb = load_win_bits(st, sc, w, start, w0, end);
+                nd += 1;
             }
-            __syncthreads();
-            if (nd >= MAX_DIRTY && pos < end) {
+            wave_sync();
+            DAgg a = L.dag[j];
+            if (a.B + 1 > a.cap) {  // no slot left for one more live request
+                if (lane == 0) raise_error(&cp->err, DEV_ESLOTS);
+                err = true;
+                cut = true;
+                pos = ip + 1;
+                break;
+            }
+            int32_t* ge = st.e + a.base;
+            int32_t* gs = st.s + a.base;
+            if (hot != j) {
+                if (pending) {
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+                    pending = false;
+                }
+                for (int k = lane; k < a.B; k += NT) {
+                    L.he[k] = col<true>(ge + a.head, k);
+                    L.hs[k] = col<true>(gs + a.head, k);
+                }
+                hot = j;
+            }
+            wave_sync();
+            const int32_t eq = plp + tau, sq = plin - tau;
+            // insertion point: after every live request ending no later than the query
+            int u = 0;
+            for (int k0 = 0; k0 < a.B; k0 += NT) u += __popcll(__ballot(k0 + lane < a.B && L.he[k0 + lane] <= eq));
+            // shift [u, B) up by one, highest block first (each pass reads before it writes)
+            for (int top = a.B; top > u; top -= NT) {
+                const int k = top - NT + lane;
+                const bool mv = k >= u && k < top;
+                int32_t ve = 0, vs = 0;
+                if (mv) { ve = L.he[k]; vs = L.hs[k]; }
+                wave_sync();
+                if (mv) { L.he[k + 1] = ve; L.hs[k + 1] = vs; }
+                wave_sync();
+            }
+            if (lane == 0) {
+                L.he[u] = eq;
+                L.hs[u] = sq;
+            }
+            wave_sync();
+            const int B1 = a.B + 1;
+            int head = a.head;
+            int from = u;
+            if (head + B1 > a.cap) {  // reclaim the slots of finished requests
+                head = 0;
+                from = 0;
+            }
+            for (int k = from + lane; k < B1; k += NT) {
+                ge[head + k] = L.he[k];
+                gs[head + k] = L.hs[k];
+            }
+            pending = true;
+            // aggregates
+            a.B = B1;
+            a.head = head;
+            a.n = head + B1;
+            a.SC += plin;
+            a.SR += plp;
+            a.DS += ((int64_t)plin << sc.gs) + (int64_t)sc.gn * plp;
+            const int64_t X = (int64_t)B1 << sc.gs;
+            if ((a.DS >= ((int64_t)1 << 31) || X >= ((int64_t)1 << 31)) && lane == 0) raise_error(&cp->err, DEV_EOVERFLOW);
+            a.key = (uint64_t)(X * X) + (uint64_t)(a.DS * a.DS);
+            a.rhs = sc.theta * ((sc.tdec - sc.c3) - sc.c2 * (double)(B1 + 1));
+            const bool curhb = a.hbs == hb;
+            a.S1 = (curhb ? a.S1 : 0) + plin;
+            a.S2 = (curhb ? a.S2 : 0) + (int64_t)plin * plin;
+            a.hbs = hb;
+            if (a.S2 >= ((int64_t)1 << 53) && lane == 0) raise_error(&cp->err, DEV_EOVERFLOW);
+            if (lane == 0) {
+                L.dag[j] = a;
+                st.n[gw] = a.n;
+                st.head[gw] = a.head;
+                st.B[gw] = a.B;
+                st.SC[gw] = a.SC;
+                st.SR[gw] = a.SR;
+                st.DS[gw] = a.DS;
+                st.key[gw] = a.key;
+                st.rhs[gw] = a.rhs;
+                st.S1[gw] = a.S1;
+                st.S2[gw] = a.S2;
+                st.hbs[gw] = a.hbs;
+                st.built[gw] = 0;
+            }
+            wave_sync();
+            ++commits;
+            if (w == next_empty) next_empty = next_empty_worker(st, sc, L, nd, w + 1);
+            if (nd >= MAX_DIRTY && w0 + cur < end) {
+                pos = w0 + cur;
                 cut = true;
                 break;
             }
         }
-        __syncthreads();
+        if (err) break;
+        if (!cut) pos = min(end, w0 + NT);
     }
-    if (tid == 0) {
+    // the workers whose summaries the next round must rebuild
+    for (int k = lane; k < nd; k += NT) st.dlist[s * MAX_DIRTY + k] = sc.wbase + L.dag[k].w;
+    if (lane == 0) {
+        if (nrej) atomicAdd(&cp->n_rej, nrej);
+        if (firstrej != INT32_MAX) atomicMin(&cp->first_rej, firstrej);
+        st.dcount[s] = nd;
         const int32_t processed = pos - c.start;
         const int32_t since = c.since_hb + processed;
         if (pos == end && c.H > 0 && since >= c.H) {
@@ -898,9 +1319,10 @@ hipError_t launch_ingest(const State& st, int32_t W, const int64_t* res_off, con
     return hipGetLastError();
 }
 
-hipError_t launch_build(const State& st, hipStream_t stream, int force)
+hipError_t launch_build(const State& st, hipStream_t stream, int mode)
 {
-    hipLaunchKernelGGL(k_build, dim3(st.NW), dim3(BUILD_THREADS), 0, stream, st, force);
+    const int blocks = mode == 1 ? st.S * MAX_DIRTY : st.NW;
+    hipLaunchKernelGGL(k_build, dim3(blocks), dim3(BUILD_THREADS), 0, stream, st, mode);
     return hipGetLastError();
 }
 
