@@ -206,12 +206,22 @@ class Evaluator:
         self.load(trace.n_workers, trace.model, trace.kv_capacity, trace.res_offsets, trace.res_l_in,
                   trace.res_l_pred, trace.res_generated, slots_per_worker)
 
-    def place_device(self, q_l_in, q_l_pred, heartbeat_every=0, diag=True):
-        """Device tensors in, device tensors out (no host copies)."""
+    def place_device(self, q_l_in, q_l_pred, heartbeat_every=0, diag=True, out=None, diag_out=None):
+        """Device tensors in, device tensors out (no host copies).  `out` (int32
+        [Q]) and `diag_out` (uint8 [Q * 40]) may be passed to reuse buffers."""
         t = self.torch
         Q = int(q_l_in.numel())
-        out = t.empty(Q, dtype=t.int32, device=self.device)
-        d = t.empty(Q * DIAG_DTYPE.itemsize, dtype=t.uint8, device=self.device) if diag else None
+        if out is None:
+            out = t.empty(Q, dtype=t.int32, device=self.device)
+        elif out.dtype != t.int32 or out.numel() < Q:
+            raise ValueError("out must be an int32 tensor of at least Q elements")
+        d = None
+        if diag:
+            d = diag_out
+            if d is None:
+                d = t.empty(Q * DIAG_DTYPE.itemsize, dtype=t.uint8, device=self.device)
+            elif d.dtype != t.uint8 or d.numel() < Q * DIAG_DTYPE.itemsize:
+                raise ValueError("diag_out must be a uint8 tensor of at least Q * %d bytes" % DIAG_DTYPE.itemsize)
         ald_place_stream(self.h, Q, q_l_in, q_l_pred, heartbeat_every, out, d)
         return out, d
 

@@ -16,7 +16,8 @@ using namespace ald;
 namespace {
 
 struct Arena {
-    std::vector<void*> allocs;
+    void* mem = nullptr;  // every worker, slot and control array, carved from one allocation
+    size_t mem_bytes = 0;
     State st{};
     std::vector<Scen> hscen;
     std::vector<int32_t> hW;  // workers per scenario
@@ -26,11 +27,14 @@ struct Arena {
     size_t scratch_bytes = 0;
     void* scratch = nullptr;
     Scen* dscen = nullptr;
+    Ctl* hctl = nullptr;  // pinned host copy of the control blocks
+    int32_t hctl_n = 0;
 
     ~Arena()
     {
-        for (void* p : allocs) (void)hipFree(p);
+        if (mem) (void)hipFree(mem);
         if (scratch) (void)hipFree(scratch);
+        if (hctl) (void)hipHostFree(hctl);
     }
 };
 
@@ -47,11 +51,14 @@ struct ald_handle {
     std::string err;
     int32_t tile = 4096;
     Arena* main = nullptr;
+    Arena* sweep = nullptr;  // kept between sweeps so that its memory is reused
     int32_t W = 0;
     ald_model_t model{};
     int32_t max_cap = 0;
     // stream position carried across ald_place_stream calls
     int32_t tau = 0, hb_index = 0, since_hb = 0, round = 0;
+    bool rebuild_pending = false;  // the last call ended with a heartbeat: every worker is stale
+    bool dirty_pending = false;    // the last commit round left workers with stale summaries
     int32_t* err_word = nullptr;
     bool prof = false;
     std::vector<Events> pending;
@@ -119,19 +126,24 @@ Scen make_scen(const ald_model_t& m)
     s.c3 = m.c3; s.c2 = m.c2; s.k2 = m.k2;
     s.ttft = m.ttft_slo; s.tdec = m.decode_slo; s.theta = m.theta;
     s.gn = m.gamma_num; s.gs = m.gamma_log2den;
+    s.mono = (m.k1 >= 0.0 && m.k1q >= 0.0) ? 1 : 0;
     return s;
 }
 
-template <typename T>
-int dalloc(ald_handle* h, Arena* a, T** p, size_t count)
-{
-    void* q = nullptr;
-    if (count == 0) count = 1;
-    HIPCHK(h, hipMalloc(&q, count * sizeof(T)));
-    a->allocs.push_back(q);
-    *p = (T*)q;
-    return ALD_OK;
-}
+// Hands out 256-byte aligned pieces of one buffer; with a null base it only
+// adds up the size.
+struct Carver {
+    char* base;
+    size_t off = 0;
+    template <typename T>
+    void take(T** p, size_t count)
+    {
+        if (count == 0) count = 1;
+        off = (off + 255) & ~(size_t)255;
+        *p = base ? (T*)(base + off) : nullptr;
+        off += count * sizeof(T);
+    }
+};
 
 // Worker and slot arrays for S scenarios.  caps[w] = request slots of worker w.
 int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std::vector<int32_t>& W,
@@ -156,34 +168,43 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
         wb += W[s];
     }
     State& st = a->st;
-    int rc = ALD_OK;
-#define A(field, count) if ((rc = dalloc(h, a, &st.field, (size_t)(count))) != ALD_OK) return rc
-    A(slot_base, NW); A(cap, NW); A(n, NW); A(head, NW); A(M, NW); A(S1, NW); A(S2, NW);
-    A(hbs, NW); A(built, NW); A(B, NW); A(DS, NW); A(key, NW); A(peak, NW);
-    A(rhs, NW); A(SC, NW); A(SR, NW);
-    A(e, slots); A(s, slots); A(pme, slots); A(sm, slots); A(ss, slots);
     Ctl* ctl = nullptr;
     TileInfo* ti = nullptr;
-    if ((rc = dalloc(h, a, &st.dlist, (size_t)a->S * MAX_DIRTY)) != ALD_OK) return rc;
-    if ((rc = dalloc(h, a, &st.dcount, a->S)) != ALD_OK) return rc;
-    if ((rc = dalloc(h, a, &ctl, a->S)) != ALD_OK) return rc;
-    if ((rc = dalloc(h, a, &ti, a->S)) != ALD_OK) return rc;
-    if ((rc = dalloc(h, a, &a->dscen, a->S)) != ALD_OK) return rc;
-#undef A
+    size_t worker_bytes = 0;
+    auto carve = [&](Carver& c) {
+        c.take(&st.slot_base, NW); c.take(&st.cap, NW); c.take(&st.n, NW); c.take(&st.head, NW);
+        c.take(&st.M, NW); c.take(&st.S1, NW); c.take(&st.S2, NW); c.take(&st.hbs, NW);
+        c.take(&st.built, NW); c.take(&st.B, NW); c.take(&st.DS, NW); c.take(&st.key, NW);
+        c.take(&st.peak, NW); c.take(&st.rhs, NW); c.take(&st.SC, NW); c.take(&st.SR, NW);
+        c.take(&st.dq_max, NW); c.take(&st.ntd_lo, NW); c.take(&st.ntd_hi, NW);
+        c.take(&st.lthr, NW); c.take(&st.ntt_lo, NW); c.take(&st.ntt_hi, NW);
+        worker_bytes = c.off;
+        c.take(&st.e, slots); c.take(&st.s, slots); c.take(&st.pme, slots); c.take(&st.sm, slots);
+        c.take(&st.ss, slots);
+        c.take(&st.dlist, (size_t)a->S * MAX_DIRTY); c.take(&st.dcount, a->S);
+        c.take(&ctl, a->S); c.take(&ti, a->S); c.take(&a->dscen, a->S);
+    };
+    Carver sizing{nullptr};
+    carve(sizing);
+    if (sizing.off > a->mem_bytes) {
+        if (a->mem) HIPCHK(h, hipFree(a->mem));
+        a->mem = nullptr;
+        a->mem_bytes = 0;
+        HIPCHK(h, hipMalloc(&a->mem, sizing.off));
+        a->mem_bytes = sizing.off;
+    }
+    Carver placing{(char*)a->mem};
+    carve(placing);
     st.ctl = ctl;
     st.tinfo = ti;
     st.scen = a->dscen;
     st.S = a->S;
     st.NW = a->NW;
+    // every per-worker array starts at zero, then slot bases, slot counts and capacities
+    HIPCHK(h, hipMemsetAsync(a->mem, 0, worker_bytes, h->stream));
     HIPCHK(h, hipMemcpyAsync(st.slot_base, base.data(), NW * sizeof(int64_t), hipMemcpyHostToDevice, h->stream));
     HIPCHK(h, hipMemcpyAsync(st.cap, caps.data(), NW * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
     HIPCHK(h, hipMemcpyAsync(st.M, Ms.data(), NW * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
-    for (auto* p : {(void*)st.n, (void*)st.head, (void*)st.hbs, (void*)st.built, (void*)st.B,
-                    (void*)st.peak})
-        HIPCHK(h, hipMemsetAsync(p, 0, NW * sizeof(int32_t), h->stream));
-    for (auto* p : {(void*)st.S1, (void*)st.S2, (void*)st.DS, (void*)st.key, (void*)st.SC, (void*)st.SR,
-                    (void*)st.rhs})
-        HIPCHK(h, hipMemsetAsync(p, 0, NW * sizeof(int64_t), h->stream));
     HIPCHK(h, hipMemsetAsync(st.dcount, 0, a->S * sizeof(int32_t), h->stream));
     // empty workers of a scenario are interchangeable when they share one capacity
     int64_t w0 = 0;
@@ -199,30 +220,34 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
 // Lay out the tile scratch for tile length T and fill in the grid geometry.
 int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
 {
-    const int32_t nchunks = (T + EVAL_THREADS - 1) / EVAL_THREADS;
+    // evaluation: blocks of EVAL_Q queries x wpb workers; selection: blocks of
+    // SEL_THREADS queries; bit words: one per 64 queries and worker
+    const int32_t echunks = (T + EVAL_Q - 1) / EVAL_Q;
+    const int32_t schunks = (T + SEL_THREADS - 1) / SEL_THREADS;
+    const int64_t groups = (int64_t)echunks * (EVAL_Q / 64);
     int64_t NWtot = 0;
     for (int s = 0; s < a->S; ++s) NWtot += a->hW[s];
-    int32_t wpb = (int32_t)std::max<int64_t>(1, (NWtot * nchunks + target_blocks - 1) / target_blocks);
+    int32_t wpb = (int32_t)std::max<int64_t>(1, (NWtot * echunks + target_blocks - 1) / target_blocks);
     int64_t bits = 0, part = 0, qs = 0;
     int32_t eb = 0, sb = 0, cb = 0;
-    const int32_t nfin = std::min(256, std::max(1, nchunks / 2));
+    const int32_t nfin = std::min(256, std::max(1, schunks / 2));
     for (int s = 0; s < a->S; ++s) {
         Scen& sc = a->hscen[s];
         sc.wpb = std::min(wpb, std::max(1, sc.W));
         sc.nblk = (sc.W + sc.wpb - 1) / sc.wpb;
         sc.eval_blk0 = eb;
-        eb += sc.nblk * nchunks;
+        eb += sc.nblk * echunks;
         sc.sel_blk0 = sb;
-        sb += nchunks;
+        sb += schunks;
         sc.nfin = nfin;
         sc.fin_blk0 = cb;
         cb += 1 + nfin;
         sc.bits_off = bits;
-        bits += (int64_t)nchunks * (EVAL_THREADS / 64) * sc.W;
+        bits += groups * sc.W;
         sc.part_off = part;
-        part += (int64_t)nchunks * EVAL_THREADS * sc.nblk;
+        part += (int64_t)echunks * EVAL_Q * sc.nblk;
         sc.qsum_off = qs;
-        qs += (int64_t)nchunks * EVAL_THREADS;
+        qs += (int64_t)schunks * SEL_THREADS;
     }
     a->eval_blocks = eb;
     a->sel_blocks = sb;
@@ -328,24 +353,34 @@ int64_t rounds_needed(const std::vector<Ctl>& c)
 
 // Drive the tile pipeline until every scenario has consumed its queries.
 // `hc` holds the control blocks as last written to the device; on return it
-// holds their final device values.
-int run_rounds(ald_handle* h, Arena* a, bool build_every_round, std::vector<Ctl>& hc)
+// holds their final device values.  The first round's build runs in
+// `first_mode` (-1: skipped, nothing is stale); later rounds check every worker
+// when a heartbeat can have moved tau, else only the ones the previous commit
+// round listed.
+int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, std::vector<Ctl>& hc)
 {
+    if (a->hctl_n < a->S) {
+        if (a->hctl) HIPCHK(h, hipHostFree(a->hctl));
+        a->hctl = nullptr;
+        a->hctl_n = 0;
+        HIPCHK(h, hipHostMalloc((void**)&a->hctl, a->S * sizeof(Ctl), hipHostMallocDefault));
+        a->hctl_n = a->S;
+    }
     bool first = true;
     for (;;) {
         int64_t need = rounds_needed(hc);
         if (need == 0) break;
         for (int64_t r = 0; r < need; ++r) {
-            // full check after a heartbeat can have moved tau; otherwise only the
-            // workers the previous commit touched
-            LAUNCH(h, 0, launch_build(a->st, h->stream, (build_every_round || first) ? 0 : 1));
+            const int mode = first ? first_mode : (build_every_round ? 0 : 1);
             first = false;
+            if (mode >= 0) LAUNCH(h, 0, launch_build(a->st, h->stream, mode));
             LAUNCH(h, 1, launch_eval(a->st, a->eval_blocks, h->stream));
             LAUNCH(h, 2, launch_select(a->st, a->sel_blocks, h->stream));
             LAUNCH(h, 3, launch_commit(a->st, a->commit_blocks, h->stream));
         }
-        HIPCHK(h, hipMemcpyAsync(hc.data(), a->st.ctl, a->S * sizeof(Ctl), hipMemcpyDeviceToHost, h->stream));
+        HIPCHK(h, hipMemcpyAsync(a->hctl, a->st.ctl, a->S * sizeof(Ctl), hipMemcpyDeviceToHost, h->stream));
         HIPCHK(h, hipStreamSynchronize(h->stream));
+        std::copy(a->hctl, a->hctl + a->S, hc.begin());
         prof_collect(h);
         for (const Ctl& x : hc)
             if (x.err) return map_dev_error(h, x.err);
@@ -397,6 +432,7 @@ int ald_destroy(ald_handle_t h)
     (void)hipSetDevice(h->device);
     (void)hipStreamSynchronize(h->stream);
     delete h->main;
+    delete h->sweep;
     (void)hipFree(h->err_word);
     for (Events& e : h->pool) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
     for (Events& e : h->pending) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
@@ -504,6 +540,7 @@ int ald_load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const 
     h->model = *model;
     h->max_cap = maxcap;
     h->tau = h->hb_index = h->since_hb = h->round = 0;
+    h->rebuild_pending = h->dirty_pending = false;
     return ALD_OK;
 }
 
@@ -519,7 +556,7 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
     int rc = ALD_OK;
     const int32_t H = heartbeat_every;
     int32_t tau = h->tau, hb = h->hb_index, since = h->since_hb;
-    bool rebuild = false;
+    bool rebuild = h->rebuild_pending;
     if (H > 0 && since >= H) {  // a heartbeat already due from an earlier, longer period
         tau += 1;
         hb += 1;
@@ -533,7 +570,7 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
     int32_t T = std::min(h->tile, Q);
     if (H > 0) T = std::min(T, H);
     if (T != a->T) {
-        rc = layout_scratch(h, a, T, 4096);
+        rc = layout_scratch(h, a, T, 2048);
         if (rc != ALD_OK) return rc;
     }
     Ctl c{};
@@ -549,21 +586,24 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
     c.round = h->round;
     TileInfo ti{};
     ti.first_pc[0] = ti.first_pc[1] = INT32_MAX;
-    HIPCHK(h, hipMemcpyAsync(a->st.ctl, &c, sizeof(Ctl), hipMemcpyHostToDevice, h->stream));
-    HIPCHK(h, hipMemcpyAsync(a->st.tinfo, &ti, sizeof(TileInfo), hipMemcpyHostToDevice, h->stream));
-    HIPCHK(h, launch_query_stats(q_l_in, q_l_pred, Q, a->st.ctl, 1, h->stream));
+    HIPCHK(h, launch_begin(c, ti, a->st.ctl, a->st.tinfo, q_l_in, q_l_pred, Q, h->stream));
     a->st.q_lin = q_l_in;
     a->st.q_lpred = q_l_pred;
     a->st.out_worker = out_worker;
     a->st.out_diag = (Diag*)out_diag;
     std::vector<Ctl> hc(1, c);
-    rc = run_rounds(h, a, H > 0, hc);
+    // first build: every worker after a heartbeat, the last commit round's
+    // workers if it changed any, else nothing
+    const int first_mode = (rebuild || H > 0) ? 0 : (h->dirty_pending ? 1 : -1);
+    rc = run_rounds(h, a, H > 0, first_mode, hc);
     if (rc != ALD_OK) return rc;
     c = hc[0];
     h->tau = c.tau;
     h->hb_index = c.hb_index;
     h->since_hb = c.since_hb;
     h->round = c.round;
+    h->rebuild_pending = c.rebuild != 0;
+    h->dirty_pending = c.ndirty > 0;
     return ALD_OK;
 }
 
@@ -605,7 +645,9 @@ int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, i
             Ms.push_back((int32_t)scen[s].kv_capacity);
         }
     }
-    Arena a;
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    if (!h->sweep) h->sweep = new Arena();
+    Arena& a = *h->sweep;
     int rc = make_arena(h, &a, sc, W, caps, Ms);
     if (rc != ALD_OK) return rc;
     const int32_t T = std::max(1, std::min(h->tile, Q));
@@ -632,7 +674,7 @@ int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, i
     HIPCHK(h, hipMemcpyAsync(a.dscen, a.hscen.data(), S * sizeof(Scen), hipMemcpyHostToDevice, h->stream));
     if (Q > 0) {
         HIPCHK(h, launch_query_stats(q_l_in, q_l_pred, Q, a.st.ctl, S, h->stream));
-        rc = run_rounds(h, &a, false, c);
+        rc = run_rounds(h, &a, false, 0, c);
         if (rc != ALD_OK) return rc;
     }
     HIPCHK(h, launch_sweep_outputs(a.st, out_rejected, out_first_reject, h->stream));
@@ -650,6 +692,8 @@ int ald_worker_summary(ald_handle_t h, int32_t* B, int64_t* sum_c, int64_t* sum_
     HIPCHK(h, launch_build(h->main->st, h->stream, 2));
     HIPCHK(h, launch_summary(h->main->st, h->W, B, sum_c, sum_r, peak, h->stream));
     HIPCHK(h, hipStreamSynchronize(h->stream));
+    h->rebuild_pending = false;
+    h->dirty_pending = false;
     return ALD_OK;
 }
 

@@ -31,7 +31,10 @@
 namespace ald {
 
 constexpr int TOPK = 4;            // feasible candidates kept per query
-constexpr int EVAL_THREADS = 256;  // queries per pair-evaluation block
+constexpr int EVAL_THREADS = 256;  // threads per pair-evaluation block
+constexpr int EVAL_QPT = 4;        // queries per pair-evaluation thread
+constexpr int EVAL_Q = EVAL_THREADS * EVAL_QPT;  // queries per pair-evaluation block
+constexpr int STAGE_MAX = 1024;    // live requests of a worker the evaluation stages in LDS
 constexpr int SEL_THREADS = 256;   // queries per selection block
 constexpr int COMMIT_THREADS = 64;  // the arrival-order commit runs as one wave
 constexpr int HOT = 8192;          // most request slots per worker (commit keeps one worker in LDS)
@@ -56,7 +59,7 @@ struct Scen {
     int32_t fin_blk0;   // first commit block (1 sequential + nfin finalizers)
     int32_t nfin;
     int32_t uniform_M;  // every worker has the same capacity: empty workers are interchangeable
-    int32_t pad0;
+    int32_t mono;       // k1, k1q >= 0: the TTFT of a pair grows with l_in (integer thresholds apply)
     int64_t bits_off;   // uint64 words into bits_feas / bits_nt
     int64_t part_off;   // int4 entries into part
     int64_t qsum_off;   // QSum entries into qsum
@@ -80,7 +83,8 @@ struct Ctl {
     int32_t aborts;     // tiles cut short (statistics)
     int32_t round;      // rounds run
     int32_t commits;    // placements made
-    int32_t pad0, pad1;
+    int32_t ndirty;     // workers the last commit round changed (their summaries are stale)
+    int32_t pad1;
 };
 
 // Tile description published by the selection kernel for the commit kernel.
@@ -134,6 +138,16 @@ struct State {
     double* rhs;       // theta * ((T_dec - c3) - c2 * (B + 1))
     int64_t* SC;       // sum(c)
     int64_t* SR;       // sum(r)
+    // Integer forms of the latency checks at the built state, for a query with
+    // qD = 2^gs l_in + gn l_pred:  decode (b) holds iff qD <= dq_max, TTFT (c)
+    // iff l_in <= lthr (with Scen::mono); a near-tie margin is only possible
+    // for qD in [ntd_lo, ntd_hi] or l_in in [ntt_lo, ntt_hi].
+    int64_t* dq_max;
+    int64_t* ntd_lo;
+    int64_t* ntd_hi;
+    int32_t* lthr;
+    int32_t* ntt_lo;
+    int32_t* ntt_hi;
     // per slot
     int32_t* e;
     int32_t* s;
@@ -182,6 +196,8 @@ hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream);
 hipError_t launch_commit(const State& st, int32_t blocks, hipStream_t stream);
 hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q, Ctl* ctl, int32_t S,
                               hipStream_t stream);
+hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* tinfo, const int32_t* lin,
+                        const int32_t* lpred, int32_t Q, hipStream_t stream);
 hipError_t launch_summary(const State& st, int32_t W, int32_t* B, int64_t* sc, int64_t* sr, int64_t* peak,
                           hipStream_t stream);
 hipError_t launch_sweep_outputs(const State& st, int32_t* rejected, int32_t* first_reject, hipStream_t stream);

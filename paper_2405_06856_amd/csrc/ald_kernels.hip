@@ -141,6 +141,24 @@ struct View {
     double rhs;
 };
 
+// Integer forms of a built worker's latency checks (see State).
+struct Thr {
+    int64_t dq_max, ntd_lo, ntd_hi;
+    int32_t lthr, ntt_lo, ntt_hi;
+};
+
+__device__ __forceinline__ Thr load_thr(const State& st, int gw)
+{
+    Thr t;
+    t.dq_max = st.dq_max[gw];
+    t.ntd_lo = st.ntd_lo[gw];
+    t.ntd_hi = st.ntd_hi[gw];
+    t.lthr = st.lthr[gw];
+    t.ntt_lo = st.ntt_lo[gw];
+    t.ntt_hi = st.ntt_hi[gw];
+    return t;
+}
+
 __device__ __forceinline__ View load_view(const State& st, int gw, int32_t hb)
 {
     View v;
@@ -177,22 +195,54 @@ struct Latency {
     bool dec_ok, ttft_ok, nt;
 };
 
+// Left side of constraint (b) for a worker whose DS with the query added is x
+// (sum of D = x * 2^-gs exactly).
+__device__ __forceinline__ double dec_lhs(const Scen& sc, int64_t x) { return sc.k2 * ldexp((double)x, -sc.gs); }
+
+// Prefill time of constraint (c) for TTFT sums S1, S2 that include the query.
+__device__ __forceinline__ double ttft_of(const Scen& sc, int64_t S1, int64_t S2)
+{
+    return (sc.c1 + sc.k1 * (double)S1) + sc.k1q * (double)S2;
+}
+
 // Decode constraint (b) and TTFT constraint (c) of one pair.
 __device__ __forceinline__ Latency latency(const Scen& sc, const View& v, int32_t lin, int32_t lp, int32_t b)
 {
     Latency o;
     const int64_t DSq = v.DS + ((int64_t)lin << sc.gs) + (int64_t)sc.gn * lp;
-    const double sumD = ldexp((double)DSq, -sc.gs);
-    o.lhs = sc.k2 * sumD;
+    o.lhs = dec_lhs(sc, DSq);
     o.dec_ok = o.lhs <= v.rhs;
-    const int64_t S1 = v.S1 + lin;
-    const int64_t S2 = v.S2 + (int64_t)lin * lin;
-    o.ttft = (sc.c1 + sc.k1 * (double)S1) + sc.k1q * (double)S2;
+    o.ttft = ttft_of(sc, v.S1 + lin, v.S2 + (int64_t)lin * lin);
     o.ttft_ok = o.ttft <= sc.ttft;
     o.nt = near_tie(o.lhs, v.rhs) || near_tie(o.ttft, sc.ttft);
-    o.tdec = (sc.c3 + sc.c2 * (double)b) + sc.k2 * sumD;
+    o.tdec = (sc.c3 + sc.c2 * (double)b) + o.lhs;
     return o;
 }
+
+// Largest x in [lo, hi] for which `pred` holds, where pred holds on a prefix of
+// [lo, hi]; lo - 1 if it holds nowhere.  The 64 lanes of the wave test 64
+// evenly spaced points per step, so a range of 2^36 takes six steps.  All
+// lanes of the wave must call it; all get the result.
+template <typename F>
+__device__ int64_t wave_last_true(int64_t lo, int64_t hi, F pred)
+{
+    int64_t a = lo - 1, b = hi;  // the answer lies in [a, b]
+    while (a < b) {
+        const int64_t step = (b - a + 63) >> 6;
+        const int64_t x = a + step * (lane_id() + 1);
+        const bool t = x <= b && pred(x);
+        const int cnt = __popcll(__ballot(t));
+        a += step * cnt;
+        const int64_t nb = a + step - 1;
+        b = nb < b ? nb : b;
+    }
+    return a;
+}
+
+// Half-width of an interval around y that holds every x with near_tie(x, y):
+// near_tie gives |x - y| <= 1e-9 max(|x|, |y|) up to rounding, which implies
+// |x - y| < 1.0000002e-9 |y|; the extra 25% covers the rounding of y +- width.
+__device__ __forceinline__ double tie_band(double y) { return 1.25e-9 * fabs(y); }
 
 // Scenario owning block `blk` given each scenario's first block (field offset).
 template <int32_t Scen::*FIRST>
@@ -225,7 +275,7 @@ __device__ __forceinline__ void raise_error(int32_t* err, int32_t code)
 // Breakpoint summaries of one worker (whole block).  Drops finished requests
 // (e < tau), recomputes ss / pme / sm over the live slots and the worker's
 // aggregates.  Called with every thread of a BUILD_THREADS block.
-__device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t tau, int32_t* err)
+__device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t tau, int32_t hb, int32_t* err)
 {
     constexpr int NT = BUILD_THREADS;
     __shared__ int64_t red[NT / 64];
@@ -281,14 +331,15 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
         const int64_t Pe = P + e[k];
         runpm = Pe > runpm ? Pe : runpm;
     }
+    const int64_t SC = tot_s + (int64_t)B * tau;
+    const int64_t SR = tot_e - (int64_t)B * tau;
+    const int64_t DS = (SC << sc.gs) + (int64_t)sc.gn * SR;
+    const double rhs = sc.theta * ((sc.tdec - sc.c3) - sc.c2 * (double)(B + 1));
     if (tid == 0) {
         ss[n] = 0;
         sm[n] = NEG;
         pme[n] = totPe == INT64_MIN ? NEG : (int32_t)totPe;
         if (B == 0) pme[head] = NEG;
-        const int64_t SC = tot_s + (int64_t)B * tau;
-        const int64_t SR = tot_e - (int64_t)B * tau;
-        const int64_t DS = (SC << sc.gs) + (int64_t)sc.gn * SR;
         const int64_t X = (int64_t)B << sc.gs;
         if (DS >= ((int64_t)1 << 31) || X >= ((int64_t)1 << 31) || DS < 0) raise_error(err, DEV_EOVERFLOW);
         const uint64_t key = (uint64_t)(X * X) + (uint64_t)(DS * DS);
@@ -299,7 +350,48 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
         st.DS[gw] = DS;
         st.key[gw] = key;
         st.peak[gw] = B > 0 ? (int32_t)totP : 0;
-        st.rhs[gw] = sc.theta * ((sc.tdec - sc.c3) - sc.c2 * (double)(B + 1));
+        st.rhs[gw] = rhs;
+    }
+    // Integer forms of the latency checks.  Both left sides are rounded fp64
+    // expressions that never decrease as DS + qD (resp. l_in) grows -- each step
+    // is an exact conversion, a product with a non-negative constant or a sum,
+    // and rounding is monotone -- so each check holds exactly up to a threshold,
+    // found by searching with the very expression the pair check evaluates.
+    // Queries have qD <= 2^33 and l_in <= 2^24; DS < 2^31.
+    constexpr int64_t XMAX = (int64_t)1 << 36;
+    constexpr int64_t LMAX = (int64_t)1 << 24;
+    const int wv = wave_id();
+    const bool l0 = lane_id() == 0;
+    if (wv == 0) {
+        const int64_t x = wave_last_true(0, XMAX, [&](int64_t v) { return dec_lhs(sc, v) <= rhs; });
+        if (l0) st.dq_max[gw] = x - DS;
+    } else if (wv == 1) {
+        const double band = tie_band(rhs);
+        const double lo = rhs - band, hi = rhs + band;
+        const int64_t xl = wave_last_true(0, XMAX, [&](int64_t v) { return dec_lhs(sc, v) < lo; }) + 1;
+        const int64_t xh = wave_last_true(0, XMAX, [&](int64_t v) { return dec_lhs(sc, v) <= hi; });
+        if (l0) {
+            st.ntd_lo[gw] = xl - DS;
+            st.ntd_hi[gw] = xh - DS;
+        }
+    } else if (wv <= 3) {
+        const bool cur = st.hbs[gw] == hb;
+        const int64_t S1 = cur ? st.S1[gw] : 0;
+        const int64_t S2 = cur ? st.S2[gw] : 0;
+        auto tt = [&](int64_t l) { return ttft_of(sc, S1 + l, S2 + l * l); };
+        if (wv == 2) {
+            const int64_t l = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) <= sc.ttft; });
+            if (l0) st.lthr[gw] = (int32_t)l;
+        } else {
+            const double band = tie_band(sc.ttft);
+            const double lo = sc.ttft - band, hi = sc.ttft + band;
+            const int64_t ll = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) < lo; }) + 1;
+            const int64_t lh = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) <= hi; });
+            if (l0) {
+                st.ntt_lo[gw] = (int32_t)ll;
+                st.ntt_hi[gw] = (int32_t)lh;
+            }
+        }
     }
     __syncthreads();
 }
@@ -412,14 +504,22 @@ __global__ __launch_bounds__(BUILD_THREADS) void k_build(State st, int mode)
         if (!c->rebuild && st.built[gw]) return;
     }
     const Scen sc = st.scen[s];
-    build_worker(st, sc, gw, c->tau, &st.ctl[s].err);
+    build_worker(st, sc, gw, c->tau, c->hb_index, &st.ctl[s].err);
     if (threadIdx.x == 0) st.built[gw] = 1;
 }
 
 // ---------------------------------------------------------------------------------------------
-// Pair evaluation: block = (scenario, worker block, 256-query chunk).
+// Pair evaluation: block = (scenario, worker block, chunk of EVAL_Q queries).
+// Thread t holds queries t, t + 256, t + 512, t + 768 of the chunk.  For each
+// worker of the block, its live columns and summaries are staged in LDS (when
+// they fit) and every query finds its breakpoint by binary search there.
 __global__ __launch_bounds__(EVAL_THREADS) void k_eval(State st)
 {
+    constexpr int NT = EVAL_THREADS;
+    constexpr int QPT = EVAL_QPT;
+    __shared__ int32_t Es[STAGE_MAX];
+    __shared__ int4 Ss[STAGE_MAX + 1];  // {pme, sm, ss, -} of live slot k, k = 0..B
+
     const int s = find_scen<&Scen::eval_blk0>(st, blockIdx.x);
     const Scen sc = st.scen[s];
     const Ctl* cp = st.ctl + s;
@@ -429,35 +529,117 @@ __global__ __launch_bounds__(EVAL_THREADS) void k_eval(State st)
     const int local = blockIdx.x - sc.eval_blk0;
     const int wb = local % sc.nblk;
     const int qc = local / sc.nblk;
-    const int q0 = start + qc * EVAL_THREADS;
+    const int q0 = start + qc * EVAL_Q;
     if (q0 >= end) return;
     const int32_t tau = cp->tau, hb = cp->hb_index;
-    const int qi = q0 + threadIdx.x;
-    const bool act = qi < end;
-    const int32_t lin = act ? st.q_lin[qi] : 1;
-    const int32_t lp = act ? st.q_lpred[qi] : 1;
-    const int32_t sq = lin - tau, eq = lp + tau;
+    const int tid = threadIdx.x;
+    const bool want_ex = st.out_diag != nullptr;
 
-    int32_t ex1 = INT32_MAX, w1 = -1, ex2 = INT32_MAX, w2 = -1;
+    int32_t lin[QPT], lp[QPT], sq[QPT], eq[QPT];
+    int64_t qD[QPT];
+    bool act[QPT];
+    int32_t ex1[QPT], w1[QPT], ex2[QPT], w2[QPT];
+#pragma unroll
+    for (int m = 0; m < QPT; ++m) {
+        const int qi = q0 + m * NT + tid;
+        act[m] = qi < end;
+        lin[m] = act[m] ? st.q_lin[qi] : 1;
+        lp[m] = act[m] ? st.q_lpred[qi] : 1;
+        sq[m] = lin[m] - tau;
+        eq[m] = lp[m] + tau;
+        qD[m] = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
+        ex1[m] = ex2[m] = INT32_MAX;
+        w1[m] = w2[m] = -1;
+    }
     const int wbeg = wb * sc.wpb;
     const int wend = min(sc.W, wbeg + sc.wpb);
-    const int64_t row = sc.bits_off + (int64_t)((q0 - start) >> 6) * sc.W + (threadIdx.x >> 6) * (int64_t)sc.W;
+    // bit word of (query group, worker): group of queries m * NT + 64 * wave
+    const int64_t row0 = sc.bits_off + (int64_t)(((q0 - start) >> 6) + wave_id()) * sc.W;
     for (int w = wbeg; w < wend; ++w) {
         const int gw = sc.wbase + w;
         const View v = load_view(st, gw, hb);
-        const int64_t peak = kv_peak_with(v, sq, eq);
-        const Latency L = latency(sc, v, lin, lp, v.n - v.head + 1);
-        const bool kv_ok = peak <= v.M;
-        const bool feas = act && kv_ok && L.dec_ok && L.ttft_ok;
-        const uint64_t bf = __ballot(feas);
-        const uint64_t bn = __ballot(act && L.nt);
-        if (lane_id() == 0) {
-            st.bits_feas[row + w] = bf;
-            st.bits_nt[row + w] = bn;
+        const Thr th = load_thr(st, gw);
+        const int B = v.n - v.head;
+        const bool staged = B < STAGE_MAX;  // block-uniform
+        // staged: 2^K - 1 >= B slots, the ones past B padded with INT32_MAX, so
+        // that a fixed-step search needs no bounds test
+        const int K = 32 - __clz(B);
+        int l[QPT];
+        if (staged) {
+            __syncthreads();  // the previous worker's readers are done
+            const int P = (1 << K) - 1;
+            for (int k = tid; k < P; k += NT) Es[k] = k < B ? v.e[v.head + k] : INT32_MAX;
+            for (int k = tid; k <= B; k += NT)
+                Ss[k] = make_int4(v.pme[v.head + k], v.sm[v.head + k], v.ss[v.head + k], 0);
+            __syncthreads();
+            // l = number of live requests ending before the query (lower bound
+            // of eq), for all queries of the thread in lockstep
+#pragma unroll
+            for (int m = 0; m < QPT; ++m) l[m] = 0;
+            for (int step = K > 0 ? 1 << (K - 1) : 0; step > 0; step >>= 1) {
+#pragma unroll
+                for (int m = 0; m < QPT; ++m) {
+                    const int c = l[m] + step;
+                    l[m] = Es[c - 1] < eq[m] ? c : l[m];
+                }
+            }
         }
-        min2_insert(ex1, w1, ex2, w2, (int32_t)(peak - v.M), w);
+#pragma unroll
+        for (int m = 0; m < QPT; ++m) {
+            int64_t peak;
+            if (staged) {
+                const int4 t = Ss[l[m]];
+                const int64_t a = (int64_t)t.x + sq[m];
+                const int64_t b = (int64_t)t.y;
+                const int64_t c = (int64_t)t.z + (int64_t)(B - l[m]) * eq[m] + sq[m] + eq[m];
+                peak = a > b ? a : b;
+                peak = peak > c ? peak : c;
+            } else {
+                peak = kv_peak_with(v, sq[m], eq[m]);
+            }
+            bool dec_ok, ttft_ok, nt;
+            if (sc.mono) {
+                dec_ok = qD[m] <= th.dq_max;
+                ttft_ok = lin[m] <= th.lthr;
+                const bool maybe = (qD[m] >= th.ntd_lo && qD[m] <= th.ntd_hi) ||
+                                   (lin[m] >= th.ntt_lo && lin[m] <= th.ntt_hi);
+                nt = maybe && latency(sc, v, lin[m], lp[m], B + 1).nt;
+            } else {
+                const Latency L = latency(sc, v, lin[m], lp[m], B + 1);
+                dec_ok = L.dec_ok;
+                ttft_ok = L.ttft_ok;
+                nt = L.nt;
+            }
+            const bool feas = act[m] && peak <= v.M && dec_ok && ttft_ok;
+            const uint64_t bf = __ballot(feas);
+            const uint64_t bn = __ballot(act[m] && nt);
+            if (lane_id() == 0) {
+                const int64_t row = row0 + (int64_t)(m * (NT / 64)) * sc.W + w;
+                st.bits_feas[row] = bf;
+                st.bits_nt[row] = bn;
+            }
+            if (want_ex) min2_insert(ex1[m], w1[m], ex2[m], w2[m], (int32_t)(peak - v.M), w);
+        }
     }
-    if (act) st.part[sc.part_off + (int64_t)(qi - start) * sc.nblk + wb] = make_int4(ex1, w1, ex2, w2);
+#pragma unroll
+    for (int m = 0; m < QPT; ++m) {
+        const int qi = q0 + m * NT + tid;
+        if (act[m]) st.part[sc.part_off + (int64_t)(qi - start) * sc.nblk + wb] = make_int4(ex1[m], w1[m], ex2[m], w2[m]);
+    }
+}
+
+// Read a lane's value (uniform result).
+__device__ __forceinline__ int32_t rdlane(int32_t v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ uint64_t rdlane64(uint64_t v, int l)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ int64_t rdlane64s(int64_t v, int l) { return (int64_t)rdlane64((uint64_t)v, l); }
+__device__ __forceinline__ double rdlane_f64(double v, int l)
+{
+    return __builtin_bit_cast(double, rdlane64(__builtin_bit_cast(uint64_t, v), l));
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -492,25 +674,38 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     int32_t nfeas = 0, ntcnt = 0, ntw = -1, ncand = 0;
     bool efeas = false;
     uint64_t ntkey = 0;
-    const int64_t row = sc.bits_off + (int64_t)((qi - start) >> 6) * sc.W;
-    for (int w = 0; w < sc.W; ++w) {
-        const uint64_t fw = st.bits_feas[row + w];
-        const uint64_t nw = st.bits_nt[row + w];
-        if ((fw | nw) == 0) continue;  // wave-uniform
-        const uint64_t key = st.key[sc.wbase + w];
-        const bool f = (fw >> lane) & 1;
-        const bool nb = (nw >> lane) & 1;
-        nfeas += f ? 1 : 0;
-        // an empty worker has rank key 0; with uniform capacity all empty
-        // workers are alike and stand in one class
-        const bool cls = sc.uniform_M && key == 0;
-        efeas = efeas | (cls & f);
-        ncand += (f & !cls) ? 1 : 0;
-        topk_insert<TOPK>(tkey, tw, key, (f && !cls) ? w : -1);
-        ntcnt += nb ? 1 : 0;
-        const bool better = nb & ranks_before(key, w, ntkey, ntw);
-        ntkey = better ? key : ntkey;
-        ntw = better ? w : ntw;
+    // this wave's 64 queries share one bit word per worker; 64 workers' words
+    // are read at once and only workers with a set bit are visited
+    const int64_t row = sc.bits_off + (int64_t)((q0 - start) >> 6) * sc.W + (int64_t)wave_id() * sc.W;
+    for (int wb0 = 0; wb0 < sc.W; wb0 += 64) {
+        const int wl = wb0 + lane;
+        const bool in = wl < sc.W;
+        const uint64_t fl = in ? st.bits_feas[row + wl] : 0;
+        const uint64_t nl = in ? st.bits_nt[row + wl] : 0;
+        uint64_t mask = __ballot((fl | nl) != 0);
+        if (!mask) continue;
+        const uint64_t kl = in ? st.key[sc.wbase + wl] : 0;
+        while (mask) {
+            const int j = __ffsll((unsigned long long)mask) - 1;
+            mask &= mask - 1;
+            const uint64_t fw = rdlane64(fl, j);
+            const uint64_t nw = rdlane64(nl, j);
+            const uint64_t key = rdlane64(kl, j);
+            const int w = wb0 + j;
+            const bool f = (fw >> lane) & 1;
+            const bool nb = (nw >> lane) & 1;
+            nfeas += f ? 1 : 0;
+            // an empty worker has rank key 0; with uniform capacity all empty
+            // workers are alike and stand in one class
+            const bool cls = sc.uniform_M && key == 0;
+            efeas = efeas | (cls & f);
+            ncand += (f & !cls) ? 1 : 0;
+            topk_insert<TOPK>(tkey, tw, key, (f && !cls) ? w : -1);
+            ntcnt += nb ? 1 : 0;
+            const bool better = nb & ranks_before(key, w, ntkey, ntw);
+            ntkey = better ? key : ntkey;
+            ntw = better ? w : ntw;
+        }
     }
     int32_t ex1 = INT32_MAX, w1 = -1, ex2 = INT32_MAX, w2 = -1;
     const int4* prow = st.part + sc.part_off + (int64_t)(qi - start) * sc.nblk;
@@ -551,19 +746,6 @@ constexpr int DBITS_W = 2048;  // dirty bitmap words in LDS: scenarios of up to 
 
 // ---- cross-lane primitives of the commit wave (DPP and readlane; no LDS
 // permutes on the sequential path)
-
-__device__ __forceinline__ int32_t rdlane(int32_t v, int l) { return __builtin_amdgcn_readlane(v, l); }
-__device__ __forceinline__ uint64_t rdlane64(uint64_t v, int l)
-{
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
-    return ((uint64_t)hi << 32) | lo;
-}
-__device__ __forceinline__ int64_t rdlane64s(int64_t v, int l) { return (int64_t)rdlane64((uint64_t)v, l); }
-__device__ __forceinline__ double rdlane_f64(double v, int l)
-{
-    return __builtin_bit_cast(double, rdlane64(__builtin_bit_cast(uint64_t, v), l));
-}
 
 // Inclusive scan over the 64 lanes (lane 0 first) with DPP row shifts and row
 // broadcasts; lanes without a source keep the identity.
@@ -1257,6 +1439,7 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
         if (nrej) atomicAdd(&cp->n_rej, nrej);
         if (firstrej != INT32_MAX) atomicMin(&cp->first_rej, firstrej);
         st.dcount[s] = nd;
+        cp->ndirty = nd;
         const int32_t processed = pos - c.start;
         const int32_t since = c.since_hb + processed;
         if (pos == end && c.H > 0 && since >= c.H) {
@@ -1290,6 +1473,27 @@ __global__ __launch_bounds__(256) void k_query_stats(const int32_t* lin, const i
     bad = block_reduce<256>(bad, 0, OpAdd(), red);
     if (threadIdx.x == 0 && bad)
         for (int s = 0; s < S; ++s) atomicCAS(&ctl[s].err, 0, DEV_EINVAL);
+}
+
+// Start of an ald_place_stream call (one scenario): one block writes the
+// control block and tile record, then checks every query length; an invalid
+// one sets the control block's error, which makes every later kernel of the
+// call a no-op.  A single block, so no other block can race with the writes.
+__global__ __launch_bounds__(1024) void k_begin(Ctl c, TileInfo ti, Ctl* ctl, TileInfo* tinfo, const int32_t* lin,
+                                                const int32_t* lpred, int32_t Q)
+{
+    __shared__ int64_t red[16];
+    if (threadIdx.x == 0) {
+        *ctl = c;
+        *tinfo = ti;
+    }
+    int64_t bad = 0;
+    for (int i = threadIdx.x; i < Q; i += 1024) {
+        const int32_t a = lin[i], p = lpred[i];
+        bad += (a >= 1 && p >= 1 && a <= (1 << 24) && p <= (1 << 24)) ? 0 : 1;
+    }
+    bad = block_reduce<1024>(bad, 0, OpAdd(), red);
+    if (threadIdx.x == 0 && bad) ctl->err = DEV_EINVAL;
 }
 
 __global__ void k_summary(State st, int32_t W, int32_t* B, int64_t* sc, int64_t* sr, int64_t* peak)
@@ -1351,6 +1555,13 @@ hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t 
     if (blocks > 256) blocks = 256;
     if (blocks < 1) blocks = 1;
     hipLaunchKernelGGL(k_query_stats, dim3(blocks), dim3(256), 0, stream, lin, lpred, Q, ctl, S);
+    return hipGetLastError();
+}
+
+hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* tinfo, const int32_t* lin,
+                        const int32_t* lpred, int32_t Q, hipStream_t stream)
+{
+    hipLaunchKernelGGL(k_begin, dim3(1), dim3(1024), 0, stream, c, ti, ctl, tinfo, lin, lpred, Q);
     return hipGetLastError();
 }
 

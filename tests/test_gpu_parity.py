@@ -110,6 +110,25 @@ def test_stream_continues_across_calls(aladdin):
     compare(*gpu_place(aladdin, t, tile=256, chunks=cuts), ref.place_trace(t), "chunks")
 
 
+@pytest.mark.parametrize("k1,k1q", [(2e-5, -3e-10), (-1e-7, 1e-9)])
+def test_ttft_not_monotone_in_lin(aladdin, k1, k1q):
+    # with a negative prefill coefficient the TTFT check has no integer
+    # threshold in l_in and every pair takes the exact fp64 path
+    model = dataclasses.replace(wl.BASE_MODEL, k1=k1, k1q=k1q, ttft_slo=0.03)
+    t = wl.make_trace("ttft_nm", 23, W=20, R=10, Q=900, kv_capacity=30000, model=model, heartbeat_every=50)
+    compare(*gpu_place(aladdin, t, tile=128), ref.place_trace(t), "ttft_nm")
+
+
+def test_chunks_ending_on_heartbeats(aladdin):
+    # calls that end exactly where a heartbeat falls: the next call must start
+    # from summaries rebuilt at the advanced decode iteration
+    t = wl.make_trace("hbchunks", 22, W=16, R=24, Q=700, kv_capacity=20000, model=wl.BASE_MODEL,
+                      heartbeat_every=37)
+    cuts = [(0, 37), (37, 74), (74, 111), (111, 333), (333, 370), (370, 700)]
+    for tile in (64, 256):
+        compare(*gpu_place(aladdin, t, tile=tile, chunks=cuts), ref.place_trace(t), "hbchunks tile %d" % tile)
+
+
 @pytest.mark.parametrize("seed", range(12))
 def test_random_ragged_traces(aladdin, seed):
     rng = np.random.default_rng(1000 + seed)
