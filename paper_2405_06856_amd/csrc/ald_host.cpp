@@ -27,6 +27,7 @@ struct Arena {
     size_t scratch_bytes = 0;
     void* scratch = nullptr;
     Scen* dscen = nullptr;
+    bool mono = true;     // every scenario's TTFT grows with l_in
     Ctl* hctl = nullptr;  // pinned host copy of the control blocks
     int32_t hctl_n = 0;
 
@@ -179,8 +180,7 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
         c.take(&st.dq_max, NW); c.take(&st.ntd_lo, NW); c.take(&st.ntd_hi, NW);
         c.take(&st.lthr, NW); c.take(&st.ntt_lo, NW); c.take(&st.ntt_hi, NW);
         worker_bytes = c.off;
-        c.take(&st.e, slots); c.take(&st.s, slots); c.take(&st.pme, slots); c.take(&st.sm, slots);
-        c.take(&st.ss, slots);
+        c.take(&st.e, slots); c.take(&st.s, slots); c.take(&st.pms, slots);
         c.take(&st.dlist, (size_t)a->S * MAX_DIRTY); c.take(&st.dcount, a->S);
         c.take(&ctl, a->S); c.take(&ti, a->S); c.take(&a->dscen, a->S);
     };
@@ -206,6 +206,8 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
     HIPCHK(h, hipMemcpyAsync(st.cap, caps.data(), NW * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
     HIPCHK(h, hipMemcpyAsync(st.M, Ms.data(), NW * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
     HIPCHK(h, hipMemsetAsync(st.dcount, 0, a->S * sizeof(int32_t), h->stream));
+    a->mono = true;
+    for (int s = 0; s < a->S; ++s) a->mono = a->mono && a->hscen[s].mono;
     // empty workers of a scenario are interchangeable when they share one capacity
     int64_t w0 = 0;
     for (int s = 0; s < a->S; ++s) {
@@ -228,6 +230,7 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
     int64_t NWtot = 0;
     for (int s = 0; s < a->S; ++s) NWtot += a->hW[s];
     int32_t wpb = (int32_t)std::max<int64_t>(1, (NWtot * echunks + target_blocks - 1) / target_blocks);
+    wpb = std::min(wpb, EVAL_WPB_MAX);
     int64_t bits = 0, part = 0, qs = 0;
     int32_t eb = 0, sb = 0, cb = 0;
     const int32_t nfin = std::min(256, std::max(1, schunks / 2));
@@ -374,7 +377,7 @@ int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, 
             const int mode = first ? first_mode : (build_every_round ? 0 : 1);
             first = false;
             if (mode >= 0) LAUNCH(h, 0, launch_build(a->st, h->stream, mode));
-            LAUNCH(h, 1, launch_eval(a->st, a->eval_blocks, h->stream));
+            LAUNCH(h, 1, launch_eval(a->st, a->eval_blocks, a->mono, h->stream));
             LAUNCH(h, 2, launch_select(a->st, a->sel_blocks, h->stream));
             LAUNCH(h, 3, launch_commit(a->st, a->commit_blocks, h->stream));
         }
@@ -502,7 +505,7 @@ int ald_load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const 
         total += c + 1;
         maxcap = std::max(maxcap, (int32_t)c);
     }
-    if (total * 20 > ((int64_t)64 << 30)) return fail(h, ALD_EINVAL, "worker state would exceed 64 GiB");
+    if (total * 24 > ((int64_t)64 << 30)) return fail(h, ALD_EINVAL, "worker state would exceed 64 GiB");
 
     HIPCHK(h, hipStreamSynchronize(h->stream));
     delete h->main;
@@ -634,7 +637,7 @@ int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, i
         slots += scen[s].n_workers * (cap + 1);
     }
     if (NW > (1 << 30)) return fail(h, ALD_EINVAL, "too many workers");
-    if (slots * 20 > ((int64_t)128 << 30)) return fail(h, ALD_EINVAL, "sweep state would exceed 128 GiB");
+    if (slots * 24 > ((int64_t)128 << 30)) return fail(h, ALD_EINVAL, "sweep state would exceed 128 GiB");
     for (int s = 0; s < S; ++s) {
         sc[s] = make_scen(scen[s].model);
         W[s] = scen[s].n_workers;

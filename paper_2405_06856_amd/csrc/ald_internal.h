@@ -14,9 +14,10 @@
 //   With P_k = sum_{j >= k} (s_j + e_k)  (the KV demand at the end point of
 //   request k counted over the requests at or after slot k; it equals the
 //   demand at iteration r_k whenever k is the first of its tie group, and is
-//   below it otherwise), the summaries are
+//   below it otherwise), the summaries, kept together in one int4 per slot
+//   (pms = {pme, sm, ss, unused}), are
 //       ss[k]  = sum_{j >= k} s_j                     (ss[n] = 0)
-//       pme[k] = max_{head <= j < k} (P_j + e_j)       (pme[head] = NEG)
+//       pme[k] = max_{head <= j < k} (P_j + e_j)       (pme[head] = PME_NONE)
 //       sm[k]  = max_{j >= k} P_j                     (sm[n] = NEG)
 //   For a query with sq = l_in - tau, eq = l_pred + tau and
 //   l = first live slot with e >= eq, the demand peak with the query added is
@@ -34,13 +35,18 @@ constexpr int TOPK = 4;            // feasible candidates kept per query
 constexpr int EVAL_THREADS = 256;  // threads per pair-evaluation block
 constexpr int EVAL_QPT = 4;        // queries per pair-evaluation thread
 constexpr int EVAL_Q = EVAL_THREADS * EVAL_QPT;  // queries per pair-evaluation block
-constexpr int STAGE_MAX = 1024;    // live requests of a worker the evaluation stages in LDS
+constexpr int EVAL_WPB_MAX = 64;  // workers per pair-evaluation block at most
+constexpr int STAGE_MAX = 768;     // live requests of a worker the evaluation stages in LDS (fewer than)
 constexpr int SEL_THREADS = 256;   // queries per selection block
 constexpr int COMMIT_THREADS = 64;  // the arrival-order commit runs as one wave
 constexpr int HOT = 8192;          // most request slots per worker (commit keeps one worker in LDS)
 constexpr int BUILD_THREADS = 256;
 constexpr int MAX_DIRTY = 64;      // workers changed within one tile before the tile is cut
 constexpr int32_t NEG = INT32_MIN;
+// pme with no slot before it: far below every demand, yet pme + sq cannot wrap
+// in 32 bits (|sq| < 2^28)
+constexpr int32_t PME_NONE = -(1 << 30);
+constexpr int LB_MAX = 2048;       // l_pred range of the per-block breakpoint table
 
 // error codes raised on the device (mirrors ALD_E* in aladdin.h)
 constexpr int32_t DEV_EINVAL = -1;
@@ -151,9 +157,7 @@ struct State {
     // per slot
     int32_t* e;
     int32_t* s;
-    int32_t* pme;
-    int32_t* sm;
-    int32_t* ss;
+    int4* pms;         // {pme, sm, ss, unused}
     // per scenario [S]
     const Scen* scen;
     Ctl* ctl;
@@ -191,7 +195,7 @@ hipError_t launch_ingest(const State& st, int32_t W, const int64_t* res_off, con
 // mode 0: every worker whose summaries are stale; 1: only the workers listed by
 // the last commit; 2: every worker unconditionally
 hipError_t launch_build(const State& st, hipStream_t stream, int mode);
-hipError_t launch_eval(const State& st, int32_t blocks, hipStream_t stream);
+hipError_t launch_eval(const State& st, int32_t blocks, bool mono, hipStream_t stream);
 hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream);
 hipError_t launch_commit(const State& st, int32_t blocks, hipStream_t stream);
 hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q, Ctl* ctl, int32_t S,

@@ -132,9 +132,7 @@ __device__ __forceinline__ bool near_tie(double x, double y)
 // Everything a pair evaluation needs from one worker.
 struct View {
     const int32_t* e;
-    const int32_t* pme;
-    const int32_t* sm;
-    const int32_t* ss;
+    const int4* pms;
     int32_t head, n, M;
     int64_t DS, S1, S2;
     uint64_t key;
@@ -164,9 +162,7 @@ __device__ __forceinline__ View load_view(const State& st, int gw, int32_t hb)
     View v;
     const int64_t base = st.slot_base[gw];
     v.e = st.e + base;
-    v.pme = st.pme + base;
-    v.sm = st.sm + base;
-    v.ss = st.ss + base;
+    v.pms = st.pms + base;
     v.head = st.head[gw];
     v.n = st.n[gw];
     v.M = st.M[gw];
@@ -183,9 +179,10 @@ __device__ __forceinline__ View load_view(const State& st, int gw, int32_t hb)
 __device__ __forceinline__ int64_t kv_peak_with(const View& v, int32_t sq, int32_t eq)
 {
     const int l = lower_bound_i32(v.e, v.head, v.n, eq);
-    const int64_t a = (int64_t)v.pme[l] + sq;
-    const int64_t b = (int64_t)v.sm[l];
-    const int64_t c = (int64_t)v.ss[l] + (int64_t)(v.n - l) * eq + sq + eq;
+    const int4 t = v.pms[l];
+    const int64_t a = (int64_t)t.x + sq;
+    const int64_t b = (int64_t)t.y;
+    const int64_t c = (int64_t)t.z + (int64_t)(v.n - l) * eq + sq + eq;
     int64_t p = a > b ? a : b;
     return p > c ? p : c;
 }
@@ -271,6 +268,51 @@ __device__ __forceinline__ void raise_error(int32_t* err, int32_t code)
     atomicCAS(err, 0, code);
 }
 
+// ---- cross-lane primitives (readlane and DPP; no LDS permutes)
+
+// Read a lane's value (uniform result).
+__device__ __forceinline__ int32_t rdlane(int32_t v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ uint64_t rdlane64(uint64_t v, int l)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ int64_t rdlane64s(int64_t v, int l) { return (int64_t)rdlane64((uint64_t)v, l); }
+__device__ __forceinline__ double rdlane_f64(double v, int l)
+{
+    return __builtin_bit_cast(double, rdlane64(__builtin_bit_cast(uint64_t, v), l));
+}
+
+// Inclusive scan over the 64 lanes (lane 0 first) with DPP row shifts and row
+// broadcasts; lanes without a source keep the identity.
+template <typename Op>
+__device__ __forceinline__ int32_t wave_incl_scan(int32_t x, int32_t ident, Op op)
+{
+    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x111, 0xf, 0xf, false));  // row_shr:1
+    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x112, 0xf, 0xf, false));  // row_shr:2
+    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x114, 0xf, 0xf, false));  // row_shr:4
+    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x118, 0xf, 0xf, false));  // row_shr:8
+    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x142, 0xa, 0xf, false));  // row_bcast:15
+    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x143, 0xc, 0xf, false));  // row_bcast:31
+    return x;
+}
+struct Add32 {
+    __device__ int32_t operator()(int32_t a, int32_t b) const { return a + b; }
+};
+struct Max32 {
+    __device__ int32_t operator()(int32_t a, int32_t b) const { return a > b ? a : b; }
+};
+__device__ __forceinline__ int32_t wave_sum32(int32_t v) { return rdlane(wave_incl_scan(v, 0, Add32()), 63); }
+__device__ __forceinline__ int32_t wave_max32(int32_t v) { return rdlane(wave_incl_scan(v, INT32_MIN, Max32()), 63); }
+__device__ __forceinline__ int64_t wave_sum64(int64_t v)
+{
+#pragma unroll
+    for (int d = 32; d > 0; d >>= 1) v += __shfl_xor(v, d, 64);
+    return v;
+}
+
+
 // ---------------------------------------------------------------------------------------------
 // Breakpoint summaries of one worker (whole block).  Drops finished requests
 // (e < tau), recomputes ss / pme / sm over the live slots and the worker's
@@ -283,9 +325,7 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
     const int64_t base = st.slot_base[gw];
     int32_t* e = st.e + base;
     int32_t* s = st.s + base;
-    int32_t* ss = st.ss + base;
-    int32_t* pme = st.pme + base;
-    int32_t* sm = st.sm + base;
+    int4* pms = st.pms + base;
     const int n = st.n[gw];
     int head = st.head[gw];
 
@@ -308,7 +348,7 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
     int64_t run = soff, lmaxP = INT64_MIN, lmaxPe = INT64_MIN;
     for (int k = k1 - 1; k >= k0; --k) {
         run += s[k];
-        ss[k] = (int32_t)run;
+        pms[k].z = (int32_t)run;
         const int64_t P = run + (int64_t)(n - k) * e[k];
         lmaxP = P > lmaxP ? P : lmaxP;
         const int64_t Pe = P + e[k];
@@ -320,14 +360,14 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
 
     int64_t runmax = smoff;
     for (int k = k1 - 1; k >= k0; --k) {
-        const int64_t P = (int64_t)ss[k] + (int64_t)(n - k) * e[k];
+        const int64_t P = (int64_t)pms[k].z + (int64_t)(n - k) * e[k];
         runmax = P > runmax ? P : runmax;
-        sm[k] = (int32_t)runmax;
+        pms[k].y = (int32_t)runmax;
     }
     int64_t runpm = pmoff;
     for (int k = k0; k < k1; ++k) {
-        pme[k] = runpm == INT64_MIN ? NEG : (int32_t)runpm;
-        const int64_t P = (int64_t)ss[k] + (int64_t)(n - k) * e[k];
+        pms[k].x = runpm == INT64_MIN ? PME_NONE : (int32_t)runpm;
+        const int64_t P = (int64_t)pms[k].z + (int64_t)(n - k) * e[k];
         const int64_t Pe = P + e[k];
         runpm = Pe > runpm ? Pe : runpm;
     }
@@ -336,10 +376,7 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
     const int64_t DS = (SC << sc.gs) + (int64_t)sc.gn * SR;
     const double rhs = sc.theta * ((sc.tdec - sc.c3) - sc.c2 * (double)(B + 1));
     if (tid == 0) {
-        ss[n] = 0;
-        sm[n] = NEG;
-        pme[n] = totPe == INT64_MIN ? NEG : (int32_t)totPe;
-        if (B == 0) pme[head] = NEG;
+        pms[n] = make_int4(totPe == INT64_MIN ? PME_NONE : (int32_t)totPe, NEG, 0, 0);
         const int64_t X = (int64_t)B << sc.gs;
         if (DS >= ((int64_t)1 << 31) || X >= ((int64_t)1 << 31) || DS < 0) raise_error(err, DEV_EOVERFLOW);
         const uint64_t key = (uint64_t)(X * X) + (uint64_t)(DS * DS);
@@ -509,16 +546,104 @@ __global__ __launch_bounds__(BUILD_THREADS) void k_build(State st, int mode)
 }
 
 // ---------------------------------------------------------------------------------------------
+// What the pair evaluation needs of one worker, gathered into LDS once per
+// block so that the evaluation loop reads no per-worker global data.
+struct WInfo {
+    int64_t base;  // first live slot
+    int64_t DS, S1, S2;
+    double rhs;
+    int64_t dq_max, ntd_lo, ntd_hi;
+    int32_t head, n, M, lthr, ntt_lo, ntt_hi;
+};
+
+__device__ __forceinline__ View winfo_view(const State& st, const WInfo& wi)
+{
+    View v;
+    v.e = st.e + (wi.base - wi.head);
+    v.pms = st.pms + (wi.base - wi.head);
+    v.head = wi.head;
+    v.n = wi.n;
+    v.M = wi.M;
+    v.DS = wi.DS;
+    v.S1 = wi.S1;
+    v.S2 = wi.S2;
+    v.key = 0;
+    v.rhs = wi.rhs;
+    return v;
+}
+
+// Block-wide reductions of one int64 per thread (all threads get the result).
+template <int NT, typename Op>
+__device__ __forceinline__ int64_t block_all(int64_t v, int64_t ident, Op op, int64_t* lds)
+{
+#pragma unroll
+    for (int d = 32; d > 0; d >>= 1) v = op(v, __shfl_xor(v, d, 64));
+    if (lane_id() == 0) lds[wave_id()] = v;
+    __syncthreads();
+    int64_t r = ident;
+#pragma unroll
+    for (int j = 0; j < NT / 64; ++j) r = op(r, lds[j]);
+    __syncthreads();
+    return r;
+}
+
+// Two smallest KV excesses of a query as packed keys: excess (offset to
+// unsigned) in the high word, the complement of the worker index in the low
+// word -- smaller key = smaller excess, then higher index (the order the
+// commit's tie rule expects).  ~0 marks an empty entry.
+__device__ __forceinline__ uint64_t ex_key(int32_t ex, int32_t w)
+{
+    return ((uint64_t)((uint32_t)ex ^ 0x80000000u) << 32) | (uint32_t)~(uint32_t)w;
+}
+__device__ __forceinline__ void ex_unpack(uint64_t k, int32_t& ex, int32_t& w)
+{
+    ex = k == ~0ull ? INT32_MAX : (int32_t)((uint32_t)(k >> 32) ^ 0x80000000u);
+    w = k == ~0ull ? -1 : (int32_t)~(uint32_t)k;
+}
+
+// One thread's share of a staged worker: slots tid + j * EVAL_THREADS of the
+// e column and of the summaries (clamped to slot B, which exists).
+constexpr int PF_N = (STAGE_MAX + EVAL_THREADS - 1) / EVAL_THREADS;
+struct Prefetch {
+    int32_t e[PF_N];
+    int4 p[PF_N];
+};
+
+__device__ __forceinline__ Prefetch prefetch_worker(const State& st, const WInfo& x, int tid)
+{
+    Prefetch f;
+    const int B = x.n - x.head;
+#pragma unroll
+    for (int j = 0; j < PF_N; ++j) {
+        const int k = min(tid + j * EVAL_THREADS, B);
+        f.e[j] = st.e[x.base + k];
+        f.p[j] = st.pms[x.base + k];
+    }
+    return f;
+}
+
 // Pair evaluation: block = (scenario, worker block, chunk of EVAL_Q queries).
 // Thread t holds queries t, t + 256, t + 512, t + 768 of the chunk.  For each
-// worker of the block, its live columns and summaries are staged in LDS (when
-// they fit) and every query finds its breakpoint by binary search there.
+// worker of the block, with its live set staged in LDS:
+//   LB[v] = number of live requests with remaining length below v, for v up to
+//           the longest l_pred of the chunk (a histogram of remaining lengths
+//           and a block scan), so a query's breakpoint slot is l = LB[l_pred];
+//   the summaries of slot l then give the KV peak with the query added.
+// Workers with B >= STAGE_MAX, or chunks with an l_pred above LB_MAX, take the
+// binary search over global memory instead.  MONO: the latency checks use the
+// worker's integer thresholds; EX: the two smallest KV excesses are tracked
+// (diagnostics).
+template <bool MONO, bool EX>
 __global__ __launch_bounds__(EVAL_THREADS) void k_eval(State st)
 {
     constexpr int NT = EVAL_THREADS;
     constexpr int QPT = EVAL_QPT;
-    __shared__ int32_t Es[STAGE_MAX];
-    __shared__ int4 Ss[STAGE_MAX + 1];  // {pme, sm, ss, -} of live slot k, k = 0..B
+    constexpr int LCH = (LB_MAX + 1 + NT - 1) / NT; // table entries per thread
+    __shared__ int32_t Hs[LB_MAX];                 // histogram of remaining lengths
+    __shared__ int32_t LBs[LCH * NT];              // breakpoint table
+    __shared__ int4 Ss[PF_N * NT];                 // pms of live slot k, k = 0..B
+    __shared__ WInfo Wi[EVAL_WPB_MAX];
+    __shared__ int64_t red[NT / 64];
 
     const int s = find_scen<&Scen::eval_blk0>(st, blockIdx.x);
     const Scen sc = st.scen[s];
@@ -533,113 +658,174 @@ __global__ __launch_bounds__(EVAL_THREADS) void k_eval(State st)
     if (q0 >= end) return;
     const int32_t tau = cp->tau, hb = cp->hb_index;
     const int tid = threadIdx.x;
-    const bool want_ex = st.out_diag != nullptr;
+    const int lane = lane_id();
 
-    int32_t lin[QPT], lp[QPT], sq[QPT], eq[QPT];
-    int64_t qD[QPT];
+    int32_t lin[QPT], lp[QPT];
     bool act[QPT];
-    int32_t ex1[QPT], w1[QPT], ex2[QPT], w2[QPT];
+    uint64_t k1[QPT], k2[QPT];
+    int64_t lpmax = 0, qdmin = INT64_MAX, qdmax = INT64_MIN, lnmin = INT64_MAX, lnmax = INT64_MIN;
 #pragma unroll
     for (int m = 0; m < QPT; ++m) {
         const int qi = q0 + m * NT + tid;
         act[m] = qi < end;
         lin[m] = act[m] ? st.q_lin[qi] : 1;
         lp[m] = act[m] ? st.q_lpred[qi] : 1;
-        sq[m] = lin[m] - tau;
-        eq[m] = lp[m] + tau;
-        qD[m] = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
-        ex1[m] = ex2[m] = INT32_MAX;
-        w1[m] = w2[m] = -1;
+        k1[m] = k2[m] = ~0ull;
+        const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
+        if (act[m]) {
+            lpmax = lp[m] > lpmax ? lp[m] : lpmax;
+            qdmin = qD < qdmin ? qD : qdmin;
+            qdmax = qD > qdmax ? qD : qdmax;
+            lnmin = lin[m] < lnmin ? lin[m] : lnmin;
+            lnmax = lin[m] > lnmax ? lin[m] : lnmax;
+        }
     }
+    lpmax = block_all<NT>(lpmax, 0, OpMax(), red);
+    qdmin = block_all<NT>(qdmin, INT64_MAX, OpMin(), red);
+    qdmax = block_all<NT>(qdmax, INT64_MIN, OpMax(), red);
+    lnmin = block_all<NT>(lnmin, INT64_MAX, OpMin(), red);
+    lnmax = block_all<NT>(lnmax, INT64_MIN, OpMax(), red);
+    const int L = (int)lpmax;  // table covers v = 0 .. L
+    const bool use_lb = L <= LB_MAX;
+
     const int wbeg = wb * sc.wpb;
-    const int wend = min(sc.W, wbeg + sc.wpb);
-    // bit word of (query group, worker): group of queries m * NT + 64 * wave
-    const int64_t row0 = sc.bits_off + (int64_t)(((q0 - start) >> 6) + wave_id()) * sc.W;
-    for (int w = wbeg; w < wend; ++w) {
-        const int gw = sc.wbase + w;
-        const View v = load_view(st, gw, hb);
-        const Thr th = load_thr(st, gw);
-        const int B = v.n - v.head;
-        const bool staged = B < STAGE_MAX;  // block-uniform
-        // staged: 2^K - 1 >= B slots, the ones past B padded with INT32_MAX, so
-        // that a fixed-step search needs no bounds test
-        const int K = 32 - __clz(B);
-        int l[QPT];
+    const int nw = min(sc.W, wbeg + sc.wpb) - wbeg;
+    if (tid < nw) {
+        const int gw = sc.wbase + wbeg + tid;
+        WInfo x;
+        x.head = st.head[gw];
+        x.n = st.n[gw];
+        x.base = st.slot_base[gw] + x.head;
+        x.M = st.M[gw];
+        x.DS = st.DS[gw];
+        const bool cur = st.hbs[gw] == hb;
+        x.S1 = cur ? st.S1[gw] : 0;
+        x.S2 = cur ? st.S2[gw] : 0;
+        x.rhs = st.rhs[gw];
+        x.dq_max = st.dq_max[gw];
+        x.ntd_lo = st.ntd_lo[gw];
+        x.ntd_hi = st.ntd_hi[gw];
+        x.lthr = st.lthr[gw];
+        x.ntt_lo = st.ntt_lo[gw];
+        x.ntt_hi = st.ntt_hi[gw];
+        Wi[tid] = x;
+    }
+    for (int k = tid; k < LB_MAX; k += NT) Hs[k] = 0;
+    __syncthreads();
+
+    // The next worker's e column and summaries travel in registers while the
+    // current one is evaluated.  Plain loads of clamped (in-range) slots, masked
+    // only where they are used, so nothing waits for them before then.
+    Prefetch pf;
+    // bit word of (query group, worker) for lane j < 8 of each wave: feasibility
+    // (j < 4) or near-tie (j >= 4) of the wave's queries m = j & 3
+    const int64_t brow = sc.bits_off + (int64_t)(((q0 - start) >> 6) + wave_id() + (lane & 3) * (NT / 64)) * sc.W;
+    uint64_t* const bdst = (lane < 4 ? st.bits_feas : st.bits_nt) + brow;
+
+    if (nw > 0 && use_lb && Wi[0].n - Wi[0].head < STAGE_MAX) pf = prefetch_worker(st, Wi[0], tid);
+    for (int j0 = 0; j0 < nw; ++j0) {
+        const int w = wbeg + j0;
+        const WInfo wi = Wi[j0];
+        const int B = wi.n - wi.head;
+        const bool staged = use_lb && B < STAGE_MAX;  // block-uniform
         if (staged) {
-            __syncthreads();  // the previous worker's readers are done
-            const int P = (1 << K) - 1;
-            for (int k = tid; k < P; k += NT) Es[k] = k < B ? v.e[v.head + k] : INT32_MAX;
-            for (int k = tid; k <= B; k += NT)
-                Ss[k] = make_int4(v.pme[v.head + k], v.sm[v.head + k], v.ss[v.head + k], 0);
+            __syncthreads();  // the previous worker's readers of LBs / Ss are done
+#pragma unroll
+            for (int j = 0; j < PF_N; ++j) Ss[tid + j * NT] = pf.p[j];  // slots past B: copies, never read
+#pragma unroll
+            for (int j = 0; j < PF_N; ++j) {
+                const int32_t r = pf.e[j] - tau;  // remaining length; live requests have r >= 0
+                if (tid + j * NT < B && (uint32_t)r < (uint32_t)L) atomicAdd(&Hs[r], 1);
+            }
             __syncthreads();
-            // l = number of live requests ending before the query (lower bound
-            // of eq), for all queries of the thread in lockstep
+            // LBs[v] = sum of Hs[r] over r < v, v = 0 .. L; Hs is cleared behind
+            const int v0 = tid * LCH;
+            int32_t loc = 0;
 #pragma unroll
-            for (int m = 0; m < QPT; ++m) l[m] = 0;
-            for (int step = K > 0 ? 1 << (K - 1) : 0; step > 0; step >>= 1) {
+            for (int j = 0; j < LCH; ++j) {
+                const int v = v0 + j;
+                loc += (v < L) ? Hs[v] : 0;
+            }
+            const int32_t incl = wave_incl_scan(loc, 0, Add32());
+            if (lane == 63) red[wave_id()] = incl;
+            __syncthreads();
+            int32_t run = incl - loc;
 #pragma unroll
-                for (int m = 0; m < QPT; ++m) {
-                    const int c = l[m] + step;
-                    l[m] = Es[c - 1] < eq[m] ? c : l[m];
+            for (int j = 0; j < NT / 64; ++j) run += j < wave_id() ? (int32_t)red[j] : 0;
+#pragma unroll
+            for (int j = 0; j < LCH; ++j) {
+                const int v = v0 + j;
+                if (v <= L) LBs[v] = run;
+                if (v < L) {
+                    run += Hs[v];
+                    Hs[v] = 0;
                 }
             }
+            __syncthreads();
         }
+        if (j0 + 1 < nw && use_lb && Wi[j0 + 1].n - Wi[j0 + 1].head < STAGE_MAX)
+            pf = prefetch_worker(st, Wi[j0 + 1], tid);
+
+        const View v = winfo_view(st, wi);
+        // a near-tie margin needs some query of the chunk inside a tie band
+        const bool nt_any = !MONO || (qdmax >= wi.ntd_lo && qdmin <= wi.ntd_hi) ||
+                            (lnmax >= wi.ntt_lo && lnmin <= wi.ntt_hi);
+        uint64_t bits = 0;  // lane j < 8: the word it stores
 #pragma unroll
         for (int m = 0; m < QPT; ++m) {
-            int64_t peak;
+            const int32_t sq = lin[m] - tau, eq = lp[m] + tau;
+            int32_t peak;
             if (staged) {
-                const int4 t = Ss[l[m]];
-                const int64_t a = (int64_t)t.x + sq[m];
-                const int64_t b = (int64_t)t.y;
-                const int64_t c = (int64_t)t.z + (int64_t)(B - l[m]) * eq[m] + sq[m] + eq[m];
-                peak = a > b ? a : b;
+                // every candidate below is a KV demand with the query added, so
+                // it lies under the worker's peak (<= 2^30) plus l_in + l_pred:
+                // 32-bit wrap-around arithmetic gives it exactly
+                const int l = LBs[lp[m]];
+                const int4 t = Ss[l];
+                const int32_t a = (int32_t)((uint32_t)t.x + (uint32_t)sq);
+                const int32_t c = (int32_t)((uint32_t)t.z + (uint32_t)(B - l) * (uint32_t)eq + (uint32_t)sq +
+                                            (uint32_t)eq);
+                peak = a > t.y ? a : t.y;
                 peak = peak > c ? peak : c;
             } else {
-                peak = kv_peak_with(v, sq[m], eq[m]);
+                peak = (int32_t)kv_peak_with(v, sq, eq);
             }
-            bool dec_ok, ttft_ok, nt;
-            if (sc.mono) {
-                dec_ok = qD[m] <= th.dq_max;
-                ttft_ok = lin[m] <= th.lthr;
-                const bool maybe = (qD[m] >= th.ntd_lo && qD[m] <= th.ntd_hi) ||
-                                   (lin[m] >= th.ntt_lo && lin[m] <= th.ntt_hi);
-                nt = maybe && latency(sc, v, lin[m], lp[m], B + 1).nt;
+            bool dec_ok, ttft_ok, nt = false;
+            if (MONO) {
+                const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
+                dec_ok = qD <= wi.dq_max;
+                ttft_ok = lin[m] <= wi.lthr;
+                if (nt_any) {
+                    const bool maybe = (qD >= wi.ntd_lo && qD <= wi.ntd_hi) ||
+                                       (lin[m] >= wi.ntt_lo && lin[m] <= wi.ntt_hi);
+                    nt = maybe && latency(sc, v, lin[m], lp[m], B + 1).nt;
+                }
             } else {
-                const Latency L = latency(sc, v, lin[m], lp[m], B + 1);
-                dec_ok = L.dec_ok;
-                ttft_ok = L.ttft_ok;
-                nt = L.nt;
+                const Latency Lt = latency(sc, v, lin[m], lp[m], B + 1);
+                dec_ok = Lt.dec_ok;
+                ttft_ok = Lt.ttft_ok;
+                nt = Lt.nt;
             }
-            const bool feas = act[m] && peak <= v.M && dec_ok && ttft_ok;
-            const uint64_t bf = __ballot(feas);
-            const uint64_t bn = __ballot(act[m] && nt);
-            if (lane_id() == 0) {
-                const int64_t row = row0 + (int64_t)(m * (NT / 64)) * sc.W + w;
-                st.bits_feas[row] = bf;
-                st.bits_nt[row] = bn;
+            const uint64_t bf = __ballot(act[m] && peak <= wi.M && dec_ok && ttft_ok);
+            const uint64_t bn = nt_any ? __ballot(act[m] && nt) : 0;
+            bits = (lane == m) ? bf : bits;
+            bits = (lane == m + 4) ? bn : bits;
+            if (EX) {
+                const uint64_t key = ex_key(peak - wi.M, w);
+                const uint64_t hi = key > k1[m] ? key : k1[m];
+                k1[m] = key < k1[m] ? key : k1[m];
+                k2[m] = hi < k2[m] ? hi : k2[m];
             }
-            if (want_ex) min2_insert(ex1[m], w1[m], ex2[m], w2[m], (int32_t)(peak - v.M), w);
         }
+        if (lane < 8) bdst[w] = bits;
     }
 #pragma unroll
     for (int m = 0; m < QPT; ++m) {
         const int qi = q0 + m * NT + tid;
-        if (act[m]) st.part[sc.part_off + (int64_t)(qi - start) * sc.nblk + wb] = make_int4(ex1[m], w1[m], ex2[m], w2[m]);
+        int32_t ex1, w1, ex2, w2;
+        ex_unpack(k1[m], ex1, w1);
+        ex_unpack(k2[m], ex2, w2);
+        if (act[m]) st.part[sc.part_off + (int64_t)(qi - start) * sc.nblk + wb] = make_int4(ex1, w1, ex2, w2);
     }
-}
-
-// Read a lane's value (uniform result).
-__device__ __forceinline__ int32_t rdlane(int32_t v, int l) { return __builtin_amdgcn_readlane(v, l); }
-__device__ __forceinline__ uint64_t rdlane64(uint64_t v, int l)
-{
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
-    return ((uint64_t)hi << 32) | lo;
-}
-__device__ __forceinline__ int64_t rdlane64s(int64_t v, int l) { return (int64_t)rdlane64((uint64_t)v, l); }
-__device__ __forceinline__ double rdlane_f64(double v, int l)
-{
-    return __builtin_bit_cast(double, rdlane64(__builtin_bit_cast(uint64_t, v), l));
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -743,37 +929,6 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
 // device-coherent loads after a release fence.
 
 constexpr int DBITS_W = 2048;  // dirty bitmap words in LDS: scenarios of up to 65536 workers
-
-// ---- cross-lane primitives of the commit wave (DPP and readlane; no LDS
-// permutes on the sequential path)
-
-// Inclusive scan over the 64 lanes (lane 0 first) with DPP row shifts and row
-// broadcasts; lanes without a source keep the identity.
-template <typename Op>
-__device__ __forceinline__ int32_t wave_incl_scan(int32_t x, int32_t ident, Op op)
-{
-    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x111, 0xf, 0xf, false));  // row_shr:1
-    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x112, 0xf, 0xf, false));  // row_shr:2
-    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x114, 0xf, 0xf, false));  // row_shr:4
-    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x118, 0xf, 0xf, false));  // row_shr:8
-    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x142, 0xa, 0xf, false));  // row_bcast:15
-    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x143, 0xc, 0xf, false));  // row_bcast:31
-    return x;
-}
-struct Add32 {
-    __device__ int32_t operator()(int32_t a, int32_t b) const { return a + b; }
-};
-struct Max32 {
-    __device__ int32_t operator()(int32_t a, int32_t b) const { return a > b ? a : b; }
-};
-__device__ __forceinline__ int32_t wave_sum32(int32_t v) { return rdlane(wave_incl_scan(v, 0, Add32()), 63); }
-__device__ __forceinline__ int32_t wave_max32(int32_t v) { return rdlane(wave_incl_scan(v, INT32_MIN, Max32()), 63); }
-__device__ __forceinline__ int64_t wave_sum64(int64_t v)
-{
-#pragma unroll
-    for (int d = 32; d > 0; d >>= 1) v += __shfl_xor(v, d, 64);
-    return v;
-}
 
 // Lane holding the best (key, index) by Algorithm 1's order among lanes with
 // `valid`, or -1.  A scalar walk over the (few) candidate lanes.
@@ -902,7 +1057,8 @@ __device__ __forceinline__ bool win_bit(uint64_t lo, uint64_t hi, int start, int
 __device__ __forceinline__ View dagg_view(const DAgg& a, int32_t hb)
 {
     View v;
-    v.e = v.pme = v.sm = v.ss = nullptr;
+    v.e = nullptr;
+    v.pms = nullptr;
     v.head = a.head;
     v.n = a.n;
     v.M = a.M;
@@ -1530,9 +1686,13 @@ hipError_t launch_build(const State& st, hipStream_t stream, int mode)
     return hipGetLastError();
 }
 
-hipError_t launch_eval(const State& st, int32_t blocks, hipStream_t stream)
+hipError_t launch_eval(const State& st, int32_t blocks, bool mono, hipStream_t stream)
 {
-    hipLaunchKernelGGL(k_eval, dim3(blocks), dim3(EVAL_THREADS), 0, stream, st);
+    const bool ex = st.out_diag != nullptr;
+    if (mono && ex) hipLaunchKernelGGL((k_eval<true, true>), dim3(blocks), dim3(EVAL_THREADS), 0, stream, st);
+    else if (mono) hipLaunchKernelGGL((k_eval<true, false>), dim3(blocks), dim3(EVAL_THREADS), 0, stream, st);
+    else if (ex) hipLaunchKernelGGL((k_eval<false, true>), dim3(blocks), dim3(EVAL_THREADS), 0, stream, st);
+    else hipLaunchKernelGGL((k_eval<false, false>), dim3(blocks), dim3(EVAL_THREADS), 0, stream, st);
     return hipGetLastError();
 }
 
