@@ -142,8 +142,11 @@ int ald_worker_summary(ald_handle_t handle, int32_t* B, int64_t* sum_c, int64_t*
 
 /* Kernel timing with HIP events on the handle's stream (off by default).
  * kind: 0 = state build, 1 = pair evaluation, 2 = per-query selection,
- * 3 = commit.  Totals accumulate over calls while enabled; enabling resets them. */
-int ald_set_profiling(ald_handle_t handle, int32_t enable);
+ * 3 = commit.  `kinds` is a bit mask of the kinds to time (bit k = kind k,
+ * 15 = all, 0 = off; anything else outside 0..15 is ALD_EINVAL).  Each timed
+ * launch records two events, so time only what is needed.  Totals accumulate
+ * over calls while enabled; a nonzero mask resets them. */
+int ald_set_profiling(ald_handle_t handle, int32_t kinds);
 int ald_kernel_time(ald_handle_t handle, int32_t kind, double* total_ms, int64_t* launches);
 
 /* Message for the last error on this handle, or for a code. */

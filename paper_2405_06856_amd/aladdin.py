@@ -135,8 +135,8 @@ def ald_worker_summary(h, B, sum_c, sum_r, peak) -> None:
     _check(h, _L.ald_worker_summary(h, _dptr(B), _dptr(sum_c), _dptr(sum_r), _dptr(peak)))
 
 
-def ald_set_profiling(h, enable: bool) -> None:
-    _check(h, _L.ald_set_profiling(h, int(bool(enable))))
+def ald_set_profiling(h, kinds: int) -> None:
+    _check(h, _L.ald_set_profiling(h, int(kinds)))
 
 
 def ald_kernel_time(h, kind: int):
@@ -262,8 +262,17 @@ class Evaluator:
         return (rej.cpu().numpy(), first.cpu().numpy(),
                 ow.cpu().numpy().reshape(S, Q) if want_workers else None)
 
-    def profiling(self, enable=True):
-        ald_set_profiling(self.h, enable)
+    def profiling(self, enable=True, kinds=None):
+        """Time kernel kinds with HIP events: all of them, or the names in `kinds`."""
+        if not enable:
+            mask = 0
+        elif kinds is None:
+            mask = 15
+        else:
+            mask = 0
+            for k in kinds:
+                mask |= 1 << KERNEL_KINDS[k]
+        ald_set_profiling(self.h, mask)
 
     def kernel_time(self, kind: str):
         return ald_kernel_time(self.h, KERNEL_KINDS[kind])

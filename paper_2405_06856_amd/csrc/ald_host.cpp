@@ -61,7 +61,7 @@ struct ald_handle {
     bool rebuild_pending = false;  // the last call ended with a heartbeat: every worker is stale
     bool dirty_pending = false;    // the last commit round left workers with stale summaries
     int32_t* err_word = nullptr;
-    bool prof = false;
+    int32_t prof = 0;  // kernel kinds timed (bit k = kind k)
     std::vector<Events> pending;
     std::vector<Events> pool;
     double tot_ms[4] = {0, 0, 0, 0};
@@ -280,7 +280,8 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
 
 hipError_t prof_begin(ald_handle* h, int kind, Events* ev)
 {
-    if (!h->prof) return hipSuccess;
+    ev->kind = -1;
+    if (!((h->prof >> kind) & 1)) return hipSuccess;
     if (h->pool.empty()) {
         Events e;
         hipError_t r = hipEventCreate(&e.a);
@@ -297,7 +298,7 @@ hipError_t prof_begin(ald_handle* h, int kind, Events* ev)
 
 hipError_t prof_end(ald_handle* h, Events* ev)
 {
-    if (!h->prof) return hipSuccess;
+    if (ev->kind < 0) return hipSuccess;
     h->pending.push_back(*ev);
     return hipEventRecord(ev->b, h->stream);
 }
@@ -451,10 +452,11 @@ int ald_set_tile(ald_handle_t h, int32_t tile_queries)
     return ALD_OK;
 }
 
-int ald_set_profiling(ald_handle_t h, int32_t enable)
+int ald_set_profiling(ald_handle_t h, int32_t kinds)
 {
     if (!h) return ALD_EINVAL;
-    h->prof = enable != 0;
+    if (kinds < 0 || kinds > 15) return fail(h, ALD_EINVAL, "kinds must be a mask of bits 0..3");
+    h->prof = kinds;
     if (h->prof) {
         for (int k = 0; k < 4; ++k) { h->tot_ms[k] = 0; h->launches[k] = 0; }
     }
