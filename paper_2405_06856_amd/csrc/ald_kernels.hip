@@ -622,6 +622,76 @@ __device__ __forceinline__ Prefetch prefetch_worker(const State& st, const WInfo
     return f;
 }
 
+// Ranges of a chunk's query figures, for skipping near-tie work per worker.
+struct QRange {
+    int64_t qdmin, qdmax, lnmin, lnmax;
+};
+
+// Evaluate this thread's queries against one worker and store the wave's bit
+// words (lane j < 8 stores word j).  STAGED: breakpoint slot from the block's
+// table and summaries in LDS; else binary search over global memory.
+template <bool MONO, bool EX, bool STAGED>
+__device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, const WInfo& wi, int w, int32_t tau,
+                                            const int32_t (&lin)[EVAL_QPT], const int32_t (&lp)[EVAL_QPT],
+                                            const bool (&act)[EVAL_QPT], uint64_t (&k1)[EVAL_QPT],
+                                            uint64_t (&k2)[EVAL_QPT], const int32_t* LBs, const int4* Ss,
+                                            const QRange& qr, uint64_t* bdst)
+{
+    const int lane = lane_id();
+    const int B = wi.n - wi.head;
+    const View v = winfo_view(st, wi);
+    // a near-tie margin needs some query of the chunk inside a tie band
+    const bool nt_any = !MONO || (qr.qdmax >= wi.ntd_lo && qr.qdmin <= wi.ntd_hi) ||
+                        (qr.lnmax >= wi.ntt_lo && qr.lnmin <= wi.ntt_hi);
+    uint64_t bits = 0;  // lane j < 8: the word it stores
+#pragma unroll
+    for (int m = 0; m < EVAL_QPT; ++m) {
+        const int32_t sq = lin[m] - tau, eq = lp[m] + tau;
+        int32_t peak;
+        if (STAGED) {
+            // every candidate below is a KV demand with the query added, so it
+            // lies under the worker's peak (<= 2^30) plus l_in + l_pred: 32-bit
+            // wrap-around arithmetic gives it exactly
+            const int l = LBs[lp[m]];
+            const int4 t = Ss[l];
+            const int32_t a = (int32_t)((uint32_t)t.x + (uint32_t)sq);
+            const int32_t c =
+                (int32_t)((uint32_t)t.z + (uint32_t)(B - l) * (uint32_t)eq + (uint32_t)sq + (uint32_t)eq);
+            peak = a > t.y ? a : t.y;
+            peak = peak > c ? peak : c;
+        } else {
+            peak = (int32_t)kv_peak_with(v, sq, eq);
+        }
+        bool dec_ok, ttft_ok, nt = false;
+        if (MONO) {
+            const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
+            dec_ok = qD <= wi.dq_max;
+            ttft_ok = lin[m] <= wi.lthr;
+            if (nt_any) {
+                const bool maybe =
+                    (qD >= wi.ntd_lo && qD <= wi.ntd_hi) || (lin[m] >= wi.ntt_lo && lin[m] <= wi.ntt_hi);
+                nt = maybe && latency(sc, v, lin[m], lp[m], B + 1).nt;
+            }
+        } else {
+            const Latency Lt = latency(sc, v, lin[m], lp[m], B + 1);
+            dec_ok = Lt.dec_ok;
+            ttft_ok = Lt.ttft_ok;
+            nt = Lt.nt;
+        }
+        const uint64_t bf = __ballot(act[m] && peak <= wi.M && dec_ok && ttft_ok);
+        const uint64_t bn = nt_any ? __ballot(act[m] && nt) : 0;
+        bits = (lane == m) ? bf : bits;
+        bits = (lane == m + 4) ? bn : bits;
+        if (EX) {
+            const uint64_t key = ex_key(peak - wi.M, w);
+            const uint64_t hi = key > k1[m] ? key : k1[m];
+            k1[m] = key < k1[m] ? key : k1[m];
+            k2[m] = hi < k2[m] ? hi : k2[m];
+        }
+    }
+    if (lane < 8) bdst[w] = bits;
+}
+
 // Pair evaluation: block = (scenario, worker block, chunk of EVAL_Q queries).
 // Thread t holds queries t, t + 256, t + 512, t + 768 of the chunk.  For each
 // worker of the block, with its live set staged in LDS:
@@ -634,7 +704,7 @@ __device__ __forceinline__ Prefetch prefetch_worker(const State& st, const WInfo
 // worker's integer thresholds; EX: the two smallest KV excesses are tracked
 // (diagnostics).
 template <bool MONO, bool EX>
-__global__ __launch_bounds__(EVAL_THREADS) void k_eval(State st)
+__global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4))) void k_eval(State st)
 {
     constexpr int NT = EVAL_THREADS;
     constexpr int QPT = EVAL_QPT;
@@ -681,10 +751,11 @@ __global__ __launch_bounds__(EVAL_THREADS) void k_eval(State st)
         }
     }
     lpmax = block_all<NT>(lpmax, 0, OpMax(), red);
-    qdmin = block_all<NT>(qdmin, INT64_MAX, OpMin(), red);
-    qdmax = block_all<NT>(qdmax, INT64_MIN, OpMax(), red);
-    lnmin = block_all<NT>(lnmin, INT64_MAX, OpMin(), red);
-    lnmax = block_all<NT>(lnmax, INT64_MIN, OpMax(), red);
+    QRange qr;
+    qr.qdmin = block_all<NT>(qdmin, INT64_MAX, OpMin(), red);
+    qr.qdmax = block_all<NT>(qdmax, INT64_MIN, OpMax(), red);
+    qr.lnmin = block_all<NT>(lnmin, INT64_MAX, OpMin(), red);
+    qr.lnmax = block_all<NT>(lnmax, INT64_MIN, OpMax(), red);
     const int L = (int)lpmax;  // table covers v = 0 .. L
     const bool use_lb = L <= LB_MAX;
 
@@ -766,57 +837,14 @@ __global__ __launch_bounds__(EVAL_THREADS) void k_eval(State st)
         if (j0 + 1 < nw && use_lb && Wi[j0 + 1].n - Wi[j0 + 1].head < STAGE_MAX)
             pf = prefetch_worker(st, Wi[j0 + 1], tid);
 
-        const View v = winfo_view(st, wi);
-        // a near-tie margin needs some query of the chunk inside a tie band
-        const bool nt_any = !MONO || (qdmax >= wi.ntd_lo && qdmin <= wi.ntd_hi) ||
-                            (lnmax >= wi.ntt_lo && lnmin <= wi.ntt_hi);
-        uint64_t bits = 0;  // lane j < 8: the word it stores
-#pragma unroll
-        for (int m = 0; m < QPT; ++m) {
-            const int32_t sq = lin[m] - tau, eq = lp[m] + tau;
-            int32_t peak;
-            if (staged) {
-                // every candidate below is a KV demand with the query added, so
-                // it lies under the worker's peak (<= 2^30) plus l_in + l_pred:
-                // 32-bit wrap-around arithmetic gives it exactly
-                const int l = LBs[lp[m]];
-                const int4 t = Ss[l];
-                const int32_t a = (int32_t)((uint32_t)t.x + (uint32_t)sq);
-                const int32_t c = (int32_t)((uint32_t)t.z + (uint32_t)(B - l) * (uint32_t)eq + (uint32_t)sq +
-                                            (uint32_t)eq);
-                peak = a > t.y ? a : t.y;
-                peak = peak > c ? peak : c;
-            } else {
-                peak = (int32_t)kv_peak_with(v, sq, eq);
-            }
-            bool dec_ok, ttft_ok, nt = false;
-            if (MONO) {
-                const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
-                dec_ok = qD <= wi.dq_max;
-                ttft_ok = lin[m] <= wi.lthr;
-                if (nt_any) {
-                    const bool maybe = (qD >= wi.ntd_lo && qD <= wi.ntd_hi) ||
-                                       (lin[m] >= wi.ntt_lo && lin[m] <= wi.ntt_hi);
-                    nt = maybe && latency(sc, v, lin[m], lp[m], B + 1).nt;
-                }
-            } else {
-                const Latency Lt = latency(sc, v, lin[m], lp[m], B + 1);
-                dec_ok = Lt.dec_ok;
-                ttft_ok = Lt.ttft_ok;
-                nt = Lt.nt;
-            }
-            const uint64_t bf = __ballot(act[m] && peak <= wi.M && dec_ok && ttft_ok);
-            const uint64_t bn = nt_any ? __ballot(act[m] && nt) : 0;
-            bits = (lane == m) ? bf : bits;
-            bits = (lane == m + 4) ? bn : bits;
-            if (EX) {
-                const uint64_t key = ex_key(peak - wi.M, w);
-                const uint64_t hi = key > k1[m] ? key : k1[m];
-                k1[m] = key < k1[m] ? key : k1[m];
-                k2[m] = hi < k2[m] ? hi : k2[m];
-            }
-        }
-        if (lane < 8) bdst[w] = bits;
+        if (staged)
+            eval_worker<MONO, EX, true>(st, sc, wi, w, tau, lin, lp, act, k1, k2, LBs, Ss, qr, bdst);
+    }
+    // workers too large to stage: binary search over global memory
+    for (int j0 = 0; j0 < nw; ++j0) {
+        const WInfo wi = Wi[j0];
+        if (use_lb && wi.n - wi.head < STAGE_MAX) continue;
+        eval_worker<MONO, EX, false>(st, sc, wi, wbeg + j0, tau, lin, lp, act, k1, k2, LBs, Ss, qr, bdst);
     }
 #pragma unroll
     for (int m = 0; m < QPT; ++m) {
