@@ -990,11 +990,12 @@ __device__ __forceinline__ int32_t col(const int32_t* p, int k)
 }
 
 // KV demand peak with the query added, from a worker's live columns e, s
-// (B entries sorted by e).  All lanes take part; all get the result.  Lane l
-// takes chunk 63 - l, so a prefix over lanes is a suffix over slots.  Every
-// partial sum here is a token count below 2^31 (checked at the boundary).
+// (B entries sorted by e).  All lanes take part; all get the result, and the
+// worker's peak without the query in *p0.  Lane l takes chunk 63 - l, so a
+// prefix over lanes is a suffix over slots.  Every value here is a KV demand
+// below 2^31 (the worker's peak is at most 2^30, the query adds l_in + l_pred).
 template <bool GLOBAL>
-__device__ int64_t wave_kv_peak(const int32_t* e, const int32_t* s, int B, int32_t sq, int32_t eq)
+__device__ int64_t wave_kv_peak(const int32_t* e, const int32_t* s, int B, int32_t sq, int32_t eq, int32_t* p0)
 {
     const int lane = lane_id();
     const int CH = (B + 63) >> 6;
@@ -1004,7 +1005,7 @@ __device__ int64_t wave_kv_peak(const int32_t* e, const int32_t* s, int B, int32
     int32_t ls = 0;
     for (int k = k0; k < k1; ++k) ls += col<GLOBAL>(s, k);
     int64_t run = (int64_t)(wave_incl_scan(ls, 0, Add32()) - ls);  // slots after this chunk
-    int32_t best = INT32_MIN, ssge = 0, cge = 0;
+    int32_t best = INT32_MIN, best0 = 0, ssge = 0, cge = 0;
     for (int k = k1 - 1; k >= k0; --k) {
         const int32_t ek = col<GLOBAL>(e, k), sk = col<GLOBAL>(s, k);
         run += sk;  // sum of s over slots >= k
@@ -1012,9 +1013,11 @@ __device__ int64_t wave_kv_peak(const int32_t* e, const int32_t* s, int B, int32
         const bool before = ek < eq;  // the query is still alive at this end point
         const int32_t val = (int32_t)(before ? P + sq + ek : P);
         best = val > best ? val : best;
+        best0 = (int32_t)P > best0 ? (int32_t)P : best0;
         ssge += before ? 0 : sk;
         cge += before ? 0 : 1;
     }
+    *p0 = wave_max32(best0);
     const int64_t bmax = wave_max32(best);
     const int64_t own = (int64_t)wave_sum32(ssge) + (int64_t)wave_sum32(cge) * eq + sq + eq;
     return bmax > own ? bmax : own;
@@ -1039,21 +1042,24 @@ __device__ int64_t lane_kv_peak(const int32_t* e, const int32_t* s, int B, int32
     return best > own ? best : own;
 }
 
-// A worker committed to earlier in the tile.
+// Orders LDS traffic between the lanes of the (single-wave) commit block
+// without waiting for outstanding global memory operations.
+__device__ __forceinline__ void wave_sync() { __builtin_amdgcn_wave_barrier(); }
+
+// A worker committed to earlier in the tile.  The commit wave holds the j-th
+// such worker in lane j's registers.
 struct DAgg {
-    int32_t w;       // scenario-local index
+    int32_t w;       // scenario-local index, -1 = none
     int32_t B, n, head, M, hbs;
     int32_t empty0;  // it was empty when the tile started
     int32_t cap;
+    int32_t pub;     // upper bound of its KV peak without a new query (exact after a scan)
+    int32_t pad;
     int64_t base;    // first slot
     int64_t DS, S1, S2, SC, SR;
     uint64_t key;
     double rhs;
 };
-
-// Orders LDS traffic between the lanes of the (single-wave) commit block
-// without waiting for outstanding global memory operations.
-__device__ __forceinline__ void wave_sync() { __builtin_amdgcn_wave_barrier(); }
 
 // Bit words of the tile-start feasibility / near-tie masks that cover one
 // 64-query window, cached per dirty worker (one worker per lane).
@@ -1099,28 +1105,30 @@ __device__ __forceinline__ View dagg_view(const DAgg& a, int32_t hb)
     return v;
 }
 
-// Per-launch commit state held in LDS.
+// Per-launch commit state held in LDS.  dag[] mirrors the lanes' DAgg for the
+// per-lane diagnostics of rejected queries (diagnostics only); dw[] and dbits
+// say which workers are dirty.
 struct CommitLDS {
     DAgg dag[MAX_DIRTY];
+    int32_t dw[MAX_DIRTY];
     uint32_t dbits[DBITS_W];
     int32_t he[HOT];
     int32_t hs[HOT];
 };
 
-// Is worker w (scenario-local) dirty in this tile?
+// Is worker w (scenario-local) dirty in this tile?  (any lane, any w)
 __device__ __forceinline__ bool dirty_w(const CommitLDS& L, int W, int nd, int w)
 {
     if (W <= DBITS_W * 32) return (L.dbits[w >> 5] >> (w & 31)) & 1u;
     bool d = false;
-    for (int j = 0; j < nd; ++j) d = d | (L.dag[j].w == w);
+    for (int j = 0; j < nd; ++j) d = d | (L.dw[j] == w);
     return d;
 }
 
-// dag entry of a dirty worker (wave-cooperative; -1 if absent)
-__device__ __forceinline__ int dag_slot(const CommitLDS& L, int nd, int w)
+// Lane holding dirty worker w (wave-uniform w; -1 if w is not dirty).
+__device__ __forceinline__ int dirty_lane(const DAgg& a, int w)
 {
-    const int lane = lane_id();
-    const uint64_t m = __ballot(lane < nd && L.dag[lane < nd ? lane : 0].w == w);
+    const uint64_t m = __ballot(a.w == w && w >= 0);
     return m ? __ffsll((unsigned long long)m) - 1 : -1;
 }
 
@@ -1166,7 +1174,8 @@ __device__ __forceinline__ QView broadcast_q(const QSum& q, int p)
 }
 
 // Diagnostics of a query with no feasible worker at tile start (so none now),
-// decided by its own lane.
+// decided by its own lane (diagnostics only: reads the LDS mirror of the dirty
+// workers).
 __device__ Diag reject_diag(const State& st, const Scen& sc, const QSum& q, int i, int start, int w0, int32_t lin,
                             int32_t lp, int32_t tau, int32_t hb, const CommitLDS& L, int nd, int hot,
                             const WinBits& wb, int* abort)
@@ -1187,7 +1196,7 @@ __device__ Diag reject_diag(const State& st, const Scen& sc, const QSum& q, int 
             return d;
         }
         int j = 0;
-        while (j < nd && L.dag[j].w != q.w1) ++j;
+        while (j < nd && L.dw[j] != q.w1) ++j;
         const DAgg& a = L.dag[j];
         const int64_t base = a.base + a.head;
         const int64_t pk = (j == hot) ? lane_kv_peak<false>(L.he, L.hs, a.B, sq, eq)
@@ -1212,17 +1221,98 @@ __device__ Diag reject_diag(const State& st, const Scen& sc, const QSum& q, int 
 
 struct Decision {
     int32_t w;      // chosen worker, -1 = rejected
+    int32_t lane;   // dirty lane holding w, -1 when w was untouched in the tile
     int32_t abort;  // the tile-start lists cannot decide this query exactly
     Diag d;
 };
 
-// Decide one query with the whole wave.
+// Exact KV scans a decision ran, per lane.
+struct Scan {
+    bool done;   // this lane's worker was scanned for the query
+    int32_t pk;  // its KV peak with the query
+    int32_t p0;  // its KV peak without
+};
+
+// Number of entries of the sorted a[0, n) that are <= x.
+__device__ __forceinline__ int upper_bound_i32(const int32_t* a, int n, int32_t x)
+{
+    int lo = 0, len = n;
+    while (len > 0) {
+        const int half = len >> 1;
+        const bool right = a[lo + half] <= x;
+        lo = right ? lo + half + 1 : lo;
+        len = right ? len - half - 1 : half;
+    }
+    return lo;
+}
+
+// Insert (x, y) into the sorted LDS columns he/hs[0, B), after every entry
+// with he <= x (whole wave; the columns must have room for B + 1 entries).
+__device__ __forceinline__ void lds_sorted_insert(CommitLDS& L, int B, int32_t x, int32_t y)
+{
+    const int lane = lane_id();
+    int u = 0;
+    for (int k0 = 0; k0 < B; k0 += COMMIT_THREADS)
+        u += __popcll(__ballot(k0 + lane < B && L.he[k0 + lane] <= x));
+    // shift [u, B) up by one, highest block first (each pass reads before it writes)
+    for (int top = B; top > u; top -= COMMIT_THREADS) {
+        const int k = top - COMMIT_THREADS + lane;
+        const bool mv = k >= u && k < top;
+        int32_t ve = 0, vs = 0;
+        if (mv) {
+            ve = L.he[k];
+            vs = L.hs[k];
+        }
+        wave_sync();
+        if (mv) {
+            L.he[k + 1] = ve;
+            L.hs[k + 1] = vs;
+        }
+        wave_sync();
+    }
+    if (lane == 0) {
+        L.he[u] = x;
+        L.hs[u] = y;
+    }
+    wave_sync();
+}
+
+// The hot worker's LDS columns are a sorted prefix [0, Bs) and, without
+// diagnostics, an unsorted tail [Bs, Bs + m) of requests committed since it
+// became hot, in commit order.  Sort the tail into the prefix (in commit order,
+// so equal end points keep the order a sorted insert would give them).
+__device__ __noinline__ void lds_merge_tail(CommitLDS& L, int& Bs, int& m)
+{
+    for (int t = 0; t < m; ++t) {
+        const int32_t x = L.he[Bs + t], y = L.hs[Bs + t];  // read before the insert may move it
+        lds_sorted_insert(L, Bs + t, x, y);
+    }
+    Bs += m;
+    m = 0;
+}
+
+// KV peak with the query for dirty lane bl (whole wave): the hot worker's
+// columns from LDS (its tail sorted in first), the others from HBM.
+__device__ __forceinline__ int64_t dirty_kv_peak(const State& st, CommitLDS& L, const DAgg& a, int bl, int hot,
+                                                 int& hotBs, int& hotm, int32_t sq, int32_t eq, int32_t* p0)
+{
+    const int32_t cB = rdlane(a.B, bl);
+    if (bl == hot) {
+        if (hotm > 0) lds_merge_tail(L, hotBs, hotm);
+        return wave_kv_peak<false>(L.he, L.hs, cB, sq, eq, p0);
+    }
+    const int64_t base = rdlane64s(a.base, bl) + rdlane(a.head, bl);
+    return wave_kv_peak<true>(st.e + base, st.s + base, cB, sq, eq, p0);
+}
+
+// Decide one query with the whole wave.  `a` is this lane's dirty worker.
 __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int i, int start, int w0, int32_t lin,
-                           int32_t lp, int32_t tau, int32_t hb, const CommitLDS& L, int nd, int hot,
-                           int next_empty, bool want_diag, const WinBits& wb)
+                           int32_t lp, int32_t tau, int32_t hb, CommitLDS& L, int nd, int hot, int& hotBs,
+                           int& hotm, int next_empty, bool want_diag, const WinBits& wb, const DAgg& a, Scan& sn)
 {
     Decision r;
     r.w = -1;
+    r.lane = -1;
     r.abort = 0;
     r.d.n_feasible = 0;
     r.d.near_tie = 0;
@@ -1230,6 +1320,8 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
     r.d.kv_excess_min = 0;
     r.d.ttft_chosen = 0.0;
     r.d.tdec_chosen = 0.0;
+    sn.done = false;
+    sn.pk = sn.p0 = 0;
     const int lane = lane_id();
     const int32_t sq = lin - tau, eq = lp + tau;
     // best untouched candidate from the tile-start list
@@ -1240,7 +1332,8 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
 #pragma unroll
     for (int k = 0; k < TOPK; ++k) {
         const int w = q.tw[k];
-        const bool clean = (k < lim) && (w >= 0) && !dirty_w(L, sc.W, nd, w >= 0 ? w : 0);
+        const bool listed = (k < lim) && (w >= 0);
+        const bool clean = listed && dirty_lane(a, w) < 0;
         const bool take = clean & !have;
         bk = take ? q.tkey[k] : bk;
         bw = take ? w : bw;
@@ -1257,14 +1350,6 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
     }
     // workers changed earlier in the tile: one per lane
     const bool valid = lane < nd;
-    DAgg a;
-    a.w = -1;
-    a.B = a.n = a.head = a.M = a.hbs = a.empty0 = a.cap = 0;
-    a.base = 0;
-    a.DS = a.S1 = a.S2 = a.SC = a.SR = 0;
-    a.key = 0;
-    a.rhs = 0.0;
-    if (valid) a = L.dag[lane];
     bool fs = false, ns = false;
     Latency Lt;
     Lt.dec_ok = Lt.ttft_ok = Lt.nt = false;
@@ -1274,58 +1359,84 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
         ns = win_bit(wb.n0, wb.n1, start, w0, i);
         Lt = latency(sc, dagg_view(a, hb), lin, lp, a.B + 1);
     }
-    bool unknown = valid && fs && Lt.dec_ok && Lt.ttft_ok;  // KV check still needed
+    const bool unknown = valid && fs && Lt.dec_ok && Lt.ttft_ok;  // KV check still needed
+
+    if (!want_diag) {
+        // best-ranked first, stop at the first feasible one; a worker whose peak
+        // bound plus the query's own demand fits needs no scan (the query adds at
+        // most l_in + l_pred to the demand at any iteration)
+        bool cand = unknown && ranks_before(a.key, a.w, bk, bw);
+        const bool sure = cand && (int64_t)a.pub + lin + lp <= (int64_t)a.M;
+        for (;;) {
+            const int bl = wave_best_lane(a.key, a.w, cand);
+            if (bl < 0) break;
+            if ((__ballot(sure) >> bl) & 1) {
+                r.w = rdlane(a.w, bl);
+                r.lane = bl;
+                return r;
+            }
+            int32_t p0;
+            const int64_t pk = dirty_kv_peak(st, L, a, bl, hot, hotBs, hotm, sq, eq, &p0);
+            if (lane == bl) {
+                sn.done = true;
+                sn.pk = (int32_t)pk;
+                sn.p0 = p0;
+                cand = false;
+            }
+            if (pk <= rdlane(a.M, bl)) {
+                r.w = rdlane(a.w, bl);
+                r.lane = bl;
+                return r;
+            }
+        }
+        r.w = have ? bw : -1;
+        return r;
+    }
+
+    // ---- with diagnostics: every dirty candidate is scanned
+    bool cand = unknown;
     bool feas_now = false;
-    int64_t peak_now = 0;
-    // evaluate candidates best-first; without diagnostics stop at the first
-    // feasible one ranked above the current best
     for (;;) {
-        const bool cand = unknown && (want_diag || ranks_before(a.key, a.w, bk, bw));
         const int bl = wave_best_lane(a.key, a.w, cand);
         if (bl < 0) break;
-        const int32_t cB = rdlane(a.B, bl);
-        const int32_t chead = rdlane(a.head, bl);
-        const int32_t cM = rdlane(a.M, bl);
-        const int64_t base = rdlane64s(a.base, bl) + chead;
-        const int64_t pk = (bl == hot) ? wave_kv_peak<false>(L.he, L.hs, cB, sq, eq)
-                                       : wave_kv_peak<true>(st.e + base, st.s + base, cB, sq, eq);
-        const bool ok = pk <= cM;
+        int32_t p0;
+        const int64_t pk = dirty_kv_peak(st, L, a, bl, hot, hotBs, hotm, sq, eq, &p0);
+        const bool ok = pk <= rdlane(a.M, bl);
         if (lane == bl) {
-            unknown = false;
+            cand = false;
             feas_now = ok;
-            peak_now = pk;
+            sn.done = true;
+            sn.pk = (int32_t)pk;
+            sn.p0 = p0;
         }
-        if (!want_diag && ok) break;
     }
     const bool fdirty = valid && feas_now;
-    const int bl = wave_best_lane(a.key, a.w, fdirty);
-    if (bl >= 0) {
-        const uint64_t dk = rdlane64(a.key, bl);
-        const int32_t dw = rdlane(a.w, bl);
-        if (!have || ranks_before(dk, dw, bk, bw)) {
-            have = true;
-            bk = dk;
-            bw = dw;
+    {
+        const int bl = wave_best_lane(a.key, a.w, fdirty);
+        if (bl >= 0) {
+            const uint64_t dk = rdlane64(a.key, bl);
+            const int32_t dw = rdlane(a.w, bl);
+            if (!have || ranks_before(dk, dw, bk, bw)) {
+                have = true;
+                bk = dk;
+                bw = dw;
+                r.lane = bl;
+            }
         }
     }
     r.w = have ? bw : -1;
-    if (!want_diag) return r;
-
-    // ---- diagnostics at the current state
     r.d.n_feasible = q.nfeas - __popcll(__ballot(valid && fs)) + __popcll(__ballot(fdirty));
     // smallest KV excess
     int64_t exmin = q.ex1;
-    if (q.w1 >= 0 && dirty_w(L, sc.W, nd, q.w1)) {
-        if (q.w2 >= 0 && dirty_w(L, sc.W, nd, q.w2)) {
+    const int j1 = dirty_lane(a, q.w1);
+    if (q.w1 >= 0 && j1 >= 0) {
+        if (q.w2 >= 0 && dirty_lane(a, q.w2) >= 0) {
             r.abort = 1;
             return r;
         }
-        const int j = dag_slot(L, nd, q.w1);
-        const int32_t jB = rdlane(a.B, j), jhead = rdlane(a.head, j), jM = rdlane(a.M, j);
-        const int64_t base = rdlane64s(a.base, j) + jhead;
-        const int64_t pk = (j == hot) ? wave_kv_peak<false>(L.he, L.hs, jB, sq, eq)
-                                      : wave_kv_peak<true>(st.e + base, st.s + base, jB, sq, eq);
-        const int64_t ex_now = pk - jM;
+        int32_t p0;
+        const int64_t pk = dirty_kv_peak(st, L, a, j1, hot, hotBs, hotm, sq, eq, &p0);
+        const int64_t ex_now = pk - rdlane(a.M, j1);
         exmin = q.w2 < 0 ? ex_now : (ex_now < q.ex2 ? ex_now : (int64_t)q.ex2);
     }
     r.d.kv_excess_min = exmin;
@@ -1333,7 +1444,7 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
     const int clean_nt = q.ntcnt - __popcll(__ballot(valid && ns));
     bool nt = false;
     if (clean_nt > 0) {
-        if (q.ntw >= 0 && !dirty_w(L, sc.W, nd, q.ntw)) {
+        if (q.ntw >= 0 && dirty_lane(a, q.ntw) < 0) {
             nt = r.w < 0 || !ranks_before(bk, bw, q.ntkey, q.ntw);
         } else if (r.w < 0) {
             nt = true;
@@ -1347,11 +1458,10 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
     r.d.near_tie = nt ? 1 : 0;
     // the chosen worker's figures
     if (r.w >= 0) {
-        const int j = dag_slot(L, nd, r.w);
-        if (j >= 0) {
-            r.d.kv_peak_chosen = rdlane64s(peak_now, j);
-            r.d.ttft_chosen = rdlane_f64(Lt.ttft, j);
-            r.d.tdec_chosen = rdlane_f64(Lt.tdec, j);
+        if (r.lane >= 0) {
+            r.d.kv_peak_chosen = rdlane(sn.pk, r.lane);
+            r.d.ttft_chosen = rdlane_f64(Lt.ttft, r.lane);
+            r.d.tdec_chosen = rdlane_f64(Lt.tdec, r.lane);
         } else {
             // untouched in this tile: its summaries are current
             const View v = load_view(st, sc.wbase + r.w, hb);
@@ -1362,6 +1472,61 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
         }
     }
     return r;
+}
+
+// Write the hot worker's LDS columns back to its slot range in sorted order
+// (from slot 0 when the range would run past the worker's last slot) and
+// point its aggregates at them.  A prefix entry moves up by the number of tail
+// entries ending strictly before it; a tail entry lands after every prefix
+// entry ending no later and after earlier tail entries ending no later.  Whole
+// wave.
+__device__ void writeback_hot(const State& st, CommitLDS& L, DAgg& a, int hot, int Bs, int m, bool mirror)
+{
+    const int lane = lane_id();
+    const int B = Bs + m;
+    const int cap = rdlane(a.cap, hot);
+    const int head0 = rdlane(a.head, hot);
+    const int head = head0 + B <= cap ? head0 : 0;
+    int32_t* ge = st.e + rdlane64s(a.base, hot) + head;
+    int32_t* gs = st.s + rdlane64s(a.base, hot) + head;
+    for (int k0 = 0; k0 < Bs; k0 += COMMIT_THREADS) {
+        const int k = k0 + lane;
+        const bool in = k < Bs;
+        const int32_t x = in ? L.he[k] : 0, y = in ? L.hs[k] : 0;
+        int cnt = 0;
+        for (int t0 = 0; t0 < m; t0 += COMMIT_THREADS) {
+            const int32_t tv = t0 + lane < m ? L.he[Bs + t0 + lane] : INT32_MAX;
+            const int lim = min(COMMIT_THREADS, m - t0);
+            for (int jj = 0; jj < lim; ++jj) cnt += rdlane(tv, jj) < x ? 1 : 0;
+        }
+        if (in) {
+            ge[k + cnt] = x;
+            gs[k + cnt] = y;
+        }
+    }
+    for (int t0 = 0; t0 < m; t0 += COMMIT_THREADS) {
+        const int t = t0 + lane;
+        const bool in = t < m;
+        const int32_t x = in ? L.he[Bs + t] : 0, y = in ? L.hs[Bs + t] : 0;
+        int pos = upper_bound_i32(L.he, Bs, x);
+        for (int u0 = 0; u0 < m; u0 += COMMIT_THREADS) {
+            const int32_t tv = u0 + lane < m ? L.he[Bs + u0 + lane] : INT32_MAX;
+            const int lim = min(COMMIT_THREADS, m - u0);
+            for (int jj = 0; jj < lim; ++jj) {
+                const int32_t v = rdlane(tv, jj);
+                pos += (v < x || (v == x && u0 + jj < t)) ? 1 : 0;
+            }
+        }
+        if (in) {
+            ge[pos] = x;
+            gs[pos] = y;
+        }
+    }
+    if (lane == hot) {
+        a.head = head;
+        a.n = head + B;
+        if (mirror) L.dag[hot] = a;
+    }
 }
 
 __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
@@ -1412,12 +1577,20 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
     if (lane == 0) cp->rebuild = 0;
     wave_sync();
     const bool want_diag = st.out_diag != nullptr;
-    int nd = 0;            // dirty workers (wave-uniform)
-    // Column stores go only to the hot worker; they are fenced when another
-    // worker becomes hot, so every non-hot dirty worker's columns can be read
-    // back from HBM (coherently) and the hot one is read from LDS.
-    int hot = -1;          // dag entry whose columns are in L.he / L.hs
-    bool pending = false;  // hot-worker column stores not yet fenced
+    int nd = 0;    // dirty workers (wave-uniform); lane j < nd holds the j-th in `a`
+    DAgg a;
+    a.w = -1;
+    a.B = a.n = a.head = a.M = a.hbs = a.empty0 = a.cap = a.pub = a.pad = 0;
+    a.base = 0;
+    a.DS = a.S1 = a.S2 = a.SC = a.SR = 0;
+    a.key = 0;
+    a.rhs = 0.0;
+    // The hot worker's sorted live columns are in L.he / L.hs and its HBM copy
+    // is stale until it is written back (when another worker becomes hot, and at
+    // the end); every other dirty worker's columns are current in HBM and are
+    // read with device-coherent loads after the write-back's release fence.
+    int hot = -1;
+    int hotBs = 0, hotm = 0;  // the hot worker's sorted prefix and unsorted tail in L.he / L.hs
     int next_empty = sc.uniform_M ? next_empty_worker(st, sc, L, nd, 0) : -1;
     int pos = fpc;
     bool cut = false, err = false;
@@ -1438,7 +1611,7 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
         } else {
             q.nfeas = 0;
         }
-        if (lane < nd) wb = load_win_bits(st, sc, L.dag[lane].w, start, w0, end);
+        if (lane < nd) wb = load_win_bits(st, sc, a.w, start, w0, end);
         const uint64_t potm = __ballot(act && q.nfeas > 0);
         int cur = 0;
         while (cur < NT && w0 + cur < end) {
@@ -1472,8 +1645,9 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
             const int ip = w0 + p;
             const QView qv = broadcast_q(q, p);
             const int32_t plin = rdlane(lin, p), plp = rdlane(lp, p);
-            const Decision dc = decide(st, sc, qv, ip, start, w0, plin, plp, tau, hb, L, nd, hot, next_empty,
-                                       want_diag, wb);
+            Scan sn;
+            const Decision dc = decide(st, sc, qv, ip, start, w0, plin, plp, tau, hb, L, nd, hot, hotBs, hotm,
+                                       next_empty, want_diag, wb, a, sn);
             if (dc.abort) {
                 pos = ip;
                 cut = true;
@@ -1484,6 +1658,8 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
                 if (want_diag) st.out_diag[ip] = dc.d;
             }
             cur = p + 1;
+            // a scanned worker that does not take the query keeps its exact peak
+            if (sn.done && lane != dc.lane) a.pub = sn.p0;
             if (dc.w < 0) {
                 nrej += 1;
                 if (firstrej == INT32_MAX) firstrej = ip;
@@ -1492,118 +1668,91 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
 
             // ---- commit the query to worker w
             const int w = dc.w;
-            const int gw = sc.wbase + w;
-            int j = dag_slot(L, nd, w);
-            if (j < 0) {
+            int j = dc.lane;
+            if (j < 0) {  // first commit to w in this tile: its tile-start state is in HBM
                 j = nd;
-                DAgg x;
-                x.w = w;
-                x.n = st.n[gw];
-                x.head = st.head[gw];
-                x.B = st.B[gw];
-                x.M = st.M[gw];
-                x.hbs = st.hbs[gw];
-                x.empty0 = x.B == 0 ? 1 : 0;
-                x.cap = st.cap[gw];
-                x.base = st.slot_base[gw];
-                x.DS = st.DS[gw];
-                x.S1 = st.S1[gw];
-                x.S2 = st.S2[gw];
-                x.SC = st.SC[gw];
-                x.SR = st.SR[gw];
-                x.key = st.key[gw];
-                x.rhs = st.rhs[gw];
+                const int gw = sc.wbase + w;
+                if (lane == j) {
+                    a.w = w;
+                    a.n = st.n[gw];
+                    a.head = st.head[gw];
+                    a.B = st.B[gw];
+                    a.M = st.M[gw];
+                    a.hbs = st.hbs[gw];
+                    a.empty0 = a.B == 0 ? 1 : 0;
+                    a.cap = st.cap[gw];
+                    a.pub = a.B == 0 ? 0 : st.peak[gw];
+                    a.base = st.slot_base[gw];
+                    a.DS = st.DS[gw];
+                    a.S1 = st.S1[gw];
+                    a.S2 = st.S2[gw];
+                    a.SC = st.SC[gw];
+                    a.SR = st.SR[gw];
+                    a.key = st.key[gw];
+                    a.rhs = st.rhs[gw];
+                    wb = load_win_bits(st, sc, w, start, w0, end);
+                }
                 if (lane == 0) {
-                    L.dag[j] = x;
+                    L.dw[j] = w;
                     if (sc.W <= DBITS_W * 32) L.dbits[w >> 5] |= 1u << (w & 31);
                 }
-                if (lane == j) wb = load_win_bits(st, sc, w, start, w0, end);
                 nd += 1;
             }
-            wave_sync();
-            DAgg a = L.dag[j];
-            if (a.B + 1 > a.cap) {  // no slot left for one more live request
+            const int B0 = rdlane(a.B, j);
+            if (B0 + 1 > rdlane(a.cap, j)) {  // no slot left for one more live request
                 if (lane == 0) raise_error(&cp->err, DEV_ESLOTS);
                 err = true;
                 cut = true;
                 pos = ip + 1;
                 break;
             }
-            int32_t* ge = st.e + a.base;
-            int32_t* gs = st.s + a.base;
             if (hot != j) {
-                if (pending) {
+                if (hot >= 0) {
+                    writeback_hot(st, L, a, hot, hotBs, hotm, want_diag);
                     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-                    pending = false;
                 }
-                for (int k = lane; k < a.B; k += NT) {
-                    L.he[k] = col<true>(ge + a.head, k);
-                    L.hs[k] = col<true>(gs + a.head, k);
+                const int64_t gb = rdlane64s(a.base, j) + rdlane(a.head, j);
+                for (int k = lane; k < B0; k += NT) {
+                    L.he[k] = col<true>(st.e + gb, k);
+                    L.hs[k] = col<true>(st.s + gb, k);
                 }
                 hot = j;
+                hotBs = B0;
+                hotm = 0;
             }
             wave_sync();
             const int32_t eq = plp + tau, sq = plin - tau;
-            // insertion point: after every live request ending no later than the query
-            int u = 0;
-            for (int k0 = 0; k0 < a.B; k0 += NT) u += __popcll(__ballot(k0 + lane < a.B && L.he[k0 + lane] <= eq));
-            // shift [u, B) up by one, highest block first (each pass reads before it writes)
-            for (int top = a.B; top > u; top -= NT) {
-                const int k = top - NT + lane;
-                const bool mv = k >= u && k < top;
-                int32_t ve = 0, vs = 0;
-                if (mv) { ve = L.he[k]; vs = L.hs[k]; }
+            if (want_diag) {
+                // the per-lane diagnostics of rejected queries read sorted columns
+                lds_sorted_insert(L, B0, eq, sq);
+                hotBs = B0 + 1;
+            } else {
+                if (lane == 0) {
+                    L.he[B0] = eq;
+                    L.hs[B0] = sq;
+                }
+                hotm += 1;
                 wave_sync();
-                if (mv) { L.he[k + 1] = ve; L.hs[k + 1] = vs; }
-                wave_sync();
             }
-            if (lane == 0) {
-                L.he[u] = eq;
-                L.hs[u] = sq;
-            }
-            wave_sync();
-            const int B1 = a.B + 1;
-            int head = a.head;
-            int from = u;
-            if (head + B1 > a.cap) {  // reclaim the slots of finished requests
-                head = 0;
-                from = 0;
-            }
-            for (int k = from + lane; k < B1; k += NT) {
-                ge[head + k] = L.he[k];
-                gs[head + k] = L.hs[k];
-            }
-            pending = true;
-            // aggregates
-            a.B = B1;
-            a.head = head;
-            a.n = head + B1;
-            a.SC += plin;
-            a.SR += plp;
-            a.DS += ((int64_t)plin << sc.gs) + (int64_t)sc.gn * plp;
-            const int64_t X = (int64_t)B1 << sc.gs;
-            if ((a.DS >= ((int64_t)1 << 31) || X >= ((int64_t)1 << 31)) && lane == 0) raise_error(&cp->err, DEV_EOVERFLOW);
-            a.key = (uint64_t)(X * X) + (uint64_t)(a.DS * a.DS);
-            a.rhs = sc.theta * ((sc.tdec - sc.c3) - sc.c2 * (double)(B1 + 1));
-            const bool curhb = a.hbs == hb;
-            a.S1 = (curhb ? a.S1 : 0) + plin;
-            a.S2 = (curhb ? a.S2 : 0) + (int64_t)plin * plin;
-            a.hbs = hb;
-            if (a.S2 >= ((int64_t)1 << 53) && lane == 0) raise_error(&cp->err, DEV_EOVERFLOW);
-            if (lane == 0) {
-                L.dag[j] = a;
-                st.n[gw] = a.n;
-                st.head[gw] = a.head;
-                st.B[gw] = a.B;
-                st.SC[gw] = a.SC;
-                st.SR[gw] = a.SR;
-                st.DS[gw] = a.DS;
-                st.key[gw] = a.key;
-                st.rhs[gw] = a.rhs;
-                st.S1[gw] = a.S1;
-                st.S2[gw] = a.S2;
-                st.hbs[gw] = a.hbs;
-                st.built[gw] = 0;
+            // aggregates of lane j
+            if (lane == j) {
+                const int B1 = B0 + 1;
+                a.B = B1;
+                a.SC += plin;
+                a.SR += plp;
+                a.DS += ((int64_t)plin << sc.gs) + (int64_t)sc.gn * plp;
+                const int64_t X = (int64_t)B1 << sc.gs;
+                if (a.DS >= ((int64_t)1 << 31) || X >= ((int64_t)1 << 31)) raise_error(&cp->err, DEV_EOVERFLOW);
+                a.key = (uint64_t)(X * X) + (uint64_t)(a.DS * a.DS);
+                a.rhs = sc.theta * ((sc.tdec - sc.c3) - sc.c2 * (double)(B1 + 1));
+                const bool curhb = a.hbs == hb;
+                a.S1 = (curhb ? a.S1 : 0) + plin;
+                a.S2 = (curhb ? a.S2 : 0) + (int64_t)plin * plin;
+                a.hbs = hb;
+                if (a.S2 >= ((int64_t)1 << 53)) raise_error(&cp->err, DEV_EOVERFLOW);
+                // exact peak when this decision scanned the worker, else a bound
+                a.pub = sn.done ? sn.pk : (int32_t)((int64_t)a.pub + plin + plp);
+                if (want_diag) L.dag[j] = a;
             }
             wave_sync();
             ++commits;
@@ -1617,8 +1766,25 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
         if (err) break;
         if (!cut) pos = min(end, w0 + NT);
     }
-    // the workers whose summaries the next round must rebuild
-    for (int k = lane; k < nd; k += NT) st.dlist[s * MAX_DIRTY + k] = sc.wbase + L.dag[k].w;
+    // write back the hot worker's columns and every dirty worker's aggregates;
+    // list the workers whose summaries the next round must rebuild
+    if (hot >= 0) writeback_hot(st, L, a, hot, hotBs, hotm, false);
+    if (lane < nd) {
+        const int gw = sc.wbase + a.w;
+        st.n[gw] = a.n;
+        st.head[gw] = a.head;
+        st.B[gw] = a.B;
+        st.SC[gw] = a.SC;
+        st.SR[gw] = a.SR;
+        st.DS[gw] = a.DS;
+        st.key[gw] = a.key;
+        st.rhs[gw] = a.rhs;
+        st.S1[gw] = a.S1;
+        st.S2[gw] = a.S2;
+        st.hbs[gw] = a.hbs;
+        st.built[gw] = 0;
+        st.dlist[s * MAX_DIRTY + lane] = gw;
+    }
     if (lane == 0) {
         if (nrej) atomicAdd(&cp->n_rej, nrej);
         if (firstrej != INT32_MAX) atomicMin(&cp->first_rej, firstrej);
