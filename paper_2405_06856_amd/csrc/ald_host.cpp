@@ -171,6 +171,7 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
     State& st = a->st;
     Ctl* ctl = nullptr;
     TileInfo* ti = nullptr;
+    int32_t* qbad = nullptr;
     size_t worker_bytes = 0;
     auto carve = [&](Carver& c) {
         c.take(&st.slot_base, NW); c.take(&st.cap, NW); c.take(&st.n, NW); c.take(&st.head, NW);
@@ -182,7 +183,7 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
         worker_bytes = c.off;
         c.take(&st.e, slots); c.take(&st.s, slots); c.take(&st.pms, slots);
         c.take(&st.dlist, (size_t)a->S * MAX_DIRTY); c.take(&st.dcount, a->S);
-        c.take(&ctl, a->S); c.take(&ti, a->S); c.take(&a->dscen, a->S);
+        c.take(&ctl, a->S); c.take(&ti, a->S); c.take(&a->dscen, a->S); c.take(&qbad, 1);
     };
     Carver sizing{nullptr};
     carve(sizing);
@@ -198,6 +199,7 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
     st.ctl = ctl;
     st.tinfo = ti;
     st.scen = a->dscen;
+    st.qbad = a->S == 1 ? qbad : nullptr;  // the sweep checks its queries up front instead
     st.S = a->S;
     st.NW = a->NW;
     // every per-worker array starts at zero, then slot bases, slot counts and capacities
@@ -248,7 +250,8 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
         sc.bits_off = bits;
         bits += groups * sc.W;
         sc.part_off = part;
-        part += (int64_t)echunks * EVAL_Q * sc.nblk;
+        sc.pstride = (int64_t)echunks * EVAL_Q;
+        part += sc.pstride * sc.nblk;
         sc.qsum_off = qs;
         qs += (int64_t)schunks * SEL_THREADS;
     }
@@ -591,7 +594,7 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
     c.round = h->round;
     TileInfo ti{};
     ti.first_pc[0] = ti.first_pc[1] = INT32_MAX;
-    HIPCHK(h, launch_begin(c, ti, a->st.ctl, a->st.tinfo, q_l_in, q_l_pred, Q, h->stream));
+    HIPCHK(h, launch_begin(c, ti, a->st.ctl, a->st.tinfo, a->st.qbad, h->stream));
     a->st.q_lin = q_l_in;
     a->st.q_lpred = q_l_pred;
     a->st.out_worker = out_worker;

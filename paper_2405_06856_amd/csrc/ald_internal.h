@@ -67,7 +67,8 @@ struct Scen {
     int32_t uniform_M;  // every worker has the same capacity: empty workers are interchangeable
     int32_t mono;       // k1, k1q >= 0: the TTFT of a pair grows with l_in (integer thresholds apply)
     int64_t bits_off;   // uint64 words into bits_feas / bits_nt
-    int64_t part_off;   // int4 entries into part
+    int64_t part_off;   // int4 entries into part (worker block major: part_off + wb * pstride + query)
+    int64_t pstride;    // queries per tile rounded up to whole evaluation chunks
     int64_t qsum_off;   // QSum entries into qsum
     int64_t out_off;    // offset into out_worker
 };
@@ -177,6 +178,7 @@ struct State {
     int32_t* out_worker;
     Diag* out_diag;    // only with S == 1
     int32_t* err_word; // load-time validation
+    int32_t* qbad;     // nonzero: a query length of this call is invalid (one-scenario calls; else null)
 };
 
 inline __host__ __device__ int32_t tile_end(int32_t start, int32_t Q, int32_t T, int32_t H, int32_t since_hb) {
@@ -200,8 +202,8 @@ hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream);
 hipError_t launch_commit(const State& st, int32_t blocks, hipStream_t stream);
 hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q, Ctl* ctl, int32_t S,
                               hipStream_t stream);
-hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* tinfo, const int32_t* lin,
-                        const int32_t* lpred, int32_t Q, hipStream_t stream);
+hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* tinfo, int32_t* qbad,
+                        hipStream_t stream);
 hipError_t launch_summary(const State& st, int32_t W, int32_t* B, int64_t* sc, int64_t* sr, int64_t* peak,
                           hipStream_t stream);
 hipError_t launch_sweep_outputs(const State& st, int32_t* rejected, int32_t* first_reject, hipStream_t stream);

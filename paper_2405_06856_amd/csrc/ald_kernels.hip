@@ -719,6 +719,16 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
     const Scen sc = st.scen[s];
     const Ctl* cp = st.ctl + s;
     const int32_t start = cp->start, Q = cp->Q;
+    if (st.qbad != nullptr && start == 0) {
+        // first round of a one-scenario call: check every query length of the
+        // call before the first commit can run (grid-stride over all queries)
+        bool bad = false;
+        for (int64_t i = (int64_t)blockIdx.x * EVAL_THREADS + threadIdx.x; i < Q; i += (int64_t)gridDim.x * EVAL_THREADS) {
+            const int32_t a = st.q_lin[i], p = st.q_lpred[i];
+            bad = bad || !(a >= 1 && p >= 1 && a <= (1 << 24) && p <= (1 << 24));
+        }
+        if (__ballot(bad) != 0 && lane_id() == 0) atomicOr(st.qbad, 1);
+    }
     if (cp->err || start >= Q) return;
     const int32_t end = tile_end(start, Q, cp->T, cp->H, cp->since_hb);
     const int local = blockIdx.x - sc.eval_blk0;
@@ -846,13 +856,14 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
         if (use_lb && wi.n - wi.head < STAGE_MAX) continue;
         eval_worker<MONO, EX, false>(st, sc, wi, wbeg + j0, tau, lin, lp, act, k1, k2, LBs, Ss, qr, bdst);
     }
+    if (!EX) return;
 #pragma unroll
     for (int m = 0; m < QPT; ++m) {
         const int qi = q0 + m * NT + tid;
         int32_t ex1, w1, ex2, w2;
         ex_unpack(k1[m], ex1, w1);
         ex_unpack(k2[m], ex2, w2);
-        if (act[m]) st.part[sc.part_off + (int64_t)(qi - start) * sc.nblk + wb] = make_int4(ex1, w1, ex2, w2);
+        if (act[m]) st.part[sc.part_off + (int64_t)wb * sc.pstride + (qi - start)] = make_int4(ex1, w1, ex2, w2);
     }
 }
 
@@ -922,10 +933,11 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
         }
     }
     int32_t ex1 = INT32_MAX, w1 = -1, ex2 = INT32_MAX, w2 = -1;
-    const int4* prow = st.part + sc.part_off + (int64_t)(qi - start) * sc.nblk;
-    if (act) {
+    // the two smallest KV excesses feed only the diagnostics
+    const int4* prow = st.part + sc.part_off + (qi - start);
+    if (act && st.out_diag) {
         for (int b = 0; b < sc.nblk; ++b) {
-            const int4 p = prow[b];
+            const int4 p = prow[(int64_t)b * sc.pstride];
             min2_insert(ex1, w1, ex2, w2, p.x, p.y);
             min2_insert(ex1, w1, ex2, w2, p.z, p.w);
         }
@@ -1538,6 +1550,10 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
     const TileInfo ti = st.tinfo[s];
     Ctl* cp = st.ctl + s;
     const int lane = threadIdx.x;
+    if (st.qbad != nullptr && *st.qbad) {  // an invalid query length: nothing is written
+        if (part == 0 && lane == 0) cp->err = DEV_EINVAL;
+        return;
+    }
     if (ti.start >= ti.end) return;
     const int32_t start = ti.start, end = ti.end;
     const int32_t fpc = min(ti.first_pc[ti.parity], end);
@@ -1825,25 +1841,14 @@ __global__ __launch_bounds__(256) void k_query_stats(const int32_t* lin, const i
         for (int s = 0; s < S; ++s) atomicCAS(&ctl[s].err, 0, DEV_EINVAL);
 }
 
-// Start of an ald_place_stream call (one scenario): one block writes the
-// control block and tile record, then checks every query length; an invalid
-// one sets the control block's error, which makes every later kernel of the
-// call a no-op.  A single block, so no other block can race with the writes.
-__global__ __launch_bounds__(1024) void k_begin(Ctl c, TileInfo ti, Ctl* ctl, TileInfo* tinfo, const int32_t* lin,
-                                                const int32_t* lpred, int32_t Q)
+// Start of an ald_place_stream call (one scenario): the control block, the
+// tile record and a cleared query-error word (the first round's pair
+// evaluation checks the query lengths).
+__global__ void k_begin(Ctl c, TileInfo ti, Ctl* ctl, TileInfo* tinfo, int32_t* qbad)
 {
-    __shared__ int64_t red[16];
-    if (threadIdx.x == 0) {
-        *ctl = c;
-        *tinfo = ti;
-    }
-    int64_t bad = 0;
-    for (int i = threadIdx.x; i < Q; i += 1024) {
-        const int32_t a = lin[i], p = lpred[i];
-        bad += (a >= 1 && p >= 1 && a <= (1 << 24) && p <= (1 << 24)) ? 0 : 1;
-    }
-    bad = block_reduce<1024>(bad, 0, OpAdd(), red);
-    if (threadIdx.x == 0 && bad) ctl->err = DEV_EINVAL;
+    *ctl = c;
+    *tinfo = ti;
+    *qbad = 0;
 }
 
 __global__ void k_summary(State st, int32_t W, int32_t* B, int64_t* sc, int64_t* sr, int64_t* peak)
@@ -1912,10 +1917,10 @@ hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t 
     return hipGetLastError();
 }
 
-hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* tinfo, const int32_t* lin,
-                        const int32_t* lpred, int32_t Q, hipStream_t stream)
+hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* tinfo, int32_t* qbad,
+                        hipStream_t stream)
 {
-    hipLaunchKernelGGL(k_begin, dim3(1), dim3(1024), 0, stream, c, ti, ctl, tinfo, lin, lpred, Q);
+    hipLaunchKernelGGL(k_begin, dim3(1), dim3(1), 0, stream, c, ti, ctl, tinfo, qbad);
     return hipGetLastError();
 }
 

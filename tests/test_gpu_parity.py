@@ -252,6 +252,34 @@ def test_invalid_inputs_are_rejected(aladdin):
     ev.close()
 
 
+def test_invalid_query_late_in_stream_writes_nothing(aladdin):
+    # a bad length in a later tile is caught before the first commit of the
+    # call: outputs and worker state stay as they were, and the handle stays usable
+    import torch
+    t = wl.make_config("tiny")
+    ev = aladdin.Evaluator(0, tile=64)
+    ev.load_trace(t)
+    before = ev.summary()
+    dev = torch.device("cuda", 0)
+    ql = np.array(t.q_l_in, np.int32)
+    qp = np.array(t.q_l_pred, np.int32)
+    for idx, field, val in ((200, "lin", 0), (255, "lp", (1 << 24) + 1), (130, "lin", -5)):
+        a, b = ql.copy(), qp.copy()
+        (a if field == "lin" else b)[idx] = val
+        out = torch.full((len(a),), 12345, dtype=torch.int32, device=dev)
+        dg = torch.full((len(a) * 40,), 7, dtype=torch.uint8, device=dev)
+        with pytest.raises(aladdin.AladdinError) as ei:
+            ev.place_device(torch.as_tensor(a).to(dev), torch.as_tensor(b).to(dev), 0, True, out, dg)
+        assert ei.value.code == aladdin.ALD_EINVAL
+        assert bool((out == 12345).all()) and bool((dg == 7).all())
+        after = ev.summary()
+        assert all(np.array_equal(before[k], after[k]) for k in before)
+    res = ev.place(ql, qp, 0)
+    ev.close()
+    want = ref.place_trace(t)
+    assert np.array_equal(res.worker, want.worker)
+
+
 def test_sweep_small_matches_oracle(aladdin):
     s = wl.make_sweep("mini", 9, Q=700, worker_counts=(2, 3, 5, 16), gpu_counts=(1, 2), base_capacity=6000,
                       model=wl.BASE_MODEL, in_dist=wl.MID_IN, out_dist=wl.MID_OUT, rate=None)
