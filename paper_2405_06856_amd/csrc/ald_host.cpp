@@ -182,6 +182,7 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
         c.take(&st.lthr, NW); c.take(&st.ntt_lo, NW); c.take(&st.ntt_hi, NW);
         worker_bytes = c.off;
         c.take(&st.e, slots); c.take(&st.s, slots); c.take(&st.pms, slots);
+        c.take(&st.lbt, (size_t)NW * LB_MAX);
         c.take(&st.dlist, (size_t)a->S * MAX_DIRTY); c.take(&st.dcount, a->S);
         c.take(&ctl, a->S); c.take(&ti, a->S); c.take(&a->dscen, a->S); c.take(&qbad, 1);
     };
@@ -259,7 +260,7 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
     a->sel_blocks = sb;
     a->commit_blocks = cb;
     a->T = T;
-    const size_t need = (size_t)bits * 16 + (size_t)part * sizeof(int4) + (size_t)qs * sizeof(QSum) + 1024;
+    const size_t need = (size_t)bits * 16 + (size_t)part * sizeof(ulonglong2) + (size_t)qs * sizeof(QSum) + 1024;
     if (need > a->scratch_bytes) {
         if (a->scratch) HIPCHK(h, hipFree(a->scratch));
         a->scratch = nullptr;
@@ -273,8 +274,8 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
     a->st.bits_nt = (uint64_t*)p;
     p += (size_t)bits * 8;
     p = (char*)(((uintptr_t)p + 255) & ~(uintptr_t)255);
-    a->st.part = (int4*)p;
-    p += (size_t)part * sizeof(int4);
+    a->st.part = (ulonglong2*)p;
+    p += (size_t)part * sizeof(ulonglong2);
     p = (char*)(((uintptr_t)p + 255) & ~(uintptr_t)255);
     a->st.qsum = (QSum*)p;
     HIPCHK(h, hipMemcpyAsync(a->dscen, a->hscen.data(), a->S * sizeof(Scen), hipMemcpyHostToDevice, h->stream));
@@ -642,7 +643,7 @@ int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, i
         slots += scen[s].n_workers * (cap + 1);
     }
     if (NW > (1 << 30)) return fail(h, ALD_EINVAL, "too many workers");
-    if (slots * 24 > ((int64_t)128 << 30)) return fail(h, ALD_EINVAL, "sweep state would exceed 128 GiB");
+    if (slots * 24 + NW * (int64_t)LB_MAX * 2 > ((int64_t)128 << 30)) return fail(h, ALD_EINVAL, "sweep state would exceed 128 GiB");
     for (int s = 0; s < S; ++s) {
         sc[s] = make_scen(scen[s].model);
         W[s] = scen[s].n_workers;

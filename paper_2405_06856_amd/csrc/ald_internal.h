@@ -46,7 +46,7 @@ constexpr int32_t NEG = INT32_MIN;
 // pme with no slot before it: far below every demand, yet pme + sq cannot wrap
 // in 32 bits (|sq| < 2^28)
 constexpr int32_t PME_NONE = -(1 << 30);
-constexpr int LB_MAX = 2048;       // l_pred range of the per-block breakpoint table
+constexpr int LB_MAX = 2048;       // l_pred range of a worker's breakpoint table
 
 // error codes raised on the device (mirrors ALD_E* in aladdin.h)
 constexpr int32_t DEV_EINVAL = -1;
@@ -159,6 +159,9 @@ struct State {
     int32_t* e;
     int32_t* s;
     int4* pms;         // {pme, sm, ss, unused}
+    // per worker [NW * LB_MAX] (built workers with B > 0): entry v - 1 = number of
+    // live requests with remaining length below v, v = 1 .. LB_MAX
+    uint16_t* lbt;
     // per scenario [S]
     const Scen* scen;
     Ctl* ctl;
@@ -170,7 +173,7 @@ struct State {
     // tile scratch
     uint64_t* bits_feas;
     uint64_t* bits_nt;
-    int4* part;
+    ulonglong2* part;  // per (worker block, query): the two smallest KV-excess keys
     QSum* qsum;
     // queries and outputs
     const int32_t* q_lin;

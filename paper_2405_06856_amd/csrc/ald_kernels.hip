@@ -389,6 +389,31 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
         st.peak[gw] = B > 0 ? (int32_t)totP : 0;
         st.rhs[gw] = rhs;
     }
+    // Breakpoint table: a histogram of the remaining lengths r = e - tau of the
+    // live requests (those below LB_MAX), then an exclusive scan, so that entry
+    // v - 1 = number of live requests with r < v.
+    if (B > 0) {
+        __shared__ int32_t hist[LB_MAX];
+        for (int v = tid; v < LB_MAX; v += NT) hist[v] = 0;
+        __syncthreads();
+        for (int k = head + tid; k < n; k += NT) {
+            const int32_t r = e[k] - tau;
+            if ((uint32_t)r < (uint32_t)LB_MAX) atomicAdd(&hist[r], 1);
+        }
+        __syncthreads();
+        constexpr int CHV = LB_MAX / NT;  // entries per thread
+        int32_t loc = 0;
+#pragma unroll
+        for (int j = 0; j < CHV; ++j) loc += hist[tid * CHV + j];
+        int64_t tot;
+        int32_t run = (int32_t)block_scan_excl<NT, false>(loc, 0, OpAdd(), &tot, red);
+        uint16_t* out = st.lbt + (int64_t)gw * LB_MAX;
+#pragma unroll
+        for (int j = 0; j < CHV; ++j) {
+            run += hist[tid * CHV + j];  // now: requests with r <= tid * CHV + j
+            out[tid * CHV + j] = (uint16_t)run;  // entry v - 1 with v = tid * CHV + j + 1
+        }
+    }
     // Integer forms of the latency checks.  Both left sides are rounded fp64
     // expressions that never decrease as DS + qD (resp. l_in) grows -- each step
     // is an exact conversion, a product with a non-negative constant or a sum,
@@ -602,23 +627,21 @@ __device__ __forceinline__ void ex_unpack(uint64_t k, int32_t& ex, int32_t& w)
 }
 
 // One thread's share of a staged worker: slots tid + j * EVAL_THREADS of the
-// e column and of the summaries (clamped to slot B, which exists).
+// summaries (clamped to slot B, which exists) and 8 entries of its table.
 constexpr int PF_N = (STAGE_MAX + EVAL_THREADS - 1) / EVAL_THREADS;
 struct Prefetch {
-    int32_t e[PF_N];
     int4 p[PF_N];
+    uint4 lb;  // 8 entries of the worker's breakpoint table (zeros for an empty worker)
 };
 
-__device__ __forceinline__ Prefetch prefetch_worker(const State& st, const WInfo& x, int tid)
+__device__ __forceinline__ Prefetch prefetch_worker(const State& st, const WInfo& x, int gw, int tid)
 {
     Prefetch f;
     const int B = x.n - x.head;
 #pragma unroll
-    for (int j = 0; j < PF_N; ++j) {
-        const int k = min(tid + j * EVAL_THREADS, B);
-        f.e[j] = st.e[x.base + k];
-        f.p[j] = st.pms[x.base + k];
-    }
+    for (int j = 0; j < PF_N; ++j) f.p[j] = st.pms[x.base + min(tid + j * EVAL_THREADS, B)];
+    f.lb = make_uint4(0, 0, 0, 0);
+    if (B > 0) f.lb = reinterpret_cast<const uint4*>(st.lbt + (int64_t)gw * LB_MAX)[tid];
     return f;
 }
 
@@ -634,7 +657,7 @@ template <bool MONO, bool EX, bool STAGED>
 __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, const WInfo& wi, int w, int32_t tau,
                                             const int32_t (&lin)[EVAL_QPT], const int32_t (&lp)[EVAL_QPT],
                                             const bool (&act)[EVAL_QPT], uint64_t (&k1)[EVAL_QPT],
-                                            uint64_t (&k2)[EVAL_QPT], const int32_t* LBs, const int4* Ss,
+                                            uint64_t (&k2)[EVAL_QPT], const uint16_t* LBs, const int4* Ss,
                                             const QRange& qr, uint64_t* bdst)
 {
     const int lane = lane_id();
@@ -652,7 +675,7 @@ __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, con
             // every candidate below is a KV demand with the query added, so it
             // lies under the worker's peak (<= 2^30) plus l_in + l_pred: 32-bit
             // wrap-around arithmetic gives it exactly
-            const int l = LBs[lp[m]];
+            const int l = LBs[lp[m] - 1];  // live requests ending before the query
             const int4 t = Ss[l];
             const int32_t a = (int32_t)((uint32_t)t.x + (uint32_t)sq);
             const int32_t c =
@@ -694,23 +717,21 @@ __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, con
 
 // Pair evaluation: block = (scenario, worker block, chunk of EVAL_Q queries).
 // Thread t holds queries t, t + 256, t + 512, t + 768 of the chunk.  For each
-// worker of the block, with its live set staged in LDS:
-//   LB[v] = number of live requests with remaining length below v, for v up to
-//           the longest l_pred of the chunk (a histogram of remaining lengths
-//           and a block scan), so a query's breakpoint slot is l = LB[l_pred];
-//   the summaries of slot l then give the KV peak with the query added.
-// Workers with B >= STAGE_MAX, or chunks with an l_pred above LB_MAX, take the
-// binary search over global memory instead.  MONO: the latency checks use the
-// worker's integer thresholds; EX: the two smallest KV excesses are tracked
-// (diagnostics).
+// worker of the block, its summaries and breakpoint table (built with the
+// summaries) are staged in LDS; a query's breakpoint slot is then one table
+// read, l = LB[l_pred - 1], and the summaries of slot l give the KV peak with the
+// query added.  The next worker's data travels in registers while the current
+// one is evaluated.  Workers with B >= STAGE_MAX, or chunks with an l_pred above
+// LB_MAX, take the binary search over global memory instead.  MONO: the
+// latency checks use the worker's integer thresholds; EX: the two smallest KV
+// excesses are tracked (diagnostics).
 template <bool MONO, bool EX>
 __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4))) void k_eval(State st)
 {
     constexpr int NT = EVAL_THREADS;
     constexpr int QPT = EVAL_QPT;
-    constexpr int LCH = (LB_MAX + 1 + NT - 1) / NT; // table entries per thread
-    __shared__ int32_t Hs[LB_MAX];                 // histogram of remaining lengths
-    __shared__ int32_t LBs[LCH * NT];              // breakpoint table
+    static_assert(LB_MAX == 8 * NT, "one 16-byte table load per thread");
+    __shared__ uint16_t LBs[LB_MAX];               // the worker's breakpoint table
     __shared__ int4 Ss[PF_N * NT];                 // pms of live slot k, k = 0..B
     __shared__ WInfo Wi[EVAL_WPB_MAX];
     __shared__ int64_t red[NT / 64];
@@ -791,7 +812,6 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
         x.ntt_hi = st.ntt_hi[gw];
         Wi[tid] = x;
     }
-    for (int k = tid; k < LB_MAX; k += NT) Hs[k] = 0;
     __syncthreads();
 
     // The next worker's e column and summaries travel in registers while the
@@ -803,7 +823,7 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
     const int64_t brow = sc.bits_off + (int64_t)(((q0 - start) >> 6) + wave_id() + (lane & 3) * (NT / 64)) * sc.W;
     uint64_t* const bdst = (lane < 4 ? st.bits_feas : st.bits_nt) + brow;
 
-    if (nw > 0 && use_lb && Wi[0].n - Wi[0].head < STAGE_MAX) pf = prefetch_worker(st, Wi[0], tid);
+    if (nw > 0 && use_lb && Wi[0].n - Wi[0].head < STAGE_MAX) pf = prefetch_worker(st, Wi[0], sc.wbase + wbeg, tid);
     for (int j0 = 0; j0 < nw; ++j0) {
         const int w = wbeg + j0;
         const WInfo wi = Wi[j0];
@@ -813,39 +833,11 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
             __syncthreads();  // the previous worker's readers of LBs / Ss are done
 #pragma unroll
             for (int j = 0; j < PF_N; ++j) Ss[tid + j * NT] = pf.p[j];  // slots past B: copies, never read
-#pragma unroll
-            for (int j = 0; j < PF_N; ++j) {
-                const int32_t r = pf.e[j] - tau;  // remaining length; live requests have r >= 0
-                if (tid + j * NT < B && (uint32_t)r < (uint32_t)L) atomicAdd(&Hs[r], 1);
-            }
-            __syncthreads();
-            // LBs[v] = sum of Hs[r] over r < v, v = 0 .. L; Hs is cleared behind
-            const int v0 = tid * LCH;
-            int32_t loc = 0;
-#pragma unroll
-            for (int j = 0; j < LCH; ++j) {
-                const int v = v0 + j;
-                loc += (v < L) ? Hs[v] : 0;
-            }
-            const int32_t incl = wave_incl_scan(loc, 0, Add32());
-            if (lane == 63) red[wave_id()] = incl;
-            __syncthreads();
-            int32_t run = incl - loc;
-#pragma unroll
-            for (int j = 0; j < NT / 64; ++j) run += j < wave_id() ? (int32_t)red[j] : 0;
-#pragma unroll
-            for (int j = 0; j < LCH; ++j) {
-                const int v = v0 + j;
-                if (v <= L) LBs[v] = run;
-                if (v < L) {
-                    run += Hs[v];
-                    Hs[v] = 0;
-                }
-            }
+            reinterpret_cast<uint4*>(LBs)[tid] = pf.lb;
             __syncthreads();
         }
         if (j0 + 1 < nw && use_lb && Wi[j0 + 1].n - Wi[j0 + 1].head < STAGE_MAX)
-            pf = prefetch_worker(st, Wi[j0 + 1], tid);
+            pf = prefetch_worker(st, Wi[j0 + 1], sc.wbase + w + 1, tid);
 
         if (staged)
             eval_worker<MONO, EX, true>(st, sc, wi, w, tau, lin, lp, act, k1, k2, LBs, Ss, qr, bdst);
@@ -860,10 +852,7 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
 #pragma unroll
     for (int m = 0; m < QPT; ++m) {
         const int qi = q0 + m * NT + tid;
-        int32_t ex1, w1, ex2, w2;
-        ex_unpack(k1[m], ex1, w1);
-        ex_unpack(k2[m], ex2, w2);
-        if (act[m]) st.part[sc.part_off + (int64_t)wb * sc.pstride + (qi - start)] = make_int4(ex1, w1, ex2, w2);
+        if (act[m]) st.part[sc.part_off + (int64_t)wb * sc.pstride + (qi - start)] = make_ulonglong2(k1[m], k2[m]);
     }
 }
 
@@ -933,14 +922,22 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
         }
     }
     int32_t ex1 = INT32_MAX, w1 = -1, ex2 = INT32_MAX, w2 = -1;
-    // the two smallest KV excesses feed only the diagnostics
-    const int4* prow = st.part + sc.part_off + (qi - start);
+    // the two smallest KV excesses feed only the diagnostics: merge the worker
+    // blocks' two smallest keys (new first = smaller first; new second =
+    // min(larger first, smaller second))
     if (act && st.out_diag) {
+        const ulonglong2* prow = st.part + sc.part_off + (qi - start);
+        uint64_t a1 = ~0ull, a2 = ~0ull;
         for (int b = 0; b < sc.nblk; ++b) {
-            const int4 p = prow[(int64_t)b * sc.pstride];
-            min2_insert(ex1, w1, ex2, w2, p.x, p.y);
-            min2_insert(ex1, w1, ex2, w2, p.z, p.w);
+            const ulonglong2 p = prow[(int64_t)b * sc.pstride];
+            const uint64_t lo = p.x < a1 ? p.x : a1;
+            const uint64_t hi = p.x < a1 ? a1 : p.x;
+            const uint64_t s2 = p.y < a2 ? p.y : a2;
+            a1 = lo;
+            a2 = hi < s2 ? hi : s2;
         }
+        ex_unpack(a1, ex1, w1);
+        ex_unpack(a2, ex2, w2);
     }
     if (!act) return;
     QSum q;
