@@ -374,6 +374,7 @@ int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, 
         HIPCHK(h, hipHostMalloc((void**)&a->hctl, a->S * sizeof(Ctl), hipHostMallocDefault));
         a->hctl_n = a->S;
     }
+    HIPCHK(h, hipHostGetDevicePointer((void**)&a->st.ctl_host, a->hctl, 0));
     bool first = true;
     for (;;) {
         int64_t need = rounds_needed(hc);
@@ -386,7 +387,7 @@ int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, 
             LAUNCH(h, 2, launch_select(a->st, a->sel_blocks, h->stream));
             LAUNCH(h, 3, launch_commit(a->st, a->commit_blocks, h->stream));
         }
-        HIPCHK(h, hipMemcpyAsync(a->hctl, a->st.ctl, a->S * sizeof(Ctl), hipMemcpyDeviceToHost, h->stream));
+        // every commit launch wrote its scenarios' control blocks to the pinned mirror
         HIPCHK(h, hipStreamSynchronize(h->stream));
         std::copy(a->hctl, a->hctl + a->S, hc.begin());
         prof_collect(h);

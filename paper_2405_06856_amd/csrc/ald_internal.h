@@ -165,6 +165,7 @@ struct State {
     // per scenario [S]
     const Scen* scen;
     Ctl* ctl;
+    Ctl* ctl_host;     // pinned host mirror of ctl, written by the commit kernel
     TileInfo* tinfo;
     int32_t* dlist;    // [S * MAX_DIRTY] workers changed in the last tile (global index)
     int32_t* dcount;   // [S]

@@ -891,34 +891,45 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     // this wave's 64 queries share one bit word per worker; 64 workers' words
     // are read at once and only workers with a set bit are visited
     const int64_t row = sc.bits_off + (int64_t)((q0 - start) >> 6) * sc.W + (int64_t)wave_id() * sc.W;
-    for (int wb0 = 0; wb0 < sc.W; wb0 += 64) {
-        const int wl = wb0 + lane;
-        const bool in = wl < sc.W;
-        const uint64_t fl = in ? st.bits_feas[row + wl] : 0;
-        const uint64_t nl = in ? st.bits_nt[row + wl] : 0;
-        uint64_t mask = __ballot((fl | nl) != 0);
-        if (!mask) continue;
-        const uint64_t kl = in ? st.key[sc.wbase + wl] : 0;
-        while (mask) {
-            const int j = __ffsll((unsigned long long)mask) - 1;
-            mask &= mask - 1;
-            const uint64_t fw = rdlane64(fl, j);
-            const uint64_t nw = rdlane64(nl, j);
-            const uint64_t key = rdlane64(kl, j);
-            const int w = wb0 + j;
-            const bool f = (fw >> lane) & 1;
-            const bool nb = (nw >> lane) & 1;
-            nfeas += f ? 1 : 0;
-            // an empty worker has rank key 0; with uniform capacity all empty
-            // workers are alike and stand in one class
-            const bool cls = sc.uniform_M && key == 0;
-            efeas = efeas | (cls & f);
-            ncand += (f & !cls) ? 1 : 0;
-            topk_insert<TOPK>(tkey, tw, key, (f && !cls) ? w : -1);
-            ntcnt += nb ? 1 : 0;
-            const bool better = nb & ranks_before(key, w, ntkey, ntw);
-            ntkey = better ? key : ntkey;
-            ntw = better ? w : ntw;
+    constexpr int UB = 8;  // 64-worker batches whose words are loaded together
+    for (int g0 = 0; g0 < sc.W; g0 += 64 * UB) {
+        uint64_t fls[UB], nls[UB];
+#pragma unroll
+        for (int u = 0; u < UB; ++u) {
+            const int wl = g0 + u * 64 + lane;
+            const bool in = wl < sc.W;
+            fls[u] = in ? st.bits_feas[row + wl] : 0;
+            nls[u] = in ? st.bits_nt[row + wl] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < UB; ++u) {
+            const int wb0 = g0 + u * 64;
+            const uint64_t fl = fls[u], nl = nls[u];
+            uint64_t mask = __ballot((fl | nl) != 0);
+            if (!mask) continue;
+            const int wl = wb0 + lane;
+            const uint64_t kl = wl < sc.W ? st.key[sc.wbase + wl] : 0;
+            while (mask) {
+                const int j = __ffsll((unsigned long long)mask) - 1;
+                mask &= mask - 1;
+                const uint64_t fw = rdlane64(fl, j);
+                const uint64_t nw = rdlane64(nl, j);
+                const uint64_t key = rdlane64(kl, j);
+                const int w = wb0 + j;
+                const bool f = (fw >> lane) & 1;
+                const bool nb = (nw >> lane) & 1;
+                nfeas += f ? 1 : 0;
+                // an empty worker has rank key 0; with uniform capacity all empty
+                // workers are alike and stand in one class
+                const bool cls = sc.uniform_M && key == 0;
+                efeas = efeas | (cls & f);
+                ncand += (f & !cls) ? 1 : 0;
+                topk_insert<TOPK>(tkey, tw, key, (f && !cls) ? w : -1);
+                ntcnt += nb ? 1 : 0;
+                const bool better = nb & ranks_before(key, w, ntkey, ntw);
+                ntkey = better ? key : ntkey;
+                ntw = better ? w : ntw;
+            }
         }
     }
     int32_t ex1 = INT32_MAX, w1 = -1, ex2 = INT32_MAX, w2 = -1;
@@ -928,6 +939,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     if (act && st.out_diag) {
         const ulonglong2* prow = st.part + sc.part_off + (qi - start);
         uint64_t a1 = ~0ull, a2 = ~0ull;
+#pragma unroll 8
         for (int b = 0; b < sc.nblk; ++b) {
             const ulonglong2 p = prow[(int64_t)b * sc.pstride];
             const uint64_t lo = p.x < a1 ? p.x : a1;
@@ -1547,11 +1559,19 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
     const TileInfo ti = st.tinfo[s];
     Ctl* cp = st.ctl + s;
     const int lane = threadIdx.x;
+    // the control block as the host will read it (after the stream synchronises)
+    auto publish = [&]() {
+        if (st.ctl_host != nullptr && part == 0 && lane == 0) st.ctl_host[s] = *cp;
+    };
     if (st.qbad != nullptr && *st.qbad) {  // an invalid query length: nothing is written
         if (part == 0 && lane == 0) cp->err = DEV_EINVAL;
+        publish();
         return;
     }
-    if (ti.start >= ti.end) return;
+    if (ti.start >= ti.end) {
+        publish();
+        return;
+    }
     const int32_t start = ti.start, end = ti.end;
     const int32_t fpc = min(ti.first_pc[ti.parity], end);
 
@@ -1582,7 +1602,10 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
 
     // ---- the sequential wave
     const Ctl c = *cp;
-    if (c.err) return;
+    if (c.err) {
+        publish();
+        return;
+    }
     const int32_t tau = c.tau, hb = c.hb_index;
     __shared__ CommitLDS L;
     if (sc.W <= DBITS_W * 32)
@@ -1819,6 +1842,7 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
         cp->round = c.round + 1;
         st.tinfo[s].first_pc[(c.round + 1) & 1] = INT32_MAX;
     }
+    publish();
 }
 
 // ---------------------------------------------------------------------------------------------
