@@ -236,7 +236,7 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
     wpb = std::min(wpb, EVAL_WPB_MAX);
     int64_t bits = 0, part = 0, qs = 0;
     int32_t eb = 0, sb = 0, cb = 0;
-    const int32_t nfin = std::min(256, std::max(1, schunks / 2));
+    const int32_t nfin = 0;  // one commit wave per scenario, no helper blocks
     for (int s = 0; s < a->S; ++s) {
         Scen& sc = a->hscen[s];
         sc.wpb = std::min(wpb, std::max(1, sc.W));

@@ -965,7 +965,25 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     q.ex2 = ex2; q.w2 = w2;
     q.pad = 0;
     st.qsum[sc.qsum_off + (qi - start)] = q;
-    if (nfeas > 0) atomicMin(&st.tinfo[s].first_pc[parity], qi);
+    if (nfeas > 0) {
+        atomicMin(&st.tinfo[s].first_pc[parity], qi);
+    } else if (st.qbad == nullptr || *st.qbad == 0) {
+        // no feasible worker at tile start: rejected whatever the tile commits
+        // before it.  These tile-start diagnostics are exact for the queries
+        // before the tile's first commit; the commit overwrites every query
+        // from its first feasible one on.
+        if (st.out_worker) st.out_worker[sc.out_off + qi] = -1;
+        if (st.out_diag) {
+            Diag d;
+            d.n_feasible = 0;
+            d.near_tie = ntcnt > 0 ? 1 : 0;
+            d.kv_peak_chosen = 0;
+            d.kv_excess_min = ex1;
+            d.ttft_chosen = 0.0;
+            d.tdec_chosen = 0.0;
+            st.out_diag[qi] = d;
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -1555,7 +1573,7 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
     constexpr int NT = COMMIT_THREADS;
     const int s = find_scen<&Scen::fin_blk0>(st, blockIdx.x);
     const Scen sc = st.scen[s];
-    const int part = blockIdx.x - sc.fin_blk0;
+    const int part = blockIdx.x - sc.fin_blk0;  // 0: one block per scenario
     const TileInfo ti = st.tinfo[s];
     Ctl* cp = st.ctl + s;
     const int lane = threadIdx.x;
@@ -1574,31 +1592,6 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
     }
     const int32_t start = ti.start, end = ti.end;
     const int32_t fpc = min(ti.first_pc[ti.parity], end);
-
-    if (part > 0) {
-        // queries before the first one with any feasible worker: rejected, and
-        // no worker of the tile has changed yet when they are decided
-        int64_t cnt = 0;
-        for (int i = start + (part - 1) * NT + lane; i < fpc; i += sc.nfin * NT) {
-            const QSum& q = st.qsum[sc.qsum_off + (i - start)];
-            if (st.out_worker) st.out_worker[sc.out_off + i] = -1;
-            if (st.out_diag) {
-                Diag d;
-                d.n_feasible = 0;
-                d.near_tie = q.ntcnt > 0 ? 1 : 0;
-                d.kv_peak_chosen = 0;
-                d.kv_excess_min = q.ex1;
-                d.ttft_chosen = 0.0;
-                d.tdec_chosen = 0.0;
-                st.out_diag[i] = d;
-            }
-            ++cnt;
-        }
-        cnt = wave_sum64(cnt);
-        if (lane == 0 && cnt > 0) atomicAdd(&cp->n_rej, (int)cnt);
-        if (lane == 0 && part == 1 && fpc > start) atomicMin(&cp->first_rej, start);
-        return;
-    }
 
     // ---- the sequential wave
     const Ctl c = *cp;
@@ -1627,10 +1620,15 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
     // read with device-coherent loads after the write-back's release fence.
     int hot = -1;
     int hotBs = 0, hotm = 0;  // the hot worker's sorted prefix and unsorted tail in L.he / L.hs
-    int next_empty = sc.uniform_M ? next_empty_worker(st, sc, L, nd, 0) : -1;
+    // lowest-index empty untouched worker, looked up only when a decision can
+    // use it (-2 = not looked up yet; the search resumes at next_from)
+    int next_empty = sc.uniform_M ? -2 : -1;
+    int next_from = 0;
     int pos = fpc;
     bool cut = false, err = false;
-    int commits = 0, nrej = 0, firstrej = INT32_MAX;
+    int commits = 0;
+    int nrej = fpc - start;  // the rejected prefix (its outputs come from the selection kernel)
+    int firstrej = fpc > start ? start : INT32_MAX;
     WinBits wb;
     wb.f0 = wb.f1 = wb.n0 = wb.n1 = 0;
     while (pos < end && !cut) {
@@ -1681,6 +1679,7 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
             const int ip = w0 + p;
             const QView qv = broadcast_q(q, p);
             const int32_t plin = rdlane(lin, p), plp = rdlane(lp, p);
+            if (next_empty == -2 && qv.efeas) next_empty = next_empty_worker(st, sc, L, nd, next_from);
             Scan sn;
             const Decision dc = decide(st, sc, qv, ip, start, w0, plin, plp, tau, hb, L, nd, hot, hotBs, hotm,
                                        next_empty, want_diag, wb, a, sn);
@@ -1792,7 +1791,10 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
             }
             wave_sync();
             ++commits;
-            if (w == next_empty) next_empty = next_empty_worker(st, sc, L, nd, w + 1);
+            if (w == next_empty) {
+                next_empty = -2;
+                next_from = w + 1;
+            }
             if (nd >= MAX_DIRTY && w0 + cur < end) {
                 pos = w0 + cur;
                 cut = true;
