@@ -645,6 +645,22 @@ __device__ __forceinline__ Prefetch prefetch_worker(const State& st, const WInfo
     return f;
 }
 
+// Write one thread's share of a staged worker into an LDS buffer.
+__device__ __forceinline__ void stage_put(uint16_t* LBs, int4* Ss, const Prefetch& pf, int tid)
+{
+#pragma unroll
+    for (int j = 0; j < PF_N; ++j) Ss[tid + j * EVAL_THREADS] = pf.p[j];  // slots past B: copies, never read
+    reinterpret_cast<uint4*>(LBs)[tid] = pf.lb;
+}
+
+// First worker at or after j (block-local index) that is evaluated from LDS.
+__device__ __forceinline__ int next_staged(const WInfo* Wi, int nw, bool use_lb, int j)
+{
+    if (!use_lb) return nw;
+    while (j < nw && Wi[j].n - Wi[j].head >= STAGE_MAX) ++j;
+    return j;
+}
+
 // Ranges of a chunk's query figures, for skipping near-tie work per worker.
 struct QRange {
     int64_t qdmin, qdmax, lnmin, lnmax;
@@ -666,50 +682,74 @@ __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, con
     // a near-tie margin needs some query of the chunk inside a tie band
     const bool nt_any = !MONO || (qr.qdmax >= wi.ntd_lo && qr.qdmin <= wi.ntd_hi) ||
                         (qr.lnmax >= wi.ntt_lo && qr.lnmin <= wi.ntt_hi);
-    uint64_t bits = 0;  // lane j < 8: the word it stores
+    // KV peaks first: the table reads of all queries, then their summary reads,
+    // so that the LDS latencies overlap
+    int32_t peak[EVAL_QPT];
+    if (STAGED) {
+        int l[EVAL_QPT];
+        int4 t[EVAL_QPT];
 #pragma unroll
-    for (int m = 0; m < EVAL_QPT; ++m) {
-        const int32_t sq = lin[m] - tau, eq = lp[m] + tau;
-        int32_t peak;
-        if (STAGED) {
+        for (int m = 0; m < EVAL_QPT; ++m) l[m] = LBs[lp[m] - 1];  // live requests ending before the query
+#pragma unroll
+        for (int m = 0; m < EVAL_QPT; ++m) t[m] = Ss[l[m]];
+#pragma unroll
+        for (int m = 0; m < EVAL_QPT; ++m) {
             // every candidate below is a KV demand with the query added, so it
             // lies under the worker's peak (<= 2^30) plus l_in + l_pred: 32-bit
             // wrap-around arithmetic gives it exactly
-            const int l = LBs[lp[m] - 1];  // live requests ending before the query
-            const int4 t = Ss[l];
-            const int32_t a = (int32_t)((uint32_t)t.x + (uint32_t)sq);
-            const int32_t c =
-                (int32_t)((uint32_t)t.z + (uint32_t)(B - l) * (uint32_t)eq + (uint32_t)sq + (uint32_t)eq);
-            peak = a > t.y ? a : t.y;
-            peak = peak > c ? peak : c;
-        } else {
-            peak = (int32_t)kv_peak_with(v, sq, eq);
+            const uint32_t sq = (uint32_t)(lin[m] - tau), eq = (uint32_t)(lp[m] + tau);
+            const int32_t a = (int32_t)((uint32_t)t[m].x + sq);
+            const int32_t c = (int32_t)((uint32_t)t[m].z + (uint32_t)(B - l[m]) * eq + sq + eq);
+            const int32_t p = a > t[m].y ? a : t[m].y;
+            peak[m] = p > c ? p : c;
         }
-        bool dec_ok, ttft_ok, nt = false;
-        if (MONO) {
+    } else {
+#pragma unroll
+        for (int m = 0; m < EVAL_QPT; ++m) peak[m] = (int32_t)kv_peak_with(v, lin[m] - tau, lp[m] + tau);
+    }
+    uint64_t bits = 0;  // lane j < 8: the word it stores
+    if (MONO && !nt_any) {
+        // no query of the chunk can have a near-tie margin with this worker
+#pragma unroll
+        for (int m = 0; m < EVAL_QPT; ++m) {
             const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
-            dec_ok = qD <= wi.dq_max;
-            ttft_ok = lin[m] <= wi.lthr;
-            if (nt_any) {
+            const bool ok = act[m] && peak[m] <= wi.M && qD <= wi.dq_max && lin[m] <= wi.lthr;
+            const uint64_t bf = __ballot(ok);
+            bits = (lane == m) ? bf : bits;
+            if (EX) {
+                const uint64_t key = ex_key(peak[m] - wi.M, w);
+                const uint64_t hi = key > k1[m] ? key : k1[m];
+                k1[m] = key < k1[m] ? key : k1[m];
+                k2[m] = hi < k2[m] ? hi : k2[m];
+            }
+        }
+    } else {
+#pragma unroll
+        for (int m = 0; m < EVAL_QPT; ++m) {
+            bool dec_ok, ttft_ok, nt = false;
+            if (MONO) {
+                const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
+                dec_ok = qD <= wi.dq_max;
+                ttft_ok = lin[m] <= wi.lthr;
                 const bool maybe =
                     (qD >= wi.ntd_lo && qD <= wi.ntd_hi) || (lin[m] >= wi.ntt_lo && lin[m] <= wi.ntt_hi);
                 nt = maybe && latency(sc, v, lin[m], lp[m], B + 1).nt;
+            } else {
+                const Latency Lt = latency(sc, v, lin[m], lp[m], B + 1);
+                dec_ok = Lt.dec_ok;
+                ttft_ok = Lt.ttft_ok;
+                nt = Lt.nt;
             }
-        } else {
-            const Latency Lt = latency(sc, v, lin[m], lp[m], B + 1);
-            dec_ok = Lt.dec_ok;
-            ttft_ok = Lt.ttft_ok;
-            nt = Lt.nt;
-        }
-        const uint64_t bf = __ballot(act[m] && peak <= wi.M && dec_ok && ttft_ok);
-        const uint64_t bn = nt_any ? __ballot(act[m] && nt) : 0;
-        bits = (lane == m) ? bf : bits;
-        bits = (lane == m + 4) ? bn : bits;
-        if (EX) {
-            const uint64_t key = ex_key(peak - wi.M, w);
-            const uint64_t hi = key > k1[m] ? key : k1[m];
-            k1[m] = key < k1[m] ? key : k1[m];
-            k2[m] = hi < k2[m] ? hi : k2[m];
+            const uint64_t bf = __ballot(act[m] && peak[m] <= wi.M && dec_ok && ttft_ok);
+            const uint64_t bn = __ballot(act[m] && nt);
+            bits = (lane == m) ? bf : bits;
+            bits = (lane == m + 4) ? bn : bits;
+            if (EX) {
+                const uint64_t key = ex_key(peak[m] - wi.M, w);
+                const uint64_t hi = key > k1[m] ? key : k1[m];
+                k1[m] = key < k1[m] ? key : k1[m];
+                k2[m] = hi < k2[m] ? hi : k2[m];
+            }
         }
     }
     if (lane < 8) bdst[w] = bits;
@@ -823,24 +863,17 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
     const int64_t brow = sc.bits_off + (int64_t)(((q0 - start) >> 6) + wave_id() + (lane & 3) * (NT / 64)) * sc.W;
     uint64_t* const bdst = (lane < 4 ? st.bits_feas : st.bits_nt) + brow;
 
-    if (nw > 0 && use_lb && Wi[0].n - Wi[0].head < STAGE_MAX) pf = prefetch_worker(st, Wi[0], sc.wbase + wbeg, tid);
-    for (int j0 = 0; j0 < nw; ++j0) {
-        const int w = wbeg + j0;
-        const WInfo wi = Wi[j0];
-        const int B = wi.n - wi.head;
-        const bool staged = use_lb && B < STAGE_MAX;  // block-uniform
-        if (staged) {
-            __syncthreads();  // the previous worker's readers of LBs / Ss are done
-#pragma unroll
-            for (int j = 0; j < PF_N; ++j) Ss[tid + j * NT] = pf.p[j];  // slots past B: copies, never read
-            reinterpret_cast<uint4*>(LBs)[tid] = pf.lb;
-            __syncthreads();
-        }
-        if (j0 + 1 < nw && use_lb && Wi[j0 + 1].n - Wi[j0 + 1].head < STAGE_MAX)
-            pf = prefetch_worker(st, Wi[j0 + 1], sc.wbase + w + 1, tid);
-
-        if (staged)
-            eval_worker<MONO, EX, true>(st, sc, wi, w, tau, lin, lp, act, k1, k2, LBs, Ss, qr, bdst);
+    int cur = next_staged(Wi, nw, use_lb, 0);
+    if (cur < nw) pf = prefetch_worker(st, Wi[cur], sc.wbase + wbeg + cur, tid);
+    while (cur < nw) {
+        __syncthreads();  // the previous worker's readers of LBs / Ss are done
+        stage_put(LBs, Ss, pf, tid);
+        __syncthreads();
+        const int nxt = next_staged(Wi, nw, use_lb, cur + 1);
+        if (nxt < nw) pf = prefetch_worker(st, Wi[nxt], sc.wbase + wbeg + nxt, tid);
+        const WInfo wi = Wi[cur];
+        eval_worker<MONO, EX, true>(st, sc, wi, wbeg + cur, tau, lin, lp, act, k1, k2, LBs, Ss, qr, bdst);
+        cur = nxt;
     }
     // workers too large to stage: binary search over global memory
     for (int j0 = 0; j0 < nw; ++j0) {
