@@ -119,6 +119,31 @@ def test_ttft_not_monotone_in_lin(aladdin, k1, k1q):
     compare(*gpu_place(aladdin, t, tile=128), ref.place_trace(t), "ttft_nm")
 
 
+@pytest.mark.parametrize("seed", range(3))
+def test_unequal_capacities(aladdin, seed):
+    # capacities differ between workers (some equal), some workers start empty:
+    # empty workers are then ranked one by one instead of as one class
+    rng = np.random.default_rng(3000 + seed)
+    W = int(rng.integers(8, 48))
+    R = rng.integers(0, 3, W) * rng.integers(0, 30, W)  # about a third empty
+    t = wl.make_trace("capmix%d" % seed, 3100 + seed, W=W, R=0, Q=1500, kv_capacity=1, model=wl.BASE_MODEL,
+                      heartbeat_every=int(rng.choice([0, 40])), R_per_worker=R)
+    caps = rng.choice([9000, 16000, 16000, 30000, 60000], W).astype(np.int64)
+    t = dataclasses.replace(t, kv_capacity=caps)
+    compare(*gpu_place(aladdin, t, tile=int(rng.choice([64, 256]))), ref.place_trace(t), "capmix%d" % seed)
+
+
+def test_more_workers_than_the_dirty_bitmap(aladdin):
+    # 66,000 workers (the commit's LDS dirty bitmap covers 65,536) and a batch
+    # limit of about three requests, so a tile dirties many workers
+    model = dataclasses.replace(wl.BASE_MODEL, c2=0.012)
+    t = wl.make_trace("wide", 24, W=66000, R=0, Q=420, kv_capacity=200000, model=model)
+    got = gpu_place(aladdin, t, tile=256)
+    want = ref.place_trace(t, n_threads=16)
+    assert (want.worker >= 0).sum() > 200
+    compare(*got, want, "wide")
+
+
 def test_chunks_ending_on_heartbeats(aladdin):
     # calls that end exactly where a heartbeat falls: the next call must start
     # from summaries rebuilt at the advanced decode iteration
