@@ -218,6 +218,32 @@ def test_ttft_margin_exactly_zero_is_feasible():
     assert res.worker[1] == 1
 
 
+def test_decode_near_tie_band_is_relative():
+    # lhs = k2 * l_in = 0.1 against rhs = T_dec: a margin of 2e-10 is 2e-9
+    # relative (outside the 1e-9 band, although it is below 1e-9 in absolute
+    # terms); a margin of 5e-11 is 5e-10 relative (inside)
+    import math
+    for margin, flagged in ((2e-10, 0), (5e-11, 1)):
+        m = dataclasses.replace(FREE, c3=0.0, c2=0.0, k2=0.01, decode_slo=0.1 + margin, theta=1.0, gamma_num=0)
+        lhs, rhs = 0.01 * 10, 0.1 + margin
+        assert (abs(lhs - rhs) <= 1e-9 * max(abs(lhs), abs(rhs))) == bool(flagged)
+        assert math.isclose(abs(lhs - rhs), margin, rel_tol=1e-6)
+        res = run(1, 10 ** 6, [[]], m, [(10, 3)])
+        assert res.worker[0] == 0 and res.near_tie[0] == flagged, margin
+
+
+def test_capacity_norm_is_taken_before_placement():
+    # Algorithm 1 sorts the bins by ||(B, sum D)||_2 before placing the query.
+    # Worker 0: one request c=4, r=3 (sum D = 4 + 3/2); worker 1: three requests
+    # c=1, r=1 (sum D = 3 * 3/2).  Before placement worker 0 ranks first; with the
+    # query's batch slot already counted (B + 1) worker 1 would.
+    import math
+    assert math.hypot(1, 5.5) > math.hypot(3, 4.5)
+    assert math.hypot(1 + 1, 5.5) < math.hypot(3 + 1, 4.5)
+    res = run(2, 10 ** 6, [[(4, 3, 0)], [(1, 1, 0)] * 3], FREE, [(1, 1)])
+    assert res.worker[0] == 0
+
+
 def test_capacity_norm_ranking_picks_fullest_feasible():
     # worker 1 holds more context -> ranked first; worker 0 chosen only when 1 is full
     res = run(2, [100, 30], [[(2, 2, 0)], [(10, 5, 0)]], FREE, [(3, 3), (3, 3), (3, 3)])

@@ -1,0 +1,84 @@
+"""The oracle's pins have teeth: plant one plausible mistake at a time in a copy
+of the oracle's C source (never in the oracle itself), build it, and require
+that at least one pin of ``test_oracle.py`` fails against it (CPU only)."""
+from __future__ import annotations
+
+import os
+import subprocess
+
+import pytest
+
+from oracle import ref
+from tests import test_oracle as pins
+
+SRC = open(ref.SRC).read()
+
+# (name, original text, planted mistake)
+MUTANTS = [
+    ("kv end point one iteration early", "int64_t d_ = sumc + cnt * (t);", "int64_t d_ = sumc + cnt * ((t) - 1);"),
+    ("query's own end point not checked", "sumc += cq; cnt += 1;\n        DEMAND_AT(rq);", "sumc += cq; cnt += 1;"),
+    ("generated tokens not in the context", "add_request(&ws[i], lin + g, lp - g)", "add_request(&ws[i], lin, lp - g)"),
+    ("remaining length ignores generated tokens", "add_request(&ws[i], lin + g, lp - g)",
+     "add_request(&ws[i], lin + g, lp)"),
+    ("batch size without the query", "const int64_t b = B + 1;", "const int64_t b = B;"),
+    ("gamma applied to the context", "const int64_t DS = SC * ((int64_t)1 << gs) + gn * SR;",
+     "const int64_t DS = SC * gn + SR * ((int64_t)1 << gs);"),
+    ("TTFT without the query's prefill", "const int64_t S1 = w->S1 + lin;", "const int64_t S1 = w->S1;"),
+    ("quadratic prefill term linear", "const int64_t S2 = w->S2 + lin * lin;", "const int64_t S2 = w->S2 + lin;"),
+    ("ties to the highest index", "    return a < b;\n}", "    return a > b;\n}"),
+    ("rank key after placement", "(unsigned __int128)(B * ((int64_t)1 << gs));",
+     "(unsigned __int128)((B + 1) * ((int64_t)1 << gs));"),
+    ("heartbeat keeps the prefill sums", "    w->S1 = 0;\n    w->S2 = 0;\n}", "}"),
+    ("heartbeat evicts one iteration early", "if (w->r[i] >= 0) { keep = i + 1;", "if (w->r[i] > 0) { keep = i + 1;"),
+    ("heartbeat does not grow contexts", "        w->c[i] += 1;\n", ""),
+    ("near tie absolute", "return fabs(x - y) <= 1e-9 * m;", "return fabs(x - y) <= 1e-9;"),
+    ("KV check strict", "o->kv_ok = o->peak <= w->M;", "o->kv_ok = o->peak < w->M;"),
+    ("decode check strict", "o->dec_ok = o->lhs <= o->rhs;", "o->dec_ok = o->lhs < o->rhs;"),
+    ("TTFT check strict", "o->ttft_ok = o->ttft <= m->ttft_slo;", "o->ttft_ok = o->ttft < m->ttft_slo;"),
+    ("heartbeat counts only placements", "if (H > 0 && !no_commit) {\n            since_hb += 1;",
+     "if (H > 0 && !no_commit && best >= 0) {\n            since_hb += 1;"),
+    ("smallest excess over feasible workers only", "if (ex < excess_min) excess_min = ex;",
+     "if (pr[i].feasible && ex < excess_min) excess_min = ex;"),
+]
+
+PINS = [
+    pins.test_fig3_worked_example,
+    pins.test_peak_equals_footprint_vector_sum,
+    pins.test_lone_request_peak_closed_form,
+    pins.test_peak_ties_and_exact_capacity,
+    lambda: pins.test_placement_matches_bruteforce(0),
+    lambda: pins.test_placement_matches_bruteforce(1),
+    lambda: pins.test_placement_matches_bruteforce(3),
+    pins.test_heartbeat_is_one_iteration_shift,
+    pins.test_committed_placements_respect_every_constraint,
+    pins.test_decode_margin_exactly_zero_is_feasible_and_near_tie,
+    pins.test_ttft_margin_exactly_zero_is_feasible,
+    pins.test_capacity_norm_ranking_picks_fullest_feasible,
+    pins.test_decode_near_tie_band_is_relative,
+    pins.test_capacity_norm_is_taken_before_placement,
+]
+
+
+def test_mutant_table_applies():
+    for name, old, new in MUTANTS:
+        assert SRC.count(old) >= 1, name
+
+
+@pytest.mark.parametrize("idx", range(len(MUTANTS)), ids=[m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(idx, tmp_path, monkeypatch):
+    name, old, new = MUTANTS[idx]
+    src = tmp_path / "mutant.c"
+    src.write_text(SRC.replace(old, new, 1))
+    lib = tmp_path / "libmutant.so"
+    subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-fPIC",
+                           "-shared", "-o", str(lib), str(src), "-lm"])
+    monkeypatch.setattr(ref, "SRC", str(src))
+    monkeypatch.setattr(ref, "LIB", str(lib))
+    monkeypatch.setattr(ref, "_lib", None)
+    caught = []
+    for pin in PINS:
+        try:
+            pin()
+        except Exception as e:  # AssertionError, or an oracle error code
+            caught.append(getattr(pin, "__name__", "bruteforce") + ": " + type(e).__name__)
+    assert caught, "no pin caught the planted mistake: " + name
