@@ -232,11 +232,15 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
     const int64_t groups = (int64_t)echunks * (EVAL_Q / 64);
     int64_t NWtot = 0;
     for (int s = 0; s < a->S; ++s) NWtot += a->hW[s];
+    int32_t Wmax = 1;
+    for (int s = 0; s < a->S; ++s) Wmax = std::max(Wmax, a->hW[s]);
     int32_t wpb = (int32_t)std::max<int64_t>(1, (NWtot * echunks + target_blocks - 1) / target_blocks);
+    // at most 256 worker blocks per scenario: the selection merges one excess
+    // entry per worker block and query
+    wpb = std::max(wpb, (Wmax + 255) / 256);
     wpb = std::min(wpb, EVAL_WPB_MAX);
     int64_t bits = 0, part = 0, qs = 0;
     int32_t eb = 0, sb = 0, cb = 0;
-    const int32_t nfin = 0;  // one commit wave per scenario, no helper blocks
     for (int s = 0; s < a->S; ++s) {
         Scen& sc = a->hscen[s];
         sc.wpb = std::min(wpb, std::max(1, sc.W));
@@ -244,10 +248,14 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
         sc.eval_blk0 = eb;
         eb += sc.nblk * echunks;
         sc.sel_blk0 = sb;
-        sb += schunks;
-        sc.nfin = nfin;
+        // waves per 64-query group: more for wide scenarios, whose per-query
+        // scan over workers is long
+        sc.sel_g = sc.W >= 2048 ? 4 : (sc.W >= 1024 ? 2 : 1);
+        const int32_t qgroups = (T + 63) / 64;
+        const int32_t per_blk = (SEL_THREADS / 64) / sc.sel_g;
+        sb += (qgroups + per_blk - 1) / per_blk;
         sc.fin_blk0 = cb;
-        cb += 1 + nfin;
+        cb += 1;
         sc.bits_off = bits;
         bits += groups * sc.W;
         sc.part_off = part;

@@ -63,7 +63,7 @@ struct Scen {
     int32_t eval_blk0;  // first pair-evaluation block of this scenario
     int32_t sel_blk0;   // first selection block
     int32_t fin_blk0;   // the scenario's commit block
-    int32_t nfin;       // extra commit blocks (none)
+    int32_t sel_g;      // waves of a selection block that share one 64-query group (1, 2 or 4)
     int32_t uniform_M;  // every worker has the same capacity: empty workers are interchangeable
     int32_t mono;       // k1, k1q >= 0: the TTFT of a pair grows with l_in (integer thresholds apply)
     int64_t bits_off;   // uint64 words into bits_feas / bits_nt

@@ -908,11 +908,18 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
         ti->parity = parity;
     }
     if (done) return;
-    const int q0 = start + local * SEL_THREADS;
-    if (q0 >= end) return;
-    const int qi = q0 + threadIdx.x;
-    const bool act = qi < end;
+    // waves of the block: sel_g of them per 64-query group, each scanning its
+    // share of the workers
+    constexpr int NWV = SEL_THREADS / 64;
+    const int G = sc.sel_g;
+    const int wv = wave_id();
+    const int group = local * (NWV / G) + wv / G;  // 64-query group of this wave
+    const int slice = wv % G;                       // its share of the workers
+    const int q0 = start + group * 64;
+    const bool live = q0 < end;                     // wave-uniform
     const int lane = lane_id();
+    const int qi = q0 + lane;
+    const bool act = live && qi < end;
 
     uint64_t tkey[TOPK];
     int32_t tw[TOPK];
@@ -921,16 +928,19 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     int32_t nfeas = 0, ntcnt = 0, ntw = -1, ncand = 0;
     bool efeas = false;
     uint64_t ntkey = 0;
-    // this wave's 64 queries share one bit word per worker; 64 workers' words
+    // the group's 64 queries share one bit word per worker; 64 workers' words
     // are read at once and only workers with a set bit are visited
-    const int64_t row = sc.bits_off + (int64_t)((q0 - start) >> 6) * sc.W + (int64_t)wave_id() * sc.W;
+    const int64_t row = sc.bits_off + (int64_t)group * sc.W;
+    const int span = ((sc.W + G * 64 - 1) / (G * 64)) * 64;  // workers per wave, whole batches
+    const int wlo = live ? min(sc.W, slice * span) : 0;
+    const int whi = live ? min(sc.W, wlo + span) : 0;
     constexpr int UB = 8;  // 64-worker batches whose words are loaded together
-    for (int g0 = 0; g0 < sc.W; g0 += 64 * UB) {
+    for (int g0 = wlo; g0 < whi; g0 += 64 * UB) {
         uint64_t fls[UB], nls[UB];
 #pragma unroll
         for (int u = 0; u < UB; ++u) {
             const int wl = g0 + u * 64 + lane;
-            const bool in = wl < sc.W;
+            const bool in = wl < whi;
             fls[u] = in ? st.bits_feas[row + wl] : 0;
             nls[u] = in ? st.bits_nt[row + wl] : 0;
         }
@@ -941,7 +951,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
             uint64_t mask = __ballot((fl | nl) != 0);
             if (!mask) continue;
             const int wl = wb0 + lane;
-            const uint64_t kl = wl < sc.W ? st.key[sc.wbase + wl] : 0;
+            const uint64_t kl = wl < whi ? st.key[sc.wbase + wl] : 0;
             while (mask) {
                 const int j = __ffsll((unsigned long long)mask) - 1;
                 mask &= mask - 1;
@@ -965,6 +975,43 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
             }
         }
     }
+    // merge the group's partial results into its first wave (lists by rank,
+    // counts summed)
+    struct Part {
+        uint64_t tkey[TOPK];
+        int32_t tw[TOPK];
+        uint64_t ntkey;
+        int32_t ntw, nfeas, ncand, ntcnt, efeas, pad;
+    };
+    __shared__ Part parts[NWV][64];
+    if (G > 1) {
+        if (slice > 0) {
+            Part& pt = parts[wv][lane];
+#pragma unroll
+            for (int k = 0; k < TOPK; ++k) { pt.tkey[k] = tkey[k]; pt.tw[k] = tw[k]; }
+            pt.ntkey = ntkey;
+            pt.ntw = ntw;
+            pt.nfeas = nfeas;
+            pt.ncand = ncand;
+            pt.ntcnt = ntcnt;
+            pt.efeas = efeas ? 1 : 0;
+        }
+        __syncthreads();
+        if (slice > 0) return;
+        for (int v = wv + 1; v < wv + G; ++v) {
+            const Part& pt = parts[v][lane];
+#pragma unroll
+            for (int k = 0; k < TOPK; ++k) topk_insert<TOPK>(tkey, tw, pt.tkey[k], pt.tw[k]);
+            const bool better = ranks_before(pt.ntkey, pt.ntw, ntkey, ntw);
+            ntkey = better ? pt.ntkey : ntkey;
+            ntw = better ? pt.ntw : ntw;
+            nfeas += pt.nfeas;
+            ncand += pt.ncand;
+            ntcnt += pt.ntcnt;
+            efeas = efeas | (pt.efeas != 0);
+        }
+    }
+    if (!live) return;
     int32_t ex1 = INT32_MAX, w1 = -1, ex2 = INT32_MAX, w2 = -1;
     // the two smallest KV excesses feed only the diagnostics: merge the worker
     // blocks' two smallest keys (new first = smaller first; new second =
