@@ -27,7 +27,7 @@ struct Arena {
     size_t scratch_bytes = 0;
     void* scratch = nullptr;
     Scen* dscen = nullptr;
-    bool mono = true;     // every scenario's TTFT grows with l_in
+    int eval_mode = 2;    // how the pair evaluation takes the latency checks (launch_eval)
     Ctl* hctl = nullptr;  // pinned host copy of the control blocks
     int32_t hctl_n = 0;
 
@@ -120,6 +120,24 @@ int64_t batch_bound(const ald_model_t& m)
     return lo;
 }
 
+// Whether every near-tie band of a scenario spans at most 64 integer values,
+// for workers of up to `capmax` live requests.  Decode: the band around
+// rhs = theta ((T_dec - c3) - c2 (B + 1)) is under 3e-9 |rhs| wide including
+// rounding, while the left side grows by k2 2^-gs per unit of qD.  TTFT: the
+// band around T_pre is under 3e-9 T_pre wide plus the rounding of two TTFT
+// values (under 2e-15 (|c1| + T_pre)), while the TTFT grows by at least
+// k1 + k1q per unit of l_in.  Three values of slack on each side.
+bool nt_integer(const Scen& s, int32_t capmax)
+{
+    if (!s.mono) return false;
+    const double rmax = s.theta * (std::fabs(s.tdec - s.c3) + std::fabs(s.c2) * ((double)capmax + 1.0)) * (1.0 + 1e-12);
+    const double wd = 3e-9 * rmax / std::ldexp(s.k2, -s.gs) + 3.0;
+    const double tstep = s.k1 + s.k1q;
+    if (!(tstep > 0.0)) return false;
+    const double wt = (3e-9 * std::fabs(s.ttft) + 2e-15 * (std::fabs(s.c1) + std::fabs(s.ttft))) / tstep + 3.0;
+    return wd <= 64.0 && wt <= 64.0;
+}
+
 Scen make_scen(const ald_model_t& m)
 {
     Scen s{};
@@ -180,6 +198,7 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
         c.take(&st.peak, NW); c.take(&st.rhs, NW); c.take(&st.SC, NW); c.take(&st.SR, NW);
         c.take(&st.dq_max, NW); c.take(&st.ntd_lo, NW); c.take(&st.ntd_hi, NW);
         c.take(&st.lthr, NW); c.take(&st.ntt_lo, NW); c.take(&st.ntt_hi, NW);
+        c.take(&st.ntd_mask, NW); c.take(&st.ntt_mask, NW);
         worker_bytes = c.off;
         c.take(&st.e, slots); c.take(&st.s, slots); c.take(&st.pms, slots);
         c.take(&st.lbt, (size_t)NW * LB_MAX);
@@ -209,8 +228,17 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
     HIPCHK(h, hipMemcpyAsync(st.cap, caps.data(), NW * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
     HIPCHK(h, hipMemcpyAsync(st.M, Ms.data(), NW * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
     HIPCHK(h, hipMemsetAsync(st.dcount, 0, a->S * sizeof(int32_t), h->stream));
-    a->mono = true;
-    for (int s = 0; s < a->S; ++s) a->mono = a->mono && a->hscen[s].mono;
+    bool mono = true, ntint = true;
+    int64_t wfirst = 0;
+    for (int s = 0; s < a->S; ++s) {
+        int32_t capmax = 0;
+        for (int32_t i = 0; i < W[s]; ++i) capmax = std::max(capmax, caps[wfirst + i]);
+        wfirst += W[s];
+        a->hscen[s].ntint = nt_integer(a->hscen[s], capmax) ? 1 : 0;
+        mono = mono && a->hscen[s].mono;
+        ntint = ntint && a->hscen[s].ntint;
+    }
+    a->eval_mode = ntint ? 2 : (mono ? 1 : 0);
     // empty workers of a scenario are interchangeable when they share one capacity
     int64_t w0 = 0;
     for (int s = 0; s < a->S; ++s) {
@@ -391,7 +419,7 @@ int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, 
             const int mode = first ? first_mode : (build_every_round ? 0 : 1);
             first = false;
             if (mode >= 0) LAUNCH(h, 0, launch_build(a->st, h->stream, mode));
-            LAUNCH(h, 1, launch_eval(a->st, a->eval_blocks, a->mono, h->stream));
+            LAUNCH(h, 1, launch_eval(a->st, a->eval_blocks, a->eval_mode, h->stream));
             LAUNCH(h, 2, launch_select(a->st, a->sel_blocks, h->stream));
             LAUNCH(h, 3, launch_commit(a->st, a->commit_blocks, h->stream));
         }

@@ -66,6 +66,8 @@ struct Scen {
     int32_t sel_g;      // waves of a selection block that share one 64-query group (1, 2 or 4)
     int32_t uniform_M;  // every worker has the same capacity: empty workers are interchangeable
     int32_t mono;       // k1, k1q >= 0: the TTFT of a pair grows with l_in (integer thresholds apply)
+    int32_t ntint;      // with mono: every near-tie band spans at most 64 integer values (bound
+                        // from the coefficients), so near-tie margins have integer forms too
     int64_t bits_off;   // uint64 words into bits_feas / bits_nt
     int64_t part_off;   // int4 entries into part (worker block major: part_off + wb * pstride + query)
     int64_t pstride;    // queries per tile rounded up to whole evaluation chunks
@@ -155,6 +157,11 @@ struct State {
     int32_t* lthr;
     int32_t* ntt_lo;
     int32_t* ntt_hi;
+    // Exact near-tie sets where a band spans at most 64 values: bit i of ntd_mask
+    // is the decode margin test at qD = ntd_lo + i, bit i of ntt_mask the TTFT
+    // margin test at l_in = ntt_lo + i (zero where the band is wider).
+    uint64_t* ntd_mask;
+    uint64_t* ntt_mask;
     // per slot
     int32_t* e;
     int32_t* s;
@@ -201,7 +208,9 @@ hipError_t launch_ingest(const State& st, int32_t W, const int64_t* res_off, con
 // mode 0: every worker whose summaries are stale; 1: only the workers listed by
 // the last commit; 2: every worker unconditionally
 hipError_t launch_build(const State& st, hipStream_t stream, int mode);
-hipError_t launch_eval(const State& st, int32_t blocks, bool mono, hipStream_t stream);
+// mode 0: latency checks in fp64; 1: integer thresholds, near-tie margins in
+// fp64; 2: integer thresholds and near-tie sets
+hipError_t launch_eval(const State& st, int32_t blocks, int mode, hipStream_t stream);
 hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream);
 hipError_t launch_commit(const State& st, int32_t blocks, hipStream_t stream);
 hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q, Ctl* ctl, int32_t S,

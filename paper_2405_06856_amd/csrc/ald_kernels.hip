@@ -424,6 +424,8 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
     constexpr int64_t LMAX = (int64_t)1 << 24;
     const int wv = wave_id();
     const bool l0 = lane_id() == 0;
+    // Inside a band of at most 64 values the margin test itself is run once per
+    // value (one per lane), giving the exact near-tie set as a bit mask.
     if (wv == 0) {
         const int64_t x = wave_last_true(0, XMAX, [&](int64_t v) { return dec_lhs(sc, v) <= rhs; });
         if (l0) st.dq_max[gw] = x - DS;
@@ -432,9 +434,13 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
         const double lo = rhs - band, hi = rhs + band;
         const int64_t xl = wave_last_true(0, XMAX, [&](int64_t v) { return dec_lhs(sc, v) < lo; }) + 1;
         const int64_t xh = wave_last_true(0, XMAX, [&](int64_t v) { return dec_lhs(sc, v) <= hi; });
+        const int64_t width = xh - xl + 1;
+        const uint64_t mask = __ballot(lane_id() < width && near_tie(dec_lhs(sc, xl + lane_id()), rhs));
         if (l0) {
             st.ntd_lo[gw] = xl - DS;
             st.ntd_hi[gw] = xh - DS;
+            st.ntd_mask[gw] = width <= 64 ? mask : 0;
+            if (width > 64 && sc.ntint) raise_error(err, DEV_EOVERFLOW);
         }
     } else if (wv <= 3) {
         const bool cur = st.hbs[gw] == hb;
@@ -449,9 +455,13 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
             const double lo = sc.ttft - band, hi = sc.ttft + band;
             const int64_t ll = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) < lo; }) + 1;
             const int64_t lh = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) <= hi; });
+            const int64_t width = lh - ll + 1;
+            const uint64_t mask = __ballot(lane_id() < width && near_tie(tt(ll + lane_id()), sc.ttft));
             if (l0) {
                 st.ntt_lo[gw] = (int32_t)ll;
                 st.ntt_hi[gw] = (int32_t)lh;
+                st.ntt_mask[gw] = width <= 64 ? mask : 0;
+                if (width > 64 && sc.ntint) raise_error(err, DEV_EOVERFLOW);
             }
         }
     }
@@ -578,7 +588,9 @@ struct WInfo {
     int64_t DS, S1, S2;
     double rhs;
     int64_t dq_max, ntd_lo, ntd_hi;
+    uint64_t ntd_mask, ntt_mask;
     int32_t head, n, M, lthr, ntt_lo, ntt_hi;
+    int32_t nt_any;  // some query of the block's chunk may have a near-tie margin with this worker
 };
 
 __device__ __forceinline__ View winfo_view(const State& st, const WInfo& wi)
@@ -626,6 +638,21 @@ __device__ __forceinline__ void ex_unpack(uint64_t k, int32_t& ex, int32_t& w)
     w = k == ~0ull ? -1 : (int32_t)~(uint32_t)k;
 }
 
+// Keep a query's two smallest KV excesses as (excess, worker) pairs, smaller
+// excess first, then the higher index; e1 = INT32_MAX, w1 = -1 when empty
+// (every excess is below INT32_MAX).  IN_ORDER: w is above every index seen so
+// far, so an equal excess replaces.
+template <bool IN_ORDER>
+__device__ __forceinline__ void keep_two(int32_t ex, int32_t w, int32_t& e1, int32_t& w1, int32_t& e2, int32_t& w2)
+{
+    const bool b1 = IN_ORDER ? ex <= e1 : ((ex < e1) | ((ex == e1) & (w > w1)));
+    const bool b2 = IN_ORDER ? ex <= e2 : ((ex < e2) | ((ex == e2) & (w > w2)));
+    e2 = b1 ? e1 : (b2 ? ex : e2);
+    w2 = b1 ? w1 : (b2 ? w : w2);
+    e1 = b1 ? ex : e1;
+    w1 = b1 ? w : w1;
+}
+
 // One thread's share of a staged worker: slots tid + j * EVAL_THREADS of the
 // summaries (clamped to slot B, which exists) and 8 entries of its table.
 constexpr int PF_N = (STAGE_MAX + EVAL_THREADS - 1) / EVAL_THREADS;
@@ -668,20 +695,20 @@ struct QRange {
 
 // Evaluate this thread's queries against one worker and store the wave's bit
 // words (lane j < 8 stores word j).  STAGED: breakpoint slot from the block's
-// table and summaries in LDS; else binary search over global memory.
-template <bool MONO, bool EX, bool STAGED>
+// table and summaries in LDS; else binary search over global memory.  MODE as
+// for launch_eval.
+template <int MODE, bool EX, bool STAGED>
 __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, const WInfo& wi, int w, int32_t tau,
                                             const int32_t (&lin)[EVAL_QPT], const int32_t (&lp)[EVAL_QPT],
-                                            const bool (&act)[EVAL_QPT], uint64_t (&k1)[EVAL_QPT],
-                                            uint64_t (&k2)[EVAL_QPT], const uint16_t* LBs, const int4* Ss,
-                                            const QRange& qr, uint64_t* bdst)
+                                            const bool (&act)[EVAL_QPT], int32_t (&e1)[EVAL_QPT],
+                                            int32_t (&w1)[EVAL_QPT], int32_t (&e2)[EVAL_QPT],
+                                            int32_t (&w2)[EVAL_QPT], const uint16_t* LBs, const int4* Ss,
+                                            uint64_t* bdst)
 {
+    constexpr bool MONO = MODE >= 1;
     const int lane = lane_id();
     const int B = wi.n - wi.head;
     const View v = winfo_view(st, wi);
-    // a near-tie margin needs some query of the chunk inside a tie band
-    const bool nt_any = !MONO || (qr.qdmax >= wi.ntd_lo && qr.qdmin <= wi.ntd_hi) ||
-                        (qr.lnmax >= wi.ntt_lo && qr.lnmin <= wi.ntt_hi);
     // KV peaks first: the table reads of all queries, then their summary reads,
     // so that the LDS latencies overlap
     int32_t peak[EVAL_QPT];
@@ -708,51 +735,65 @@ __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, con
         for (int m = 0; m < EVAL_QPT; ++m) peak[m] = (int32_t)kv_peak_with(v, lin[m] - tau, lp[m] + tau);
     }
     uint64_t bits = 0;  // lane j < 8: the word it stores
-    if (MONO && !nt_any) {
-        // no query of the chunk can have a near-tie margin with this worker
+    if (MONO) {
+        // feasibility from the integer thresholds (the worker's figures read
+        // once; no short-circuit, so no branch per query)
+        const int32_t M = wi.M, lthr = wi.lthr;
+        const int64_t dq_max = wi.dq_max;
 #pragma unroll
         for (int m = 0; m < EVAL_QPT; ++m) {
             const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
-            const bool ok = act[m] && peak[m] <= wi.M && qD <= wi.dq_max && lin[m] <= wi.lthr;
+            const bool ok = act[m] & (peak[m] <= M) & (qD <= dq_max) & (lin[m] <= lthr);
             const uint64_t bf = __ballot(ok);
             bits = (lane == m) ? bf : bits;
-            if (EX) {
-                const uint64_t key = ex_key(peak[m] - wi.M, w);
-                const uint64_t hi = key > k1[m] ? key : k1[m];
-                k1[m] = key < k1[m] ? key : k1[m];
-                k2[m] = hi < k2[m] ? hi : k2[m];
-            }
+            if (EX) keep_two<STAGED>(peak[m] - M, w, e1[m], w1[m], e2[m], w2[m]);
         }
+        // near-tie words (lanes 4..7) stay zero here: near_tie_words fills
+        // them in for the workers with nt_any
     } else {
 #pragma unroll
         for (int m = 0; m < EVAL_QPT; ++m) {
-            bool dec_ok, ttft_ok, nt = false;
-            if (MONO) {
-                const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
-                dec_ok = qD <= wi.dq_max;
-                ttft_ok = lin[m] <= wi.lthr;
-                const bool maybe =
-                    (qD >= wi.ntd_lo && qD <= wi.ntd_hi) || (lin[m] >= wi.ntt_lo && lin[m] <= wi.ntt_hi);
-                nt = maybe && latency(sc, v, lin[m], lp[m], B + 1).nt;
-            } else {
-                const Latency Lt = latency(sc, v, lin[m], lp[m], B + 1);
-                dec_ok = Lt.dec_ok;
-                ttft_ok = Lt.ttft_ok;
-                nt = Lt.nt;
-            }
-            const uint64_t bf = __ballot(act[m] && peak[m] <= wi.M && dec_ok && ttft_ok);
-            const uint64_t bn = __ballot(act[m] && nt);
+            const Latency Lt = latency(sc, v, lin[m], lp[m], B + 1);
+            const uint64_t bf = __ballot(act[m] && peak[m] <= wi.M && Lt.dec_ok && Lt.ttft_ok);
+            const uint64_t bn = __ballot(act[m] && Lt.nt);
             bits = (lane == m) ? bf : bits;
             bits = (lane == m + 4) ? bn : bits;
-            if (EX) {
-                const uint64_t key = ex_key(peak[m] - wi.M, w);
-                const uint64_t hi = key > k1[m] ? key : k1[m];
-                k1[m] = key < k1[m] ? key : k1[m];
-                k2[m] = hi < k2[m] ? hi : k2[m];
-            }
+            if (EX) keep_two<STAGED>(peak[m] - wi.M, w, e1[m], w1[m], e2[m], w2[m]);
         }
     }
     if (lane < 8) bdst[w] = bits;
+}
+
+// Near-tie words of one worker (lanes 4..7 store the wave's words for its
+// queries m = lane - 4), with the integer thresholds (MODE >= 1): from the
+// worker's exact near-tie sets (MODE 2) or by the fp64 margin tests of the
+// queries inside a tie band (MODE 1).  Independent of the KV peak, so it runs
+// after the staged loop, apart from its registers.
+template <int MODE>
+__device__ __forceinline__ void near_tie_words(const State& st, const Scen& sc, const WInfo& wi, int w,
+                                               const int32_t (&lin)[EVAL_QPT], const int32_t (&lp)[EVAL_QPT],
+                                               const bool (&act)[EVAL_QPT], uint64_t* bdst)
+{
+    const int lane = lane_id();
+    const View v = winfo_view(st, wi);
+    const int B = wi.n - wi.head;
+    uint64_t bits = 0;
+#pragma unroll
+    for (int m = 0; m < EVAL_QPT; ++m) {
+        const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
+        bool nt;
+        if (MODE == 2) {
+            const uint64_t dd = (uint64_t)(qD - wi.ntd_lo);
+            const uint32_t dl = (uint32_t)(lin[m] - wi.ntt_lo);
+            nt = (dd < 64 && ((wi.ntd_mask >> dd) & 1)) || (dl < 64 && ((wi.ntt_mask >> dl) & 1));
+        } else {
+            const bool maybe = (qD >= wi.ntd_lo && qD <= wi.ntd_hi) || (lin[m] >= wi.ntt_lo && lin[m] <= wi.ntt_hi);
+            nt = maybe && latency(sc, v, lin[m], lp[m], B + 1).nt;
+        }
+        const uint64_t bn = __ballot(act[m] && nt);
+        bits = (lane == m + 4) ? bn : bits;
+    }
+    if (lane >= 4 && lane < 8) bdst[w] = bits;
 }
 
 // Pair evaluation: block = (scenario, worker block, chunk of EVAL_Q queries).
@@ -762,10 +803,10 @@ __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, con
 // read, l = LB[l_pred - 1], and the summaries of slot l give the KV peak with the
 // query added.  The next worker's data travels in registers while the current
 // one is evaluated.  Workers with B >= STAGE_MAX, or chunks with an l_pred above
-// LB_MAX, take the binary search over global memory instead.  MONO: the
-// latency checks use the worker's integer thresholds; EX: the two smallest KV
-// excesses are tracked (diagnostics).
-template <bool MONO, bool EX>
+// LB_MAX, take the binary search over global memory instead.  MODE: how the
+// latency checks are taken (launch_eval); EX: the two smallest KV excesses are
+// tracked (diagnostics).
+template <int MODE, bool EX>
 __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4))) void k_eval(State st)
 {
     constexpr int NT = EVAL_THREADS;
@@ -803,7 +844,7 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
 
     int32_t lin[QPT], lp[QPT];
     bool act[QPT];
-    uint64_t k1[QPT], k2[QPT];
+    int32_t e1[QPT], w1[QPT], e2[QPT], w2[QPT];  // two smallest KV excesses per query
     int64_t lpmax = 0, qdmin = INT64_MAX, qdmax = INT64_MIN, lnmin = INT64_MAX, lnmax = INT64_MIN;
 #pragma unroll
     for (int m = 0; m < QPT; ++m) {
@@ -811,7 +852,8 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
         act[m] = qi < end;
         lin[m] = act[m] ? st.q_lin[qi] : 1;
         lp[m] = act[m] ? st.q_lpred[qi] : 1;
-        k1[m] = k2[m] = ~0ull;
+        e1[m] = e2[m] = INT32_MAX;
+        w1[m] = w2[m] = -1;
         const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
         if (act[m]) {
             lpmax = lp[m] > lpmax ? lp[m] : lpmax;
@@ -850,6 +892,11 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
         x.lthr = st.lthr[gw];
         x.ntt_lo = st.ntt_lo[gw];
         x.ntt_hi = st.ntt_hi[gw];
+        x.ntd_mask = st.ntd_mask[gw];
+        x.ntt_mask = st.ntt_mask[gw];
+        // a near-tie margin needs some query of the chunk inside a tie band
+        x.nt_any = MODE == 0 || (qr.qdmax >= x.ntd_lo && qr.qdmin <= x.ntd_hi) ||
+                   (qr.lnmax >= x.ntt_lo && qr.lnmin <= x.ntt_hi);
         Wi[tid] = x;
     }
     __syncthreads();
@@ -871,21 +918,26 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
         __syncthreads();
         const int nxt = next_staged(Wi, nw, use_lb, cur + 1);
         if (nxt < nw) pf = prefetch_worker(st, Wi[nxt], sc.wbase + wbeg + nxt, tid);
-        const WInfo wi = Wi[cur];
-        eval_worker<MONO, EX, true>(st, sc, wi, wbeg + cur, tau, lin, lp, act, k1, k2, LBs, Ss, qr, bdst);
+        eval_worker<MODE, EX, true>(st, sc, Wi[cur], wbeg + cur, tau, lin, lp, act, e1, w1, e2, w2, LBs, Ss, bdst);
         cur = nxt;
     }
     // workers too large to stage: binary search over global memory
     for (int j0 = 0; j0 < nw; ++j0) {
         const WInfo wi = Wi[j0];
         if (use_lb && wi.n - wi.head < STAGE_MAX) continue;
-        eval_worker<MONO, EX, false>(st, sc, wi, wbeg + j0, tau, lin, lp, act, k1, k2, LBs, Ss, qr, bdst);
+        eval_worker<MODE, EX, false>(st, sc, wi, wbeg + j0, tau, lin, lp, act, e1, w1, e2, w2, LBs, Ss, bdst);
+    }
+    if (MODE >= 1) {
+        for (int j0 = 0; j0 < nw; ++j0)
+            if (Wi[j0].nt_any) near_tie_words<MODE>(st, sc, Wi[j0], wbeg + j0, lin, lp, act, bdst);
     }
     if (!EX) return;
 #pragma unroll
     for (int m = 0; m < QPT; ++m) {
         const int qi = q0 + m * NT + tid;
-        if (act[m]) st.part[sc.part_off + (int64_t)wb * sc.pstride + (qi - start)] = make_ulonglong2(k1[m], k2[m]);
+        const uint64_t k1 = w1[m] < 0 ? ~0ull : ex_key(e1[m], w1[m]);
+        const uint64_t k2 = w2[m] < 0 ? ~0ull : ex_key(e2[m], w2[m]);
+        if (act[m]) st.part[sc.part_off + (int64_t)wb * sc.pstride + (qi - start)] = make_ulonglong2(k1, k2);
     }
 }
 
@@ -1988,13 +2040,20 @@ hipError_t launch_build(const State& st, hipStream_t stream, int mode)
     return hipGetLastError();
 }
 
-hipError_t launch_eval(const State& st, int32_t blocks, bool mono, hipStream_t stream)
+hipError_t launch_eval(const State& st, int32_t blocks, int mode, hipStream_t stream)
 {
     const bool ex = st.out_diag != nullptr;
-    if (mono && ex) hipLaunchKernelGGL((k_eval<true, true>), dim3(blocks), dim3(EVAL_THREADS), 0, stream, st);
-    else if (mono) hipLaunchKernelGGL((k_eval<true, false>), dim3(blocks), dim3(EVAL_THREADS), 0, stream, st);
-    else if (ex) hipLaunchKernelGGL((k_eval<false, true>), dim3(blocks), dim3(EVAL_THREADS), 0, stream, st);
-    else hipLaunchKernelGGL((k_eval<false, false>), dim3(blocks), dim3(EVAL_THREADS), 0, stream, st);
+    const dim3 g(blocks), b(EVAL_THREADS);
+    if (mode == 2) {
+        if (ex) hipLaunchKernelGGL((k_eval<2, true>), g, b, 0, stream, st);
+        else hipLaunchKernelGGL((k_eval<2, false>), g, b, 0, stream, st);
+    } else if (mode == 1) {
+        if (ex) hipLaunchKernelGGL((k_eval<1, true>), g, b, 0, stream, st);
+        else hipLaunchKernelGGL((k_eval<1, false>), g, b, 0, stream, st);
+    } else {
+        if (ex) hipLaunchKernelGGL((k_eval<0, true>), g, b, 0, stream, st);
+        else hipLaunchKernelGGL((k_eval<0, false>), g, b, 0, stream, st);
+    }
     return hipGetLastError();
 }
 

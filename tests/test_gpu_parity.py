@@ -247,6 +247,25 @@ def test_near_tie_margins_are_flagged(aladdin):
     assert d["near_tie"][0] == 1
 
 
+@pytest.mark.parametrize("seed", [0, 1])
+def test_near_tie_sets_with_integer_forms(aladdin, seed):
+    # k1 > 0 and narrow bands: the evaluation takes near-tie margins from each
+    # worker's exact integer near-tie sets.  The TTFT margin is zero where
+    # S1 + l_in = 10 and the decode margin where sum(c) + l_in = 10, so the tie
+    # sits at a different l_in on each worker as the workers fill.
+    m = wl.Model(c1=0.0, k1=0.25, k1q=0.0, c3=0.0, c2=0.0, k2=0.5, ttft_slo=2.5, decode_slo=5.0,
+                 gamma_num=0, gamma_log2den=1)
+    rng = np.random.default_rng(seed)
+    res = [[(int(rng.integers(1, 4)), int(rng.integers(1, 4)), 0)] for _ in range(6)] + [[], []]
+    q = [(int(a), int(b)) for a, b in zip(rng.integers(1, 12, 300), rng.integers(1, 6, 300))]
+    t = _trace(8, 10 ** 6, res, q, model=m)
+    want = ref.place_trace(t)
+    assert want.near_tie.sum() > 0
+    for tile in (64, 4096):
+        w, d, s = gpu_place(aladdin, t, tile=tile, slots=64)
+        compare(w, d, s, want, "integer near-tie sets, tile %d" % tile)
+
+
 def test_slots_exhausted_is_reported(aladdin):
     t = _trace(1, 10 ** 6, [[]], [(3, 2)] * 50)
     ev = aladdin.Evaluator(0, tile=64)
