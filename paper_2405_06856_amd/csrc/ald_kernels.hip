@@ -216,6 +216,10 @@ __device__ __forceinline__ Latency latency(const Scen& sc, const View& v, int32_
     return o;
 }
 
+// Lanes (of the active ones) where p holds.  Takes the predicate as a bool, so
+// that a compare result feeds the mask directly.
+__device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+
 // Largest x in [lo, hi] for which `pred` holds, where pred holds on a prefix of
 // [lo, hi]; lo - 1 if it holds nowhere.  The 64 lanes of the wave test 64
 // evenly spaced points per step, so a range of 2^36 takes six steps.  All
@@ -228,7 +232,7 @@ __device__ int64_t wave_last_true(int64_t lo, int64_t hi, F pred)
         const int64_t step = (b - a + 63) >> 6;
         const int64_t x = a + step * (lane_id() + 1);
         const bool t = x <= b && pred(x);
-        const int cnt = __popcll(__ballot(t));
+        const int cnt = __popcll(ballot(t));
         a += step * cnt;
         const int64_t nb = a + step - 1;
         b = nb < b ? nb : b;
@@ -435,7 +439,7 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
         const int64_t xl = wave_last_true(0, XMAX, [&](int64_t v) { return dec_lhs(sc, v) < lo; }) + 1;
         const int64_t xh = wave_last_true(0, XMAX, [&](int64_t v) { return dec_lhs(sc, v) <= hi; });
         const int64_t width = xh - xl + 1;
-        const uint64_t mask = __ballot(lane_id() < width && near_tie(dec_lhs(sc, xl + lane_id()), rhs));
+        const uint64_t mask = ballot(lane_id() < width && near_tie(dec_lhs(sc, xl + lane_id()), rhs));
         if (l0) {
             st.ntd_lo[gw] = xl - DS;
             st.ntd_hi[gw] = xh - DS;
@@ -456,7 +460,7 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
             const int64_t ll = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) < lo; }) + 1;
             const int64_t lh = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) <= hi; });
             const int64_t width = lh - ll + 1;
-            const uint64_t mask = __ballot(lane_id() < width && near_tie(tt(ll + lane_id()), sc.ttft));
+            const uint64_t mask = ballot(lane_id() < width && near_tie(tt(ll + lane_id()), sc.ttft));
             if (l0) {
                 st.ntt_lo[gw] = (int32_t)ll;
                 st.ntt_hi[gw] = (int32_t)lh;
@@ -638,6 +642,35 @@ __device__ __forceinline__ void ex_unpack(uint64_t k, int32_t& ex, int32_t& w)
     w = k == ~0ull ? -1 : (int32_t)~(uint32_t)k;
 }
 
+// Word `acc` with lane J's value replaced by the wave-uniform `v`
+// (v_writelane_b32 on each half, the lane an inline constant).  The s_nop
+// gives an SGPR that a VALU instruction wrote just before (a compare's lane
+// mask) its wait states before v_writelane reads it: the compiler does not
+// look inside the asm for that hazard, and without the wait the lanes took
+// stale words.
+template <int J>
+__device__ __forceinline__ uint64_t put_lane_c(uint64_t acc, uint64_t v)
+{
+    uint32_t lo = (uint32_t)acc, hi = (uint32_t)(acc >> 32);
+    asm("s_nop 4\n\tv_writelane_b32 %0, %2, %4\n\tv_writelane_b32 %1, %3, %4"
+        : "+v"(lo), "+v"(hi)
+        : "s"((uint32_t)v), "s"((uint32_t)(v >> 32)), "n"(J));
+    return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t put_lane(uint64_t acc, uint64_t v, int j)
+{
+    switch (j) {
+    case 0: return put_lane_c<0>(acc, v);
+    case 1: return put_lane_c<1>(acc, v);
+    case 2: return put_lane_c<2>(acc, v);
+    case 3: return put_lane_c<3>(acc, v);
+    case 4: return put_lane_c<4>(acc, v);
+    case 5: return put_lane_c<5>(acc, v);
+    case 6: return put_lane_c<6>(acc, v);
+    default: return put_lane_c<7>(acc, v);
+    }
+}
+
 // Keep a query's two smallest KV excesses as (excess, worker) pairs, smaller
 // excess first, then the higher index; e1 = INT32_MAX, w1 = -1 when empty
 // (every excess is below INT32_MAX).  IN_ORDER: w is above every index seen so
@@ -700,7 +733,8 @@ struct QRange {
 template <int MODE, bool EX, bool STAGED>
 __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, const WInfo& wi, int w, int32_t tau,
                                             const int32_t (&lin)[EVAL_QPT], const int32_t (&lp)[EVAL_QPT],
-                                            const bool (&act)[EVAL_QPT], int32_t (&e1)[EVAL_QPT],
+                                            const bool (&act)[EVAL_QPT], const uint64_t (&am)[EVAL_QPT],
+                                            int32_t (&e1)[EVAL_QPT],
                                             int32_t (&w1)[EVAL_QPT], int32_t (&e2)[EVAL_QPT],
                                             int32_t (&w2)[EVAL_QPT], const uint16_t* LBs, const int4* Ss,
                                             uint64_t* bdst)
@@ -743,9 +777,9 @@ __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, con
 #pragma unroll
         for (int m = 0; m < EVAL_QPT; ++m) {
             const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
-            const bool ok = act[m] & (peak[m] <= M) & (qD <= dq_max) & (lin[m] <= lthr);
-            const uint64_t bf = __ballot(ok);
-            bits = (lane == m) ? bf : bits;
+            // one ballot per compare: each compare's lane mask is its ballot
+            const uint64_t bf = am[m] & ballot(peak[m] <= M) & ballot(qD <= dq_max) & ballot(lin[m] <= lthr);
+            bits = put_lane(bits, bf, m);
             if (EX) keep_two<STAGED>(peak[m] - M, w, e1[m], w1[m], e2[m], w2[m]);
         }
         // near-tie words (lanes 4..7) stay zero here: near_tie_words fills
@@ -754,10 +788,10 @@ __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, con
 #pragma unroll
         for (int m = 0; m < EVAL_QPT; ++m) {
             const Latency Lt = latency(sc, v, lin[m], lp[m], B + 1);
-            const uint64_t bf = __ballot(act[m] && peak[m] <= wi.M && Lt.dec_ok && Lt.ttft_ok);
-            const uint64_t bn = __ballot(act[m] && Lt.nt);
-            bits = (lane == m) ? bf : bits;
-            bits = (lane == m + 4) ? bn : bits;
+            const uint64_t bf = ballot(act[m] && peak[m] <= wi.M && Lt.dec_ok && Lt.ttft_ok);
+            const uint64_t bn = ballot(act[m] && Lt.nt);
+            bits = put_lane(bits, bf, m);
+            bits = put_lane(bits, bn, m + 4);
             if (EX) keep_two<STAGED>(peak[m] - wi.M, w, e1[m], w1[m], e2[m], w2[m]);
         }
     }
@@ -790,8 +824,8 @@ __device__ __forceinline__ void near_tie_words(const State& st, const Scen& sc, 
             const bool maybe = (qD >= wi.ntd_lo && qD <= wi.ntd_hi) || (lin[m] >= wi.ntt_lo && lin[m] <= wi.ntt_hi);
             nt = maybe && latency(sc, v, lin[m], lp[m], B + 1).nt;
         }
-        const uint64_t bn = __ballot(act[m] && nt);
-        bits = (lane == m + 4) ? bn : bits;
+        const uint64_t bn = ballot(act[m] && nt);
+        bits = put_lane(bits, bn, m + 4);
     }
     if (lane >= 4 && lane < 8) bdst[w] = bits;
 }
@@ -829,7 +863,7 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
             const int32_t a = st.q_lin[i], p = st.q_lpred[i];
             bad = bad || !(a >= 1 && p >= 1 && a <= (1 << 24) && p <= (1 << 24));
         }
-        if (__ballot(bad) != 0 && lane_id() == 0) atomicOr(st.qbad, 1);
+        if (ballot(bad) != 0 && lane_id() == 0) atomicOr(st.qbad, 1);
     }
     if (cp->err || start >= Q) return;
     const int32_t end = tile_end(start, Q, cp->T, cp->H, cp->since_hb);
@@ -863,6 +897,9 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
             lnmax = lin[m] > lnmax ? lin[m] : lnmax;
         }
     }
+    uint64_t am[QPT];  // the wave's lanes holding a query m
+#pragma unroll
+    for (int m = 0; m < QPT; ++m) am[m] = ballot(act[m]);
     lpmax = block_all<NT>(lpmax, 0, OpMax(), red);
     QRange qr;
     qr.qdmin = block_all<NT>(qdmin, INT64_MAX, OpMin(), red);
@@ -918,14 +955,14 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
         __syncthreads();
         const int nxt = next_staged(Wi, nw, use_lb, cur + 1);
         if (nxt < nw) pf = prefetch_worker(st, Wi[nxt], sc.wbase + wbeg + nxt, tid);
-        eval_worker<MODE, EX, true>(st, sc, Wi[cur], wbeg + cur, tau, lin, lp, act, e1, w1, e2, w2, LBs, Ss, bdst);
+        eval_worker<MODE, EX, true>(st, sc, Wi[cur], wbeg + cur, tau, lin, lp, act, am, e1, w1, e2, w2, LBs, Ss, bdst);
         cur = nxt;
     }
     // workers too large to stage: binary search over global memory
     for (int j0 = 0; j0 < nw; ++j0) {
         const WInfo wi = Wi[j0];
         if (use_lb && wi.n - wi.head < STAGE_MAX) continue;
-        eval_worker<MODE, EX, false>(st, sc, wi, wbeg + j0, tau, lin, lp, act, e1, w1, e2, w2, LBs, Ss, bdst);
+        eval_worker<MODE, EX, false>(st, sc, wi, wbeg + j0, tau, lin, lp, act, am, e1, w1, e2, w2, LBs, Ss, bdst);
     }
     if (MODE >= 1) {
         for (int j0 = 0; j0 < nw; ++j0)
@@ -1000,7 +1037,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
         for (int u = 0; u < UB; ++u) {
             const int wb0 = g0 + u * 64;
             const uint64_t fl = fls[u], nl = nls[u];
-            uint64_t mask = __ballot((fl | nl) != 0);
+            uint64_t mask = ballot((fl | nl) != 0);
             if (!mask) continue;
             const int wl = wb0 + lane;
             const uint64_t kl = wl < whi ? st.key[sc.wbase + wl] : 0;
@@ -1133,7 +1170,7 @@ constexpr int DBITS_W = 2048;  // dirty bitmap words in LDS: scenarios of up to 
 // `valid`, or -1.  A scalar walk over the (few) candidate lanes.
 __device__ __forceinline__ int wave_best_lane(uint64_t key, int32_t w, bool valid)
 {
-    uint64_t m = __ballot(valid);
+    uint64_t m = ballot(valid);
     int best = -1;
     uint64_t bk = 0;
     int32_t bw = -1;
@@ -1299,7 +1336,7 @@ __device__ __forceinline__ bool dirty_w(const CommitLDS& L, int W, int nd, int w
 // Lane holding dirty worker w (wave-uniform w; -1 if w is not dirty).
 __device__ __forceinline__ int dirty_lane(const DAgg& a, int w)
 {
-    const uint64_t m = __ballot(a.w == w && w >= 0);
+    const uint64_t m = ballot(a.w == w && w >= 0);
     return m ? __ffsll((unsigned long long)m) - 1 : -1;
 }
 
@@ -1310,7 +1347,7 @@ __device__ int next_empty_worker(const State& st, const Scen& sc, const CommitLD
     for (int base = from; base < sc.W; base += 64) {
         const int w = base + lane_id();
         const bool emp = w < sc.W && st.key[sc.wbase + w] == 0 && !dirty_w(L, sc.W, nd, w);
-        const uint64_t m = __ballot(emp);
+        const uint64_t m = ballot(emp);
         if (m) return base + __ffsll((unsigned long long)m) - 1;
     }
     return -1;
@@ -1424,7 +1461,7 @@ __device__ __forceinline__ void lds_sorted_insert(CommitLDS& L, int B, int32_t x
     const int lane = lane_id();
     int u = 0;
     for (int k0 = 0; k0 < B; k0 += COMMIT_THREADS)
-        u += __popcll(__ballot(k0 + lane < B && L.he[k0 + lane] <= x));
+        u += __popcll(ballot(k0 + lane < B && L.he[k0 + lane] <= x));
     // shift [u, B) up by one, highest block first (each pass reads before it writes)
     for (int top = B; top > u; top -= COMMIT_THREADS) {
         const int k = top - COMMIT_THREADS + lane;
@@ -1541,7 +1578,7 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
         for (;;) {
             const int bl = wave_best_lane(a.key, a.w, cand);
             if (bl < 0) break;
-            if ((__ballot(sure) >> bl) & 1) {
+            if ((ballot(sure) >> bl) & 1) {
                 r.w = rdlane(a.w, bl);
                 r.lane = bl;
                 return r;
@@ -1596,7 +1633,7 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
         }
     }
     r.w = have ? bw : -1;
-    r.d.n_feasible = q.nfeas - __popcll(__ballot(valid && fs)) + __popcll(__ballot(fdirty));
+    r.d.n_feasible = q.nfeas - __popcll(ballot(valid && fs)) + __popcll(ballot(fdirty));
     // smallest KV excess
     int64_t exmin = q.ex1;
     const int j1 = dirty_lane(a, q.w1);
@@ -1612,7 +1649,7 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
     }
     r.d.kv_excess_min = exmin;
     // near tie among workers ranked at or above the choice (all when rejected)
-    const int clean_nt = q.ntcnt - __popcll(__ballot(valid && ns));
+    const int clean_nt = q.ntcnt - __popcll(ballot(valid && ns));
     bool nt = false;
     if (clean_nt > 0) {
         if (q.ntw >= 0 && dirty_lane(a, q.ntw) < 0) {
@@ -1625,7 +1662,7 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
         }
     }
     const bool dnt = valid && Lt.nt && (r.w < 0 || !ranks_before(bk, bw, a.key, a.w));
-    nt = nt | (__ballot(dnt) != 0);
+    nt = nt | (ballot(dnt) != 0);
     r.d.near_tie = nt ? 1 : 0;
     // the chosen worker's figures
     if (r.w >= 0) {
@@ -1778,7 +1815,7 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
             q.nfeas = 0;
         }
         if (lane < nd) wb = load_win_bits(st, sc, a.w, start, w0, end);
-        const uint64_t potm = __ballot(act && q.nfeas > 0);
+        const uint64_t potm = ballot(act && q.nfeas > 0);
         int cur = 0;
         while (cur < NT && w0 + cur < end) {
             const uint64_t pm = potm & (~0ull << cur);
@@ -1788,14 +1825,14 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
             int ab = 0;
             const bool mine = act && lane >= cur && lane < p;
             if (want_diag && mine) dr = reject_diag(st, sc, q, i, start, w0, lin, lp, tau, hb, L, nd, hot, wb, &ab);
-            const uint64_t am = __ballot(mine && ab);
+            const uint64_t am = ballot(mine && ab);
             const int abl = am ? __ffsll((unsigned long long)am) - 1 : NT;
             const int lim = min(p, abl);
             if (act && lane >= cur && lane < lim) {
                 if (st.out_worker) st.out_worker[sc.out_off + i] = -1;
                 if (want_diag) st.out_diag[i] = dr;
             }
-            const uint64_t rm = __ballot(act && lane >= cur && lane < lim);
+            const uint64_t rm = ballot(act && lane >= cur && lane < lim);
             nrej += __popcll(rm);
             if (rm && firstrej == INT32_MAX) firstrej = w0 + __ffsll((unsigned long long)rm) - 1;
             if (abl < p) {
