@@ -1489,14 +1489,13 @@ __device__ __forceinline__ void lds_sorted_insert(CommitLDS& L, int B, int32_t x
 // diagnostics, an unsorted tail [Bs, Bs + m) of requests committed since it
 // became hot, in commit order.  Sort the tail into the prefix (in commit order,
 // so equal end points keep the order a sorted insert would give them).
-__device__ __noinline__ void lds_merge_tail(CommitLDS& L, int& Bs, int& m)
+__device__ __noinline__ int lds_merge_tail(CommitLDS& L, int Bs, int m)
 {
     for (int t = 0; t < m; ++t) {
         const int32_t x = L.he[Bs + t], y = L.hs[Bs + t];  // read before the insert may move it
         lds_sorted_insert(L, Bs + t, x, y);
     }
-    Bs += m;
-    m = 0;
+    return Bs + m;
 }
 
 // KV peak with the query for dirty lane bl (whole wave): the hot worker's
@@ -1506,7 +1505,10 @@ __device__ __forceinline__ int64_t dirty_kv_peak(const State& st, CommitLDS& L, 
 {
     const int32_t cB = rdlane(a.B, bl);
     if (bl == hot) {
-        if (hotm > 0) lds_merge_tail(L, hotBs, hotm);
+        if (hotm > 0) {
+            hotBs = lds_merge_tail(L, hotBs, hotm);
+            hotm = 0;
+        }
         return wave_kv_peak<false>(L.he, L.hs, cB, sq, eq, p0);
     }
     const int64_t base = rdlane64s(a.base, bl) + rdlane(a.head, bl);
@@ -1737,6 +1739,7 @@ __device__ void writeback_hot(const State& st, CommitLDS& L, DAgg& a, int hot, i
     }
 }
 
+template <bool DIAG>
 __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
 {
     constexpr int NT = COMMIT_THREADS;
@@ -1760,7 +1763,7 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
         return;
     }
     const int32_t start = ti.start, end = ti.end;
-    const int32_t fpc = min(ti.first_pc[ti.parity], end);
+    const int32_t fpc = min(st.tinfo[s].first_pc[ti.parity & 1], end);  // (no local copy indexed at run time)
 
     // ---- the sequential wave
     const Ctl c = *cp;
@@ -1774,7 +1777,7 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
         for (int k = lane; k < (sc.W + 31) / 32; k += NT) L.dbits[k] = 0u;
     if (lane == 0) cp->rebuild = 0;
     wave_sync();
-    const bool want_diag = st.out_diag != nullptr;
+    constexpr bool want_diag = DIAG;  // st.out_diag != nullptr
     int nd = 0;    // dirty workers (wave-uniform); lane j < nd holds the j-th in `a`
     DAgg a;
     a.w = -1;
@@ -2102,7 +2105,10 @@ hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream)
 
 hipError_t launch_commit(const State& st, int32_t blocks, hipStream_t stream)
 {
-    hipLaunchKernelGGL(k_commit, dim3(blocks), dim3(COMMIT_THREADS), 0, stream, st);
+    if (st.out_diag != nullptr)
+        hipLaunchKernelGGL(k_commit<true>, dim3(blocks), dim3(COMMIT_THREADS), 0, stream, st);
+    else
+        hipLaunchKernelGGL(k_commit<false>, dim3(blocks), dim3(COMMIT_THREADS), 0, stream, st);
     return hipGetLastError();
 }
 
