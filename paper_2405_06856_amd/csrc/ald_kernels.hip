@@ -304,11 +304,20 @@ __device__ __forceinline__ int32_t wave_incl_scan(int32_t x, int32_t ident, Op o
 struct Add32 {
     __device__ int32_t operator()(int32_t a, int32_t b) const { return a + b; }
 };
+struct Or32 {
+    __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a | b; }
+};
 struct Max32 {
     __device__ int32_t operator()(int32_t a, int32_t b) const { return a > b ? a : b; }
 };
 __device__ __forceinline__ int32_t wave_sum32(int32_t v) { return rdlane(wave_incl_scan(v, 0, Add32()), 63); }
 __device__ __forceinline__ int32_t wave_max32(int32_t v) { return rdlane(wave_incl_scan(v, INT32_MIN, Max32()), 63); }
+__device__ __forceinline__ uint64_t wave_or64(uint64_t v)
+{
+    const uint32_t lo = (uint32_t)rdlane((int32_t)wave_incl_scan((int32_t)(uint32_t)v, 0, Or32()), 63);
+    const uint32_t hi = (uint32_t)rdlane((int32_t)wave_incl_scan((int32_t)(uint32_t)(v >> 32), 0, Or32()), 63);
+    return ((uint64_t)hi << 32) | lo;
+}
 __device__ __forceinline__ int64_t wave_sum64(int64_t v)
 {
 #pragma unroll
@@ -964,7 +973,7 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
         if (use_lb && wi.n - wi.head < STAGE_MAX) continue;
         eval_worker<MODE, EX, false>(st, sc, wi, wbeg + j0, tau, lin, lp, act, am, e1, w1, e2, w2, LBs, Ss, bdst);
     }
-    if (MODE >= 1) {
+    if (MODE >= 1 && EX) {  // near-tie margins feed only the diagnostics
         for (int j0 = 0; j0 < nw; ++j0)
             if (Wi[j0].nt_any) near_tie_words<MODE>(st, sc, Wi[j0], wbeg + j0, lin, lp, act, bdst);
     }
@@ -1023,6 +1032,12 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     const int span = ((sc.W + G * 64 - 1) / (G * 64)) * 64;  // workers per wave, whole batches
     const int wlo = live ? min(sc.W, slice * span) : 0;
     const int whi = live ? min(sc.W, wlo + span) : 0;
+    // Without diagnostics only the choice matters: near-tie words are not
+    // read, and the interchangeable empty workers of a uniform-capacity
+    // scenario are taken 64 at a time (an OR of their words); nfeas then only
+    // says whether some worker is feasible.
+    const bool diag = st.out_diag != nullptr;
+    const bool bulk_empty = !diag && sc.uniform_M;
     constexpr int UB = 8;  // 64-worker batches whose words are loaded together
     for (int g0 = wlo; g0 < whi; g0 += 64 * UB) {
         uint64_t fls[UB], nls[UB];
@@ -1031,7 +1046,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
             const int wl = g0 + u * 64 + lane;
             const bool in = wl < whi;
             fls[u] = in ? st.bits_feas[row + wl] : 0;
-            nls[u] = in ? st.bits_nt[row + wl] : 0;
+            nls[u] = (in && diag) ? st.bits_nt[row + wl] : 0;
         }
 #pragma unroll
         for (int u = 0; u < UB; ++u) {
@@ -1041,6 +1056,14 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
             if (!mask) continue;
             const int wl = wb0 + lane;
             const uint64_t kl = wl < whi ? st.key[sc.wbase + wl] : 0;
+            if (bulk_empty) {
+                const uint64_t em = mask & ballot(kl == 0);
+                if (em) {
+                    const uint64_t any = wave_or64(((em >> lane) & 1) ? fl : 0);
+                    efeas = efeas | (((any >> lane) & 1) != 0);
+                    mask &= ~em;
+                }
+            }
             while (mask) {
                 const int j = __ffsll((unsigned long long)mask) - 1;
                 mask &= mask - 1;
@@ -1127,14 +1150,14 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     q.ntkey = ntkey;
     q.ntw = ntw;
     q.ntcnt = ntcnt;
-    q.nfeas = nfeas;
+    q.nfeas = bulk_empty ? ncand + (efeas ? 1 : 0) : nfeas;  // bulk: > 0 exactly when some worker is feasible
     q.ncand = ncand;
     q.efeas = efeas ? 1 : 0;
     q.ex1 = ex1; q.w1 = w1;
     q.ex2 = ex2; q.w2 = w2;
     q.pad = 0;
     st.qsum[sc.qsum_off + (qi - start)] = q;
-    if (nfeas > 0) {
+    if (q.nfeas > 0) {
         atomicMin(&st.tinfo[s].first_pc[parity], qi);
     } else if (st.qbad == nullptr || *st.qbad == 0) {
         // no feasible worker at tile start: rejected whatever the tile commits
