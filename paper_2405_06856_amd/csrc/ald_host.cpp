@@ -616,7 +616,7 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
     int32_t T = std::min(h->tile, Q);
     if (H > 0) T = std::min(T, H);
     if (T != a->T) {
-        rc = layout_scratch(h, a, T, 2048);
+        rc = layout_scratch(h, a, T, 2048 * 256 / EVAL_THREADS);  // about 8192 evaluation waves
         if (rc != ALD_OK) return rc;
     }
     Ctl c{};

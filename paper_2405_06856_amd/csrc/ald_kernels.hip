@@ -14,6 +14,8 @@
 //             extra blocks finalize the rejected prefix in parallel.
 #include "ald_internal.h"
 
+#include <type_traits>
+
 namespace ald {
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
@@ -652,7 +654,7 @@ __device__ __forceinline__ void ex_unpack(uint64_t k, int32_t& ex, int32_t& w)
 }
 
 // Word `acc` with lane J's value replaced by the wave-uniform `v`
-// (v_writelane_b32 on each half, the lane an inline constant).  The s_nop
+// (v_writelane_b32 on each half, the lane an inline constant, J < 16).  The s_nop
 // gives an SGPR that a VALU instruction wrote just before (a compare's lane
 // mask) its wait states before v_writelane reads it: the compiler does not
 // look inside the asm for that hazard, and without the wait the lanes took
@@ -676,7 +678,15 @@ __device__ __forceinline__ uint64_t put_lane(uint64_t acc, uint64_t v, int j)
     case 4: return put_lane_c<4>(acc, v);
     case 5: return put_lane_c<5>(acc, v);
     case 6: return put_lane_c<6>(acc, v);
-    default: return put_lane_c<7>(acc, v);
+    case 7: return put_lane_c<7>(acc, v);
+    case 8: return put_lane_c<8>(acc, v);
+    case 9: return put_lane_c<9>(acc, v);
+    case 10: return put_lane_c<10>(acc, v);
+    case 11: return put_lane_c<11>(acc, v);
+    case 12: return put_lane_c<12>(acc, v);
+    case 13: return put_lane_c<13>(acc, v);
+    case 14: return put_lane_c<14>(acc, v);
+    default: return put_lane_c<15>(acc, v);
     }
 }
 
@@ -696,11 +706,14 @@ __device__ __forceinline__ void keep_two(int32_t ex, int32_t w, int32_t& e1, int
 }
 
 // One thread's share of a staged worker: slots tid + j * EVAL_THREADS of the
-// summaries (clamped to slot B, which exists) and 8 entries of its table.
+// summaries (clamped to slot B, which exists) and LBV entries of its table.
 constexpr int PF_N = (STAGE_MAX + EVAL_THREADS - 1) / EVAL_THREADS;
+constexpr int LBV = LB_MAX / EVAL_THREADS;  // table entries per thread (8 or 4)
+static_assert(LBV == 8 || LBV == 4, "one 16- or 8-byte table load per thread");
+using LBVec = std::conditional_t<LBV == 8, uint4, uint2>;
 struct Prefetch {
     int4 p[PF_N];
-    uint4 lb;  // 8 entries of the worker's breakpoint table (zeros for an empty worker)
+    LBVec lb;  // LBV entries of the worker's breakpoint table (zeros for an empty worker)
 };
 
 __device__ __forceinline__ Prefetch prefetch_worker(const State& st, const WInfo& x, int gw, int tid)
@@ -709,17 +722,19 @@ __device__ __forceinline__ Prefetch prefetch_worker(const State& st, const WInfo
     const int B = x.n - x.head;
 #pragma unroll
     for (int j = 0; j < PF_N; ++j) f.p[j] = st.pms[x.base + min(tid + j * EVAL_THREADS, B)];
-    f.lb = make_uint4(0, 0, 0, 0);
-    if (B > 0) f.lb = reinterpret_cast<const uint4*>(st.lbt + (int64_t)gw * LB_MAX)[tid];
+    f.lb = LBVec{};
+    if (B > 0) f.lb = reinterpret_cast<const LBVec*>(st.lbt + (int64_t)gw * LB_MAX)[tid];
     return f;
 }
 
-// Write one thread's share of a staged worker into an LDS buffer.
-__device__ __forceinline__ void stage_put(uint16_t* LBs, int4* Ss, const Prefetch& pf, int tid)
+// Write one thread's share of a staged worker into LDS: the summaries of
+// slots 0 .. B and the table entries below L (the chunk's largest l_pred).
+__device__ __forceinline__ void stage_put(uint16_t* LBs, int4* Ss, const Prefetch& pf, int tid, int B, int L)
 {
 #pragma unroll
-    for (int j = 0; j < PF_N; ++j) Ss[tid + j * EVAL_THREADS] = pf.p[j];  // slots past B: copies, never read
-    reinterpret_cast<uint4*>(LBs)[tid] = pf.lb;
+    for (int j = 0; j < PF_N; ++j)
+        if (tid + j * EVAL_THREADS <= B) Ss[tid + j * EVAL_THREADS] = pf.p[j];
+    if (LBV * tid < L) reinterpret_cast<LBVec*>(LBs)[tid] = pf.lb;
 }
 
 // First worker at or after j (block-local index) that is evaluated from LDS.
@@ -736,7 +751,7 @@ struct QRange {
 };
 
 // Evaluate this thread's queries against one worker and store the wave's bit
-// words (lane j < 8 stores word j).  STAGED: breakpoint slot from the block's
+// words (lane j < 2 EVAL_QPT stores word j).  STAGED: breakpoint slot from the block's
 // table and summaries in LDS; else binary search over global memory.  MODE as
 // for launch_eval.
 template <int MODE, bool EX, bool STAGED>
@@ -777,7 +792,7 @@ __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, con
 #pragma unroll
         for (int m = 0; m < EVAL_QPT; ++m) peak[m] = (int32_t)kv_peak_with(v, lin[m] - tau, lp[m] + tau);
     }
-    uint64_t bits = 0;  // lane j < 8: the word it stores
+    uint64_t bits = 0;  // lane j < 2 EVAL_QPT: the word it stores
     if (MONO) {
         // feasibility from the integer thresholds (the worker's figures read
         // once; no short-circuit, so no branch per query)
@@ -791,7 +806,7 @@ __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, con
             bits = put_lane(bits, bf, m);
             if (EX) keep_two<STAGED>(peak[m] - M, w, e1[m], w1[m], e2[m], w2[m]);
         }
-        // near-tie words (lanes 4..7) stay zero here: near_tie_words fills
+        // near-tie words (lanes EVAL_QPT .. 2 EVAL_QPT - 1) stay zero here: near_tie_words fills
         // them in for the workers with nt_any
     } else {
 #pragma unroll
@@ -800,15 +815,15 @@ __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, con
             const uint64_t bf = ballot(act[m] && peak[m] <= wi.M && Lt.dec_ok && Lt.ttft_ok);
             const uint64_t bn = ballot(act[m] && Lt.nt);
             bits = put_lane(bits, bf, m);
-            bits = put_lane(bits, bn, m + 4);
+            bits = put_lane(bits, bn, m + EVAL_QPT);
             if (EX) keep_two<STAGED>(peak[m] - wi.M, w, e1[m], w1[m], e2[m], w2[m]);
         }
     }
-    if (lane < 8) bdst[w] = bits;
+    if (lane < 2 * EVAL_QPT) bdst[w] = bits;
 }
 
-// Near-tie words of one worker (lanes 4..7 store the wave's words for its
-// queries m = lane - 4), with the integer thresholds (MODE >= 1): from the
+// Near-tie words of one worker (lanes EVAL_QPT .. 2 EVAL_QPT - 1 store the
+// wave's words for its queries m = lane - EVAL_QPT), with the integer thresholds (MODE >= 1): from the
 // worker's exact near-tie sets (MODE 2) or by the fp64 margin tests of the
 // queries inside a tie band (MODE 1).  Independent of the KV peak, so it runs
 // after the staged loop, apart from its registers.
@@ -834,9 +849,9 @@ __device__ __forceinline__ void near_tie_words(const State& st, const Scen& sc, 
             nt = maybe && latency(sc, v, lin[m], lp[m], B + 1).nt;
         }
         const uint64_t bn = ballot(act[m] && nt);
-        bits = put_lane(bits, bn, m + 4);
+        bits = put_lane(bits, bn, m + EVAL_QPT);
     }
-    if (lane >= 4 && lane < 8) bdst[w] = bits;
+    if (lane >= EVAL_QPT && lane < 2 * EVAL_QPT) bdst[w] = bits;
 }
 
 // Pair evaluation: block = (scenario, worker block, chunk of EVAL_Q queries).
@@ -854,7 +869,7 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
 {
     constexpr int NT = EVAL_THREADS;
     constexpr int QPT = EVAL_QPT;
-    static_assert(LB_MAX == 8 * NT, "one 16-byte table load per thread");
+    static_assert(2 * QPT <= 16, "lane words by put_lane");
     __shared__ uint16_t LBs[LB_MAX];               // the worker's breakpoint table
     __shared__ int4 Ss[PF_N * NT];                 // pms of live slot k, k = 0..B
     __shared__ WInfo Wi[EVAL_WPB_MAX];
@@ -951,16 +966,16 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
     // current one is evaluated.  Plain loads of clamped (in-range) slots, masked
     // only where they are used, so nothing waits for them before then.
     Prefetch pf;
-    // bit word of (query group, worker) for lane j < 8 of each wave: feasibility
-    // (j < 4) or near-tie (j >= 4) of the wave's queries m = j & 3
-    const int64_t brow = sc.bits_off + (int64_t)(((q0 - start) >> 6) + wave_id() + (lane & 3) * (NT / 64)) * sc.W;
-    uint64_t* const bdst = (lane < 4 ? st.bits_feas : st.bits_nt) + brow;
+    // bit word of (query group, worker) for lane j < 2 QPT of each wave:
+    // feasibility (j < QPT) or near-tie (j >= QPT) of the wave's queries m = j % QPT
+    const int64_t brow = sc.bits_off + (int64_t)(((q0 - start) >> 6) + wave_id() + (lane % QPT) * (NT / 64)) * sc.W;
+    uint64_t* const bdst = (lane < QPT ? st.bits_feas : st.bits_nt) + brow;
 
     int cur = next_staged(Wi, nw, use_lb, 0);
     if (cur < nw) pf = prefetch_worker(st, Wi[cur], sc.wbase + wbeg + cur, tid);
     while (cur < nw) {
         __syncthreads();  // the previous worker's readers of LBs / Ss are done
-        stage_put(LBs, Ss, pf, tid);
+        stage_put(LBs, Ss, pf, tid, Wi[cur].n - Wi[cur].head, L);
         __syncthreads();
         const int nxt = next_staged(Wi, nw, use_lb, cur + 1);
         if (nxt < nw) pf = prefetch_worker(st, Wi[nxt], sc.wbase + wbeg + nxt, tid);
