@@ -44,8 +44,21 @@
  *  decode iteration: c += 1, r -= 1, requests with r < 0 leave, and the
  *  per-heartbeat prefill sums S1, S2 restart at zero.
  *
- * Constraint (d) needs decoding-time history that the workloads do not define
- * and is not evaluated.
+ *  Constraint (d), evaluated when the caller gives each resident's decode time
+ *  so far: prefill preempts the decoding of the ongoing requests, so the
+ *  prefill time of the heartbeat's new requests (the same t_p as in (c)) may
+ *  not exceed theta times the smallest time an ongoing request has saved
+ *  against the ATGT limit:  t_p <= theta * min_j (T_dec * g_j - t_dec_j), with
+ *  g_j the tokens generated so far.  Ongoing = residents and requests placed in
+ *  earlier heartbeats; a worker with none has no such limit.  At a heartbeat a
+ *  worker's decode iteration takes t_iter = (c3 + c2*b) + k2*sum(c) (Eq. 3, b
+ *  the batch and sum(c) its total context before the iteration); every request
+ *  in it gains one token and t_iter of decode time, so its slack
+ *  T_dec*g - t_dec grows by T_dec - t_iter, the same for all of them.  The
+ *  worker keeps that running gain as phi and each request its slack minus phi
+ *  (s0): slack = s0 + phi.  A request placed in heartbeat window h starts
+ *  decoding at the end of h with zero slack, so s0 = -phi at placement (phi
+ *  does not change within a window).
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -73,13 +86,16 @@ typedef struct {
     int64_t M;          /* KV capacity in tokens */
     int64_t n, cap;     /* number of requests, allocated length */
     int64_t *c, *r;     /* current context, remaining iterations; sorted by r descending */
+    double* s0;         /* per request: slack minus phi (constraint (d)) */
+    int64_t* win;       /* per request: heartbeat window it was placed in (-1: resident) */
     int64_t SC, SR;     /* sum of c and sum of r over the requests */
     int64_t S1, S2;     /* prefill sums of requests placed in this heartbeat */
+    double phi;         /* running slack gain of the ongoing requests (constraint (d)) */
 } worker_t;
 
 typedef struct {
     int rc;
-    int feasible, kv_ok, dec_ok, ttft_ok, near_tie;
+    int feasible, kv_ok, dec_ok, ttft_ok, pre_ok, near_tie;
     int64_t peak;
     double lhs, rhs, ttft, tdec;
     unsigned __int128 key;
@@ -127,8 +143,11 @@ static int near(double x, double y)
 }
 
 /* One (query, worker) evaluation; returns ORA_EOVERFLOW when an integer
- * quantity leaves the range where its fp64 conversion is exact. */
-static int eval_pair(const worker_t* w, const ora_model_t* m, int64_t lin, int64_t lpred, pair_t* o)
+ * quantity leaves the range where its fp64 conversion is exact.  use_d: the
+ * decode history is known and (d) is checked; hb: the current heartbeat
+ * window. */
+static int eval_pair(const worker_t* w, const ora_model_t* m, int64_t lin, int64_t lpred, int use_d, int64_t hb,
+                     pair_t* o)
 {
     const int gs = m->gamma_log2den;
     const int64_t gn = m->gamma_num;
@@ -156,9 +175,28 @@ static int eval_pair(const worker_t* w, const ora_model_t* m, int64_t lin, int64
     o->ttft = (m->c1 + m->k1 * (double)S1) + m->k1q * (double)S2;
     o->ttft_ok = o->ttft <= m->ttft_slo;
 
-    o->feasible = o->kv_ok && o->dec_ok && o->ttft_ok;
+    /* (d) the same prefill time against the ongoing requests' smallest slack */
+    o->pre_ok = 1;
+    int pre_near = 0;
+    if (use_d) {
+        int any = 0;
+        double smin = 0.0;
+        for (int64_t i = 0; i < w->n; ++i) {
+            if (w->win[i] >= hb) continue;  /* placed in this heartbeat: not decoding yet */
+            const double slack = w->s0[i] + w->phi;
+            if (!any || slack < smin) smin = slack;
+            any = 1;
+        }
+        if (any) {
+            const double lim = m->theta * smin;
+            o->pre_ok = o->ttft <= lim;
+            pre_near = near(o->ttft, lim);
+        }
+    }
+
+    o->feasible = o->kv_ok && o->dec_ok && o->ttft_ok && o->pre_ok;
     o->tdec = (m->c3 + m->c2 * (double)b) + m->k2 * sumD;
-    o->near_tie = near(o->lhs, o->rhs) || near(o->ttft, m->ttft_slo);
+    o->near_tie = near(o->lhs, o->rhs) || near(o->ttft, m->ttft_slo) || pre_near;
 
     /* rank key of Algorithm 1, before placement */
     const unsigned __int128 x = (unsigned __int128)(B * ((int64_t)1 << gs));
@@ -184,7 +222,7 @@ static int cmp_rank(const void* pa, const void* pb)
     return 0;
 }
 
-static int add_request(worker_t* w, int64_t c, int64_t r)
+static int add_request(worker_t* w, int64_t c, int64_t r, double s0, int64_t win)
 {
     if (w->n == w->cap) {
         int64_t nc = w->cap ? 2 * w->cap : 16;
@@ -194,6 +232,12 @@ static int add_request(worker_t* w, int64_t c, int64_t r)
         int64_t* rr = (int64_t*)realloc(w->r, (size_t)nc * sizeof(int64_t));
         if (!rr) return ORA_ENOMEM;
         w->r = rr;
+        double* ss = (double*)realloc(w->s0, (size_t)nc * sizeof(double));
+        if (!ss) return ORA_ENOMEM;
+        w->s0 = ss;
+        int64_t* ww = (int64_t*)realloc(w->win, (size_t)nc * sizeof(int64_t));
+        if (!ww) return ORA_ENOMEM;
+        w->win = ww;
         w->cap = nc;
     }
     /* keep r descending: insert after every request with r >= the new one */
@@ -201,16 +245,25 @@ static int add_request(worker_t* w, int64_t c, int64_t r)
     while (pos > 0 && w->r[pos - 1] < r) pos -= 1;
     memmove(w->c + pos + 1, w->c + pos, (size_t)(w->n - pos) * sizeof(int64_t));
     memmove(w->r + pos + 1, w->r + pos, (size_t)(w->n - pos) * sizeof(int64_t));
+    memmove(w->s0 + pos + 1, w->s0 + pos, (size_t)(w->n - pos) * sizeof(double));
+    memmove(w->win + pos + 1, w->win + pos, (size_t)(w->n - pos) * sizeof(int64_t));
     w->c[pos] = c;
     w->r[pos] = r;
+    w->s0[pos] = s0;
+    w->win[pos] = win;
     w->n += 1;
     w->SC += c;
     w->SR += r;
     return ORA_OK;
 }
 
-static void heartbeat(worker_t* w)
+static void heartbeat(worker_t* w, const ora_model_t* m)
 {
+    /* the iteration's time, from the batch before it (constraint (d)'s slack gain) */
+    if (w->n > 0) {
+        const double t_iter = (m->c3 + m->c2 * (double)w->n) + m->k2 * (double)w->SC;
+        w->phi = w->phi + (m->decode_slo - t_iter);
+    }
     int64_t keep = 0, SC = 0, SR = 0;
     for (int64_t i = 0; i < w->n; ++i) {
         w->c[i] += 1;
@@ -227,7 +280,7 @@ static void heartbeat(worker_t* w)
 static void free_workers(worker_t* ws, int32_t W)
 {
     if (!ws) return;
-    for (int32_t i = 0; i < W; ++i) { free(ws[i].c); free(ws[i].r); }
+    for (int32_t i = 0; i < W; ++i) { free(ws[i].c); free(ws[i].r); free(ws[i].s0); free(ws[i].win); }
     free(ws);
 }
 
@@ -244,7 +297,9 @@ static int valid_model(const ora_model_t* m)
 /*
  * Place a stream of queries.
  *   W workers with capacities M[W]; residents in CSR form (res_off[W+1]) with
- *   input length, predicted output length and tokens generated so far.
+ *   input length, predicted output length and tokens generated so far, and
+ *   optionally their decode time so far in seconds (res_tdec; NULL: constraint
+ *   (d) is not evaluated).
  *   H: heartbeat period in processed queries (0 = none).
  *   no_commit: evaluate every query against the initial state and commit
  *   nothing (used to sample a stream in which no query is ever placed).
@@ -257,7 +312,7 @@ static int valid_model(const ora_model_t* m)
  * final per-worker batch size, sum(c), sum(r), KV peak, S1, S2.
  */
 int ora_place(int32_t W, const int64_t* M, const int64_t* res_off,
-              const int32_t* res_lin, const int32_t* res_lpred, const int32_t* res_g,
+              const int32_t* res_lin, const int32_t* res_lpred, const int32_t* res_g, const double* res_tdec,
               const ora_model_t* model, int32_t Q, const int32_t* q_lin, const int32_t* q_lpred,
               int32_t H, int32_t no_commit, int32_t check, int32_t n_threads,
               int32_t* out_worker, int32_t* out_nfeas, int32_t* out_near_tie,
@@ -279,11 +334,18 @@ int ora_place(int32_t W, const int64_t* M, const int64_t* res_off,
         for (int64_t k = res_off ? res_off[i] : 0; res_off && k < res_off[i + 1]; ++k) {
             int64_t lin = res_lin[k], lp = res_lpred[k], g = res_g[k];
             if (lin < 1 || lp < 1 || g < 0 || g >= lp) { rc = ORA_EINVAL; goto done; }
-            rc = add_request(&ws[i], lin + g, lp - g);
+            double s0 = 0.0;  /* phi = 0 at load: s0 = the resident's slack */
+            if (res_tdec) {
+                if (!isfinite(res_tdec[k]) || res_tdec[k] < 0.0) { rc = ORA_EINVAL; goto done; }
+                s0 = model->decode_slo * (double)g - res_tdec[k];
+            }
+            rc = add_request(&ws[i], lin + g, lp - g, s0, -1);
             if (rc) goto done;
         }
     }
 
+    const int use_d = res_tdec != NULL;
+    int64_t hb = 0;  /* heartbeat window */
     int32_t since_hb = 0;
     for (int32_t q = 0; q < Q; ++q) {
         const int64_t lin = q_lin[q], lp = q_lpred[q];
@@ -294,7 +356,7 @@ int ora_place(int32_t W, const int64_t* M, const int64_t* res_off,
 #ifdef _OPENMP
 #pragma omp parallel for num_threads(n_threads > 0 ? n_threads : 1) schedule(static)
 #endif
-        for (int32_t i = 0; i < W; ++i) pr[i].rc = eval_pair(&ws[i], model, lin, lp, &pr[i]);
+        for (int32_t i = 0; i < W; ++i) pr[i].rc = eval_pair(&ws[i], model, lin, lp, use_d, hb, &pr[i]);
         for (int32_t i = 0; i < W; ++i) {
             if (pr[i].rc) { rc = pr[i].rc; goto done; }
             nfeas += pr[i].feasible;
@@ -313,7 +375,7 @@ int ora_place(int32_t W, const int64_t* M, const int64_t* res_off,
             if (first != best) { rc = ORA_ECHECK; goto done; }
         }
         /* near tie: any worker ranked at or above the choice (all, if rejected)
-         * whose decode or TTFT margin is within 1e-9 relative */
+         * whose decode, TTFT or (d) margin is within 1e-9 relative */
         int nt = 0;
         for (int32_t i = 0; i < W; ++i) {
             if (!pr[i].near_tie) continue;
@@ -329,7 +391,7 @@ int ora_place(int32_t W, const int64_t* M, const int64_t* res_off,
 
         if (best >= 0 && !no_commit) {
             worker_t* w = &ws[best];
-            rc = add_request(w, lin, lp);
+            rc = add_request(w, lin, lp, -w->phi, hb);
             if (rc) goto done;
             w->S1 += lin;
             w->S2 += lin * lin;
@@ -338,8 +400,9 @@ int ora_place(int32_t W, const int64_t* M, const int64_t* res_off,
         if (H > 0 && !no_commit) {
             since_hb += 1;
             if (since_hb == H) {
-                for (int32_t i = 0; i < W; ++i) heartbeat(&ws[i]);
+                for (int32_t i = 0; i < W; ++i) heartbeat(&ws[i], model);
                 since_hb = 0;
+                hb += 1;
             }
         }
     }
@@ -390,7 +453,7 @@ int ora_sweep(int32_t S, const ora_scenario_t* scen, int32_t Q, const int32_t* q
         int32_t* dst = out_worker ? out_worker + (int64_t)s * Q : tmp;
         if (rc == ORA_OK) {
             for (int32_t i = 0; i < W; ++i) M[i] = scen[s].kv_capacity;
-            rc = ora_place(W, M, NULL, NULL, NULL, NULL, &scen[s].model, Q, q_lin, q_lpred, 0, 0, 0, 1,
+            rc = ora_place(W, M, NULL, NULL, NULL, NULL, NULL, &scen[s].model, Q, q_lin, q_lpred, 0, 0, 0, 1,
                            dst, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL);
         }
         if (rc == ORA_OK) {
@@ -415,8 +478,8 @@ int64_t ora_kv_peak(int64_t n, const int64_t* c, const int64_t* r)
 {
     worker_t w;
     memset(&w, 0, sizeof w);
-    for (int64_t i = 0; i < n; ++i) if (add_request(&w, c[i], r[i])) return -1;
+    for (int64_t i = 0; i < n; ++i) if (add_request(&w, c[i], r[i], 0.0, -1)) return -1;
     int64_t p = kv_peak(&w, 0, 0, 0);
-    free(w.c); free(w.r);
+    free(w.c); free(w.r); free(w.s0); free(w.win);
     return p;
 }

@@ -55,7 +55,7 @@ def lib():
         L = ctypes.CDLL(LIB)
         P = ctypes.c_void_p
         i32, i64 = ctypes.c_int32, ctypes.c_int64
-        L.ora_place.argtypes = [i32, P, P, P, P, P, ctypes.POINTER(OraModel), i32, P, P, i32, i32, i32,
+        L.ora_place.argtypes = [i32, P, P, P, P, P, P, ctypes.POINTER(OraModel), i32, P, P, i32, i32, i32,
                                 i32, P, P, P, P, P, P, P, P, P, P, P, P, P]
         L.ora_place.restype = ctypes.c_int
         L.ora_sweep.argtypes = [i32, P, i32, P, P, i32, P, P, P]
@@ -93,7 +93,9 @@ class PlaceResult:
 
 
 def place(W, kv_capacity, res_offsets, res_l_in, res_l_pred, res_generated, model, q_l_in, q_l_pred,
-          heartbeat_every=0, no_commit=False, check=False, n_threads=1) -> PlaceResult:
+          heartbeat_every=0, no_commit=False, check=False, n_threads=1, res_t_dec=None) -> PlaceResult:
+    """res_t_dec: each resident's decode time so far in seconds; when given,
+    constraint (d) is evaluated as well."""
     L = lib()
     Q = int(len(q_l_in))
     c64 = lambda a: np.ascontiguousarray(a, dtype=np.int64)
@@ -101,12 +103,13 @@ def place(W, kv_capacity, res_offsets, res_l_in, res_l_pred, res_generated, mode
     M = c64(kv_capacity)
     off = c64(res_offsets) if res_offsets is not None else None
     rl, rp, rg = (c32(a) if a is not None else None for a in (res_l_in, res_l_pred, res_generated))
+    td = np.ascontiguousarray(res_t_dec, dtype=np.float64) if res_t_dec is not None else None
     ql, qp = c32(q_l_in), c32(q_l_pred)
     out = PlaceResult(*(np.zeros(Q, t) for t in (np.int32, np.int32, np.int32, np.int64, np.int64,
                                                  np.float64, np.float64)),
                       *(np.zeros(W, np.int64) for _ in range(6)))
     m = to_model(model)
-    rc = L.ora_place(W, _ptr(M), _ptr(off), _ptr(rl), _ptr(rp), _ptr(rg), ctypes.byref(m), Q,
+    rc = L.ora_place(W, _ptr(M), _ptr(off), _ptr(rl), _ptr(rp), _ptr(rg), _ptr(td), ctypes.byref(m), Q,
                      _ptr(ql), _ptr(qp), int(heartbeat_every), int(bool(no_commit)), int(bool(check)),
                      int(n_threads), _ptr(out.worker), _ptr(out.n_feasible), _ptr(out.near_tie),
                      _ptr(out.kv_peak_chosen), _ptr(out.kv_excess_min), _ptr(out.ttft_chosen),
@@ -122,7 +125,7 @@ def place_trace(trace, q_slice=slice(None), **kw) -> PlaceResult:
     return place(trace.n_workers, trace.kv_capacity, trace.res_offsets, trace.res_l_in,
                  trace.res_l_pred, trace.res_generated, trace.model, trace.q_l_in[q_slice],
                  trace.q_l_pred[q_slice], heartbeat_every=kw.pop("heartbeat_every", trace.heartbeat_every),
-                 **kw)
+                 res_t_dec=kw.pop("res_t_dec", getattr(trace, "res_t_dec", None)), **kw)
 
 
 def sweep(scenarios, q_l_in, q_l_pred, want_workers=False, n_threads=1):

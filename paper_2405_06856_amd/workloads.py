@@ -97,6 +97,7 @@ class Trace:
     q_l_pred: np.ndarray           # int32 [Q]
     arrivals: Optional[np.ndarray]  # float64 [Q] seconds, or None
     heartbeat_every: int = 0       # 0: the whole stream is one heartbeat
+    res_t_dec: Optional[np.ndarray] = None  # float64 [n_res] decode time so far (s), or None
 
     @property
     def n_workers(self) -> int:
@@ -236,6 +237,16 @@ CONFIGS = {
     "long": "W=2048, M=1048576, R=1024, Q=131072, long lengths, heartbeat every 100, "
             "TTFT 4 s, decode 0.08 s",
 }
+
+
+def with_decode_history(trace: Trace, seed: int, lo: float = 0.2, hi: float = 0.9) -> Trace:
+    """A copy of `trace` whose residents carry a decode time so far: each one's
+    g generated tokens took g * T_dec * f seconds, f uniform in [lo, hi) (seeded),
+    so some residents are ahead of the per-token decode target and some behind."""
+    rng = np.random.default_rng(seed)
+    f = rng.uniform(lo, hi, trace.n_resident)
+    t_dec = trace.res_generated.astype(np.float64) * trace.model.decode_slo * f
+    return dataclasses.replace(trace, name=trace.name + "+history", res_t_dec=t_dec)
 
 
 def make_config(name: str):

@@ -15,6 +15,12 @@ form from the oracle:
   large to small with ties to the lower index, then the first feasible worker.
 * A heartbeat drops the first element of every footprint vector (one decode
   iteration has run); empty vectors leave.
+* Constraint (d), with decode history: every request keeps its generated-token
+  count g and decode time t_dec literally (exact rationals); a heartbeat's
+  iteration time is Eq. 3, (c3 + c2*b) + k2*sum(context), over the batch before
+  the iteration, and every request in the batch gains one token and that time.
+  A request placed in the current heartbeat has not decoded yet and is not
+  ongoing.  Prefill time (as in (c)) <= theta * min over ongoing (T_dec*g - t_dec).
 """
 from __future__ import annotations
 
@@ -24,10 +30,11 @@ from typing import List
 
 
 class Req:
-    __slots__ = ("l_in", "l_pred", "g", "new")
+    __slots__ = ("l_in", "l_pred", "g", "new", "t_dec")
 
-    def __init__(self, l_in, l_pred, g=0, new=False):
+    def __init__(self, l_in, l_pred, g=0, new=False, t_dec=0.0):
         self.l_in, self.l_pred, self.g, self.new = int(l_in), int(l_pred), int(g), bool(new)
+        self.t_dec = Fraction(t_dec)
 
     def footprint(self) -> List[int]:
         return [self.l_in + k for k in range(self.g, self.l_pred + 1)]
@@ -46,23 +53,28 @@ class BruteWorker:
     def __init__(self, M, reqs=()):
         self.M = int(M)
         self.vecs = [r.footprint() for r in reqs]
-        # per request: (context-now, remaining, l_in, is_new)
-        self.meta = [[r.l_in + r.g, r.l_pred - r.g, r.l_in, False] for r in reqs]
+        # per request: (context-now, remaining, l_in, is_new, generated, decode time)
+        self.meta = [[r.l_in + r.g, r.l_pred - r.g, r.l_in, False, r.g, r.t_dec] for r in reqs]
 
-    def heartbeat(self):
+    def heartbeat(self, model=None):
+        F = Fraction
+        t_iter = F(0)
+        if model is not None and self.meta:
+            b = len(self.meta)
+            t_iter = F(model.c3) + F(model.c2) * b + F(model.k2) * sum(F(m[0]) for m in self.meta)
         keep_v, keep_m = [], []
         for v, m in zip(self.vecs, self.meta):
             v = v[1:]
             if v:
                 keep_v.append(v)
-                keep_m.append([m[0] + 1, m[1] - 1, m[2], False])
+                keep_m.append([m[0] + 1, m[1] - 1, m[2], False, m[4] + 1, m[5] + t_iter])
         self.vecs, self.meta = keep_v, keep_m
 
     def batch(self):
         return len(self.vecs)
 
 
-def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0):
+def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0, use_d=False):
     """Per query a dict: chosen worker (-1 = none), n_feasible, per-worker KV
     peaks and a flag telling whether any exact latency margin is so small that
     fp64 rounding could decide it (those queries are not comparable bit for bit)."""
@@ -81,19 +93,26 @@ def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0):
             kv_ok = peak <= w.M
             # sum of (l_in + gamma * l_out) with l_out split into generated (counted
             # fully, it is already in the context) and remaining (weighted by gamma)
-            sumD = sum(F(c) + gamma * F(r) for c, r, _, _ in w.meta) + F(l_in) + gamma * F(l_pred)
+            sumD = sum(F(c) + gamma * F(r) for c, r, _, _, _, _ in w.meta) + F(l_in) + gamma * F(l_pred)
             ld = (F(model.decode_slo) - F(model.c3) - F(model.c2) * b) / F(model.k2)
             dec_ok = sumD <= F(model.theta) * ld
-            S1 = sum(F(li) for _, _, li, new in w.meta if new) + F(l_in)
-            S2 = sum(F(li) ** 2 for _, _, li, new in w.meta if new) + F(l_in) ** 2
+            S1 = sum(F(li) for _, _, li, new, _, _ in w.meta if new) + F(l_in)
+            S2 = sum(F(li) ** 2 for _, _, li, new, _, _ in w.meta if new) + F(l_in) ** 2
             ttft = F(model.c1) + F(model.k1) * S1 + F(model.k1q) * S2
             ttft_ok = ttft <= F(model.ttft_slo)
             lim = F(model.theta) * ld
             if abs(lim - sumD) <= F(1, 10 ** 9) * max(abs(lim), abs(sumD)) or \
                abs(F(model.ttft_slo) - ttft) <= F(1, 10 ** 9) * max(abs(ttft), abs(F(model.ttft_slo))):
                 close = True
-            feas.append(kv_ok and dec_ok and ttft_ok)
-            sumD_now = sum(F(c) + gamma * F(r) for c, r, _, _ in w.meta)
+            pre_ok = True
+            ongoing = [F(model.decode_slo) * g - td for _, _, _, new, g, td in w.meta if not new]
+            if use_d and ongoing:
+                dl = F(model.theta) * min(ongoing)
+                pre_ok = ttft <= dl
+                if abs(ttft - dl) <= F(1, 10 ** 9) * max(abs(ttft), abs(dl)):
+                    close = True
+            feas.append(kv_ok and dec_ok and ttft_ok and pre_ok)
+            sumD_now = sum(F(c) + gamma * F(r) for c, r, _, _, _, _ in w.meta)
             norms.append(math.hypot(float(w.batch()), float(sumD_now)))
             peaks.append(peak)
         order = sorted(range(len(workers)), key=lambda i: (-norms[i], i))
@@ -101,13 +120,13 @@ def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0):
         if chosen >= 0:
             w = workers[chosen]
             w.vecs.append(qv)
-            w.meta.append([l_in, l_pred, l_in, True])
+            w.meta.append([l_in, l_pred, l_in, True, 0, F(0)])
         out.append({"worker": chosen, "n_feasible": sum(feas), "peaks": peaks, "norms": norms,
                     "close": close})
         if heartbeat_every:
             since += 1
             if since == heartbeat_every:
                 for w in workers:
-                    w.heartbeat()
+                    w.heartbeat(model)
                 since = 0
     return out

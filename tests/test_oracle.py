@@ -24,18 +24,22 @@ GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 FREE = wl.Model(c1=0.0, k1=0.0, k1q=0.0, c3=0.0, c2=0.0, k2=1e-12, ttft_slo=1e9, decode_slo=1e9)
 
 
-def run(W, M, residents, model, queries, H=0, check=True):
-    """residents: list per worker of (l_in, l_pred, g)."""
+def run(W, M, residents, model, queries, H=0, check=True, t_dec=None):
+    """residents: list per worker of (l_in, l_pred, g); t_dec: list per worker of
+    the residents' decode times (constraint (d) on), or None."""
     off = np.zeros(W + 1, np.int64)
-    rl, rp, rg = [], [], []
+    rl, rp, rg, td = [], [], [], []
     for i in range(W):
-        for (a, b, g) in residents[i]:
+        for k, (a, b, g) in enumerate(residents[i]):
             rl.append(a); rp.append(b); rg.append(g)
+            if t_dec is not None:
+                td.append(t_dec[i][k])
         off[i + 1] = len(rl)
     q = np.array(queries, np.int32).reshape(-1, 2)
     return ref.place(W, np.full(W, M, np.int64) if np.isscalar(M) else np.asarray(M, np.int64), off,
                      np.array(rl, np.int32), np.array(rp, np.int32), np.array(rg, np.int32), model,
-                     q[:, 0], q[:, 1], heartbeat_every=H, check=check)
+                     q[:, 0], q[:, 1], heartbeat_every=H, check=check,
+                     res_t_dec=None if t_dec is None else np.array(td, np.float64))
 
 
 # --------------------------------------------------------------------------- paper's worked example
@@ -132,6 +136,79 @@ def test_placement_matches_bruteforce(H):
                 assert res.kv_peak_chosen[k] == wq["peaks"][wq["worker"]]
             compared += 1
     assert compared > 1500
+
+
+@pytest.mark.parametrize("H", [0, 1, 3])
+def test_preemption_limit_matches_bruteforce(H):
+    # constraint (d) against the literal per-request decode history (exact
+    # rationals, tokens and decode time accumulated request by request)
+    rng = np.random.default_rng(300 + H)
+    compared = blocked = 0
+    for case in range(400):
+        W = int(rng.integers(1, 5))
+        model = _random_model(rng)
+        model = dataclasses.replace(model, c1=float(rng.uniform(0.0, 0.02)), k1=float(rng.uniform(0.0, 0.004)),
+                                    ttft_slo=1.0)
+        residents, t_dec = [], []
+        for _ in range(W):
+            rs, ts = [], []
+            for _ in range(int(rng.integers(0, 5))):
+                lp = int(rng.integers(1, 9))
+                g = int(rng.integers(0, lp))
+                rs.append((int(rng.integers(1, 9)), lp, g))
+                ts.append(float(g * model.decode_slo * rng.uniform(0.0, 1.2)))
+            residents.append(rs)
+            t_dec.append(ts)
+        M = [int(rng.integers(8, 60)) for _ in range(W)]
+        queries = [(int(rng.integers(1, 9)), int(rng.integers(1, 9))) for _ in range(int(rng.integers(1, 12)))]
+        res = run(W, M, residents, model, queries, H=H, t_dec=t_dec)
+        free = run(W, M, residents, model, queries, H=H)
+        bw = [BruteWorker(M[i], [Req(a, b, g, t_dec=t_dec[i][k]) for k, (a, b, g) in enumerate(residents[i])])
+              for i in range(W)]
+        want = brute_place(bw, model, queries, heartbeat_every=H, use_d=True)
+        for k, wq in enumerate(want):
+            if wq["close"]:
+                break
+            norms = sorted(wq["norms"])
+            if any(0 < b - a <= 1e-12 * b for a, b in zip(norms, norms[1:])):
+                break
+            assert res.worker[k] == wq["worker"], (case, k)
+            assert res.n_feasible[k] == wq["n_feasible"], (case, k)
+            blocked += int(res.n_feasible[k] < free.n_feasible[k]) if k == 0 else 0
+            compared += 1
+    assert compared > 1200
+    assert blocked > 20  # the limit does bind in this population
+
+
+def test_preemption_limit_worked_example():
+    # one worker, one resident (l_in 10, l_pred 100, 10 tokens in 0.5 s), heartbeat
+    # after every query, T_dec = 0.05 s: its slack is 10 * 0.05 - 0.5 = 0 at first.
+    m = wl.Model(c1=0.001, k1=1e-3, k1q=0.0, c3=0.01, c2=0.001, k2=1e-4, ttft_slo=10.0, decode_slo=0.05)
+    q = [(30, 5), (30, 5), (40, 5), (40, 5)]
+    res = run(1, 10 ** 6, [[(10, 100, 10)]], m, q, H=1, t_dec=[[0.5]])
+    # q0: prefill 0.031 s > 1.0 * 0 -> rejected.  Heartbeat 1 (batch 1, context 20):
+    # t_iter = (0.01 + 0.001) + 1e-4 * 20 = 0.013, slack 0.037.
+    # q1: 0.031 <= 0.037 -> placed.  Heartbeat 2 (batch 2, context 21 + 30):
+    # t_iter = 0.012 + 0.0051 = 0.0171; the resident's slack 0.0699, q1's (its
+    # first iteration) 0.05 - 0.0171 = 0.0329.
+    # q2: 0.041 > 0.0329 -> rejected.  Heartbeat 3 (batch 2, context 22 + 31):
+    # t_iter = 0.012 + 0.0053 = 0.0173, q1's slack 0.0329 + 0.0327 = 0.0656.
+    # q3: 0.041 <= 0.0656 -> placed (decode: 1e-4 * 142.5 <= 0.037).
+    assert list(res.worker) == [-1, 0, -1, 0]
+    # without the decode history only (b), (c), (e) apply and every query fits
+    assert list(run(1, 10 ** 6, [[(10, 100, 10)]], m, q, H=1).worker) == [0] * 4
+
+
+def test_preemption_limit_needs_an_ongoing_request():
+    # zero slack (nothing generated yet) blocks every prefill on its worker; a
+    # worker with no ongoing request has no such limit, also once it holds
+    # requests placed in the current heartbeat
+    m = wl.Model(c1=0.01, k1=1e-5, k1q=0.0, c3=0.0, c2=0.0, k2=1e-9, ttft_slo=10.0, decode_slo=0.05)
+    q = [(50, 10)] * 5
+    res = run(2, 10 ** 6, [[(100, 50, 0)], []], m, q, t_dec=[[0.0], []])
+    assert list(res.worker) == [1] * 5
+    res = run(2, 10 ** 6, [[(100, 50, 0)], []], m, q)  # no history: the fuller worker
+    assert list(res.worker) == [0] * 5
 
 
 def test_heartbeat_is_one_iteration_shift():

@@ -17,9 +17,9 @@ SRC = open(ref.SRC).read()
 MUTANTS = [
     ("kv end point one iteration early", "int64_t d_ = sumc + cnt * (t);", "int64_t d_ = sumc + cnt * ((t) - 1);"),
     ("query's own end point not checked", "sumc += cq; cnt += 1;\n        DEMAND_AT(rq);", "sumc += cq; cnt += 1;"),
-    ("generated tokens not in the context", "add_request(&ws[i], lin + g, lp - g)", "add_request(&ws[i], lin, lp - g)"),
-    ("remaining length ignores generated tokens", "add_request(&ws[i], lin + g, lp - g)",
-     "add_request(&ws[i], lin + g, lp)"),
+    ("generated tokens not in the context", "add_request(&ws[i], lin + g, lp - g,", "add_request(&ws[i], lin, lp - g,"),
+    ("remaining length ignores generated tokens", "add_request(&ws[i], lin + g, lp - g,",
+     "add_request(&ws[i], lin + g, lp,"),
     ("batch size without the query", "const int64_t b = B + 1;", "const int64_t b = B;"),
     ("gamma applied to the context", "const int64_t DS = SC * ((int64_t)1 << gs) + gn * SR;",
      "const int64_t DS = SC * gn + SR * ((int64_t)1 << gs);"),
@@ -39,6 +39,17 @@ MUTANTS = [
      "if (H > 0 && !no_commit && best >= 0) {\n            since_hb += 1;"),
     ("smallest excess over feasible workers only", "if (ex < excess_min) excess_min = ex;",
      "if (pr[i].feasible && ex < excess_min) excess_min = ex;"),
+    # constraint (d)
+    ("(d) not part of feasibility", "o->feasible = o->kv_ok && o->dec_ok && o->ttft_ok && o->pre_ok;",
+     "o->feasible = o->kv_ok && o->dec_ok && o->ttft_ok;"),
+    ("(d) counts this heartbeat's requests as ongoing", "if (w->win[i] >= hb) continue;", "if (w->win[i] > hb) continue;"),
+    ("(d) limit without theta", "const double lim = m->theta * smin;", "const double lim = smin;"),
+    ("(d) new request starts at the worker's gain", "add_request(w, lin, lp, -w->phi, hb)", "add_request(w, lin, lp, 0.0, hb)"),
+    ("(d) slack gain with the sign flipped", "w->phi = w->phi + (m->decode_slo - t_iter);",
+     "w->phi = w->phi + (t_iter - m->decode_slo);"),
+    ("(d) iteration time without the batch term", "(m->c3 + m->c2 * (double)w->n)", "(m->c3 + m->c2 * (double)(w->n - 1))"),
+    ("(d) resident slack from the predicted length", "s0 = model->decode_slo * (double)g - res_tdec[k];",
+     "s0 = model->decode_slo * (double)lp - res_tdec[k];"),
 ]
 
 PINS = [
@@ -56,6 +67,11 @@ PINS = [
     pins.test_capacity_norm_ranking_picks_fullest_feasible,
     pins.test_decode_near_tie_band_is_relative,
     pins.test_capacity_norm_is_taken_before_placement,
+    lambda: pins.test_preemption_limit_matches_bruteforce(0),
+    lambda: pins.test_preemption_limit_matches_bruteforce(1),
+    lambda: pins.test_preemption_limit_matches_bruteforce(3),
+    pins.test_preemption_limit_worked_example,
+    pins.test_preemption_limit_needs_an_ongoing_request,
 ]
 
 
