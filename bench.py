@@ -33,9 +33,14 @@ def algorithmic_bytes_per_pair(residents_per_worker: int) -> int:
     return 8 * residents_per_worker + 40
 
 
+# the translation unit of the pair-evaluation kernel
+EVAL_SOURCES = ("ald_kernels.hip", "ald_device.h", "ald_internal.h")
+
+
 def kernel_source_sha256() -> str:
     h = hashlib.sha256()
-    for p in ("paper_2405_06856_amd/csrc/ald_kernels.hip", "paper_2405_06856_amd/csrc/ald_internal.h"):
+    for p in EVAL_SOURCES:
+        p = os.path.join("paper_2405_06856_amd", "csrc", p)
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()

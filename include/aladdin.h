@@ -25,7 +25,13 @@
  *   - heartbeat: after every H processed queries each worker runs one decode
  *     iteration (c += 1, r -= 1, finished requests leave) and the TTFT sums of
  *     constraint (c) restart at zero.
- * Constraint (d) (prefill preemption slack) is not evaluated.
+ *   - constraint (d), prefill preemption (only with a decode history, see
+ *     ald_load_workers_history): the same prefill time as (c) must also stay
+ *     <= theta * min over the worker's ongoing requests of (T_dec * g - t_dec),
+ *     g = tokens generated so far, t_dec = decode time so far; each heartbeat's
+ *     decode iteration takes (c3 + c2*b) + k2*sum(c) (Eq. 3) and adds one token
+ *     and that time to every request in it.  Ongoing = resident at load or placed
+ *     in an earlier heartbeat; a worker with none has no such limit.
  *
  * Conventions
  *   - Every array argument except where marked "host" is a DEVICE pointer to
@@ -117,6 +123,18 @@ int ald_load_workers(ald_handle_t handle, int32_t W, const ald_model_t* model,
                      const int64_t* kv_capacity, const int64_t* res_offsets,
                      const int32_t* res_l_in, const int32_t* res_l_pred,
                      const int32_t* res_generated, int32_t slots_per_worker);
+
+/* As ald_load_workers, and every resident's decode time so far in seconds
+ * (device array res_t_dec[res_offsets[W]], finite, >= 0), so that constraint
+ * (d) of the placement MIP (Sec. 4.2: the new requests' prefill may not exceed
+ * the time the ongoing ones have saved against the ATGT limit, scaled by theta)
+ * is checked for every later placement.  ALD_EINVAL for a NULL or invalid
+ * history.  Costs one fp64 slack base and a window index per request slot. */
+int ald_load_workers_history(ald_handle_t handle, int32_t W, const ald_model_t* model,
+                             const int64_t* kv_capacity, const int64_t* res_offsets,
+                             const int32_t* res_l_in, const int32_t* res_l_pred,
+                             const int32_t* res_generated, const double* res_t_dec,
+                             int32_t slots_per_worker);
 
 /* Place Q queries (device arrays q_l_in[Q], q_l_pred[Q], values >= 1) in index
  * (arrival) order on the loaded workers, committing every placement.  Repeated

@@ -46,7 +46,8 @@ DIAG_DTYPE = np.dtype([("n_feasible", "<i4"), ("near_tie", "<i4"), ("kv_peak_cho
                        ("kv_excess_min", "<i8"), ("ttft_chosen", "<f8"), ("tdec_chosen", "<f8")])
 assert DIAG_DTYPE.itemsize == 40
 
-SYMBOLS = ("ald_create", "ald_destroy", "ald_set_tile", "ald_load_workers", "ald_place_stream",
+SYMBOLS = ("ald_create", "ald_destroy", "ald_set_tile", "ald_load_workers", "ald_load_workers_history",
+           "ald_place_stream",
            "ald_sweep_scenarios", "ald_worker_summary", "ald_set_profiling", "ald_kernel_time",
            "ald_last_error", "ald_strerror")
 
@@ -61,6 +62,7 @@ def _load():
         "ald_destroy": ([P], ctypes.c_int),
         "ald_set_tile": ([P, i32], ctypes.c_int),
         "ald_load_workers": ([P, i32, ctypes.POINTER(Model), P, P, P, P, P, i32], ctypes.c_int),
+        "ald_load_workers_history": ([P, i32, ctypes.POINTER(Model), P, P, P, P, P, P, i32], ctypes.c_int),
         "ald_place_stream": ([P, i32, P, P, i32, P, P], ctypes.c_int),
         "ald_sweep_scenarios": ([P, i32, P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_worker_summary": ([P, P, P, P, P], ctypes.c_int),
@@ -117,6 +119,13 @@ def ald_load_workers(h, W: int, model: Model, kv_capacity, res_offsets, res_l_in
     _check(h, _L.ald_load_workers(h, int(W), ctypes.byref(model), _dptr(kv_capacity), _dptr(res_offsets),
                                   _dptr(res_l_in), _dptr(res_l_pred), _dptr(res_generated),
                                   int(slots_per_worker)))
+
+
+def ald_load_workers_history(h, W: int, model: Model, kv_capacity, res_offsets, res_l_in, res_l_pred,
+                             res_generated, res_t_dec, slots_per_worker: int = 0) -> None:
+    _check(h, _L.ald_load_workers_history(h, int(W), ctypes.byref(model), _dptr(kv_capacity), _dptr(res_offsets),
+                                          _dptr(res_l_in), _dptr(res_l_pred), _dptr(res_generated),
+                                          _dptr(res_t_dec), int(slots_per_worker)))
 
 
 def ald_place_stream(h, Q: int, q_l_in, q_l_pred, heartbeat_every: int, out_worker, out_diag=None) -> None:
@@ -194,17 +203,25 @@ class Evaluator:
         t = self.torch
         return t.as_tensor(np.ascontiguousarray(a), dtype=dtype).to(self.device)
 
-    def load(self, W, model, kv_capacity, res_offsets, res_l_in, res_l_pred, res_generated, slots_per_worker=0):
+    def load(self, W, model, kv_capacity, res_offsets, res_l_in, res_l_pred, res_generated, slots_per_worker=0,
+             res_t_dec=None):
+        """res_t_dec: the residents' decode times so far (seconds); given, constraint
+        (d) is checked for every later placement."""
         t = self.torch
         self._keep = [self._dev(kv_capacity, t.int64), self._dev(res_offsets, t.int64),
                       self._dev(res_l_in, t.int32), self._dev(res_l_pred, t.int32),
                       self._dev(res_generated, t.int32)]
-        ald_load_workers(self.h, W, to_model(model), *self._keep, slots_per_worker=slots_per_worker)
+        if res_t_dec is None:
+            ald_load_workers(self.h, W, to_model(model), *self._keep, slots_per_worker=slots_per_worker)
+        else:
+            self._keep.append(self._dev(res_t_dec, t.float64))
+            ald_load_workers_history(self.h, W, to_model(model), *self._keep, slots_per_worker=slots_per_worker)
         self.W = W
 
     def load_trace(self, trace, slots_per_worker=0):
         self.load(trace.n_workers, trace.model, trace.kv_capacity, trace.res_offsets, trace.res_l_in,
-                  trace.res_l_pred, trace.res_generated, slots_per_worker)
+                  trace.res_l_pred, trace.res_generated, slots_per_worker,
+                  res_t_dec=getattr(trace, "res_t_dec", None))
 
     def place_device(self, q_l_in, q_l_pred, heartbeat_every=0, diag=True, out=None, diag_out=None):
         """Device tensors in, device tensors out (no host copies).  `out` (int32

@@ -28,6 +28,7 @@ struct Arena {
     void* scratch = nullptr;
     Scen* dscen = nullptr;
     int eval_mode = 2;    // how the pair evaluation takes the latency checks (launch_eval)
+    bool use_d = false;   // some scenario checks constraint (d)
     Ctl* hctl = nullptr;  // pinned host copy of the control blocks
     int32_t hctl_n = 0;
 
@@ -191,6 +192,9 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
     TileInfo* ti = nullptr;
     int32_t* qbad = nullptr;
     size_t worker_bytes = 0;
+    bool use_d = false;  // constraint (d)'s per-request log is only kept where it is checked
+    for (const Scen& x : scen) use_d = use_d || x.use_d;
+    const int64_t log_slots = use_d ? slots : 1;
     auto carve = [&](Carver& c) {
         c.take(&st.slot_base, NW); c.take(&st.cap, NW); c.take(&st.n, NW); c.take(&st.head, NW);
         c.take(&st.M, NW); c.take(&st.S1, NW); c.take(&st.S2, NW); c.take(&st.hbs, NW);
@@ -199,8 +203,11 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
         c.take(&st.dq_max, NW); c.take(&st.ntd_lo, NW); c.take(&st.ntd_hi, NW);
         c.take(&st.lthr, NW); c.take(&st.ntt_lo, NW); c.take(&st.ntt_hi, NW);
         c.take(&st.ntd_mask, NW); c.take(&st.ntt_mask, NW);
+        c.take(&st.phi, NW); c.take(&st.phi_hb, NW); c.take(&st.dlim, NW); c.take(&st.ntp_lo, NW);
+        c.take(&st.ntp_hi, NW); c.take(&st.lgn, NW);
         worker_bytes = c.off;
         c.take(&st.e, slots); c.take(&st.s, slots); c.take(&st.pms, slots);
+        c.take(&st.lge, log_slots); c.take(&st.lgw, log_slots); c.take(&st.lgs, log_slots);
         c.take(&st.lbt, (size_t)NW * LB_MAX);
         c.take(&st.dlist, (size_t)a->S * MAX_DIRTY); c.take(&st.dcount, a->S);
         c.take(&ctl, a->S); c.take(&ti, a->S); c.take(&a->dscen, a->S); c.take(&qbad, 1);
@@ -234,11 +241,14 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
         int32_t capmax = 0;
         for (int32_t i = 0; i < W[s]; ++i) capmax = std::max(capmax, caps[wfirst + i]);
         wfirst += W[s];
-        a->hscen[s].ntint = nt_integer(a->hscen[s], capmax) ? 1 : 0;
+        // constraint (d)'s limit depends on the decode history, so its near-tie
+        // band has no bound from the coefficients
+        a->hscen[s].ntint = (nt_integer(a->hscen[s], capmax) && !a->hscen[s].use_d) ? 1 : 0;
         mono = mono && a->hscen[s].mono;
         ntint = ntint && a->hscen[s].ntint;
     }
     a->eval_mode = ntint ? 2 : (mono ? 1 : 0);
+    a->use_d = use_d;
     // empty workers of a scenario are interchangeable when they share one capacity
     int64_t w0 = 0;
     for (int s = 0; s < a->S; ++s) {
@@ -421,7 +431,7 @@ int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, 
             if (mode >= 0) LAUNCH(h, 0, launch_build(a->st, h->stream, mode));
             LAUNCH(h, 1, launch_eval(a->st, a->eval_blocks, a->eval_mode, h->stream));
             LAUNCH(h, 2, launch_select(a->st, a->sel_blocks, h->stream));
-            LAUNCH(h, 3, launch_commit(a->st, a->commit_blocks, h->stream));
+            LAUNCH(h, 3, launch_commit(a->st, a->commit_blocks, a->use_d, h->stream));
         }
         // every commit launch wrote its scenarios' control blocks to the pinned mirror
         HIPCHK(h, hipStreamSynchronize(h->stream));
@@ -512,9 +522,10 @@ int ald_kernel_time(ald_handle_t h, int32_t kind, double* total_ms, int64_t* lau
     return ALD_OK;
 }
 
-int ald_load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const int64_t* kv_capacity,
-                     const int64_t* res_offsets, const int32_t* res_l_in, const int32_t* res_l_pred,
-                     const int32_t* res_generated, int32_t slots_per_worker)
+namespace {
+int load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const int64_t* kv_capacity,
+                 const int64_t* res_offsets, const int32_t* res_l_in, const int32_t* res_l_pred,
+                 const int32_t* res_generated, int32_t slots_per_worker, const double* res_t_dec)
 {
     if (!h) return ALD_EINVAL;
     HIPCHK(h, hipSetDevice(h->device));
@@ -555,18 +566,21 @@ int ald_load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const 
     h->main = nullptr;
     Arena* a = new Arena();
     std::vector<Scen> sc(1, make_scen(*model));
+    sc[0].use_d = res_t_dec != nullptr ? 1 : 0;
     int rc = make_arena(h, a, sc, std::vector<int32_t>(1, W), caps, Ms);
     if (rc == ALD_OK) rc = layout_scratch(h, a, 256, 4096);
     if (rc != ALD_OK) { delete a; return rc; }
     a->st.err_word = h->err_word;
     HIPCHK(h, hipMemsetAsync(h->err_word, 0, sizeof(int32_t), h->stream));
-    HIPCHK(h, launch_ingest(a->st, W, res_offsets, res_l_in, res_l_pred, res_generated, h->stream));
+    HIPCHK(h, launch_ingest(a->st, W, res_offsets, res_l_in, res_l_pred, res_generated, res_t_dec, h->stream));
     int32_t dev_err = 0;
     HIPCHK(h, hipMemcpyAsync(&dev_err, h->err_word, sizeof(int32_t), hipMemcpyDeviceToHost, h->stream));
     HIPCHK(h, hipStreamSynchronize(h->stream));
     if (dev_err) {
         delete a;
-        if (dev_err == DEV_EINVAL) return fail(h, ALD_EINVAL, "resident lengths must satisfy 1 <= l_in, l_pred <= 2^24 and 0 <= generated < l_pred");
+        if (dev_err == DEV_EINVAL)
+            return fail(h, ALD_EINVAL, "resident lengths must satisfy 1 <= l_in, l_pred <= 2^24 and 0 <= generated < l_pred "
+                                       "(and decode times be finite and >= 0)");
         if (dev_err == DEV_EOVERFLOW) return fail(h, ALD_EOVERFLOW, "a worker's residents exceed 2^30 tokens of future KV demand");
         return map_dev_error(h, dev_err);
     }
@@ -588,6 +602,24 @@ int ald_load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const 
     h->tau = h->hb_index = h->since_hb = h->round = 0;
     h->rebuild_pending = h->dirty_pending = false;
     return ALD_OK;
+}
+}  // namespace
+
+int ald_load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const int64_t* kv_capacity,
+                     const int64_t* res_offsets, const int32_t* res_l_in, const int32_t* res_l_pred,
+                     const int32_t* res_generated, int32_t slots_per_worker)
+{
+    return load_workers(h, W, model, kv_capacity, res_offsets, res_l_in, res_l_pred, res_generated,
+                        slots_per_worker, nullptr);
+}
+
+int ald_load_workers_history(ald_handle_t h, int32_t W, const ald_model_t* model, const int64_t* kv_capacity,
+                             const int64_t* res_offsets, const int32_t* res_l_in, const int32_t* res_l_pred,
+                             const int32_t* res_generated, const double* res_t_dec, int32_t slots_per_worker)
+{
+    if (!res_t_dec) return fail(h, ALD_EINVAL, "null decode history");
+    return load_workers(h, W, model, kv_capacity, res_offsets, res_l_in, res_l_pred, res_generated,
+                        slots_per_worker, res_t_dec);
 }
 
 int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,

@@ -68,6 +68,7 @@ struct Scen {
     int32_t mono;       // k1, k1q >= 0: the TTFT of a pair grows with l_in (integer thresholds apply)
     int32_t ntint;      // with mono: every near-tie band spans at most 64 integer values (bound
                         // from the coefficients), so near-tie margins have integer forms too
+    int32_t use_d;      // the residents' decode history is known: constraint (d) is checked
     int64_t bits_off;   // uint64 words into bits_feas / bits_nt
     int64_t part_off;   // int4 entries into part (worker block major: part_off + wb * pstride + query)
     int64_t pstride;    // queries per tile rounded up to whole evaluation chunks
@@ -162,6 +163,23 @@ struct State {
     // margin test at l_in = ntt_lo + i (zero where the band is wider).
     uint64_t* ntd_mask;
     uint64_t* ntt_mask;
+    // Constraint (d) (with Scen::use_d): every ongoing request's slack
+    // T_dec * g - t_dec grows by T_dec - t_iter at each heartbeat; the worker
+    // keeps that running gain in phi (brought up to heartbeat phi_hb) and each
+    // request slack - phi in its log entry.  dlim = theta * the smallest slack
+    // of the ongoing live requests at the built state (+inf: no limit); the
+    // TTFT threshold lthr includes it, and [ntp_lo, ntp_hi] holds every l_in
+    // whose prefill time can be within a near tie of dlim.
+    double* phi;
+    int32_t* phi_hb;
+    double* dlim;
+    int32_t* ntp_lo;
+    int32_t* ntp_hi;
+    int32_t* lgn;      // log entries of the worker
+    // per slot (the worker's slot range, unordered): the log of its requests
+    int32_t* lge;      // e of the request (it has finished once e < tau)
+    int32_t* lgw;      // heartbeat window it was placed in (-1: resident at load)
+    double* lgs;       // slack - phi
     // per slot
     int32_t* e;
     int32_t* s;
@@ -204,7 +222,7 @@ inline __host__ __device__ int32_t tile_end(int32_t start, int32_t Q, int32_t T,
 
 // host-side launchers (ald_kernels.hip)
 hipError_t launch_ingest(const State& st, int32_t W, const int64_t* res_off, const int32_t* lin,
-                         const int32_t* lpred, const int32_t* gen, hipStream_t stream);
+                         const int32_t* lpred, const int32_t* gen, const double* tdec, hipStream_t stream);
 // mode 0: every worker whose summaries are stale; 1: only the workers listed by
 // the last commit; 2: every worker unconditionally
 hipError_t launch_build(const State& st, hipStream_t stream, int mode);
@@ -212,7 +230,8 @@ hipError_t launch_build(const State& st, hipStream_t stream, int mode);
 // fp64; 2: integer thresholds and near-tie sets
 hipError_t launch_eval(const State& st, int32_t blocks, int mode, hipStream_t stream);
 hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream);
-hipError_t launch_commit(const State& st, int32_t blocks, hipStream_t stream);
+// use_d: some scenario checks constraint (d)
+hipError_t launch_commit(const State& st, int32_t blocks, bool use_d, hipStream_t stream);
 hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q, Ctl* ctl, int32_t S,
                               hipStream_t stream);
 hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* tinfo, int32_t* qbad,

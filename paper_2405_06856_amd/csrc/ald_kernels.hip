@@ -11,322 +11,13 @@
 //   k_commit  arrival-order commit: one block per scenario walks the tile,
 //             re-evaluating only workers changed earlier in the same tile, and
 //             cuts the tile when the tile-start lists cannot decide exactly;
-//             extra blocks finalize the rejected prefix in parallel.
-#include "ald_internal.h"
+//             extra blocks finalize the rejected prefix in parallel
+//             (ald_commit.h; launched from ald_commit.hip and ald_commit_d.hip).
+#include "ald_device.h"
 
 #include <type_traits>
 
 namespace ald {
-
-__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
-__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
-
-struct OpAdd {
-    __device__ int64_t operator()(int64_t a, int64_t b) const { return a + b; }
-};
-struct OpMax {
-    __device__ int64_t operator()(int64_t a, int64_t b) const { return a > b ? a : b; }
-};
-struct OpMin {
-    __device__ int64_t operator()(int64_t a, int64_t b) const { return a < b ? a : b; }
-};
-
-// Exclusive scan over the threads of the block (prefix: threads before, suffix:
-// threads after) of one int64 per thread; *total gets the whole reduction.
-// `lds` must hold NT/64 entries.  Contains two block barriers.
-template <int NT, bool SUFFIX, typename Op>
-__device__ int64_t block_scan_excl(int64_t v, int64_t ident, Op op, int64_t* total, int64_t* lds)
-{
-    const int lane = lane_id(), wid = wave_id();
-    int64_t x = v;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        int64_t o = SUFFIX ? __shfl_down(x, d, 64) : __shfl_up(x, d, 64);
-        bool ok = SUFFIX ? (lane + d < 64) : (lane >= d);
-        if (ok) x = op(x, o);
-    }
-    int64_t ex = SUFFIX ? __shfl_down(x, 1, 64) : __shfl_up(x, 1, 64);
-    if (SUFFIX ? lane == 63 : lane == 0) ex = ident;
-    if (SUFFIX ? lane == 0 : lane == 63) lds[wid] = x;
-    __syncthreads();
-    int64_t carry = ident, tot = ident;
-#pragma unroll
-    for (int j = 0; j < NT / 64; ++j) {
-        int64_t t = lds[j];
-        tot = op(tot, t);
-        if (SUFFIX ? j > wid : j < wid) carry = op(carry, t);
-    }
-    __syncthreads();
-    *total = tot;
-    return op(carry, ex);
-}
-
-template <int NT, typename Op>
-__device__ int64_t block_reduce(int64_t v, int64_t ident, Op op, int64_t* lds)
-{
-    int64_t tot;
-    block_scan_excl<NT, false>(v, ident, op, &tot, lds);
-    return tot;
-}
-
-// first index in [lo, hi) with a[i] >= x (hi if none)
-__device__ __forceinline__ int lower_bound_i32(const int32_t* a, int lo, int hi, int32_t x)
-{
-    int len = hi - lo;
-    while (len > 0) {
-        int half = len >> 1;
-        int mid = lo + half;
-        if (a[mid] < x) {
-            lo = mid + 1;
-            len = len - half - 1;
-        } else {
-            len = half;
-        }
-    }
-    return lo;
-}
-
-// Algorithm 1 order: does (ka, a) rank strictly before (kb, b)?  An index < 0
-// marks an absent entry, which ranks after every present one.
-__device__ __forceinline__ bool ranks_before(uint64_t ka, int a, uint64_t kb, int b)
-{
-    const bool better = (ka > kb) | ((ka == kb) & (a < b));
-    return (a >= 0) & ((b < 0) | better);
-}
-
-// Insert candidate (ck, cw) into a best-first list of N entries (cw < 0: no-op).
-// Written as a compare-exchange chain of selects: no divergent branch touches
-// the register-resident list.
-template <int N>
-__device__ __forceinline__ void topk_insert(uint64_t (&key)[N], int32_t (&idx)[N], uint64_t ck, int32_t cw)
-{
-#pragma unroll
-    for (int k = 0; k < N; ++k) {
-        const bool sw = ranks_before(ck, cw, key[k], idx[k]);
-        const uint64_t ok = key[k];
-        const int32_t ow = idx[k];
-        key[k] = sw ? ck : ok;
-        idx[k] = sw ? cw : ow;
-        ck = sw ? ok : ck;
-        cw = sw ? ow : cw;
-    }
-}
-
-// Keep the two smallest (excess, index) pairs, ordered by excess ascending and
-// then index descending.  y < 0: no candidate.
-__device__ __forceinline__ void min2_insert(int32_t& ex1, int32_t& w1, int32_t& ex2, int32_t& w2, int32_t x, int32_t y)
-{
-    const bool present = y >= 0;
-    const bool b1 = present & ((w1 < 0) | (x < ex1) | ((x == ex1) & (y > w1)));
-    const bool b2 = present & !b1 & ((w2 < 0) | (x < ex2) | ((x == ex2) & (y > w2)));
-    ex2 = b1 ? ex1 : (b2 ? x : ex2);
-    w2 = b1 ? w1 : (b2 ? y : w2);
-    ex1 = b1 ? x : ex1;
-    w1 = b1 ? y : w1;
-}
-
-__device__ __forceinline__ bool near_tie(double x, double y)
-{
-    double m = fmax(fabs(x), fabs(y));
-    return fabs(x - y) <= 1e-9 * m;
-}
-
-// Everything a pair evaluation needs from one worker.
-struct View {
-    const int32_t* e;
-    const int4* pms;
-    int32_t head, n, M;
-    int64_t DS, S1, S2;
-    uint64_t key;
-    double rhs;
-};
-
-// Integer forms of a built worker's latency checks (see State).
-struct Thr {
-    int64_t dq_max, ntd_lo, ntd_hi;
-    int32_t lthr, ntt_lo, ntt_hi;
-};
-
-__device__ __forceinline__ Thr load_thr(const State& st, int gw)
-{
-    Thr t;
-    t.dq_max = st.dq_max[gw];
-    t.ntd_lo = st.ntd_lo[gw];
-    t.ntd_hi = st.ntd_hi[gw];
-    t.lthr = st.lthr[gw];
-    t.ntt_lo = st.ntt_lo[gw];
-    t.ntt_hi = st.ntt_hi[gw];
-    return t;
-}
-
-__device__ __forceinline__ View load_view(const State& st, int gw, int32_t hb)
-{
-    View v;
-    const int64_t base = st.slot_base[gw];
-    v.e = st.e + base;
-    v.pms = st.pms + base;
-    v.head = st.head[gw];
-    v.n = st.n[gw];
-    v.M = st.M[gw];
-    v.DS = st.DS[gw];
-    const bool cur = st.hbs[gw] == hb;
-    v.S1 = cur ? st.S1[gw] : 0;
-    v.S2 = cur ? st.S2[gw] : 0;
-    v.key = st.key[gw];
-    v.rhs = st.rhs[gw];
-    return v;
-}
-
-// KV demand peak of the worker with the query (sq = l_in - tau, eq = l_pred + tau) added.
-__device__ __forceinline__ int64_t kv_peak_with(const View& v, int32_t sq, int32_t eq)
-{
-    const int l = lower_bound_i32(v.e, v.head, v.n, eq);
-    const int4 t = v.pms[l];
-    const int64_t a = (int64_t)t.x + sq;
-    const int64_t b = (int64_t)t.y;
-    const int64_t c = (int64_t)t.z + (int64_t)(v.n - l) * eq + sq + eq;
-    int64_t p = a > b ? a : b;
-    return p > c ? p : c;
-}
-
-struct Latency {
-    double lhs, ttft, tdec;
-    bool dec_ok, ttft_ok, nt;
-};
-
-// Left side of constraint (b) for a worker whose DS with the query added is x
-// (sum of D = x * 2^-gs exactly).
-__device__ __forceinline__ double dec_lhs(const Scen& sc, int64_t x) { return sc.k2 * ldexp((double)x, -sc.gs); }
-
-// Prefill time of constraint (c) for TTFT sums S1, S2 that include the query.
-__device__ __forceinline__ double ttft_of(const Scen& sc, int64_t S1, int64_t S2)
-{
-    return (sc.c1 + sc.k1 * (double)S1) + sc.k1q * (double)S2;
-}
-
-// Decode constraint (b) and TTFT constraint (c) of one pair.
-__device__ __forceinline__ Latency latency(const Scen& sc, const View& v, int32_t lin, int32_t lp, int32_t b)
-{
-    Latency o;
-    const int64_t DSq = v.DS + ((int64_t)lin << sc.gs) + (int64_t)sc.gn * lp;
-    o.lhs = dec_lhs(sc, DSq);
-    o.dec_ok = o.lhs <= v.rhs;
-    o.ttft = ttft_of(sc, v.S1 + lin, v.S2 + (int64_t)lin * lin);
-    o.ttft_ok = o.ttft <= sc.ttft;
-    o.nt = near_tie(o.lhs, v.rhs) || near_tie(o.ttft, sc.ttft);
-    o.tdec = (sc.c3 + sc.c2 * (double)b) + o.lhs;
-    return o;
-}
-
-// Lanes (of the active ones) where p holds.  Takes the predicate as a bool, so
-// that a compare result feeds the mask directly.
-__device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
-
-// Largest x in [lo, hi] for which `pred` holds, where pred holds on a prefix of
-// [lo, hi]; lo - 1 if it holds nowhere.  The 64 lanes of the wave test 64
-// evenly spaced points per step, so a range of 2^36 takes six steps.  All
-// lanes of the wave must call it; all get the result.
-template <typename F>
-__device__ int64_t wave_last_true(int64_t lo, int64_t hi, F pred)
-{
-    int64_t a = lo - 1, b = hi;  // the answer lies in [a, b]
-    while (a < b) {
-        const int64_t step = (b - a + 63) >> 6;
-        const int64_t x = a + step * (lane_id() + 1);
-        const bool t = x <= b && pred(x);
-        const int cnt = __popcll(ballot(t));
-        a += step * cnt;
-        const int64_t nb = a + step - 1;
-        b = nb < b ? nb : b;
-    }
-    return a;
-}
-
-// Half-width of an interval around y that holds every x with near_tie(x, y):
-// near_tie gives |x - y| <= 1e-9 max(|x|, |y|) up to rounding, which implies
-// |x - y| < 1.0000002e-9 |y|; the extra 25% covers the rounding of y +- width.
-__device__ __forceinline__ double tie_band(double y) { return 1.25e-9 * fabs(y); }
-
-// Scenario owning block `blk` given each scenario's first block (field offset).
-template <int32_t Scen::*FIRST>
-__device__ __forceinline__ int find_scen(const State& st, int blk)
-{
-    int lo = 0, hi = st.S - 1;
-    while (lo < hi) {
-        int mid = (lo + hi + 1) >> 1;
-        if (st.scen[mid].*FIRST <= blk) lo = mid; else hi = mid - 1;
-    }
-    return lo;
-}
-
-__device__ __forceinline__ int find_scen_by_worker(const State& st, int gw)
-{
-    int lo = 0, hi = st.S - 1;
-    while (lo < hi) {
-        int mid = (lo + hi + 1) >> 1;
-        if (st.scen[mid].wbase <= gw) lo = mid; else hi = mid - 1;
-    }
-    return lo;
-}
-
-__device__ __forceinline__ void raise_error(int32_t* err, int32_t code)
-{
-    atomicCAS(err, 0, code);
-}
-
-// ---- cross-lane primitives (readlane and DPP; no LDS permutes)
-
-// Read a lane's value (uniform result).
-__device__ __forceinline__ int32_t rdlane(int32_t v, int l) { return __builtin_amdgcn_readlane(v, l); }
-__device__ __forceinline__ uint64_t rdlane64(uint64_t v, int l)
-{
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
-    return ((uint64_t)hi << 32) | lo;
-}
-__device__ __forceinline__ int64_t rdlane64s(int64_t v, int l) { return (int64_t)rdlane64((uint64_t)v, l); }
-__device__ __forceinline__ double rdlane_f64(double v, int l)
-{
-    return __builtin_bit_cast(double, rdlane64(__builtin_bit_cast(uint64_t, v), l));
-}
-
-// Inclusive scan over the 64 lanes (lane 0 first) with DPP row shifts and row
-// broadcasts; lanes without a source keep the identity.
-template <typename Op>
-__device__ __forceinline__ int32_t wave_incl_scan(int32_t x, int32_t ident, Op op)
-{
-    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x111, 0xf, 0xf, false));  // row_shr:1
-    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x112, 0xf, 0xf, false));  // row_shr:2
-    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x114, 0xf, 0xf, false));  // row_shr:4
-    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x118, 0xf, 0xf, false));  // row_shr:8
-    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x142, 0xa, 0xf, false));  // row_bcast:15
-    x = op(x, __builtin_amdgcn_update_dpp(ident, x, 0x143, 0xc, 0xf, false));  // row_bcast:31
-    return x;
-}
-struct Add32 {
-    __device__ int32_t operator()(int32_t a, int32_t b) const { return a + b; }
-};
-struct Or32 {
-    __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a | b; }
-};
-struct Max32 {
-    __device__ int32_t operator()(int32_t a, int32_t b) const { return a > b ? a : b; }
-};
-__device__ __forceinline__ int32_t wave_sum32(int32_t v) { return rdlane(wave_incl_scan(v, 0, Add32()), 63); }
-__device__ __forceinline__ int32_t wave_max32(int32_t v) { return rdlane(wave_incl_scan(v, INT32_MIN, Max32()), 63); }
-__device__ __forceinline__ uint64_t wave_or64(uint64_t v)
-{
-    const uint32_t lo = (uint32_t)rdlane((int32_t)wave_incl_scan((int32_t)(uint32_t)v, 0, Or32()), 63);
-    const uint32_t hi = (uint32_t)rdlane((int32_t)wave_incl_scan((int32_t)(uint32_t)(v >> 32), 0, Or32()), 63);
-    return ((uint64_t)hi << 32) | lo;
-}
-__device__ __forceinline__ int64_t wave_sum64(int64_t v)
-{
-#pragma unroll
-    for (int d = 32; d > 0; d >>= 1) v += __shfl_xor(v, d, 64);
-    return v;
-}
-
 
 // ---------------------------------------------------------------------------------------------
 // Breakpoint summaries of one worker (whole block).  Drops finished requests
@@ -343,6 +34,40 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
     int4* pms = st.pms + base;
     const int n = st.n[gw];
     int head = st.head[gw];
+
+    // Constraint (d): bring the worker's slack gain phi up to the current
+    // heartbeat.  Each heartbeat since the last update ran one decode iteration
+    // over the requests live at its start (e >= that iteration's tau; nothing
+    // is placed between heartbeats without a build), taking Eq. 3's time.
+    double phi = 0.0;
+    if (sc.use_d) {
+        phi = st.phi[gw];
+        const int pending = hb - st.phi_hb[gw];
+        if (pending < 0 || pending > 8) {
+            if (tid == 0) raise_error(err, DEV_EINVAL);
+        } else {
+            for (int p = 0; p < pending; ++p) {
+                const int32_t tk = tau - pending + p;
+                int64_t cnt = 0, ssum = 0;
+                for (int k = head + tid; k < n; k += NT) {
+                    const bool in = e[k] >= tk;
+                    cnt += in ? 1 : 0;
+                    ssum += in ? s[k] : 0;
+                }
+                cnt = block_reduce<NT>(cnt, 0, OpAdd(), red);
+                ssum = block_reduce<NT>(ssum, 0, OpAdd(), red);
+                if (cnt > 0) {
+                    const int64_t ctx = ssum + cnt * (int64_t)tk;  // sum of the contexts c = s + tau
+                    const double t_iter = (sc.c3 + sc.c2 * (double)cnt) + sc.k2 * (double)ctx;
+                    phi = phi + (sc.tdec - t_iter);
+                }
+            }
+            if (tid == 0) {
+                st.phi[gw] = phi;
+                st.phi_hb[gw] = hb;
+            }
+        }
+    }
 
     // finished requests form a prefix of the live range (sorted by e)
     int64_t fin = 0;
@@ -386,6 +111,41 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
         const int64_t Pe = P + e[k];
         runpm = Pe > runpm ? Pe : runpm;
     }
+    // Constraint (d)'s limit: drop finished requests from the worker's log and
+    // take theta * the smallest slack of the ongoing ones (placed before this
+    // heartbeat).  In place, 256 entries at a time: every entry of a chunk is
+    // read before any kept one is written, and kept entries only move down.
+    double dl = INFINITY;
+    if (sc.use_d) {
+        int32_t* lge = st.lge + base;
+        int32_t* lgw = st.lgw + base;
+        double* lgs = st.lgs + base;
+        const int L0 = st.lgn[gw];
+        int wpos = 0;
+        double mn = INFINITY;
+        for (int c0 = 0; c0 < L0; c0 += NT) {
+            const int k = c0 + tid;
+            const bool in = k < L0;
+            const int32_t ek = in ? lge[k] : 0, wk = in ? lgw[k] : 0;
+            const double sk = in ? lgs[k] : 0.0;
+            const bool keep = in && ek >= tau;
+            if (keep && wk < hb) mn = fmin(mn, sk);
+            int64_t kept;
+            const int pos = (int)block_scan_excl<NT, false>(keep ? 1 : 0, 0, OpAdd(), &kept, red);
+            if (keep) {
+                lge[wpos + pos] = ek;
+                lgw[wpos + pos] = wk;
+                lgs[wpos + pos] = sk;
+            }
+            wpos += (int)kept;
+            __syncthreads();
+        }
+        mn = double_of(block_reduce<NT>(ord_of(mn), ord_of(INFINITY), OpMin(), red));
+        if (mn != INFINITY) dl = sc.theta * (mn + phi);
+        if (tid == 0) st.lgn[gw] = wpos;
+    }
+    if (tid == 0) st.dlim[gw] = dl;
+
     const int64_t SC = tot_s + (int64_t)B * tau;
     const int64_t SR = tot_e - (int64_t)B * tau;
     const int64_t DS = (SC << sc.gs) + (int64_t)sc.gn * SR;
@@ -463,7 +223,8 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
         const int64_t S2 = cur ? st.S2[gw] : 0;
         auto tt = [&](int64_t l) { return ttft_of(sc, S1 + l, S2 + l * l); };
         if (wv == 2) {
-            const int64_t l = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) <= sc.ttft; });
+            // (c) and (d) bound the same prefill time
+            const int64_t l = wave_last_true(1, LMAX, [&](int64_t v) { const double t = tt(v); return t <= sc.ttft && t <= dl; });
             if (l0) st.lthr[gw] = (int32_t)l;
         } else {
             const double band = tie_band(sc.ttft);
@@ -478,6 +239,18 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
                 st.ntt_mask[gw] = width <= 64 ? mask : 0;
                 if (width > 64 && sc.ntint) raise_error(err, DEV_EOVERFLOW);
             }
+            // the band of (d)'s limit (empty without one)
+            int64_t pl = 1, ph = 0;
+            if (dl != INFINITY) {
+                const double pband = tie_band(dl);
+                const double plo = dl - pband, phi_ = dl + pband;
+                pl = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) < plo; }) + 1;
+                ph = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) <= phi_; });
+            }
+            if (l0) {
+                st.ntp_lo[gw] = (int32_t)pl;
+                st.ntp_hi[gw] = (int32_t)ph;
+            }
         }
     }
     __syncthreads();
@@ -489,7 +262,7 @@ constexpr int SORT_MAX = 4096;
 
 __global__ __launch_bounds__(BUILD_THREADS) void k_ingest(State st, const int64_t* res_off,
                                                           const int32_t* lin, const int32_t* lpred,
-                                                          const int32_t* gen)
+                                                          const int32_t* gen, const double* tdec)
 {
     constexpr int NT = BUILD_THREADS;
     __shared__ uint64_t keys[SORT_MAX];
@@ -506,7 +279,8 @@ __global__ __launch_bounds__(BUILD_THREADS) void k_ingest(State st, const int64_
     int64_t bad = 0, tot = 0;
     for (int k = tid; k < R; k += NT) {
         const int32_t a = lin[r0 + k], p = lpred[r0 + k], g = gen[r0 + k];
-        const bool ok = a >= 1 && p >= 1 && a <= LIM && p <= LIM && g >= 0 && g < p;
+        const bool ok = a >= 1 && p >= 1 && a <= LIM && p <= LIM && g >= 0 && g < p &&
+                        (tdec == nullptr || (isfinite(tdec[r0 + k]) && tdec[r0 + k] >= 0.0));
         bad += ok ? 0 : 1;
         tot += ok ? ((int64_t)a + p) : 0;  // sum of (c + r), an upper bound of the KV peak
     }
@@ -561,6 +335,17 @@ __global__ __launch_bounds__(BUILD_THREADS) void k_ingest(State st, const int64_
             s[pos] = (int32_t)(x & 0xffffffffu);
         }
     }
+    if (tdec != nullptr) {
+        // constraint (d)'s log, in input order: phi = 0 at load, so each
+        // resident's entry holds its slack T_dec * g - t_dec
+        const Scen& sc = st.scen[0];
+        for (int k = tid; k < R; k += NT) {
+            const int32_t p = lpred[r0 + k], g = gen[r0 + k];
+            st.lge[base + k] = p - g;  // e at tau = 0
+            st.lgw[base + k] = -1;
+            st.lgs[base + k] = sc.tdec * (double)g - tdec[r0 + k];
+        }
+    }
     if (tid == 0) {
         st.n[gw] = R;
         st.head[gw] = 0;
@@ -568,6 +353,7 @@ __global__ __launch_bounds__(BUILD_THREADS) void k_ingest(State st, const int64_
         st.S1[gw] = 0;
         st.S2[gw] = 0;
         st.hbs[gw] = -1;
+        st.lgn[gw] = tdec != nullptr ? R : 0;
     }
 }
 
@@ -604,8 +390,9 @@ struct WInfo {
     double rhs;
     int64_t dq_max, ntd_lo, ntd_hi;
     uint64_t ntd_mask, ntt_mask;
-    int32_t head, n, M, lthr, ntt_lo, ntt_hi;
+    int32_t head, n, M, lthr, ntt_lo, ntt_hi, ntp_lo, ntp_hi;  // (head, n, M, lthr: one 16-byte read)
     int32_t nt_any;  // some query of the block's chunk may have a near-tie margin with this worker
+    double dlim;
 };
 
 __device__ __forceinline__ View winfo_view(const State& st, const WInfo& wi)
@@ -621,6 +408,7 @@ __device__ __forceinline__ View winfo_view(const State& st, const WInfo& wi)
     v.S2 = wi.S2;
     v.key = 0;
     v.rhs = wi.rhs;
+    v.dlim = wi.dlim;
     return v;
 }
 
@@ -845,7 +633,8 @@ __device__ __forceinline__ void near_tie_words(const State& st, const Scen& sc, 
             const uint32_t dl = (uint32_t)(lin[m] - wi.ntt_lo);
             nt = (dd < 64 && ((wi.ntd_mask >> dd) & 1)) || (dl < 64 && ((wi.ntt_mask >> dl) & 1));
         } else {
-            const bool maybe = (qD >= wi.ntd_lo && qD <= wi.ntd_hi) || (lin[m] >= wi.ntt_lo && lin[m] <= wi.ntt_hi);
+            const bool maybe = (qD >= wi.ntd_lo && qD <= wi.ntd_hi) || (lin[m] >= wi.ntt_lo && lin[m] <= wi.ntt_hi) ||
+                               (lin[m] >= wi.ntp_lo && lin[m] <= wi.ntp_hi);
             nt = maybe && latency(sc, v, lin[m], lp[m], B + 1).nt;
         }
         const uint64_t bn = ballot(act[m] && nt);
@@ -955,9 +744,13 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
         x.ntt_hi = st.ntt_hi[gw];
         x.ntd_mask = st.ntd_mask[gw];
         x.ntt_mask = st.ntt_mask[gw];
+        // constraint (d) never runs with the integer near-tie sets (mode 2)
+        x.dlim = MODE == 2 ? INFINITY : st.dlim[gw];
+        x.ntp_lo = MODE == 2 ? 1 : st.ntp_lo[gw];
+        x.ntp_hi = MODE == 2 ? 0 : st.ntp_hi[gw];
         // a near-tie margin needs some query of the chunk inside a tie band
         x.nt_any = MODE == 0 || (qr.qdmax >= x.ntd_lo && qr.qdmin <= x.ntd_hi) ||
-                   (qr.lnmax >= x.ntt_lo && qr.lnmin <= x.ntt_hi);
+                   (qr.lnmax >= x.ntt_lo && qr.lnmin <= x.ntt_hi) || (qr.lnmax >= x.ntp_lo && qr.lnmin <= x.ntp_hi);
         Wi[tid] = x;
     }
     __syncthreads();
@@ -1194,870 +987,6 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
 }
 
 // ---------------------------------------------------------------------------------------------
-// Commit.  One wave per scenario walks the tile in arrival order.  Workers
-// committed to earlier in the tile ("dirty") are re-evaluated from their live
-// aggregates, kept in LDS; the worker last committed to keeps its live request
-// columns in LDS.  A commit updates the columns in LDS, writes them through to
-// HBM and only marks the worker's summaries stale: the build kernel of the next
-// round rebuilds them.  Columns this wave wrote are read back only with
-// device-coherent loads after a release fence.
-
-constexpr int DBITS_W = 2048;  // dirty bitmap words in LDS: scenarios of up to 65536 workers
-
-// Lane holding the best (key, index) by Algorithm 1's order among lanes with
-// `valid`, or -1.  A scalar walk over the (few) candidate lanes.
-__device__ __forceinline__ int wave_best_lane(uint64_t key, int32_t w, bool valid)
-{
-    uint64_t m = ballot(valid);
-    int best = -1;
-    uint64_t bk = 0;
-    int32_t bw = -1;
-    while (m) {
-        const int l = __ffsll((unsigned long long)m) - 1;
-        m &= m - 1;
-        const uint64_t k = rdlane64(key, l);
-        const int32_t ww = rdlane(w, l);
-        if (ranks_before(k, ww, bk, bw)) {
-            best = l;
-            bk = k;
-            bw = ww;
-        }
-    }
-    return best;
-}
-
-// Column element: plain LDS read, or a device-coherent global read of data
-// that this wave may have written earlier in the launch.
-template <bool GLOBAL>
-__device__ __forceinline__ int32_t col(const int32_t* p, int k)
-{
-    if (GLOBAL) return __hip_atomic_load(p + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return p[k];
-}
-
-// KV demand peak with the query added, from a worker's live columns e, s
-// (B entries sorted by e).  All lanes take part; all get the result, and the
-// worker's peak without the query in *p0.  Lane l takes chunk 63 - l, so a
-// prefix over lanes is a suffix over slots.  Every value here is a KV demand
-// below 2^31 (the worker's peak is at most 2^30, the query adds l_in + l_pred).
-template <bool GLOBAL>
-__device__ int64_t wave_kv_peak(const int32_t* e, const int32_t* s, int B, int32_t sq, int32_t eq, int32_t* p0)
-{
-    const int lane = lane_id();
-    const int CH = (B + 63) >> 6;
-    const int c = 63 - lane;
-    const int k0 = min(B, c * CH);
-    const int k1 = min(B, k0 + CH);
-    int32_t ls = 0;
-    for (int k = k0; k < k1; ++k) ls += col<GLOBAL>(s, k);
-    int64_t run = (int64_t)(wave_incl_scan(ls, 0, Add32()) - ls);  // slots after this chunk
-    int32_t best = INT32_MIN, best0 = 0, ssge = 0, cge = 0;
-    for (int k = k1 - 1; k >= k0; --k) {
-        const int32_t ek = col<GLOBAL>(e, k), sk = col<GLOBAL>(s, k);
-        run += sk;  // sum of s over slots >= k
-        const int64_t P = run + (int64_t)(B - k) * ek;
-        const bool before = ek < eq;  // the query is still alive at this end point
-        const int32_t val = (int32_t)(before ? P + sq + ek : P);
-        best = val > best ? val : best;
-        best0 = (int32_t)P > best0 ? (int32_t)P : best0;
-        ssge += before ? 0 : sk;
-        cge += before ? 0 : 1;
-    }
-    *p0 = wave_max32(best0);
-    const int64_t bmax = wave_max32(best);
-    const int64_t own = (int64_t)wave_sum32(ssge) + (int64_t)wave_sum32(cge) * eq + sq + eq;
-    return bmax > own ? bmax : own;
-}
-
-// The same, evaluated by one lane alone.
-template <bool GLOBAL>
-__device__ int64_t lane_kv_peak(const int32_t* e, const int32_t* s, int B, int32_t sq, int32_t eq)
-{
-    int64_t run = 0, best = INT64_MIN, ssge = 0, cge = 0;
-    for (int k = B - 1; k >= 0; --k) {
-        const int32_t ek = col<GLOBAL>(e, k), sk = col<GLOBAL>(s, k);
-        run += sk;
-        const int64_t P = run + (int64_t)(B - k) * ek;
-        const bool before = ek < eq;
-        const int64_t val = before ? P + sq + ek : P;
-        best = val > best ? val : best;
-        ssge += before ? 0 : sk;
-        cge += before ? 0 : 1;
-    }
-    const int64_t own = ssge + cge * eq + sq + eq;
-    return best > own ? best : own;
-}
-
-// Orders LDS traffic between the lanes of the (single-wave) commit block
-// without waiting for outstanding global memory operations.
-__device__ __forceinline__ void wave_sync() { __builtin_amdgcn_wave_barrier(); }
-
-// A worker committed to earlier in the tile.  The commit wave holds the j-th
-// such worker in lane j's registers.
-struct DAgg {
-    int32_t w;       // scenario-local index, -1 = none
-    int32_t B, n, head, M, hbs;
-    int32_t empty0;  // it was empty when the tile started
-    int32_t cap;
-    int32_t pub;     // upper bound of its KV peak without a new query (exact after a scan)
-    int32_t pad;
-    int64_t base;    // first slot
-    int64_t DS, S1, S2, SC, SR;
-    uint64_t key;
-    double rhs;
-};
-
-// Bit words of the tile-start feasibility / near-tie masks that cover one
-// 64-query window, cached per dirty worker (one worker per lane).
-struct WinBits {
-    uint64_t f0, f1, n0, n1;
-};
-
-__device__ __forceinline__ WinBits load_win_bits(const State& st, const Scen& sc, int w, int start, int w0, int end)
-{
-    WinBits b;
-    const int64_t g0 = (w0 - start) >> 6;
-    const int64_t row0 = sc.bits_off + g0 * sc.W + w;
-    b.f0 = st.bits_feas[row0];
-    b.n0 = st.bits_nt[row0];
-    const bool two = (int64_t)(end - start) > (g0 + 1) * 64;
-    b.f1 = two ? st.bits_feas[row0 + sc.W] : 0;
-    b.n1 = two ? st.bits_nt[row0 + sc.W] : 0;
-    return b;
-}
-
-// bit of query i (tile offset) in a cached window
-__device__ __forceinline__ bool win_bit(uint64_t lo, uint64_t hi, int start, int w0, int i)
-{
-    const int g = ((i - start) >> 6) - ((w0 - start) >> 6);
-    const uint64_t word = g == 0 ? lo : hi;
-    return (word >> ((i - start) & 63)) & 1;
-}
-
-__device__ __forceinline__ View dagg_view(const DAgg& a, int32_t hb)
-{
-    View v;
-    v.e = nullptr;
-    v.pms = nullptr;
-    v.head = a.head;
-    v.n = a.n;
-    v.M = a.M;
-    v.DS = a.DS;
-    const bool cur = a.hbs == hb;
-    v.S1 = cur ? a.S1 : 0;
-    v.S2 = cur ? a.S2 : 0;
-    v.key = a.key;
-    v.rhs = a.rhs;
-    return v;
-}
-
-// Per-launch commit state held in LDS.  dag[] mirrors the lanes' DAgg for the
-// per-lane diagnostics of rejected queries (diagnostics only); dw[] and dbits
-// say which workers are dirty.
-struct CommitLDS {
-    DAgg dag[MAX_DIRTY];
-    int32_t dw[MAX_DIRTY];
-    uint32_t dbits[DBITS_W];
-    int32_t he[HOT];
-    int32_t hs[HOT];
-};
-
-// Is worker w (scenario-local) dirty in this tile?  (any lane, any w)
-__device__ __forceinline__ bool dirty_w(const CommitLDS& L, int W, int nd, int w)
-{
-    if (W <= DBITS_W * 32) return (L.dbits[w >> 5] >> (w & 31)) & 1u;
-    bool d = false;
-    for (int j = 0; j < nd; ++j) d = d | (L.dw[j] == w);
-    return d;
-}
-
-// Lane holding dirty worker w (wave-uniform w; -1 if w is not dirty).
-__device__ __forceinline__ int dirty_lane(const DAgg& a, int w)
-{
-    const uint64_t m = ballot(a.w == w && w >= 0);
-    return m ? __ffsll((unsigned long long)m) - 1 : -1;
-}
-
-// Lowest-index worker at or after `from` that is empty and untouched in this
-// tile (wave-cooperative; -1 if none).  Empty workers have rank key 0.
-__device__ int next_empty_worker(const State& st, const Scen& sc, const CommitLDS& L, int nd, int from)
-{
-    for (int base = from; base < sc.W; base += 64) {
-        const int w = base + lane_id();
-        const bool emp = w < sc.W && st.key[sc.wbase + w] == 0 && !dirty_w(L, sc.W, nd, w);
-        const uint64_t m = ballot(emp);
-        if (m) return base + __ffsll((unsigned long long)m) - 1;
-    }
-    return -1;
-}
-
-struct QView {  // the committing query's summary, broadcast to the whole wave
-    uint64_t tkey[TOPK];
-    int32_t tw[TOPK];
-    uint64_t ntkey;
-    int32_t ntw, ntcnt, nfeas, ncand, efeas, ex1, w1, ex2, w2;
-};
-
-__device__ __forceinline__ QView broadcast_q(const QSum& q, int p)
-{
-    QView v;
-#pragma unroll
-    for (int k = 0; k < TOPK; ++k) {
-        v.tkey[k] = rdlane64(q.tkey[k], p);
-        v.tw[k] = rdlane(q.tw[k], p);
-    }
-    v.ntkey = rdlane64(q.ntkey, p);
-    v.ntw = rdlane(q.ntw, p);
-    v.ntcnt = rdlane(q.ntcnt, p);
-    v.nfeas = rdlane(q.nfeas, p);
-    v.ncand = rdlane(q.ncand, p);
-    v.efeas = rdlane(q.efeas, p);
-    v.ex1 = rdlane(q.ex1, p);
-    v.w1 = rdlane(q.w1, p);
-    v.ex2 = rdlane(q.ex2, p);
-    v.w2 = rdlane(q.w2, p);
-    return v;
-}
-
-// Diagnostics of a query with no feasible worker at tile start (so none now),
-// decided by its own lane (diagnostics only: reads the LDS mirror of the dirty
-// workers).
-__device__ Diag reject_diag(const State& st, const Scen& sc, const QSum& q, int i, int start, int w0, int32_t lin,
-                            int32_t lp, int32_t tau, int32_t hb, const CommitLDS& L, int nd, int hot,
-                            const WinBits& wb, int* abort)
-{
-    Diag d;
-    d.n_feasible = 0;
-    d.kv_peak_chosen = 0;
-    d.ttft_chosen = 0.0;
-    d.tdec_chosen = 0.0;
-    d.kv_excess_min = 0;
-    d.near_tie = 0;
-    *abort = 0;
-    const int32_t sq = lin - tau, eq = lp + tau;
-    int64_t exmin = q.ex1;
-    if (q.w1 >= 0 && dirty_w(L, sc.W, nd, q.w1)) {
-        if (q.w2 >= 0 && dirty_w(L, sc.W, nd, q.w2)) {
-            *abort = 1;
-            return d;
-        }
-        int j = 0;
-        while (j < nd && L.dw[j] != q.w1) ++j;
-        const DAgg& a = L.dag[j];
-        const int64_t base = a.base + a.head;
-        const int64_t pk = (j == hot) ? lane_kv_peak<false>(L.he, L.hs, a.B, sq, eq)
-                                      : lane_kv_peak<true>(st.e + base, st.s + base, a.B, sq, eq);
-        const int64_t ex_now = pk - a.M;
-        exmin = q.w2 < 0 ? ex_now : (ex_now < q.ex2 ? ex_now : (int64_t)q.ex2);
-    }
-    d.kv_excess_min = exmin;
-    // near tie over every worker (the query is rejected)
-    int clean_nt = q.ntcnt;
-    bool nt = false;
-    for (int j = 0; j < nd; ++j) {
-        const DAgg& a = L.dag[j];
-        const uint64_t n0 = rdlane64(wb.n0, j), n1 = rdlane64(wb.n1, j);
-        clean_nt -= win_bit(n0, n1, start, w0, i) ? 1 : 0;
-        nt = nt | latency(sc, dagg_view(a, hb), lin, lp, a.B + 1).nt;
-    }
-    nt = nt | (clean_nt > 0);
-    d.near_tie = nt ? 1 : 0;
-    return d;
-}
-
-struct Decision {
-    int32_t w;      // chosen worker, -1 = rejected
-    int32_t lane;   // dirty lane holding w, -1 when w was untouched in the tile
-    int32_t abort;  // the tile-start lists cannot decide this query exactly
-    Diag d;
-};
-
-// Exact KV scans a decision ran, per lane.
-struct Scan {
-    bool done;   // this lane's worker was scanned for the query
-    int32_t pk;  // its KV peak with the query
-    int32_t p0;  // its KV peak without
-};
-
-// Number of entries of the sorted a[0, n) that are <= x.
-__device__ __forceinline__ int upper_bound_i32(const int32_t* a, int n, int32_t x)
-{
-    int lo = 0, len = n;
-    while (len > 0) {
-        const int half = len >> 1;
-        const bool right = a[lo + half] <= x;
-        lo = right ? lo + half + 1 : lo;
-        len = right ? len - half - 1 : half;
-    }
-    return lo;
-}
-
-// Insert (x, y) into the sorted LDS columns he/hs[0, B), after every entry
-// with he <= x (whole wave; the columns must have room for B + 1 entries).
-__device__ __forceinline__ void lds_sorted_insert(CommitLDS& L, int B, int32_t x, int32_t y)
-{
-    const int lane = lane_id();
-    int u = 0;
-    for (int k0 = 0; k0 < B; k0 += COMMIT_THREADS)
-        u += __popcll(ballot(k0 + lane < B && L.he[k0 + lane] <= x));
-    // shift [u, B) up by one, highest block first (each pass reads before it writes)
-    for (int top = B; top > u; top -= COMMIT_THREADS) {
-        const int k = top - COMMIT_THREADS + lane;
-        const bool mv = k >= u && k < top;
-        int32_t ve = 0, vs = 0;
-        if (mv) {
-            ve = L.he[k];
-            vs = L.hs[k];
-        }
-        wave_sync();
-        if (mv) {
-            L.he[k + 1] = ve;
-            L.hs[k + 1] = vs;
-        }
-        wave_sync();
-    }
-    if (lane == 0) {
-        L.he[u] = x;
-        L.hs[u] = y;
-    }
-    wave_sync();
-}
-
-// The hot worker's LDS columns are a sorted prefix [0, Bs) and, without
-// diagnostics, an unsorted tail [Bs, Bs + m) of requests committed since it
-// became hot, in commit order.  Sort the tail into the prefix (in commit order,
-// so equal end points keep the order a sorted insert would give them).
-__device__ __noinline__ int lds_merge_tail(CommitLDS& L, int Bs, int m)
-{
-    for (int t = 0; t < m; ++t) {
-        const int32_t x = L.he[Bs + t], y = L.hs[Bs + t];  // read before the insert may move it
-        lds_sorted_insert(L, Bs + t, x, y);
-    }
-    return Bs + m;
-}
-
-// KV peak with the query for dirty lane bl (whole wave): the hot worker's
-// columns from LDS (its tail sorted in first), the others from HBM.
-__device__ __forceinline__ int64_t dirty_kv_peak(const State& st, CommitLDS& L, const DAgg& a, int bl, int hot,
-                                                 int& hotBs, int& hotm, int32_t sq, int32_t eq, int32_t* p0)
-{
-    const int32_t cB = rdlane(a.B, bl);
-    if (bl == hot) {
-        if (hotm > 0) {
-            hotBs = lds_merge_tail(L, hotBs, hotm);
-            hotm = 0;
-        }
-        return wave_kv_peak<false>(L.he, L.hs, cB, sq, eq, p0);
-    }
-    const int64_t base = rdlane64s(a.base, bl) + rdlane(a.head, bl);
-    return wave_kv_peak<true>(st.e + base, st.s + base, cB, sq, eq, p0);
-}
-
-// Decide one query with the whole wave.  `a` is this lane's dirty worker.
-__device__ Decision decide(const State& st, const Scen& sc, const QView& q, int i, int start, int w0, int32_t lin,
-                           int32_t lp, int32_t tau, int32_t hb, CommitLDS& L, int nd, int hot, int& hotBs,
-                           int& hotm, int next_empty, bool want_diag, const WinBits& wb, const DAgg& a, Scan& sn)
-{
-    Decision r;
-    r.w = -1;
-    r.lane = -1;
-    r.abort = 0;
-    r.d.n_feasible = 0;
-    r.d.near_tie = 0;
-    r.d.kv_peak_chosen = 0;
-    r.d.kv_excess_min = 0;
-    r.d.ttft_chosen = 0.0;
-    r.d.tdec_chosen = 0.0;
-    sn.done = false;
-    sn.pk = sn.p0 = 0;
-    const int lane = lane_id();
-    const int32_t sq = lin - tau, eq = lp + tau;
-    // best untouched candidate from the tile-start list
-    bool have = false;
-    uint64_t bk = 0;
-    int32_t bw = -1;
-    const int lim = q.ncand < TOPK ? q.ncand : TOPK;
-#pragma unroll
-    for (int k = 0; k < TOPK; ++k) {
-        const int w = q.tw[k];
-        const bool listed = (k < lim) && (w >= 0);
-        const bool clean = listed && dirty_lane(a, w) < 0;
-        const bool take = clean & !have;
-        bk = take ? q.tkey[k] : bk;
-        bw = take ? w : bw;
-        have = have | take;
-    }
-    if (!have && q.ncand > TOPK) {
-        r.abort = 1;
-        return r;
-    }
-    if (!have && sc.uniform_M && q.efeas && next_empty >= 0) {
-        have = true;
-        bk = 0;
-        bw = next_empty;
-    }
-    // workers changed earlier in the tile: one per lane
-    const bool valid = lane < nd;
-    bool fs = false, ns = false;
-    Latency Lt;
-    Lt.dec_ok = Lt.ttft_ok = Lt.nt = false;
-    Lt.lhs = Lt.ttft = Lt.tdec = 0.0;
-    if (valid) {
-        fs = (sc.uniform_M && a.empty0) ? (q.efeas != 0) : win_bit(wb.f0, wb.f1, start, w0, i);
-        ns = win_bit(wb.n0, wb.n1, start, w0, i);
-        Lt = latency(sc, dagg_view(a, hb), lin, lp, a.B + 1);
-    }
-    const bool unknown = valid && fs && Lt.dec_ok && Lt.ttft_ok;  // KV check still needed
-
-    if (!want_diag) {
-        // best-ranked first, stop at the first feasible one; a worker whose peak
-        // bound plus the query's own demand fits needs no scan (the query adds at
-        // most l_in + l_pred to the demand at any iteration)
-        bool cand = unknown && ranks_before(a.key, a.w, bk, bw);
-        const bool sure = cand && (int64_t)a.pub + lin + lp <= (int64_t)a.M;
-        for (;;) {
-            const int bl = wave_best_lane(a.key, a.w, cand);
-            if (bl < 0) break;
-            if ((ballot(sure) >> bl) & 1) {
-                r.w = rdlane(a.w, bl);
-                r.lane = bl;
-                return r;
-            }
-            int32_t p0;
-            const int64_t pk = dirty_kv_peak(st, L, a, bl, hot, hotBs, hotm, sq, eq, &p0);
-            if (lane == bl) {
-                sn.done = true;
-                sn.pk = (int32_t)pk;
-                sn.p0 = p0;
-                cand = false;
-            }
-            if (pk <= rdlane(a.M, bl)) {
-                r.w = rdlane(a.w, bl);
-                r.lane = bl;
-                return r;
-            }
-        }
-        r.w = have ? bw : -1;
-        return r;
-    }
-
-    // ---- with diagnostics: every dirty candidate is scanned
-    bool cand = unknown;
-    bool feas_now = false;
-    for (;;) {
-        const int bl = wave_best_lane(a.key, a.w, cand);
-        if (bl < 0) break;
-        int32_t p0;
-        const int64_t pk = dirty_kv_peak(st, L, a, bl, hot, hotBs, hotm, sq, eq, &p0);
-        const bool ok = pk <= rdlane(a.M, bl);
-        if (lane == bl) {
-            cand = false;
-            feas_now = ok;
-            sn.done = true;
-            sn.pk = (int32_t)pk;
-            sn.p0 = p0;
-        }
-    }
-    const bool fdirty = valid && feas_now;
-    {
-        const int bl = wave_best_lane(a.key, a.w, fdirty);
-        if (bl >= 0) {
-            const uint64_t dk = rdlane64(a.key, bl);
-            const int32_t dw = rdlane(a.w, bl);
-            if (!have || ranks_before(dk, dw, bk, bw)) {
-                have = true;
-                bk = dk;
-                bw = dw;
-                r.lane = bl;
-            }
-        }
-    }
-    r.w = have ? bw : -1;
-    r.d.n_feasible = q.nfeas - __popcll(ballot(valid && fs)) + __popcll(ballot(fdirty));
-    // smallest KV excess
-    int64_t exmin = q.ex1;
-    const int j1 = dirty_lane(a, q.w1);
-    if (q.w1 >= 0 && j1 >= 0) {
-        if (q.w2 >= 0 && dirty_lane(a, q.w2) >= 0) {
-            r.abort = 1;
-            return r;
-        }
-        int32_t p0;
-        const int64_t pk = dirty_kv_peak(st, L, a, j1, hot, hotBs, hotm, sq, eq, &p0);
-        const int64_t ex_now = pk - rdlane(a.M, j1);
-        exmin = q.w2 < 0 ? ex_now : (ex_now < q.ex2 ? ex_now : (int64_t)q.ex2);
-    }
-    r.d.kv_excess_min = exmin;
-    // near tie among workers ranked at or above the choice (all when rejected)
-    const int clean_nt = q.ntcnt - __popcll(ballot(valid && ns));
-    bool nt = false;
-    if (clean_nt > 0) {
-        if (q.ntw >= 0 && dirty_lane(a, q.ntw) < 0) {
-            nt = r.w < 0 || !ranks_before(bk, bw, q.ntkey, q.ntw);
-        } else if (r.w < 0) {
-            nt = true;
-        } else {
-            r.abort = 1;
-            return r;
-        }
-    }
-    const bool dnt = valid && Lt.nt && (r.w < 0 || !ranks_before(bk, bw, a.key, a.w));
-    nt = nt | (ballot(dnt) != 0);
-    r.d.near_tie = nt ? 1 : 0;
-    // the chosen worker's figures
-    if (r.w >= 0) {
-        if (r.lane >= 0) {
-            r.d.kv_peak_chosen = rdlane(sn.pk, r.lane);
-            r.d.ttft_chosen = rdlane_f64(Lt.ttft, r.lane);
-            r.d.tdec_chosen = rdlane_f64(Lt.tdec, r.lane);
-        } else {
-            // untouched in this tile: its summaries are current
-            const View v = load_view(st, sc.wbase + r.w, hb);
-            const Latency Lc = latency(sc, v, lin, lp, v.n - v.head + 1);
-            r.d.kv_peak_chosen = kv_peak_with(v, sq, eq);
-            r.d.ttft_chosen = Lc.ttft;
-            r.d.tdec_chosen = Lc.tdec;
-        }
-    }
-    return r;
-}
-
-// Write the hot worker's LDS columns back to its slot range in sorted order
-// (from slot 0 when the range would run past the worker's last slot) and
-// point its aggregates at them.  A prefix entry moves up by the number of tail
-// entries ending strictly before it; a tail entry lands after every prefix
-// entry ending no later and after earlier tail entries ending no later.  Whole
-// wave.
-__device__ void writeback_hot(const State& st, CommitLDS& L, DAgg& a, int hot, int Bs, int m, bool mirror)
-{
-    const int lane = lane_id();
-    const int B = Bs + m;
-    const int cap = rdlane(a.cap, hot);
-    const int head0 = rdlane(a.head, hot);
-    const int head = head0 + B <= cap ? head0 : 0;
-    int32_t* ge = st.e + rdlane64s(a.base, hot) + head;
-    int32_t* gs = st.s + rdlane64s(a.base, hot) + head;
-    for (int k0 = 0; k0 < Bs; k0 += COMMIT_THREADS) {
-        const int k = k0 + lane;
-        const bool in = k < Bs;
-        const int32_t x = in ? L.he[k] : 0, y = in ? L.hs[k] : 0;
-        int cnt = 0;
-        for (int t0 = 0; t0 < m; t0 += COMMIT_THREADS) {
-            const int32_t tv = t0 + lane < m ? L.he[Bs + t0 + lane] : INT32_MAX;
-            const int lim = min(COMMIT_THREADS, m - t0);
-            for (int jj = 0; jj < lim; ++jj) cnt += rdlane(tv, jj) < x ? 1 : 0;
-        }
-        if (in) {
-            ge[k + cnt] = x;
-            gs[k + cnt] = y;
-        }
-    }
-    for (int t0 = 0; t0 < m; t0 += COMMIT_THREADS) {
-        const int t = t0 + lane;
-        const bool in = t < m;
-        const int32_t x = in ? L.he[Bs + t] : 0, y = in ? L.hs[Bs + t] : 0;
-        int pos = upper_bound_i32(L.he, Bs, x);
-        for (int u0 = 0; u0 < m; u0 += COMMIT_THREADS) {
-            const int32_t tv = u0 + lane < m ? L.he[Bs + u0 + lane] : INT32_MAX;
-            const int lim = min(COMMIT_THREADS, m - u0);
-            for (int jj = 0; jj < lim; ++jj) {
-                const int32_t v = rdlane(tv, jj);
-                pos += (v < x || (v == x && u0 + jj < t)) ? 1 : 0;
-            }
-        }
-        if (in) {
-            ge[pos] = x;
-            gs[pos] = y;
-        }
-    }
-    if (lane == hot) {
-        a.head = head;
-        a.n = head + B;
-        if (mirror) L.dag[hot] = a;
-    }
-}
-
-template <bool DIAG>
-__global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
-{
-    constexpr int NT = COMMIT_THREADS;
-    const int s = find_scen<&Scen::fin_blk0>(st, blockIdx.x);
-    const Scen sc = st.scen[s];
-    const int part = blockIdx.x - sc.fin_blk0;  // 0: one block per scenario
-    const TileInfo ti = st.tinfo[s];
-    Ctl* cp = st.ctl + s;
-    const int lane = threadIdx.x;
-    // the control block as the host will read it (after the stream synchronises)
-    auto publish = [&]() {
-        if (st.ctl_host != nullptr && part == 0 && lane == 0) st.ctl_host[s] = *cp;
-    };
-    if (st.qbad != nullptr && *st.qbad) {  // an invalid query length: nothing is written
-        if (part == 0 && lane == 0) cp->err = DEV_EINVAL;
-        publish();
-        return;
-    }
-    if (ti.start >= ti.end) {
-        publish();
-        return;
-    }
-    const int32_t start = ti.start, end = ti.end;
-    const int32_t fpc = min(st.tinfo[s].first_pc[ti.parity & 1], end);  // (no local copy indexed at run time)
-
-    // ---- the sequential wave
-    const Ctl c = *cp;
-    if (c.err) {
-        publish();
-        return;
-    }
-    const int32_t tau = c.tau, hb = c.hb_index;
-    __shared__ CommitLDS L;
-    if (sc.W <= DBITS_W * 32)
-        for (int k = lane; k < (sc.W + 31) / 32; k += NT) L.dbits[k] = 0u;
-    if (lane == 0) cp->rebuild = 0;
-    wave_sync();
-    constexpr bool want_diag = DIAG;  // st.out_diag != nullptr
-    int nd = 0;    // dirty workers (wave-uniform); lane j < nd holds the j-th in `a`
-    DAgg a;
-    a.w = -1;
-    a.B = a.n = a.head = a.M = a.hbs = a.empty0 = a.cap = a.pub = a.pad = 0;
-    a.base = 0;
-    a.DS = a.S1 = a.S2 = a.SC = a.SR = 0;
-    a.key = 0;
-    a.rhs = 0.0;
-    // The hot worker's sorted live columns are in L.he / L.hs and its HBM copy
-    // is stale until it is written back (when another worker becomes hot, and at
-    // the end); every other dirty worker's columns are current in HBM and are
-    // read with device-coherent loads after the write-back's release fence.
-    int hot = -1;
-    int hotBs = 0, hotm = 0;  // the hot worker's sorted prefix and unsorted tail in L.he / L.hs
-    // lowest-index empty untouched worker, looked up only when a decision can
-    // use it (-2 = not looked up yet; the search resumes at next_from)
-    int next_empty = sc.uniform_M ? -2 : -1;
-    int next_from = 0;
-    int pos = fpc;
-    bool cut = false, err = false;
-    int commits = 0;
-    int nrej = fpc - start;  // the rejected prefix (its outputs come from the selection kernel)
-    int firstrej = fpc > start ? start : INT32_MAX;
-    WinBits wb;
-    wb.f0 = wb.f1 = wb.n0 = wb.n1 = 0;
-    while (pos < end && !cut) {
-        // one window of 64 queries; `cur` is the first undecided lane
-        const int w0 = pos;
-        const int i = w0 + lane;
-        const bool act = i < end;
-        QSum q;
-        int32_t lin = 1, lp = 1;
-        if (act) {
-            q = st.qsum[sc.qsum_off + (i - start)];
-            lin = st.q_lin[i];
-            lp = st.q_lpred[i];
-        } else {
-            q.nfeas = 0;
-        }
-        if (lane < nd) wb = load_win_bits(st, sc, a.w, start, w0, end);
-        const uint64_t potm = ballot(act && q.nfeas > 0);
-        int cur = 0;
-        while (cur < NT && w0 + cur < end) {
-            const uint64_t pm = potm & (~0ull << cur);
-            const int p = pm ? __ffsll((unsigned long long)pm) - 1 : NT;
-            // lanes cur..p-1: rejected whatever happened earlier in the tile
-            Diag dr;
-            int ab = 0;
-            const bool mine = act && lane >= cur && lane < p;
-            if (want_diag && mine) dr = reject_diag(st, sc, q, i, start, w0, lin, lp, tau, hb, L, nd, hot, wb, &ab);
-            const uint64_t am = ballot(mine && ab);
-            const int abl = am ? __ffsll((unsigned long long)am) - 1 : NT;
-            const int lim = min(p, abl);
-            if (act && lane >= cur && lane < lim) {
-                if (st.out_worker) st.out_worker[sc.out_off + i] = -1;
-                if (want_diag) st.out_diag[i] = dr;
-            }
-            const uint64_t rm = ballot(act && lane >= cur && lane < lim);
-            nrej += __popcll(rm);
-            if (rm && firstrej == INT32_MAX) firstrej = w0 + __ffsll((unsigned long long)rm) - 1;
-            if (abl < p) {
-                pos = w0 + abl;
-                cut = true;
-                break;
-            }
-            if (p >= NT) {
-                cur = NT;
-                break;
-            }
-            // the query of lane p, decided by the whole wave
-            const int ip = w0 + p;
-            const QView qv = broadcast_q(q, p);
-            const int32_t plin = rdlane(lin, p), plp = rdlane(lp, p);
-            if (next_empty == -2 && qv.efeas) next_empty = next_empty_worker(st, sc, L, nd, next_from);
-            Scan sn;
-            const Decision dc = decide(st, sc, qv, ip, start, w0, plin, plp, tau, hb, L, nd, hot, hotBs, hotm,
-                                       next_empty, want_diag, wb, a, sn);
-            if (dc.abort) {
-                pos = ip;
-                cut = true;
-                break;
-            }
-            if (lane == 0) {
-                if (st.out_worker) st.out_worker[sc.out_off + ip] = dc.w;
-                if (want_diag) st.out_diag[ip] = dc.d;
-            }
-            cur = p + 1;
-            // a scanned worker that does not take the query keeps its exact peak
-            if (sn.done && lane != dc.lane) a.pub = sn.p0;
-            if (dc.w < 0) {
-                nrej += 1;
-                if (firstrej == INT32_MAX) firstrej = ip;
-                continue;
-            }
-
-            // ---- commit the query to worker w
-            const int w = dc.w;
-            int j = dc.lane;
-            if (j < 0) {  // first commit to w in this tile: its tile-start state is in HBM
-                j = nd;
-                const int gw = sc.wbase + w;
-                if (lane == j) {
-                    a.w = w;
-                    a.n = st.n[gw];
-                    a.head = st.head[gw];
-                    a.B = st.B[gw];
-                    a.M = st.M[gw];
-                    a.hbs = st.hbs[gw];
-                    a.empty0 = a.B == 0 ? 1 : 0;
-                    a.cap = st.cap[gw];
-                    a.pub = a.B == 0 ? 0 : st.peak[gw];
-                    a.base = st.slot_base[gw];
-                    a.DS = st.DS[gw];
-                    a.S1 = st.S1[gw];
-                    a.S2 = st.S2[gw];
-                    a.SC = st.SC[gw];
-                    a.SR = st.SR[gw];
-                    a.key = st.key[gw];
-                    a.rhs = st.rhs[gw];
-                    wb = load_win_bits(st, sc, w, start, w0, end);
-                }
-                if (lane == 0) {
-                    L.dw[j] = w;
-                    if (sc.W <= DBITS_W * 32) L.dbits[w >> 5] |= 1u << (w & 31);
-                }
-                nd += 1;
-            }
-            const int B0 = rdlane(a.B, j);
-            if (B0 + 1 > rdlane(a.cap, j)) {  // no slot left for one more live request
-                if (lane == 0) raise_error(&cp->err, DEV_ESLOTS);
-                err = true;
-                cut = true;
-                pos = ip + 1;
-                break;
-            }
-            if (hot != j) {
-                if (hot >= 0) {
-                    writeback_hot(st, L, a, hot, hotBs, hotm, want_diag);
-                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-                }
-                const int64_t gb = rdlane64s(a.base, j) + rdlane(a.head, j);
-                for (int k = lane; k < B0; k += NT) {
-                    L.he[k] = col<true>(st.e + gb, k);
-                    L.hs[k] = col<true>(st.s + gb, k);
-                }
-                hot = j;
-                hotBs = B0;
-                hotm = 0;
-            }
-            wave_sync();
-            const int32_t eq = plp + tau, sq = plin - tau;
-            if (want_diag) {
-                // the per-lane diagnostics of rejected queries read sorted columns
-                lds_sorted_insert(L, B0, eq, sq);
-                hotBs = B0 + 1;
-            } else {
-                if (lane == 0) {
-                    L.he[B0] = eq;
-                    L.hs[B0] = sq;
-                }
-                hotm += 1;
-                wave_sync();
-            }
-            // aggregates of lane j
-            if (lane == j) {
-                const int B1 = B0 + 1;
-                a.B = B1;
-                a.SC += plin;
-                a.SR += plp;
-                a.DS += ((int64_t)plin << sc.gs) + (int64_t)sc.gn * plp;
-                const int64_t X = (int64_t)B1 << sc.gs;
-                if (a.DS >= ((int64_t)1 << 31) || X >= ((int64_t)1 << 31)) raise_error(&cp->err, DEV_EOVERFLOW);
-                a.key = (uint64_t)(X * X) + (uint64_t)(a.DS * a.DS);
-                a.rhs = sc.theta * ((sc.tdec - sc.c3) - sc.c2 * (double)(B1 + 1));
-                const bool curhb = a.hbs == hb;
-                a.S1 = (curhb ? a.S1 : 0) + plin;
-                a.S2 = (curhb ? a.S2 : 0) + (int64_t)plin * plin;
-                a.hbs = hb;
-                if (a.S2 >= ((int64_t)1 << 53)) raise_error(&cp->err, DEV_EOVERFLOW);
-                // exact peak when this decision scanned the worker, else a bound
-                a.pub = sn.done ? sn.pk : (int32_t)((int64_t)a.pub + plin + plp);
-                if (want_diag) L.dag[j] = a;
-            }
-            wave_sync();
-            ++commits;
-            if (w == next_empty) {
-                next_empty = -2;
-                next_from = w + 1;
-            }
-            if (nd >= MAX_DIRTY && w0 + cur < end) {
-                pos = w0 + cur;
-                cut = true;
-                break;
-            }
-        }
-        if (err) break;
-        if (!cut) pos = min(end, w0 + NT);
-    }
-    // write back the hot worker's columns and every dirty worker's aggregates;
-    // list the workers whose summaries the next round must rebuild
-    if (hot >= 0) writeback_hot(st, L, a, hot, hotBs, hotm, false);
-    if (lane < nd) {
-        const int gw = sc.wbase + a.w;
-        st.n[gw] = a.n;
-        st.head[gw] = a.head;
-        st.B[gw] = a.B;
-        st.SC[gw] = a.SC;
-        st.SR[gw] = a.SR;
-        st.DS[gw] = a.DS;
-        st.key[gw] = a.key;
-        st.rhs[gw] = a.rhs;
-        st.S1[gw] = a.S1;
-        st.S2[gw] = a.S2;
-        st.hbs[gw] = a.hbs;
-        st.built[gw] = 0;
-        st.dlist[s * MAX_DIRTY + lane] = gw;
-    }
-    if (lane == 0) {
-        if (nrej) atomicAdd(&cp->n_rej, nrej);
-        if (firstrej != INT32_MAX) atomicMin(&cp->first_rej, firstrej);
-        st.dcount[s] = nd;
-        cp->ndirty = nd;
-        const int32_t processed = pos - c.start;
-        const int32_t since = c.since_hb + processed;
-        if (pos == end && c.H > 0 && since >= c.H) {
-            cp->tau = c.tau + 1;
-            cp->hb_index = c.hb_index + 1;
-            cp->since_hb = 0;
-            cp->rebuild = 1;
-        } else {
-            cp->since_hb = since;
-        }
-        cp->start = pos;
-        cp->aborts = c.aborts + (cut ? 1 : 0);
-        cp->commits = c.commits + commits;
-        cp->round = c.round + 1;
-        st.tinfo[s].first_pc[(c.round + 1) & 1] = INT32_MAX;
-    }
-    publish();
-}
-
-// ---------------------------------------------------------------------------------------------
 // Query validation for one call: any length outside [1, 2^24] sets the error
 // word of every scenario, which makes every later kernel of the call a no-op.
 __global__ __launch_bounds__(256) void k_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q,
@@ -2105,9 +1034,9 @@ __global__ void k_sweep_outputs(State st, int32_t* rejected, int32_t* first_reje
 
 // ---------------------------------------------------------------------------------------------
 hipError_t launch_ingest(const State& st, int32_t W, const int64_t* res_off, const int32_t* lin,
-                         const int32_t* lpred, const int32_t* gen, hipStream_t stream)
+                         const int32_t* lpred, const int32_t* gen, const double* tdec, hipStream_t stream)
 {
-    hipLaunchKernelGGL(k_ingest, dim3(W), dim3(BUILD_THREADS), 0, stream, st, res_off, lin, lpred, gen);
+    hipLaunchKernelGGL(k_ingest, dim3(W), dim3(BUILD_THREADS), 0, stream, st, res_off, lin, lpred, gen, tdec);
     return hipGetLastError();
 }
 
@@ -2138,15 +1067,6 @@ hipError_t launch_eval(const State& st, int32_t blocks, int mode, hipStream_t st
 hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream)
 {
     hipLaunchKernelGGL(k_select, dim3(blocks), dim3(SEL_THREADS), 0, stream, st);
-    return hipGetLastError();
-}
-
-hipError_t launch_commit(const State& st, int32_t blocks, hipStream_t stream)
-{
-    if (st.out_diag != nullptr)
-        hipLaunchKernelGGL(k_commit<true>, dim3(blocks), dim3(COMMIT_THREADS), 0, stream, st);
-    else
-        hipLaunchKernelGGL(k_commit<false>, dim3(blocks), dim3(COMMIT_THREADS), 0, stream, st);
     return hipGetLastError();
 }
 

@@ -266,6 +266,64 @@ def test_near_tie_sets_with_integer_forms(aladdin, seed):
         compare(w, d, s, want, "integer near-tie sets, tile %d" % tile)
 
 
+# ----------------------------------------------------------------------------- constraint (d)
+@pytest.mark.parametrize("tile", [64, 4096])
+def test_decode_history_matches_oracle(aladdin, tile):
+    t = wl.with_decode_history(wl.make_config("medium"), 7)
+    want = ref.place_trace(t)
+    assert 0 < int((want.worker >= 0).sum()) < 719  # the limit binds on part of the pool
+    compare(*gpu_place(aladdin, t, tile=tile), want, "history medium tile %d" % tile)
+
+
+def test_decode_history_without_diagnostics_same_choices(aladdin):
+    t = wl.with_decode_history(wl.make_config("medium"), 8, 0.0, 0.6)
+    w, _, s = gpu_place(aladdin, t, tile=256, diag=False)
+    compare(w, None, s, ref.place_trace(t), "history no diag")
+
+
+@pytest.mark.parametrize("tile", [64, 256, 4096])
+def test_decode_history_across_heartbeats(aladdin, tile):
+    # slack grows at every heartbeat and new requests join the ongoing set;
+    # calls end on and between heartbeats
+    t = wl.with_decode_history(wl.make_trace("hbhist", 23, W=16, R=24, Q=700, kv_capacity=20000,
+                                             model=wl.BASE_MODEL, heartbeat_every=37), 9)
+    want = ref.place_trace(t)
+    assert int((want.worker >= 0).sum()) > 50
+    cuts = [(0, 37), (37, 74), (74, 100), (100, 333), (333, 370), (370, 700)]
+    compare(*gpu_place(aladdin, t, tile=tile, chunks=cuts), want, "history hb tile %d" % tile)
+    compare(*gpu_place(aladdin, t, tile=tile), want, "history hb one call tile %d" % tile)
+
+
+def test_decode_history_fp64_checks(aladdin):
+    # a negative prefill coefficient: every pair takes the fp64 checks
+    m = dataclasses.replace(wl.BASE_MODEL, k1=-1e-6, k1q=2e-9)
+    t = wl.with_decode_history(wl.make_trace("hbneg", 24, W=12, R=16, Q=500, kv_capacity=20000, model=m,
+                                             heartbeat_every=25), 10)
+    compare(*gpu_place(aladdin, t, tile=64), ref.place_trace(t), "history fp64")
+
+
+def test_decode_history_near_tie(aladdin):
+    # the resident saved 2 * 0.5 - 0.5 = 0.5 s; a prefill of 0.25 * 2 = 0.5 s meets
+    # constraint (d) exactly (feasible, flagged)
+    m = wl.Model(c1=0.0, k1=0.25, k1q=0.0, c3=0.0, c2=0.0, k2=1e-9, ttft_slo=100.0, decode_slo=0.5)
+    t = _trace(2, 10 ** 6, [[(4, 8, 2)], []], [(2, 3), (3, 3), (1, 1)], model=m)
+    t = dataclasses.replace(t, res_t_dec=np.array([0.5]))
+    want = ref.place_trace(t)
+    assert want.near_tie[0] == 1 and want.worker[0] == 0
+    compare(*gpu_place(aladdin, t, tile=64, slots=16), want, "history near tie")
+
+
+def test_invalid_decode_history_is_rejected(aladdin):
+    t = wl.make_config("tiny")
+    for bad in (-1.0, float("nan"), float("inf")):
+        td = np.full(t.n_resident, 0.1)
+        td[3] = bad
+        ev = aladdin.Evaluator(0)
+        with pytest.raises(aladdin.AladdinError):
+            ev.load_trace(dataclasses.replace(t, res_t_dec=td))
+        ev.close()
+
+
 def test_slots_exhausted_is_reported(aladdin):
     t = _trace(1, 10 ** 6, [[]], [(3, 2)] * 50)
     ev = aladdin.Evaluator(0, tile=64)
