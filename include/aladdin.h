@@ -91,9 +91,10 @@ typedef struct {
 
 /* Per-query diagnostics (40 bytes, device array of Q). */
 typedef struct {
-    int32_t n_feasible;        /* workers meeting (b), (c), (e) for this query */
+    int32_t n_feasible;        /* workers meeting (b), (c), (e) (and (d) with a decode
+                                  history) for this query */
     int32_t near_tie;          /* 1 if a worker ranked at or above the choice (every worker
-                                  when rejected) has a decode or TTFT margin within 1e-9
+                                  when rejected) has a decode, TTFT or (d) margin within 1e-9
                                   relative: fp64 rounding could have decided it */
     int64_t kv_peak_chosen;    /* KV peak of the chosen worker with q added (0 if rejected) */
     int64_t kv_excess_min;     /* min over all workers of (KV peak with q) - capacity */
