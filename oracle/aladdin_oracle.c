@@ -59,6 +59,10 @@
  *  (s0): slack = s0 + phi.  A request placed in heartbeat window h starts
  *  decoding at the end of h with zero slack, so s0 = -phi at placement (phi
  *  does not change within a window).
+ *
+ *  Algorithm 2 (ora_rebalance, at the end of this file): per-worker errors of
+ *  the output-length predictions and greedy moves of the new requests that
+ *  lower the summed distance of the workers' error lines from the origin.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -482,4 +486,117 @@ int64_t ora_kv_peak(int64_t n, const int64_t* c, const int64_t* r)
     int64_t p = kv_peak(&w, 0, 0, 0);
     free(w.c); free(w.r); free(w.s0); free(w.win);
     return p;
+}
+
+/* ------------------------------------------------------------------ */
+/*
+ * Algorithm 2 (Sec. 4.3): re-balancing new requests against output-length
+ * prediction errors.
+ *
+ * Error of each worker i, from its ongoing requests j (the two tests of the
+ * algorithm, applied literally):
+ *   l_out_j > l_pred_j (still decoding past its prediction, under-estimate):
+ *       l^e_i += l'^pred_j (the re-predicted output length),  b^e_i += 1
+ *   l_real_j < l_pred_j (finished before its prediction, over-estimate):
+ *       l^e_i += l_real_j - l_pred_j,                          b^e_i -= 1
+ * Error line: Eq. 4 bounds k2 * (context) + c2 * (batch); the errors shift a
+ * worker's operating point by (l^e, b^e), which moves its decode time by
+ * k2 * l^e + c2 * b^e.  Divided by k2 (the distance of a line from the origin
+ * does not change when all its coefficients are scaled) this is
+ *   c_i = l^e_i + rho * b^e_i,   rho = c2 / k2 rounded to whole tokens,
+ * and the distance of worker i's error line from the origin is
+ * |c_i| / sqrt(1 + rho^2).  The objective is the sum over workers.
+ * Moving a new request j (predicted length l_pred_j) from worker x to worker
+ * y changes c_x by -(l_pred_j + rho) and c_y by +(l_pred_j + rho).
+ * Search (the paper gives only the objective): repeatedly apply the single
+ * move with the largest decrease of sum |c_i| -- ties to the lowest request
+ * index, then the lowest target worker -- while that decrease is positive;
+ * a request moves at most once.  New requests that were not placed (worker
+ * -1) stay where they are.  Everything is int64, so the choices are exact.
+ *
+ * Inputs: W workers; n_old ongoing requests (worker, l_pred, l_out = tokens
+ * generated so far, l_real = real output length, with l_out <= l_real, and
+ * l_repred = the re-prediction); n_new new requests (l_pred, worker in/out).
+ * Outputs (any may be NULL): final l^e, b^e per worker; number of moves; the
+ * moves in order (request, target); sum |c_i| before and after.
+ */
+static int64_t rb_abs(int64_t v) { return v < 0 ? -v : v; }
+
+int64_t ora_rebalance_rho(const ora_model_t* m)
+{
+    if (!(m->k2 > 0.0) || !(m->c2 >= 0.0) || !isfinite(m->c2 / m->k2) || m->c2 / m->k2 > 1e9) return -1;
+    return (int64_t)llrint(m->c2 / m->k2);
+}
+
+int ora_rebalance(int32_t W, const ora_model_t* m,
+                  int32_t n_old, const int32_t* old_worker, const int32_t* old_lpred, const int32_t* old_lout,
+                  const int32_t* old_lreal, const int32_t* old_lrepred,
+                  int32_t n_new, const int32_t* new_lpred, int32_t* new_worker,
+                  int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t* out_log,
+                  int64_t* out_obj_before, int64_t* out_obj_after)
+{
+    const int32_t LMAX = 1 << 24;
+    if (W < 1 || n_old < 0 || n_new < 0 || !m || !new_worker) return ORA_EINVAL;
+    const int64_t rho = ora_rebalance_rho(m);
+    if (rho < 0) return ORA_EINVAL;
+    for (int32_t j = 0; j < n_old; ++j) {
+        if (old_worker[j] < 0 || old_worker[j] >= W) return ORA_EINVAL;
+        if (old_lpred[j] < 1 || old_lpred[j] > LMAX || old_lout[j] < 0 || old_lreal[j] < 1 ||
+            old_lreal[j] > LMAX || old_lout[j] > old_lreal[j] || old_lrepred[j] < 0 || old_lrepred[j] > LMAX)
+            return ORA_EINVAL;
+    }
+    for (int32_t j = 0; j < n_new; ++j)
+        if (new_lpred[j] < 1 || new_lpred[j] > LMAX || new_worker[j] < -1 || new_worker[j] >= W) return ORA_EINVAL;
+
+    int64_t* le = (int64_t*)calloc((size_t)W, sizeof(int64_t));
+    int64_t* be = (int64_t*)calloc((size_t)W, sizeof(int64_t));
+    char* moved = (char*)calloc((size_t)(n_new > 0 ? n_new : 1), 1);
+    if (!le || !be || !moved) { free(le); free(be); free(moved); return ORA_ENOMEM; }
+
+    /* the per-worker errors of the ongoing requests */
+    for (int32_t j = 0; j < n_old; ++j) {
+        const int32_t i = old_worker[j];
+        if (old_lout[j] > old_lpred[j]) { le[i] += old_lrepred[j]; be[i] += 1; }
+        if (old_lreal[j] < old_lpred[j]) { le[i] += (int64_t)old_lreal[j] - old_lpred[j]; be[i] -= 1; }
+    }
+#define RB_C(i) (le[i] + rho * be[i])
+    int64_t obj = 0;
+    for (int32_t i = 0; i < W; ++i) obj += rb_abs(RB_C(i));
+    if (out_obj_before) *out_obj_before = obj;
+
+    /* greedy moves: every (unmoved placed request, other worker) pair, in
+     * request-then-worker order, keeping the first largest decrease */
+    int32_t moves = 0;
+    for (;;) {
+        int64_t best = 0;
+        int32_t bj = -1, by = -1;
+        for (int32_t j = 0; j < n_new; ++j) {
+            const int32_t x = new_worker[j];
+            if (moved[j] || x < 0) continue;
+            const int64_t d = (int64_t)new_lpred[j] + rho;
+            const int64_t cx = RB_C(x);
+            for (int32_t y = 0; y < W; ++y) {
+                if (y == x) continue;
+                const int64_t cy = RB_C(y);
+                const int64_t gain = (rb_abs(cx) + rb_abs(cy)) - (rb_abs(cx - d) + rb_abs(cy + d));
+                if (gain > best) { best = gain; bj = j; by = y; }
+            }
+        }
+        if (bj < 0) break;
+        const int32_t x = new_worker[bj];
+        le[x] -= new_lpred[bj]; be[x] -= 1;
+        le[by] += new_lpred[bj]; be[by] += 1;
+        new_worker[bj] = by;
+        moved[bj] = 1;
+        if (out_log) { out_log[2 * moves] = bj; out_log[2 * moves + 1] = by; }
+        moves += 1;
+        obj -= best;
+    }
+#undef RB_C
+    if (out_obj_after) *out_obj_after = obj;
+    if (out_moves) *out_moves = moves;
+    if (out_le) memcpy(out_le, le, (size_t)W * sizeof(int64_t));
+    if (out_be) memcpy(out_be, be, (size_t)W * sizeof(int64_t));
+    free(le); free(be); free(moved);
+    return ORA_OK;
 }

@@ -62,6 +62,11 @@ def lib():
         L.ora_sweep.restype = ctypes.c_int
         L.ora_kv_peak.argtypes = [i64, P, P]
         L.ora_kv_peak.restype = i64
+        L.ora_rebalance_rho.argtypes = [ctypes.POINTER(OraModel)]
+        L.ora_rebalance_rho.restype = i64
+        L.ora_rebalance.argtypes = [i32, ctypes.POINTER(OraModel), i32, P, P, P, P, P, i32, P, P, P, P, P, P,
+                                    P, P]
+        L.ora_rebalance.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -164,3 +169,43 @@ def min_gpus(scenarios, rejected):
             if best is None or g < best:
                 best, idx = g, i
     return best, idx
+
+
+@dataclass
+class RebalanceResult:
+    worker: np.ndarray      # int32 [n_new] worker of each new request after the moves
+    le: np.ndarray          # int64 [W] output-length error per worker after the moves
+    be: np.ndarray          # int64 [W] batch-size error per worker after the moves
+    moves: np.ndarray       # int32 [n_moves, 2] (request, target worker) in the order applied
+    obj_before: int         # sum over workers of |l^e + rho * b^e| before the moves
+    obj_after: int
+    rho: int
+
+
+def rebalance_rho(model) -> int:
+    return int(lib().ora_rebalance_rho(ctypes.byref(to_model(model))))
+
+
+def rebalance(W, model, old_worker, old_l_pred, old_l_out, old_l_real, old_l_repred, new_l_pred,
+              new_worker) -> RebalanceResult:
+    """Algorithm 2 on explicit arrays (the new requests' workers are not modified)."""
+    L = lib()
+    c32 = lambda a: np.ascontiguousarray(a, dtype=np.int32)
+    ow, op, oo, orl, orp = (c32(a) for a in (old_worker, old_l_pred, old_l_out, old_l_real, old_l_repred))
+    nlp = c32(new_l_pred)
+    nw = np.array(new_worker, dtype=np.int32, copy=True)
+    n_old, n_new = len(ow), len(nlp)
+    le = np.zeros(W, np.int64)
+    be = np.zeros(W, np.int64)
+    log = np.zeros(2 * max(n_new, 1), np.int32)
+    nm = ctypes.c_int32(0)
+    ob = ctypes.c_int64(0)
+    oa = ctypes.c_int64(0)
+    m = to_model(model)
+    rc = L.ora_rebalance(int(W), ctypes.byref(m), n_old, _ptr(ow), _ptr(op), _ptr(oo), _ptr(orl), _ptr(orp),
+                         n_new, _ptr(nlp), _ptr(nw), _ptr(le), _ptr(be), ctypes.byref(nm), _ptr(log),
+                         ctypes.byref(ob), ctypes.byref(oa))
+    if rc != ORA_OK:
+        raise RuntimeError("oracle ora_rebalance failed with code %d" % rc)
+    k = nm.value
+    return RebalanceResult(nw, le, be, log[:2 * k].reshape(k, 2), ob.value, oa.value, rebalance_rho(model))

@@ -355,3 +355,170 @@ def test_invalid_inputs_rejected():
         run(1, 10, [[(3, 2, 2)]], FREE, [(1, 1)])   # g must be < l_pred
     with pytest.raises(RuntimeError):
         run(1, 10, [[]], FREE, [(0, 1)])            # l_in >= 1
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 2 (Sec. 4.3): re-balancing against output-length prediction errors
+
+def _rb_model(c2=1e-4, k2=2e-7):
+    return wl.Model(c1=0.0, k1=0.0, k1q=0.0, c3=0.0, c2=c2, k2=k2, ttft_slo=1.0, decode_slo=1.0, theta=1.0,
+                    gamma_num=1, gamma_log2den=1)
+
+
+def test_rebalance_worked_example():
+    g = json.load(open(os.path.join(GOLDEN, "rebalance_example.json")))
+    m = _rb_model(**g["model"])
+    o, n = g["ongoing"], g["new"]
+    r = ref.rebalance(g["W"], m, o["worker"], o["l_pred"], o["l_out"], o["l_real"], o["l_repred"],
+                      n["l_pred"], n["worker"])
+    e = g["expected"]
+    assert r.rho == 500
+    assert r.worker.tolist() == e["worker"]
+    assert r.le.tolist() == e["le"] and r.be.tolist() == e["be"]
+    assert r.moves.tolist() == e["moves"]
+    assert (r.obj_before, r.obj_after) == (e["obj_before"], e["obj_after"])
+
+
+def test_rebalance_errors_closed_forms():
+    """All under-estimated: l^e = sum of the re-predictions, b^e = count; all
+    over-estimated: l^e = sum(l_real - l_pred), b^e = -count; predictions that
+    were right (l_out <= l_pred <= l_real) leave no error."""
+    m = _rb_model()
+    rng = np.random.default_rng(3)
+    n = 50
+    lp = rng.integers(10, 100, n)
+    rp = rng.integers(100, 300, n)
+    r = ref.rebalance(2, m, np.zeros(n), lp, lp + 1, lp + 5, rp, [], [])
+    assert r.le.tolist() == [int(rp.sum()), 0] and r.be.tolist() == [n, 0]
+    lr = lp - rng.integers(1, 9, n)
+    r = ref.rebalance(2, m, np.ones(n), lp, lr, lr, rp, [], [])
+    assert r.le.tolist() == [0, int((lr - lp).sum())] and r.be.tolist() == [0, -n]
+    r = ref.rebalance(2, m, np.ones(n), lp, lp, lp + rng.integers(0, 9, n), rp, [], [])
+    assert r.le.tolist() == [0, 0] and r.be.tolist() == [0, 0] and r.obj_before == 0
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_rebalance_two_workers_closed_form(seed):
+    """Two workers, every new request on worker 0 with one length: k moves give
+    the objective f(k) = |c0 - k d| + |c1 + k d| (d = l_pred + rho), a convex
+    function of k, so the greedy search stops at the smallest minimiser of f
+    over 0 .. n."""
+    rng = np.random.default_rng(seed)
+    m = _rb_model(c2=float(rng.choice([1e-4, 3e-5, 0.0])), k2=2e-7)
+    rho = ref.rebalance_rho(m)
+    nu, no, n = (int(x) for x in rng.integers(1, 30, 3))
+    lpu = rng.integers(10, 50, nu)
+    rpu = rng.integers(50, 400, nu)
+    lpo = rng.integers(100, 400, no)
+    lro = lpo - rng.integers(1, 90, no)
+    L = int(rng.integers(5, 200))
+    ow = np.r_[np.zeros(nu), np.ones(no)]
+    r = ref.rebalance(2, m, ow, np.r_[lpu, lpo], np.r_[lpu + 1, lro], np.r_[lpu + 3, lro], np.r_[rpu, np.zeros(no)],
+                      np.full(n, L), np.zeros(n))
+    c0 = int(rpu.sum()) + rho * nu
+    c1 = int((lro - lpo).sum()) - rho * no
+    d = L + rho
+    f = [abs(c0 - k * d) + abs(c1 + k * d) for k in range(n + 1)]
+    kstar = int(np.argmin(f))
+    assert len(r.moves) == kstar
+    assert r.obj_before == f[0] and r.obj_after == f[kstar]
+    assert r.moves.tolist() == [[j, 1] for j in range(kstar)]
+    assert (r.worker == 1).sum() == kstar
+
+
+def _objective(le, be, rho):
+    return sum(abs(int(a) + rho * int(b)) for a, b in zip(le, be))
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_rebalance_moves_replayed_by_bruteforce(seed):
+    """Replay the move log: before each move, try every (unmoved placed request,
+    other worker) on a copy of the state and recompute the whole objective; the
+    applied move must reach the smallest objective, be the first such pair in
+    request-then-worker order, and lower the objective.  At the end no move of an
+    unmoved request lowers it, each request moved at most once, unplaced ones
+    stayed, and the reported errors and objectives match the replayed state."""
+    rng = np.random.default_rng(100 + seed)
+    W = int(rng.integers(1, 7))
+    m = _rb_model(c2=float(rng.choice([1e-4, 2e-6, 0.0])), k2=float(rng.choice([2e-7, 1e-6])))
+    n_old, n_new = int(rng.integers(0, 25)), int(rng.integers(0, 12))
+    ow = rng.integers(0, W, n_old)
+    lp = rng.integers(1, 60, n_old)
+    lr = np.maximum(1, (lp * np.exp(rng.normal(0, 0.6, n_old))).astype(np.int64))
+    lo = np.array([int(rng.integers(0, x + 1)) for x in lr], np.int64)
+    rp = lp + rng.integers(0, 80, n_old)
+    nlp = rng.integers(1, 300, n_new)
+    nw = rng.integers(-1, W, n_new)
+    _replay_check(W, m, ow, lp, lo, lr, rp, nlp, nw)
+
+
+def test_rebalance_request_moves_at_most_once():
+    """An input (found by a search over seeds) on which greedy moves without the
+    at-most-once rule would move request 2 a second time."""
+    rng = np.random.default_rng(12935)
+    W = int(rng.integers(2, 6))
+    n_old, n_new = int(rng.integers(0, 20)), int(rng.integers(1, 10))
+    ow = rng.integers(0, W, n_old)
+    lp = rng.integers(1, 60, n_old)
+    lr = np.maximum(1, (lp * np.exp(rng.normal(0, 0.8, n_old))).astype(np.int64))
+    lo = np.array([int(rng.integers(0, x + 1)) for x in lr], np.int64)
+    rp = lp + rng.integers(0, 80, n_old)
+    nlp = rng.integers(1, 100, n_new)
+    nw = rng.integers(0, W, n_new)
+    r = _replay_check(W, _rb_model(c2=0.0), ow, lp, lo, lr, rp, nlp, nw)
+    assert r.moves[:, 0].tolist().count(2) == 1
+
+
+def _replay_check(W, m, ow, lp, lo, lr, rp, nlp, nw):
+    rho = ref.rebalance_rho(m)
+    n_old, n_new = len(ow), len(nlp)
+    r = ref.rebalance(W, m, ow, lp, lo, lr, rp, nlp, nw)
+    # the errors, from the two tests of the algorithm, one request at a time
+    le = [0] * W
+    be = [0] * W
+    for j in range(n_old):
+        if lo[j] > lp[j]:
+            le[ow[j]] += int(rp[j]); be[ow[j]] += 1
+        if lr[j] < lp[j]:
+            le[ow[j]] += int(lr[j] - lp[j]); be[ow[j]] -= 1
+    assert r.obj_before == _objective(le, be, rho)
+    cur = [int(x) for x in nw]
+    moved = set()
+
+    def after(j, y):
+        le2, be2 = list(le), list(be)
+        le2[cur[j]] -= int(nlp[j]); be2[cur[j]] -= 1
+        le2[y] += int(nlp[j]); be2[y] += 1
+        return _objective(le2, be2, rho)
+
+    def candidates():
+        return [(after(j, y), j, y) for j in range(n_new) if j not in moved and cur[j] >= 0
+                for y in range(W) if y != cur[j]]
+
+    for j, y in r.moves.tolist():
+        obj = _objective(le, be, rho)
+        best = min(candidates())
+        assert (best[1], best[2]) == (j, y) and best[0] < obj
+        le[cur[j]] -= int(nlp[j]); be[cur[j]] -= 1
+        le[y] += int(nlp[j]); be[y] += 1
+        cur[j] = y
+        moved.add(j)
+    obj = _objective(le, be, rho)
+    assert all(o >= obj for o, _, _ in candidates())
+    assert r.obj_after == obj
+    assert r.worker.tolist() == cur and r.le.tolist() == le and r.be.tolist() == be
+    assert all(r.worker[j] == -1 for j in range(n_new) if nw[j] == -1)
+    assert len(set(r.moves[:, 0].tolist())) == len(r.moves)
+    return r
+
+
+def test_rebalance_rejects_invalid_input():
+    m = _rb_model()
+    with pytest.raises(RuntimeError):  # generated more than the real length
+        ref.rebalance(2, m, [0], [10], [6], [5], [0], [], [])
+    with pytest.raises(RuntimeError):  # worker out of range
+        ref.rebalance(2, m, [2], [10], [1], [5], [0], [], [])
+    with pytest.raises(RuntimeError):  # new request on a worker out of range
+        ref.rebalance(2, m, [], [], [], [], [], [5], [2])
+    with pytest.raises(RuntimeError):  # no decode slope: the error line is undefined
+        ref.rebalance(2, _rb_model(k2=0.0), [], [], [], [], [], [], [])

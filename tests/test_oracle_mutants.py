@@ -50,6 +50,18 @@ MUTANTS = [
     ("(d) iteration time without the batch term", "(m->c3 + m->c2 * (double)w->n)", "(m->c3 + m->c2 * (double)(w->n - 1))"),
     ("(d) resident slack from the predicted length", "s0 = model->decode_slo * (double)g - res_tdec[k];",
      "s0 = model->decode_slo * (double)lp - res_tdec[k];"),
+    # Algorithm 2
+    ("A2 over-estimate error with the sign flipped", "le[i] += (int64_t)old_lreal[j] - old_lpred[j]; be[i] -= 1;",
+     "le[i] += (int64_t)old_lpred[j] - old_lreal[j]; be[i] -= 1;"),
+    ("A2 under-estimate counts the old prediction", "le[i] += old_lrepred[j]; be[i] += 1;",
+     "le[i] += old_lpred[j]; be[i] += 1;"),
+    ("A2 under-estimate test non-strict", "if (old_lout[j] > old_lpred[j])", "if (old_lout[j] >= old_lpred[j])"),
+    ("A2 batch error left out of the line", "#define RB_C(i) (le[i] + rho * be[i])", "#define RB_C(i) (le[i])"),
+    ("A2 a move shifts only the length", "const int64_t d = (int64_t)new_lpred[j] + rho;",
+     "const int64_t d = (int64_t)new_lpred[j];"),
+    ("A2 ties to the last pair", "if (gain > best) { best = gain;", "if (gain >= best && gain > 0) { best = gain;"),
+    ("A2 a request may move twice", "        moved[bj] = 1;\n", ""),
+    ("A2 rho truncated", "return (int64_t)llrint(m->c2 / m->k2);", "return (int64_t)(m->c2 / m->k2 * 0.999);"),
 ]
 
 PINS = [
@@ -72,7 +84,11 @@ PINS = [
     lambda: pins.test_preemption_limit_matches_bruteforce(3),
     pins.test_preemption_limit_worked_example,
     pins.test_preemption_limit_needs_an_ongoing_request,
-]
+    pins.test_rebalance_worked_example,
+    pins.test_rebalance_errors_closed_forms,
+    pins.test_rebalance_request_moves_at_most_once,
+] + [lambda s=s: pins.test_rebalance_two_workers_closed_form(s) for s in range(6)] + [
+    lambda s=s: pins.test_rebalance_moves_replayed_by_bruteforce(s) for s in range(25)]
 
 
 def test_mutant_table_applies():
