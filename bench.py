@@ -108,6 +108,63 @@ def time_sweep(steps: int):
             "queries": sw.n_queries, "min_total_gpus": gpus, "min_gpus_scenario": idx}
 
 
+def time_rebalance(steps: int, oracle_problems: int = 0):
+    """Algorithm 2 over the 256-problem workload, inputs resident on the device;
+    every call starts from the same placement (a device copy inside the loop)."""
+    import numpy as np
+    import torch
+
+    from paper_2405_06856_amd import aladdin
+    from paper_2405_06856_amd import workloads as wl
+    b = wl.make_config("rebalance")
+    ev = aladdin.Evaluator(0)
+    dev = ev.device
+    d32 = lambda a: torch.as_tensor(np.ascontiguousarray(a), dtype=torch.int32).to(dev)
+    old = [d32(x) for x in (b.old_worker, b.old_l_pred, b.old_l_out, b.old_l_real, b.old_l_repred)]
+    nl, nw0 = d32(b.new_l_pred), d32(b.new_worker)
+    nw = torch.empty_like(nw0)
+    Wt = int(b.n_workers.sum())
+    le = torch.empty(Wt, dtype=torch.int64, device=dev)
+    be = torch.empty_like(le)
+    mv = torch.empty(b.P, dtype=torch.int32, device=dev)
+    obj = torch.empty(2 * b.P, dtype=torch.int64, device=dev)
+    models = (aladdin.Model * b.P)(*[aladdin.to_model(m) for m in b.models])
+
+    def call():
+        nw.copy_(nw0)
+        aladdin.ald_rebalance(ev.h, b.P, b.n_workers, models, b.old_offsets, *old, b.new_offsets, nl, nw,
+                              le, be, mv, None, obj)
+
+    for _ in range(2):
+        call()
+    ev.profiling(True, kinds=("rebalance",))
+    torch.cuda.synchronize()
+    gc.collect()
+    gc.disable()
+    try:
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            call()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / steps
+    finally:
+        gc.enable()
+    k_ms, k_n = ev.kernel_time("rebalance")
+    moves = int(mv.sum().item())
+    ev.close()
+    out = {"problems_per_s": b.P / dt, "ms_per_call": dt * 1e3, "kernel_ms_per_call": k_ms / max(k_n, 1),
+           "problems": b.P, "workers": Wt, "ongoing": int(b.old_offsets[-1]), "new": int(b.new_offsets[-1]),
+           "moves": moves}
+    if oracle_problems > 0:
+        from oracle import ref  # the CPU baseline leg may use the oracle
+        t0 = time.perf_counter()
+        for p in range(oracle_problems):
+            ref.rebalance(*b.problem(p))
+        out["oracle_problems_per_s"] = oracle_problems / (time.perf_counter() - t0)
+        out["oracle_sample"] = "first %d problems, one thread" % oracle_problems
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -117,6 +174,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--sweep-only", action="store_true", help="time only the scaling sweep (for profiling)")
+    ap.add_argument("--no-rebalance", action="store_true")
+    ap.add_argument("--rebalance-only", action="store_true", help="time only Algorithm 2 (for profiling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="also run a plain device-to-device copy of MIB MiB (a reference kernel of known "
                          "traffic for scaling memory counters)")
@@ -135,6 +194,9 @@ def main():
     dev = torch.device("cuda", 0)
     if args.sweep_only:
         print(json.dumps({"sweep": time_sweep(args.sweep_steps)}), flush=True)
+        return
+    if args.rebalance_only:
+        print(json.dumps({"rebalance": time_rebalance(args.steps)}), flush=True)
         return
     if args.calibrate_copy > 0:
         n = args.calibrate_copy * (1 << 20) // 4
@@ -206,6 +268,7 @@ def main():
     traffic = measured_traffic() if pairs_per_eval_launch == pairs else None
 
     sweep_info = None if args.no_sweep else time_sweep(args.sweep_steps)
+    rb_info = None if args.no_rebalance else time_rebalance(args.steps, 0 if args.no_cpu else 32)
     line = {
         "metric": "query x worker placement evals/sec (+ scenario sweeps/sec; % of HBM roofline)",
         "value": value,
@@ -232,6 +295,7 @@ def main():
         "wall_ms_per_step": wall * 1e3 / args.steps,
         "load_ms": load_s * 1e3,
         "sweep": sweep_info,
+        "rebalance": rb_info,
     }
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(trace)

@@ -155,14 +155,52 @@ int ald_sweep_scenarios(ald_handle_t handle, int32_t S, const ald_scenario_t* sc
                         const int32_t* q_l_in, const int32_t* q_l_pred, int32_t* out_rejected,
                         int32_t* out_first_reject, int32_t* out_worker);
 
+/* Algorithm 2 (Sec. 4.3): re-balance the new requests of a heartbeat against
+ * the output-length prediction errors of the ongoing ones, for P independent
+ * problems (clusters) at once.  Stateless: the loaded workers are not used.
+ *
+ * Per worker i, from its ongoing requests j:
+ *   l_out_j > l_pred_j (decoding past the prediction): l^e_i += l_repred_j, b^e_i += 1
+ *   l_real_j < l_pred_j (finished before it):          l^e_i += l_real_j - l_pred_j, b^e_i -= 1
+ * The error line of Eq. 4, divided by k2, is c_i = l^e_i + rho * b^e_i with
+ * rho = c2 / k2 rounded to whole tokens (llrint); its distance from the
+ * origin is |c_i| / sqrt(1 + rho^2).  Moving new request j (predicted length
+ * l_pred_j) from worker x to y moves l_pred_j and one batch slot of error:
+ * c_x -= l_pred_j + rho, c_y += l_pred_j + rho.  The moves are greedy: while
+ * some (request, other worker) pair lowers sum_i |c_i|, the pair that lowers
+ * it most is applied (ties: lowest request, then lowest worker); a request
+ * moves at most once, and unplaced requests (worker -1) stay.  All integer:
+ * the result is exact.
+ *
+ * Host arrays: n_workers[P] (1 .. 4096), models[P] (k2 > 0, 0 <= c2/k2 <= 1e9;
+ * only c2 and k2 are used), old_offsets[P+1] and new_offsets[P+1] (CSR over the
+ * request arrays, starting at 0; at most 8192 new requests per problem).
+ * Device arrays: old_worker, old_l_pred, old_l_out (tokens generated so far),
+ * old_l_real (real output length, >= old_l_out), old_l_repred (re-predicted
+ * output length) [old_offsets[P]]; new_l_pred [new_offsets[P]]; new_worker
+ * [new_offsets[P]] in/out.  Worker indices are local to their problem; lengths
+ * lie in [1, 2^24] (l_out and l_repred may be 0).
+ * Device outputs (each may be NULL): out_le, out_be [sum n_workers] (final
+ * errors, problem p's workers after those of problems < p); out_moves[P];
+ * out_log[2 * new_offsets[P]] (problem p's moves in order as (request, target)
+ * pairs starting at entry 2 * new_offsets[p]); out_obj[2P] (sum |c_i| before
+ * and after).  ALD_EINVAL for a bad argument or any invalid request; then
+ * new_worker is left unchanged. */
+int ald_rebalance(ald_handle_t handle, int32_t P, const int32_t* n_workers, const ald_model_t* models,
+                  const int64_t* old_offsets, const int32_t* old_worker, const int32_t* old_l_pred,
+                  const int32_t* old_l_out, const int32_t* old_l_real, const int32_t* old_l_repred,
+                  const int64_t* new_offsets, const int32_t* new_l_pred, int32_t* new_worker,
+                  int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t* out_log, int64_t* out_obj);
+
 /* Current state of every loaded worker (device arrays of W): batch size, sum of
  * contexts, sum of remaining lengths, KV peak over future iterations. */
 int ald_worker_summary(ald_handle_t handle, int32_t* B, int64_t* sum_c, int64_t* sum_r, int64_t* peak);
 
 /* Kernel timing with HIP events on the handle's stream (off by default).
  * kind: 0 = state build, 1 = pair evaluation, 2 = per-query selection,
- * 3 = commit.  `kinds` is a bit mask of the kinds to time (bit k = kind k,
- * 15 = all, 0 = off; anything else outside 0..15 is ALD_EINVAL).  Each timed
+ * 3 = commit, 4 = re-balancing (both of its kernels).  `kinds` is a bit mask
+ * of the kinds to time (bit k = kind k, 31 = all, 0 = off; anything else
+ * outside 0..31 is ALD_EINVAL).  Each timed
  * launch records two events, so time only what is needed.  Totals accumulate
  * over calls while enabled; a nonzero mask resets them. */
 int ald_set_profiling(ald_handle_t handle, int32_t kinds);

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(PKG, "libaladdin.so")
 
 ALD_OK, ALD_EINVAL, ALD_EHIP, ALD_ESLOTS, ALD_ESTATE, ALD_EOVERFLOW = 0, -1, -2, -3, -4, -5
 
-KERNEL_KINDS = {"build": 0, "eval": 1, "select": 2, "commit": 3}
+KERNEL_KINDS = {"build": 0, "eval": 1, "select": 2, "commit": 3, "rebalance": 4}
 
 
 class AladdinError(RuntimeError):
@@ -48,7 +48,7 @@ assert DIAG_DTYPE.itemsize == 40
 
 SYMBOLS = ("ald_create", "ald_destroy", "ald_set_tile", "ald_load_workers", "ald_load_workers_history",
            "ald_place_stream",
-           "ald_sweep_scenarios", "ald_worker_summary", "ald_set_profiling", "ald_kernel_time",
+           "ald_sweep_scenarios", "ald_rebalance", "ald_worker_summary", "ald_set_profiling", "ald_kernel_time",
            "ald_last_error", "ald_strerror")
 
 
@@ -65,6 +65,7 @@ def _load():
         "ald_load_workers_history": ([P, i32, ctypes.POINTER(Model), P, P, P, P, P, P, i32], ctypes.c_int),
         "ald_place_stream": ([P, i32, P, P, i32, P, P], ctypes.c_int),
         "ald_sweep_scenarios": ([P, i32, P, i32, P, P, P, P, P], ctypes.c_int),
+        "ald_rebalance": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P], ctypes.c_int),
         "ald_worker_summary": ([P, P, P, P, P], ctypes.c_int),
         "ald_set_profiling": ([P, i32], ctypes.c_int),
         "ald_kernel_time": ([P, i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)], ctypes.c_int),
@@ -138,6 +139,21 @@ def ald_sweep_scenarios(h, S: int, scen, Q: int, q_l_in, q_l_pred, out_rejected,
     _check(h, _L.ald_sweep_scenarios(h, int(S), ctypes.cast(scen, ctypes.c_void_p), int(Q), _dptr(q_l_in),
                                      _dptr(q_l_pred), _dptr(out_rejected), _dptr(out_first_reject),
                                      _dptr(out_worker)))
+
+
+def ald_rebalance(h, P: int, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out, old_l_real,
+                  old_l_repred, new_offsets, new_l_pred, new_worker, out_le=None, out_be=None, out_moves=None,
+                  out_log=None, out_obj=None) -> None:
+    """n_workers (int32), models (Model array) and the offsets (int64) are host
+    arrays; everything else is a device tensor."""
+    nw = np.ascontiguousarray(n_workers, dtype=np.int32)
+    oo = np.ascontiguousarray(old_offsets, dtype=np.int64)
+    no = np.ascontiguousarray(new_offsets, dtype=np.int64)
+    _check(h, _L.ald_rebalance(h, int(P), nw.ctypes.data_as(ctypes.c_void_p), ctypes.cast(models, ctypes.c_void_p),
+                               oo.ctypes.data_as(ctypes.c_void_p), _dptr(old_worker), _dptr(old_l_pred),
+                               _dptr(old_l_out), _dptr(old_l_real), _dptr(old_l_repred),
+                               no.ctypes.data_as(ctypes.c_void_p), _dptr(new_l_pred), _dptr(new_worker),
+                               _dptr(out_le), _dptr(out_be), _dptr(out_moves), _dptr(out_log), _dptr(out_obj)))
 
 
 def ald_worker_summary(h, B, sum_c, sum_r, peak) -> None:
@@ -279,12 +295,35 @@ class Evaluator:
         return (rej.cpu().numpy(), first.cpu().numpy(),
                 ow.cpu().numpy().reshape(S, Q) if want_workers else None)
 
+    def rebalance(self, batch, want_log=False):
+        """Algorithm 2 on a workloads.RebalanceBatch; returns the new workers and
+        per-problem results as numpy arrays."""
+        t = self.torch
+        P = batch.P
+        models = (Model * P)(*[to_model(m) for m in batch.models])
+        d32 = lambda a: self._dev(a, t.int32)
+        nw = d32(batch.new_worker)
+        Wt = int(np.sum(batch.n_workers))
+        le = t.empty(Wt, dtype=t.int64, device=self.device)
+        be = t.empty(Wt, dtype=t.int64, device=self.device)
+        mv = t.empty(P, dtype=t.int32, device=self.device)
+        obj = t.empty(2 * P, dtype=t.int64, device=self.device)
+        log = t.empty(max(1, 2 * int(batch.new_offsets[-1])), dtype=t.int32, device=self.device) if want_log else None
+        ald_rebalance(self.h, P, batch.n_workers, models, batch.old_offsets, d32(batch.old_worker),
+                      d32(batch.old_l_pred), d32(batch.old_l_out), d32(batch.old_l_real), d32(batch.old_l_repred),
+                      batch.new_offsets, d32(batch.new_l_pred), nw, le, be, mv, log, obj)
+        out = {"worker": nw.cpu().numpy(), "le": le.cpu().numpy(), "be": be.cpu().numpy(),
+               "moves": mv.cpu().numpy(), "obj": obj.cpu().numpy().reshape(P, 2)}
+        if want_log:
+            out["log"] = log.cpu().numpy()
+        return out
+
     def profiling(self, enable=True, kinds=None):
         """Time kernel kinds with HIP events: all of them, or the names in `kinds`."""
         if not enable:
             mask = 0
         elif kinds is None:
-            mask = 15
+            mask = 31
         else:
             mask = 0
             for k in kinds:

@@ -1,0 +1,48 @@
+// Algorithm 2 (re-balancing a heartbeat's new requests against the output-length
+// prediction errors of the ongoing ones): limits, tables and launch.
+#pragma once
+
+#include "ald_internal.h"
+
+namespace ald {
+
+constexpr int RB_THREADS = 1024;
+constexpr int RB_WMAX = 4096;     // workers per problem (the error accumulators live in LDS)
+constexpr int RB_JMAX = 8192;     // new requests per problem
+constexpr int RB_ETHREADS = 256;  // threads per error-accumulation block
+constexpr int RB_CHUNK = 2048;    // ongoing requests per error-accumulation block
+constexpr int32_t RB_LEN_MAX = 1 << 24;
+
+struct RbProblem {
+    int64_t old0, old1;  // its ongoing requests [old0, old1)
+    int64_t new0;        // its first new request
+    int64_t wbase;       // its first worker in the error arrays
+    int64_t rho;         // c2 / k2 in whole tokens
+    int32_t W, n_new;
+};
+struct RbChunk {
+    int64_t begin, end;  // ongoing requests of one problem
+    int32_t p, pad;
+};
+struct RbArgs {
+    const RbProblem* prob;
+    const RbChunk* chunk;
+    int32_t nchunk, P;
+    const int32_t* old_worker;
+    const int32_t* old_lpred;
+    const int32_t* old_lout;
+    const int32_t* old_lreal;
+    const int32_t* old_lrepred;
+    const int32_t* new_lpred;
+    int32_t* new_worker;  // in/out
+    int64_t* le;          // per worker, zero before the launch; final errors after
+    int64_t* be;
+    int32_t* moves;       // per problem (nullable)
+    int32_t* log;         // (request, target) pairs at 2 * new0 (nullable)
+    int64_t* obj;         // per problem: sum |c| before and after (nullable)
+    int32_t* err;
+};
+// error accumulation (nchunk + P blocks), then the greedy moves (P blocks)
+hipError_t launch_rebalance(const RbArgs& a, hipStream_t stream);
+
+}  // namespace ald

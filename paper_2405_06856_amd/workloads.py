@@ -32,7 +32,7 @@ import numpy as np
 
 __all__ = [
     "Model", "Trace", "Scenario", "SweepTrace", "CONFIGS", "make_config",
-    "make_trace", "make_sweep", "BASE_MODEL", "scenario_index",
+    "make_trace", "make_sweep", "BASE_MODEL", "scenario_index", "RebalanceBatch", "make_rebalance",
 ]
 
 
@@ -236,6 +236,8 @@ CONFIGS = {
              "Q=16384 @500/s mid lengths, M=65536*gpus, slopes / (0.8*gpus)",
     "long": "W=2048, M=1048576, R=1024, Q=131072, long lengths, heartbeat every 100, "
             "TTFT 4 s, decode 0.08 s",
+    "rebalance": "Algorithm 2: 256 problems of W=128 workers x 64 ongoing requests and 1024 new ones, "
+                 "mid output lengths, prediction error exp(0.5 N(0,1)), base model (rho = 500 tokens)",
 }
 
 
@@ -247,6 +249,80 @@ def with_decode_history(trace: Trace, seed: int, lo: float = 0.2, hi: float = 0.
     f = rng.uniform(lo, hi, trace.n_resident)
     t_dec = trace.res_generated.astype(np.float64) * trace.model.decode_slo * f
     return dataclasses.replace(trace, name=trace.name + "+history", res_t_dec=t_dec)
+
+
+@dataclasses.dataclass
+class RebalanceBatch:
+    """P independent re-balancing problems (Algorithm 2): per problem, W workers
+    with R ongoing requests each and n_new new requests of one heartbeat, in
+    CSR form (worker indices local to the problem)."""
+    name: str
+    models: List[Model]
+    n_workers: np.ndarray     # int32 [P]
+    old_offsets: np.ndarray   # int64 [P+1]
+    old_worker: np.ndarray    # int32 [n_old]
+    old_l_pred: np.ndarray
+    old_l_out: np.ndarray     # tokens generated so far
+    old_l_real: np.ndarray    # real output length where it is known (finished), else max(l_out, l_pred)
+    old_l_repred: np.ndarray  # re-prediction for a request decoding past its prediction
+    new_offsets: np.ndarray   # int64 [P+1]
+    new_l_pred: np.ndarray    # int32 [n_new]
+    new_worker: np.ndarray    # int32 [n_new], -1 = not placed
+
+    @property
+    def P(self) -> int:
+        return len(self.n_workers)
+
+    def problem(self, p: int):
+        """Problem p's arrays (views)."""
+        o0, o1 = int(self.old_offsets[p]), int(self.old_offsets[p + 1])
+        n0, n1 = int(self.new_offsets[p]), int(self.new_offsets[p + 1])
+        return (int(self.n_workers[p]), self.models[p], self.old_worker[o0:o1], self.old_l_pred[o0:o1],
+                self.old_l_out[o0:o1], self.old_l_real[o0:o1], self.old_l_repred[o0:o1],
+                self.new_l_pred[n0:n1], self.new_worker[n0:n1])
+
+
+def make_rebalance(name: str, seed: int, P: int, W, R, n_new, model: Model = None, out_dist=None,
+                   sigma_err: float = 0.5, unplaced: float = 0.02) -> RebalanceBatch:
+    """Synthetic prediction errors: a request's real output length is its
+    predicted one times exp(sigma_err * N(0, 1)) (unbiased in the log, as the
+    paper's predictor is unbiased), clipped to [1, 4 * the length range's top].
+    Each ongoing request has run t ~ integers(0, max(l_pred, l_real) + 1)
+    iterations: it generated l_out = min(t, l_real) tokens and has finished
+    when t >= l_real; a finished request reports its real length, a running
+    one max(l_out, l_pred) (its real length is not known yet).  The
+    re-prediction is the mean real length given that it exceeds the
+    prediction, l_pred * 2 exp(sigma^2 / 2) Phi(sigma), rounded.  New requests
+    draw a predicted length and a worker uniformly, a fraction `unplaced` none.
+    W, R, n_new: an int, or a per-problem sequence.
+    Draw order: per problem, ongoing l_pred, error factors, progress t, then
+    new l_pred, new workers, unplaced flags."""
+    model = model or BASE_MODEL
+    mu, sg, lo, hi = out_dist or MID_OUT
+    rng = np.random.default_rng(seed)
+    per = lambda v: [int(x) for x in (v if hasattr(v, "__len__") else [v] * P)]
+    Ws, Rs, Ns = per(W), per(R), per(n_new)
+    boost = 2.0 * math.exp(sigma_err * sigma_err / 2.0) * 0.5 * (1.0 + math.erf(sigma_err / math.sqrt(2.0)))
+    cols = {k: [] for k in ("ow", "lp", "lo", "lr", "rp", "nl", "nw")}
+    for p in range(P):
+        n = Ws[p] * Rs[p]
+        lp = _lengths(rng, mu, sg, lo, hi, n).astype(np.int64)
+        real = np.clip(np.rint(lp * np.exp(sigma_err * rng.standard_normal(n))), 1, 4 * hi).astype(np.int64)
+        t = rng.integers(0, np.maximum(lp, real) + 1)
+        lout = np.minimum(t, real)
+        rep_real = np.where(t >= real, real, np.maximum(lout, lp))
+        cols["ow"].append(np.repeat(np.arange(Ws[p]), Rs[p]))
+        cols["lp"].append(lp)
+        cols["lo"].append(lout)
+        cols["lr"].append(rep_real)
+        cols["rp"].append(np.rint(lp * boost).astype(np.int64))
+        cols["nl"].append(_lengths(rng, mu, sg, lo, hi, Ns[p]))
+        w = rng.integers(0, Ws[p], Ns[p])
+        cols["nw"].append(np.where(rng.random(Ns[p]) < unplaced, -1, w))
+    cat = lambda k: np.concatenate(cols[k]).astype(np.int32) if cols[k] else np.zeros(0, np.int32)
+    off = lambda ns: np.concatenate([[0], np.cumsum(ns)]).astype(np.int64)
+    return RebalanceBatch(name, [model] * P, np.array(Ws, np.int32), off([w * r for w, r in zip(Ws, Rs)]),
+                          cat("ow"), cat("lp"), cat("lo"), cat("lr"), cat("rp"), off(Ns), cat("nl"), cat("nw"))
 
 
 def make_config(name: str):
@@ -265,6 +341,8 @@ def make_config(name: str):
         return make_sweep("sweep", 3, Q=16384, worker_counts=range(16, 1025, 16),
                           gpu_counts=(1, 2, 4, 8), base_capacity=65536, model=BASE_MODEL,
                           in_dist=MID_IN, out_dist=MID_OUT, rate=500.0)
+    if name == "rebalance":
+        return make_rebalance("rebalance", 5, P=256, W=128, R=64, n_new=1024)
     if name == "long":
         model = dataclasses.replace(BASE_MODEL, ttft_slo=4.0, decode_slo=0.08)
         return make_trace("long", 4, W=2048, R=1024, Q=131072, kv_capacity=1048576, model=model,

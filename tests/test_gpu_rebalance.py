@@ -1,0 +1,145 @@
+"""Algorithm 2 (re-balancing) on the GPU vs the CPU oracle (needs an MI355X).
+
+Everything is integer, so the new workers, per-worker errors, move logs and
+objectives must match the oracle exactly."""
+from __future__ import annotations
+
+import dataclasses
+
+import numpy as np
+import pytest
+
+from oracle import ref
+from paper_2405_06856_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2405_06856_amd import aladdin
+    e = aladdin.Evaluator(0)
+    yield e
+    e.close()
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def check_against_oracle(batch, got, problems=None):
+    wb = np.concatenate([[0], np.cumsum(batch.n_workers)])
+    for p in (range(batch.P) if problems is None else problems):
+        W = int(batch.n_workers[p])
+        want = ref.rebalance(*batch.problem(p))
+        n0, n1 = int(batch.new_offsets[p]), int(batch.new_offsets[p + 1])
+        k = len(want.moves)
+        assert got["worker"][n0:n1].tolist() == want.worker.tolist(), "problem %d: workers differ" % p
+        assert got["le"][wb[p]:wb[p] + W].tolist() == want.le.tolist(), "problem %d: l^e differs" % p
+        assert got["be"][wb[p]:wb[p] + W].tolist() == want.be.tolist(), "problem %d: b^e differs" % p
+        assert int(got["moves"][p]) == k
+        assert got["obj"][p].tolist() == [want.obj_before, want.obj_after]
+        if "log" in got:
+            assert got["log"][2 * n0:2 * n0 + 2 * k].reshape(k, 2).tolist() == want.moves.tolist()
+
+
+SMALL = [
+    # (name, P, W, R, n_new, sigma_err)
+    ("one worker", 2, 1, 5, 9, 0.5),
+    ("tiny", 3, 5, 4, 11, 0.8),
+    ("mixed sizes", 4, [3, 64, 17, 1], [0, 9, 40, 3], [50, 0, 300, 7], 0.6),
+    ("several waves of requests", 2, 33, 20, 2000, 0.7),
+    ("many workers", 1, 4096, 2, 64, 0.9),
+    ("most new requests", 1, 40, 8, 8192, 0.7),
+    ("no prediction error", 2, 16, 30, 100, 0.0),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_rebalance_matches_oracle(ev, case):
+    name, P, W, R, n_new, sig = case
+    say("rebalance case", name)
+    b = wl.make_rebalance(name, 40 + SMALL.index(case), P, W, R, n_new, sigma_err=sig)
+    got = ev.rebalance(b, want_log=True)
+    check_against_oracle(b, got)
+
+
+def test_rebalance_models_per_problem(ev):
+    """Each problem takes its own rho = c2 / k2 (rounded to whole tokens)."""
+    b = wl.make_rebalance("rho", 7, 4, 24, 12, 400, sigma_err=0.7)
+    base = b.models[0]
+    b.models = [dataclasses.replace(base, c2=c2) for c2 in (0.0, 3e-5, 1.00005e-4, 4e-4)]
+    assert [ref.rebalance_rho(m) for m in b.models] == [0, 150, 500, 2000]
+    got = ev.rebalance(b, want_log=True)
+    check_against_oracle(b, got)
+
+
+def test_rebalance_full_size(ev):
+    """The 256-problem workload: every problem against the oracle, plus the
+    invariants (a move keeps sum c, lowers sum |c|, touches a request once)."""
+    b = wl.make_config("rebalance")
+    say("rebalance full size", b.P)
+    got = ev.rebalance(b, want_log=True)
+    check_against_oracle(b, got)
+    wb = np.concatenate([[0], np.cumsum(b.n_workers)])
+    for p in range(b.P):
+        assert got["obj"][p][1] <= got["obj"][p][0]
+        n0, k = int(b.new_offsets[p]), int(got["moves"][p])
+        moved = got["log"][2 * n0:2 * n0 + 2 * k:2]
+        assert len(set(moved.tolist())) == k
+    assert int(got["moves"].sum()) > 0
+    # a move takes its request's length and one batch slot from one worker to
+    # another: the sum of c over a problem's workers does not change
+    rho = ref.rebalance_rho(b.models[0])
+    for p in range(b.P):
+        n0, n1 = int(b.new_offsets[p]), int(b.new_offsets[p + 1])
+        c = got["le"][wb[p]:wb[p + 1]] + rho * got["be"][wb[p]:wb[p + 1]]
+        changed = got["worker"][n0:n1] != b.new_worker[n0:n1]
+        assert int(changed.sum()) == int(got["moves"][p])
+        want = ref.rebalance(*b.problem(p)[:7], [], [])  # the errors alone, no new requests
+        assert int(c.sum()) == int((want.le + rho * want.be).sum())
+
+
+def test_rebalance_twice_in_a_row(ev):
+    """Tables and error arrays are reused between calls of different sizes."""
+    b1 = wl.make_rebalance("a", 11, 6, 50, 10, 700)
+    b2 = wl.make_rebalance("b", 12, 2, 9, 3, 40)
+    check_against_oracle(b1, ev.rebalance(b1, want_log=True))
+    check_against_oracle(b2, ev.rebalance(b2, want_log=True))
+    check_against_oracle(b1, ev.rebalance(b1))
+
+
+def test_rebalance_invalid_input_changes_nothing(ev):
+    from paper_2405_06856_amd import aladdin
+    b = wl.make_rebalance("bad", 13, 3, 8, 5, 30)
+    k = int(b.old_offsets[2]) + 1  # a request of the last problem
+    b.old_l_out = b.old_l_out.copy()
+    b.old_l_out[k] = b.old_l_real[k] + 1  # more tokens generated than the real length
+    with pytest.raises(aladdin.AladdinError) as e:
+        ev.rebalance(b)
+    assert e.value.code == aladdin.ALD_EINVAL
+    b2 = wl.make_rebalance("bad2", 14, 2, 8, 5, 30)
+    b2.new_worker = b2.new_worker.copy()
+    b2.new_worker[3] = 8  # worker out of range
+    import torch
+    t = torch
+    nw = t.as_tensor(b2.new_worker).to(ev.device)
+    before = nw.clone()
+    models = (aladdin.Model * b2.P)(*[aladdin.to_model(m) for m in b2.models])
+    d = lambda a: t.as_tensor(a, dtype=t.int32).to(ev.device)
+    with pytest.raises(aladdin.AladdinError):
+        aladdin.ald_rebalance(ev.h, b2.P, b2.n_workers, models, b2.old_offsets, d(b2.old_worker), d(b2.old_l_pred),
+                              d(b2.old_l_out), d(b2.old_l_real), d(b2.old_l_repred), b2.new_offsets,
+                              d(b2.new_l_pred), nw)
+    assert t.equal(nw, before)
+    # host-side checks: too many workers, a model without decode slope
+    b3 = wl.make_rebalance("big", 15, 1, 4097, 0, 1)
+    with pytest.raises(aladdin.AladdinError):
+        ev.rebalance(b3)
+    b4 = wl.make_rebalance("k2", 16, 1, 4, 2, 3)
+    b4.models = [dataclasses.replace(b4.models[0], k2=0.0)]
+    with pytest.raises(aladdin.AladdinError):
+        ev.rebalance(b4)
