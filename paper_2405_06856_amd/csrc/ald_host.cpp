@@ -338,9 +338,10 @@ hipError_t prof_begin(ald_handle* h, int kind, Events* ev)
     if (!((h->prof >> kind) & 1)) return hipSuccess;
     if (h->pool.empty()) {
         Events e;
-        hipError_t r = hipEventCreate(&e.a);
+        // timing only: no system-scope fence when the events are recorded
+        hipError_t r = hipEventCreateWithFlags(&e.a, hipEventDisableSystemFence);
         if (r != hipSuccess) return r;
-        r = hipEventCreate(&e.b);
+        r = hipEventCreateWithFlags(&e.b, hipEventDisableSystemFence);
         if (r != hipSuccess) return r;
         h->pool.push_back(e);
     }
