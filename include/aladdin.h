@@ -155,6 +155,19 @@ int ald_sweep_scenarios(ald_handle_t handle, int32_t S, const ald_scenario_t* sc
                         const int32_t* q_l_in, const int32_t* q_l_pred, int32_t* out_rejected,
                         int32_t* out_first_reject, int32_t* out_worker);
 
+/* As ald_sweep_scenarios, with heartbeats (Sec. 4.2, placement per heartbeat):
+ * scenario s runs one decode iteration on all its workers after every
+ * heartbeat_every[s] processed queries (host array [S], >= 0; 0 = none), as
+ * ald_place_stream does.  With one decode iteration per heartbeat and arrival
+ * rate r, a period of r * T_dec queries stands for the stream arriving at r,
+ * which gives the smallest cluster per arrival rate (Sec. 4.4, Eq. 7).
+ * ALD_EOVERFLOW when a scenario would run more decode iterations than the
+ * 32-bit request state holds. */
+int ald_sweep_scenarios_hb(ald_handle_t handle, int32_t S, const ald_scenario_t* scen,
+                           const int32_t* heartbeat_every, int32_t Q, const int32_t* q_l_in,
+                           const int32_t* q_l_pred, int32_t* out_rejected, int32_t* out_first_reject,
+                           int32_t* out_worker);
+
 /* Algorithm 2 (Sec. 4.3): re-balance the new requests of a heartbeat against
  * the output-length prediction errors of the ongoing ones, for P independent
  * problems (clusters) at once.  Stateless: the loaded workers are not used.

@@ -435,11 +435,12 @@ typedef struct {
 
 /*
  * Scaling sweep: every scenario starts with empty workers and places the same
- * query stream on its own (no heartbeat).  Per scenario: number of rejected
- * queries and the index of the first rejection (-1 if none); optionally the
- * full placement (out_worker[s*Q + q]).
+ * query stream on its own, with a heartbeat after every H[s] processed queries
+ * (H NULL or H[s] = 0: none).  Per scenario: number of rejected queries and
+ * the index of the first rejection (-1 if none); optionally the full placement
+ * (out_worker[s*Q + q]).
  */
-int ora_sweep(int32_t S, const ora_scenario_t* scen, int32_t Q, const int32_t* q_lin,
+int ora_sweep(int32_t S, const ora_scenario_t* scen, const int32_t* H, int32_t Q, const int32_t* q_lin,
               const int32_t* q_lpred, int32_t n_threads, int32_t* out_rejected,
               int32_t* out_first_reject, int32_t* out_worker)
 {
@@ -457,7 +458,7 @@ int ora_sweep(int32_t S, const ora_scenario_t* scen, int32_t Q, const int32_t* q
         int32_t* dst = out_worker ? out_worker + (int64_t)s * Q : tmp;
         if (rc == ORA_OK) {
             for (int32_t i = 0; i < W; ++i) M[i] = scen[s].kv_capacity;
-            rc = ora_place(W, M, NULL, NULL, NULL, NULL, NULL, &scen[s].model, Q, q_lin, q_lpred, 0, 0, 0, 1,
+            rc = ora_place(W, M, NULL, NULL, NULL, NULL, NULL, &scen[s].model, Q, q_lin, q_lpred, H ? H[s] : 0, 0, 0, 1,
                            dst, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL);
         }
         if (rc == ORA_OK) {

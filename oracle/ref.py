@@ -58,7 +58,7 @@ def lib():
         L.ora_place.argtypes = [i32, P, P, P, P, P, P, ctypes.POINTER(OraModel), i32, P, P, i32, i32, i32,
                                 i32, P, P, P, P, P, P, P, P, P, P, P, P, P]
         L.ora_place.restype = ctypes.c_int
-        L.ora_sweep.argtypes = [i32, P, i32, P, P, i32, P, P, P]
+        L.ora_sweep.argtypes = [i32, P, P, i32, P, P, i32, P, P, P]
         L.ora_sweep.restype = ctypes.c_int
         L.ora_kv_peak.argtypes = [i64, P, P]
         L.ora_kv_peak.restype = i64
@@ -133,7 +133,8 @@ def place_trace(trace, q_slice=slice(None), **kw) -> PlaceResult:
                  res_t_dec=kw.pop("res_t_dec", getattr(trace, "res_t_dec", None)), **kw)
 
 
-def sweep(scenarios, q_l_in, q_l_pred, want_workers=False, n_threads=1):
+def sweep(scenarios, q_l_in, q_l_pred, want_workers=False, n_threads=1, heartbeat_every=None):
+    """heartbeat_every: None (no heartbeat), one period for every scenario, or one per scenario."""
     L = lib()
     S = len(scenarios)
     Q = int(len(q_l_in))
@@ -145,7 +146,10 @@ def sweep(scenarios, q_l_in, q_l_pred, want_workers=False, n_threads=1):
     workers = np.zeros(S * Q, np.int32) if want_workers else None
     ql = np.ascontiguousarray(q_l_in, dtype=np.int32)
     qp = np.ascontiguousarray(q_l_pred, dtype=np.int32)
-    rc = L.ora_sweep(S, ctypes.cast(arr, ctypes.c_void_p), Q, _ptr(ql), _ptr(qp), int(n_threads), _ptr(rej),
+    H = None
+    if heartbeat_every is not None:
+        H = np.ascontiguousarray(np.broadcast_to(np.asarray(heartbeat_every, dtype=np.int32), (S,)))
+    rc = L.ora_sweep(S, ctypes.cast(arr, ctypes.c_void_p), _ptr(H), Q, _ptr(ql), _ptr(qp), int(n_threads), _ptr(rej),
                      _ptr(first), _ptr(workers))
     if rc != ORA_OK:
         raise RuntimeError("oracle ora_sweep failed with code %d" % rc)

@@ -48,7 +48,7 @@ assert DIAG_DTYPE.itemsize == 40
 
 SYMBOLS = ("ald_create", "ald_destroy", "ald_set_tile", "ald_load_workers", "ald_load_workers_history",
            "ald_place_stream",
-           "ald_sweep_scenarios", "ald_rebalance", "ald_worker_summary", "ald_set_profiling", "ald_kernel_time",
+           "ald_sweep_scenarios", "ald_sweep_scenarios_hb", "ald_rebalance", "ald_worker_summary", "ald_set_profiling", "ald_kernel_time",
            "ald_last_error", "ald_strerror")
 
 
@@ -65,6 +65,7 @@ def _load():
         "ald_load_workers_history": ([P, i32, ctypes.POINTER(Model), P, P, P, P, P, P, i32], ctypes.c_int),
         "ald_place_stream": ([P, i32, P, P, i32, P, P], ctypes.c_int),
         "ald_sweep_scenarios": ([P, i32, P, i32, P, P, P, P, P], ctypes.c_int),
+        "ald_sweep_scenarios_hb": ([P, i32, P, P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_rebalance": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P], ctypes.c_int),
         "ald_worker_summary": ([P, P, P, P, P], ctypes.c_int),
         "ald_set_profiling": ([P, i32], ctypes.c_int),
@@ -139,6 +140,17 @@ def ald_sweep_scenarios(h, S: int, scen, Q: int, q_l_in, q_l_pred, out_rejected,
     _check(h, _L.ald_sweep_scenarios(h, int(S), ctypes.cast(scen, ctypes.c_void_p), int(Q), _dptr(q_l_in),
                                      _dptr(q_l_pred), _dptr(out_rejected), _dptr(out_first_reject),
                                      _dptr(out_worker)))
+
+
+def ald_sweep_scenarios_hb(h, S: int, scen, heartbeat_every, Q: int, q_l_in, q_l_pred, out_rejected,
+                           out_first_reject, out_worker=None) -> None:
+    """heartbeat_every: host array of S periods."""
+    hb = np.ascontiguousarray(heartbeat_every, dtype=np.int32)
+    if hb.shape != (S,):
+        raise ValueError("heartbeat_every must hold one period per scenario")
+    _check(h, _L.ald_sweep_scenarios_hb(h, int(S), ctypes.cast(scen, ctypes.c_void_p),
+                                        hb.ctypes.data_as(ctypes.c_void_p), int(Q), _dptr(q_l_in), _dptr(q_l_pred),
+                                        _dptr(out_rejected), _dptr(out_first_reject), _dptr(out_worker)))
 
 
 def ald_rebalance(h, P: int, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out, old_l_real,
@@ -279,7 +291,8 @@ class Evaluator:
         return {"B": B.cpu().numpy(), "sum_c": sc.cpu().numpy(), "sum_r": sr.cpu().numpy(),
                 "peak": pk.cpu().numpy()}
 
-    def sweep(self, scenarios, q_l_in, q_l_pred, want_workers=False):
+    def sweep(self, scenarios, q_l_in, q_l_pred, want_workers=False, heartbeat_every=None):
+        """heartbeat_every: None (no heartbeat), one period for all scenarios, or one per scenario."""
         t = self.torch
         S = len(scenarios)
         arr = (Scenario * S)()
@@ -291,7 +304,11 @@ class Evaluator:
         rej = t.empty(S, dtype=t.int32, device=self.device)
         first = t.empty(S, dtype=t.int32, device=self.device)
         ow = t.empty(S * Q, dtype=t.int32, device=self.device) if want_workers else None
-        ald_sweep_scenarios(self.h, S, arr, Q, ql, qp, rej, first, ow)
+        if heartbeat_every is None:
+            ald_sweep_scenarios(self.h, S, arr, Q, ql, qp, rej, first, ow)
+        else:
+            hb = np.broadcast_to(np.asarray(heartbeat_every, dtype=np.int32), (S,))
+            ald_sweep_scenarios_hb(self.h, S, arr, hb, Q, ql, qp, rej, first, ow)
         return (rej.cpu().numpy(), first.cpu().numpy(),
                 ow.cpu().numpy().reshape(S, Q) if want_workers else None)
 

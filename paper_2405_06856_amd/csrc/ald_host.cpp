@@ -691,15 +691,24 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
     return ALD_OK;
 }
 
-int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, int32_t Q, const int32_t* q_l_in,
-                        const int32_t* q_l_pred, int32_t* out_rejected, int32_t* out_first_reject,
-                        int32_t* out_worker)
+}  // extern "C"
+
+namespace {
+
+// The sweep, with a heartbeat period per scenario (H null: none).
+int sweep(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* H, int32_t Q, const int32_t* q_l_in,
+          const int32_t* q_l_pred, int32_t* out_rejected, int32_t* out_first_reject, int32_t* out_worker)
 {
     if (!h) return ALD_EINVAL;
     HIPCHK(h, hipSetDevice(h->device));
     if (S <= 0 || Q < 0) return fail(h, ALD_EINVAL, "S must be >= 1 and Q >= 0");
     if (!scen || !out_rejected || !out_first_reject) return fail(h, ALD_EINVAL, "null argument");
     if (Q > 0 && (!q_l_in || !q_l_pred)) return fail(h, ALD_EINVAL, "null query array");
+    bool any_hb = false;
+    for (int32_t s = 0; s < S && H; ++s) {
+        if (H[s] < 0) return fail(h, ALD_EINVAL, "heartbeat_every must be >= 0");
+        any_hb = any_hb || H[s] > 0;
+    }
     std::vector<Scen> sc(S);
     std::vector<int32_t> W(S), caps, Ms;
     int64_t NW = 0, slots = 0;
@@ -715,6 +724,12 @@ int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, i
         if (cap > HOT)
             return fail(h, ALD_EINVAL, "scenario " + std::to_string(s) + " admits more than " + std::to_string(HOT - 1) +
                                            " requests per worker");
+        if (H && H[s] > 0) {  // the 32-bit request state counts decode iterations (as in ald_place_stream)
+            const int64_t tau_final = (int64_t)Q / H[s] + 2;
+            if (tau_final >= ((int64_t)1 << 27) || cap * tau_final >= ((int64_t)1 << 27))
+                return fail(h, ALD_EOVERFLOW, "scenario " + std::to_string(s) + ": too many heartbeats for the "
+                                                                                  "32-bit request state");
+        }
         slots += scen[s].n_workers * (cap + 1);
     }
     if (NW > (1 << 30)) return fail(h, ALD_EINVAL, "too many workers");
@@ -742,6 +757,7 @@ int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, i
         c[s] = Ctl{};
         c[s].Q = Q;
         c[s].T = T;
+        c[s].H = H ? H[s] : 0;
         c[s].rebuild = 1;
         c[s].first_rej = INT32_MAX;
     }
@@ -758,12 +774,31 @@ int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, i
     HIPCHK(h, hipMemcpyAsync(a.dscen, a.hscen.data(), S * sizeof(Scen), hipMemcpyHostToDevice, h->stream));
     if (Q > 0) {
         HIPCHK(h, launch_query_stats(q_l_in, q_l_pred, Q, a.st.ctl, S, h->stream));
-        rc = run_rounds(h, &a, false, 0, c);
+        rc = run_rounds(h, &a, any_hb, 0, c);
         if (rc != ALD_OK) return rc;
     }
     HIPCHK(h, launch_sweep_outputs(a.st, out_rejected, out_first_reject, h->stream));
     HIPCHK(h, hipStreamSynchronize(h->stream));
     return ALD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, int32_t Q, const int32_t* q_l_in,
+                        const int32_t* q_l_pred, int32_t* out_rejected, int32_t* out_first_reject,
+                        int32_t* out_worker)
+{
+    return sweep(h, S, scen, nullptr, Q, q_l_in, q_l_pred, out_rejected, out_first_reject, out_worker);
+}
+
+int ald_sweep_scenarios_hb(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* heartbeat_every,
+                           int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred, int32_t* out_rejected,
+                           int32_t* out_first_reject, int32_t* out_worker)
+{
+    if (h && !heartbeat_every) return fail(h, ALD_EINVAL, "null heartbeat_every");
+    return sweep(h, S, scen, heartbeat_every, Q, q_l_in, q_l_pred, out_rejected, out_first_reject, out_worker);
 }
 
 int ald_rebalance(ald_handle_t h, int32_t P, const int32_t* n_workers, const ald_model_t* models,

@@ -394,6 +394,32 @@ def test_sweep_small_matches_oracle(aladdin):
     assert np.array_equal(first, ofirst)
 
 
+@pytest.mark.parametrize("tile", [64, 1024])
+def test_sweep_with_heartbeats_matches_oracle(aladdin, tile):
+    s = wl.make_sweep("mini-hb", 10, Q=2500, worker_counts=(1, 2, 3, 5, 16, 40), gpu_counts=(1, 2), base_capacity=65536,
+                      model=wl.BASE_MODEL, in_dist=wl.MID_IN, out_dist=wl.MID_OUT, rate=None)
+    H = np.array([0, 1, 2, 7, 25, 64, 100, 333, 1000, 2499, 2500, 5000], np.int32)
+    say("sweep with heartbeats, tile", tile)
+    ev = aladdin.Evaluator(0, tile=tile)
+    rej, first, workers = ev.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True, heartbeat_every=H)
+    ev.close()
+    orej, ofirst, oworkers = ref.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True, heartbeat_every=H,
+                                       n_threads=4)
+    assert np.array_equal(workers, oworkers)
+    assert np.array_equal(rej, orej)
+    assert np.array_equal(first, ofirst)
+
+
+def test_sweep_heartbeat_arguments_checked(aladdin):
+    s = wl.make_sweep("mini-hb", 11, Q=50, worker_counts=(2,), gpu_counts=(1,), base_capacity=6000,
+                      model=wl.BASE_MODEL, in_dist=wl.MID_IN, out_dist=wl.MID_OUT, rate=None)
+    ev = aladdin.Evaluator(0)
+    with pytest.raises(aladdin.AladdinError) as e:
+        ev.sweep(s.scenarios, s.q_l_in, s.q_l_pred, heartbeat_every=[-1])
+    assert e.value.code == aladdin.ALD_EINVAL
+    ev.close()
+
+
 def test_repeat_runs_bitwise_identical(aladdin):
     t = wl.make_config("medium")
     a = gpu_place(aladdin, t, tile=1024)

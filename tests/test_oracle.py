@@ -341,6 +341,23 @@ def test_sweep_equals_independent_places():
     assert rej.min() < rej.max()
 
 
+def test_sweep_with_heartbeats_equals_independent_places():
+    """Per-scenario heartbeat periods: each scenario is the single-stream
+    placement with that period (and the periods do change the result)."""
+    s = wl.make_sweep("mini", 10, Q=400, worker_counts=(2, 3, 6), gpu_counts=(1, 2), base_capacity=6000,
+                      model=wl.BASE_MODEL, in_dist=wl.MID_IN, out_dist=wl.MID_OUT, rate=None)
+    H = np.array([0, 1, 3, 17, 60, 400], np.int32)
+    rej, first, workers = ref.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True, n_threads=2,
+                                    heartbeat_every=H)
+    for i, sc in enumerate(s.scenarios):
+        r = ref.place(sc.n_workers, np.full(sc.n_workers, sc.kv_capacity, np.int64), None, None, None, None,
+                      sc.model, s.q_l_in, s.q_l_pred, heartbeat_every=int(H[i]))
+        assert np.array_equal(r.worker, workers[i])
+        assert rej[i] == int((r.worker < 0).sum())
+    r0, _, _ = ref.sweep(s.scenarios, s.q_l_in, s.q_l_pred)
+    assert not np.array_equal(r0, rej)
+
+
 def test_threads_do_not_change_results():
     t = wl.make_config("medium")
     a = ref.place_trace(t, n_threads=1)
