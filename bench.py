@@ -108,6 +108,28 @@ def time_sweep(steps: int):
             "queries": sw.n_queries, "min_total_gpus": gpus, "min_gpus_scenario": idx}
 
 
+def scaling_over_rates(rates=(100.0, 200.0, 300.0, 400.0, 500.0), gpus_per_worker: int = 1):
+    """Smallest cluster per arrival rate over the sweep's scenarios (heartbeat
+    every rate * T_dec queries) and the Eq. 7 line fitted through them.  The
+    rates keep the 16,384-query stream at 650 or more decode iterations, well
+    past a typical output length, so the clusters reach a steady state."""
+    from paper_2405_06856_amd import aladdin, scaling
+    from paper_2405_06856_amd import workloads as wl
+    sw = wl.make_config("sweep")
+    ev = aladdin.Evaluator(0, tile=1024)
+    t0 = time.perf_counter()
+    pts = scaling.min_cluster_per_rate(ev, sw, rates, gpus_per_worker)
+    dt = time.perf_counter() - t0
+    ev.close()
+    ok = [p for p in pts if p.workers is not None]
+    k5 = c5 = None
+    if len(ok) >= 2:
+        k5, c5 = scaling.fit_eq7([p.rate for p in ok], [p.workers for p in ok])
+    return {"gpus_per_worker": gpus_per_worker, "seconds": dt,
+            "points": [{"rate": p.rate, "heartbeat_every": p.heartbeat_every, "workers": p.workers} for p in pts],
+            "eq7_k5": k5, "eq7_c5": c5}
+
+
 def time_rebalance(steps: int, oracle_problems: int = 0):
     """Algorithm 2 over the 256-problem workload, inputs resident on the device;
     every call starts from the same placement (a device copy inside the loop)."""
@@ -175,6 +197,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--sweep-only", action="store_true", help="time only the scaling sweep (for profiling)")
     ap.add_argument("--no-rebalance", action="store_true")
+    ap.add_argument("--no-scaling", action="store_true", help="skip the smallest cluster per arrival rate")
     ap.add_argument("--rebalance-only", action="store_true", help="time only Algorithm 2 (for profiling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="also run a plain device-to-device copy of MIB MiB (a reference kernel of known "
@@ -269,6 +292,7 @@ def main():
 
     sweep_info = None if args.no_sweep else time_sweep(args.sweep_steps)
     rb_info = None if args.no_rebalance else time_rebalance(args.steps, 0 if args.no_cpu else 32)
+    scaling_info = None if (args.no_sweep or args.no_scaling) else scaling_over_rates()
     line = {
         "metric": "query x worker placement evals/sec (+ scenario sweeps/sec; % of HBM roofline)",
         "value": value,
@@ -296,6 +320,7 @@ def main():
         "load_ms": load_s * 1e3,
         "sweep": sweep_info,
         "rebalance": rb_info,
+        "scaling": scaling_info,
     }
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(trace)

@@ -14,6 +14,9 @@ from dataclasses import dataclass
 from typing import Optional
 
 import numpy as np
+# torch first: it loads the HIP runtime it was built with, which the library
+# then shares; loaded the other way round the process can hold two runtimes
+import torch  # noqa: F401
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libaladdin.so")

@@ -539,3 +539,4 @@ def test_rebalance_rejects_invalid_input():
         ref.rebalance(2, m, [], [], [], [], [], [5], [2])
     with pytest.raises(RuntimeError):  # no decode slope: the error line is undefined
         ref.rebalance(2, _rb_model(k2=0.0), [], [], [], [], [], [], [])
+

@@ -1,0 +1,51 @@
+"""The scaling layer over arrival rates (Sec. 4.4, Eq. 7): host arithmetic on
+CPU; the smallest cluster per rate on the GPU against the oracle's sweep."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from oracle import ref
+from paper_2405_06856_amd import scaling
+from paper_2405_06856_amd import workloads as wl
+
+
+def test_eq7_fit_recovers_a_line():
+    rates = [100.0, 250.0, 400.0, 900.0]
+    k5, c5 = scaling.fit_eq7(rates, [0.02 * r + 3.0 for r in rates])
+    assert abs(k5 - 0.02) < 1e-12 and abs(c5 - 3.0) < 1e-9
+    assert scaling.predict_workers(k5, c5, 500.0) == 13
+    assert scaling.predict_workers(0.02, 3.0, 510.0) == 14  # 13.2 rounds up
+    # noisy counts: the least-squares line through (0, 1), (1, 3), (2, 4)
+    k5, c5 = scaling.fit_eq7([0, 1, 2], [1, 3, 4])
+    assert abs(k5 - 1.5) < 1e-12 and abs(c5 - 7.0 / 6.0) < 1e-12
+    with pytest.raises(ValueError):
+        scaling.fit_eq7([5.0, 5.0], [1, 2])
+
+
+def test_heartbeat_period_of_a_rate():
+    assert scaling.heartbeat_period(500.0, 0.05) == 25
+    assert scaling.heartbeat_period(10.0, 0.05) == 1  # under one query per iteration
+
+
+@pytest.mark.gpu
+def test_min_cluster_per_rate_matches_oracle():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2405_06856_amd import aladdin
+    s = wl.make_sweep("rates", 12, Q=3000, worker_counts=range(1, 25), gpu_counts=(1, 2), base_capacity=65536,
+                      model=wl.BASE_MODEL, in_dist=wl.SHORT_IN, out_dist=wl.SHORT_OUT, rate=None)
+    rates = [20.0, 60.0, 140.0, 300.0]
+    ev = aladdin.Evaluator(0, tile=256)
+    got = scaling.min_cluster_per_rate(ev, s, rates, gpus_per_worker=1)
+    ev.close()
+    one = [i for i, sc in enumerate(s.scenarios) if sc.gpus_per_worker == 1]
+    for pt in got:
+        rej, _, _ = ref.sweep([s.scenarios[i] for i in one], s.q_l_in, s.q_l_pred, n_threads=4,
+                              heartbeat_every=pt.heartbeat_every)
+        ok = [s.scenarios[one[k]].n_workers for k in range(len(one)) if rej[k] == 0]
+        print("rate", pt.rate, "H", pt.heartbeat_every, "workers", pt.workers, flush=True)
+        assert pt.workers == (min(ok) if ok else None)
+    w = [pt.workers for pt in got]
+    assert None not in w and w == sorted(w) and w[0] < w[-1]
