@@ -60,6 +60,10 @@
  *  decoding at the end of h with zero slack, so s0 = -phi at placement (phi
  *  does not change within a window).
  *
+ *  Split-phase serving (Sec. 5): a decode worker receives requests whose
+ *  prefill ran elsewhere, so only (b) and (e) apply; an infinite TTFT SLO
+ *  marks such workers.
+ *
  *  Algorithm 2 (ora_rebalance, at the end of this file): per-worker errors of
  *  the output-length predictions and greedy moves of the new requests that
  *  lower the summed distance of the workers' error lines from the origin.
@@ -172,17 +176,20 @@ static int eval_pair(const worker_t* w, const ora_model_t* m, int64_t lin, int64
     o->rhs = m->theta * ((m->decode_slo - m->c3) - m->c2 * (double)b);
     o->dec_ok = o->lhs <= o->rhs;
 
-    /* (c) TTFT of this heartbeat's prefill batch including q */
+    /* (c) TTFT of this heartbeat's prefill batch including q.  A decode
+     * worker of split-phase serving (Sec. 5) runs no prefill: an infinite
+     * T_pre marks it, and then neither (c) nor (d) applies. */
+    const int decode_only = isinf(m->ttft_slo);
     const int64_t S1 = w->S1 + lin;
     const int64_t S2 = w->S2 + lin * lin;
     if (S2 >= ((int64_t)1 << 53)) return ORA_EOVERFLOW;
     o->ttft = (m->c1 + m->k1 * (double)S1) + m->k1q * (double)S2;
-    o->ttft_ok = o->ttft <= m->ttft_slo;
+    o->ttft_ok = decode_only || o->ttft <= m->ttft_slo;
 
     /* (d) the same prefill time against the ongoing requests' smallest slack */
     o->pre_ok = 1;
     int pre_near = 0;
-    if (use_d) {
+    if (use_d && !decode_only) {
         int any = 0;
         double smin = 0.0;
         for (int64_t i = 0; i < w->n; ++i) {
@@ -200,7 +207,7 @@ static int eval_pair(const worker_t* w, const ora_model_t* m, int64_t lin, int64
 
     o->feasible = o->kv_ok && o->dec_ok && o->ttft_ok && o->pre_ok;
     o->tdec = (m->c3 + m->c2 * (double)b) + m->k2 * sumD;
-    o->near_tie = near(o->lhs, o->rhs) || near(o->ttft, m->ttft_slo) || pre_near;
+    o->near_tie = near(o->lhs, o->rhs) || (!decode_only && near(o->ttft, m->ttft_slo)) || pre_near;
 
     /* rank key of Algorithm 1, before placement */
     const unsigned __int128 x = (unsigned __int128)(B * ((int64_t)1 << gs));
@@ -291,8 +298,8 @@ static void free_workers(worker_t* ws, int32_t W)
 static int valid_model(const ora_model_t* m)
 {
     if (!(isfinite(m->c1) && isfinite(m->k1) && isfinite(m->k1q) && isfinite(m->c3) &&
-          isfinite(m->c2) && isfinite(m->k2) && isfinite(m->ttft_slo) && isfinite(m->decode_slo) &&
-          isfinite(m->theta))) return 0;
+          isfinite(m->c2) && isfinite(m->k2) && (isfinite(m->ttft_slo) || m->ttft_slo == INFINITY) &&
+          isfinite(m->decode_slo) && isfinite(m->theta))) return 0;
     if (m->gamma_log2den < 0 || m->gamma_log2den > 8) return 0;
     if (m->gamma_num < 0 || m->gamma_num > (1 << m->gamma_log2den)) return 0;
     return 1;

@@ -15,6 +15,7 @@ form from the oracle:
   large to small with ties to the lower index, then the first feasible worker.
 * A heartbeat drops the first element of every footprint vector (one decode
   iteration has run); empty vectors leave.
+* Split-phase serving: a decode worker (infinite TTFT SLO) checks only (b) and (e).
 * Constraint (d), with decode history: every request keeps its generated-token
   count g and decode time t_dec literally (exact rationals); a heartbeat's
   iteration time is Eq. 3, (c3 + c2*b) + k2*sum(context), over the batch before
@@ -80,6 +81,7 @@ def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0, u
     fp64 rounding could decide it (those queries are not comparable bit for bit)."""
     gamma = Fraction(model.gamma_num, 2 ** model.gamma_log2den)
     F = Fraction
+    decode_only = math.isinf(model.ttft_slo)  # a decode worker of split-phase serving
     out = []
     since = 0
     for (l_in, l_pred) in queries:
@@ -96,13 +98,21 @@ def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0, u
             sumD = sum(F(c) + gamma * F(r) for c, r, _, _, _, _ in w.meta) + F(l_in) + gamma * F(l_pred)
             ld = (F(model.decode_slo) - F(model.c3) - F(model.c2) * b) / F(model.k2)
             dec_ok = sumD <= F(model.theta) * ld
+            lim = F(model.theta) * ld
+            if abs(lim - sumD) <= F(1, 10 ** 9) * max(abs(lim), abs(sumD)):
+                close = True
+            if decode_only:
+                # split-phase decode worker: the prefill ran elsewhere, only (b) and (e)
+                feas.append(kv_ok and dec_ok)
+                sumD_now = sum(F(c) + gamma * F(r) for c, r, _, _, _, _ in w.meta)
+                norms.append(math.hypot(float(w.batch()), float(sumD_now)))
+                peaks.append(peak)
+                continue
             S1 = sum(F(li) for _, _, li, new, _, _ in w.meta if new) + F(l_in)
             S2 = sum(F(li) ** 2 for _, _, li, new, _, _ in w.meta if new) + F(l_in) ** 2
             ttft = F(model.c1) + F(model.k1) * S1 + F(model.k1q) * S2
             ttft_ok = ttft <= F(model.ttft_slo)
-            lim = F(model.theta) * ld
-            if abs(lim - sumD) <= F(1, 10 ** 9) * max(abs(lim), abs(sumD)) or \
-               abs(F(model.ttft_slo) - ttft) <= F(1, 10 ** 9) * max(abs(ttft), abs(F(model.ttft_slo))):
+            if abs(F(model.ttft_slo) - ttft) <= F(1, 10 ** 9) * max(abs(ttft), abs(F(model.ttft_slo))):
                 close = True
             pre_ok = True
             ongoing = [F(model.decode_slo) * g - td for _, _, _, new, g, td in w.meta if not new]

@@ -8,6 +8,7 @@ literally with a floating-point capacity_norm.
 from __future__ import annotations
 
 import dataclasses
+import math
 import json
 import os
 
@@ -136,6 +137,49 @@ def test_placement_matches_bruteforce(H):
                 assert res.kv_peak_chosen[k] == wq["peaks"][wq["worker"]]
             compared += 1
     assert compared > 1500
+
+
+@pytest.mark.parametrize("H", [0, 2])
+def test_decode_workers_match_bruteforce(H):
+    """Split-phase decode workers (infinite TTFT SLO): only (b) and (e), even
+    with a decode history; against the brute force, and the TTFT limit of the
+    same model with a finite SLO does bind in this population."""
+    rng = np.random.default_rng(500 + H)
+    compared = differ = 0
+    for case in range(300):
+        W = int(rng.integers(1, 5))
+        model = _random_model(rng)
+        model = dataclasses.replace(model, c1=float(rng.uniform(0.0, 0.02)), k1=float(rng.uniform(0.0, 0.004)),
+                                    ttft_slo=0.03)
+        dmodel = dataclasses.replace(model, ttft_slo=math.inf)
+        residents, t_dec = [], []
+        for _ in range(W):
+            rs, ts = [], []
+            for _ in range(int(rng.integers(0, 6))):
+                lp = int(rng.integers(1, 9))
+                g = int(rng.integers(0, lp))
+                rs.append((int(rng.integers(1, 9)), lp, g))
+                ts.append(float(rng.uniform(0.0, 2.0)) * g * model.decode_slo)
+            residents.append(rs)
+            t_dec.append(ts)
+        M = [int(rng.integers(8, 60)) for _ in range(W)]
+        queries = [(int(rng.integers(1, 9)), int(rng.integers(1, 9))) for _ in range(int(rng.integers(1, 12)))]
+        res = run(W, M, residents, dmodel, queries, H=H, t_dec=t_dec)
+        fin = run(W, M, residents, model, queries, H=H)
+        differ += int(not np.array_equal(res.worker, fin.worker))
+        bw = [BruteWorker(M[i], [Req(a, b, g) for (a, b, g) in residents[i]]) for i in range(W)]
+        want = brute_place(bw, dmodel, queries, heartbeat_every=H)
+        for k, wq in enumerate(want):
+            if wq["close"]:
+                break
+            norms = sorted(wq["norms"])
+            if any(0 < b - a <= 1e-12 * b for a, b in zip(norms, norms[1:])):
+                break
+            assert res.worker[k] == wq["worker"], (case, k)
+            assert res.n_feasible[k] == wq["n_feasible"], (case, k)
+            assert res.near_tie[k] == 0 or wq["close"]
+            compared += 1
+    assert compared > 1000 and differ > 30
 
 
 @pytest.mark.parametrize("H", [0, 1, 3])

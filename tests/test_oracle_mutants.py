@@ -34,7 +34,8 @@ MUTANTS = [
     ("near tie absolute", "return fabs(x - y) <= 1e-9 * m;", "return fabs(x - y) <= 1e-9;"),
     ("KV check strict", "o->kv_ok = o->peak <= w->M;", "o->kv_ok = o->peak < w->M;"),
     ("decode check strict", "o->dec_ok = o->lhs <= o->rhs;", "o->dec_ok = o->lhs < o->rhs;"),
-    ("TTFT check strict", "o->ttft_ok = o->ttft <= m->ttft_slo;", "o->ttft_ok = o->ttft < m->ttft_slo;"),
+    ("TTFT check strict", "o->ttft_ok = decode_only || o->ttft <= m->ttft_slo;",
+     "o->ttft_ok = decode_only || o->ttft < m->ttft_slo;"),
     ("heartbeat counts only placements", "if (H > 0 && !no_commit) {\n            since_hb += 1;",
      "if (H > 0 && !no_commit && best >= 0) {\n            since_hb += 1;"),
     ("smallest excess over feasible workers only", "if (ex < excess_min) excess_min = ex;",
@@ -50,6 +51,9 @@ MUTANTS = [
     ("(d) iteration time without the batch term", "(m->c3 + m->c2 * (double)w->n)", "(m->c3 + m->c2 * (double)(w->n - 1))"),
     ("(d) resident slack from the predicted length", "s0 = model->decode_slo * (double)g - res_tdec[k];",
      "s0 = model->decode_slo * (double)lp - res_tdec[k];"),
+    # split-phase decode workers
+    ("decode workers still check (d)", "if (use_d && !decode_only) {", "if (use_d) {"),
+    ("decode workers flag TTFT near ties", "(!decode_only && near(o->ttft, m->ttft_slo))", "near(o->ttft, m->ttft_slo)"),
     # Algorithm 2
     ("A2 over-estimate error with the sign flipped", "le[i] += (int64_t)old_lreal[j] - old_lpred[j]; be[i] -= 1;",
      "le[i] += (int64_t)old_lpred[j] - old_lreal[j]; be[i] -= 1;"),
@@ -84,6 +88,8 @@ PINS = [
     lambda: pins.test_preemption_limit_matches_bruteforce(3),
     pins.test_preemption_limit_worked_example,
     pins.test_preemption_limit_needs_an_ongoing_request,
+    lambda: pins.test_decode_workers_match_bruteforce(0),
+    lambda: pins.test_decode_workers_match_bruteforce(2),
     pins.test_rebalance_worked_example,
     pins.test_rebalance_errors_closed_forms,
     pins.test_rebalance_request_moves_at_most_once,
