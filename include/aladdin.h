@@ -74,7 +74,9 @@ typedef struct ald_handle* ald_handle_t;
 typedef struct {
     double c1, k1, k1q;        /* prefill: T_p = (c1 + k1*S1) + k1q*S2            (Eq. 2) */
     double c3, c2, k2;         /* decode:  T_d = (c3 + c2*b) + k2*context          (Eq. 3) */
-    double ttft_slo;           /* T_pre, seconds                                   (Table 1) */
+    double ttft_slo;           /* T_pre, seconds                                   (Table 1);
+                                  +INFINITY: a decode worker of split-phase serving (Sec. 5),
+                                  where only (b) and (e) apply (no TTFT, no (d)) */
     double decode_slo;         /* T_dec, seconds per output token; must exceed c3  (Eq. 4) */
     double theta;              /* prediction-error knob of constraint (b), in (0, 1] */
     int32_t gamma_num;         /* strictness knob gamma = gamma_num / 2^gamma_log2den, */

@@ -217,7 +217,8 @@ __device__ __forceinline__ Latency latency(const Scen& sc, const View& v, int32_
     // (c) and (d) bound the same prefill time
     const bool has_d = v.dlim != INFINITY;
     o.ttft_ok = o.ttft <= sc.ttft && (!has_d || o.ttft <= v.dlim);
-    o.nt = near_tie(o.lhs, v.rhs) || near_tie(o.ttft, sc.ttft) || (has_d && near_tie(o.ttft, v.dlim));
+    o.nt = near_tie(o.lhs, v.rhs) || (sc.ttft != INFINITY && near_tie(o.ttft, sc.ttft)) ||
+           (has_d && near_tie(o.ttft, v.dlim));
     o.tdec = (sc.c3 + sc.c2 * (double)b) + o.lhs;
     return o;
 }

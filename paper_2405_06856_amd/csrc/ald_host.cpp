@@ -88,12 +88,14 @@ int fail(ald_handle* h, int code, const std::string& msg)
             return fail((h), ALD_EHIP, std::string(#call) + ": " + hipGetErrorString(e_)); \
     } while (0)
 
+// Finite coefficients; the TTFT SLO may also be +inf (a decode worker of
+// split-phase serving: no prefill runs there, so (c) and (d) do not apply).
 bool finite_model(const ald_model_t& m)
 {
-    const double v[] = {m.c1, m.k1, m.k1q, m.c3, m.c2, m.k2, m.ttft_slo, m.decode_slo, m.theta};
+    const double v[] = {m.c1, m.k1, m.k1q, m.c3, m.c2, m.k2, m.decode_slo, m.theta};
     for (double x : v)
         if (!std::isfinite(x)) return false;
-    return true;
+    return std::isfinite(m.ttft_slo) || m.ttft_slo == INFINITY;
 }
 
 // Reasons a model is unusable, or empty.
@@ -139,6 +141,7 @@ bool nt_integer(const Scen& s, int32_t capmax)
     const double wd = 3e-9 * rmax / std::ldexp(s.k2, -s.gs) + 3.0;
     const double tstep = s.k1 + s.k1q;
     if (!(tstep > 0.0)) return false;
+    if (s.ttft == INFINITY) return wd <= 64.0;  // no TTFT band
     const double wt = (3e-9 * std::fabs(s.ttft) + 2e-15 * (std::fabs(s.c1) + std::fabs(s.ttft))) / tstep + 3.0;
     return wd <= 64.0 && wt <= 64.0;
 }
@@ -572,7 +575,7 @@ int load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const int6
     h->main = nullptr;
     Arena* a = new Arena();
     std::vector<Scen> sc(1, make_scen(*model));
-    sc[0].use_d = res_t_dec != nullptr ? 1 : 0;
+    sc[0].use_d = (res_t_dec != nullptr && model->ttft_slo != INFINITY) ? 1 : 0;
     int rc = make_arena(h, a, sc, std::vector<int32_t>(1, W), caps, Ms);
     if (rc == ALD_OK) rc = layout_scratch(h, a, 256, 4096);
     if (rc != ALD_OK) { delete a; return rc; }

@@ -227,10 +227,14 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
             const int64_t l = wave_last_true(1, LMAX, [&](int64_t v) { const double t = tt(v); return t <= sc.ttft && t <= dl; });
             if (l0) st.lthr[gw] = (int32_t)l;
         } else {
-            const double band = tie_band(sc.ttft);
-            const double lo = sc.ttft - band, hi = sc.ttft + band;
-            const int64_t ll = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) < lo; }) + 1;
-            const int64_t lh = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) <= hi; });
+            // the TTFT band (empty on a decode worker, whose T_pre is +inf)
+            int64_t ll = 1, lh = 0;
+            if (sc.ttft != INFINITY) {
+                const double band = tie_band(sc.ttft);
+                const double lo = sc.ttft - band, hi = sc.ttft + band;
+                ll = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) < lo; }) + 1;
+                lh = wave_last_true(1, LMAX, [&](int64_t v) { return tt(v) <= hi; });
+            }
             const int64_t width = lh - ll + 1;
             const uint64_t mask = ballot(lane_id() < width && near_tie(tt(ll + lane_id()), sc.ttft));
             if (l0) {

@@ -13,6 +13,7 @@ from __future__ import annotations
 import dataclasses
 import hashlib
 import json
+import math
 import os
 
 import numpy as np
@@ -117,6 +118,25 @@ def test_ttft_not_monotone_in_lin(aladdin, k1, k1q):
     model = dataclasses.replace(wl.BASE_MODEL, k1=k1, k1q=k1q, ttft_slo=0.03)
     t = wl.make_trace("ttft_nm", 23, W=20, R=10, Q=900, kv_capacity=30000, model=model, heartbeat_every=50)
     compare(*gpu_place(aladdin, t, tile=128), ref.place_trace(t), "ttft_nm")
+
+
+@pytest.mark.parametrize("case", ["integer", "fp64", "history"])
+def test_decode_workers_match_oracle(aladdin, case):
+    """Split-phase decode workers (TTFT SLO +inf): only (b) and (e) are checked;
+    with the integer thresholds, with the fp64 checks (a negative prefill
+    coefficient), and with a decode history that (d) must then ignore."""
+    m = dataclasses.replace(wl.BASE_MODEL, ttft_slo=math.inf)
+    if case == "fp64":
+        m = dataclasses.replace(m, k1=-1e-7, k1q=1e-9)
+    t = wl.make_trace("decode-" + case, 25, W=16, R=24, Q=3000, kv_capacity=30000, model=m, heartbeat_every=60)
+    if case == "history":
+        t = wl.with_decode_history(t, 11)
+    say("decode workers", case)
+    for tile in (64, 1024):
+        compare(*gpu_place(aladdin, t, tile=tile), ref.place_trace(t), "decode/%s/%d" % (case, tile))
+    # the same stream with a finite TTFT SLO places differently
+    fin = dataclasses.replace(t, model=dataclasses.replace(m, ttft_slo=0.02))
+    assert not np.array_equal(ref.place_trace(fin).worker, ref.place_trace(t).worker)
 
 
 @pytest.mark.parametrize("seed", range(3))
