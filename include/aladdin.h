@@ -148,6 +148,21 @@ int ald_load_workers_history(ald_handle_t handle, int32_t W, const ald_model_t* 
 int ald_place_stream(ald_handle_t handle, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
                      int32_t heartbeat_every, int32_t* out_worker, ald_query_diag_t* out_diag);
 
+/* Grouped placement (App. A, distributed scheduling): the loaded workers are
+ * split into G consecutive groups of group_workers[g] workers (host array,
+ * each >= 1, summing to W); query x of the stream (counted across calls since
+ * the load) goes to group x mod G (round robin), and each group places its own
+ * queries on its own workers in arrival order with Algorithm 1, as its own
+ * scheduler would.  Device arrays as for ald_place_stream; out_worker gets
+ * the global worker index (or -1) and out_diag (or NULL) each query's
+ * diagnostics over its group's workers.  heartbeat_every must be a multiple of
+ * G (every heartbeat window then holds heartbeat_every / G queries of every
+ * group), and with heartbeats the call must end at one.  Grouped and ungrouped
+ * calls may alternate on one handle. */
+int ald_place_grouped(ald_handle_t handle, int32_t G, const int32_t* group_workers, int32_t Q,
+                      const int32_t* q_l_in, const int32_t* q_l_pred, int32_t heartbeat_every,
+                      int32_t* out_worker, ald_query_diag_t* out_diag);
+
 /* Scaling sweep: S scenarios (host array scen[S]), each starting with empty
  * workers, each placing the same Q queries (device arrays) with no heartbeat.
  * Device outputs: out_rejected[S], out_first_reject[S] (-1 if none) and, if not

@@ -50,7 +50,7 @@ DIAG_DTYPE = np.dtype([("n_feasible", "<i4"), ("near_tie", "<i4"), ("kv_peak_cho
 assert DIAG_DTYPE.itemsize == 40
 
 SYMBOLS = ("ald_create", "ald_destroy", "ald_set_tile", "ald_load_workers", "ald_load_workers_history",
-           "ald_place_stream",
+           "ald_place_stream", "ald_place_grouped",
            "ald_sweep_scenarios", "ald_sweep_scenarios_hb", "ald_rebalance", "ald_worker_summary", "ald_set_profiling", "ald_kernel_time",
            "ald_last_error", "ald_strerror")
 
@@ -67,6 +67,7 @@ def _load():
         "ald_load_workers": ([P, i32, ctypes.POINTER(Model), P, P, P, P, P, i32], ctypes.c_int),
         "ald_load_workers_history": ([P, i32, ctypes.POINTER(Model), P, P, P, P, P, P, i32], ctypes.c_int),
         "ald_place_stream": ([P, i32, P, P, i32, P, P], ctypes.c_int),
+        "ald_place_grouped": ([P, i32, P, i32, P, P, i32, P, P], ctypes.c_int),
         "ald_sweep_scenarios": ([P, i32, P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_sweep_scenarios_hb": ([P, i32, P, P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_rebalance": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P], ctypes.c_int),
@@ -136,6 +137,16 @@ def ald_load_workers_history(h, W: int, model: Model, kv_capacity, res_offsets, 
 def ald_place_stream(h, Q: int, q_l_in, q_l_pred, heartbeat_every: int, out_worker, out_diag=None) -> None:
     _check(h, _L.ald_place_stream(h, int(Q), _dptr(q_l_in), _dptr(q_l_pred), int(heartbeat_every),
                                   _dptr(out_worker), _dptr(out_diag)))
+
+
+def ald_place_grouped(h, G: int, group_workers, Q: int, q_l_in, q_l_pred, heartbeat_every: int, out_worker,
+                      out_diag=None) -> None:
+    """group_workers: host array of G group sizes."""
+    gw = np.ascontiguousarray(group_workers, dtype=np.int32)
+    if gw.shape != (G,):
+        raise ValueError("group_workers must hold G sizes")
+    _check(h, _L.ald_place_grouped(h, int(G), gw.ctypes.data_as(ctypes.c_void_p), int(Q), _dptr(q_l_in),
+                                   _dptr(q_l_pred), int(heartbeat_every), _dptr(out_worker), _dptr(out_diag)))
 
 
 def ald_sweep_scenarios(h, S: int, scen, Q: int, q_l_in, q_l_pred, out_rejected, out_first_reject,
@@ -281,6 +292,20 @@ class Evaluator:
         res = Placement(worker=out.cpu().numpy())
         if d is not None:
             res.diag = d.cpu().numpy().view(DIAG_DTYPE)
+        return res
+
+    def place_grouped(self, group_workers, q_l_in, q_l_pred, heartbeat_every=0, diag=True) -> Placement:
+        """Grouped placement (App. A): query x of the stream goes to group x mod G."""
+        t = self.torch
+        ql = self._dev(q_l_in, t.int32)
+        qp = self._dev(q_l_pred, t.int32)
+        Q = int(ql.numel())
+        out = t.empty(max(Q, 1), dtype=t.int32, device=self.device)
+        d = t.empty(max(Q, 1) * DIAG_DTYPE.itemsize, dtype=t.uint8, device=self.device) if diag else None
+        ald_place_grouped(self.h, len(group_workers), group_workers, Q, ql, qp, heartbeat_every, out, d)
+        res = Placement(worker=out[:Q].cpu().numpy())
+        if diag:
+            res.diag = d[:Q * DIAG_DTYPE.itemsize].cpu().numpy().view(DIAG_DTYPE)
         return res
 
     def summary(self):

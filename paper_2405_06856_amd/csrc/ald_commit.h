@@ -670,8 +670,8 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
         int32_t lin = 1, lp = 1;
         if (act) {
             q = st.qsum[sc.qsum_off + (i - start)];
-            lin = st.q_lin[i];
-            lp = st.q_lpred[i];
+            lin = st.q_lin[q_at(sc, i)];
+            lp = st.q_lpred[q_at(sc, i)];
         } else {
             q.nfeas = 0;
         }
@@ -690,8 +690,8 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
             const int abl = am ? __ffsll((unsigned long long)am) - 1 : NT;
             const int lim = min(p, abl);
             if (act && lane >= cur && lane < lim) {
-                if (st.out_worker) st.out_worker[sc.out_off + i] = -1;
-                if (want_diag) st.out_diag[i] = dr;
+                if (st.out_worker) st.out_worker[sc.out_off + q_at(sc, i)] = -1;
+                if (want_diag) st.out_diag[q_at(sc, i)] = dr;
             }
             const uint64_t rm = ballot(act && lane >= cur && lane < lim);
             nrej += __popcll(rm);
@@ -719,8 +719,8 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
                 break;
             }
             if (lane == 0) {
-                if (st.out_worker) st.out_worker[sc.out_off + ip] = dc.w;
-                if (want_diag) st.out_diag[ip] = dc.d;
+                if (st.out_worker) st.out_worker[sc.out_off + q_at(sc, ip)] = dc.w < 0 ? dc.w : dc.w + sc.out_add;
+                if (want_diag) st.out_diag[q_at(sc, ip)] = dc.d;
             }
             cur = p + 1;
             // a scanned worker that does not take the query keeps its exact peak

@@ -62,6 +62,9 @@ struct ald_handle {
     int32_t tau = 0, hb_index = 0, since_hb = 0, round = 0;
     bool rebuild_pending = false;  // the last call ended with a heartbeat: every worker is stale
     bool dirty_pending = false;    // the last commit round left workers with stale summaries
+    bool check_all = false;        // stale workers are not listed (after grouped placement): check every one
+    int64_t qcount = 0;            // queries processed since the load (routes grouped placement)
+    Arena* grouped = nullptr;      // scenario view of the loaded workers for grouped placement
     int32_t* err_word = nullptr;
     int32_t prof = 0;  // kernel kinds timed (bit k = kind k)
     std::vector<Events> pending;
@@ -154,6 +157,7 @@ Scen make_scen(const ald_model_t& m)
     s.ttft = m.ttft_slo; s.tdec = m.decode_slo; s.theta = m.theta;
     s.gn = m.gamma_num; s.gs = m.gamma_log2den;
     s.mono = (m.k1 >= 0.0 && m.k1q >= 0.0) ? 1 : 0;
+    s.q_stride = 1;
     return s;
 }
 
@@ -403,6 +407,7 @@ int64_t rounds_needed(const std::vector<Ctl>& c)
         int32_t pos = x.start, since = x.since_hb;
         while (pos < x.Q) {
             int32_t end = tile_end(pos, x.Q, x.T, x.H, since);
+            if (end <= pos) return -1;  // a tile that cannot advance (never set up so)
             since += end - pos;
             if (x.H > 0 && since >= x.H) since = 0;
             pos = end;
@@ -432,6 +437,7 @@ int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, 
     bool first = true;
     for (;;) {
         int64_t need = rounds_needed(hc);
+        if (need < 0) return fail(h, ALD_EHIP, "internal error: a tile of no queries");
         if (need == 0) break;
         for (int64_t r = 0; r < need; ++r) {
             const int mode = first ? first_mode : (build_every_round ? 0 : 1);
@@ -494,6 +500,7 @@ int ald_destroy(ald_handle_t h)
     if (!h) return ALD_OK;
     (void)hipSetDevice(h->device);
     (void)hipStreamSynchronize(h->stream);
+    delete h->grouped;
     delete h->main;
     delete h->sweep;
     (void)hipFree(h->err_word);
@@ -571,6 +578,8 @@ int load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const int6
     if (total * 24 > ((int64_t)64 << 30)) return fail(h, ALD_EINVAL, "worker state would exceed 64 GiB");
 
     HIPCHK(h, hipStreamSynchronize(h->stream));
+    delete h->grouped;
+    h->grouped = nullptr;
     delete h->main;
     h->main = nullptr;
     Arena* a = new Arena();
@@ -609,7 +618,8 @@ int load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const int6
     h->model = *model;
     h->max_cap = maxcap;
     h->tau = h->hb_index = h->since_hb = h->round = 0;
-    h->rebuild_pending = h->dirty_pending = false;
+    h->rebuild_pending = h->dirty_pending = h->check_all = false;
+    h->qcount = 0;
     return ALD_OK;
 }
 }  // namespace
@@ -681,16 +691,190 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
     std::vector<Ctl> hc(1, c);
     // first build: every worker after a heartbeat, the last commit round's
     // workers if it changed any, else nothing
-    const int first_mode = (rebuild || H > 0) ? 0 : (h->dirty_pending ? 1 : -1);
+    const int first_mode = (rebuild || H > 0 || h->check_all) ? 0 : (h->dirty_pending ? 1 : -1);
     rc = run_rounds(h, a, H > 0, first_mode, hc);
     if (rc != ALD_OK) return rc;
     c = hc[0];
+    h->qcount += Q;
+    h->check_all = false;
     h->tau = c.tau;
     h->hb_index = c.hb_index;
     h->since_hb = c.since_hb;
     h->round = c.round;
     h->rebuild_pending = c.rebuild != 0;
     h->dirty_pending = c.ndirty > 0;
+    return ALD_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Group g's queries among global positions [a, b) when query x goes to group x mod G.
+int64_t group_count(int64_t a, int64_t b, int32_t G, int32_t g)
+{
+    auto upto = [&](int64_t n) {  // x in [0, n) with x mod G == g (n >= 0)
+        return n <= g ? 0 : (n - 1 - g) / G + 1;
+    };
+    return upto(b) - upto(a);
+}
+
+// A scenario view of the loaded workers, one scenario per group: the worker
+// arrays are the loaded arena's, the control and scratch arrays its own.
+int grouped_view(ald_handle* h, int32_t G, const int32_t* sizes)
+{
+    Arena* m = h->main;
+    if (!h->grouped) h->grouped = new Arena();
+    Arena& a = *h->grouped;
+    a.S = G;
+    a.NW = m->NW;
+    a.hW.assign(sizes, sizes + G);
+    a.hscen.assign(G, m->hscen[0]);
+    int32_t wb = 0;
+    for (int32_t g = 0; g < G; ++g) {
+        a.hscen[g].W = sizes[g];
+        a.hscen[g].wbase = wb;
+        wb += sizes[g];
+    }
+    a.eval_mode = m->eval_mode;
+    a.use_d = m->use_d;
+    a.st = m->st;  // worker and slot arrays
+    Carver c{nullptr};
+    Ctl* ctl = nullptr;
+    TileInfo* ti = nullptr;
+    int32_t* dlist = nullptr;
+    int32_t* dcount = nullptr;
+    Scen* dscen = nullptr;
+    auto carve = [&](Carver& k) {
+        k.take(&ctl, G); k.take(&ti, G); k.take(&dscen, G); k.take(&dlist, (size_t)G * MAX_DIRTY); k.take(&dcount, G);
+    };
+    carve(c);
+    if (c.off > a.mem_bytes) {
+        if (a.mem) HIPCHK(h, hipFree(a.mem));
+        a.mem = nullptr;
+        a.mem_bytes = 0;
+        HIPCHK(h, hipMalloc(&a.mem, c.off));
+        a.mem_bytes = c.off;
+    }
+    Carver k{(char*)a.mem};
+    carve(k);
+    a.dscen = dscen;
+    a.st.scen = dscen;
+    a.st.ctl = ctl;
+    a.st.tinfo = ti;
+    a.st.dlist = dlist;
+    a.st.dcount = dcount;
+    a.st.qbad = nullptr;  // the queries are checked up front
+    a.st.S = G;
+    HIPCHK(h, hipMemsetAsync(dcount, 0, G * sizeof(int32_t), h->stream));
+    a.T = 0;  // lay the scratch out again
+    return ALD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ald_place_grouped(ald_handle_t h, int32_t G, const int32_t* group_workers, int32_t Q, const int32_t* q_l_in,
+                      const int32_t* q_l_pred, int32_t heartbeat_every, int32_t* out_worker,
+                      ald_query_diag_t* out_diag)
+{
+    if (!h) return ALD_EINVAL;
+    HIPCHK(h, hipSetDevice(h->device));
+    if (!h->main) return fail(h, ALD_ESTATE, "ald_load_workers has not been called");
+    if (G < 1 || !group_workers) return fail(h, ALD_EINVAL, "G must be >= 1 with a size per group");
+    int64_t wsum = 0;
+    for (int32_t g = 0; g < G; ++g) {
+        if (group_workers[g] < 1) return fail(h, ALD_EINVAL, "every group needs a worker");
+        wsum += group_workers[g];
+    }
+    if (wsum != h->W) return fail(h, ALD_EINVAL, "the group sizes must add up to the loaded worker count");
+    const int32_t H = heartbeat_every;
+    if (Q < 0 || H < 0) return fail(h, ALD_EINVAL, "Q and heartbeat_every must be >= 0");
+    if (H % G != 0) return fail(h, ALD_EINVAL, "heartbeat_every must be a multiple of G");
+    if (Q == 0) return ALD_OK;
+    if (!q_l_in || !q_l_pred || !out_worker) return fail(h, ALD_EINVAL, "null argument");
+    int32_t tau = h->tau, hb = h->hb_index, since = h->since_hb;
+    bool rebuild = h->rebuild_pending;
+    if (H > 0 && since >= H) {  // a heartbeat already due from an earlier, longer period
+        tau += 1;
+        hb += 1;
+        since = 0;
+        rebuild = true;
+    }
+    // Each group keeps its own heartbeat clock within the call; they agree
+    // again (and with the stream's) at every heartbeat, so a call with
+    // heartbeats ends at one.
+    if (H > 0 && ((int64_t)since + Q) % H != 0)
+        return fail(h, ALD_EINVAL, "with heartbeats a grouped call must end at a heartbeat (the stream's position "
+                                   "in its heartbeat window plus Q a multiple of heartbeat_every)");
+    const int64_t tau_final = (int64_t)tau + (H > 0 ? (int64_t)Q / H + 2 : 0);
+    if (tau_final >= ((int64_t)1 << 27) || (int64_t)h->max_cap * tau_final >= ((int64_t)1 << 27))
+        return fail(h, ALD_EOVERFLOW, "too many heartbeats for the 32-bit request state");
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    int rc = grouped_view(h, G, group_workers);
+    if (rc != ALD_OK) return rc;
+    Arena& a = *h->grouped;
+    // query x (counted since the load) goes to group x mod G; each window of H
+    // queries holds H / G of every group, so every group's heartbeat period is
+    // H / G of its own queries and its position in the window is counted here
+    const int64_t P0 = h->qcount, W0 = P0 - since;
+    const int32_t Hg = H / G;
+    std::vector<Ctl> c(G);
+    int32_t qmax = 1;
+    for (int32_t g = 0; g < G; ++g) {
+        Scen& sc = a.hscen[g];
+        const int32_t first = (int32_t)(((g - P0) % G + G) % G);  // first query of the call in group g
+        sc.q_first = first;
+        sc.q_stride = G;
+        sc.out_off = 0;
+        sc.out_add = sc.wbase;
+        Ctl& x = c[g];
+        x = Ctl{};
+        x.Q = first < Q ? (Q - 1 - first) / G + 1 : 0;
+        x.H = Hg;
+        x.since_hb = (int32_t)group_count(W0, P0, G, g);
+        x.tau = tau;
+        x.hb_index = hb;
+        x.rebuild = rebuild ? 1 : 0;
+        if (Hg > 0 && x.since_hb >= Hg) {  // this group finished its window: its heartbeat comes first
+            x.tau += 1;
+            x.hb_index += 1;
+            x.since_hb = 0;
+            x.rebuild = 1;
+        }
+        x.first_rej = INT32_MAX;
+        qmax = std::max(qmax, x.Q);
+    }
+    int32_t T = std::min(h->tile, qmax);
+    if (Hg > 0) T = std::min(T, Hg);
+    for (Ctl& x : c) x.T = T;
+    rc = layout_scratch(h, &a, T, 2048 * 256 / EVAL_THREADS);  // also copies the scenario table
+    if (rc != ALD_OK) return rc;
+    std::vector<TileInfo> ti(G);
+    for (auto& t : ti) { t = TileInfo{}; t.first_pc[0] = t.first_pc[1] = INT32_MAX; }
+    HIPCHK(h, hipMemcpyAsync(a.st.ctl, c.data(), G * sizeof(Ctl), hipMemcpyHostToDevice, h->stream));
+    HIPCHK(h, hipMemcpyAsync(a.st.tinfo, ti.data(), G * sizeof(TileInfo), hipMemcpyHostToDevice, h->stream));
+    a.st.q_lin = q_l_in;
+    a.st.q_lpred = q_l_pred;
+    a.st.out_worker = out_worker;
+    a.st.out_diag = (Diag*)out_diag;
+    a.st.err_word = h->err_word;
+    HIPCHK(h, launch_query_stats(q_l_in, q_l_pred, Q, a.st.ctl, G, h->stream));
+    rc = run_rounds(h, &a, H > 0, 0, c);
+    if (rc != ALD_OK) return rc;
+    // the call's state as one stream: heartbeats after every H queries
+    const int64_t total = (int64_t)since + Q;
+    const int64_t fired = H > 0 ? total / H : 0;
+    h->tau = tau + (int32_t)fired;
+    h->hb_index = hb + (int32_t)fired;
+    h->since_hb = (int32_t)(total - fired * H);
+    h->qcount += Q;
+    // a call with heartbeats ended at one (workers not yet rebuilt), and the
+    // groups' lists of changed workers are not the loaded arena's
+    h->rebuild_pending = rebuild || fired > 0;
+    h->dirty_pending = false;
+    h->check_all = true;
     return ALD_OK;
 }
 

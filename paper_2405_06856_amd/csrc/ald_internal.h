@@ -74,7 +74,15 @@ struct Scen {
     int64_t pstride;    // queries per tile rounded up to whole evaluation chunks
     int64_t qsum_off;   // QSum entries into qsum
     int64_t out_off;    // offset into out_worker
+    // The scenario's query i is entry q_first + i * q_stride of the call's
+    // query arrays (and of out_worker after out_off, and of out_diag); grouped
+    // placement routes every G-th query to a group.  out_add is added to the
+    // worker index written (a group's first worker; 0 elsewhere).
+    int32_t q_first, q_stride;
+    int32_t out_add, pad;
 };
+
+__host__ __device__ inline int64_t q_at(const Scen& sc, int32_t i) { return sc.q_first + (int64_t)i * sc.q_stride; }
 
 // Per-scenario control block.  Written by the commit kernel's sequential block
 // only; every other kernel only reads it (kernel boundaries order the accesses).

@@ -701,8 +701,8 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
     for (int m = 0; m < QPT; ++m) {
         const int qi = q0 + m * NT + tid;
         act[m] = qi < end;
-        lin[m] = act[m] ? st.q_lin[qi] : 1;
-        lp[m] = act[m] ? st.q_lpred[qi] : 1;
+        lin[m] = act[m] ? st.q_lin[q_at(sc, qi)] : 1;
+        lp[m] = act[m] ? st.q_lpred[q_at(sc, qi)] : 1;
         e1[m] = e2[m] = INT32_MAX;
         w1[m] = w2[m] = -1;
         const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
@@ -976,7 +976,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
         // before it.  These tile-start diagnostics are exact for the queries
         // before the tile's first commit; the commit overwrites every query
         // from its first feasible one on.
-        if (st.out_worker) st.out_worker[sc.out_off + qi] = -1;
+        if (st.out_worker) st.out_worker[sc.out_off + q_at(sc, qi)] = -1;
         if (st.out_diag) {
             Diag d;
             d.n_feasible = 0;
@@ -985,7 +985,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
             d.kv_excess_min = ex1;
             d.ttft_chosen = 0.0;
             d.tdec_chosen = 0.0;
-            st.out_diag[qi] = d;
+            st.out_diag[q_at(sc, qi)] = d;
         }
     }
 }

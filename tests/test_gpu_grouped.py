@@ -1,0 +1,126 @@
+"""Grouped placement (App. A) on the GPU vs the CPU oracle (needs an MI355X).
+
+The reference is the definition: query x of the stream goes to group x mod G,
+and each group is an independent placement (the oracle's) of its own queries
+on its own workers, with a heartbeat after every H / G of its queries."""
+from __future__ import annotations
+
+import dataclasses
+
+import numpy as np
+import pytest
+
+from oracle import ref
+from paper_2405_06856_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+FIELDS = ("n_feasible", "near_tie", "kv_peak_chosen", "kv_excess_min", "ttft_chosen", "tdec_chosen")
+
+
+@pytest.fixture(scope="module")
+def aladdin():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2405_06856_amd import aladdin as mod
+    return mod
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def oracle_grouped(t, sizes, H):
+    """Per query: global worker (or -1) and diagnostics, group by group."""
+    G = len(sizes)
+    Q = t.n_queries
+    worker = np.full(Q, -2, np.int32)
+    diag = {f: np.zeros(Q, np.float64 if f.endswith("chosen") and f[0] == "t" else np.int64) for f in FIELDS}
+    wb = 0
+    for g, n in enumerate(sizes):
+        o0, o1 = int(t.res_offsets[wb]), int(t.res_offsets[wb + n])
+        off = t.res_offsets[wb:wb + n + 1] - o0
+        td = None if t.res_t_dec is None else t.res_t_dec[o0:o1]
+        r = ref.place(n, np.broadcast_to(t.kv_capacity, (t.n_workers,))[wb:wb + n], off, t.res_l_in[o0:o1],
+                      t.res_l_pred[o0:o1], t.res_generated[o0:o1], t.model, t.q_l_in[g::G], t.q_l_pred[g::G],
+                      heartbeat_every=H // G, res_t_dec=td)
+        worker[g::G] = np.where(r.worker >= 0, r.worker + wb, -1)
+        for f in FIELDS:
+            diag[f][g::G] = getattr(r, f)
+        wb += n
+    assert (worker != -2).all()
+    return worker, diag
+
+
+def check(got, want_w, want_d, label):
+    assert np.array_equal(got.worker, want_w), (label, np.flatnonzero(got.worker != want_w)[:10])
+    for f in FIELDS:
+        g, w = got.diag[f], want_d[f]
+        if f.startswith(("ttft", "tdec")):
+            assert np.allclose(g, w, rtol=1e-9, atol=0.0), (label, f)
+        else:
+            assert np.array_equal(g.astype(np.int64), w.astype(np.int64)), (label, f, np.flatnonzero(g != w)[:10])
+
+
+CASES = [
+    # (G, sizes, H, tile)
+    (1, [40], 0, 256),
+    (3, [10, 17, 13], 0, 64),
+    (4, [10, 10, 10, 10], 48, 256),
+    (5, [1, 2, 30, 3, 4], 60, 1024),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=["G%d-H%d-t%d" % (c[0], c[2], c[3]) for c in CASES])
+def test_grouped_matches_oracle(aladdin, case):
+    G, sizes, H, tile = case
+    t = wl.make_trace("grouped", 31, W=40, R=16, Q=2400, kv_capacity=30000, model=wl.BASE_MODEL)
+    say("grouped", case)
+    ev = aladdin.Evaluator(0, tile=tile)
+    ev.load_trace(t)
+    got = ev.place_grouped(sizes, t.q_l_in, t.q_l_pred, heartbeat_every=H)
+    summ = ev.summary()
+    ev.close()
+    w, d = oracle_grouped(t, sizes, H)
+    check(got, w, d, "grouped %s" % (case,))
+    assert 0 < int((w >= 0).sum()) < t.n_queries
+    # one group is the ungrouped placement
+    if G == 1:
+        want = ref.place_trace(dataclasses.replace(t, heartbeat_every=H))
+        assert np.array_equal(got.worker, want.worker)
+        assert np.array_equal(summ["B"].astype(np.int64), want.B)
+
+
+def test_grouped_in_calls_with_history(aladdin):
+    """Calls ending at heartbeats continue one stream; constraint (d) with a
+    decode history holds per group."""
+    G, sizes, H = 3, [7, 11, 6], 30
+    t = wl.with_decode_history(wl.make_trace("grouped-d", 32, W=24, R=12, Q=1800, kv_capacity=20000,
+                                             model=wl.BASE_MODEL), 5)
+    ev = aladdin.Evaluator(0, tile=128)
+    ev.load_trace(t)
+    parts, ds = [], []
+    for a, b in [(0, 30), (30, 300), (300, 1800)]:
+        r = ev.place_grouped(sizes, t.q_l_in[a:b], t.q_l_pred[a:b], heartbeat_every=H)
+        parts.append(r.worker)
+        ds.append(r.diag)
+    ev.close()
+    got = type(r)(worker=np.concatenate(parts), diag=np.concatenate(ds))
+    w, d = oracle_grouped(t, sizes, H)
+    check(got, w, d, "grouped calls")
+
+
+def test_grouped_arguments_checked(aladdin):
+    t = wl.make_trace("grouped-bad", 33, W=8, R=2, Q=100, kv_capacity=30000, model=wl.BASE_MODEL)
+    ev = aladdin.Evaluator(0)
+    ev.load_trace(t)
+    bad = [([4, 3], 0, 100),       # sizes do not add up to W
+           ([4, 4], 3, 99),        # period not a multiple of G
+           ([4, 4], 10, 95),       # the call would not end at a heartbeat
+           ([8, 0], 0, 10)]        # empty group
+    for sizes, H, Q in bad:
+        with pytest.raises(aladdin.AladdinError) as e:
+            ev.place_grouped(sizes, t.q_l_in[:Q], t.q_l_pred[:Q], heartbeat_every=H)
+        assert e.value.code == aladdin.ALD_EINVAL
+    ev.close()
