@@ -1,5 +1,6 @@
 """Worker-count prediction over arrival rates (Sec. 4.4, Eq. 7), on top of the
-scaling sweep.
+scaling sweep; the worker configuration (Sec. 4.1, Eq. 5-6) and the group
+count of distributed scheduling (App. A, Eq. 8).
 
 For an arrival rate r the sweep runs each cluster scenario with a heartbeat
 after every H = r * T_dec processed queries: one heartbeat is one decode
@@ -68,3 +69,58 @@ def fit_eq7(rates: Sequence[float], workers: Sequence[int]):
 def predict_workers(k5: float, c5: float, rate: float) -> int:
     """Eq. 7: the smallest integer not below k5 * rate + c5."""
     return int(math.ceil(k5 * rate + c5))
+
+
+# --------------------------------------------------------------------------- worker configuration
+@dataclass
+class WorkerConfig:
+    gpus: int           # N_g
+    kv_capacity: float  # M = N_g m_gpu - m_model
+    iter_time: float    # t_compute + t_comm at the batch M / m_r
+    batch_slo: int      # B: the largest batch meeting the ATGT SLO
+    t_max: float        # Eq. 6, per GPU
+
+
+def worker_throughput(n_gpus: int, m_gpu: float, m_model: float, m_r: float, k4: float, c4: float,
+                      k_comm: float, decode_slo: float, c3: float, c2: float, k2: float, l_ave: float) -> WorkerConfig:
+    """Eq. 6 for a tensor-parallel worker of n_gpus GPUs:
+        T_max = min(M / (N_g m_r (t_compute + t_comm)), B / (N_g T_decode))
+    with M = N_g m_gpu - m_model (Sec. 4.1), t_compute = k4 / N_g + c4 (Eq. 5),
+    t_comm = k_comm (N_g - 1) / N_g (the all-reduce share the paper scales the
+    communication time by), and B the largest batch whose decode iteration
+    (Eq. 3 at average context l_ave) stays within T_decode:
+    (k2 l_ave + c2) B + c3 <= T_decode.  Memory in any unit shared by m_gpu,
+    m_model and m_r; a worker whose model does not fit has T_max = 0."""
+    g = int(n_gpus)
+    M = g * m_gpu - m_model
+    t_iter = (k4 / g + c4) + k_comm * (g - 1) / g
+    B = max(0, int(math.floor((decode_slo - c3) / (k2 * l_ave + c2))))
+    if M <= 0:
+        return WorkerConfig(g, M, t_iter, B, 0.0)
+    t_max = min(M / (g * m_r * t_iter), B / (g * decode_slo))
+    return WorkerConfig(g, M, t_iter, B, t_max)
+
+
+def best_worker_config(candidates: Sequence[int], **kw) -> WorkerConfig:
+    """The GPU count per worker with the largest per-GPU throughput (ties: fewer GPUs)."""
+    best = None
+    for g in sorted(candidates):
+        w = worker_throughput(g, **kw)
+        if best is None or w.t_max > best.t_max:
+            best = w
+    return best
+
+
+# --------------------------------------------------------------------------- App. A group count
+def group_count(rate: float, workers: int, err: float, rate_limit: float) -> int:
+    """Eq. 8: N_group groups of rates r_i = rate / N_group with 1 / (2 err) <=
+    (workers per group) and r_i <= r(T_s) = rate_limit (the rate one scheduler
+    places within the scheduling latency limit).  The fewest groups meeting the
+    rate limit, as long as every group keeps at least ceil(1 / (2 err))
+    workers; None when both cannot hold."""
+    if rate <= 0 or workers < 1 or not (0 < err) or rate_limit <= 0:
+        raise ValueError("need rate > 0, workers >= 1, err > 0, rate_limit > 0")
+    need = max(1, int(math.ceil(rate / rate_limit - 1e-12)))
+    per_group = int(math.ceil(1.0 / (2.0 * err) - 1e-12))
+    most = workers // per_group
+    return need if need <= most else None

@@ -28,6 +28,33 @@ def test_heartbeat_period_of_a_rate():
     assert scaling.heartbeat_period(10.0, 0.05) == 1  # under one query per iteration
 
 
+def test_worker_throughput_worked_example():
+    """Eq. 6 by hand: m_gpu 80, m_model 140, m_r 1, k4 0.08, c4 0.01,
+    k_comm 0.004, T_dec 0.05, c3 0.008, c2 1e-4, k2 2e-7, l_ave 1000.
+    B = floor(0.042 / 3e-4) = 140.
+    N_g = 2: M = 20, t = 0.04 + 0.01 + 0.002 = 0.052; min(20 / (2 * 0.052), 140 / 0.1) = 192.3.
+    N_g = 4: M = 180, t = 0.02 + 0.01 + 0.003 = 0.033; min(180 / 0.132, 140 / 0.2) = 700.
+    N_g = 8: M = 500, t = 0.01 + 0.01 + 0.0035 = 0.0235; min(500 / 0.188, 140 / 0.4) = 350.
+    N_g = 1: the model does not fit."""
+    kw = dict(m_gpu=80.0, m_model=140.0, m_r=1.0, k4=0.08, c4=0.01, k_comm=0.004, decode_slo=0.05, c3=0.008,
+              c2=1e-4, k2=2e-7, l_ave=1000.0)
+    w = {g: scaling.worker_throughput(g, **kw) for g in (1, 2, 4, 8)}
+    assert w[1].t_max == 0.0
+    assert w[2].batch_slo == 140
+    assert abs(w[2].t_max - 20 / (2 * 0.052)) < 1e-9
+    assert abs(w[4].t_max - 140 / 0.2) < 1e-9
+    assert abs(w[8].t_max - 140 / 0.4) < 1e-9
+    assert scaling.best_worker_config([1, 2, 4, 8], **kw).gpus == 4
+
+
+def test_group_count():
+    # 10 % extra workers -> groups of at least 5 workers (App. A's example)
+    assert scaling.group_count(rate=1000.0, workers=100, err=0.1, rate_limit=300.0) == 4
+    assert scaling.group_count(rate=250.0, workers=100, err=0.1, rate_limit=300.0) == 1
+    assert scaling.group_count(rate=1000.0, workers=12, err=0.1, rate_limit=300.0) is None  # 4 groups of 3
+    assert scaling.group_count(rate=600.0, workers=10, err=0.1, rate_limit=300.0) == 2
+
+
 @pytest.mark.gpu
 def test_min_cluster_per_rate_matches_oracle():
     import torch
