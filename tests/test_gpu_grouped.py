@@ -111,6 +111,24 @@ def test_grouped_in_calls_with_history(aladdin):
     check(got, w, d, "grouped calls")
 
 
+def test_grouped_edge_cases(aladdin):
+    """Fewer queries than groups (some groups get none), one worker per group,
+    and a decode-worker model."""
+    import math
+    t = wl.make_trace("grouped-edge", 34, W=12, R=6, Q=900, kv_capacity=25000, model=wl.BASE_MODEL)
+    for sizes, Q, H, model in (([3, 4, 5], 2, 0, None), ([1] * 12, 900, 0, None), ([1] * 12, 840, 24, None),
+                               ([6, 6], 900, 0, dataclasses.replace(wl.BASE_MODEL, ttft_slo=math.inf))):
+        tt = t if model is None else dataclasses.replace(t, model=model)
+        tt = dataclasses.replace(tt, q_l_in=tt.q_l_in[:Q], q_l_pred=tt.q_l_pred[:Q], arrivals=None)
+        say("grouped edge", sizes, Q, H)
+        ev = aladdin.Evaluator(0, tile=128)
+        ev.load_trace(tt)
+        got = ev.place_grouped(sizes, tt.q_l_in, tt.q_l_pred, heartbeat_every=H)
+        ev.close()
+        w, d = oracle_grouped(tt, sizes, H)
+        check(got, w, d, "edge %s Q=%d H=%d" % (sizes, Q, H))
+
+
 def test_grouped_arguments_checked(aladdin):
     t = wl.make_trace("grouped-bad", 33, W=8, R=2, Q=100, kv_capacity=30000, model=wl.BASE_MODEL)
     ev = aladdin.Evaluator(0)
