@@ -322,17 +322,20 @@ static int valid_model(const ora_model_t* m)
  * Outputs (any may be NULL): worker per query (-1 = rejected) and diagnostics;
  * final per-worker batch size, sum(c), sum(r), KV peak, S1, S2.
  */
-int ora_place(int32_t W, const int64_t* M, const int64_t* res_off,
-              const int32_t* res_lin, const int32_t* res_lpred, const int32_t* res_g, const double* res_tdec,
-              const ora_model_t* model, int32_t Q, const int32_t* q_lin, const int32_t* q_lpred,
-              int32_t H, int32_t no_commit, int32_t check, int32_t n_threads,
-              int32_t* out_worker, int32_t* out_nfeas, int32_t* out_near_tie,
-              int64_t* out_peak_chosen, int64_t* out_excess_min,
-              double* out_ttft_chosen, double* out_tdec_chosen,
-              int64_t* fin_B, int64_t* fin_SC, int64_t* fin_SR, int64_t* fin_peak,
-              int64_t* fin_S1, int64_t* fin_S2)
+static int place_impl(int32_t W, const int64_t* M, const int64_t* res_off,
+                      const int32_t* res_lin, const int32_t* res_lpred, const int32_t* res_g, const double* res_tdec,
+                      const ora_model_t* model, int32_t Q, const int32_t* q_lin, const int32_t* q_lpred,
+                      int32_t H, const int32_t* hb_before, int32_t no_commit, int32_t check, int32_t n_threads,
+                      int32_t* out_worker, int32_t* out_nfeas, int32_t* out_near_tie,
+                      int64_t* out_peak_chosen, int64_t* out_excess_min,
+                      double* out_ttft_chosen, double* out_tdec_chosen,
+                      int64_t* fin_B, int64_t* fin_SC, int64_t* fin_SR, int64_t* fin_peak,
+                      int64_t* fin_S1, int64_t* fin_S2)
 {
     if (W <= 0 || Q < 0 || H < 0 || !model || !valid_model(model)) return ORA_EINVAL;
+    if (hb_before && H != 0) return ORA_EINVAL;
+    for (int32_t q = 0; hb_before && q < Q; ++q)
+        if (hb_before[q] < 0) return ORA_EINVAL;
     worker_t* ws = (worker_t*)calloc((size_t)W, sizeof(worker_t));
     pair_t* pr = (pair_t*)calloc((size_t)W, sizeof(pair_t));
     int* order = (int*)calloc((size_t)W, sizeof(int));
@@ -361,6 +364,12 @@ int ora_place(int32_t W, const int64_t* M, const int64_t* res_off,
     for (int32_t q = 0; q < Q; ++q) {
         const int64_t lin = q_lin[q], lp = q_lpred[q];
         if (lin < 1 || lp < 1) { rc = ORA_EINVAL; goto done; }
+        /* heartbeats driven by the caller's clock: hb_before[q] decode
+         * iterations (each its own heartbeat) run before query q */
+        for (int32_t k = 0; hb_before && !no_commit && k < hb_before[q]; ++k) {
+            for (int32_t i = 0; i < W; ++i) heartbeat(&ws[i], model);
+            hb += 1;
+        }
         int best = -1;
         int nfeas = 0;
         int64_t excess_min = INT64_MAX;
@@ -439,6 +448,40 @@ typedef struct {
     int64_t kv_capacity;
     ora_model_t model;
 } ora_scenario_t;
+
+int ora_place(int32_t W, const int64_t* M, const int64_t* res_off,
+              const int32_t* res_lin, const int32_t* res_lpred, const int32_t* res_g, const double* res_tdec,
+              const ora_model_t* model, int32_t Q, const int32_t* q_lin, const int32_t* q_lpred,
+              int32_t H, int32_t no_commit, int32_t check, int32_t n_threads,
+              int32_t* out_worker, int32_t* out_nfeas, int32_t* out_near_tie,
+              int64_t* out_peak_chosen, int64_t* out_excess_min,
+              double* out_ttft_chosen, double* out_tdec_chosen,
+              int64_t* fin_B, int64_t* fin_SC, int64_t* fin_SR, int64_t* fin_peak,
+              int64_t* fin_S1, int64_t* fin_S2)
+{
+    return place_impl(W, M, res_off, res_lin, res_lpred, res_g, res_tdec, model, Q, q_lin, q_lpred, H, NULL,
+                      no_commit, check, n_threads, out_worker, out_nfeas, out_near_tie, out_peak_chosen,
+                      out_excess_min, out_ttft_chosen, out_tdec_chosen, fin_B, fin_SC, fin_SR, fin_peak, fin_S1,
+                      fin_S2);
+}
+
+/* As ora_place, with the heartbeats given per query instead of by a period:
+ * hb_before[q] >= 0 decode iterations run before query q is placed. */
+int ora_place_hb(int32_t W, const int64_t* M, const int64_t* res_off,
+                 const int32_t* res_lin, const int32_t* res_lpred, const int32_t* res_g, const double* res_tdec,
+                 const ora_model_t* model, int32_t Q, const int32_t* q_lin, const int32_t* q_lpred,
+                 const int32_t* hb_before, int32_t check,
+                 int32_t* out_worker, int32_t* out_nfeas, int32_t* out_near_tie,
+                 int64_t* out_peak_chosen, int64_t* out_excess_min,
+                 double* out_ttft_chosen, double* out_tdec_chosen,
+                 int64_t* fin_B, int64_t* fin_SC, int64_t* fin_SR, int64_t* fin_peak,
+                 int64_t* fin_S1, int64_t* fin_S2)
+{
+    if (!hb_before && Q > 0) return ORA_EINVAL;
+    return place_impl(W, M, res_off, res_lin, res_lpred, res_g, res_tdec, model, Q, q_lin, q_lpred, 0, hb_before,
+                      0, check, 1, out_worker, out_nfeas, out_near_tie, out_peak_chosen, out_excess_min,
+                      out_ttft_chosen, out_tdec_chosen, fin_B, fin_SC, fin_SR, fin_peak, fin_S1, fin_S2);
+}
 
 /*
  * Scaling sweep: every scenario starts with empty workers and places the same

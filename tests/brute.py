@@ -14,7 +14,8 @@ form from the oracle:
 * Algorithm 1's ranking uses capacity_norm = hypot(B, sum(D)) in fp64, sorted
   large to small with ties to the lower index, then the first feasible worker.
 * A heartbeat drops the first element of every footprint vector (one decode
-  iteration has run); empty vectors leave.
+  iteration has run); empty vectors leave.  Heartbeats come after every H
+  processed queries, or hb_before[q] of them before query q.
 * Split-phase serving: a decode worker (infinite TTFT SLO) checks only (b) and (e).
 * Constraint (d), with decode history: every request keeps its generated-token
   count g and decode time t_dec literally (exact rationals); a heartbeat's
@@ -75,7 +76,7 @@ class BruteWorker:
         return len(self.vecs)
 
 
-def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0, use_d=False):
+def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0, use_d=False, hb_before=None):
     """Per query a dict: chosen worker (-1 = none), n_feasible, per-worker KV
     peaks and a flag telling whether any exact latency margin is so small that
     fp64 rounding could decide it (those queries are not comparable bit for bit)."""
@@ -84,7 +85,10 @@ def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0, u
     decode_only = math.isinf(model.ttft_slo)  # a decode worker of split-phase serving
     out = []
     since = 0
-    for (l_in, l_pred) in queries:
+    for qi, (l_in, l_pred) in enumerate(queries):
+        for _ in range(hb_before[qi] if hb_before is not None else 0):
+            for w in workers:
+                w.heartbeat(model)
         q = Req(l_in, l_pred, 0, True)
         qv = q.footprint()
         feas, norms, peaks = [], [], []

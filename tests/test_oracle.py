@@ -139,6 +139,80 @@ def test_placement_matches_bruteforce(H):
     assert compared > 1500
 
 
+def _hb_from_period(Q, H):
+    hb = np.zeros(Q, np.int32)
+    if H > 0:
+        hb[H::H] = 1
+    return hb
+
+
+@pytest.mark.parametrize("H", [1, 7, 100])
+def test_heartbeats_per_query_equal_a_period(H):
+    """hb_before = 1 at every H-th query is the same stream as heartbeat_every = H
+    (whose heartbeat after the last query, when H divides Q, has no query to
+    precede: the final states are compared only when it does not happen)."""
+    t = wl.with_decode_history(wl.make_trace("hbq", 41, W=10, R=12, Q=703, kv_capacity=20000, model=wl.BASE_MODEL), 3)
+    a = ref.place_trace(t, heartbeat_every=H, check=True)
+    b = ref.place_hb(t.n_workers, t.kv_capacity, t.res_offsets, t.res_l_in, t.res_l_pred, t.res_generated, t.model,
+                     t.q_l_in, t.q_l_pred, _hb_from_period(t.n_queries, H), check=True, res_t_dec=t.res_t_dec)
+    fields = ["worker", "n_feasible", "near_tie", "kv_peak_chosen", "kv_excess_min"]
+    if t.n_queries % H:
+        fields += ["B", "sum_c", "sum_r", "peak"]
+    for f in fields:
+        assert np.array_equal(getattr(a, f), getattr(b, f)), f
+    assert np.array_equal(a.ttft_chosen, b.ttft_chosen) and np.array_equal(a.tdec_chosen, b.tdec_chosen)
+
+
+@pytest.mark.parametrize("use_d", [False, True])
+def test_heartbeats_per_query_match_bruteforce(use_d):
+    """Arrival-time heartbeats: any number of decode iterations (bursts, idle
+    gaps) before a query, against the brute force, with and without (d)."""
+    rng = np.random.default_rng(700 + int(use_d))
+    compared = 0
+    for case in range(300):
+        W = int(rng.integers(1, 5))
+        model = _random_model(rng)
+        model = dataclasses.replace(model, c1=float(rng.uniform(0.0, 0.02)), k1=float(rng.uniform(0.0, 0.004)),
+                                    ttft_slo=1.0)
+        residents, t_dec = [], []
+        for _ in range(W):
+            rs, ts = [], []
+            for _ in range(int(rng.integers(0, 6))):
+                lp = int(rng.integers(1, 9))
+                g = int(rng.integers(0, lp))
+                rs.append((int(rng.integers(1, 9)), lp, g))
+                ts.append(float(rng.uniform(0.0, 2.0)) * g * model.decode_slo)
+            residents.append(rs)
+            t_dec.append(ts)
+        M = [int(rng.integers(8, 60)) for _ in range(W)]
+        Q = int(rng.integers(1, 12))
+        queries = [(int(rng.integers(1, 9)), int(rng.integers(1, 9))) for _ in range(Q)]
+        hbb = rng.choice([0, 0, 0, 1, 2, 5], Q).astype(np.int32)
+        off = np.zeros(W + 1, np.int64)
+        rl, rp, rg, td = [], [], [], []
+        for i in range(W):
+            for k, (a, b, g) in enumerate(residents[i]):
+                rl.append(a); rp.append(b); rg.append(g); td.append(t_dec[i][k])
+            off[i + 1] = len(rl)
+        q = np.array(queries, np.int32).reshape(-1, 2)
+        res = ref.place_hb(W, np.asarray(M, np.int64), off, np.array(rl, np.int32), np.array(rp, np.int32),
+                           np.array(rg, np.int32), model, q[:, 0], q[:, 1], hbb, check=True,
+                           res_t_dec=np.array(td, np.float64) if use_d else None)
+        bw = [BruteWorker(M[i], [Req(a, b, g, t_dec=t_dec[i][k]) for k, (a, b, g) in enumerate(residents[i])])
+              for i in range(W)]
+        want = brute_place(bw, model, queries, use_d=use_d, hb_before=hbb)
+        for k, wq in enumerate(want):
+            if wq["close"]:
+                break
+            norms = sorted(wq["norms"])
+            if any(0 < b - a <= 1e-12 * b for a, b in zip(norms, norms[1:])):
+                break
+            assert res.worker[k] == wq["worker"], (case, k)
+            assert res.n_feasible[k] == wq["n_feasible"], (case, k)
+            compared += 1
+    assert compared > 1000
+
+
 @pytest.mark.parametrize("H", [0, 2])
 def test_decode_workers_match_bruteforce(H):
     """Split-phase decode workers (infinite TTFT SLO): only (b) and (e), even

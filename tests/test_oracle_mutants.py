@@ -51,6 +51,7 @@ MUTANTS = [
     ("(d) iteration time without the batch term", "(m->c3 + m->c2 * (double)w->n)", "(m->c3 + m->c2 * (double)(w->n - 1))"),
     ("(d) resident slack from the predicted length", "s0 = model->decode_slo * (double)g - res_tdec[k];",
      "s0 = model->decode_slo * (double)lp - res_tdec[k];"),
+    ("one heartbeat fewer before a query", "k < hb_before[q]; ++k)", "k + 1 < hb_before[q]; ++k)"),
     # split-phase decode workers
     ("decode workers still check (d)", "if (use_d && !decode_only) {", "if (use_d) {"),
     ("decode workers flag TTFT near ties", "(!decode_only && near(o->ttft, m->ttft_slo))", "near(o->ttft, m->ttft_slo)"),
@@ -88,6 +89,8 @@ PINS = [
     lambda: pins.test_preemption_limit_matches_bruteforce(3),
     pins.test_preemption_limit_worked_example,
     pins.test_preemption_limit_needs_an_ongoing_request,
+    lambda: pins.test_heartbeats_per_query_match_bruteforce(False),
+    lambda: pins.test_heartbeats_per_query_match_bruteforce(True),
     lambda: pins.test_decode_workers_match_bruteforce(0),
     lambda: pins.test_decode_workers_match_bruteforce(2),
     pins.test_rebalance_worked_example,
