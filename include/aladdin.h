@@ -148,6 +148,19 @@ int ald_load_workers_history(ald_handle_t handle, int32_t W, const ald_model_t* 
 int ald_place_stream(ald_handle_t handle, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
                      int32_t heartbeat_every, int32_t* out_worker, ald_query_diag_t* out_diag);
 
+/* As ald_place_stream, with heartbeats driven by the caller's clock instead
+ * of a period: hb_before[q] >= 0 (host array [Q]) decode iterations run
+ * before query q is placed, each one a heartbeat (one decode iteration on
+ * every worker, finished requests leave, the TTFT window restarts).  With
+ * arrival times t_q and one decode iteration per T_dec seconds,
+ * hb_before[q] = floor(t_q / T_dec) - floor(t_{q-1} / T_dec) (the scheduler
+ * places the requests that arrived since its last heartbeat, Sec. 4.2).
+ * Counts continue ald_place_stream's stream; ALD_EINVAL for a negative count,
+ * ALD_EOVERFLOW when the stream would run more decode iterations than the
+ * 32-bit request state holds. */
+int ald_place_stream_hb(ald_handle_t handle, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
+                        const int32_t* hb_before, int32_t* out_worker, ald_query_diag_t* out_diag);
+
 /* Grouped placement (App. A, distributed scheduling): the loaded workers are
  * split into G consecutive groups of group_workers[g] workers (host array,
  * each >= 1, summing to W); query x of the stream (counted across calls since

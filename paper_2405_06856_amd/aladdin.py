@@ -50,7 +50,7 @@ DIAG_DTYPE = np.dtype([("n_feasible", "<i4"), ("near_tie", "<i4"), ("kv_peak_cho
 assert DIAG_DTYPE.itemsize == 40
 
 SYMBOLS = ("ald_create", "ald_destroy", "ald_set_tile", "ald_load_workers", "ald_load_workers_history",
-           "ald_place_stream", "ald_place_grouped",
+           "ald_place_stream", "ald_place_stream_hb", "ald_place_grouped",
            "ald_sweep_scenarios", "ald_sweep_scenarios_hb", "ald_rebalance", "ald_worker_summary", "ald_set_profiling", "ald_kernel_time",
            "ald_last_error", "ald_strerror")
 
@@ -68,6 +68,7 @@ def _load():
         "ald_load_workers_history": ([P, i32, ctypes.POINTER(Model), P, P, P, P, P, P, i32], ctypes.c_int),
         "ald_place_stream": ([P, i32, P, P, i32, P, P], ctypes.c_int),
         "ald_place_grouped": ([P, i32, P, i32, P, P, i32, P, P], ctypes.c_int),
+        "ald_place_stream_hb": ([P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_sweep_scenarios": ([P, i32, P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_sweep_scenarios_hb": ([P, i32, P, P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_rebalance": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P], ctypes.c_int),
@@ -137,6 +138,15 @@ def ald_load_workers_history(h, W: int, model: Model, kv_capacity, res_offsets, 
 def ald_place_stream(h, Q: int, q_l_in, q_l_pred, heartbeat_every: int, out_worker, out_diag=None) -> None:
     _check(h, _L.ald_place_stream(h, int(Q), _dptr(q_l_in), _dptr(q_l_pred), int(heartbeat_every),
                                   _dptr(out_worker), _dptr(out_diag)))
+
+
+def ald_place_stream_hb(h, Q: int, q_l_in, q_l_pred, hb_before, out_worker, out_diag=None) -> None:
+    """hb_before: host array of Q heartbeat counts."""
+    hb = np.ascontiguousarray(hb_before, dtype=np.int32)
+    if hb.shape != (int(Q),):
+        raise ValueError("hb_before must hold one count per query")
+    _check(h, _L.ald_place_stream_hb(h, int(Q), _dptr(q_l_in), _dptr(q_l_pred), hb.ctypes.data_as(ctypes.c_void_p),
+                                     _dptr(out_worker), _dptr(out_diag)))
 
 
 def ald_place_grouped(h, G: int, group_workers, Q: int, q_l_in, q_l_pred, heartbeat_every: int, out_worker,
@@ -284,11 +294,20 @@ class Evaluator:
         ald_place_stream(self.h, Q, q_l_in, q_l_pred, heartbeat_every, out, d)
         return out, d
 
-    def place(self, q_l_in, q_l_pred, heartbeat_every=0, diag=True) -> Placement:
+    def place(self, q_l_in, q_l_pred, heartbeat_every=0, diag=True, hb_before=None) -> Placement:
+        """hb_before: decode iterations before each query (instead of a period)."""
         t = self.torch
         ql = self._dev(q_l_in, t.int32)
         qp = self._dev(q_l_pred, t.int32)
-        out, d = self.place_device(ql, qp, heartbeat_every, diag)
+        if hb_before is None:
+            out, d = self.place_device(ql, qp, heartbeat_every, diag)
+        else:
+            Q = int(ql.numel())
+            out = t.empty(max(Q, 1), dtype=t.int32, device=self.device)
+            d = t.empty(max(Q, 1) * DIAG_DTYPE.itemsize, dtype=t.uint8, device=self.device) if diag else None
+            ald_place_stream_hb(self.h, Q, ql, qp, hb_before, out, d)
+            out = out[:Q]
+            d = None if d is None else d[:Q * DIAG_DTYPE.itemsize]
         res = Placement(worker=out.cpu().numpy())
         if d is not None:
             res.diag = d.cpu().numpy().view(DIAG_DTYPE)

@@ -867,6 +867,20 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
         st.built[gw] = 0;
         st.dlist[s * MAX_DIRTY + lane] = gw;
     }
+    // per-query heartbeats: the tile ended at a query that heartbeats precede;
+    // they run now, and the whole wave finds the next such query
+    const bool hb_here = st.hb_before != nullptr && pos == end && pos == c.hb_next && pos < c.Q;
+    int32_t hb_n = 0, hb_after = c.Q;
+    if (hb_here) {
+        hb_n = st.hb_before[pos];
+        for (int32_t b = pos + 1; b < c.Q; b += NT) {
+            const uint64_t m = ballot(b + lane < c.Q && st.hb_before[b + lane] > 0);
+            if (m) {
+                hb_after = b + __ffsll((unsigned long long)m) - 1;
+                break;
+            }
+        }
+    }
     if (lane == 0) {
         if (nrej) atomicAdd(&cp->n_rej, nrej);
         if (firstrej != INT32_MAX) atomicMin(&cp->first_rej, firstrej);
@@ -879,6 +893,12 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
             cp->hb_index = c.hb_index + 1;
             cp->since_hb = 0;
             cp->rebuild = 1;
+        } else if (hb_here) {  // hb_n decode iterations, each its own heartbeat
+            cp->tau = c.tau + hb_n;
+            cp->hb_index = c.hb_index + hb_n;
+            cp->since_hb = 0;
+            cp->rebuild = 1;
+            cp->hb_next = hb_after;
         } else {
             cp->since_hb = since;
         }

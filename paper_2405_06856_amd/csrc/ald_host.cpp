@@ -65,6 +65,9 @@ struct ald_handle {
     bool check_all = false;        // stale workers are not listed (after grouped placement): check every one
     int64_t qcount = 0;            // queries processed since the load (routes grouped placement)
     Arena* grouped = nullptr;      // scenario view of the loaded workers for grouped placement
+    const int32_t* hb_host = nullptr;  // per-query heartbeats of the running call (host), or null
+    int32_t* hb_dev = nullptr;         // their device copy
+    size_t hb_dev_n = 0;
     int32_t* err_word = nullptr;
     int32_t prof = 0;  // kernel kinds timed (bit k = kind k)
     std::vector<Events> pending;
@@ -397,19 +400,32 @@ int map_dev_error(ald_handle* h, int32_t code)
     }
 }
 
-// Rounds needed to finish every scenario from its control state, if no tile is cut.
-int64_t rounds_needed(const std::vector<Ctl>& c)
+// First query after `from` that heartbeats precede (Q if none).
+int32_t next_hb(const int32_t* hb, int32_t from, int32_t Q)
+{
+    int32_t j = from + 1;
+    while (j < Q && hb[j] == 0) ++j;
+    return j;
+}
+
+// Rounds needed to finish every scenario from its control state, if no tile
+// is cut (hb: the call's per-query heartbeats, or null).
+int64_t rounds_needed(const std::vector<Ctl>& c, const int32_t* hb)
 {
     int64_t most = 0;
     for (const Ctl& x : c) {
         if (x.err) continue;
         int64_t r = 0;
-        int32_t pos = x.start, since = x.since_hb;
+        int32_t pos = x.start, since = x.since_hb, nxt = x.hb_next;
         while (pos < x.Q) {
-            int32_t end = tile_end(pos, x.Q, x.T, x.H, since);
+            int32_t end = tile_end(pos, x.Q, x.T, x.H, since, nxt);
             if (end <= pos) return -1;  // a tile that cannot advance (never set up so)
             since += end - pos;
             if (x.H > 0 && since >= x.H) since = 0;
+            if (hb && end == nxt && end < x.Q) {
+                since = 0;
+                nxt = next_hb(hb, end, x.Q);
+            }
             pos = end;
             ++r;
         }
@@ -436,7 +452,7 @@ int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, 
     HIPCHK(h, hipHostGetDevicePointer((void**)&a->st.ctl_host, a->hctl, 0));
     bool first = true;
     for (;;) {
-        int64_t need = rounds_needed(hc);
+        int64_t need = rounds_needed(hc, h->hb_host);
         if (need < 0) return fail(h, ALD_EHIP, "internal error: a tile of no queries");
         if (need == 0) break;
         for (int64_t r = 0; r < need; ++r) {
@@ -505,6 +521,7 @@ int ald_destroy(ald_handle_t h)
     delete h->sweep;
     (void)hipFree(h->err_word);
     if (h->rb_mem) (void)hipFree(h->rb_mem);
+    if (h->hb_dev) (void)hipFree(h->hb_dev);
     for (Events& e : h->pool) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
     for (Events& e : h->pending) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
     delete h;
@@ -641,8 +658,20 @@ int ald_load_workers_history(ald_handle_t h, int32_t W, const ald_model_t* model
                         slots_per_worker, res_t_dec);
 }
 
-int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
-                     int32_t heartbeat_every, int32_t* out_worker, ald_query_diag_t* out_diag)
+}  // extern "C"
+
+namespace {
+
+// Clears the handle's per-query heartbeats when a call ends, however it ends.
+struct HbScope {
+    ald_handle* h;
+    ~HbScope() { h->hb_host = nullptr; }
+};
+
+// One stream call: heartbeats every H processed queries, or hb_before[q]
+// (host array) decode iterations before query q.
+int place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred, int32_t heartbeat_every,
+                 const int32_t* hb_before, int32_t* out_worker, ald_query_diag_t* out_diag)
 {
     if (!h) return ALD_EINVAL;
     HIPCHK(h, hipSetDevice(h->device));
@@ -660,9 +689,38 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
         since = 0;
         rebuild = true;
     }
-    const int64_t tau_final = (int64_t)tau + (H > 0 ? (int64_t)Q / H + 2 : 0);
+    int64_t iters = H > 0 ? (int64_t)Q / H + 2 : 0;
+    if (hb_before) {
+        int64_t tot = 0;
+        for (int32_t q = 0; q < Q; ++q) {
+            if (hb_before[q] < 0) return fail(h, ALD_EINVAL, "hb_before must be >= 0");
+            tot += hb_before[q];
+        }
+        if (hb_before[0] > 0) {  // the heartbeats before the first query run first
+            tau += hb_before[0];
+            hb += hb_before[0];
+            since = 0;
+            rebuild = true;
+            tot -= hb_before[0];
+        }
+        iters = tot + 2;
+    }
+    const int64_t tau_final = (int64_t)tau + iters;
     if (tau_final >= ((int64_t)1 << 27) || (int64_t)h->max_cap * tau_final >= ((int64_t)1 << 27))
         return fail(h, ALD_EOVERFLOW, "too many heartbeats for the 32-bit request state");
+    HbScope hb_scope{h};
+    if (hb_before) {
+        if ((size_t)Q > h->hb_dev_n) {
+            HIPCHK(h, hipStreamSynchronize(h->stream));
+            if (h->hb_dev) HIPCHK(h, hipFree(h->hb_dev));
+            h->hb_dev = nullptr;
+            h->hb_dev_n = 0;
+            HIPCHK(h, hipMalloc(&h->hb_dev, (size_t)Q * sizeof(int32_t)));
+            h->hb_dev_n = Q;
+        }
+        HIPCHK(h, hipMemcpyAsync(h->hb_dev, hb_before, (size_t)Q * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
+        h->hb_host = hb_before;
+    }
     Arena* a = h->main;
     int32_t T = std::min(h->tile, Q);
     if (H > 0) T = std::min(T, H);
@@ -681,18 +739,21 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
     c.rebuild = rebuild ? 1 : 0;
     c.first_rej = INT32_MAX;
     c.round = h->round;
+    c.hb_next = hb_before ? next_hb(hb_before, 0, Q) : 0;
     TileInfo ti{};
     ti.first_pc[0] = ti.first_pc[1] = INT32_MAX;
     HIPCHK(h, launch_begin(c, ti, a->st.ctl, a->st.tinfo, a->st.qbad, h->stream));
     a->st.q_lin = q_l_in;
     a->st.q_lpred = q_l_pred;
+    a->st.hb_before = h->hb_host ? h->hb_dev : nullptr;
     a->st.out_worker = out_worker;
     a->st.out_diag = (Diag*)out_diag;
     std::vector<Ctl> hc(1, c);
     // first build: every worker after a heartbeat, the last commit round's
     // workers if it changed any, else nothing
-    const int first_mode = (rebuild || H > 0 || h->check_all) ? 0 : (h->dirty_pending ? 1 : -1);
-    rc = run_rounds(h, a, H > 0, first_mode, hc);
+    const bool moves = H > 0 || hb_before != nullptr;  // heartbeats can move tau within the call
+    const int first_mode = (rebuild || moves || h->check_all) ? 0 : (h->dirty_pending ? 1 : -1);
+    rc = run_rounds(h, a, moves, first_mode, hc);
     if (rc != ALD_OK) return rc;
     c = hc[0];
     h->qcount += Q;
@@ -704,6 +765,23 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
     h->rebuild_pending = c.rebuild != 0;
     h->dirty_pending = c.ndirty > 0;
     return ALD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
+                     int32_t heartbeat_every, int32_t* out_worker, ald_query_diag_t* out_diag)
+{
+    return place_stream(h, Q, q_l_in, q_l_pred, heartbeat_every, nullptr, out_worker, out_diag);
+}
+
+int ald_place_stream_hb(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
+                        const int32_t* hb_before, int32_t* out_worker, ald_query_diag_t* out_diag)
+{
+    if (h && Q > 0 && !hb_before) return fail(h, ALD_EINVAL, "null hb_before");
+    return place_stream(h, Q, q_l_in, q_l_pred, 0, Q > 0 ? hb_before : nullptr, out_worker, out_diag);
 }
 
 }  // extern "C"
@@ -765,6 +843,7 @@ int grouped_view(ald_handle* h, int32_t G, const int32_t* sizes)
     a.st.dlist = dlist;
     a.st.dcount = dcount;
     a.st.qbad = nullptr;  // the queries are checked up front
+    a.st.hb_before = nullptr;
     a.st.S = G;
     HIPCHK(h, hipMemsetAsync(dcount, 0, G * sizeof(int32_t), h->stream));
     a.T = 0;  // lay the scratch out again

@@ -102,7 +102,8 @@ struct Ctl {
     int32_t round;      // rounds run
     int32_t commits;    // placements made
     int32_t ndirty;     // workers the last commit round changed (their summaries are stale)
-    int32_t pad1;
+    int32_t hb_next;    // with per-query heartbeats: the next query (> start) that heartbeats
+                        // precede, Q if none; 0 otherwise
 };
 
 // Tile description published by the selection kernel for the commit kernel.
@@ -212,19 +213,22 @@ struct State {
     // queries and outputs
     const int32_t* q_lin;
     const int32_t* q_lpred;
+    const int32_t* hb_before;  // per query of the call: heartbeats before it (null: by period)
     int32_t* out_worker;
     Diag* out_diag;    // only with S == 1
     int32_t* err_word; // load-time validation
     int32_t* qbad;     // nonzero: a query length of this call is invalid (one-scenario calls; else null)
 };
 
-inline __host__ __device__ int32_t tile_end(int32_t start, int32_t Q, int32_t T, int32_t H, int32_t since_hb) {
+inline __host__ __device__ int32_t tile_end(int32_t start, int32_t Q, int32_t T, int32_t H, int32_t since_hb,
+                                            int32_t hb_next) {
     int64_t end = (int64_t)start + T;
     if (end > Q) end = Q;
     if (H > 0) {
         int64_t hb = (int64_t)start + (H - since_hb);
         if (hb < end) end = hb;
     }
+    if (hb_next > start && hb_next < end) end = hb_next;
     return (int32_t)end;
 }
 

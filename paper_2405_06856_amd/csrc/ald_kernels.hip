@@ -43,7 +43,7 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
     if (sc.use_d) {
         phi = st.phi[gw];
         const int pending = hb - st.phi_hb[gw];
-        if (pending < 0 || pending > 8) {
+        if (pending < 0) {
             if (tid == 0) raise_error(err, DEV_EINVAL);
         } else {
             for (int p = 0; p < pending; ++p) {
@@ -56,11 +56,10 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
                 }
                 cnt = block_reduce<NT>(cnt, 0, OpAdd(), red);
                 ssum = block_reduce<NT>(ssum, 0, OpAdd(), red);
-                if (cnt > 0) {
-                    const int64_t ctx = ssum + cnt * (int64_t)tk;  // sum of the contexts c = s + tau
-                    const double t_iter = (sc.c3 + sc.c2 * (double)cnt) + sc.k2 * (double)ctx;
-                    phi = phi + (sc.tdec - t_iter);
-                }
+                if (cnt == 0) break;  // the live set only shrinks: no later iteration runs a batch
+                const int64_t ctx = ssum + cnt * (int64_t)tk;  // sum of the contexts c = s + tau
+                const double t_iter = (sc.c3 + sc.c2 * (double)cnt) + sc.k2 * (double)ctx;
+                phi = phi + (sc.tdec - t_iter);
             }
             if (tid == 0) {
                 st.phi[gw] = phi;
@@ -683,7 +682,7 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
         if (ballot(bad) != 0 && lane_id() == 0) atomicOr(st.qbad, 1);
     }
     if (cp->err || start >= Q) return;
-    const int32_t end = tile_end(start, Q, cp->T, cp->H, cp->since_hb);
+    const int32_t end = tile_end(start, Q, cp->T, cp->H, cp->since_hb, cp->hb_next);
     const int local = blockIdx.x - sc.eval_blk0;
     const int wb = local % sc.nblk;
     const int qc = local / sc.nblk;
@@ -809,7 +808,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     const int32_t start = cp->start, Q = cp->Q;
     const int local = blockIdx.x - sc.sel_blk0;
     const bool done = cp->err || start >= Q;
-    const int32_t end = done ? start : tile_end(start, Q, cp->T, cp->H, cp->since_hb);
+    const int32_t end = done ? start : tile_end(start, Q, cp->T, cp->H, cp->since_hb, cp->hb_next);
     const int parity = cp->round & 1;
     if (local == 0 && threadIdx.x == 0) {
         TileInfo* ti = st.tinfo + s;

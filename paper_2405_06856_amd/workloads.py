@@ -241,6 +241,17 @@ CONFIGS = {
 }
 
 
+def heartbeats_from_arrivals(arrivals: np.ndarray, period: float) -> np.ndarray:
+    """Decode iterations (one per `period` seconds) that run before each query:
+    the number of period boundaries crossed since the previous arrival (since
+    time 0 for the first query)."""
+    k = np.floor(np.asarray(arrivals, dtype=np.float64) / period).astype(np.int64)
+    out = np.diff(np.concatenate([[0], k]))
+    if (out < 0).any():
+        raise ValueError("arrivals must not decrease")
+    return out.astype(np.int32)
+
+
 def with_decode_history(trace: Trace, seed: int, lo: float = 0.2, hi: float = 0.9) -> Trace:
     """A copy of `trace` whose residents carry a decode time so far: each one's
     g generated tokens took g * T_dec * f seconds, f uniform in [lo, hi) (seeded),

@@ -139,6 +139,64 @@ def test_decode_workers_match_oracle(aladdin, case):
     assert not np.array_equal(ref.place_trace(fin).worker, ref.place_trace(t).worker)
 
 
+def oracle_hb(t, hb):
+    return ref.place_hb(t.n_workers, t.kv_capacity, t.res_offsets, t.res_l_in, t.res_l_pred, t.res_generated, t.model,
+                        t.q_l_in, t.q_l_pred, hb, res_t_dec=t.res_t_dec)
+
+
+@pytest.mark.parametrize("tile", [64, 1024])
+def test_heartbeats_per_query_equal_a_period(aladdin, tile):
+    t = wl.make_trace("hbq", 26, W=30, R=20, Q=2501, kv_capacity=30000, model=wl.BASE_MODEL)
+    hb = np.zeros(t.n_queries, np.int32)
+    hb[37::37] = 1
+    ev = aladdin.Evaluator(0, tile=tile)
+    ev.load_trace(t)
+    a = ev.place(t.q_l_in, t.q_l_pred, hb_before=hb)
+    ev.close()
+    ev = aladdin.Evaluator(0, tile=tile)
+    ev.load_trace(t)
+    b = ev.place(t.q_l_in, t.q_l_pred, heartbeat_every=37)
+    ev.close()
+    assert np.array_equal(a.worker, b.worker)
+    for f in FIELDS_INT + FIELDS_FP:
+        assert np.array_equal(a.diag[f], b.diag[f]), f
+    compare(a.worker, a.diag, None, oracle_hb(t, hb), "hb per query / %d" % tile)
+
+
+@pytest.mark.parametrize("history", [False, True])
+def test_arrival_time_heartbeats_match_oracle(aladdin, history):
+    """Poisson arrivals, one decode iteration per T_dec: bursts (several queries
+    per iteration) and gaps (several iterations per query), in three calls."""
+    t = wl.make_trace("arrivals", 27, W=12, R=16, Q=3000, kv_capacity=20000, model=wl.BASE_MODEL, rate=60.0)
+    if history:
+        t = wl.with_decode_history(t, 12)
+    hb = wl.heartbeats_from_arrivals(t.arrivals, t.model.decode_slo)
+    assert hb.max() >= 2 and (hb == 0).mean() > 0.2
+    say("arrival-time heartbeats, history", history, "iterations", int(hb.sum()))
+    ev = aladdin.Evaluator(0, tile=256)
+    ev.load_trace(t)
+    ws, ds = [], []
+    for a, b in [(0, 1), (1, 1700), (1700, 3000)]:
+        r = ev.place(t.q_l_in[a:b], t.q_l_pred[a:b], hb_before=hb[a:b])
+        ws.append(r.worker)
+        ds.append(r.diag)
+    summ = ev.summary()
+    ev.close()
+    compare(np.concatenate(ws), np.concatenate(ds), summ, oracle_hb(t, hb), "arrivals/%s" % history)
+
+
+def test_heartbeats_per_query_checked(aladdin):
+    t = wl.make_trace("hbbad", 28, W=4, R=2, Q=10, kv_capacity=30000, model=wl.BASE_MODEL)
+    ev = aladdin.Evaluator(0)
+    ev.load_trace(t)
+    hb = np.zeros(10, np.int32)
+    hb[4] = -1
+    with pytest.raises(aladdin.AladdinError) as e:
+        ev.place(t.q_l_in, t.q_l_pred, hb_before=hb)
+    assert e.value.code == aladdin.ALD_EINVAL
+    ev.close()
+
+
 @pytest.mark.parametrize("seed", range(3))
 def test_unequal_capacities(aladdin, seed):
     # capacities differ between workers (some equal), some workers start empty:
