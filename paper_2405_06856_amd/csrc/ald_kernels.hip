@@ -361,27 +361,43 @@ __global__ __launch_bounds__(BUILD_THREADS) void k_ingest(State st, const int64_
 }
 
 // ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(BUILD_THREADS) void k_build(State st, int mode)
+// One worker's rebuild decision and build (all threads of the block).
+__device__ __forceinline__ void build_one(const State& st, int mode, int gw, int s)
 {
-    int gw, s;
-    if (mode == 1) {
-        s = blockIdx.x / MAX_DIRTY;
-        const int j = blockIdx.x % MAX_DIRTY;
-        if (s >= st.S || j >= st.dcount[s]) return;
-        gw = st.dlist[s * MAX_DIRTY + j];
-        if (st.built[gw]) return;
-    } else {
-        gw = blockIdx.x;
-        s = find_scen_by_worker(st, gw);
-    }
     const Ctl* c = st.ctl + s;
     if (mode == 0) {
         if (c->err || c->start >= c->Q) return;
-        if (!c->rebuild && st.built[gw]) return;
+        if (st.built[gw]) {
+            if (!c->rebuild) return;
+            // A worker that held no live request at its last build and has taken
+            // none since (a placement clears `built`), with no prefill sum, has
+            // the same summaries and thresholds at any tau: only the slack clock
+            // of constraint (d) moves on (its gain is zero without a batch).
+            if (st.B[gw] == 0 && st.S1[gw] == 0) {
+                if (threadIdx.x == 0 && st.scen[s].use_d) st.phi_hb[gw] = c->hb_index;
+                return;
+            }
+        }
     }
     const Scen sc = st.scen[s];
     build_worker(st, sc, gw, c->tau, c->hb_index, &st.ctl[s].err);
     if (threadIdx.x == 0) st.built[gw] = 1;
+}
+
+// mode 1: the workers the last commit round listed; modes 0 and 2: every
+// worker (one block each).
+__global__ __launch_bounds__(BUILD_THREADS) void k_build(State st, int mode)
+{
+    if (mode == 1) {
+        const int s = blockIdx.x / MAX_DIRTY;
+        const int j = blockIdx.x % MAX_DIRTY;
+        if (s >= st.S || j >= st.dcount[s]) return;
+        const int gw = st.dlist[s * MAX_DIRTY + j];
+        if (st.built[gw]) return;
+        build_one(st, mode, gw, s);
+        return;
+    }
+    build_one(st, mode, blockIdx.x, find_scen_by_worker(st, blockIdx.x));
 }
 
 // ---------------------------------------------------------------------------------------------
