@@ -22,9 +22,10 @@
  *   - Algorithm 1: among workers meeting (b), (c), (e), choose the largest
  *     capacity_norm = ||(B, sum(D))||_2 before placement (compared exactly as an
  *     integer), ties to the lowest worker index; none -> rejected (-1).
- *   - heartbeat: after every H processed queries each worker runs one decode
- *     iteration (c += 1, r -= 1, finished requests leave) and the TTFT sums of
- *     constraint (c) restart at zero.
+ *   - heartbeat: after every H processed queries (or as many as the caller's
+ *     clock puts before a query, ald_place_stream_hb) each worker runs one
+ *     decode iteration (c += 1, r -= 1, finished requests leave) and the TTFT
+ *     sums of constraint (c) restart at zero.
  *   - constraint (d), prefill preemption (only with a decode history, see
  *     ald_load_workers_history): the same prefill time as (c) must also stay
  *     <= theta * min over the worker's ongoing requests of (T_dec * g - t_dec),
@@ -32,6 +33,13 @@
  *     decode iteration takes (c3 + c2*b) + k2*sum(c) (Eq. 3) and adds one token
  *     and that time to every request in it.  Ongoing = resident at load or placed
  *     in an earlier heartbeat; a worker with none has no such limit.
+ *   - split-phase decode workers (Sec. 5): a model with ttft_slo = +INFINITY
+ *     checks only (b) and (e).
+ *
+ * Around the placement: grouped placement (App. A, ald_place_grouped), the
+ * sweep with heartbeats (per arrival rate, Eq. 7; ald_sweep_scenarios_hb), and
+ * Algorithm 2's re-balancing against output-length prediction errors
+ * (ald_rebalance).
  *
  * Conventions
  *   - Every array argument except where marked "host" is a DEVICE pointer to
