@@ -322,10 +322,42 @@ static int valid_model(const ora_model_t* m)
  * Outputs (any may be NULL): worker per query (-1 = rejected) and diagnostics;
  * final per-worker batch size, sum(c), sum(r), KV peak, S1, S2.
  */
+/* Move the request of query j (placed in the current heartbeat window hb on
+ * worker wk[j]) to worker y, as if it had been placed there: it leaves x's
+ * request list and prefill sums and joins y's, with y's slack origin for (d). */
+static int move_request(worker_t* ws, int32_t W, int32_t* wk, const int64_t* win_of, const int32_t* q_lin,
+                        const int32_t* q_lpred, int64_t hb, int32_t j, int32_t y)
+{
+    const int32_t x = wk[j];
+    if (x < 0 || y < 0 || y >= W || x == y || win_of[j] != hb) return ORA_EINVAL;
+    worker_t* w = &ws[x];
+    const int64_t lin = q_lin[j], lp = q_lpred[j];
+    int64_t i = 0;
+    while (i < w->n && !(w->c[i] == lin && w->r[i] == lp && w->win[i] == hb)) ++i;
+    if (i == w->n) return ORA_EINVAL;
+    memmove(w->c + i, w->c + i + 1, (size_t)(w->n - i - 1) * sizeof(int64_t));
+    memmove(w->r + i, w->r + i + 1, (size_t)(w->n - i - 1) * sizeof(int64_t));
+    memmove(w->s0 + i, w->s0 + i + 1, (size_t)(w->n - i - 1) * sizeof(double));
+    memmove(w->win + i, w->win + i + 1, (size_t)(w->n - i - 1) * sizeof(int64_t));
+    w->n -= 1;
+    w->SC -= lin;
+    w->SR -= lp;
+    w->S1 -= lin;
+    w->S2 -= lin * lin;
+    worker_t* v = &ws[y];
+    const int rc = add_request(v, lin, lp, -v->phi, hb);
+    if (rc) return rc;
+    v->S1 += lin;
+    v->S2 += lin * lin;
+    wk[j] = y;
+    return ORA_OK;
+}
+
 static int place_impl(int32_t W, const int64_t* M, const int64_t* res_off,
                       const int32_t* res_lin, const int32_t* res_lpred, const int32_t* res_g, const double* res_tdec,
                       const ora_model_t* model, int32_t Q, const int32_t* q_lin, const int32_t* q_lpred,
-                      int32_t H, const int32_t* hb_before, int32_t no_commit, int32_t check, int32_t n_threads,
+                      int32_t H, const int32_t* hb_before, int32_t n_moves, const int32_t* mv_at,
+                      const int32_t* mv_query, const int32_t* mv_to, int32_t no_commit, int32_t check, int32_t n_threads,
                       int32_t* out_worker, int32_t* out_nfeas, int32_t* out_near_tie,
                       int64_t* out_peak_chosen, int64_t* out_excess_min,
                       double* out_ttft_chosen, double* out_tdec_chosen,
@@ -340,6 +372,8 @@ static int place_impl(int32_t W, const int64_t* M, const int64_t* res_off,
     pair_t* pr = (pair_t*)calloc((size_t)W, sizeof(pair_t));
     int* order = (int*)calloc((size_t)W, sizeof(int));
     unsigned __int128* keys = (unsigned __int128*)calloc((size_t)W, sizeof(unsigned __int128));
+    int32_t* wk = NULL;     /* with moves: each query's worker */
+    int64_t* win_of = NULL; /* and the window it was placed in */
     int rc = ORA_OK;
     if (!ws || !pr || !order || !keys) { rc = ORA_ENOMEM; goto done; }
 
@@ -361,7 +395,23 @@ static int place_impl(int32_t W, const int64_t* M, const int64_t* res_off,
     const int use_d = res_tdec != NULL;
     int64_t hb = 0;  /* heartbeat window */
     int32_t since_hb = 0;
-    for (int32_t q = 0; q < Q; ++q) {
+    if (n_moves > 0) {  /* moves need each query's worker and placement window */
+        wk = (int32_t*)malloc((size_t)(Q > 0 ? Q : 1) * sizeof(int32_t));
+        win_of = (int64_t*)malloc((size_t)(Q > 0 ? Q : 1) * sizeof(int64_t));
+        if (!wk || !win_of) { rc = ORA_ENOMEM; goto done; }
+        for (int32_t q = 0; q < Q; ++q) { wk[q] = -1; win_of[q] = -1; }
+    }
+    int32_t next_move = 0;
+    for (int32_t q = 0; q <= Q; ++q) {
+        /* moves scheduled before query q (after the last query when q == Q) */
+        while (next_move < n_moves && mv_at[next_move] == q) {
+            if (mv_query[next_move] < 0 || mv_query[next_move] >= q) { rc = ORA_EINVAL; goto done; }
+            rc = move_request(ws, W, wk, win_of, q_lin, q_lpred, hb, mv_query[next_move], mv_to[next_move]);
+            if (rc) goto done;
+            if (out_worker) out_worker[mv_query[next_move]] = mv_to[next_move];
+            next_move += 1;
+        }
+        if (q == Q) break;
         const int64_t lin = q_lin[q], lp = q_lpred[q];
         if (lin < 1 || lp < 1) { rc = ORA_EINVAL; goto done; }
         /* heartbeats driven by the caller's clock: hb_before[q] decode
@@ -412,6 +462,7 @@ static int place_impl(int32_t W, const int64_t* M, const int64_t* res_off,
         if (best >= 0 && !no_commit) {
             worker_t* w = &ws[best];
             rc = add_request(w, lin, lp, -w->phi, hb);
+            if (wk) { wk[q] = best; win_of[q] = hb; }
             if (rc) goto done;
             w->S1 += lin;
             w->S2 += lin * lin;
@@ -439,6 +490,8 @@ done:
     free(pr);
     free(order);
     free(keys);
+    free(wk);
+    free(win_of);
     return rc;
 }
 
@@ -460,7 +513,7 @@ int ora_place(int32_t W, const int64_t* M, const int64_t* res_off,
               int64_t* fin_S1, int64_t* fin_S2)
 {
     return place_impl(W, M, res_off, res_lin, res_lpred, res_g, res_tdec, model, Q, q_lin, q_lpred, H, NULL,
-                      no_commit, check, n_threads, out_worker, out_nfeas, out_near_tie, out_peak_chosen,
+                      0, NULL, NULL, NULL, no_commit, check, n_threads, out_worker, out_nfeas, out_near_tie, out_peak_chosen,
                       out_excess_min, out_ttft_chosen, out_tdec_chosen, fin_B, fin_SC, fin_SR, fin_peak, fin_S1,
                       fin_S2);
 }
@@ -479,8 +532,33 @@ int ora_place_hb(int32_t W, const int64_t* M, const int64_t* res_off,
 {
     if (!hb_before && Q > 0) return ORA_EINVAL;
     return place_impl(W, M, res_off, res_lin, res_lpred, res_g, res_tdec, model, Q, q_lin, q_lpred, 0, hb_before,
-                      0, check, 1, out_worker, out_nfeas, out_near_tie, out_peak_chosen, out_excess_min,
+                      0, NULL, NULL, NULL, 0, check, 1, out_worker, out_nfeas, out_near_tie, out_peak_chosen, out_excess_min,
                       out_ttft_chosen, out_tdec_chosen, fin_B, fin_SC, fin_SR, fin_peak, fin_S1, fin_S2);
+}
+
+/* As ora_place_hb (hb_before may be NULL: no heartbeat), with n_moves moves of
+ * placed requests: before query mv_at[k] (mv_at non-decreasing; Q = after the
+ * last query), the request of query mv_query[k], placed in the current
+ * heartbeat window, moves to worker mv_to[k] as if it had been placed there
+ * (out_worker records the move).  ORA_EINVAL for a move of a request that is
+ * not in the current window. */
+int ora_place_moves(int32_t W, const int64_t* M, const int64_t* res_off,
+                    const int32_t* res_lin, const int32_t* res_lpred, const int32_t* res_g, const double* res_tdec,
+                    const ora_model_t* model, int32_t Q, const int32_t* q_lin, const int32_t* q_lpred,
+                    const int32_t* hb_before, int32_t n_moves, const int32_t* mv_at, const int32_t* mv_query,
+                    const int32_t* mv_to, int32_t* out_worker, int32_t* out_nfeas, int32_t* out_near_tie,
+                    int64_t* out_peak_chosen, int64_t* out_excess_min,
+                    double* out_ttft_chosen, double* out_tdec_chosen,
+                    int64_t* fin_B, int64_t* fin_SC, int64_t* fin_SR, int64_t* fin_peak,
+                    int64_t* fin_S1, int64_t* fin_S2)
+{
+    if (n_moves < 0 || (n_moves > 0 && (!mv_at || !mv_query || !mv_to))) return ORA_EINVAL;
+    for (int32_t k = 0; k < n_moves; ++k)
+        if (mv_at[k] < 0 || mv_at[k] > Q || (k > 0 && mv_at[k] < mv_at[k - 1])) return ORA_EINVAL;
+    return place_impl(W, M, res_off, res_lin, res_lpred, res_g, res_tdec, model, Q, q_lin, q_lpred, 0, hb_before,
+                      n_moves, mv_at, mv_query, mv_to, 0, 1, 1, out_worker, out_nfeas, out_near_tie,
+                      out_peak_chosen, out_excess_min, out_ttft_chosen, out_tdec_chosen, fin_B, fin_SC, fin_SR,
+                      fin_peak, fin_S1, fin_S2);
 }
 
 /*

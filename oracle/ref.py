@@ -61,6 +61,9 @@ def lib():
         L.ora_place_hb.argtypes = [i32, P, P, P, P, P, P, ctypes.POINTER(OraModel), i32, P, P, P, i32,
                                    P, P, P, P, P, P, P, P, P, P, P, P, P]
         L.ora_place_hb.restype = ctypes.c_int
+        L.ora_place_moves.argtypes = [i32, P, P, P, P, P, P, ctypes.POINTER(OraModel), i32, P, P, P, i32, P, P, P,
+                                      P, P, P, P, P, P, P, P, P, P, P, P, P]
+        L.ora_place_moves.restype = ctypes.c_int
         L.ora_sweep.argtypes = [i32, P, P, i32, P, P, i32, P, P, P]
         L.ora_sweep.restype = ctypes.c_int
         L.ora_kv_peak.argtypes = [i64, P, P]
@@ -151,6 +154,37 @@ def place_hb(W, kv_capacity, res_offsets, res_l_in, res_l_pred, res_generated, m
                         _ptr(out.sum_r), _ptr(out.peak), _ptr(out.S1), _ptr(out.S2))
     if rc != ORA_OK:
         raise RuntimeError("oracle ora_place_hb failed with code %d" % rc)
+    return out
+
+
+def place_moves(W, kv_capacity, res_offsets, res_l_in, res_l_pred, res_generated, model, q_l_in, q_l_pred,
+                moves, hb_before=None, res_t_dec=None) -> PlaceResult:
+    """As place_hb (hb_before None: no heartbeat), with moves = [(at, query, to)]:
+    before query `at` the request of `query` (placed in the current window)
+    moves to worker `to`."""
+    L = lib()
+    Q = int(len(q_l_in))
+    c64 = lambda a: np.ascontiguousarray(a, dtype=np.int64)
+    c32 = lambda a: np.ascontiguousarray(a, dtype=np.int32)
+    M = c64(kv_capacity)
+    off = c64(res_offsets) if res_offsets is not None else None
+    rl, rp, rg = (c32(a) if a is not None else None for a in (res_l_in, res_l_pred, res_generated))
+    td = np.ascontiguousarray(res_t_dec, dtype=np.float64) if res_t_dec is not None else None
+    ql, qp = c32(q_l_in), c32(q_l_pred)
+    hbb = c32(hb_before) if hb_before is not None else None
+    mv = np.asarray(moves, dtype=np.int32).reshape(-1, 3)
+    at, qi, to = (np.ascontiguousarray(mv[:, k]) for k in range(3))
+    out = PlaceResult(*(np.zeros(Q, t) for t in (np.int32, np.int32, np.int32, np.int64, np.int64,
+                                                 np.float64, np.float64)),
+                      *(np.zeros(W, np.int64) for _ in range(6)))
+    m = to_model(model)
+    rc = L.ora_place_moves(W, _ptr(M), _ptr(off), _ptr(rl), _ptr(rp), _ptr(rg), _ptr(td), ctypes.byref(m), Q,
+                           _ptr(ql), _ptr(qp), _ptr(hbb), len(mv), _ptr(at), _ptr(qi), _ptr(to), _ptr(out.worker),
+                           _ptr(out.n_feasible), _ptr(out.near_tie), _ptr(out.kv_peak_chosen),
+                           _ptr(out.kv_excess_min), _ptr(out.ttft_chosen), _ptr(out.tdec_chosen), _ptr(out.B),
+                           _ptr(out.sum_c), _ptr(out.sum_r), _ptr(out.peak), _ptr(out.S1), _ptr(out.S2))
+    if rc != ORA_OK:
+        raise RuntimeError("oracle ora_place_moves failed with code %d" % rc)
     return out
 
 

@@ -76,7 +76,8 @@ class BruteWorker:
         return len(self.vecs)
 
 
-def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0, use_d=False, hb_before=None):
+def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0, use_d=False, hb_before=None,
+                moves=()):
     """Per query a dict: chosen worker (-1 = none), n_feasible, per-worker KV
     peaks and a flag telling whether any exact latency margin is so small that
     fp64 rounding could decide it (those queries are not comparable bit for bit)."""
@@ -85,7 +86,27 @@ def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0, u
     decode_only = math.isinf(model.ttft_slo)  # a decode worker of split-phase serving
     out = []
     since = 0
+    placed = {}  # query -> worker, for the moves
+    moves = sorted(moves, key=lambda m: m[0])
+
+    def apply_moves(at):
+        for m_at, j, y in moves:
+            if m_at != at:
+                continue
+            x = placed[j]
+            # the query's own request: new this window, nothing generated yet
+            k = next(k for k, m in enumerate(workers[x].meta)
+                     if m[3] and m[2] == queries[j][0] and m[1] == queries[j][1])
+            workers[x].vecs.pop(k)
+            workers[x].meta.pop(k)
+            q = Req(queries[j][0], queries[j][1], 0, True)
+            workers[y].vecs.append(q.footprint())
+            workers[y].meta.append([q.l_in, q.l_pred, q.l_in, True, 0, Fraction(0)])
+            placed[j] = y
+            out[j]["worker"] = y
+
     for qi, (l_in, l_pred) in enumerate(queries):
+        apply_moves(qi)
         for _ in range(hb_before[qi] if hb_before is not None else 0):
             for w in workers:
                 w.heartbeat(model)
@@ -135,6 +156,7 @@ def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0, u
             w = workers[chosen]
             w.vecs.append(qv)
             w.meta.append([l_in, l_pred, l_in, True, 0, F(0)])
+            placed[qi] = chosen
         out.append({"worker": chosen, "n_feasible": sum(feas), "peaks": peaks, "norms": norms,
                     "close": close})
         if heartbeat_every:
@@ -143,4 +165,5 @@ def brute_place(workers: List[BruteWorker], model, queries, heartbeat_every=0, u
                 for w in workers:
                     w.heartbeat(model)
                 since = 0
+    apply_moves(len(queries))
     return out

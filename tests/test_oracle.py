@@ -213,6 +213,109 @@ def test_heartbeats_per_query_match_bruteforce(use_d):
     assert compared > 1000
 
 
+def _moves_case(rng, use_d):
+    W = int(rng.integers(2, 5))
+    model = _random_model(rng)
+    model = dataclasses.replace(model, c1=float(rng.uniform(0.0, 0.02)), k1=float(rng.uniform(0.0, 0.004)),
+                                ttft_slo=float(rng.uniform(0.02, 0.06)))
+    residents, t_dec = [], []
+    for _ in range(W):
+        rs, ts = [], []
+        for _ in range(int(rng.integers(0, 5))):
+            lp = int(rng.integers(1, 9))
+            g = int(rng.integers(0, lp))
+            rs.append((int(rng.integers(1, 9)), lp, g))
+            ts.append(float(rng.uniform(0.0, 2.0)) * g * model.decode_slo)
+        residents.append(rs)
+        t_dec.append(ts)
+    M = [int(rng.integers(20, 80)) for _ in range(W)]
+    Q = int(rng.integers(2, 14))
+    queries = [(int(rng.integers(1, 9)), int(rng.integers(1, 9))) for _ in range(Q)]
+    hbb = rng.choice([0, 0, 1, 2], Q).astype(np.int32)
+    off = np.zeros(W + 1, np.int64)
+    rl, rp, rg, td = [], [], [], []
+    for i in range(W):
+        for k, (a, b, g) in enumerate(residents[i]):
+            rl.append(a); rp.append(b); rg.append(g); td.append(t_dec[i][k])
+        off[i + 1] = len(rl)
+    q = np.array(queries, np.int32).reshape(-1, 2)
+    args = (W, np.asarray(M, np.int64), off, np.array(rl, np.int32), np.array(rp, np.int32), np.array(rg, np.int32),
+            model, q[:, 0], q[:, 1])
+    td = np.array(td, np.float64) if use_d else None
+    # moves before query k (inside a window or at its end), each of a request
+    # placed earlier in the same window, chosen on the run with the moves so far
+    # (earlier placements do not depend on later moves)
+    moves = []
+    for k in range(1, Q + 1):
+        if rng.random() < 0.35:
+            start = max([i for i in range(k) if i == 0 or hbb[i] > 0])
+            r = ref.place_moves(*args, moves, hb_before=hbb, res_t_dec=td)
+            cand = [j for j in range(start, k) if r.worker[j] >= 0]
+            if cand:
+                j = int(rng.choice(cand))
+                y = int(rng.choice([w for w in range(W) if w != r.worker[j]]))
+                moves.append((k, j, y))
+    return args, hbb, td, moves, residents, t_dec, M, queries, model
+
+
+@pytest.mark.parametrize("use_d", [False, True])
+def test_moves_match_bruteforce(use_d):
+    """Moving a request placed in the current window is placing it on the new
+    worker: against the brute force with the same moves applied literally."""
+    rng = np.random.default_rng(800 + int(use_d))
+    compared = moved = 0
+    for case in range(250):
+        args, hbb, td, moves, residents, t_dec, M, queries, model = _moves_case(rng, use_d)
+        res = ref.place_moves(*args, moves, hb_before=hbb, res_t_dec=td)
+        W = args[0]
+        bw = [BruteWorker(M[i], [Req(a, b, g, t_dec=t_dec[i][k]) for k, (a, b, g) in enumerate(residents[i])])
+              for i in range(W)]
+        want = brute_place(bw, model, queries, use_d=use_d, hb_before=hbb, moves=moves)
+        moved += len(moves)
+        for k, wq in enumerate(want):
+            if wq["close"]:
+                break
+            norms = sorted(wq["norms"])
+            if any(0 < b - a <= 1e-12 * b for a, b in zip(norms, norms[1:])):
+                break
+            assert res.worker[k] == wq["worker"], (case, k, moves)
+            assert res.n_feasible[k] == wq["n_feasible"], (case, k)
+            compared += 1
+    assert compared > 800 and moved > 150
+
+
+def test_move_there_and_back_is_no_move():
+    rng = np.random.default_rng(810)
+    n = 0
+    for case in range(60):
+        args, hbb, td, moves, *_ = _moves_case(rng, False)
+        if not moves:
+            continue
+        e, j, y = moves[0]
+        base = ref.place_moves(*args, [], hb_before=hbb)
+        if base.worker[j] < 0:
+            continue
+        x = int(base.worker[j])
+        back = ref.place_moves(*args, [(e, j, y), (e, j, x)], hb_before=hbb)
+        for f in ("worker", "n_feasible", "B", "sum_c", "sum_r", "peak", "S1", "S2"):
+            assert np.array_equal(getattr(base, f), getattr(back, f)), f
+        n += 1
+    assert n > 20
+
+
+def test_move_outside_the_window_is_rejected():
+    # moves before query k come before the heartbeats that precede it: the
+    # request of query 0 can move before query 1, not before query 2 once a
+    # heartbeat preceded query 1
+    args = (2, np.array([100, 100], np.int64), np.zeros(3, np.int64), np.zeros(0, np.int32), np.zeros(0, np.int32),
+            np.zeros(0, np.int32), FREE, np.array([3, 3, 3], np.int32), np.array([4, 4, 4], np.int32))
+    hb = np.array([0, 1, 0], np.int32)
+    ok = ref.place_moves(*args, [(1, 0, 1)], hb_before=hb)
+    assert ok.worker[0] == 1
+    with pytest.raises(RuntimeError):
+        ref.place_moves(*args, [(2, 0, 1)], hb_before=hb)
+
+
 @pytest.mark.parametrize("H", [0, 2])
 def test_decode_workers_match_bruteforce(H):
     """Split-phase decode workers (infinite TTFT SLO): only (b) and (e), even

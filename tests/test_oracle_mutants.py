@@ -52,6 +52,9 @@ MUTANTS = [
     ("(d) resident slack from the predicted length", "s0 = model->decode_slo * (double)g - res_tdec[k];",
      "s0 = model->decode_slo * (double)lp - res_tdec[k];"),
     ("one heartbeat fewer before a query", "k < hb_before[q]; ++k)", "k + 1 < hb_before[q]; ++k)"),
+    ("a moved request keeps its prefill on the source", "    w->S1 -= lin;\n    w->S2 -= lin * lin;\n", ""),
+    ("a moved request takes the source's slack origin", "add_request(v, lin, lp, -v->phi, hb)",
+     "add_request(v, lin, lp, -w->phi, hb)"),
     # split-phase decode workers
     ("decode workers still check (d)", "if (use_d && !decode_only) {", "if (use_d) {"),
     ("decode workers flag TTFT near ties", "(!decode_only && near(o->ttft, m->ttft_slo))", "near(o->ttft, m->ttft_slo)"),
@@ -91,6 +94,8 @@ PINS = [
     pins.test_preemption_limit_needs_an_ongoing_request,
     lambda: pins.test_heartbeats_per_query_match_bruteforce(False),
     lambda: pins.test_heartbeats_per_query_match_bruteforce(True),
+    lambda: pins.test_moves_match_bruteforce(False),
+    lambda: pins.test_moves_match_bruteforce(True),
     lambda: pins.test_decode_workers_match_bruteforce(0),
     lambda: pins.test_decode_workers_match_bruteforce(2),
     pins.test_rebalance_worked_example,
