@@ -169,6 +169,21 @@ int ald_place_stream(ald_handle_t handle, int32_t Q, const int32_t* q_l_in, cons
 int ald_place_stream_hb(ald_handle_t handle, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
                         const int32_t* hb_before, int32_t* out_worker, ald_query_diag_t* out_diag);
 
+/* Move K requests placed in the current heartbeat window (by calls since the
+ * last heartbeat) between loaded workers, as if each had been placed on its
+ * new worker: Algorithm 2 (Sec. 4.3) re-schedules new requests before they
+ * run, and its moves (ald_rebalance) are applied with this call.  Host arrays
+ * [K]: the requests' l_in and l_pred, and their workers from and to (global
+ * indices, from != to).  A request is found on `from` by its lengths; moves
+ * run in order.  The moved requests leave the source's prefill sums of
+ * constraint (c) and join the destination's; with a decode history they start
+ * at the destination's slack origin.  ALD_EINVAL when a request is not on its
+ * worker in the current window, ALD_ESLOTS when a destination has no slot left;
+ * then nothing changes.  The placements the caller recorded are the caller's
+ * to update. */
+int ald_move_requests(ald_handle_t handle, int32_t K, const int32_t* l_in, const int32_t* l_pred,
+                      const int32_t* from, const int32_t* to);
+
 /* Grouped placement (App. A, distributed scheduling): the loaded workers are
  * split into G consecutive groups of group_workers[g] workers (host array,
  * each >= 1, summing to W); query x of the stream (counted across calls since

@@ -50,7 +50,7 @@ DIAG_DTYPE = np.dtype([("n_feasible", "<i4"), ("near_tie", "<i4"), ("kv_peak_cho
 assert DIAG_DTYPE.itemsize == 40
 
 SYMBOLS = ("ald_create", "ald_destroy", "ald_set_tile", "ald_load_workers", "ald_load_workers_history",
-           "ald_place_stream", "ald_place_stream_hb", "ald_place_grouped",
+           "ald_place_stream", "ald_place_stream_hb", "ald_place_grouped", "ald_move_requests",
            "ald_sweep_scenarios", "ald_sweep_scenarios_hb", "ald_rebalance", "ald_worker_summary", "ald_set_profiling", "ald_kernel_time",
            "ald_last_error", "ald_strerror")
 
@@ -69,6 +69,7 @@ def _load():
         "ald_place_stream": ([P, i32, P, P, i32, P, P], ctypes.c_int),
         "ald_place_grouped": ([P, i32, P, i32, P, P, i32, P, P], ctypes.c_int),
         "ald_place_stream_hb": ([P, i32, P, P, P, P, P], ctypes.c_int),
+        "ald_move_requests": ([P, i32, P, P, P, P], ctypes.c_int),
         "ald_sweep_scenarios": ([P, i32, P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_sweep_scenarios_hb": ([P, i32, P, P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_rebalance": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P], ctypes.c_int),
@@ -147,6 +148,14 @@ def ald_place_stream_hb(h, Q: int, q_l_in, q_l_pred, hb_before, out_worker, out_
         raise ValueError("hb_before must hold one count per query")
     _check(h, _L.ald_place_stream_hb(h, int(Q), _dptr(q_l_in), _dptr(q_l_pred), hb.ctypes.data_as(ctypes.c_void_p),
                                      _dptr(out_worker), _dptr(out_diag)))
+
+
+def ald_move_requests(h, K: int, l_in, l_pred, from_worker, to_worker) -> None:
+    """Host arrays of K moves."""
+    a = [np.ascontiguousarray(x, dtype=np.int32) for x in (l_in, l_pred, from_worker, to_worker)]
+    if any(x.shape != (int(K),) for x in a):
+        raise ValueError("every move array must hold K entries")
+    _check(h, _L.ald_move_requests(h, int(K), *[x.ctypes.data_as(ctypes.c_void_p) for x in a]))
 
 
 def ald_place_grouped(h, G: int, group_workers, Q: int, q_l_in, q_l_pred, heartbeat_every: int, out_worker,
@@ -312,6 +321,10 @@ class Evaluator:
         if d is not None:
             res.diag = d.cpu().numpy().view(DIAG_DTYPE)
         return res
+
+    def move_requests(self, l_in, l_pred, from_worker, to_worker) -> None:
+        """Move requests placed in the current heartbeat window between workers."""
+        ald_move_requests(self.h, len(l_in), l_in, l_pred, from_worker, to_worker)
 
     def place_grouped(self, group_workers, q_l_in, q_l_pred, heartbeat_every=0, diag=True) -> Placement:
         """Grouped placement (App. A): query x of the stream goes to group x mod G."""

@@ -10,8 +10,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libaladdin.so")
 SOURCES = [os.path.join(CSRC, f) for f in ("ald_host.cpp", "ald_kernels.hip", "ald_commit.hip", "ald_commit_d.hip",
-                                                  "ald_rebalance.hip")]
-HEADERS = [os.path.join(CSRC, f) for f in ("ald_internal.h", "ald_device.h", "ald_commit.h", "ald_rebalance.h")] + [
+                                                  "ald_rebalance.hip", "ald_move.hip")]
+HEADERS = [os.path.join(CSRC, f) for f in ("ald_internal.h", "ald_device.h", "ald_commit.h", "ald_rebalance.h", "ald_move.h")] + [
     os.path.join(ROOT, "include", "aladdin.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -4,6 +4,7 @@
 #include "../../include/aladdin.h"
 #include "ald_internal.h"
 #include "ald_rebalance.h"
+#include "ald_move.h"
 
 #include <algorithm>
 #include <cmath>
@@ -68,6 +69,8 @@ struct ald_handle {
     const int32_t* hb_host = nullptr;  // per-query heartbeats of the running call (host), or null
     int32_t* hb_dev = nullptr;         // their device copy
     size_t hb_dev_n = 0;
+    void* mv_mem = nullptr;            // tables of ald_move_requests
+    size_t mv_bytes = 0;
     int32_t* err_word = nullptr;
     int32_t prof = 0;  // kernel kinds timed (bit k = kind k)
     std::vector<Events> pending;
@@ -522,6 +525,7 @@ int ald_destroy(ald_handle_t h)
     (void)hipFree(h->err_word);
     if (h->rb_mem) (void)hipFree(h->rb_mem);
     if (h->hb_dev) (void)hipFree(h->hb_dev);
+    if (h->mv_mem) (void)hipFree(h->mv_mem);
     for (Events& e : h->pool) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
     for (Events& e : h->pending) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
     delete h;
@@ -775,6 +779,78 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
                      int32_t heartbeat_every, int32_t* out_worker, ald_query_diag_t* out_diag)
 {
     return place_stream(h, Q, q_l_in, q_l_pred, heartbeat_every, nullptr, out_worker, out_diag);
+}
+
+int ald_move_requests(ald_handle_t h, int32_t K, const int32_t* l_in, const int32_t* l_pred, const int32_t* from,
+                      const int32_t* to)
+{
+    if (!h) return ALD_EINVAL;
+    HIPCHK(h, hipSetDevice(h->device));
+    if (!h->main) return fail(h, ALD_ESTATE, "ald_load_workers has not been called");
+    if (K < 0) return fail(h, ALD_EINVAL, "K must be >= 0");
+    if (K == 0) return ALD_OK;
+    if (!l_in || !l_pred || !from || !to) return fail(h, ALD_EINVAL, "null argument");
+    const int32_t LMAX = 1 << 24;
+    // per worker: the requests it gives up, then the ones it takes
+    std::vector<std::vector<int32_t>> rm(h->W), in(h->W);
+    for (int32_t k = 0; k < K; ++k) {
+        if (from[k] < 0 || from[k] >= h->W || to[k] < 0 || to[k] >= h->W || from[k] == to[k])
+            return fail(h, ALD_EINVAL, "move " + std::to_string(k) + ": workers out of range or equal");
+        if (l_in[k] < 1 || l_in[k] > LMAX || l_pred[k] < 1 || l_pred[k] > LMAX)
+            return fail(h, ALD_EINVAL, "move " + std::to_string(k) + ": lengths must lie in [1, 2^24]");
+        rm[from[k]].push_back(k);
+        in[to[k]].push_back(k);
+    }
+    std::vector<MoveWorker> mw;
+    std::vector<int32_t> lin, lp;
+    for (int32_t w = 0; w < h->W; ++w) {
+        if (rm[w].empty() && in[w].empty()) continue;
+        MoveWorker x{};
+        x.gw = w;
+        x.rm0 = (int32_t)lin.size();
+        for (int32_t k : rm[w]) { lin.push_back(l_in[k]); lp.push_back(l_pred[k]); }
+        x.rm1 = x.in0 = (int32_t)lin.size();
+        for (int32_t k : in[w]) { lin.push_back(l_in[k]); lp.push_back(l_pred[k]); }
+        x.in1 = (int32_t)lin.size();
+        mw.push_back(x);
+    }
+    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    const size_t b_mw = up(mw.size() * sizeof(MoveWorker)), b_q = up(lin.size() * sizeof(int32_t));
+    const size_t need = b_mw + 2 * b_q;
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    if (need > h->mv_bytes) {
+        if (h->mv_mem) HIPCHK(h, hipFree(h->mv_mem));
+        h->mv_mem = nullptr;
+        h->mv_bytes = 0;
+        HIPCHK(h, hipMalloc(&h->mv_mem, need));
+        h->mv_bytes = need;
+    }
+    char* base = (char*)h->mv_mem;
+    MoveArgs a{};
+    a.mw = (const MoveWorker*)base;
+    a.nw = (int32_t)mw.size();
+    a.tau = h->tau;
+    a.hb = h->hb_index;
+    a.lin = (const int32_t*)(base + b_mw);
+    a.lpred = (const int32_t*)(base + b_mw + b_q);
+    a.err = h->err_word;
+    HIPCHK(h, hipMemcpyAsync(base, mw.data(), mw.size() * sizeof(MoveWorker), hipMemcpyHostToDevice, h->stream));
+    HIPCHK(h, hipMemcpyAsync(base + b_mw, lin.data(), lin.size() * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
+    HIPCHK(h, hipMemcpyAsync(base + b_mw + b_q, lp.data(), lp.size() * sizeof(int32_t), hipMemcpyHostToDevice,
+                             h->stream));
+    HIPCHK(h, hipMemsetAsync(h->err_word, 0, sizeof(int32_t), h->stream));
+    a.apply = 0;  // check every worker first: a move that cannot be applied changes nothing
+    HIPCHK(h, launch_move(h->main->st, a, h->stream));
+    a.apply = 1;
+    HIPCHK(h, launch_move(h->main->st, a, h->stream));
+    int32_t dev_err = 0;
+    HIPCHK(h, hipMemcpyAsync(&dev_err, h->err_word, sizeof(int32_t), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    if (dev_err == DEV_ESLOTS) return fail(h, ALD_ESLOTS, "a worker has no request slot left for a moved request");
+    if (dev_err != 0)
+        return fail(h, ALD_EINVAL, "a moved request is not on its worker in the current heartbeat window");
+    h->check_all = true;  // the changed workers are rebuilt by the next call
+    return ALD_OK;
 }
 
 int ald_place_stream_hb(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
