@@ -25,6 +25,7 @@ struct Arena {
     std::vector<int32_t> hW;  // workers per scenario
     int32_t S = 0, NW = 0;
     int32_t T = 0;            // tile the scratch is laid out for
+    int32_t target = 0;       // and the evaluation grid it aimed at
     int32_t eval_blocks = 0, sel_blocks = 0, commit_blocks = 0;
     size_t scratch_bytes = 0;
     void* scratch = nullptr;
@@ -54,6 +55,11 @@ struct ald_handle {
     hipStream_t stream = nullptr;
     std::string err;
     int32_t tile = 4096;
+    // pair-evaluation blocks the device holds at once per evaluation variant
+    // [mode][diagnostics] (compute units x blocks per unit): a placement's
+    // evaluation grid is sized to one such wave of blocks, since a partial
+    // second wave leaves most of the chip idle
+    int32_t eval_wave[3][2] = {};
     Arena* main = nullptr;
     Arena* sweep = nullptr;  // kept between sweeps so that its memory is reused
     int32_t W = 0;
@@ -323,6 +329,7 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
     a->sel_blocks = sb;
     a->commit_blocks = cb;
     a->T = T;
+    a->target = target_blocks;
     const size_t need = (size_t)bits * 16 + (size_t)part * sizeof(ulonglong2) + (size_t)qs * sizeof(QSum) + 1024;
     if (need > a->scratch_bytes) {
         if (a->scratch) HIPCHK(h, hipFree(a->scratch));
@@ -503,9 +510,20 @@ int ald_create(ald_handle_t* out, int device, void* hip_stream)
     if (hipGetDeviceCount(&count) != hipSuccess || count <= 0) return ALD_EHIP;
     if (device < 0 || device >= count) return ALD_EINVAL;
     if (hipSetDevice(device) != hipSuccess) return ALD_EHIP;
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess || cus <= 0)
+        return ALD_EHIP;
+    int32_t wave[3][2];
+    for (int m = 0; m < 3; ++m)
+        for (int x = 0; x < 2; ++x) {
+            const int per_cu = eval_blocks_per_cu(m, x == 1);
+            if (per_cu <= 0) return ALD_EHIP;
+            wave[m][x] = cus * per_cu;
+        }
     ald_handle* h = new ald_handle();
     h->device = device;
     h->stream = (hipStream_t)hip_stream;
+    std::copy(&wave[0][0], &wave[0][0] + 6, &h->eval_wave[0][0]);
     if (hipMalloc(&h->err_word, sizeof(int32_t)) != hipSuccess) {
         delete h;
         return ALD_EHIP;
@@ -728,8 +746,9 @@ int place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t
     Arena* a = h->main;
     int32_t T = std::min(h->tile, Q);
     if (H > 0) T = std::min(T, H);
-    if (T != a->T) {
-        rc = layout_scratch(h, a, T, 2048 * 256 / EVAL_THREADS);  // about 8192 evaluation waves
+    const int32_t wave = h->eval_wave[a->eval_mode][out_diag ? 1 : 0];
+    if (T != a->T || wave != a->target) {
+        rc = layout_scratch(h, a, T, wave);
         if (rc != ALD_OK) return rc;
     }
     Ctl c{};
@@ -1004,7 +1023,7 @@ int ald_place_grouped(ald_handle_t h, int32_t G, const int32_t* group_workers, i
     int32_t T = std::min(h->tile, qmax);
     if (Hg > 0) T = std::min(T, Hg);
     for (Ctl& x : c) x.T = T;
-    rc = layout_scratch(h, &a, T, 2048 * 256 / EVAL_THREADS);  // also copies the scenario table
+    rc = layout_scratch(h, &a, T, h->eval_wave[a.eval_mode][out_diag ? 1 : 0]);  // also copies the scenario table
     if (rc != ALD_OK) return rc;
     std::vector<TileInfo> ti(G);
     for (auto& t : ti) { t = TileInfo{}; t.first_pc[0] = t.first_pc[1] = INT32_MAX; }

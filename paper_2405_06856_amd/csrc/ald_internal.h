@@ -241,6 +241,9 @@ hipError_t launch_build(const State& st, hipStream_t stream, int mode);
 // mode 0: latency checks in fp64; 1: integer thresholds, near-tie margins in
 // fp64; 2: integer thresholds and near-tie sets
 hipError_t launch_eval(const State& st, int32_t blocks, int mode, hipStream_t stream);
+// pair-evaluation blocks of the variant launch_eval takes for (mode, ex) that
+// one compute unit holds at once, or 0 if the runtime cannot say
+int eval_blocks_per_cu(int mode, bool ex);
 hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream);
 // use_d: some scenario checks constraint (d)
 hipError_t launch_commit(const State& st, int32_t blocks, bool use_d, hipStream_t stream);

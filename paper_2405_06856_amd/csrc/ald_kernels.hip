@@ -1083,6 +1083,16 @@ hipError_t launch_eval(const State& st, int32_t blocks, int mode, hipStream_t st
     return hipGetLastError();
 }
 
+int eval_blocks_per_cu(int mode, bool ex)
+{
+    const void* f = mode == 2 ? (ex ? (const void*)k_eval<2, true> : (const void*)k_eval<2, false>)
+                  : mode == 1 ? (ex ? (const void*)k_eval<1, true> : (const void*)k_eval<1, false>)
+                              : (ex ? (const void*)k_eval<0, true> : (const void*)k_eval<0, false>);
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, f, EVAL_THREADS, 0) != hipSuccess) return 0;
+    return n;
+}
+
 hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream)
 {
     hipLaunchKernelGGL(k_select, dim3(blocks), dim3(SEL_THREADS), 0, stream, st);
