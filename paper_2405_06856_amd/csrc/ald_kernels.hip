@@ -338,9 +338,12 @@ __global__ __launch_bounds__(BUILD_THREADS) void k_ingest(State st, const int64_
             s[pos] = (int32_t)(x & 0xffffffffu);
         }
     }
-    if (tdec != nullptr) {
-        // constraint (d)'s log, in input order: phi = 0 at load, so each
-        // resident's entry holds its slack T_dec * g - t_dec
+    // constraint (d)'s log exists only where (d) is checked (a decode worker's
+    // model ignores the decode history, and its log arrays hold no slots)
+    const bool keep_log = tdec != nullptr && st.scen[0].use_d;
+    if (keep_log) {
+        // the log, in input order: phi = 0 at load, so each resident's entry
+        // holds its slack T_dec * g - t_dec
         const Scen& sc = st.scen[0];
         for (int k = tid; k < R; k += NT) {
             const int32_t p = lpred[r0 + k], g = gen[r0 + k];
@@ -356,7 +359,7 @@ __global__ __launch_bounds__(BUILD_THREADS) void k_ingest(State st, const int64_
         st.S1[gw] = 0;
         st.S2[gw] = 0;
         st.hbs[gw] = -1;
-        st.lgn[gw] = tdec != nullptr ? R : 0;
+        st.lgn[gw] = keep_log ? R : 0;
     }
 }
 

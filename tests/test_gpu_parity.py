@@ -144,6 +144,18 @@ def oracle_hb(t, hb):
                         t.q_l_in, t.q_l_pred, hb, res_t_dec=t.res_t_dec)
 
 
+def test_decode_workers_with_history_many_residents(aladdin):
+    """A decode worker's model ignores the decode history, so no per-request
+    log of constraint (d) is kept: loading 9,000 residents with decode times
+    must not write one (regression: the load once wrote the log whenever
+    decode times were given, past the arrays sized for no log)."""
+    m = dataclasses.replace(wl.BASE_MODEL, ttft_slo=math.inf)
+    t = wl.with_decode_history(wl.make_trace("decode-wide", 27, W=300, R=30, Q=600, kv_capacity=30000, model=m), 14)
+    say("decode workers with history, 300 x 30 residents")
+    for tile in (128, 1024):
+        compare(*gpu_place(aladdin, t, tile=tile), ref.place_trace(t), "decode-wide/%d" % tile)
+
+
 @pytest.mark.parametrize("tile", [64, 1024])
 def test_heartbeats_per_query_equal_a_period(aladdin, tile):
     t = wl.make_trace("hbq", 26, W=30, R=20, Q=2501, kv_capacity=30000, model=wl.BASE_MODEL)

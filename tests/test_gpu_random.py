@@ -27,7 +27,7 @@ def aladdin():
 
 def draw(seed):
     rng = np.random.default_rng(9000 + seed)
-    W = int(rng.choice([1, 2, 3, 7, 20, 65, 130]))
+    W = int(rng.choice([1, 2, 3, 7, 20, 65, 130, 300, 1030]))
     R = int(rng.choice([0, 1, 5, 30]))
     Q = int(rng.integers(1, 1500))
     model = wl.BASE_MODEL.scaled(float(rng.choice([0.5, 1.0, 2.0])))
@@ -48,7 +48,7 @@ def draw(seed):
     return t, H, hb, tile, diag
 
 
-@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("seed", range(64))
 def test_random_configuration_matches_oracle(aladdin, seed):
     t, H, hb, tile, diag = draw(seed)
     print("random", seed, "W", t.n_workers, "Q", t.n_queries, "H", H, "clock", hb is not None, "tile", tile,
