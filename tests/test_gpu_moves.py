@@ -2,6 +2,9 @@
 applied to the placement) on the GPU vs the oracle (needs an MI355X)."""
 from __future__ import annotations
 
+import dataclasses
+import math
+
 import numpy as np
 import pytest
 
@@ -45,9 +48,9 @@ def choose_moves(t, hb, rng, points):
     return moves
 
 
-def run_gpu(aladdin, t, hb, moves, tile=256):
+def run_gpu(aladdin, t, hb, moves, tile=256, slots=0):
     ev = aladdin.Evaluator(0, tile=tile)
-    ev.load_trace(t)
+    ev.load_trace(t, slots_per_worker=slots)
     cuts = sorted({k for k, _, _ in moves} | {0, t.n_queries})
     worker = np.full(t.n_queries, -2, np.int32)
     diags = []
@@ -155,3 +158,43 @@ def test_move_outside_the_window_changes_nothing(aladdin):
     ev.close()
     want = ref.place_hb(*oracle_args(t), hb)
     assert np.array_equal(np.concatenate([a.worker, b.worker]), want.worker)
+
+
+def draw_moves_case(seed):
+    rng = np.random.default_rng(9500 + seed)
+    W = int(rng.choice([2, 3, 7, 20, 65, 130]))
+    R = int(rng.choice([0, 5, 30]))
+    Q = int(rng.integers(20, 600))
+    model = wl.BASE_MODEL.scaled(float(rng.choice([0.5, 1.0, 2.0])))
+    if rng.random() < 0.25:
+        model = dataclasses.replace(model, ttft_slo=math.inf)  # decode workers
+    elif rng.random() < 0.2:
+        model = dataclasses.replace(model, k1=-1e-7, k1q=1e-9)  # the fp64 checks
+    t = wl.make_trace("rmoves%d" % seed, 9600 + seed, W=W, R=R, Q=Q, kv_capacity=int(rng.choice([8000, 30000])),
+                      model=model, in_dist=wl.SHORT_IN, out_dist=wl.SHORT_OUT, rate=float(rng.choice([20.0, 200.0])))
+    if R > 0 and rng.random() < 0.4:
+        t = wl.with_decode_history(t, 9700 + seed)
+    if rng.random() < 0.7:
+        hb = wl.heartbeats_from_arrivals(t.arrivals, model.decode_slo)
+    else:
+        hb = np.zeros(Q, np.int32)
+    points = sorted(rng.choice(np.arange(1, Q + 1), size=min(Q, 8), replace=False).tolist())
+    return t, hb, points, int(rng.choice([64, 256, 1024])), rng
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_moves_match_oracle(aladdin, seed):
+    """Random configurations with moves between placement calls: GPU vs oracle."""
+    t, hb, points, tile, rng = draw_moves_case(seed)
+    moves = choose_moves(t, hb, rng, points)
+    say("random moves", seed, "W", t.n_workers, "Q", t.n_queries, "moves", len(moves), "tile", tile,
+        "history", t.res_t_dec is not None, "ttft", t.model.ttft_slo)
+    want = ref.place_moves(*oracle_args(t), moves, hb_before=hb, res_t_dec=t.res_t_dec)
+    # moves are not checked against the batch limit, so leave room for them
+    slots = int(np.diff(t.res_offsets).max(initial=0)) + t.n_queries
+    worker, diag, summ = run_gpu(aladdin, t, hb, moves, tile=tile, slots=slots)
+    assert np.array_equal(worker, want.worker), np.flatnonzero(worker != want.worker)[:10]
+    for f in ("n_feasible", "near_tie", "kv_peak_chosen", "kv_excess_min"):
+        assert np.array_equal(diag[f].astype(np.int64), getattr(want, f).astype(np.int64)), f
+    for f in ("B", "sum_c", "sum_r", "peak"):
+        assert np.array_equal(summ[f].astype(np.int64), getattr(want, f)), f
