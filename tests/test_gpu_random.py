@@ -73,3 +73,38 @@ def test_random_configuration_matches_oracle(aladdin, seed):
     if hb is not None or H == 0 or t.n_queries % H:
         for f in ("B", "sum_c", "sum_r", "peak"):
             assert np.array_equal(summ[f].astype(np.int64), getattr(want, f)), f
+
+
+def draw_sweep(seed):
+    rng = np.random.default_rng(9800 + seed)
+    S = int(rng.integers(1, 24))
+    scen, H = [], []
+    for _ in range(S):
+        model = wl.BASE_MODEL.scaled(float(rng.choice([0.5, 1.0, 2.0])))
+        if rng.random() < 0.2:
+            model = dataclasses.replace(model, ttft_slo=math.inf)
+        elif rng.random() < 0.2:
+            model = dataclasses.replace(model, k1=-1e-7, k1q=1e-9)
+        scen.append(wl.Scenario(n_workers=int(rng.choice([1, 2, 3, 7, 20, 65, 130, 300])), gpus_per_worker=1,
+                                kv_capacity=int(rng.choice([4000, 8000, 30000, 120000])), model=model))
+        H.append(int(rng.choice([0, 1, 3, 17, 100])))
+    Q = int(rng.integers(1, 1500))
+    q_in = wl._lengths(rng, *wl.SHORT_IN, Q).astype(np.int32)
+    q_pred = wl._lengths(rng, *wl.SHORT_OUT, Q).astype(np.int32)
+    tile = int(rng.choice([64, 256, 1024, 4096]))
+    return scen, np.array(H, np.int32), q_in, q_pred, tile
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_sweep_matches_oracle(aladdin, seed):
+    """Random scenario sets (sizes, capacities, models, heartbeat periods) swept at once."""
+    scen, H, q_in, q_pred, tile = draw_sweep(seed)
+    print("random sweep", seed, "S", len(scen), "W", [s.n_workers for s in scen], "Q", q_in.size, "tile", tile,
+          flush=True)
+    ev = aladdin.Evaluator(0, tile=tile)
+    rej, first, workers = ev.sweep(scen, q_in, q_pred, want_workers=True, heartbeat_every=H)
+    ev.close()
+    orej, ofirst, oworkers = ref.sweep(scen, q_in, q_pred, want_workers=True, heartbeat_every=H)
+    assert np.array_equal(workers, oworkers), np.argwhere(workers != oworkers)[:5]
+    assert np.array_equal(rej, orej)
+    assert np.array_equal(first, ofirst)
