@@ -6,6 +6,7 @@ on its own workers, with a heartbeat after every H / G of its queries."""
 from __future__ import annotations
 
 import dataclasses
+import math
 
 import numpy as np
 import pytest
@@ -142,3 +143,39 @@ def test_grouped_arguments_checked(aladdin):
             ev.place_grouped(sizes, t.q_l_in[:Q], t.q_l_pred[:Q], heartbeat_every=H)
         assert e.value.code == aladdin.ALD_EINVAL
     ev.close()
+
+
+def draw_grouped(seed):
+    rng = np.random.default_rng(9900 + seed)
+    G = int(rng.integers(1, 7))
+    sizes = [int(x) for x in rng.integers(1, 25, G)]
+    W = sum(sizes)
+    R = int(rng.choice([0, 5, 16]))
+    model = wl.BASE_MODEL.scaled(float(rng.choice([0.5, 1.0, 2.0])))
+    if rng.random() < 0.2:
+        model = dataclasses.replace(model, ttft_slo=math.inf)
+    elif rng.random() < 0.2:
+        model = dataclasses.replace(model, k1=-1e-7, k1q=1e-9)
+    H = G * int(rng.choice([0, 1, 5, 20]))
+    Q = int(rng.integers(1, 1500))
+    if H > 0:
+        Q = max(1, Q // H) * H  # with heartbeats a grouped call ends at one
+    t = wl.make_trace("rgrouped%d" % seed, 9950 + seed, W=W, R=R, Q=Q, kv_capacity=int(rng.choice([8000, 30000])),
+                      model=model, in_dist=wl.SHORT_IN, out_dist=wl.SHORT_OUT)
+    if R > 0 and rng.random() < 0.3:
+        t = wl.with_decode_history(t, 9990 + seed)
+    return t, sizes, H, int(rng.choice([64, 256, 1024]))
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_grouped_matches_oracle(aladdin, seed):
+    """Random group counts and sizes, models, decode histories, heartbeats and tiles."""
+    t, sizes, H, tile = draw_grouped(seed)
+    say("random grouped", seed, "sizes", sizes, "H", H, "Q", t.n_queries, "tile", tile,
+        "history", t.res_t_dec is not None, "ttft", t.model.ttft_slo)
+    ev = aladdin.Evaluator(0, tile=tile)
+    ev.load_trace(t)
+    got = ev.place_grouped(sizes, t.q_l_in, t.q_l_pred, heartbeat_every=H)
+    ev.close()
+    w, d = oracle_grouped(t, sizes, H)
+    check(got, w, d, "random grouped %d" % seed)
