@@ -143,3 +143,22 @@ def test_rebalance_invalid_input_changes_nothing(ev):
     b4.models = [dataclasses.replace(b4.models[0], k2=0.0)]
     with pytest.raises(aladdin.AladdinError):
         ev.rebalance(b4)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_rebalance_matches_oracle(ev, seed):
+    """Random batches: problem counts, per-problem sizes, error spreads,
+    unplaced shares and per-problem rho."""
+    rng = np.random.default_rng(9400 + seed)
+    P = int(rng.integers(1, 20))
+    W = [int(x) for x in rng.choice([1, 2, 3, 9, 40, 300], P)]
+    R = [int(x) for x in rng.choice([0, 1, 7, 60], P)]
+    n_new = [int(x) for x in rng.choice([0, 1, 5, 80, 600], P)]
+    b = wl.make_rebalance("random%d" % seed, 9450 + seed, P, W, R, n_new,
+                          sigma_err=float(rng.choice([0.0, 0.3, 0.8, 1.5])), unplaced=float(rng.choice([0.0, 0.1, 0.5])))
+    if rng.random() < 0.5:
+        base = b.models[0]
+        b.models = [dataclasses.replace(base, c2=float(rng.choice([0.0, 3e-5, 1e-4, 4e-4]))) for _ in range(P)]
+    say("random rebalance", seed, "P", P, "W", W[:6], "new", n_new[:6])
+    got = ev.rebalance(b, want_log=True)
+    check_against_oracle(b, got)
