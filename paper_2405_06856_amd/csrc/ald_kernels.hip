@@ -463,19 +463,18 @@ __device__ __forceinline__ void ex_unpack(uint64_t k, int32_t& ex, int32_t& w)
     w = k == ~0ull ? -1 : (int32_t)~(uint32_t)k;
 }
 
-// Word `acc` with lane J's value replaced by the wave-uniform `v`
-// (v_writelane_b32 on each half, the lane an inline constant, J < 16).  The s_nop
-// gives an SGPR that a VALU instruction wrote just before (a compare's lane
-// mask) its wait states before v_writelane reads it: the compiler does not
-// look inside the asm for that hazard, and without the wait the lanes took
-// stale words.
+// LLVM's writelane intrinsic (v_writelane_b32): the value of lane `lane` of
+// `old` replaced by the wave-uniform `v`.  Through the intrinsic the compiler
+// sees the instruction and inserts whatever wait states its operands need.
+__device__ int ald_writelane(int v, int lane, int old) __asm("llvm.amdgcn.writelane.i32");
+
+// Word `acc` with lane J's value replaced by the wave-uniform `v` (one
+// v_writelane_b32 per half, the lane an inline constant, J < 16).
 template <int J>
 __device__ __forceinline__ uint64_t put_lane_c(uint64_t acc, uint64_t v)
 {
-    uint32_t lo = (uint32_t)acc, hi = (uint32_t)(acc >> 32);
-    asm("s_nop 4\n\tv_writelane_b32 %0, %2, %4\n\tv_writelane_b32 %1, %3, %4"
-        : "+v"(lo), "+v"(hi)
-        : "s"((uint32_t)v), "s"((uint32_t)(v >> 32)), "n"(J));
+    const uint32_t lo = (uint32_t)ald_writelane((int)(uint32_t)v, J, (int)(uint32_t)acc);
+    const uint32_t hi = (uint32_t)ald_writelane((int)(uint32_t)(v >> 32), J, (int)(uint32_t)(acc >> 32));
     return ((uint64_t)hi << 32) | lo;
 }
 __device__ __forceinline__ uint64_t put_lane(uint64_t acc, uint64_t v, int j)

@@ -508,6 +508,29 @@ def test_decode_margin_exactly_zero_is_feasible_and_near_tie():
     assert res.worker[1] == -1 and res.near_tie[1] == 0
 
 
+def test_tdec_chosen_worked_example():
+    # Eq. 3 for the chosen worker's batch with the query in it, computed by hand.
+    # Coefficients are powers of two, so every fp64 step below is exact.
+    # Resident (l_in 10, l_pred 6, generated 2): context c = 12, remaining r = 4,
+    # D = c + r/2 = 14.  Query 1 (5, 8): D = 5 + 8/2 = 9, batch b = 2:
+    #   T_d = (c3 + c2*2) + k2*(14 + 9) = (0.25 + 0.25) + 0.0625*23 = 1.9375.
+    # Query 2 (1, 2): D = 1 + 1 = 2, batch b = 3:
+    #   T_d = (0.25 + 0.375) + 0.0625*25 = 2.1875.
+    # With gamma = 1 (D = c + r): D = 16, 13, 3:
+    #   T_d = 0.5 + 0.0625*29 = 2.3125, then 0.625 + 0.0625*32 = 2.625.
+    m = dataclasses.replace(FREE, c3=0.25, c2=0.125, k2=0.0625, decode_slo=4.0, theta=1.0)
+    res = run(1, 10 ** 6, [[(10, 6, 2)]], m, [(5, 8), (1, 2)])
+    assert list(res.worker) == [0, 0]
+    assert list(res.tdec_chosen) == [1.9375, 2.1875]
+    m1 = dataclasses.replace(m, gamma_num=2, gamma_log2den=1)
+    res = run(1, 10 ** 6, [[(10, 6, 2)]], m1, [(5, 8), (1, 2)])
+    assert list(res.tdec_chosen) == [2.3125, 2.625]
+    # a rejected query reports 0
+    tight = dataclasses.replace(m, decode_slo=1.6)  # (1.6 - 0.25) - 0.25 = 1.1 < 0.0625 * 23
+    res = run(1, 10 ** 6, [[(10, 6, 2)]], tight, [(5, 8)])
+    assert res.worker[0] == -1 and res.tdec_chosen[0] == 0.0
+
+
 def test_ttft_margin_exactly_zero_is_feasible():
     m = dataclasses.replace(FREE, c1=0.5, k1=0.25, k1q=0.0, ttft_slo=3.0)
     res = run(2, 10 ** 6, [[], []], m, [(10, 2), (1, 1)])

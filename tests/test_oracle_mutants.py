@@ -38,6 +38,10 @@ MUTANTS = [
      "o->ttft_ok = decode_only || o->ttft < m->ttft_slo;"),
     ("heartbeat counts only placements", "if (H > 0 && !no_commit) {\n            since_hb += 1;",
      "if (H > 0 && !no_commit && best >= 0) {\n            since_hb += 1;"),
+    ("chosen decode time without the query's batch slot", "o->tdec = (m->c3 + m->c2 * (double)b) + m->k2 * sumD;",
+     "o->tdec = (m->c3 + m->c2 * (double)B) + m->k2 * sumD;"),
+    ("chosen decode time without the query's context", "o->tdec = (m->c3 + m->c2 * (double)b) + m->k2 * sumD;",
+     "o->tdec = (m->c3 + m->c2 * (double)b) + m->k2 * ldexp((double)DS, -gs);"),
     ("smallest excess over feasible workers only", "if (ex < excess_min) excess_min = ex;",
      "if (pr[i].feasible && ex < excess_min) excess_min = ex;"),
     # constraint (d)
@@ -83,6 +87,7 @@ PINS = [
     pins.test_heartbeat_is_one_iteration_shift,
     pins.test_committed_placements_respect_every_constraint,
     pins.test_decode_margin_exactly_zero_is_feasible_and_near_tie,
+    pins.test_tdec_chosen_worked_example,
     pins.test_ttft_margin_exactly_zero_is_feasible,
     pins.test_capacity_norm_ranking_picks_fullest_feasible,
     pins.test_decode_near_tie_band_is_relative,
