@@ -258,6 +258,22 @@ int ald_rebalance(ald_handle_t handle, int32_t P, const int32_t* n_workers, cons
                   const int64_t* new_offsets, const int32_t* new_l_pred, int32_t* new_worker,
                   int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t* out_log, int64_t* out_obj);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * computation and arguments as ald_rebalance, with every table in a fixed
+ * device array of the library (about 600 KB per device, set up by
+ * ald_create and held until the process ends) instead of handle memory.  It
+ * calls no hipMalloc or hipFree.  out_le and out_be must be given (ALD_EINVAL
+ * otherwise); at most 4096 problems and 16383 chunks of ongoing requests (a
+ * problem's ongoing requests fill chunks of 2048; ALD_EINVAL beyond).  Every
+ * call on one device shares that device's array and leaves its contents
+ * behind; calls that overlap on one device (other streams or threads) race. */
+int ald_rebalance_noalloc(ald_handle_t handle, int32_t P, const int32_t* n_workers, const ald_model_t* models,
+                          const int64_t* old_offsets, const int32_t* old_worker, const int32_t* old_l_pred,
+                          const int32_t* old_l_out, const int32_t* old_l_real, const int32_t* old_l_repred,
+                          const int64_t* new_offsets, const int32_t* new_l_pred, int32_t* new_worker,
+                          int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t* out_log, int64_t* out_obj);
+
 /* Current state of every loaded worker (device arrays of W): batch size, sum of
  * contexts, sum of remaining lengths, KV peak over future iterations. */
 int ald_worker_summary(ald_handle_t handle, int32_t* B, int64_t* sum_c, int64_t* sum_r, int64_t* peak);

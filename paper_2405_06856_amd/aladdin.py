@@ -51,7 +51,7 @@ assert DIAG_DTYPE.itemsize == 40
 
 SYMBOLS = ("ald_create", "ald_destroy", "ald_set_tile", "ald_load_workers", "ald_load_workers_history",
            "ald_place_stream", "ald_place_stream_hb", "ald_place_grouped", "ald_move_requests",
-           "ald_sweep_scenarios", "ald_sweep_scenarios_hb", "ald_rebalance", "ald_worker_summary", "ald_set_profiling", "ald_kernel_time",
+           "ald_sweep_scenarios", "ald_sweep_scenarios_hb", "ald_rebalance", "ald_rebalance_noalloc", "ald_worker_summary", "ald_set_profiling", "ald_kernel_time",
            "ald_last_error", "ald_strerror")
 
 
@@ -73,6 +73,7 @@ def _load():
         "ald_sweep_scenarios": ([P, i32, P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_sweep_scenarios_hb": ([P, i32, P, P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_rebalance": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P], ctypes.c_int),
+        "ald_rebalance_noalloc": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P], ctypes.c_int),
         "ald_worker_summary": ([P, P, P, P, P], ctypes.c_int),
         "ald_set_profiling": ([P, i32], ctypes.c_int),
         "ald_kernel_time": ([P, i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)], ctypes.c_int),
@@ -186,19 +187,37 @@ def ald_sweep_scenarios_hb(h, S: int, scen, heartbeat_every, Q: int, q_l_in, q_l
                                         _dptr(out_rejected), _dptr(out_first_reject), _dptr(out_worker)))
 
 
+def _rebalance_call(fn, h, P: int, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out, old_l_real,
+                  old_l_repred, new_offsets, new_l_pred, new_worker, out_le=None, out_be=None, out_moves=None,
+                  out_log=None, out_obj=None) -> None:
+    nw = np.ascontiguousarray(n_workers, dtype=np.int32)
+    oo = np.ascontiguousarray(old_offsets, dtype=np.int64)
+    no = np.ascontiguousarray(new_offsets, dtype=np.int64)
+    _check(h, fn(h, int(P), nw.ctypes.data_as(ctypes.c_void_p), ctypes.cast(models, ctypes.c_void_p),
+                               oo.ctypes.data_as(ctypes.c_void_p), _dptr(old_worker), _dptr(old_l_pred),
+                               _dptr(old_l_out), _dptr(old_l_real), _dptr(old_l_repred),
+                               no.ctypes.data_as(ctypes.c_void_p), _dptr(new_l_pred), _dptr(new_worker),
+                               _dptr(out_le), _dptr(out_be), _dptr(out_moves), _dptr(out_log), _dptr(out_obj)))
+
+
 def ald_rebalance(h, P: int, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out, old_l_real,
                   old_l_repred, new_offsets, new_l_pred, new_worker, out_le=None, out_be=None, out_moves=None,
                   out_log=None, out_obj=None) -> None:
     """n_workers (int32), models (Model array) and the offsets (int64) are host
     arrays; everything else is a device tensor."""
-    nw = np.ascontiguousarray(n_workers, dtype=np.int32)
-    oo = np.ascontiguousarray(old_offsets, dtype=np.int64)
-    no = np.ascontiguousarray(new_offsets, dtype=np.int64)
-    _check(h, _L.ald_rebalance(h, int(P), nw.ctypes.data_as(ctypes.c_void_p), ctypes.cast(models, ctypes.c_void_p),
-                               oo.ctypes.data_as(ctypes.c_void_p), _dptr(old_worker), _dptr(old_l_pred),
-                               _dptr(old_l_out), _dptr(old_l_real), _dptr(old_l_repred),
-                               no.ctypes.data_as(ctypes.c_void_p), _dptr(new_l_pred), _dptr(new_worker),
-                               _dptr(out_le), _dptr(out_be), _dptr(out_moves), _dptr(out_log), _dptr(out_obj)))
+    _rebalance_call(_L.ald_rebalance, h, P, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out,
+                    old_l_real, old_l_repred, new_offsets, new_l_pred, new_worker, out_le, out_be, out_moves,
+                    out_log, out_obj)
+
+
+def ald_rebalance_noalloc(h, P: int, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out,
+                          old_l_real, old_l_repred, new_offsets, new_l_pred, new_worker, out_le, out_be,
+                          out_moves=None, out_log=None, out_obj=None) -> None:
+    """As ald_rebalance, with the library's fixed device array instead of
+    allocated tables (out_le and out_be required)."""
+    _rebalance_call(_L.ald_rebalance_noalloc, h, P, n_workers, models, old_offsets, old_worker, old_l_pred,
+                    old_l_out, old_l_real, old_l_repred, new_offsets, new_l_pred, new_worker, out_le, out_be,
+                    out_moves, out_log, out_obj)
 
 
 def ald_worker_summary(h, B, sum_c, sum_r, peak) -> None:

@@ -520,6 +520,8 @@ int ald_create(ald_handle_t* out, int device, void* hip_stream)
             if (per_cu <= 0) return ALD_EHIP;
             wave[m][x] = cus * per_cu;
         }
+    // the allocation-free entry point's fixed device array, once per device
+    if (rb_static_init(device) != hipSuccess) return ALD_EHIP;
     ald_handle* h = new ald_handle();
     h->device = device;
     h->stream = (hipStream_t)hip_stream;
@@ -1056,6 +1058,115 @@ int ald_place_grouped(ald_handle_t h, int32_t G, const int32_t* group_workers, i
 
 namespace {
 
+// Algorithm 2 over P problems.  noalloc: the tables live in the library's
+// fixed device array (rb_static_ptr) and the caller passes the error arrays,
+// so nothing is allocated; otherwise they live in memory the handle keeps.
+int rebalance_impl(ald_handle_t h, int32_t P, const int32_t* n_workers, const ald_model_t* models,
+                  const int64_t* old_offsets, const int32_t* old_worker, const int32_t* old_l_pred,
+                  const int32_t* old_l_out, const int32_t* old_l_real, const int32_t* old_l_repred,
+                  const int64_t* new_offsets, const int32_t* new_l_pred, int32_t* new_worker,
+                  int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t* out_log, int64_t* out_obj,
+                   bool noalloc)
+{
+    if (!h) return ALD_EINVAL;
+    HIPCHK(h, hipSetDevice(h->device));
+    if (P < 1) return fail(h, ALD_EINVAL, "P must be >= 1");
+    if (!n_workers || !models || !old_offsets || !new_offsets) return fail(h, ALD_EINVAL, "null argument");
+    if (old_offsets[0] != 0 || new_offsets[0] != 0) return fail(h, ALD_EINVAL, "offsets must start at 0");
+    std::vector<RbProblem> prob(P);
+    std::vector<RbChunk> chunks;
+    int64_t wtot = 0;
+    for (int32_t p = 0; p < P; ++p) {
+        const std::string tag = "problem " + std::to_string(p) + ": ";
+        if (n_workers[p] < 1 || n_workers[p] > RB_WMAX)
+            return fail(h, ALD_EINVAL, tag + "n_workers must lie in [1, " + std::to_string(RB_WMAX) + "]");
+        const int64_t o0 = old_offsets[p], o1 = old_offsets[p + 1], n0 = new_offsets[p], n1 = new_offsets[p + 1];
+        if (o1 < o0 || n1 < n0) return fail(h, ALD_EINVAL, tag + "offsets must not decrease");
+        if (n1 - n0 > RB_JMAX) return fail(h, ALD_EINVAL, tag + "more than " + std::to_string(RB_JMAX) + " new requests");
+        const ald_model_t& m = models[p];
+        const double q = m.c2 / m.k2;
+        if (!(m.k2 > 0.0) || !(m.c2 >= 0.0) || !std::isfinite(q) || q > 1e9)
+            return fail(h, ALD_EINVAL, tag + "needs k2 > 0 and 0 <= c2 / k2 <= 1e9");
+        prob[p] = RbProblem{o0, o1, n0, wtot, (int64_t)std::llrint(q), n_workers[p], (int32_t)(n1 - n0)};
+        for (int64_t b = o0; b < o1; b += RB_CHUNK) chunks.push_back(RbChunk{b, std::min(o1, b + RB_CHUNK), p, 0});
+        wtot += n_workers[p];
+    }
+    const int64_t n_old = old_offsets[P], n_new = new_offsets[P];
+    if (n_old >= ((int64_t)1 << 31) || n_new >= ((int64_t)1 << 31)) return fail(h, ALD_EINVAL, "too many requests");
+    if ((n_old > 0 && (!old_worker || !old_l_pred || !old_l_out || !old_l_real || !old_l_repred)) ||
+        (n_new > 0 && (!new_l_pred || !new_worker)))
+        return fail(h, ALD_EINVAL, "null request array");
+    if (chunks.size() + (size_t)P > (size_t)INT32_MAX) return fail(h, ALD_EINVAL, "too many blocks");
+    // device tables (and error arrays when the caller passes none)
+    const bool own_err = out_le == nullptr || out_be == nullptr;
+    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    const size_t b_prob = up(P * sizeof(RbProblem)), b_chunk = up((chunks.size() + 1) * sizeof(RbChunk));
+    const size_t b_err = own_err ? up(wtot * sizeof(int64_t)) : 0;
+    const size_t need = b_prob + b_chunk + 2 * b_err;
+    char* base = nullptr;
+    int32_t* err_word = h->err_word;
+    if (noalloc) {
+        if (own_err) return fail(h, ALD_EINVAL, "the allocation-free call needs out_le and out_be");
+        if (P > RB_STATIC_P || chunks.size() + 1 > (size_t)RB_STATIC_CHUNKS)
+            return fail(h, ALD_EINVAL, "the allocation-free call takes at most " + std::to_string(RB_STATIC_P) +
+                                           " problems and " + std::to_string(RB_STATIC_CHUNKS - 1) +
+                                           " chunks of ongoing requests (a problem's requests fill chunks of " +
+                                           std::to_string(RB_CHUNK) + ")");
+        char* mem = (char*)rb_static_ptr(h->device);
+        if (mem == nullptr) return fail(h, ALD_EHIP, "the fixed device array was not set up for this device");
+        base = mem;
+        err_word = (int32_t*)(mem + RB_STATIC_TABLES);
+    } else {
+        HIPCHK(h, hipStreamSynchronize(h->stream));  // the tables may be in use by an earlier call
+        if (need > h->rb_bytes) {
+            if (h->rb_mem) HIPCHK(h, hipFree(h->rb_mem));
+            h->rb_mem = nullptr;
+            h->rb_bytes = 0;
+            HIPCHK(h, hipMalloc(&h->rb_mem, need));
+            h->rb_bytes = need;
+        }
+        base = (char*)h->rb_mem;
+    }
+    RbArgs a{};
+    a.prob = (const RbProblem*)base;
+    a.chunk = (const RbChunk*)(base + b_prob);
+    a.nchunk = (int32_t)chunks.size();
+    a.P = P;
+    a.old_worker = old_worker;
+    a.old_lpred = old_l_pred;
+    a.old_lout = old_l_out;
+    a.old_lreal = old_l_real;
+    a.old_lrepred = old_l_repred;
+    a.new_lpred = new_l_pred;
+    a.new_worker = new_worker;
+    a.le = own_err ? (int64_t*)(base + b_prob + b_chunk) : out_le;
+    a.be = own_err ? (int64_t*)(base + b_prob + b_chunk + b_err) : out_be;
+    a.moves = out_moves;
+    a.log = out_log;
+    a.obj = out_obj;
+    a.err = err_word;
+    HIPCHK(h, hipMemcpyAsync(base, prob.data(), P * sizeof(RbProblem), hipMemcpyHostToDevice, h->stream));
+    if (!chunks.empty())
+        HIPCHK(h, hipMemcpyAsync(base + b_prob, chunks.data(), chunks.size() * sizeof(RbChunk),
+                                 hipMemcpyHostToDevice, h->stream));
+    HIPCHK(h, hipMemsetAsync(a.le, 0, wtot * sizeof(int64_t), h->stream));
+    HIPCHK(h, hipMemsetAsync(a.be, 0, wtot * sizeof(int64_t), h->stream));
+    HIPCHK(h, hipMemsetAsync(err_word, 0, sizeof(int32_t), h->stream));
+    LAUNCH(h, 4, launch_rebalance(a, h->stream));
+    int32_t dev_err = 0;
+    HIPCHK(h, hipMemcpyAsync(&dev_err, err_word, sizeof(int32_t), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    prof_collect(h);
+    if (dev_err != 0) return fail(h, ALD_EINVAL, "invalid request (worker index out of range, length outside "
+                                                 "[1, 2^24], or more tokens generated than the real length)");
+    return ALD_OK;
+}
+
+
+}  // namespace
+
+namespace {
+
 // The sweep, with a heartbeat period per scenario (H null: none).
 int sweep(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* H, int32_t Q, const int32_t* q_l_in,
           const int32_t* q_l_pred, int32_t* out_rejected, int32_t* out_first_reject, int32_t* out_worker)
@@ -1168,83 +1279,20 @@ int ald_rebalance(ald_handle_t h, int32_t P, const int32_t* n_workers, const ald
                   const int64_t* new_offsets, const int32_t* new_l_pred, int32_t* new_worker,
                   int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t* out_log, int64_t* out_obj)
 {
-    if (!h) return ALD_EINVAL;
-    HIPCHK(h, hipSetDevice(h->device));
-    if (P < 1) return fail(h, ALD_EINVAL, "P must be >= 1");
-    if (!n_workers || !models || !old_offsets || !new_offsets) return fail(h, ALD_EINVAL, "null argument");
-    if (old_offsets[0] != 0 || new_offsets[0] != 0) return fail(h, ALD_EINVAL, "offsets must start at 0");
-    std::vector<RbProblem> prob(P);
-    std::vector<RbChunk> chunks;
-    int64_t wtot = 0;
-    for (int32_t p = 0; p < P; ++p) {
-        const std::string tag = "problem " + std::to_string(p) + ": ";
-        if (n_workers[p] < 1 || n_workers[p] > RB_WMAX)
-            return fail(h, ALD_EINVAL, tag + "n_workers must lie in [1, " + std::to_string(RB_WMAX) + "]");
-        const int64_t o0 = old_offsets[p], o1 = old_offsets[p + 1], n0 = new_offsets[p], n1 = new_offsets[p + 1];
-        if (o1 < o0 || n1 < n0) return fail(h, ALD_EINVAL, tag + "offsets must not decrease");
-        if (n1 - n0 > RB_JMAX) return fail(h, ALD_EINVAL, tag + "more than " + std::to_string(RB_JMAX) + " new requests");
-        const ald_model_t& m = models[p];
-        const double q = m.c2 / m.k2;
-        if (!(m.k2 > 0.0) || !(m.c2 >= 0.0) || !std::isfinite(q) || q > 1e9)
-            return fail(h, ALD_EINVAL, tag + "needs k2 > 0 and 0 <= c2 / k2 <= 1e9");
-        prob[p] = RbProblem{o0, o1, n0, wtot, (int64_t)std::llrint(q), n_workers[p], (int32_t)(n1 - n0)};
-        for (int64_t b = o0; b < o1; b += RB_CHUNK) chunks.push_back(RbChunk{b, std::min(o1, b + RB_CHUNK), p, 0});
-        wtot += n_workers[p];
-    }
-    const int64_t n_old = old_offsets[P], n_new = new_offsets[P];
-    if (n_old >= ((int64_t)1 << 31) || n_new >= ((int64_t)1 << 31)) return fail(h, ALD_EINVAL, "too many requests");
-    if ((n_old > 0 && (!old_worker || !old_l_pred || !old_l_out || !old_l_real || !old_l_repred)) ||
-        (n_new > 0 && (!new_l_pred || !new_worker)))
-        return fail(h, ALD_EINVAL, "null request array");
-    if (chunks.size() + (size_t)P > (size_t)INT32_MAX) return fail(h, ALD_EINVAL, "too many blocks");
-    // device tables (and error arrays when the caller passes none)
-    const bool own_err = out_le == nullptr || out_be == nullptr;
-    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    const size_t b_prob = up(P * sizeof(RbProblem)), b_chunk = up((chunks.size() + 1) * sizeof(RbChunk));
-    const size_t b_err = own_err ? up(wtot * sizeof(int64_t)) : 0;
-    const size_t need = b_prob + b_chunk + 2 * b_err;
-    HIPCHK(h, hipStreamSynchronize(h->stream));  // the tables may be in use by an earlier call
-    if (need > h->rb_bytes) {
-        if (h->rb_mem) HIPCHK(h, hipFree(h->rb_mem));
-        h->rb_mem = nullptr;
-        h->rb_bytes = 0;
-        HIPCHK(h, hipMalloc(&h->rb_mem, need));
-        h->rb_bytes = need;
-    }
-    char* base = (char*)h->rb_mem;
-    RbArgs a{};
-    a.prob = (const RbProblem*)base;
-    a.chunk = (const RbChunk*)(base + b_prob);
-    a.nchunk = (int32_t)chunks.size();
-    a.P = P;
-    a.old_worker = old_worker;
-    a.old_lpred = old_l_pred;
-    a.old_lout = old_l_out;
-    a.old_lreal = old_l_real;
-    a.old_lrepred = old_l_repred;
-    a.new_lpred = new_l_pred;
-    a.new_worker = new_worker;
-    a.le = own_err ? (int64_t*)(base + b_prob + b_chunk) : out_le;
-    a.be = own_err ? (int64_t*)(base + b_prob + b_chunk + b_err) : out_be;
-    a.moves = out_moves;
-    a.log = out_log;
-    a.obj = out_obj;
-    a.err = h->err_word;
-    HIPCHK(h, hipMemcpyAsync(base, prob.data(), P * sizeof(RbProblem), hipMemcpyHostToDevice, h->stream));
-    if (!chunks.empty())
-        HIPCHK(h, hipMemcpyAsync(base + b_prob, chunks.data(), chunks.size() * sizeof(RbChunk),
-                                 hipMemcpyHostToDevice, h->stream));
-    HIPCHK(h, hipMemsetAsync(a.le, 0, wtot * sizeof(int64_t), h->stream));
-    HIPCHK(h, hipMemsetAsync(a.be, 0, wtot * sizeof(int64_t), h->stream));
-    HIPCHK(h, hipMemsetAsync(h->err_word, 0, sizeof(int32_t), h->stream));
-    LAUNCH(h, 4, launch_rebalance(a, h->stream));
-    int32_t dev_err = 0;
-    HIPCHK(h, hipMemcpyAsync(&dev_err, h->err_word, sizeof(int32_t), hipMemcpyDeviceToHost, h->stream));
-    HIPCHK(h, hipStreamSynchronize(h->stream));
-    prof_collect(h);
-    if (dev_err != 0) return fail(h, ALD_EINVAL, "invalid request (worker index out of range, length outside "
-                                                 "[1, 2^24], or more tokens generated than the real length)");
-    return ALD_OK;
+    return rebalance_impl(h, P, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out, old_l_real,
+                          old_l_repred, new_offsets, new_l_pred, new_worker, out_le, out_be, out_moves, out_log,
+                          out_obj, false);
+}
+
+int ald_rebalance_noalloc(ald_handle_t h, int32_t P, const int32_t* n_workers, const ald_model_t* models,
+                          const int64_t* old_offsets, const int32_t* old_worker, const int32_t* old_l_pred,
+                          const int32_t* old_l_out, const int32_t* old_l_real, const int32_t* old_l_repred,
+                          const int64_t* new_offsets, const int32_t* new_l_pred, int32_t* new_worker,
+                          int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t* out_log, int64_t* out_obj)
+{
+    return rebalance_impl(h, P, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out, old_l_real,
+                          old_l_repred, new_offsets, new_l_pred, new_worker, out_le, out_be, out_moves, out_log,
+                          out_obj, true);
 }
 
 int ald_worker_summary(ald_handle_t h, int32_t* B, int64_t* sum_c, int64_t* sum_r, int64_t* peak)

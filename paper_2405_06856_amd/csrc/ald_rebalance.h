@@ -45,4 +45,18 @@ struct RbArgs {
 // error accumulation (nchunk + P blocks), then the greedy moves (P blocks)
 hipError_t launch_rebalance(const RbArgs& a, hipStream_t stream);
 
+// Fixed device array of the allocation-free entry point: the problem and chunk
+// tables of at most RB_STATIC_P problems and RB_STATIC_CHUNKS chunks, then the
+// error word.  One copy per device, held until the process ends.
+constexpr int RB_STATIC_P = 4096;
+constexpr int RB_STATIC_CHUNKS = 16384;
+constexpr size_t RB_STATIC_TABLES = ((RB_STATIC_P * sizeof(RbProblem) + 255) & ~(size_t)255) +
+                                    ((RB_STATIC_CHUNKS * sizeof(RbChunk) + 255) & ~(size_t)255);
+constexpr size_t RB_STATIC_BYTES = RB_STATIC_TABLES + 256;
+// Look up (once per device, with `device` current) the device address of that
+// array; later calls return the cached address.  Host code uses only this
+// address, never the array's own name.
+hipError_t rb_static_init(int device);
+void* rb_static_ptr(int device);  // null until rb_static_init succeeded for `device`
+
 }  // namespace ald

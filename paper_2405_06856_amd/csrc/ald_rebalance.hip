@@ -16,7 +16,42 @@
 #include "ald_device.h"
 #include "ald_rebalance.h"
 
+#include <mutex>
+
 namespace ald {
+
+// The allocation-free entry point's tables and error word (see rb_static_init).
+static __device__ __align__(256) unsigned char scratch[RB_STATIC_BYTES];
+
+namespace {
+constexpr int RB_STATIC_DEVICES = 64;
+std::mutex g_static_mu;
+void* g_static_ptr[RB_STATIC_DEVICES] = {};
+}  // namespace
+
+hipError_t rb_static_init(int device)
+{
+    if (device < 0 || device >= RB_STATIC_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_static_mu);
+    if (g_static_ptr[device] != nullptr) return hipSuccess;
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    if (cur != device) return hipErrorInvalidDevice;  // the caller makes `device` current
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_static_ptr[device] = p;
+    return hipSuccess;
+}
+
+void* rb_static_ptr(int device)
+{
+    if (device < 0 || device >= RB_STATIC_DEVICES) return nullptr;
+    std::lock_guard<std::mutex> lk(g_static_mu);
+    return g_static_ptr[device];
+}
 
 __device__ __forceinline__ int64_t abs64(int64_t v) { return v < 0 ? -v : v; }
 
