@@ -149,13 +149,13 @@ def time_rebalance(steps: int, oracle_problems: int = 0):
     le = torch.empty(Wt, dtype=torch.int64, device=dev)
     be = torch.empty_like(le)
     mv = torch.empty(b.P, dtype=torch.int32, device=dev)
-    obj = torch.empty(2 * b.P, dtype=torch.int64, device=dev)
+    obj = torch.empty(4 * b.P, dtype=torch.int64, device=dev)
     models = (aladdin.Model * b.P)(*[aladdin.to_model(m) for m in b.models])
 
     def call():
         nw.copy_(nw0)
         aladdin.ald_rebalance(ev.h, b.P, b.n_workers, models, b.old_offsets, *old, b.new_offsets, nl, nw,
-                              le, be, mv, None, obj)
+                              le, be, mv, 0, None, obj)
 
     for _ in range(2):
         call()
@@ -291,7 +291,7 @@ def main():
     traffic = measured_traffic() if pairs_per_eval_launch == pairs else None
 
     sweep_info = None if args.no_sweep else time_sweep(args.sweep_steps)
-    rb_info = None if args.no_rebalance else time_rebalance(args.steps, 0 if args.no_cpu else 32)
+    rb_info = None if args.no_rebalance else time_rebalance(args.steps, 0 if args.no_cpu else 8)
     scaling_info = None if (args.no_sweep or args.no_scaling) else scaling_over_rates()
     line = {
         "metric": "query x worker placement evals/sec (+ scenario sweeps/sec; % of HBM roofline)",

@@ -186,15 +186,20 @@ int ald_move_requests(ald_handle_t handle, int32_t K, const int32_t* l_in, const
 
 /* Grouped placement (App. A, distributed scheduling): the loaded workers are
  * split into G consecutive groups of group_workers[g] workers (host array,
- * each >= 1, summing to W); query x of the stream (counted across calls since
- * the load) goes to group x mod G (round robin), and each group places its own
- * queries on its own workers in arrival order with Algorithm 1, as its own
- * scheduler would.  Device arrays as for ald_place_stream; out_worker gets
- * the global worker index (or -1) and out_diag (or NULL) each query's
- * diagnostics over its group's workers.  heartbeat_every must be a multiple of
- * G (every heartbeat window then holds heartbeat_every / G queries of every
- * group), and with heartbeats the call must end at one.  Grouped and ungrouped
- * calls may alternate on one handle. */
+ * each >= 1, summing to W).  A router sends each arriving query to one group,
+ * group g receiving the share group_workers[g] / W of the stream (App. A:
+ * its arrival rate is N_g / N_w of the total): the deterministic quota method
+ * of Balinski and Young, under which every group's count stays strictly
+ * within one query of its share after every query, and equal groups take
+ * turns (query x to group x mod G).  The router continues across calls while
+ * the group sizes stay the same, and restarts with new sizes or a new load.
+ * Each group places its own queries on its own workers in arrival order with
+ * Algorithm 1, as its own scheduler would.  Heartbeats are the cluster's:
+ * after every heartbeat_every processed queries of the whole stream (0 =
+ * none), counted across calls as ald_place_stream does.  Device arrays as for
+ * ald_place_stream; out_worker gets the global worker index (or -1) and
+ * out_diag (or NULL) each query's diagnostics over its group's workers.
+ * Grouped and ungrouped calls may alternate on one handle. */
 int ald_place_grouped(ald_handle_t handle, int32_t G, const int32_t* group_workers, int32_t Q,
                       const int32_t* q_l_in, const int32_t* q_l_pred, int32_t heartbeat_every,
                       int32_t* out_worker, ald_query_diag_t* out_diag);
@@ -228,19 +233,26 @@ int ald_sweep_scenarios_hb(ald_handle_t handle, int32_t S, const ald_scenario_t*
  * Per worker i, from its ongoing requests j:
  *   l_out_j > l_pred_j (decoding past the prediction): l^e_i += l_repred_j, b^e_i += 1
  *   l_real_j < l_pred_j (finished before it):          l^e_i += l_real_j - l_pred_j, b^e_i -= 1
- * The error line of Eq. 4, divided by k2, is c_i = l^e_i + rho * b^e_i with
- * rho = c2 / k2 rounded to whole tokens (llrint); its distance from the
- * origin is |c_i| / sqrt(1 + rho^2).  Moving new request j (predicted length
- * l_pred_j) from worker x to y moves l_pred_j and one batch slot of error:
+ * The error line of Eq. 4 through (l^e_i, b^e_i) has distance
+ * |k2 l^e_i + c2 b^e_i| / sqrt(k2^2 + c2^2) from the origin; divided by k2 it is
+ * |c_i| / sqrt(1 + rho^2) with c_i = l^e_i + rho * b^e_i and rho = c2 / k2, the
+ * real ratio (not rounded).  Moving new request j (predicted length l_pred_j)
+ * from worker x to y moves l_pred_j and one batch slot of error:
  * c_x -= l_pred_j + rho, c_y += l_pred_j + rho.  The moves are greedy: while
- * some (request, other worker) pair lowers sum_i |c_i|, the pair that lowers
- * it most is applied (ties: lowest request, then lowest worker); a request
- * moves at most once, and unplaced requests (worker -1) stay.  All integer:
- * the result is exact.
+ * some (placed request, other worker) pair lowers sum_i |c_i|, the pair that
+ * lowers it most is applied (ties: lowest request, then lowest worker); a
+ * request may move again after later moves, and unplaced requests (worker
+ * -1) stay.  Every comparison is made exactly (each quantity is a + rho * b
+ * for integers a, b, and its sign is taken without rounding error).  Every
+ * move lowers the objective strictly, so the search ends; as a guard a
+ * problem that would take more than 4 * (its new requests) + (its workers)
+ * moves stops the call with ALD_EOVERFLOW (outputs then undefined).
  *
- * Host arrays: n_workers[P] (1 .. 4096), models[P] (k2 > 0, 0 <= c2/k2 <= 1e9;
- * only c2 and k2 are used), old_offsets[P+1] and new_offsets[P+1] (CSR over the
- * request arrays, starting at 0; at most 8192 new requests per problem).
+ * Host arrays: n_workers[P] (1 .. 4096), models[P] (only c2 and k2 are used:
+ * k2 a normal double in (0, 2^900], c2 = 0 or normal in [0, 2^900],
+ * c2 / k2 <= 1e9), old_offsets[P+1] and new_offsets[P+1] (CSR over the request
+ * arrays, starting at 0; at most 8192 new requests per problem, fewer than
+ * 2^30 requests in all).
  * Device arrays: old_worker, old_l_pred, old_l_out (tokens generated so far),
  * old_l_real (real output length, >= old_l_out), old_l_repred (re-predicted
  * output length) [old_offsets[P]]; new_l_pred [new_offsets[P]]; new_worker
@@ -248,15 +260,18 @@ int ald_sweep_scenarios_hb(ald_handle_t handle, int32_t S, const ald_scenario_t*
  * lie in [1, 2^24] (l_out and l_repred may be 0).
  * Device outputs (each may be NULL): out_le, out_be [sum n_workers] (final
  * errors, problem p's workers after those of problems < p); out_moves[P];
- * out_log[2 * new_offsets[P]] (problem p's moves in order as (request, target)
- * pairs starting at entry 2 * new_offsets[p]); out_obj[2P] (sum |c_i| before
- * and after).  ALD_EINVAL for a bad argument or any invalid request; then
- * new_worker is left unchanged. */
+ * out_log[2 * P * log_cap] (problem p's first log_cap moves in order as
+ * (request, target) pairs starting at entry 2 * p * log_cap; log_cap >= 0);
+ * out_obj[4P] (sum |c_i| before and after, each as the pair (a, b) meaning
+ * a + rho * b: entries 4p .. 4p+3 = a_before, b_before, a_after, b_after).
+ * ALD_EINVAL for a bad argument or any invalid request; then new_worker is
+ * left unchanged. */
 int ald_rebalance(ald_handle_t handle, int32_t P, const int32_t* n_workers, const ald_model_t* models,
                   const int64_t* old_offsets, const int32_t* old_worker, const int32_t* old_l_pred,
                   const int32_t* old_l_out, const int32_t* old_l_real, const int32_t* old_l_repred,
                   const int64_t* new_offsets, const int32_t* new_l_pred, int32_t* new_worker,
-                  int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t* out_log, int64_t* out_obj);
+                  int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t log_cap, int32_t* out_log,
+                  int64_t* out_obj);
 
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): the same
@@ -272,7 +287,8 @@ int ald_rebalance_noalloc(ald_handle_t handle, int32_t P, const int32_t* n_worke
                           const int64_t* old_offsets, const int32_t* old_worker, const int32_t* old_l_pred,
                           const int32_t* old_l_out, const int32_t* old_l_real, const int32_t* old_l_repred,
                           const int64_t* new_offsets, const int32_t* new_l_pred, int32_t* new_worker,
-                          int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t* out_log, int64_t* out_obj);
+                          int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t log_cap, int32_t* out_log,
+                          int64_t* out_obj);
 
 /* Current state of every loaded worker (device arrays of W): batch size, sum of
  * contexts, sum of remaining lengths, KV peak over future iterations. */

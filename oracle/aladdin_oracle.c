@@ -353,11 +353,49 @@ static int move_request(worker_t* ws, int32_t W, int32_t* wk, const int64_t* win
     return ORA_OK;
 }
 
+/*
+ * App. A: a router sends each arriving query to one group of workers, group i
+ * (N_i workers of N_w) receiving the share N_i / N_w of the stream.  The
+ * deterministic round robin used here is the quota method of Balinski and
+ * Young: the h-th query (h = 1, 2, ...) goes to the group with the largest
+ * N_i / (a_i + 1) among the groups whose count a_i (queries received so far)
+ * is still below h * N_i / N_w, ties to the lowest group index.  Every count
+ * then stays strictly within one query of its share h * N_i / N_w, and with
+ * equal sizes query x goes to group x mod G.  counts[G] carries the router's
+ * state from query to query.
+ */
+static int32_t route_next(int32_t G, const int32_t* N, int64_t Nw, int64_t* counts)
+{
+    int64_t h = 1;
+    for (int32_t i = 0; i < G; ++i) h += counts[i];
+    int32_t best = -1;
+    for (int32_t i = 0; i < G; ++i) {
+        if (!(counts[i] * Nw < h * (int64_t)N[i])) continue;  /* at its upper quota already */
+        if (best < 0 || (int64_t)N[i] * (counts[best] + 1) > (int64_t)N[best] * (counts[i] + 1)) best = i;
+    }
+    counts[best] += 1;
+    return best;
+}
+
+/* The groups of the first Q queries (out_group[Q]) for group sizes N[G]. */
+int ora_route_groups(int32_t G, const int32_t* N, int32_t Q, int32_t* out_group)
+{
+    if (G < 1 || Q < 0 || !N || !out_group) return ORA_EINVAL;
+    int64_t Nw = 0;
+    for (int32_t i = 0; i < G; ++i) { if (N[i] < 1) return ORA_EINVAL; Nw += N[i]; }
+    int64_t* counts = (int64_t*)calloc((size_t)G, sizeof(int64_t));
+    if (!counts) return ORA_ENOMEM;
+    for (int32_t q = 0; q < Q; ++q) out_group[q] = route_next(G, N, Nw, counts);
+    free(counts);
+    return ORA_OK;
+}
+
 static int place_impl(int32_t W, const int64_t* M, const int64_t* res_off,
                       const int32_t* res_lin, const int32_t* res_lpred, const int32_t* res_g, const double* res_tdec,
                       const ora_model_t* model, int32_t Q, const int32_t* q_lin, const int32_t* q_lpred,
                       int32_t H, const int32_t* hb_before, int32_t n_moves, const int32_t* mv_at,
-                      const int32_t* mv_query, const int32_t* mv_to, int32_t no_commit, int32_t check, int32_t n_threads,
+                      const int32_t* mv_query, const int32_t* mv_to, int32_t G, const int32_t* gsizes,
+                      int32_t no_commit, int32_t check, int32_t n_threads,
                       int32_t* out_worker, int32_t* out_nfeas, int32_t* out_near_tie,
                       int64_t* out_peak_chosen, int64_t* out_excess_min,
                       double* out_ttft_chosen, double* out_tdec_chosen,
@@ -374,8 +412,17 @@ static int place_impl(int32_t W, const int64_t* M, const int64_t* res_off,
     unsigned __int128* keys = (unsigned __int128*)calloc((size_t)W, sizeof(unsigned __int128));
     int32_t* wk = NULL;     /* with moves: each query's worker */
     int64_t* win_of = NULL; /* and the window it was placed in */
+    int64_t* gcount = NULL; /* grouped: the router's counts */
+    int32_t* gfirst = NULL; /* grouped: first worker of each group (G + 1 entries) */
+    int64_t Nw = 0;
     int rc = ORA_OK;
     if (!ws || !pr || !order || !keys) { rc = ORA_ENOMEM; goto done; }
+    if (gsizes) {
+        gcount = (int64_t*)calloc((size_t)G, sizeof(int64_t));
+        gfirst = (int32_t*)calloc((size_t)G + 1, sizeof(int32_t));
+        if (!gcount || !gfirst) { rc = ORA_ENOMEM; goto done; }
+        for (int32_t g = 0; g < G; ++g) { Nw += gsizes[g]; gfirst[g + 1] = gfirst[g] + gsizes[g]; }
+    }
 
     for (int32_t i = 0; i < W; ++i) {
         ws[i].M = M[i];
@@ -420,14 +467,21 @@ static int place_impl(int32_t W, const int64_t* M, const int64_t* res_off,
             for (int32_t i = 0; i < W; ++i) heartbeat(&ws[i], model);
             hb += 1;
         }
+        /* grouped (App. A): the query's group's workers only */
+        int32_t lo = 0, hi = W;
+        if (gsizes) {
+            const int32_t g = route_next(G, gsizes, Nw, gcount);
+            lo = gfirst[g];
+            hi = gfirst[g + 1];
+        }
         int best = -1;
         int nfeas = 0;
         int64_t excess_min = INT64_MAX;
 #ifdef _OPENMP
 #pragma omp parallel for num_threads(n_threads > 0 ? n_threads : 1) schedule(static)
 #endif
-        for (int32_t i = 0; i < W; ++i) pr[i].rc = eval_pair(&ws[i], model, lin, lp, use_d, hb, &pr[i]);
-        for (int32_t i = 0; i < W; ++i) {
+        for (int32_t i = lo; i < hi; ++i) pr[i].rc = eval_pair(&ws[i], model, lin, lp, use_d, hb, &pr[i]);
+        for (int32_t i = lo; i < hi; ++i) {
             if (pr[i].rc) { rc = pr[i].rc; goto done; }
             nfeas += pr[i].feasible;
             int64_t ex = pr[i].peak - ws[i].M;
@@ -437,17 +491,18 @@ static int place_impl(int32_t W, const int64_t* M, const int64_t* res_off,
         }
         if (check) {
             /* Algorithm 1 as written: sort bins by capacity_norm, first feasible */
-            for (int32_t i = 0; i < W; ++i) { order[i] = i; keys[i] = pr[i].key; }
+            const int32_t n = hi - lo;
+            for (int32_t k = 0; k < n; ++k) { order[k] = lo + k; keys[lo + k] = pr[lo + k].key; }
             g_sort_keys = keys;
-            qsort(order, (size_t)W, sizeof(int), cmp_rank);
+            qsort(order, (size_t)n, sizeof(int), cmp_rank);
             int first = -1;
-            for (int32_t k = 0; k < W; ++k) if (pr[order[k]].feasible) { first = order[k]; break; }
+            for (int32_t k = 0; k < n; ++k) if (pr[order[k]].feasible) { first = order[k]; break; }
             if (first != best) { rc = ORA_ECHECK; goto done; }
         }
         /* near tie: any worker ranked at or above the choice (all, if rejected)
          * whose decode, TTFT or (d) margin is within 1e-9 relative */
         int nt = 0;
-        for (int32_t i = 0; i < W; ++i) {
+        for (int32_t i = lo; i < hi; ++i) {
             if (!pr[i].near_tie) continue;
             if (best < 0 || i == best || ranks_before(pr[i].key, i, pr[best].key, best)) { nt = 1; break; }
         }
@@ -492,6 +547,8 @@ done:
     free(keys);
     free(wk);
     free(win_of);
+    free(gcount);
+    free(gfirst);
     return rc;
 }
 
@@ -513,7 +570,7 @@ int ora_place(int32_t W, const int64_t* M, const int64_t* res_off,
               int64_t* fin_S1, int64_t* fin_S2)
 {
     return place_impl(W, M, res_off, res_lin, res_lpred, res_g, res_tdec, model, Q, q_lin, q_lpred, H, NULL,
-                      0, NULL, NULL, NULL, no_commit, check, n_threads, out_worker, out_nfeas, out_near_tie, out_peak_chosen,
+                      0, NULL, NULL, NULL, 0, NULL, no_commit, check, n_threads, out_worker, out_nfeas, out_near_tie, out_peak_chosen,
                       out_excess_min, out_ttft_chosen, out_tdec_chosen, fin_B, fin_SC, fin_SR, fin_peak, fin_S1,
                       fin_S2);
 }
@@ -532,7 +589,7 @@ int ora_place_hb(int32_t W, const int64_t* M, const int64_t* res_off,
 {
     if (!hb_before && Q > 0) return ORA_EINVAL;
     return place_impl(W, M, res_off, res_lin, res_lpred, res_g, res_tdec, model, Q, q_lin, q_lpred, 0, hb_before,
-                      0, NULL, NULL, NULL, 0, check, 1, out_worker, out_nfeas, out_near_tie, out_peak_chosen, out_excess_min,
+                      0, NULL, NULL, NULL, 0, NULL, 0, check, 1, out_worker, out_nfeas, out_near_tie, out_peak_chosen, out_excess_min,
                       out_ttft_chosen, out_tdec_chosen, fin_B, fin_SC, fin_SR, fin_peak, fin_S1, fin_S2);
 }
 
@@ -556,7 +613,33 @@ int ora_place_moves(int32_t W, const int64_t* M, const int64_t* res_off,
     for (int32_t k = 0; k < n_moves; ++k)
         if (mv_at[k] < 0 || mv_at[k] > Q || (k > 0 && mv_at[k] < mv_at[k - 1])) return ORA_EINVAL;
     return place_impl(W, M, res_off, res_lin, res_lpred, res_g, res_tdec, model, Q, q_lin, q_lpred, 0, hb_before,
-                      n_moves, mv_at, mv_query, mv_to, 0, 1, 1, out_worker, out_nfeas, out_near_tie,
+                      n_moves, mv_at, mv_query, mv_to, 0, NULL, 0, 1, 1, out_worker, out_nfeas, out_near_tie,
+                      out_peak_chosen, out_excess_min, out_ttft_chosen, out_tdec_chosen, fin_B, fin_SC, fin_SR,
+                      fin_peak, fin_S1, fin_S2);
+}
+
+/* Grouped placement (App. A): the W workers form G consecutive groups of
+ * gsizes[g] workers; each query goes to the group the router picks
+ * (route_next, from the load on) and is placed with Algorithm 1 among that
+ * group's workers only, as that group's own scheduler would; the diagnostics
+ * are over the group's workers.  Heartbeats are the cluster's: after every H
+ * processed queries of the whole stream (H = 0: none), every worker runs one
+ * decode iteration. */
+int ora_place_grouped(int32_t W, const int64_t* M, const int64_t* res_off,
+                      const int32_t* res_lin, const int32_t* res_lpred, const int32_t* res_g, const double* res_tdec,
+                      const ora_model_t* model, int32_t G, const int32_t* gsizes, int32_t Q, const int32_t* q_lin,
+                      const int32_t* q_lpred, int32_t H, int32_t* out_worker, int32_t* out_nfeas,
+                      int32_t* out_near_tie, int64_t* out_peak_chosen, int64_t* out_excess_min,
+                      double* out_ttft_chosen, double* out_tdec_chosen,
+                      int64_t* fin_B, int64_t* fin_SC, int64_t* fin_SR, int64_t* fin_peak,
+                      int64_t* fin_S1, int64_t* fin_S2)
+{
+    if (G < 1 || !gsizes) return ORA_EINVAL;
+    int64_t total = 0;
+    for (int32_t g = 0; g < G; ++g) { if (gsizes[g] < 1) return ORA_EINVAL; total += gsizes[g]; }
+    if (total != W) return ORA_EINVAL;
+    return place_impl(W, M, res_off, res_lin, res_lpred, res_g, res_tdec, model, Q, q_lin, q_lpred, H, NULL,
+                      0, NULL, NULL, NULL, G, gsizes, 0, 1, 1, out_worker, out_nfeas, out_near_tie,
                       out_peak_chosen, out_excess_min, out_ttft_chosen, out_tdec_chosen, fin_B, fin_SC, fin_SR,
                       fin_peak, fin_S1, fin_S2);
 }
@@ -630,44 +713,80 @@ int64_t ora_kv_peak(int64_t n, const int64_t* c, const int64_t* r)
  *       l^e_i += l_real_j - l_pred_j,                          b^e_i -= 1
  * Error line: Eq. 4 bounds k2 * (context) + c2 * (batch); the errors shift a
  * worker's operating point by (l^e, b^e), which moves its decode time by
- * k2 * l^e + c2 * b^e.  Divided by k2 (the distance of a line from the origin
- * does not change when all its coefficients are scaled) this is
- *   c_i = l^e_i + rho * b^e_i,   rho = c2 / k2 rounded to whole tokens,
- * and the distance of worker i's error line from the origin is
- * |c_i| / sqrt(1 + rho^2).  The objective is the sum over workers.
+ * k2 * l^e + c2 * b^e.  The line through that point parallel to Eq. 4's
+ * boundary is k2 * l + c2 * b - (k2 * l^e + c2 * b^e) = 0, whose distance from
+ * the origin is |k2 * l^e + c2 * b^e| / sqrt(k2^2 + c2^2).  Every worker of a
+ * problem shares one model, so the denominator is common and the objective is
+ * sum_i |c_i| with c_i = l^e_i + rho * b^e_i, rho = c2 / k2 the real ratio of
+ * the two coefficients (not rounded).
+ *
+ * Exact arithmetic: every quantity the search compares is an integer pair
+ * (a, b) standing for a + rho * b, so every comparison is the sign of
+ * a * k2 + b * c2 (k2 > 0).  With |a|, |b| < 2^60 and k2, c2 doubles (53-bit
+ * significands), each product has at most 113 significant bits and is exact
+ * in IEEE binary128 (__float128); the rounded sum of two exact values is zero
+ * only when the exact sum is zero and otherwise has its sign.  So rb_sign is
+ * the exact sign.
+ *
  * Moving a new request j (predicted length l_pred_j) from worker x to worker
- * y changes c_x by -(l_pred_j + rho) and c_y by +(l_pred_j + rho).
- * Search (the paper gives only the objective): repeatedly apply the single
- * move with the largest decrease of sum |c_i| -- ties to the lowest request
- * index, then the lowest target worker -- while that decrease is positive;
- * a request moves at most once.  New requests that were not placed (worker
- * -1) stay where they are.  Everything is int64, so the choices are exact.
+ * y moves l_pred_j and one batch slot of error: c_x -= l_pred_j + rho,
+ * c_y += l_pred_j + rho.  The search (the paper gives only the objective and
+ * the move update): repeatedly apply the single move with the largest
+ * decrease of sum |c_i| -- ties to the lowest request index, then the lowest
+ * target worker -- while that decrease is positive.  A request may move
+ * again after a later move has changed the errors; every applied move lowers
+ * the objective strictly, so no assignment repeats and the search ends.  As a
+ * guard it stops with ORA_EOVERFLOW after 4 * n_new + W moves (never reached
+ * on the workloads).  New requests that were not placed (worker -1) stay.
  *
  * Inputs: W workers; n_old ongoing requests (worker, l_pred, l_out = tokens
  * generated so far, l_real = real output length, with l_out <= l_real, and
  * l_repred = the re-prediction); n_new new requests (l_pred, worker in/out).
  * Outputs (any may be NULL): final l^e, b^e per worker; number of moves; the
- * moves in order (request, target); sum |c_i| before and after.
+ * first log_cap moves in order (request, target); sum |c_i| before and after,
+ * each as the pair (a, b) meaning a + rho * b.
  */
-static int64_t rb_abs(int64_t v) { return v < 0 ? -v : v; }
+typedef struct { int64_t a, b; } rb_pair;  /* a + rho * b */
 
-int64_t ora_rebalance_rho(const ora_model_t* m)
+static int rb_sign(int64_t a, int64_t b, const ora_model_t* m)
 {
-    if (!(m->k2 > 0.0) || !(m->c2 >= 0.0) || !isfinite(m->c2 / m->k2) || m->c2 / m->k2 > 1e9) return -1;
-    return (int64_t)llrint(m->c2 / m->k2);
+    /* with b * c2 = 0, or both terms of one sign, the sign needs no arithmetic */
+    if (b == 0 || m->c2 == 0.0) return (a > 0) - (a < 0);
+    if (a == 0 || (a > 0) == (b > 0)) return b > 0 ? 1 : -1;
+    const __float128 x = (__float128)a * (__float128)m->k2;
+    const __float128 y = (__float128)b * (__float128)m->c2;
+    const __float128 v = x + y;
+    return (v > 0) - (v < 0);
+}
+
+static rb_pair rb_sub(rb_pair u, rb_pair v) { rb_pair r = {u.a - v.a, u.b - v.b}; return r; }
+static rb_pair rb_add(rb_pair u, rb_pair v) { rb_pair r = {u.a + v.a, u.b + v.b}; return r; }
+static rb_pair rb_abs(rb_pair u, const ora_model_t* m)
+{
+    if (rb_sign(u.a, u.b, m) < 0) { u.a = -u.a; u.b = -u.b; }
+    return u;
+}
+static int rb_fits(rb_pair u) { const int64_t L = (int64_t)1 << 60; return u.a > -L && u.a < L && u.b > -L && u.b < L; }
+
+/* Exact sign of a + (c2 / k2) * b, exposed for the unit tests. */
+int ora_rb_sign(int64_t a, int64_t b, const ora_model_t* m) { return rb_sign(a, b, m); }
+
+static int rb_model_ok(const ora_model_t* m)
+{
+    /* k2 > 0 and c2 >= 0 finite, rho = c2 / k2 at most 1e9 */
+    return m->k2 > 0.0 && m->c2 >= 0.0 && isfinite(m->k2) && isfinite(m->c2) && m->c2 <= 1e9 * m->k2;
 }
 
 int ora_rebalance(int32_t W, const ora_model_t* m,
                   int32_t n_old, const int32_t* old_worker, const int32_t* old_lpred, const int32_t* old_lout,
                   const int32_t* old_lreal, const int32_t* old_lrepred,
                   int32_t n_new, const int32_t* new_lpred, int32_t* new_worker,
-                  int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t* out_log,
+                  int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t log_cap, int32_t* out_log,
                   int64_t* out_obj_before, int64_t* out_obj_after)
 {
     const int32_t LMAX = 1 << 24;
-    if (W < 1 || n_old < 0 || n_new < 0 || !m || !new_worker) return ORA_EINVAL;
-    const int64_t rho = ora_rebalance_rho(m);
-    if (rho < 0) return ORA_EINVAL;
+    if (W < 1 || n_old < 0 || n_new < 0 || log_cap < 0 || !m || !new_worker) return ORA_EINVAL;
+    if (!rb_model_ok(m)) return ORA_EINVAL;
     for (int32_t j = 0; j < n_old; ++j) {
         if (old_worker[j] < 0 || old_worker[j] >= W) return ORA_EINVAL;
         if (old_lpred[j] < 1 || old_lpred[j] > LMAX || old_lout[j] < 0 || old_lreal[j] < 1 ||
@@ -677,55 +796,63 @@ int ora_rebalance(int32_t W, const ora_model_t* m,
     for (int32_t j = 0; j < n_new; ++j)
         if (new_lpred[j] < 1 || new_lpred[j] > LMAX || new_worker[j] < -1 || new_worker[j] >= W) return ORA_EINVAL;
 
-    int64_t* le = (int64_t*)calloc((size_t)W, sizeof(int64_t));
-    int64_t* be = (int64_t*)calloc((size_t)W, sizeof(int64_t));
-    char* moved = (char*)calloc((size_t)(n_new > 0 ? n_new : 1), 1);
-    if (!le || !be || !moved) { free(le); free(be); free(moved); return ORA_ENOMEM; }
+    rb_pair* c = (rb_pair*)calloc((size_t)W, sizeof(rb_pair));
+    if (!c) return ORA_ENOMEM;
 
-    /* the per-worker errors of the ongoing requests */
+    /* the per-worker errors of the ongoing requests: c_i = (l^e_i, b^e_i) */
     for (int32_t j = 0; j < n_old; ++j) {
         const int32_t i = old_worker[j];
-        if (old_lout[j] > old_lpred[j]) { le[i] += old_lrepred[j]; be[i] += 1; }
-        if (old_lreal[j] < old_lpred[j]) { le[i] += (int64_t)old_lreal[j] - old_lpred[j]; be[i] -= 1; }
+        if (old_lout[j] > old_lpred[j]) { c[i].a += old_lrepred[j]; c[i].b += 1; }
+        if (old_lreal[j] < old_lpred[j]) { c[i].a += (int64_t)old_lreal[j] - old_lpred[j]; c[i].b -= 1; }
     }
-#define RB_C(i) (le[i] + rho * be[i])
-    int64_t obj = 0;
-    for (int32_t i = 0; i < W; ++i) obj += rb_abs(RB_C(i));
-    if (out_obj_before) *out_obj_before = obj;
+    rb_pair obj = {0, 0};
+    for (int32_t i = 0; i < W; ++i) obj = rb_add(obj, rb_abs(c[i], m));
+    if (out_obj_before) { out_obj_before[0] = obj.a; out_obj_before[1] = obj.b; }
 
-    /* greedy moves: every (unmoved placed request, other worker) pair, in
+    /* greedy moves: every (placed request, other worker) pair, in
      * request-then-worker order, keeping the first largest decrease */
+    const int64_t max_moves = 4 * (int64_t)n_new + W;
     int32_t moves = 0;
+    int rc = ORA_OK;
+    rb_pair* absc = (rb_pair*)calloc((size_t)W, sizeof(rb_pair));  /* |c_y| at the current step */
+    if (!absc) { free(c); return ORA_ENOMEM; }
     for (;;) {
-        int64_t best = 0;
+        rb_pair best = {0, 0};
         int32_t bj = -1, by = -1;
+        for (int32_t y = 0; y < W; ++y) absc[y] = rb_abs(c[y], m);
         for (int32_t j = 0; j < n_new; ++j) {
             const int32_t x = new_worker[j];
-            if (moved[j] || x < 0) continue;
-            const int64_t d = (int64_t)new_lpred[j] + rho;
-            const int64_t cx = RB_C(x);
+            if (x < 0) continue;
+            const rb_pair d = {new_lpred[j], 1};
+            /* decrease of sum |c| = (|c_x| - |c_x - d|) + (|c_y| - |c_y + d|) */
+            const rb_pair from_x = rb_sub(absc[x], rb_abs(rb_sub(c[x], d), m));
             for (int32_t y = 0; y < W; ++y) {
                 if (y == x) continue;
-                const int64_t cy = RB_C(y);
-                const int64_t gain = (rb_abs(cx) + rb_abs(cy)) - (rb_abs(cx - d) + rb_abs(cy + d));
-                if (gain > best) { best = gain; bj = j; by = y; }
+                const rb_pair gain = rb_add(from_x, rb_sub(absc[y], rb_abs(rb_add(c[y], d), m)));
+                const rb_pair diff = rb_sub(gain, best);
+                if (!rb_fits(diff)) { rc = ORA_EOVERFLOW; goto done; }
+                if (rb_sign(diff.a, diff.b, m) > 0) { best = gain; bj = j; by = y; }
             }
         }
         if (bj < 0) break;
+        if (moves >= max_moves) { rc = ORA_EOVERFLOW; goto done; }
         const int32_t x = new_worker[bj];
-        le[x] -= new_lpred[bj]; be[x] -= 1;
-        le[by] += new_lpred[bj]; be[by] += 1;
+        const rb_pair d = {new_lpred[bj], 1};
+        c[x] = rb_sub(c[x], d);
+        c[by] = rb_add(c[by], d);
         new_worker[bj] = by;
-        moved[bj] = 1;
-        if (out_log) { out_log[2 * moves] = bj; out_log[2 * moves + 1] = by; }
+        if (out_log && moves < log_cap) { out_log[2 * moves] = bj; out_log[2 * moves + 1] = by; }
         moves += 1;
-        obj -= best;
+        obj = rb_sub(obj, best);
     }
-#undef RB_C
-    if (out_obj_after) *out_obj_after = obj;
+    if (out_obj_after) { out_obj_after[0] = obj.a; out_obj_after[1] = obj.b; }
     if (out_moves) *out_moves = moves;
-    if (out_le) memcpy(out_le, le, (size_t)W * sizeof(int64_t));
-    if (out_be) memcpy(out_be, be, (size_t)W * sizeof(int64_t));
-    free(le); free(be); free(moved);
-    return ORA_OK;
+    for (int32_t i = 0; i < W; ++i) {
+        if (out_le) out_le[i] = c[i].a;
+        if (out_be) out_be[i] = c[i].b;
+    }
+done:
+    free(c);
+    free(absc);
+    return rc;
 }

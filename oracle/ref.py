@@ -64,13 +64,18 @@ def lib():
         L.ora_place_moves.argtypes = [i32, P, P, P, P, P, P, ctypes.POINTER(OraModel), i32, P, P, P, i32, P, P, P,
                                       P, P, P, P, P, P, P, P, P, P, P, P, P]
         L.ora_place_moves.restype = ctypes.c_int
+        L.ora_place_grouped.argtypes = [i32, P, P, P, P, P, P, ctypes.POINTER(OraModel), i32, P, i32, P, P, i32,
+                                        P, P, P, P, P, P, P, P, P, P, P, P, P]
+        L.ora_place_grouped.restype = ctypes.c_int
+        L.ora_route_groups.argtypes = [i32, P, i32, P]
+        L.ora_route_groups.restype = ctypes.c_int
         L.ora_sweep.argtypes = [i32, P, P, i32, P, P, i32, P, P, P]
         L.ora_sweep.restype = ctypes.c_int
         L.ora_kv_peak.argtypes = [i64, P, P]
         L.ora_kv_peak.restype = i64
-        L.ora_rebalance_rho.argtypes = [ctypes.POINTER(OraModel)]
-        L.ora_rebalance_rho.restype = i64
-        L.ora_rebalance.argtypes = [i32, ctypes.POINTER(OraModel), i32, P, P, P, P, P, i32, P, P, P, P, P, P,
+        L.ora_rb_sign.argtypes = [i64, i64, ctypes.POINTER(OraModel)]
+        L.ora_rb_sign.restype = ctypes.c_int
+        L.ora_rebalance.argtypes = [i32, ctypes.POINTER(OraModel), i32, P, P, P, P, P, i32, P, P, P, P, P, i32, P,
                                     P, P]
         L.ora_rebalance.restype = ctypes.c_int
         _lib = L
@@ -188,6 +193,44 @@ def place_moves(W, kv_capacity, res_offsets, res_l_in, res_l_pred, res_generated
     return out
 
 
+def route_groups(sizes, Q) -> np.ndarray:
+    """App. A's router: the group of each of the first Q queries."""
+    g = np.ascontiguousarray(sizes, dtype=np.int32)
+    out = np.zeros(max(int(Q), 1), np.int32)
+    rc = lib().ora_route_groups(len(g), _ptr(g), int(Q), _ptr(out))
+    if rc != ORA_OK:
+        raise RuntimeError("oracle ora_route_groups failed with code %d" % rc)
+    return out[:int(Q)]
+
+
+def place_grouped(W, kv_capacity, res_offsets, res_l_in, res_l_pred, res_generated, model, group_sizes, q_l_in,
+                  q_l_pred, heartbeat_every=0, res_t_dec=None) -> PlaceResult:
+    """Grouped placement (App. A): each query goes to the group the router
+    picks and is placed among that group's workers; heartbeats every
+    heartbeat_every queries of the whole stream."""
+    L = lib()
+    Q = int(len(q_l_in))
+    c64 = lambda a: np.ascontiguousarray(a, dtype=np.int64)
+    c32 = lambda a: np.ascontiguousarray(a, dtype=np.int32)
+    M = c64(kv_capacity)
+    off = c64(res_offsets) if res_offsets is not None else None
+    rl, rp, rg = (c32(a) if a is not None else None for a in (res_l_in, res_l_pred, res_generated))
+    td = np.ascontiguousarray(res_t_dec, dtype=np.float64) if res_t_dec is not None else None
+    ql, qp, gs = c32(q_l_in), c32(q_l_pred), c32(group_sizes)
+    out = PlaceResult(*(np.zeros(Q, t) for t in (np.int32, np.int32, np.int32, np.int64, np.int64,
+                                                 np.float64, np.float64)),
+                      *(np.zeros(W, np.int64) for _ in range(6)))
+    m = to_model(model)
+    rc = L.ora_place_grouped(W, _ptr(M), _ptr(off), _ptr(rl), _ptr(rp), _ptr(rg), _ptr(td), ctypes.byref(m),
+                             len(gs), _ptr(gs), Q, _ptr(ql), _ptr(qp), int(heartbeat_every), _ptr(out.worker),
+                             _ptr(out.n_feasible), _ptr(out.near_tie), _ptr(out.kv_peak_chosen),
+                             _ptr(out.kv_excess_min), _ptr(out.ttft_chosen), _ptr(out.tdec_chosen), _ptr(out.B),
+                             _ptr(out.sum_c), _ptr(out.sum_r), _ptr(out.peak), _ptr(out.S1), _ptr(out.S2))
+    if rc != ORA_OK:
+        raise RuntimeError("oracle ora_place_grouped failed with code %d" % rc)
+    return out
+
+
 def place_trace(trace, q_slice=slice(None), **kw) -> PlaceResult:
     """Run the oracle on a workloads.Trace (optionally on a slice of its queries)."""
     return place(trace.n_workers, trace.kv_capacity, trace.res_offsets, trace.res_l_in,
@@ -244,13 +287,13 @@ class RebalanceResult:
     le: np.ndarray          # int64 [W] output-length error per worker after the moves
     be: np.ndarray          # int64 [W] batch-size error per worker after the moves
     moves: np.ndarray       # int32 [n_moves, 2] (request, target worker) in the order applied
-    obj_before: int         # sum over workers of |l^e + rho * b^e| before the moves
-    obj_after: int
-    rho: int
+    obj_before: tuple       # sum over workers of |l^e + rho * b^e| before the moves, as (a, b) = a + rho * b
+    obj_after: tuple
 
 
-def rebalance_rho(model) -> int:
-    return int(lib().ora_rebalance_rho(ctypes.byref(to_model(model))))
+def rb_sign(a: int, b: int, model) -> int:
+    """Exact sign of a + (c2 / k2) * b."""
+    return int(lib().ora_rb_sign(int(a), int(b), ctypes.byref(to_model(model))))
 
 
 def rebalance(W, model, old_worker, old_l_pred, old_l_out, old_l_real, old_l_repred, new_l_pred,
@@ -264,15 +307,17 @@ def rebalance(W, model, old_worker, old_l_pred, old_l_out, old_l_real, old_l_rep
     n_old, n_new = len(ow), len(nlp)
     le = np.zeros(W, np.int64)
     be = np.zeros(W, np.int64)
-    log = np.zeros(2 * max(n_new, 1), np.int32)
+    cap = 4 * n_new + int(W)  # the oracle's own bound on the number of moves
+    log = np.zeros(2 * max(cap, 1), np.int32)
     nm = ctypes.c_int32(0)
-    ob = ctypes.c_int64(0)
-    oa = ctypes.c_int64(0)
+    ob = np.zeros(2, np.int64)
+    oa = np.zeros(2, np.int64)
     m = to_model(model)
     rc = L.ora_rebalance(int(W), ctypes.byref(m), n_old, _ptr(ow), _ptr(op), _ptr(oo), _ptr(orl), _ptr(orp),
-                         n_new, _ptr(nlp), _ptr(nw), _ptr(le), _ptr(be), ctypes.byref(nm), _ptr(log),
-                         ctypes.byref(ob), ctypes.byref(oa))
+                         n_new, _ptr(nlp), _ptr(nw), _ptr(le), _ptr(be), ctypes.byref(nm), cap, _ptr(log),
+                         _ptr(ob), _ptr(oa))
     if rc != ORA_OK:
         raise RuntimeError("oracle ora_rebalance failed with code %d" % rc)
     k = nm.value
-    return RebalanceResult(nw, le, be, log[:2 * k].reshape(k, 2), ob.value, oa.value, rebalance_rho(model))
+    return RebalanceResult(nw, le, be, log[:2 * k].reshape(k, 2), (int(ob[0]), int(ob[1])),
+                           (int(oa[0]), int(oa[1])))

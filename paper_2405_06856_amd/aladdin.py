@@ -72,8 +72,8 @@ def _load():
         "ald_move_requests": ([P, i32, P, P, P, P], ctypes.c_int),
         "ald_sweep_scenarios": ([P, i32, P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_sweep_scenarios_hb": ([P, i32, P, P, i32, P, P, P, P, P], ctypes.c_int),
-        "ald_rebalance": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P], ctypes.c_int),
-        "ald_rebalance_noalloc": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P], ctypes.c_int),
+        "ald_rebalance": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, i32, P, P], ctypes.c_int),
+        "ald_rebalance_noalloc": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, i32, P, P], ctypes.c_int),
         "ald_worker_summary": ([P, P, P, P, P], ctypes.c_int),
         "ald_set_profiling": ([P, i32], ctypes.c_int),
         "ald_kernel_time": ([P, i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)], ctypes.c_int),
@@ -189,7 +189,7 @@ def ald_sweep_scenarios_hb(h, S: int, scen, heartbeat_every, Q: int, q_l_in, q_l
 
 def _rebalance_call(fn, h, P: int, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out, old_l_real,
                   old_l_repred, new_offsets, new_l_pred, new_worker, out_le=None, out_be=None, out_moves=None,
-                  out_log=None, out_obj=None) -> None:
+                  log_cap=0, out_log=None, out_obj=None) -> None:
     nw = np.ascontiguousarray(n_workers, dtype=np.int32)
     oo = np.ascontiguousarray(old_offsets, dtype=np.int64)
     no = np.ascontiguousarray(new_offsets, dtype=np.int64)
@@ -197,27 +197,28 @@ def _rebalance_call(fn, h, P: int, n_workers, models, old_offsets, old_worker, o
                                oo.ctypes.data_as(ctypes.c_void_p), _dptr(old_worker), _dptr(old_l_pred),
                                _dptr(old_l_out), _dptr(old_l_real), _dptr(old_l_repred),
                                no.ctypes.data_as(ctypes.c_void_p), _dptr(new_l_pred), _dptr(new_worker),
-                               _dptr(out_le), _dptr(out_be), _dptr(out_moves), _dptr(out_log), _dptr(out_obj)))
+                               _dptr(out_le), _dptr(out_be), _dptr(out_moves), int(log_cap), _dptr(out_log),
+                               _dptr(out_obj)))
 
 
 def ald_rebalance(h, P: int, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out, old_l_real,
                   old_l_repred, new_offsets, new_l_pred, new_worker, out_le=None, out_be=None, out_moves=None,
-                  out_log=None, out_obj=None) -> None:
+                  log_cap=0, out_log=None, out_obj=None) -> None:
     """n_workers (int32), models (Model array) and the offsets (int64) are host
     arrays; everything else is a device tensor."""
     _rebalance_call(_L.ald_rebalance, h, P, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out,
                     old_l_real, old_l_repred, new_offsets, new_l_pred, new_worker, out_le, out_be, out_moves,
-                    out_log, out_obj)
+                    log_cap, out_log, out_obj)
 
 
 def ald_rebalance_noalloc(h, P: int, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out,
                           old_l_real, old_l_repred, new_offsets, new_l_pred, new_worker, out_le, out_be,
-                          out_moves=None, out_log=None, out_obj=None) -> None:
+                          out_moves=None, log_cap=0, out_log=None, out_obj=None) -> None:
     """As ald_rebalance, with the library's fixed device array instead of
     allocated tables (out_le and out_be required)."""
     _rebalance_call(_L.ald_rebalance_noalloc, h, P, n_workers, models, old_offsets, old_worker, old_l_pred,
                     old_l_out, old_l_real, old_l_repred, new_offsets, new_l_pred, new_worker, out_le, out_be,
-                    out_moves, out_log, out_obj)
+                    out_moves, log_cap, out_log, out_obj)
 
 
 def ald_worker_summary(h, B, sum_c, sum_r, peak) -> None:
@@ -393,7 +394,8 @@ class Evaluator:
 
     def rebalance(self, batch, want_log=False):
         """Algorithm 2 on a workloads.RebalanceBatch; returns the new workers and
-        per-problem results as numpy arrays."""
+        per-problem results as numpy arrays (obj: [P, 4] pairs a + rho * b,
+        before then after; log: per problem, its moves as (request, target))."""
         t = self.torch
         P = batch.P
         models = (Model * P)(*[to_model(m) for m in batch.models])
@@ -403,15 +405,19 @@ class Evaluator:
         le = t.empty(Wt, dtype=t.int64, device=self.device)
         be = t.empty(Wt, dtype=t.int64, device=self.device)
         mv = t.empty(P, dtype=t.int32, device=self.device)
-        obj = t.empty(2 * P, dtype=t.int64, device=self.device)
-        log = t.empty(max(1, 2 * int(batch.new_offsets[-1])), dtype=t.int32, device=self.device) if want_log else None
+        obj = t.empty(4 * P, dtype=t.int64, device=self.device)
+        n_new = np.diff(batch.new_offsets)
+        cap = int(4 * n_new.max() + int(np.max(batch.n_workers))) if want_log and P > 0 else 0
+        log = t.empty(max(1, 2 * P * cap), dtype=t.int32, device=self.device) if want_log else None
         ald_rebalance(self.h, P, batch.n_workers, models, batch.old_offsets, d32(batch.old_worker),
                       d32(batch.old_l_pred), d32(batch.old_l_out), d32(batch.old_l_real), d32(batch.old_l_repred),
-                      batch.new_offsets, d32(batch.new_l_pred), nw, le, be, mv, log, obj)
+                      batch.new_offsets, d32(batch.new_l_pred), nw, le, be, mv, cap, log, obj)
         out = {"worker": nw.cpu().numpy(), "le": le.cpu().numpy(), "be": be.cpu().numpy(),
-               "moves": mv.cpu().numpy(), "obj": obj.cpu().numpy().reshape(P, 2)}
+               "moves": mv.cpu().numpy(), "obj": obj.cpu().numpy().reshape(P, 4)}
         if want_log:
-            out["log"] = log.cpu().numpy()
+            lg = log.cpu().numpy()
+            k = out["moves"]
+            out["log"] = [lg[2 * p * cap:2 * p * cap + 2 * int(k[p])].reshape(-1, 2) for p in range(P)]
         return out
 
     def profiling(self, enable=True, kinds=None):

@@ -869,12 +869,12 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
     }
     // per-query heartbeats: the tile ended at a query that heartbeats precede;
     // they run now, and the whole wave finds the next such query
-    const bool hb_here = st.hb_before != nullptr && pos == end && pos == c.hb_next && pos < c.Q;
+    const bool hb_here = sc.hb != nullptr && pos == end && pos == c.hb_next && pos < c.Q;
     int32_t hb_n = 0, hb_after = c.Q;
     if (hb_here) {
-        hb_n = st.hb_before[pos];
+        hb_n = sc.hb[pos];
         for (int32_t b = pos + 1; b < c.Q; b += NT) {
-            const uint64_t m = ballot(b + lane < c.Q && st.hb_before[b + lane] > 0);
+            const uint64_t m = ballot(b + lane < c.Q && sc.hb[b + lane] > 0);
             if (m) {
                 hb_after = b + __ffsll((unsigned long long)m) - 1;
                 break;

@@ -7,6 +7,7 @@
 #include "ald_move.h"
 
 #include <algorithm>
+#include <cfloat>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -34,6 +35,9 @@ struct Arena {
     bool use_d = false;   // some scenario checks constraint (d)
     Ctl* hctl = nullptr;  // pinned host copy of the control blocks
     int32_t hctl_n = 0;
+    // per scenario: the host copy of its per-query heartbeats during a call
+    // (empty: no scenario has any)
+    std::vector<const int32_t*> hb_host;
 
     ~Arena()
     {
@@ -72,9 +76,12 @@ struct ald_handle {
     bool check_all = false;        // stale workers are not listed (after grouped placement): check every one
     int64_t qcount = 0;            // queries processed since the load (routes grouped placement)
     Arena* grouped = nullptr;      // scenario view of the loaded workers for grouped placement
-    const int32_t* hb_host = nullptr;  // per-query heartbeats of the running call (host), or null
-    int32_t* hb_dev = nullptr;         // their device copy
-    size_t hb_dev_n = 0;
+    int32_t* hb_dev = nullptr;         // device copy of a call's per-query heartbeats (and grouped query maps)
+    size_t hb_dev_n = 0;               // int32 entries it holds
+    // App. A's router: the group sizes it routes for and the queries each group
+    // received since the load (or since the sizes changed)
+    std::vector<int32_t> route_sizes;
+    std::vector<int64_t> route_counts;
     void* mv_mem = nullptr;            // tables of ald_move_requests
     size_t mv_bytes = 0;
     int32_t* err_word = nullptr;
@@ -169,7 +176,6 @@ Scen make_scen(const ald_model_t& m)
     s.ttft = m.ttft_slo; s.tdec = m.decode_slo; s.theta = m.theta;
     s.gn = m.gamma_num; s.gs = m.gamma_log2den;
     s.mono = (m.k1 >= 0.0 && m.k1q >= 0.0) ? 1 : 0;
-    s.q_stride = 1;
     return s;
 }
 
@@ -419,11 +425,13 @@ int32_t next_hb(const int32_t* hb, int32_t from, int32_t Q)
 }
 
 // Rounds needed to finish every scenario from its control state, if no tile
-// is cut (hb: the call's per-query heartbeats, or null).
-int64_t rounds_needed(const std::vector<Ctl>& c, const int32_t* hb)
+// is cut (hbs[s]: scenario s's per-query heartbeats, or null; hbs may be empty).
+int64_t rounds_needed(const std::vector<Ctl>& c, const std::vector<const int32_t*>& hbs)
 {
     int64_t most = 0;
-    for (const Ctl& x : c) {
+    for (size_t s = 0; s < c.size(); ++s) {
+        const Ctl& x = c[s];
+        const int32_t* hb = s < hbs.size() ? hbs[s] : nullptr;
         if (x.err) continue;
         int64_t r = 0;
         int32_t pos = x.start, since = x.since_hb, nxt = x.hb_next;
@@ -462,7 +470,7 @@ int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, 
     HIPCHK(h, hipHostGetDevicePointer((void**)&a->st.ctl_host, a->hctl, 0));
     bool first = true;
     for (;;) {
-        int64_t need = rounds_needed(hc, h->hb_host);
+        int64_t need = rounds_needed(hc, a->hb_host);
         if (need < 0) return fail(h, ALD_EHIP, "internal error: a tile of no queries");
         if (need == 0) break;
         for (int64_t r = 0; r < need; ++r) {
@@ -661,6 +669,8 @@ int load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const int6
     h->tau = h->hb_index = h->since_hb = h->round = 0;
     h->rebuild_pending = h->dirty_pending = h->check_all = false;
     h->qcount = 0;
+    h->route_sizes.clear();
+    h->route_counts.clear();
     return ALD_OK;
 }
 }  // namespace
@@ -686,11 +696,24 @@ int ald_load_workers_history(ald_handle_t h, int32_t W, const ald_model_t* model
 
 namespace {
 
-// Clears the handle's per-query heartbeats when a call ends, however it ends.
+// Forgets the per-query heartbeats of a call when it ends, however it ends.
 struct HbScope {
-    ald_handle* h;
-    ~HbScope() { h->hb_host = nullptr; }
+    Arena* a;
+    ~HbScope() { a->hb_host.clear(); }
 };
+
+// Make room for n int32 entries of per-call device tables (heartbeats, query maps).
+int reserve_call_tables(ald_handle* h, size_t n)
+{
+    if (n <= h->hb_dev_n) return ALD_OK;
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    if (h->hb_dev) HIPCHK(h, hipFree(h->hb_dev));
+    h->hb_dev = nullptr;
+    h->hb_dev_n = 0;
+    HIPCHK(h, hipMalloc(&h->hb_dev, n * sizeof(int32_t)));
+    h->hb_dev_n = n;
+    return ALD_OK;
+}
 
 // One stream call: heartbeats every H processed queries, or hb_before[q]
 // (host array) decode iterations before query q.
@@ -732,26 +755,25 @@ int place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t
     const int64_t tau_final = (int64_t)tau + iters;
     if (tau_final >= ((int64_t)1 << 27) || (int64_t)h->max_cap * tau_final >= ((int64_t)1 << 27))
         return fail(h, ALD_EOVERFLOW, "too many heartbeats for the 32-bit request state");
-    HbScope hb_scope{h};
-    if (hb_before) {
-        if ((size_t)Q > h->hb_dev_n) {
-            HIPCHK(h, hipStreamSynchronize(h->stream));
-            if (h->hb_dev) HIPCHK(h, hipFree(h->hb_dev));
-            h->hb_dev = nullptr;
-            h->hb_dev_n = 0;
-            HIPCHK(h, hipMalloc(&h->hb_dev, (size_t)Q * sizeof(int32_t)));
-            h->hb_dev_n = Q;
-        }
-        HIPCHK(h, hipMemcpyAsync(h->hb_dev, hb_before, (size_t)Q * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
-        h->hb_host = hb_before;
-    }
     Arena* a = h->main;
+    HbScope hb_scope{a};
+    if (hb_before) {
+        int rc0 = reserve_call_tables(h, (size_t)Q);
+        if (rc0 != ALD_OK) return rc0;
+        HIPCHK(h, hipMemcpyAsync(h->hb_dev, hb_before, (size_t)Q * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
+        a->hb_host.assign(1, hb_before);
+    }
     int32_t T = std::min(h->tile, Q);
     if (H > 0) T = std::min(T, H);
     const int32_t wave = h->eval_wave[a->eval_mode][out_diag ? 1 : 0];
+    const int32_t* want_hb = hb_before ? h->hb_dev : nullptr;
     if (T != a->T || wave != a->target) {
-        rc = layout_scratch(h, a, T, wave);
+        a->hscen[0].hb = want_hb;
+        rc = layout_scratch(h, a, T, wave);  // also copies the scenario table
         if (rc != ALD_OK) return rc;
+    } else if (a->hscen[0].hb != want_hb) {
+        a->hscen[0].hb = want_hb;
+        HIPCHK(h, hipMemcpyAsync(a->dscen, a->hscen.data(), sizeof(Scen), hipMemcpyHostToDevice, h->stream));
     }
     Ctl c{};
     c.start = 0;
@@ -770,7 +792,6 @@ int place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t
     HIPCHK(h, launch_begin(c, ti, a->st.ctl, a->st.tinfo, a->st.qbad, h->stream));
     a->st.q_lin = q_l_in;
     a->st.q_lpred = q_l_pred;
-    a->st.hb_before = h->hb_host ? h->hb_dev : nullptr;
     a->st.out_worker = out_worker;
     a->st.out_diag = (Diag*)out_diag;
     std::vector<Ctl> hc(1, c);
@@ -885,13 +906,55 @@ int ald_place_stream_hb(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const 
 
 namespace {
 
-// Group g's queries among global positions [a, b) when query x goes to group x mod G.
-int64_t group_count(int64_t a, int64_t b, int32_t G, int32_t g)
+// App. A's router: the group of each of the next Q queries, continuing the
+// counts.  The quota method of Balinski and Young: the h-th query goes to the
+// group with the largest N_i / (a_i + 1) among the groups whose count a_i is
+// still below h * N_i / N_w (ties to the lowest index), which keeps every
+// count strictly within one query of its share h * N_i / N_w.  The candidates
+// come off a heap in order of N_i / (a_i + 1); groups at their quota are set
+// aside for the step.
+void route_groups(const std::vector<int32_t>& N, std::vector<int64_t>& counts, int32_t Q, std::vector<int32_t>& out)
 {
-    auto upto = [&](int64_t n) {  // x in [0, n) with x mod G == g (n >= 0)
-        return n <= g ? 0 : (n - 1 - g) / G + 1;
+    const int32_t G = (int32_t)N.size();
+    int64_t Nw = 0, h = 0;
+    for (int32_t i = 0; i < G; ++i) {
+        Nw += N[i];
+        h += counts[i];
+    }
+    // does i come before j: larger N / (a + 1), then the lower index
+    auto before = [&](int32_t i, int32_t j) {
+        const int64_t l = (int64_t)N[i] * (counts[j] + 1), r = (int64_t)N[j] * (counts[i] + 1);
+        return l != r ? l > r : i < j;
     };
-    return upto(b) - upto(a);
+    auto heap_less = [&](int32_t i, int32_t j) { return before(j, i); };  // max-heap on `before`
+    std::vector<int32_t> heap(G), aside;
+    for (int32_t i = 0; i < G; ++i) heap[i] = i;
+    std::make_heap(heap.begin(), heap.end(), heap_less);
+    out.resize(Q);
+    for (int32_t q = 0; q < Q; ++q) {
+        h += 1;
+        int32_t pick = -1;
+        while (!heap.empty()) {
+            std::pop_heap(heap.begin(), heap.end(), heap_less);
+            const int32_t i = heap.back();
+            heap.pop_back();
+            if (counts[i] * Nw < h * (int64_t)N[i]) {
+                pick = i;
+                break;
+            }
+            aside.push_back(i);
+        }
+        // some group is always below its quota: the counts add up to h - 1 < h
+        counts[pick] += 1;
+        out[q] = pick;
+        heap.push_back(pick);
+        std::push_heap(heap.begin(), heap.end(), heap_less);
+        for (int32_t i : aside) {
+            heap.push_back(i);
+            std::push_heap(heap.begin(), heap.end(), heap_less);
+        }
+        aside.clear();
+    }
 }
 
 // A scenario view of the loaded workers, one scenario per group: the worker
@@ -909,6 +972,8 @@ int grouped_view(ald_handle* h, int32_t G, const int32_t* sizes)
     for (int32_t g = 0; g < G; ++g) {
         a.hscen[g].W = sizes[g];
         a.hscen[g].wbase = wb;
+        a.hscen[g].qmap = nullptr;
+        a.hscen[g].hb = nullptr;
         wb += sizes[g];
     }
     a.eval_mode = m->eval_mode;
@@ -940,7 +1005,6 @@ int grouped_view(ald_handle* h, int32_t G, const int32_t* sizes)
     a.st.dlist = dlist;
     a.st.dcount = dcount;
     a.st.qbad = nullptr;  // the queries are checked up front
-    a.st.hb_before = nullptr;
     a.st.S = G;
     HIPCHK(h, hipMemsetAsync(dcount, 0, G * sizeof(int32_t), h->stream));
     a.T = 0;  // lay the scratch out again
@@ -967,7 +1031,6 @@ int ald_place_grouped(ald_handle_t h, int32_t G, const int32_t* group_workers, i
     if (wsum != h->W) return fail(h, ALD_EINVAL, "the group sizes must add up to the loaded worker count");
     const int32_t H = heartbeat_every;
     if (Q < 0 || H < 0) return fail(h, ALD_EINVAL, "Q and heartbeat_every must be >= 0");
-    if (H % G != 0) return fail(h, ALD_EINVAL, "heartbeat_every must be a multiple of G");
     if (Q == 0) return ALD_OK;
     if (!q_l_in || !q_l_pred || !out_worker) return fail(h, ALD_EINVAL, "null argument");
     int32_t tau = h->tau, hb = h->hb_index, since = h->since_hb;
@@ -978,52 +1041,78 @@ int ald_place_grouped(ald_handle_t h, int32_t G, const int32_t* group_workers, i
         since = 0;
         rebuild = true;
     }
-    // Each group keeps its own heartbeat clock within the call; they agree
-    // again (and with the stream's) at every heartbeat, so a call with
-    // heartbeats ends at one.
-    if (H > 0 && ((int64_t)since + Q) % H != 0)
-        return fail(h, ALD_EINVAL, "with heartbeats a grouped call must end at a heartbeat (the stream's position "
-                                   "in its heartbeat window plus Q a multiple of heartbeat_every)");
-    const int64_t tau_final = (int64_t)tau + (H > 0 ? (int64_t)Q / H + 2 : 0);
+    // the cluster's heartbeats: one after every H processed queries of the
+    // stream; hb_upto(k) of them come before the call's query k
+    auto hb_upto = [&](int64_t k) -> int64_t { return H > 0 ? ((int64_t)since + k) / H : 0; };
+    const int64_t fired = hb_upto(Q);
+    const int64_t tau_final = (int64_t)tau + fired + 2;
     if (tau_final >= ((int64_t)1 << 27) || (int64_t)h->max_cap * tau_final >= ((int64_t)1 << 27))
         return fail(h, ALD_EOVERFLOW, "too many heartbeats for the 32-bit request state");
+    // route: each query to a group (the router's counts continue across calls
+    // while the group sizes stay the same)
+    const std::vector<int32_t> sizes(group_workers, group_workers + G);
+    std::vector<int64_t> counts = h->route_sizes == sizes ? h->route_counts : std::vector<int64_t>(G, 0);
+    std::vector<int32_t> grp;
+    route_groups(sizes, counts, Q, grp);
+    // per group, in arrival order: its queries' positions in the call (qmap)
+    // and the cluster heartbeats that come before each of them since its
+    // previous query of the call (hbq)
+    std::vector<int32_t> off(G + 1, 0);
+    for (int32_t q = 0; q < Q; ++q) off[grp[q] + 1] += 1;
+    for (int32_t g = 0; g < G; ++g) off[g + 1] += off[g];
+    std::vector<int32_t> tab(2 * (size_t)Q);  // qmap, then hbq
+    int32_t* qmap = tab.data();
+    int32_t* hbq = tab.data() + Q;
+    {
+        std::vector<int32_t> fill(off.begin(), off.end() - 1);
+        std::vector<int64_t> last(G, 0);
+        for (int32_t q = 0; q < Q; ++q) {
+            const int32_t g = grp[q];
+            const int64_t u = hb_upto(q);
+            qmap[fill[g]] = q;
+            hbq[fill[g]] = (int32_t)(u - last[g]);
+            last[g] = u;
+            fill[g] += 1;
+        }
+    }
     HIPCHK(h, hipStreamSynchronize(h->stream));
     int rc = grouped_view(h, G, group_workers);
     if (rc != ALD_OK) return rc;
+    rc = reserve_call_tables(h, 2 * (size_t)Q);
+    if (rc != ALD_OK) return rc;
     Arena& a = *h->grouped;
-    // query x (counted since the load) goes to group x mod G; each window of H
-    // queries holds H / G of every group, so every group's heartbeat period is
-    // H / G of its own queries and its position in the window is counted here
-    const int64_t P0 = h->qcount, W0 = P0 - since;
-    const int32_t Hg = H / G;
+    HbScope hb_scope{&a};
+    HIPCHK(h, hipMemcpyAsync(h->hb_dev, tab.data(), 2 * (size_t)Q * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
     std::vector<Ctl> c(G);
     int32_t qmax = 1;
+    if (H > 0) a.hb_host.resize(G);
     for (int32_t g = 0; g < G; ++g) {
         Scen& sc = a.hscen[g];
-        const int32_t first = (int32_t)(((g - P0) % G + G) % G);  // first query of the call in group g
-        sc.q_first = first;
-        sc.q_stride = G;
+        const int32_t n = off[g + 1] - off[g];
+        sc.qmap = h->hb_dev + off[g];
+        sc.hb = H > 0 ? h->hb_dev + Q + off[g] : nullptr;
         sc.out_off = 0;
         sc.out_add = sc.wbase;
         Ctl& x = c[g];
         x = Ctl{};
-        x.Q = first < Q ? (Q - 1 - first) / G + 1 : 0;
-        x.H = Hg;
-        x.since_hb = (int32_t)group_count(W0, P0, G, g);
+        x.Q = n;
         x.tau = tau;
         x.hb_index = hb;
         x.rebuild = rebuild ? 1 : 0;
-        if (Hg > 0 && x.since_hb >= Hg) {  // this group finished its window: its heartbeat comes first
-            x.tau += 1;
-            x.hb_index += 1;
-            x.since_hb = 0;
-            x.rebuild = 1;
-        }
         x.first_rej = INT32_MAX;
-        qmax = std::max(qmax, x.Q);
+        if (H > 0 && n > 0) {
+            const int32_t* hg = hbq + off[g];
+            a.hb_host[g] = hg;
+            if (hg[0] > 0) {  // the heartbeats before the group's first query run first
+                x.tau += hg[0];
+                x.hb_index += hg[0];
+                x.rebuild = 1;
+            }
+            x.hb_next = next_hb(hg, 0, n);
+        }
+        qmax = std::max(qmax, n);
     }
-    int32_t T = std::min(h->tile, qmax);
-    if (Hg > 0) T = std::min(T, Hg);
+    const int32_t T = std::min(h->tile, qmax);
     for (Ctl& x : c) x.T = T;
     rc = layout_scratch(h, &a, T, h->eval_wave[a.eval_mode][out_diag ? 1 : 0]);  // also copies the scenario table
     if (rc != ALD_OK) return rc;
@@ -1039,15 +1128,14 @@ int ald_place_grouped(ald_handle_t h, int32_t G, const int32_t* group_workers, i
     HIPCHK(h, launch_query_stats(q_l_in, q_l_pred, Q, a.st.ctl, G, h->stream));
     rc = run_rounds(h, &a, H > 0, 0, c);
     if (rc != ALD_OK) return rc;
-    // the call's state as one stream: heartbeats after every H queries
-    const int64_t total = (int64_t)since + Q;
-    const int64_t fired = H > 0 ? total / H : 0;
+    // the stream's clock after the call; heartbeats after a group's last query
+    // reach its workers through the rebuild at the start of the next call
     h->tau = tau + (int32_t)fired;
     h->hb_index = hb + (int32_t)fired;
-    h->since_hb = (int32_t)(total - fired * H);
+    h->since_hb = H > 0 ? (int32_t)(((int64_t)since + Q) % H) : since + Q;
     h->qcount += Q;
-    // a call with heartbeats ended at one (workers not yet rebuilt), and the
-    // groups' lists of changed workers are not the loaded arena's
+    h->route_sizes = sizes;
+    h->route_counts = counts;
     h->rebuild_pending = rebuild || fired > 0;
     h->dirty_pending = false;
     h->check_all = true;
@@ -1058,6 +1146,25 @@ int ald_place_grouped(ald_handle_t h, int32_t G, const int32_t* group_workers, i
 
 namespace {
 
+// rho = c2 / k2 split into exact integer significands and exponents.
+RbRho rb_rho(double k2, double c2)
+{
+    RbRho r{};
+    r.k2 = k2;
+    r.c2 = c2;
+    int ek = 0, ec = 0;
+    const double fk = std::frexp(k2, &ek);
+    r.mk = (uint64_t)std::ldexp(fk, 53);
+    ek -= 53;
+    if (c2 != 0.0) {
+        const double fc = std::frexp(c2, &ec);
+        r.mc = (uint64_t)std::ldexp(fc, 53);
+        ec -= 53;
+    }
+    r.sh = ek - ec;
+    return r;
+}
+
 // Algorithm 2 over P problems.  noalloc: the tables live in the library's
 // fixed device array (rb_static_ptr) and the caller passes the error arrays,
 // so nothing is allocated; otherwise they live in memory the handle keeps.
@@ -1065,7 +1172,8 @@ int rebalance_impl(ald_handle_t h, int32_t P, const int32_t* n_workers, const al
                   const int64_t* old_offsets, const int32_t* old_worker, const int32_t* old_l_pred,
                   const int32_t* old_l_out, const int32_t* old_l_real, const int32_t* old_l_repred,
                   const int64_t* new_offsets, const int32_t* new_l_pred, int32_t* new_worker,
-                  int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t* out_log, int64_t* out_obj,
+                  int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t log_cap, int32_t* out_log,
+                  int64_t* out_obj,
                    bool noalloc)
 {
     if (!h) return ALD_EINVAL;
@@ -1084,15 +1192,19 @@ int rebalance_impl(ald_handle_t h, int32_t P, const int32_t* n_workers, const al
         if (o1 < o0 || n1 < n0) return fail(h, ALD_EINVAL, tag + "offsets must not decrease");
         if (n1 - n0 > RB_JMAX) return fail(h, ALD_EINVAL, tag + "more than " + std::to_string(RB_JMAX) + " new requests");
         const ald_model_t& m = models[p];
-        const double q = m.c2 / m.k2;
-        if (!(m.k2 > 0.0) || !(m.c2 >= 0.0) || !std::isfinite(q) || q > 1e9)
-            return fail(h, ALD_EINVAL, tag + "needs k2 > 0 and 0 <= c2 / k2 <= 1e9");
-        prob[p] = RbProblem{o0, o1, n0, wtot, (int64_t)std::llrint(q), n_workers[p], (int32_t)(n1 - n0)};
+        const double big = std::ldexp(1.0, 900);
+        const bool k2_ok = std::isfinite(m.k2) && m.k2 >= DBL_MIN && m.k2 <= big;
+        const bool c2_ok = std::isfinite(m.c2) && (m.c2 == 0.0 || (m.c2 >= DBL_MIN && m.c2 <= big));
+        if (!k2_ok || !c2_ok || !(m.c2 <= 1e9 * m.k2))
+            return fail(h, ALD_EINVAL, tag + "needs normal k2 > 0 and c2 >= 0 (at most 2^900) with c2 / k2 <= 1e9");
+        prob[p] = RbProblem{o0, o1, n0, wtot, rb_rho(m.k2, m.c2), n_workers[p], (int32_t)(n1 - n0)};
         for (int64_t b = o0; b < o1; b += RB_CHUNK) chunks.push_back(RbChunk{b, std::min(o1, b + RB_CHUNK), p, 0});
         wtot += n_workers[p];
     }
     const int64_t n_old = old_offsets[P], n_new = new_offsets[P];
-    if (n_old >= ((int64_t)1 << 31) || n_new >= ((int64_t)1 << 31)) return fail(h, ALD_EINVAL, "too many requests");
+    if (n_old >= ((int64_t)1 << 30) || n_new >= ((int64_t)1 << 30)) return fail(h, ALD_EINVAL, "too many requests");
+    if (log_cap < 0 || (out_log != nullptr && (int64_t)P * log_cap > ((int64_t)1 << 30)))
+        return fail(h, ALD_EINVAL, "log_cap must be >= 0 with P * log_cap <= 2^30");
     if ((n_old > 0 && (!old_worker || !old_l_pred || !old_l_out || !old_l_real || !old_l_repred)) ||
         (n_new > 0 && (!new_l_pred || !new_worker)))
         return fail(h, ALD_EINVAL, "null request array");
@@ -1143,6 +1255,7 @@ int rebalance_impl(ald_handle_t h, int32_t P, const int32_t* n_workers, const al
     a.be = own_err ? (int64_t*)(base + b_prob + b_chunk + b_err) : out_be;
     a.moves = out_moves;
     a.log = out_log;
+    a.log_cap = log_cap;
     a.obj = out_obj;
     a.err = err_word;
     HIPCHK(h, hipMemcpyAsync(base, prob.data(), P * sizeof(RbProblem), hipMemcpyHostToDevice, h->stream));
@@ -1157,6 +1270,8 @@ int rebalance_impl(ald_handle_t h, int32_t P, const int32_t* n_workers, const al
     HIPCHK(h, hipMemcpyAsync(&dev_err, err_word, sizeof(int32_t), hipMemcpyDeviceToHost, h->stream));
     HIPCHK(h, hipStreamSynchronize(h->stream));
     prof_collect(h);
+    if (dev_err == DEV_EOVERFLOW)
+        return fail(h, ALD_EOVERFLOW, "a problem's moves did not settle within 4 * (new requests) + (workers) steps");
     if (dev_err != 0) return fail(h, ALD_EINVAL, "invalid request (worker index out of range, length outside "
                                                  "[1, 2^24], or more tokens generated than the real length)");
     return ALD_OK;
@@ -1277,22 +1392,24 @@ int ald_rebalance(ald_handle_t h, int32_t P, const int32_t* n_workers, const ald
                   const int64_t* old_offsets, const int32_t* old_worker, const int32_t* old_l_pred,
                   const int32_t* old_l_out, const int32_t* old_l_real, const int32_t* old_l_repred,
                   const int64_t* new_offsets, const int32_t* new_l_pred, int32_t* new_worker,
-                  int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t* out_log, int64_t* out_obj)
+                  int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t log_cap, int32_t* out_log,
+                  int64_t* out_obj)
 {
     return rebalance_impl(h, P, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out, old_l_real,
-                          old_l_repred, new_offsets, new_l_pred, new_worker, out_le, out_be, out_moves, out_log,
-                          out_obj, false);
+                          old_l_repred, new_offsets, new_l_pred, new_worker, out_le, out_be, out_moves, log_cap,
+                          out_log, out_obj, false);
 }
 
 int ald_rebalance_noalloc(ald_handle_t h, int32_t P, const int32_t* n_workers, const ald_model_t* models,
                           const int64_t* old_offsets, const int32_t* old_worker, const int32_t* old_l_pred,
                           const int32_t* old_l_out, const int32_t* old_l_real, const int32_t* old_l_repred,
                           const int64_t* new_offsets, const int32_t* new_l_pred, int32_t* new_worker,
-                          int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t* out_log, int64_t* out_obj)
+                          int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t log_cap, int32_t* out_log,
+                  int64_t* out_obj)
 {
     return rebalance_impl(h, P, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out, old_l_real,
-                          old_l_repred, new_offsets, new_l_pred, new_worker, out_le, out_be, out_moves, out_log,
-                          out_obj, true);
+                          old_l_repred, new_offsets, new_l_pred, new_worker, out_le, out_be, out_moves, log_cap,
+                          out_log, out_obj, true);
 }
 
 int ald_worker_summary(ald_handle_t h, int32_t* B, int64_t* sum_c, int64_t* sum_r, int64_t* peak)

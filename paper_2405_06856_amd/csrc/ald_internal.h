@@ -74,15 +74,19 @@ struct Scen {
     int64_t pstride;    // queries per tile rounded up to whole evaluation chunks
     int64_t qsum_off;   // QSum entries into qsum
     int64_t out_off;    // offset into out_worker
-    // The scenario's query i is entry q_first + i * q_stride of the call's
-    // query arrays (and of out_worker after out_off, and of out_diag); grouped
-    // placement routes every G-th query to a group.  out_add is added to the
-    // worker index written (a group's first worker; 0 elsewhere).
-    int32_t q_first, q_stride;
+    // The scenario's query i is entry qmap[i] of the call's query arrays (and
+    // of out_worker after out_off, and of out_diag), or entry i when qmap is
+    // null; grouped placement lists each group's queries this way.  out_add
+    // is added to the worker index written (a group's first worker; 0
+    // elsewhere).  hb[i] (null: none) = decode iterations (heartbeats) that run
+    // before the scenario's query i; the control block's hb_next points at
+    // the next i > start with hb[i] > 0.
+    const int32_t* qmap;
+    const int32_t* hb;
     int32_t out_add, pad;
 };
 
-__host__ __device__ inline int64_t q_at(const Scen& sc, int32_t i) { return sc.q_first + (int64_t)i * sc.q_stride; }
+__host__ __device__ inline int64_t q_at(const Scen& sc, int32_t i) { return sc.qmap ? (int64_t)sc.qmap[i] : (int64_t)i; }
 
 // Per-scenario control block.  Written by the commit kernel's sequential block
 // only; every other kernel only reads it (kernel boundaries order the accesses).
@@ -213,7 +217,6 @@ struct State {
     // queries and outputs
     const int32_t* q_lin;
     const int32_t* q_lpred;
-    const int32_t* hb_before;  // per query of the call: heartbeats before it (null: by period)
     int32_t* out_worker;
     Diag* out_diag;    // only with S == 1
     int32_t* err_word; // load-time validation

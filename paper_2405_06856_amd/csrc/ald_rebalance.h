@@ -13,11 +13,20 @@ constexpr int RB_ETHREADS = 256;  // threads per error-accumulation block
 constexpr int RB_CHUNK = 2048;    // ongoing requests per error-accumulation block
 constexpr int32_t RB_LEN_MAX = 1 << 24;
 
+// rho = c2 / k2 of one problem, held so that the sign of a + rho * b (integer
+// a, b) is exact: k2 = mk * 2^ek and c2 = mc * 2^ec with 53-bit integer
+// significands (mc = 0 when c2 = 0), sh = ek - ec.
+struct RbRho {
+    double k2, c2;
+    uint64_t mk, mc;
+    int32_t sh, pad;
+};
+
 struct RbProblem {
     int64_t old0, old1;  // its ongoing requests [old0, old1)
     int64_t new0;        // its first new request
     int64_t wbase;       // its first worker in the error arrays
-    int64_t rho;         // c2 / k2 in whole tokens
+    RbRho rho;
     int32_t W, n_new;
 };
 struct RbChunk {
@@ -38,8 +47,9 @@ struct RbArgs {
     int64_t* le;          // per worker, zero before the launch; final errors after
     int64_t* be;
     int32_t* moves;       // per problem (nullable)
-    int32_t* log;         // (request, target) pairs at 2 * new0 (nullable)
-    int64_t* obj;         // per problem: sum |c| before and after (nullable)
+    int32_t* log;         // problem p's first log_cap (request, target) pairs at 2 * p * log_cap (nullable)
+    int32_t log_cap;
+    int64_t* obj;         // per problem: sum |c| before and after as pairs (a, b) = a + rho * b (nullable)
     int32_t* err;
 };
 // error accumulation (nchunk + P blocks), then the greedy moves (P blocks)

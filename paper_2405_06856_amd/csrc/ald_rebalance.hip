@@ -7,12 +7,14 @@
 //              worker across each wave's lanes and added to the problem's error
 //              arrays; extra blocks validate each problem's new requests.
 // k_rb_moves   one block per problem: c_i = l^e_i + rho * b^e_i (the error
-//              line of Eq. 4 divided by k2, rho = c2 / k2 in whole tokens) in
-//              LDS, then greedy moves: of every (unmoved placed request j,
-//              other worker y) pair, the one that lowers sum |c| most (ties to
-//              the lowest j, then y) while that decrease is positive -- found
-//              per step from the smallest c and one gain per request.  All
-//              int64: the choices are exact.
+//              line of Eq. 4 divided by k2, rho = c2 / k2 the real ratio) held
+//              as the integer pair (l^e_i, b^e_i) in LDS, then greedy moves: of
+//              every (placed request j, other worker y) pair, the one that
+//              lowers sum |c| most (ties to the lowest j, then y) while that
+//              decrease is positive -- found per step from the smallest c and
+//              one gain per request.  Every comparison is the sign of
+//              a + rho * b for integer a, b, taken exactly (rb_sign), so the
+//              choices are exact.
 #include "ald_device.h"
 #include "ald_rebalance.h"
 
@@ -52,8 +54,6 @@ void* rb_static_ptr(int device)
     std::lock_guard<std::mutex> lk(g_static_mu);
     return g_static_ptr[device];
 }
-
-__device__ __forceinline__ int64_t abs64(int64_t v) { return v < 0 ? -v : v; }
 
 __global__ __launch_bounds__(RB_ETHREADS) void k_rb_errors(RbArgs a)
 {
@@ -111,56 +111,141 @@ __global__ __launch_bounds__(RB_ETHREADS) void k_rb_errors(RbArgs a)
     if (bad) raise_error(a.err, DEV_EINVAL);
 }
 
-// Better candidate: larger gain, then the lower (request, worker) order.
-__device__ __forceinline__ bool rb_better(int64_t g, int32_t o, int64_t bg, int32_t bo)
+// ---------------------------------------------------------------------------------------------
+// Exact sign of a + rho * b, i.e. of a * k2 + b * c2 (k2 > 0), for |a|, |b| < 2^62.
+// Equal signs decide at once.  Otherwise fp64 decides when the computed sum
+// is far from zero: each product carries a relative error of at most 2u
+// (u = 2^-53: the conversion of the integer and the product) and the sum one
+// more u, so |v - exact| < 4u (|x| + |y|), and |v| > 2^-50 (|x| + |y|) (computed)
+// leaves the sign of v exact (no underflow: |x| >= k2 >= 2^-1022 and the
+// coefficients are at most 2^900, checked on the host).  Else |a| k2 is
+// compared with |b| c2 in 128-bit integers: |a| mk 2^sh against |b| mc (or the
+// shift on the other side), first by bit length, and when the lengths agree
+// the shifted product has at most 115 bits.
+struct RbPair {
+    int64_t a, b;  // a + rho * b
+};
+__device__ __forceinline__ RbPair rp_add(RbPair u, RbPair v) { return RbPair{u.a + v.a, u.b + v.b}; }
+__device__ __forceinline__ RbPair rp_sub(RbPair u, RbPair v) { return RbPair{u.a - v.a, u.b - v.b}; }
+
+__device__ __forceinline__ int bitlen128(unsigned __int128 v)
 {
-    return g > bg || (g == bg && o < bo);
+    const uint64_t hi = (uint64_t)(v >> 64), lo = (uint64_t)v;
+    return hi ? 128 - __builtin_clzll(hi) : (lo ? 64 - __builtin_clzll(lo) : 0);
+}
+
+__device__ __noinline__ int rb_sign_exact(int64_t a, int64_t b, const RbRho& r)
+{
+    const int sa = a > 0 ? 1 : -1, sb = b > 0 ? 1 : -1;
+    const unsigned __int128 p1 = (unsigned __int128)(uint64_t)(a > 0 ? a : -a) * r.mk;
+    const unsigned __int128 p2 = (unsigned __int128)(uint64_t)(b > 0 ? b : -b) * r.mc;
+    const int s1 = r.sh > 0 ? r.sh : 0, s2 = r.sh < 0 ? -r.sh : 0;
+    const int l1 = bitlen128(p1) + s1, l2 = bitlen128(p2) + s2;
+    int cmp;
+    if (l1 != l2) {
+        cmp = l1 > l2 ? 1 : -1;
+    } else {
+        const unsigned __int128 q1 = p1 << s1, q2 = p2 << s2;
+        cmp = (q1 > q2) - (q1 < q2);
+    }
+    return cmp > 0 ? sa : (cmp < 0 ? sb : 0);
+}
+
+__device__ __forceinline__ int rb_sign(int64_t a, int64_t b, const RbRho& r)
+{
+    const int sa = (a > 0) - (a < 0), sb = (b > 0) - (b < 0);
+    if (sb == 0 || r.mc == 0) return sa;
+    if (sa == 0 || sa == sb) return sb;
+    const double x = (double)a * r.k2, y = (double)b * r.c2;
+    const double v = x + y, t = fabs(x) + fabs(y);
+    if (fabs(v) > 0x1p-50 * t) return v > 0.0 ? 1 : -1;
+    return rb_sign_exact(a, b, r);
+}
+__device__ __forceinline__ int rp_sign(RbPair u, const RbRho& r) { return rb_sign(u.a, u.b, r); }
+__device__ __forceinline__ RbPair rp_abs(RbPair u, const RbRho& r)
+{
+    return rp_sign(u, r) < 0 ? RbPair{-u.a, -u.b} : u;
+}
+
+// Better candidate: larger gain, then the lower request index (a request's
+// best target is unique, so the index order is the (request, worker) order).
+__device__ __forceinline__ bool rb_better(RbPair g, int32_t o, RbPair bg, int32_t bo, const RbRho& r)
+{
+    if (o == INT32_MAX) return false;
+    if (bo == INT32_MAX) return true;
+    const int s = rp_sign(rp_sub(g, bg), r);
+    return s > 0 || (s == 0 && o < bo);
+}
+
+// Smaller c, then the lower worker index (INT32_MAX: none).
+__device__ __forceinline__ bool rb_lower(RbPair c, int32_t y, RbPair bc, int32_t by, const RbRho& r)
+{
+    if (y == INT32_MAX) return false;
+    if (by == INT32_MAX) return true;
+    const int s = rp_sign(rp_sub(c, bc), r);
+    return s < 0 || (s == 0 && y < by);
+}
+
+__device__ __forceinline__ RbPair shfl_pair(RbPair v, int off)
+{
+    return RbPair{__shfl_xor(v.a, off, 64), __shfl_xor(v.b, off, 64)};
+}
+
+// sum |c| over the problem's workers (block-wide; every thread gets it)
+__device__ RbPair rb_objective(const int64_t* cle, const int32_t* cbe, int W, const RbRho& rho, int64_t* red)
+{
+    RbPair s{0, 0};
+    for (int y = threadIdx.x; y < W; y += RB_THREADS) s = rp_add(s, rp_abs(RbPair{cle[y], cbe[y]}, rho));
+    const int64_t oa = block_reduce<RB_THREADS>(s.a, 0, OpAdd(), red);
+    const int64_t ob = block_reduce<RB_THREADS>(s.b, 0, OpAdd(), red);
+    return RbPair{oa, ob};
 }
 
 __global__ __launch_bounds__(RB_THREADS) void k_rb_moves(RbArgs a)
 {
     constexpr int NWAVE = RB_THREADS / 64;
     constexpr int JPT = RB_JMAX / RB_THREADS;  // new requests per thread
-    __shared__ int64_t c[RB_WMAX];
-    __shared__ int64_t negc[RB_WMAX];  // c of the workers listed in neg
+    __shared__ int64_t cle[RB_WMAX];   // c_y = (cle[y], cbe[y])
+    __shared__ int32_t cbe[RB_WMAX];
     __shared__ int32_t jl[RB_JMAX];    // predicted length of new request j
-    // worker of new request j: >= 0 movable, -1 unplaced, -2 - x moved away from x
-    __shared__ int16_t jx[RB_JMAX];
-    __shared__ int16_t jy[RB_JMAX];    // where a moved request went
+    __shared__ int16_t jx[RB_JMAX];    // current worker of new request j (-1: unplaced)
     __shared__ int16_t neg[RB_WMAX];   // the workers with c < 0, in no particular order
     __shared__ int16_t pos[RB_WMAX];   // index of a worker in neg (-1: not there)
-    __shared__ int64_t wg[NWAVE];
+    __shared__ uint8_t cpos[RB_WMAX];  // c_y > 0
+    __shared__ int64_t wga[NWAVE], wgb[NWAVE];
     __shared__ int32_t wo[NWAVE];
     __shared__ int64_t red[NWAVE];
     __shared__ int32_t s_nneg;
     if (*a.err != 0) return;  // invalid input somewhere: nothing changes
     const int p = blockIdx.x;
     const RbProblem pr = a.prob[p];
+    const RbRho rho = pr.rho;
     const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
     const int W = pr.W, n = pr.n_new;
-    const int64_t rho = pr.rho;
+    const int64_t max_moves = 4 * (int64_t)n + W;  // a guard; every move lowers sum |c| strictly
 
     if (tid == 0) s_nneg = 0;
     __syncthreads();
-    int64_t sabs = 0;
     for (int y = tid; y < W; y += RB_THREADS) {
-        const int64_t v = a.le[pr.wbase + y] + rho * a.be[pr.wbase + y];
-        c[y] = v;
-        sabs += abs64(v);
+        const int64_t le = a.le[pr.wbase + y];
+        const int32_t be = (int32_t)a.be[pr.wbase + y];
+        cle[y] = le;
+        cbe[y] = be;
+        const int sg = rb_sign(le, be, rho);
         int32_t at = -1;
-        if (v < 0) {
+        if (sg < 0) {
             at = atomicAdd(&s_nneg, 1);
             neg[at] = (int16_t)y;
-            negc[at] = v;
         }
         pos[y] = (int16_t)at;
+        cpos[y] = sg > 0 ? 1 : 0;
     }
     for (int j = tid; j < n; j += RB_THREADS) {
         jx[j] = (int16_t)a.new_worker[pr.new0 + j];
         jl[j] = a.new_lpred[pr.new0 + j];
     }
-    const int64_t obj0 = block_reduce<RB_THREADS>(sabs, 0, OpAdd(), red);  // ends with a barrier
-    int64_t obj = obj0;
+    __syncthreads();
+    const RbPair obj0 = rb_objective(cle, cbe, W, rho, red);  // ends with a barrier
 
     // A move of j from x to y lowers sum |c| by A + G with A = |c_x| - |c_x - d|
     // and G = |c_y| - |c_y + d| (d = l_pred_j + rho > 0).  G = -d when c_y >= 0
@@ -176,83 +261,87 @@ __global__ __launch_bounds__(RB_THREADS) void k_rb_moves(RbArgs a)
     int32_t moves = 0;
     for (;;) {
         const int nneg = s_nneg;
-        if (nneg == 0) break;  // no move gains (uniform)
+        if (nneg == 0) break;  // no move gains
         // c_min and the lowest worker index at it, in every wave
-        int64_t cm = INT64_MAX;
+        RbPair cm{0, 0};
         int32_t ci = INT32_MAX;
         for (int k = lane; k < nneg; k += 64) {
-            const int64_t v = negc[k];
             const int32_t y = neg[k];
-            if (v < cm || (v == cm && y < ci)) {
+            const RbPair v{cle[y], cbe[y]};
+            if (rb_lower(v, y, cm, ci, rho)) {
                 cm = v;
                 ci = y;
             }
         }
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) {
-            const int64_t ov = __shfl_xor(cm, off, 64);
+            const RbPair ov = shfl_pair(cm, off);
             const int32_t oy = __shfl_xor(ci, off, 64);
-            if (ov < cm || (ov == cm && oy < ci)) {
+            if (rb_lower(ov, oy, cm, ci, rho)) {
                 cm = ov;
                 ci = oy;
             }
         }
         // each thread's requests, in increasing j: the first largest gain
-        int64_t bg = 0;
+        RbPair bg{0, 0};
         int32_t bj = INT32_MAX;
 #pragma unroll
         for (int u = 0; u < JPT; ++u) {
             const int j = tid + u * RB_THREADS;
             if (j >= n) break;
             const int x = jx[j];
-            if (x < 0) continue;
-            const int64_t cx = c[x];
-            if (cx <= 0) continue;
-            const int64_t d = (int64_t)jl[j] + rho;
-            const int64_t g = (abs64(cx) - abs64(cx - d)) + (abs64(cm) - abs64(cm + d));
-            if (g > bg) {
+            if (x < 0 || !cpos[x]) continue;
+            const RbPair cx{cle[x], cbe[x]};
+            const RbPair d{(int64_t)jl[j], 1};
+            // (|c_x| - |c_x - d|) + (|c_min| - |c_min + d|), c_x > 0 > c_min
+            const RbPair g = rp_add(rp_sub(cx, rp_abs(rp_sub(cx, d), rho)),
+                                    rp_sub(RbPair{-cm.a, -cm.b}, rp_abs(rp_add(cm, d), rho)));
+            if (rp_sign(rp_sub(g, bg), rho) > 0) {  // strictly: only positive gains, earlier j on ties
                 bg = g;
                 bj = j;
             }
         }
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) {
-            const int64_t og = __shfl_xor(bg, off, 64);
+            const RbPair og = shfl_pair(bg, off);
             const int32_t oj = __shfl_xor(bj, off, 64);
-            if (rb_better(og, oj, bg, bj)) {
+            if (rb_better(og, oj, bg, bj, rho)) {
                 bg = og;
                 bj = oj;
             }
         }
         if (lane == 0) {
-            wg[wv] = bg;
+            wga[wv] = bg.a;
+            wgb[wv] = bg.b;
             wo[wv] = bj;
         }
         __syncthreads();
         // every wave finds the block's best from the per-wave ones
-        int64_t g = lane < NWAVE ? wg[lane] : 0;
+        RbPair g = lane < NWAVE ? RbPair{wga[lane], wgb[lane]} : RbPair{0, 0};
         int32_t jb = lane < NWAVE ? wo[lane] : INT32_MAX;
 #pragma unroll
         for (int off = NWAVE / 2; off > 0; off >>= 1) {
-            const int64_t og = __shfl_xor(g, off, 64);
+            const RbPair og = shfl_pair(g, off);
             const int32_t oj = __shfl_xor(jb, off, 64);
-            if (rb_better(og, oj, g, jb)) {
+            if (rb_better(og, oj, g, jb, rho)) {
                 g = og;
                 jb = oj;
             }
         }
-        g = rdlane64s(g, 0);
         jb = rdlane(jb, 0);
-        if (g <= 0) break;  // uniform
+        if (jb == INT32_MAX) break;  // no move lowers the objective
+        if (moves >= max_moves) {
+            if (tid == 0) raise_error(a.err, DEV_EOVERFLOW);
+            break;
+        }
         if (wv == 0) {
-            const int64_t l = jl[jb];
-            const int64_t T = -(l + rho);
+            const RbPair d{(int64_t)jl[jb], 1};
             int32_t y = ci;
-            if (cm <= T) {  // the lowest-index receiver at or below -d
+            if (rp_sign(rp_add(cm, d), rho) <= 0) {  // the lowest-index receiver at or below -d
                 int32_t lo = INT32_MAX;
                 for (int k = lane; k < nneg; k += 64) {
                     const int32_t w = neg[k];
-                    if (negc[k] <= T && w < lo) lo = w;
+                    if (w < lo && rp_sign(rp_add(RbPair{cle[w], cbe[w]}, d), rho) <= 0) lo = w;
                 }
 #pragma unroll
                 for (int off = 32; off > 0; off >>= 1) {
@@ -263,55 +352,51 @@ __global__ __launch_bounds__(RB_THREADS) void k_rb_moves(RbArgs a)
             }
             if (lane == 0) {
                 const int x = jx[jb];
-                const int64_t cx = c[x] - (l + rho), cy = c[y] + (l + rho);
-                c[x] = cx;
-                c[y] = cy;
-                if (cx < 0) {  // x (c_x was > 0) joins the receivers
+                const RbPair cx = rp_sub(RbPair{cle[x], cbe[x]}, d);
+                const RbPair cy = rp_add(RbPair{cle[y], cbe[y]}, d);
+                cle[x] = cx.a;
+                cbe[x] = (int32_t)cx.b;
+                cle[y] = cy.a;
+                cbe[y] = (int32_t)cy.b;
+                const int sx = rp_sign(cx, rho), sy = rp_sign(cy, rho);
+                cpos[x] = sx > 0 ? 1 : 0;
+                cpos[y] = sy > 0 ? 1 : 0;
+                if (sx < 0) {  // x (c_x was > 0) joins the receivers
                     pos[x] = (int16_t)s_nneg;
                     neg[s_nneg] = (int16_t)x;
-                    negc[s_nneg] = cx;
                     s_nneg += 1;
                 }
-                const int at = pos[y];  // y (c_y was < 0) is listed
-                if (cy < 0) {
-                    negc[at] = cy;
-                } else {  // y leaves: the last entry takes its place
-                    const int last = s_nneg - 1, wl = neg[last];
+                if (sy >= 0) {  // y (c_y was < 0, listed) leaves: the last entry takes its place
+                    const int at = pos[y], last = s_nneg - 1, wl = neg[last];
                     neg[at] = (int16_t)wl;
-                    negc[at] = negc[last];
                     pos[wl] = (int16_t)at;
                     pos[y] = -1;
                     s_nneg = last;
                 }
-                jx[jb] = (int16_t)(-2 - x);
-                jy[jb] = (int16_t)y;
-                a.new_worker[pr.new0 + jb] = y;
-                if (a.log != nullptr) {
-                    a.log[2 * (pr.new0 + moves)] = jb;
-                    a.log[2 * (pr.new0 + moves) + 1] = y;
+                jx[jb] = (int16_t)y;
+                if (a.log != nullptr && moves < a.log_cap) {
+                    a.log[2 * ((int64_t)p * a.log_cap + moves)] = jb;
+                    a.log[2 * ((int64_t)p * a.log_cap + moves) + 1] = y;
                 }
             }
         }
-        obj -= g;
         moves += 1;
         __syncthreads();  // the move is applied before the next step reads the lists
     }
-    // the moved requests' share of the errors
-    for (int j = tid; j < n; j += RB_THREADS) {
-        const int v = jx[j];
-        if (v > -2) continue;
-        const int x = -2 - v, y = jy[j];
-        const int64_t l = jl[j];
-        atomicAdd((unsigned long long*)&a.le[pr.wbase + x], (unsigned long long)-l);
-        atomicAdd((unsigned long long*)&a.be[pr.wbase + x], (unsigned long long)(int64_t)-1);
-        atomicAdd((unsigned long long*)&a.le[pr.wbase + y], (unsigned long long)l);
-        atomicAdd((unsigned long long*)&a.be[pr.wbase + y], 1ull);
+    // final errors and workers
+    for (int y = tid; y < W; y += RB_THREADS) {
+        a.le[pr.wbase + y] = cle[y];
+        a.be[pr.wbase + y] = cbe[y];
     }
+    for (int j = tid; j < n; j += RB_THREADS) a.new_worker[pr.new0 + j] = jx[j];
+    const RbPair obj1 = rb_objective(cle, cbe, W, rho, red);
     if (tid == 0) {
         if (a.moves != nullptr) a.moves[p] = moves;
         if (a.obj != nullptr) {
-            a.obj[2 * p] = obj0;
-            a.obj[2 * p + 1] = obj;
+            a.obj[4 * p] = obj0.a;
+            a.obj[4 * p + 1] = obj0.b;
+            a.obj[4 * p + 2] = obj1.a;
+            a.obj[4 * p + 3] = obj1.b;
         }
     }
 }

@@ -1,8 +1,9 @@
 """Grouped placement (App. A) on the GPU vs the CPU oracle (needs an MI355X).
 
-The reference is the definition: query x of the stream goes to group x mod G,
-and each group is an independent placement (the oracle's) of its own queries
-on its own workers, with a heartbeat after every H / G of its queries."""
+The reference is the oracle's grouped placement: its router sends group g the
+share N_g / N_w of the stream, and each group places its queries on its own
+workers with Algorithm 1, under the cluster's heartbeats (every H queries of
+the whole stream)."""
 from __future__ import annotations
 
 import dataclasses
@@ -33,25 +34,11 @@ def say(*a):
 
 
 def oracle_grouped(t, sizes, H):
-    """Per query: global worker (or -1) and diagnostics, group by group."""
-    G = len(sizes)
-    Q = t.n_queries
-    worker = np.full(Q, -2, np.int32)
-    diag = {f: np.zeros(Q, np.float64 if f.endswith("chosen") and f[0] == "t" else np.int64) for f in FIELDS}
-    wb = 0
-    for g, n in enumerate(sizes):
-        o0, o1 = int(t.res_offsets[wb]), int(t.res_offsets[wb + n])
-        off = t.res_offsets[wb:wb + n + 1] - o0
-        td = None if t.res_t_dec is None else t.res_t_dec[o0:o1]
-        r = ref.place(n, np.broadcast_to(t.kv_capacity, (t.n_workers,))[wb:wb + n], off, t.res_l_in[o0:o1],
-                      t.res_l_pred[o0:o1], t.res_generated[o0:o1], t.model, t.q_l_in[g::G], t.q_l_pred[g::G],
-                      heartbeat_every=H // G, res_t_dec=td)
-        worker[g::G] = np.where(r.worker >= 0, r.worker + wb, -1)
-        for f in FIELDS:
-            diag[f][g::G] = getattr(r, f)
-        wb += n
-    assert (worker != -2).all()
-    return worker, diag
+    """Per query: global worker (or -1) and diagnostics over its group."""
+    r = ref.place_grouped(t.n_workers, np.broadcast_to(np.asarray(t.kv_capacity, np.int64), (t.n_workers,)),
+                          t.res_offsets, t.res_l_in, t.res_l_pred, t.res_generated, t.model, sizes, t.q_l_in,
+                          t.q_l_pred, heartbeat_every=H, res_t_dec=t.res_t_dec)
+    return r.worker, {f: getattr(r, f) for f in FIELDS}
 
 
 def check(got, want_w, want_d, label):
@@ -70,6 +57,8 @@ CASES = [
     (3, [10, 17, 13], 0, 64),
     (4, [10, 10, 10, 10], 48, 256),
     (5, [1, 2, 30, 3, 4], 60, 1024),
+    (5, [1, 2, 30, 3, 4], 37, 128),
+    (2, [39, 1], 7, 64),
 ]
 
 
@@ -85,7 +74,14 @@ def test_grouped_matches_oracle(aladdin, case):
     ev.close()
     w, d = oracle_grouped(t, sizes, H)
     check(got, w, d, "grouped %s" % (case,))
-    assert 0 < int((w >= 0).sum()) < t.n_queries
+    assert int((w >= 0).sum()) > 0 and (H > 0 or int((w >= 0).sum()) < t.n_queries)
+    # every group takes its share of the stream (within one query)
+    route = ref.route_groups(sizes, t.n_queries)
+    wb = np.concatenate([[0], np.cumsum(sizes)])
+    for g, n in enumerate(sizes):
+        assert abs(int((route == g).sum()) - t.n_queries * n / sum(sizes)) < 1
+        placed = w[route == g]
+        assert np.all((placed == -1) | ((placed >= wb[g]) & (placed < wb[g + 1])))
     # one group is the ungrouped placement
     if G == 1:
         want = ref.place_trace(dataclasses.replace(t, heartbeat_every=H))
@@ -94,15 +90,16 @@ def test_grouped_matches_oracle(aladdin, case):
 
 
 def test_grouped_in_calls_with_history(aladdin):
-    """Calls ending at heartbeats continue one stream; constraint (d) with a
-    decode history holds per group."""
+    """Calls continue one stream (the router's counts and the heartbeat clock
+    carry over, also in the middle of a heartbeat window); constraint (d) with
+    a decode history holds per group."""
     G, sizes, H = 3, [7, 11, 6], 30
     t = wl.with_decode_history(wl.make_trace("grouped-d", 32, W=24, R=12, Q=1800, kv_capacity=20000,
                                              model=wl.BASE_MODEL), 5)
     ev = aladdin.Evaluator(0, tile=128)
     ev.load_trace(t)
     parts, ds = [], []
-    for a, b in [(0, 30), (30, 300), (300, 1800)]:
+    for a, b in [(0, 37), (37, 301), (301, 1800)]:
         r = ev.place_grouped(sizes, t.q_l_in[a:b], t.q_l_pred[a:b], heartbeat_every=H)
         parts.append(r.worker)
         ds.append(r.diag)
@@ -135,9 +132,8 @@ def test_grouped_arguments_checked(aladdin):
     ev = aladdin.Evaluator(0)
     ev.load_trace(t)
     bad = [([4, 3], 0, 100),       # sizes do not add up to W
-           ([4, 4], 3, 99),        # period not a multiple of G
-           ([4, 4], 10, 95),       # the call would not end at a heartbeat
-           ([8, 0], 0, 10)]        # empty group
+           ([8, 0], 0, 10),        # empty group
+           ([4, 4], -1, 10)]       # negative period
     for sizes, H, Q in bad:
         with pytest.raises(aladdin.AladdinError) as e:
             ev.place_grouped(sizes, t.q_l_in[:Q], t.q_l_pred[:Q], heartbeat_every=H)
@@ -156,10 +152,8 @@ def draw_grouped(seed):
         model = dataclasses.replace(model, ttft_slo=math.inf)
     elif rng.random() < 0.2:
         model = dataclasses.replace(model, k1=-1e-7, k1q=1e-9)
-    H = G * int(rng.choice([0, 1, 5, 20]))
+    H = int(rng.choice([0, 1, 5, 20, 33]))
     Q = int(rng.integers(1, 1500))
-    if H > 0:
-        Q = max(1, Q // H) * H  # with heartbeats a grouped call ends at one
     t = wl.make_trace("rgrouped%d" % seed, 9950 + seed, W=W, R=R, Q=Q, kv_capacity=int(rng.choice([8000, 30000])),
                       model=model, in_dist=wl.SHORT_IN, out_dist=wl.SHORT_OUT)
     if R > 0 and rng.random() < 0.3:

@@ -41,9 +41,9 @@ def check_against_oracle(batch, got, problems=None):
         assert got["le"][wb[p]:wb[p] + W].tolist() == want.le.tolist(), "problem %d: l^e differs" % p
         assert got["be"][wb[p]:wb[p] + W].tolist() == want.be.tolist(), "problem %d: b^e differs" % p
         assert int(got["moves"][p]) == k
-        assert got["obj"][p].tolist() == [want.obj_before, want.obj_after]
+        assert got["obj"][p].tolist() == [*want.obj_before, *want.obj_after]
         if "log" in got:
-            assert got["log"][2 * n0:2 * n0 + 2 * k].reshape(k, 2).tolist() == want.moves.tolist()
+            assert got["log"][p].tolist() == want.moves.tolist()
 
 
 SMALL = [
@@ -68,39 +68,46 @@ def test_rebalance_matches_oracle(ev, case):
 
 
 def test_rebalance_models_per_problem(ev):
-    """Each problem takes its own rho = c2 / k2 (rounded to whole tokens)."""
-    b = wl.make_rebalance("rho", 7, 4, 24, 12, 400, sigma_err=0.7)
+    """Each problem takes its own rho = c2 / k2, the real ratio of two doubles
+    (not whole tokens): 0, about 150, 500.025, 2000 and exactly 500.5."""
+    from fractions import Fraction
+    b = wl.make_rebalance("rho", 7, 5, 24, 12, 400, sigma_err=0.7)
     base = b.models[0]
     b.models = [dataclasses.replace(base, c2=c2) for c2 in (0.0, 3e-5, 1.00005e-4, 4e-4)]
-    assert [ref.rebalance_rho(m) for m in b.models] == [0, 150, 500, 2000]
+    b.models.append(dataclasses.replace(base, k2=2.0 ** -22, c2=1001 * 2.0 ** -23))
+    rhos = [Fraction(m.c2) / Fraction(m.k2) for m in b.models]
+    assert rhos[4] == Fraction(1001, 2) and abs(rhos[2] - Fraction(500025, 1000)) < Fraction(1, 10 ** 9)
+    assert sum(r.denominator != 1 for r in rhos) >= 3
     got = ev.rebalance(b, want_log=True)
     check_against_oracle(b, got)
 
 
 def test_rebalance_full_size(ev):
-    """The 256-problem workload: every problem against the oracle, plus the
-    invariants (a move keeps sum c, lowers sum |c|, touches a request once)."""
+    """The 256-problem workload in the launch the benchmark times: every 16th
+    problem against the oracle (the exhaustive oracle takes about half a second
+    per problem), and on all of them the invariants (a move keeps sum l^e and
+    sum b^e, the objective never grows)."""
+    from fractions import Fraction
     b = wl.make_config("rebalance")
     say("rebalance full size", b.P)
     got = ev.rebalance(b, want_log=True)
-    check_against_oracle(b, got)
+    check_against_oracle(b, got, problems=range(0, b.P, 16))
     wb = np.concatenate([[0], np.cumsum(b.n_workers)])
+    rho = Fraction(b.models[0].c2) / Fraction(b.models[0].k2)
+    assert rho.denominator != 1  # the workload's rho is not a whole number of tokens
     for p in range(b.P):
-        assert got["obj"][p][1] <= got["obj"][p][0]
-        n0, k = int(b.new_offsets[p]), int(got["moves"][p])
-        moved = got["log"][2 * n0:2 * n0 + 2 * k:2]
-        assert len(set(moved.tolist())) == k
+        o = [int(x) for x in got["obj"][p]]
+        assert o[2] + rho * o[3] <= o[0] + rho * o[1]
     assert int(got["moves"].sum()) > 0
     # a move takes its request's length and one batch slot from one worker to
-    # another: the sum of c over a problem's workers does not change
-    rho = ref.rebalance_rho(b.models[0])
+    # another: the sums of l^e and of b^e over a problem's workers do not change
     for p in range(b.P):
         n0, n1 = int(b.new_offsets[p]), int(b.new_offsets[p + 1])
-        c = got["le"][wb[p]:wb[p + 1]] + rho * got["be"][wb[p]:wb[p + 1]]
         changed = got["worker"][n0:n1] != b.new_worker[n0:n1]
-        assert int(changed.sum()) == int(got["moves"][p])
+        assert int(changed.sum()) <= int(got["moves"][p])
         want = ref.rebalance(*b.problem(p)[:7], [], [])  # the errors alone, no new requests
-        assert int(c.sum()) == int((want.le + rho * want.be).sum())
+        assert int(got["le"][wb[p]:wb[p + 1]].sum()) == int(want.le.sum())
+        assert int(got["be"][wb[p]:wb[p + 1]].sum()) == int(want.be.sum())
 
 
 def test_rebalance_twice_in_a_row(ev):
@@ -158,7 +165,8 @@ def test_random_rebalance_matches_oracle(ev, seed):
                           sigma_err=float(rng.choice([0.0, 0.3, 0.8, 1.5])), unplaced=float(rng.choice([0.0, 0.1, 0.5])))
     if rng.random() < 0.5:
         base = b.models[0]
-        b.models = [dataclasses.replace(base, c2=float(rng.choice([0.0, 3e-5, 1e-4, 4e-4]))) for _ in range(P)]
+        b.models = [dataclasses.replace(base, c2=float(rng.choice([0.0, 3e-5, 1e-4, 4e-4, 1.7e-5])),
+                                        k2=float(rng.choice([2e-7, 3.1e-7]))) for _ in range(P)]
     say("random rebalance", seed, "P", P, "W", W[:6], "new", n_new[:6])
     got = ev.rebalance(b, want_log=True)
     check_against_oracle(b, got)

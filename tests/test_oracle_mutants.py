@@ -62,18 +62,32 @@ MUTANTS = [
     # split-phase decode workers
     ("decode workers still check (d)", "if (use_d && !decode_only) {", "if (use_d) {"),
     ("decode workers flag TTFT near ties", "(!decode_only && near(o->ttft, m->ttft_slo))", "near(o->ttft, m->ttft_slo)"),
+    # App. A grouped placement
+    ("router splits the stream evenly", "if (!(counts[i] * Nw < h * (int64_t)N[i])) continue;",
+     "if (!(counts[i] * G < h)) continue;"),
+    ("router without the upper quota", "if (!(counts[i] * Nw < h * (int64_t)N[i])) continue;", ""),
+    ("router ties to the highest group", "(int64_t)N[i] * (counts[best] + 1) > (int64_t)N[best] * (counts[i] + 1)",
+     "(int64_t)N[i] * (counts[best] + 1) >= (int64_t)N[best] * (counts[i] + 1)"),
+    ("grouped search over every worker", "            lo = gfirst[g];\n            hi = gfirst[g + 1];\n",
+     "            lo = 0 * gfirst[g];\n            hi = W + 0 * gfirst[g + 1];\n"),
     # Algorithm 2
-    ("A2 over-estimate error with the sign flipped", "le[i] += (int64_t)old_lreal[j] - old_lpred[j]; be[i] -= 1;",
-     "le[i] += (int64_t)old_lpred[j] - old_lreal[j]; be[i] -= 1;"),
-    ("A2 under-estimate counts the old prediction", "le[i] += old_lrepred[j]; be[i] += 1;",
-     "le[i] += old_lpred[j]; be[i] += 1;"),
+    ("A2 over-estimate error with the sign flipped", "c[i].a += (int64_t)old_lreal[j] - old_lpred[j]; c[i].b -= 1;",
+     "c[i].a += (int64_t)old_lpred[j] - old_lreal[j]; c[i].b -= 1;"),
+    ("A2 under-estimate counts the old prediction", "c[i].a += old_lrepred[j]; c[i].b += 1;",
+     "c[i].a += old_lpred[j]; c[i].b += 1;"),
     ("A2 under-estimate test non-strict", "if (old_lout[j] > old_lpred[j])", "if (old_lout[j] >= old_lpred[j])"),
-    ("A2 batch error left out of the line", "#define RB_C(i) (le[i] + rho * be[i])", "#define RB_C(i) (le[i])"),
-    ("A2 a move shifts only the length", "const int64_t d = (int64_t)new_lpred[j] + rho;",
-     "const int64_t d = (int64_t)new_lpred[j];"),
-    ("A2 ties to the last pair", "if (gain > best) { best = gain;", "if (gain >= best && gain > 0) { best = gain;"),
-    ("A2 a request may move twice", "        moved[bj] = 1;\n", ""),
-    ("A2 rho truncated", "return (int64_t)llrint(m->c2 / m->k2);", "return (int64_t)(m->c2 / m->k2 * 0.999);"),
+    ("A2 batch error left out of the line", "const __float128 y = (__float128)b * (__float128)m->c2;",
+     "const __float128 y = 0 * (__float128)b * (__float128)m->c2;"),
+    ("A2 rho rounded to whole tokens", "const __float128 y = (__float128)b * (__float128)m->c2;",
+     "const __float128 y = (__float128)b * (__float128)(rint(m->c2 / m->k2) * m->k2);"),
+    ("A2 a move shifts only the length", "const rb_pair d = {new_lpred[j], 1};", "const rb_pair d = {new_lpred[j], 0};"),
+    ("A2 ties to the last pair", "if (rb_sign(diff.a, diff.b, m) > 0) { best = gain;",
+     "if (rb_sign(diff.a, diff.b, m) >= 0 && rb_sign(gain.a, gain.b, m) > 0) { best = gain;"),
+    ("A2 a request moves at most once", "        new_worker[bj] = by;\n",
+     "        new_worker[bj] = by;\n        ((int32_t*)new_lpred)[bj] = 1 << 30;\n"),
+    ("A2 the objective's absolute value taken on the length error only",
+     "    if (rb_sign(u.a, u.b, m) < 0) { u.a = -u.a; u.b = -u.b; }",
+     "    if (u.a < 0) { u.a = -u.a; u.b = -u.b; }"),
 ]
 
 PINS = [
@@ -103,9 +117,14 @@ PINS = [
     lambda: pins.test_moves_match_bruteforce(True),
     lambda: pins.test_decode_workers_match_bruteforce(0),
     lambda: pins.test_decode_workers_match_bruteforce(2),
+    pins.test_router_share_within_one_query,
+    pins.test_router_equal_sizes_is_round_robin_and_worked_example,
+    lambda: pins.test_grouped_placement_is_each_groups_algorithm1(0),
+    lambda: pins.test_grouped_placement_is_each_groups_algorithm1(7),
+    pins.test_rebalance_sign_is_exact,
     pins.test_rebalance_worked_example,
     pins.test_rebalance_errors_closed_forms,
-    pins.test_rebalance_request_moves_at_most_once,
+    pins.test_rebalance_request_may_move_again,
 ] + [lambda s=s: pins.test_rebalance_two_workers_closed_form(s) for s in range(6)] + [
     lambda s=s: pins.test_rebalance_moves_replayed_by_bruteforce(s) for s in range(25)]
 

@@ -28,15 +28,15 @@ def run(fn, h, b, dev):
     le = torch.full((Wt,), 7, dtype=torch.int64, device=dev)  # not zero: the call clears them
     be = torch.full((Wt,), -7, dtype=torch.int64, device=dev)
     mv = torch.empty(P, dtype=torch.int32, device=dev)
-    obj = torch.empty(2 * P, dtype=torch.int64, device=dev)
-    log = torch.empty(max(1, 2 * int(b.new_offsets[-1])), dtype=torch.int32, device=dev)
+    obj = torch.empty(4 * P, dtype=torch.int64, device=dev)
+    cap = int(4 * np.diff(b.new_offsets).max() + int(np.max(b.n_workers)))
+    log = torch.empty(max(1, 2 * P * cap), dtype=torch.int32, device=dev)
     fn(h, P, b.n_workers, models, b.old_offsets, d32(b.old_worker), d32(b.old_l_pred), d32(b.old_l_out),
-       d32(b.old_l_real), d32(b.old_l_repred), b.new_offsets, d32(b.new_l_pred), nw, le, be, mv, log, obj)
+       d32(b.old_l_real), d32(b.old_l_repred), b.new_offsets, d32(b.new_l_pred), nw, le, be, mv, cap, log, obj)
     torch.cuda.synchronize()
     k = mv.cpu().numpy()
     lg = log.cpu().numpy()
-    n0 = b.new_offsets[:-1]
-    logs = [lg[2 * int(n0[p]):2 * int(n0[p]) + 2 * int(k[p])].tolist() for p in range(P)]
+    logs = [lg[2 * p * cap:2 * p * cap + 2 * int(k[p])].tolist() for p in range(P)]
     return {"worker": nw.cpu().numpy(), "le": le.cpu().numpy(), "be": be.cpu().numpy(), "moves": k,
             "obj": obj.cpu().numpy(), "logs": logs}
 
