@@ -51,8 +51,13 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        build()
-        L = ctypes.CDLL(LIB)
+        # ORACLE_LIB: a separately built copy of the oracle (the sanitizer test
+        # builds one with AddressSanitizer and UBSan); otherwise build LIB here
+        path = os.environ.get("ORACLE_LIB")
+        if not path:
+            build()
+            path = LIB
+        L = ctypes.CDLL(path)
         P = ctypes.c_void_p
         i32, i64 = ctypes.c_int32, ctypes.c_int64
         L.ora_place.argtypes = [i32, P, P, P, P, P, P, ctypes.POINTER(OraModel), i32, P, P, i32, i32, i32,
