@@ -154,7 +154,7 @@ def time_rebalance(steps: int, oracle_problems: int = 0):
 
     def call():
         nw.copy_(nw0)
-        aladdin.ald_rebalance(ev.h, b.P, b.n_workers, models, b.old_offsets, *old, b.new_offsets, nl, nw,
+        ev.call(aladdin.ald_rebalance, b.P, b.n_workers, models, b.old_offsets, *old, b.new_offsets, nl, nw,
                               le, be, mv, 0, None, obj)
 
     for _ in range(2):

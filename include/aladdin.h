@@ -44,8 +44,14 @@
  * Conventions
  *   - Every array argument except where marked "host" is a DEVICE pointer to
  *     contiguous memory owned by the caller (e.g. a torch tensor's data_ptr());
- *     the library never frees caller memory.  Device memory for worker state and
- *     scratch is allocated by the library inside the handle.
+ *     the library never frees caller memory.
+ *   - The library allocates no device memory.  The caller attaches a device
+ *     workspace (ald_set_workspace, e.g. a torch uint8 tensor); the loaded
+ *     workers' state lives at its start and every call lays out its own
+ *     tables after it.  A call that does not fit returns ALD_ESPACE before
+ *     doing any work, and ald_workspace_needed gives the size it needed.  The
+ *     only memory the library allocates is one pinned host buffer per handle
+ *     (64 bytes per scenario) into which the kernels copy their control blocks.
  *   - All work runs on the stream given to ald_create.  Every call below returns
  *     after that stream has finished the call's work, so errors are synchronous
  *     and outputs are ready on return.
@@ -75,6 +81,7 @@ extern "C" {
 #define ALD_ESLOTS (-3)    /* a worker ran out of request slots */
 #define ALD_ESTATE (-4)    /* call order: no workers loaded */
 #define ALD_EOVERFLOW (-5) /* a value would leave the exactly representable range */
+#define ALD_ESPACE (-6)    /* the attached workspace is too small for the call (see ald_workspace_needed) */
 
 typedef struct ald_handle* ald_handle_t;
 
@@ -94,7 +101,8 @@ typedef struct {
 /* One cluster configuration of a scaling sweep (host struct). */
 typedef struct {
     int32_t n_workers;         /* >= 1 */
-    int32_t gpus_per_worker;   /* informational, not used by the evaluator */
+    int32_t gpus_per_worker;   /* 1 .. 256; counts the GPUs of the sweep's answer (the latency
+                                  model already holds the worker's speed) */
     int64_t kv_capacity;       /* tokens per worker, 1 .. 2^30 */
     ald_model_t model;
 } ald_scenario_t;
@@ -116,8 +124,35 @@ typedef struct {
  * (a hipStream_t, or NULL for the default stream). */
 int ald_create(ald_handle_t* handle, int device, void* hip_stream);
 
-/* Release the handle and all device memory it allocated.  NULL is accepted. */
+/* Release the handle (the caller's workspace is not touched).  NULL is accepted. */
 int ald_destroy(ald_handle_t handle);
+
+/* Attach the caller's device workspace: `workspace` is a device pointer,
+ * 256-byte aligned, of `bytes` bytes, kept alive by the caller while the
+ * handle uses it (NULL with bytes = 0 detaches).  With workers loaded, their
+ * state moves into the new workspace (a copy on the handle's stream, so the
+ * old one may be released once the stream has passed this call); the new one
+ * must hold it (ALD_ESPACE otherwise) and must not overlap the old state
+ * (ALD_EINVAL). */
+int ald_set_workspace(ald_handle_t handle, void* workspace, size_t bytes);
+
+/* The workspace size (bytes, including the loaded state) that the last call
+ * refused with ALD_ESPACE needed. */
+int ald_workspace_needed(ald_handle_t handle, size_t* bytes);
+
+/* Workspace for loading W workers holding n_resident requests in all (model
+ * and slots_per_worker as for ald_load_workers; with_history != 0 for
+ * ald_load_workers_history) and then placing up to Q queries per
+ * ald_place_stream or ald_place_stream_hb call, at the handle's current tile
+ * setting.  Grouped placement, moves and Algorithm 2 lay out their own tables
+ * after the state; ald_workspace_needed reports what a refused call needed. */
+int ald_workspace_size(ald_handle_t handle, int32_t W, int64_t n_resident, const ald_model_t* model,
+                       int32_t slots_per_worker, int32_t with_history, int32_t Q, size_t* bytes);
+
+/* Workspace for ald_sweep_scenarios or ald_sweep_scenarios_hb over these S
+ * scenarios (host array) and Q queries, beyond the state of loaded workers
+ * (the sweep's tables go after it). */
+int ald_sweep_workspace_size(ald_handle_t handle, int32_t S, const ald_scenario_t* scen, int32_t Q, size_t* bytes);
 
 /* Queries evaluated per speculative tile (default 4096, 64 .. 1048576).  The
  * result never depends on it; only speed does. */
@@ -148,11 +183,16 @@ int ald_load_workers_history(ald_handle_t handle, int32_t W, const ald_model_t* 
                              int32_t slots_per_worker);
 
 /* Place Q queries (device arrays q_l_in[Q], q_l_pred[Q], values >= 1) in index
- * (arrival) order on the loaded workers, committing every placement.  Repeated
- * calls continue the same stream.  heartbeat_every = H > 0: a heartbeat after
- * every H processed queries (counted across calls); 0: no heartbeat in this
- * call.  out_worker[Q] (device): chosen worker or -1.  out_diag[Q] (device) or
- * NULL. */
+ * (arrival) order on the loaded workers, committing every placement: the online
+ * best fit of Algorithm 1 under the constraints (b), (c), (d), (e) of the
+ * placement problem of Sec. 4.2 (Table 1: each query carries l_in and its
+ * predicted l_out; the SLOs are the model's).  Repeated calls continue the same
+ * stream.  heartbeat_every = H > 0: a heartbeat after every H processed queries
+ * (counted across calls; Sec. 4.2 places requests per heartbeat); 0: no
+ * heartbeat in this call.  out_worker[Q] (device): chosen worker or -1 (no
+ * worker meets every constraint: the query is rejected and nothing changes).
+ * out_diag[Q] (device) or NULL.  ALD_EINVAL (nothing written) for a length
+ * outside [1, 2^24]; ALD_ESLOTS when a worker runs out of request slots. */
 int ald_place_stream(ald_handle_t handle, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
                      int32_t heartbeat_every, int32_t* out_worker, ald_query_diag_t* out_diag);
 
@@ -204,14 +244,20 @@ int ald_place_grouped(ald_handle_t handle, int32_t G, const int32_t* group_worke
                       const int32_t* q_l_in, const int32_t* q_l_pred, int32_t heartbeat_every,
                       int32_t* out_worker, ald_query_diag_t* out_diag);
 
-/* Scaling sweep: S scenarios (host array scen[S]), each starting with empty
- * workers, each placing the same Q queries (device arrays) with no heartbeat.
- * Device outputs: out_rejected[S], out_first_reject[S] (-1 if none) and, if not
- * NULL, out_worker[S*Q] (row s = placement of scenario s).  The handle's loaded
- * workers are not touched (no ald_load_workers needed). */
+/* Scaling sweep (Sec. 4.4: the worker count needed for an arrival rate, found
+ * by placing the stream on candidate clusters; Sec. 6.4: the GPUs needed to
+ * meet every SLO): S scenarios (host array scen[S]), each starting with empty
+ * workers, each placing the same Q queries (device arrays) with Algorithm 1
+ * and no heartbeat.  Device outputs: out_rejected[S], out_first_reject[S] (-1
+ * if none), if not NULL out_worker[S*Q] (row s = placement of scenario s), and
+ * if not NULL out_min_gpus[2] = the answer: the fewest GPUs (n_workers *
+ * gpus_per_worker) over scenarios with no rejection and that scenario's index
+ * (lowest index on ties), or {-1, -1} when every scenario rejects something.
+ * gpus_per_worker lies in [1, 256]; at most 2^24 - 1 scenarios.  The handle's
+ * loaded workers are not touched (no ald_load_workers needed). */
 int ald_sweep_scenarios(ald_handle_t handle, int32_t S, const ald_scenario_t* scen, int32_t Q,
                         const int32_t* q_l_in, const int32_t* q_l_pred, int32_t* out_rejected,
-                        int32_t* out_first_reject, int32_t* out_worker);
+                        int32_t* out_first_reject, int32_t* out_worker, int64_t* out_min_gpus);
 
 /* As ald_sweep_scenarios, with heartbeats (Sec. 4.2, placement per heartbeat):
  * scenario s runs one decode iteration on all its workers after every
@@ -224,7 +270,7 @@ int ald_sweep_scenarios(ald_handle_t handle, int32_t S, const ald_scenario_t* sc
 int ald_sweep_scenarios_hb(ald_handle_t handle, int32_t S, const ald_scenario_t* scen,
                            const int32_t* heartbeat_every, int32_t Q, const int32_t* q_l_in,
                            const int32_t* q_l_pred, int32_t* out_rejected, int32_t* out_first_reject,
-                           int32_t* out_worker);
+                           int32_t* out_worker, int64_t* out_min_gpus);
 
 /* Algorithm 2 (Sec. 4.3): re-balance the new requests of a heartbeat against
  * the output-length prediction errors of the ongoing ones, for P independent
@@ -290,8 +336,11 @@ int ald_rebalance_noalloc(ald_handle_t handle, int32_t P, const int32_t* n_worke
                           int64_t* out_le, int64_t* out_be, int32_t* out_moves, int32_t log_cap, int32_t* out_log,
                           int64_t* out_obj);
 
-/* Current state of every loaded worker (device arrays of W): batch size, sum of
- * contexts, sum of remaining lengths, KV peak over future iterations. */
+/* Current state of every loaded worker (device arrays of W), the quantities of
+ * Table 1 that the constraints read: batch size B_i, sum of contexts (input
+ * plus generated tokens), sum of remaining lengths (predicted minus generated),
+ * and the KV peak over future iterations that constraint (e) compares with the
+ * capacity m_i.  Brings every worker to the current decode iteration first. */
 int ald_worker_summary(ald_handle_t handle, int32_t* B, int64_t* sum_c, int64_t* sum_r, int64_t* peak);
 
 /* Kernel timing with HIP events on the handle's stream (off by default).

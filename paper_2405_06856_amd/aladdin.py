@@ -21,7 +21,7 @@ import torch  # noqa: F401
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libaladdin.so")
 
-ALD_OK, ALD_EINVAL, ALD_EHIP, ALD_ESLOTS, ALD_ESTATE, ALD_EOVERFLOW = 0, -1, -2, -3, -4, -5
+ALD_OK, ALD_EINVAL, ALD_EHIP, ALD_ESLOTS, ALD_ESTATE, ALD_EOVERFLOW, ALD_ESPACE = 0, -1, -2, -3, -4, -5, -6
 
 KERNEL_KINDS = {"build": 0, "eval": 1, "select": 2, "commit": 3, "rebalance": 4}
 
@@ -49,7 +49,8 @@ DIAG_DTYPE = np.dtype([("n_feasible", "<i4"), ("near_tie", "<i4"), ("kv_peak_cho
                        ("kv_excess_min", "<i8"), ("ttft_chosen", "<f8"), ("tdec_chosen", "<f8")])
 assert DIAG_DTYPE.itemsize == 40
 
-SYMBOLS = ("ald_create", "ald_destroy", "ald_set_tile", "ald_load_workers", "ald_load_workers_history",
+SYMBOLS = ("ald_create", "ald_destroy", "ald_set_workspace", "ald_workspace_needed", "ald_workspace_size",
+           "ald_sweep_workspace_size", "ald_set_tile", "ald_load_workers", "ald_load_workers_history",
            "ald_place_stream", "ald_place_stream_hb", "ald_place_grouped", "ald_move_requests",
            "ald_sweep_scenarios", "ald_sweep_scenarios_hb", "ald_rebalance", "ald_rebalance_noalloc", "ald_worker_summary", "ald_set_profiling", "ald_kernel_time",
            "ald_last_error", "ald_strerror")
@@ -63,6 +64,11 @@ def _load():
     sig = {
         "ald_create": ([ctypes.POINTER(P), ctypes.c_int, P], ctypes.c_int),
         "ald_destroy": ([P], ctypes.c_int),
+        "ald_set_workspace": ([P, P, ctypes.c_size_t], ctypes.c_int),
+        "ald_workspace_needed": ([P, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
+        "ald_workspace_size": ([P, i32, i64, ctypes.POINTER(Model), i32, i32, i32, ctypes.POINTER(ctypes.c_size_t)],
+                               ctypes.c_int),
+        "ald_sweep_workspace_size": ([P, i32, P, i32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
         "ald_set_tile": ([P, i32], ctypes.c_int),
         "ald_load_workers": ([P, i32, ctypes.POINTER(Model), P, P, P, P, P, i32], ctypes.c_int),
         "ald_load_workers_history": ([P, i32, ctypes.POINTER(Model), P, P, P, P, P, P, i32], ctypes.c_int),
@@ -70,8 +76,8 @@ def _load():
         "ald_place_grouped": ([P, i32, P, i32, P, P, i32, P, P], ctypes.c_int),
         "ald_place_stream_hb": ([P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_move_requests": ([P, i32, P, P, P, P], ctypes.c_int),
-        "ald_sweep_scenarios": ([P, i32, P, i32, P, P, P, P, P], ctypes.c_int),
-        "ald_sweep_scenarios_hb": ([P, i32, P, P, i32, P, P, P, P, P], ctypes.c_int),
+        "ald_sweep_scenarios": ([P, i32, P, i32, P, P, P, P, P, P], ctypes.c_int),
+        "ald_sweep_scenarios_hb": ([P, i32, P, P, i32, P, P, P, P, P, P], ctypes.c_int),
         "ald_rebalance": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, i32, P, P], ctypes.c_int),
         "ald_rebalance_noalloc": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, i32, P, P], ctypes.c_int),
         "ald_worker_summary": ([P, P, P, P, P], ctypes.c_int),
@@ -117,6 +123,35 @@ def ald_create(device: int = 0, stream: Optional[int] = None) -> ctypes.c_void_p
 
 def ald_destroy(h) -> None:
     _L.ald_destroy(h)
+
+
+def ald_set_workspace(h, workspace, nbytes: Optional[int] = None) -> None:
+    """workspace: a contiguous device tensor (its bytes are the workspace), or None."""
+    if workspace is None:
+        _check(h, _L.ald_set_workspace(h, None, 0))
+        return
+    n = workspace.numel() * workspace.element_size() if nbytes is None else int(nbytes)
+    _check(h, _L.ald_set_workspace(h, _dptr(workspace), n))
+
+
+def ald_workspace_needed(h) -> int:
+    n = ctypes.c_size_t()
+    _check(h, _L.ald_workspace_needed(h, ctypes.byref(n)))
+    return n.value
+
+
+def ald_workspace_size(h, W: int, n_resident: int, model: Model, slots_per_worker: int = 0, with_history: bool = False,
+                       Q: int = 0) -> int:
+    n = ctypes.c_size_t()
+    _check(h, _L.ald_workspace_size(h, int(W), int(n_resident), ctypes.byref(model), int(slots_per_worker),
+                                    int(bool(with_history)), int(Q), ctypes.byref(n)))
+    return n.value
+
+
+def ald_sweep_workspace_size(h, S: int, scen, Q: int) -> int:
+    n = ctypes.c_size_t()
+    _check(h, _L.ald_sweep_workspace_size(h, int(S), ctypes.cast(scen, ctypes.c_void_p), int(Q), ctypes.byref(n)))
+    return n.value
 
 
 def ald_set_tile(h, tile_queries: int) -> None:
@@ -170,21 +205,22 @@ def ald_place_grouped(h, G: int, group_workers, Q: int, q_l_in, q_l_pred, heartb
 
 
 def ald_sweep_scenarios(h, S: int, scen, Q: int, q_l_in, q_l_pred, out_rejected, out_first_reject,
-                        out_worker=None) -> None:
+                        out_worker=None, out_min_gpus=None) -> None:
     _check(h, _L.ald_sweep_scenarios(h, int(S), ctypes.cast(scen, ctypes.c_void_p), int(Q), _dptr(q_l_in),
                                      _dptr(q_l_pred), _dptr(out_rejected), _dptr(out_first_reject),
-                                     _dptr(out_worker)))
+                                     _dptr(out_worker), _dptr(out_min_gpus)))
 
 
 def ald_sweep_scenarios_hb(h, S: int, scen, heartbeat_every, Q: int, q_l_in, q_l_pred, out_rejected,
-                           out_first_reject, out_worker=None) -> None:
+                           out_first_reject, out_worker=None, out_min_gpus=None) -> None:
     """heartbeat_every: host array of S periods."""
     hb = np.ascontiguousarray(heartbeat_every, dtype=np.int32)
     if hb.shape != (S,):
         raise ValueError("heartbeat_every must hold one period per scenario")
     _check(h, _L.ald_sweep_scenarios_hb(h, int(S), ctypes.cast(scen, ctypes.c_void_p),
                                         hb.ctypes.data_as(ctypes.c_void_p), int(Q), _dptr(q_l_in), _dptr(q_l_pred),
-                                        _dptr(out_rejected), _dptr(out_first_reject), _dptr(out_worker)))
+                                        _dptr(out_rejected), _dptr(out_first_reject), _dptr(out_worker),
+                                        _dptr(out_min_gpus)))
 
 
 def _rebalance_call(fn, h, P: int, n_workers, models, old_offsets, old_worker, old_l_pred, old_l_out, old_l_real,
@@ -257,9 +293,11 @@ class Placement:
 
 
 class Evaluator:
-    """A handle bound to one device and torch's current stream on it."""
+    """A handle bound to one device and torch's current stream on it.  It owns
+    the handle's workspace, a torch uint8 tensor that grows (by at least a
+    quarter) whenever a call reports that it needs more."""
 
-    def __init__(self, device: int = 0, tile: Optional[int] = None):
+    def __init__(self, device: int = 0, tile: Optional[int] = None, workspace_bytes: int = 0):
         import torch
         self.torch = torch
         self.device = torch.device("cuda", device)
@@ -268,11 +306,36 @@ class Evaluator:
         if tile is not None:
             ald_set_tile(self.h, tile)
         self.W = 0
+        self.ws = None
+        self.ws_bytes = 0
+        if workspace_bytes > 0:
+            self.attach_workspace(workspace_bytes)
+
+    def attach_workspace(self, nbytes: int) -> None:
+        """Give the handle a workspace of at least nbytes (the loaded state moves along)."""
+        nbytes = (int(nbytes) + (1 << 21) - 1) & ~((1 << 21) - 1)
+        ws = self.torch.empty(nbytes, dtype=self.torch.uint8, device=self.device)
+        ald_set_workspace(self.h, ws, nbytes)
+        self.ws, self.ws_bytes = ws, nbytes
+
+    def call(self, fn, *args, **kw):
+        """fn(handle, ...), growing the workspace and calling again when it is too small."""
+        while True:
+            try:
+                return fn(self.h, *args, **kw)
+            except AladdinError as e:
+                if e.code != ALD_ESPACE:
+                    raise
+                need = ald_workspace_needed(self.h)
+                if need <= self.ws_bytes:
+                    raise
+                self.attach_workspace(max(need, self.ws_bytes + self.ws_bytes // 4))
 
     def close(self):
         if self.h is not None:
             ald_destroy(self.h)
             self.h = None
+        self.ws = None
 
     def __del__(self):
         try:
@@ -293,10 +356,10 @@ class Evaluator:
                       self._dev(res_l_in, t.int32), self._dev(res_l_pred, t.int32),
                       self._dev(res_generated, t.int32)]
         if res_t_dec is None:
-            ald_load_workers(self.h, W, to_model(model), *self._keep, slots_per_worker=slots_per_worker)
+            self.call(ald_load_workers, W, to_model(model), *self._keep, slots_per_worker=slots_per_worker)
         else:
             self._keep.append(self._dev(res_t_dec, t.float64))
-            ald_load_workers_history(self.h, W, to_model(model), *self._keep, slots_per_worker=slots_per_worker)
+            self.call(ald_load_workers_history, W, to_model(model), *self._keep, slots_per_worker=slots_per_worker)
         self.W = W
 
     def load_trace(self, trace, slots_per_worker=0):
@@ -320,7 +383,7 @@ class Evaluator:
                 d = t.empty(Q * DIAG_DTYPE.itemsize, dtype=t.uint8, device=self.device)
             elif d.dtype != t.uint8 or d.numel() < Q * DIAG_DTYPE.itemsize:
                 raise ValueError("diag_out must be a uint8 tensor of at least Q * %d bytes" % DIAG_DTYPE.itemsize)
-        ald_place_stream(self.h, Q, q_l_in, q_l_pred, heartbeat_every, out, d)
+        self.call(ald_place_stream, Q, q_l_in, q_l_pred, heartbeat_every, out, d)
         return out, d
 
     def place(self, q_l_in, q_l_pred, heartbeat_every=0, diag=True, hb_before=None) -> Placement:
@@ -334,7 +397,7 @@ class Evaluator:
             Q = int(ql.numel())
             out = t.empty(max(Q, 1), dtype=t.int32, device=self.device)
             d = t.empty(max(Q, 1) * DIAG_DTYPE.itemsize, dtype=t.uint8, device=self.device) if diag else None
-            ald_place_stream_hb(self.h, Q, ql, qp, hb_before, out, d)
+            self.call(ald_place_stream_hb, Q, ql, qp, hb_before, out, d)
             out = out[:Q]
             d = None if d is None else d[:Q * DIAG_DTYPE.itemsize]
         res = Placement(worker=out.cpu().numpy())
@@ -344,7 +407,7 @@ class Evaluator:
 
     def move_requests(self, l_in, l_pred, from_worker, to_worker) -> None:
         """Move requests placed in the current heartbeat window between workers."""
-        ald_move_requests(self.h, len(l_in), l_in, l_pred, from_worker, to_worker)
+        self.call(ald_move_requests, len(l_in), l_in, l_pred, from_worker, to_worker)
 
     def place_grouped(self, group_workers, q_l_in, q_l_pred, heartbeat_every=0, diag=True) -> Placement:
         """Grouped placement (App. A): query x of the stream goes to group x mod G."""
@@ -354,7 +417,7 @@ class Evaluator:
         Q = int(ql.numel())
         out = t.empty(max(Q, 1), dtype=t.int32, device=self.device)
         d = t.empty(max(Q, 1) * DIAG_DTYPE.itemsize, dtype=t.uint8, device=self.device) if diag else None
-        ald_place_grouped(self.h, len(group_workers), group_workers, Q, ql, qp, heartbeat_every, out, d)
+        self.call(ald_place_grouped, len(group_workers), group_workers, Q, ql, qp, heartbeat_every, out, d)
         res = Placement(worker=out[:Q].cpu().numpy())
         if diag:
             res.diag = d[:Q * DIAG_DTYPE.itemsize].cpu().numpy().view(DIAG_DTYPE)
@@ -371,8 +434,10 @@ class Evaluator:
         return {"B": B.cpu().numpy(), "sum_c": sc.cpu().numpy(), "sum_r": sr.cpu().numpy(),
                 "peak": pk.cpu().numpy()}
 
-    def sweep(self, scenarios, q_l_in, q_l_pred, want_workers=False, heartbeat_every=None):
-        """heartbeat_every: None (no heartbeat), one period for all scenarios, or one per scenario."""
+    def sweep(self, scenarios, q_l_in, q_l_pred, want_workers=False, heartbeat_every=None, want_answer=False):
+        """heartbeat_every: None (no heartbeat), one period for all scenarios, or
+        one per scenario.  Returns (rejected, first rejected, workers or None),
+        and with want_answer also the device's answer (fewest GPUs, scenario)."""
         t = self.torch
         S = len(scenarios)
         arr = (Scenario * S)()
@@ -384,13 +449,17 @@ class Evaluator:
         rej = t.empty(S, dtype=t.int32, device=self.device)
         first = t.empty(S, dtype=t.int32, device=self.device)
         ow = t.empty(S * Q, dtype=t.int32, device=self.device) if want_workers else None
+        best = t.empty(2, dtype=t.int64, device=self.device)
         if heartbeat_every is None:
-            ald_sweep_scenarios(self.h, S, arr, Q, ql, qp, rej, first, ow)
+            self.call(ald_sweep_scenarios, S, arr, Q, ql, qp, rej, first, ow, best)
         else:
             hb = np.broadcast_to(np.asarray(heartbeat_every, dtype=np.int32), (S,))
-            ald_sweep_scenarios_hb(self.h, S, arr, hb, Q, ql, qp, rej, first, ow)
-        return (rej.cpu().numpy(), first.cpu().numpy(),
-                ow.cpu().numpy().reshape(S, Q) if want_workers else None)
+            self.call(ald_sweep_scenarios_hb, S, arr, hb, Q, ql, qp, rej, first, ow, best)
+        out = (rej.cpu().numpy(), first.cpu().numpy(), ow.cpu().numpy().reshape(S, Q) if want_workers else None)
+        if want_answer:
+            b = best.cpu().numpy()
+            out = out + ((None, -1) if b[0] < 0 else (int(b[0]), int(b[1])),)
+        return out
 
     def rebalance(self, batch, want_log=False):
         """Algorithm 2 on a workloads.RebalanceBatch; returns the new workers and
@@ -409,9 +478,9 @@ class Evaluator:
         n_new = np.diff(batch.new_offsets)
         cap = int(4 * n_new.max() + int(np.max(batch.n_workers))) if want_log and P > 0 else 0
         log = t.empty(max(1, 2 * P * cap), dtype=t.int32, device=self.device) if want_log else None
-        ald_rebalance(self.h, P, batch.n_workers, models, batch.old_offsets, d32(batch.old_worker),
-                      d32(batch.old_l_pred), d32(batch.old_l_out), d32(batch.old_l_real), d32(batch.old_l_repred),
-                      batch.new_offsets, d32(batch.new_l_pred), nw, le, be, mv, cap, log, obj)
+        self.call(ald_rebalance, P, batch.n_workers, models, batch.old_offsets, d32(batch.old_worker),
+                 d32(batch.old_l_pred), d32(batch.old_l_out), d32(batch.old_l_real), d32(batch.old_l_repred),
+                 batch.new_offsets, d32(batch.new_l_pred), nw, le, be, mv, cap, log, obj)
         out = {"worker": nw.cpu().numpy(), "le": le.cpu().numpy(), "be": be.cpu().numpy(),
                "moves": mv.cpu().numpy(), "obj": obj.cpu().numpy().reshape(P, 4)}
         if want_log:
@@ -437,8 +506,10 @@ class Evaluator:
 
 
 def smallest_feasible_cluster(scenarios, rejected):
-    """Scenario with no rejection and the fewest GPUs (n_workers * gpus_per_worker),
-    lowest index on ties: returns (gpus, index) or (None, -1)."""
+    """The sweep's answer recomputed from its per-scenario rejections (a
+    cross-check of the device's out_min_gpus): the scenario with no rejection
+    and the fewest GPUs (n_workers * gpus_per_worker), lowest index on ties;
+    returns (gpus, index) or (None, -1)."""
     best, idx = None, -1
     for i, s in enumerate(scenarios):
         if int(rejected[i]) != 0:

@@ -1,6 +1,13 @@
-// Host side of libaladdin: argument validation, device memory, and the round
-// loop that drives the tile pipeline (build -> eval -> select -> commit) on the
-// caller's HIP stream.  Every entry point returns after its stream work is done.
+// Host side of libaladdin: argument validation, the layout of the caller's
+// workspace, and the round loop that drives the tile pipeline (build -> eval ->
+// select -> commit) on the caller's HIP stream.  Every entry point returns
+// after its stream work is done.
+//
+// Device memory: the library allocates none.  The caller attaches a workspace
+// (ald_set_workspace); the loaded workers' state occupies its start
+// (state_bytes), and every call lays out its own tables in the rest.  A call
+// that does not fit is refused with ALD_ESPACE before any device work, and
+// ald_workspace_needed gives the size it needed.
 #include "../../include/aladdin.h"
 #include "ald_internal.h"
 #include "ald_rebalance.h"
@@ -12,6 +19,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 using namespace ald;
@@ -19,7 +27,7 @@ using namespace ald;
 namespace {
 
 struct Arena {
-    void* mem = nullptr;  // every worker, slot and control array, carved from one allocation
+    char* mem = nullptr;  // every worker, slot and control array, carved from the workspace
     size_t mem_bytes = 0;
     State st{};
     std::vector<Scen> hscen;
@@ -28,8 +36,7 @@ struct Arena {
     int32_t T = 0;            // tile the scratch is laid out for
     int32_t target = 0;       // and the evaluation grid it aimed at
     int32_t eval_blocks = 0, sel_blocks = 0, commit_blocks = 0;
-    size_t scratch_bytes = 0;
-    void* scratch = nullptr;
+    char* scratch = nullptr;  // where the tile scratch was laid out (in the call part of the workspace)
     Scen* dscen = nullptr;
     int eval_mode = 2;    // how the pair evaluation takes the latency checks (launch_eval)
     bool use_d = false;   // some scenario checks constraint (d)
@@ -41,8 +48,6 @@ struct Arena {
 
     ~Arena()
     {
-        if (mem) (void)hipFree(mem);
-        if (scratch) (void)hipFree(scratch);
         if (hctl) (void)hipHostFree(hctl);
     }
 };
@@ -65,7 +70,7 @@ struct ald_handle {
     // second wave leaves most of the chip idle
     int32_t eval_wave[3][2] = {};
     Arena* main = nullptr;
-    Arena* sweep = nullptr;  // kept between sweeps so that its memory is reused
+    Arena* sweep = nullptr;  // the arena of the last sweep (in the call part of the workspace)
     int32_t W = 0;
     ald_model_t model{};
     int32_t max_cap = 0;
@@ -76,23 +81,21 @@ struct ald_handle {
     bool check_all = false;        // stale workers are not listed (after grouped placement): check every one
     int64_t qcount = 0;            // queries processed since the load (routes grouped placement)
     Arena* grouped = nullptr;      // scenario view of the loaded workers for grouped placement
-    int32_t* hb_dev = nullptr;         // device copy of a call's per-query heartbeats (and grouped query maps)
-    size_t hb_dev_n = 0;               // int32 entries it holds
     // App. A's router: the group sizes it routes for and the queries each group
     // received since the load (or since the sizes changed)
     std::vector<int32_t> route_sizes;
     std::vector<int64_t> route_counts;
-    void* mv_mem = nullptr;            // tables of ald_move_requests
-    size_t mv_bytes = 0;
-    int32_t* err_word = nullptr;
+    // the caller's workspace: the loaded state in [ws, ws + state_bytes), each
+    // call's own tables after it
+    char* ws = nullptr;
+    size_t ws_bytes = 0;
+    size_t state_bytes = 0;
+    size_t need = 0;  // bytes the last call refused with ALD_ESPACE needed
     int32_t prof = 0;  // kernel kinds timed (bit k = kind k)
     std::vector<Events> pending;
     std::vector<Events> pool;
     double tot_ms[5] = {0, 0, 0, 0, 0};
     int64_t launches[5] = {0, 0, 0, 0, 0};
-    // re-balancing: problem and chunk tables, and error arrays when the caller passes none
-    void* rb_mem = nullptr;
-    size_t rb_bytes = 0;
 };
 
 namespace {
@@ -194,9 +197,13 @@ struct Carver {
     }
 };
 
-// Worker and slot arrays for S scenarios.  caps[w] = request slots of worker w.
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Worker and slot arrays for S scenarios, laid out at `at` (in the caller's
+// workspace).  caps[w] = request slots of worker w.  With `at` null only the
+// size is computed (*bytes).
 int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std::vector<int32_t>& W,
-               const std::vector<int32_t>& caps, const std::vector<int32_t>& Ms)
+               const std::vector<int32_t>& caps, const std::vector<int32_t>& Ms, char* at, size_t* bytes)
 {
     a->S = (int32_t)scen.size();
     a->hscen = scen;
@@ -243,14 +250,11 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
     };
     Carver sizing{nullptr};
     carve(sizing);
-    if (sizing.off > a->mem_bytes) {
-        if (a->mem) HIPCHK(h, hipFree(a->mem));
-        a->mem = nullptr;
-        a->mem_bytes = 0;
-        HIPCHK(h, hipMalloc(&a->mem, sizing.off));
-        a->mem_bytes = sizing.off;
-    }
-    Carver placing{(char*)a->mem};
+    *bytes = align256(sizing.off);
+    if (!at) return ALD_OK;
+    a->mem = at;
+    a->mem_bytes = *bytes;
+    Carver placing{at};
     carve(placing);
     st.ctl = ctl;
     st.tinfo = ti;
@@ -289,8 +293,10 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
     return ALD_OK;
 }
 
-// Lay out the tile scratch for tile length T and fill in the grid geometry.
-int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
+// Lay out the tile scratch for tile length T at `base` (in the call part of
+// the workspace) and fill in the grid geometry; with base null only the
+// geometry and the size (*bytes) are computed.
+int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks, char* base, size_t* bytes)
 {
     // evaluation: blocks of EVAL_Q queries x wpb workers; selection: blocks of
     // SEL_THREADS queries; bit words: one per 64 queries and worker
@@ -308,8 +314,9 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
     wpb = std::min(wpb, EVAL_WPB_MAX);
     int64_t bits = 0, part = 0, qs = 0;
     int32_t eb = 0, sb = 0, cb = 0;
+    std::vector<Scen> hs = a->hscen;  // the arena changes only when the layout is placed
     for (int s = 0; s < a->S; ++s) {
-        Scen& sc = a->hscen[s];
+        Scen& sc = hs[s];
         sc.wpb = std::min(wpb, std::max(1, sc.W));
         sc.nblk = (sc.W + sc.wpb - 1) / sc.wpb;
         sc.eval_blk0 = eb;
@@ -331,20 +338,16 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks)
         sc.qsum_off = qs;
         qs += (int64_t)schunks * SEL_THREADS;
     }
+    *bytes = align256((size_t)bits * 16 + (size_t)part * sizeof(ulonglong2) + (size_t)qs * sizeof(QSum) + 1024);
+    if (!base) return ALD_OK;
+    a->hscen = hs;
     a->eval_blocks = eb;
     a->sel_blocks = sb;
     a->commit_blocks = cb;
     a->T = T;
     a->target = target_blocks;
-    const size_t need = (size_t)bits * 16 + (size_t)part * sizeof(ulonglong2) + (size_t)qs * sizeof(QSum) + 1024;
-    if (need > a->scratch_bytes) {
-        if (a->scratch) HIPCHK(h, hipFree(a->scratch));
-        a->scratch = nullptr;
-        a->scratch_bytes = 0;
-        HIPCHK(h, hipMalloc(&a->scratch, need));
-        a->scratch_bytes = need;
-    }
-    char* p = (char*)a->scratch;
+    a->scratch = base;
+    char* p = base;
     a->st.bits_feas = (uint64_t*)p;
     p += (size_t)bits * 8;
     a->st.bits_nt = (uint64_t*)p;
@@ -405,6 +408,32 @@ void prof_collect(ald_handle* h)
         HIPCHK(h, (expr));                            \
         HIPCHK(h, prof_end(h, &ev_));                 \
     } while (0)
+
+// Refuse a call that needs more workspace than is attached (before any device work).
+int need_space(ald_handle* h, size_t need)
+{
+    h->need = need;
+    return fail(h, ALD_ESPACE, "the call needs a workspace of " + std::to_string(need) + " bytes (" +
+                                   std::to_string(h->ws_bytes) + " attached)");
+}
+
+// Move every pointer of the arena that points into [from, from + n) by d bytes.
+void relocate(Arena* a, const char* from, size_t n, ptrdiff_t d)
+{
+    auto mv = [&](auto*& p) {
+        const char* c = (const char*)p;
+        if (p != nullptr && c >= from && c < from + n) p = (std::remove_reference_t<decltype(p)>)(c + d);
+    };
+    State& st = a->st;
+    mv(st.slot_base); mv(st.cap); mv(st.n); mv(st.head); mv(st.M); mv(st.S1); mv(st.S2); mv(st.hbs);
+    mv(st.built); mv(st.B); mv(st.DS); mv(st.key); mv(st.peak); mv(st.rhs); mv(st.SC); mv(st.SR);
+    mv(st.dq_max); mv(st.ntd_lo); mv(st.ntd_hi); mv(st.lthr); mv(st.ntt_lo); mv(st.ntt_hi);
+    mv(st.ntd_mask); mv(st.ntt_mask); mv(st.phi); mv(st.phi_hb); mv(st.dlim); mv(st.ntp_lo); mv(st.ntp_hi);
+    mv(st.lgn); mv(st.lge); mv(st.lgw); mv(st.lgs); mv(st.e); mv(st.s); mv(st.pms); mv(st.lbt);
+    mv(st.scen); mv(st.ctl); mv(st.tinfo); mv(st.dlist); mv(st.dcount); mv(st.qbad);
+    mv(a->dscen);
+    a->mem += d;
+}
 
 int map_dev_error(ald_handle* h, int32_t code)
 {
@@ -534,11 +563,48 @@ int ald_create(ald_handle_t* out, int device, void* hip_stream)
     h->device = device;
     h->stream = (hipStream_t)hip_stream;
     std::copy(&wave[0][0], &wave[0][0] + 6, &h->eval_wave[0][0]);
-    if (hipMalloc(&h->err_word, sizeof(int32_t)) != hipSuccess) {
-        delete h;
-        return ALD_EHIP;
-    }
     *out = h;
+    return ALD_OK;
+}
+
+int ald_set_workspace(ald_handle_t h, void* workspace, size_t bytes)
+{
+    if (!h) return ALD_EINVAL;
+    HIPCHK(h, hipSetDevice(h->device));
+    if (bytes > 0 && !workspace) return fail(h, ALD_EINVAL, "null workspace");
+    if (((uintptr_t)workspace & 255) != 0) return fail(h, ALD_EINVAL, "the workspace must be 256-byte aligned");
+    char* ws = bytes > 0 ? (char*)workspace : nullptr;
+    if (h->main) {
+        if (bytes < h->state_bytes) {
+            h->need = h->state_bytes;
+            return fail(h, ALD_ESPACE, "the loaded workers' state needs " + std::to_string(h->state_bytes) + " bytes");
+        }
+        if (ws != h->ws) {
+            if (ws < h->ws + h->state_bytes && h->ws < ws + h->state_bytes)
+                return fail(h, ALD_EINVAL, "the new workspace overlaps the loaded state");
+            // the state moves with its pointers; the call part is laid out again by the next call
+            HIPCHK(h, hipMemcpyAsync(ws, h->ws, h->state_bytes, hipMemcpyDeviceToDevice, h->stream));
+            relocate(h->main, h->ws, h->state_bytes, ws - h->ws);
+            h->main->scratch = nullptr;
+            h->main->T = 0;
+            HIPCHK(h, hipMemcpyAsync(h->main->dscen, h->main->hscen.data(), h->main->S * sizeof(Scen),
+                                     hipMemcpyHostToDevice, h->stream));
+        }
+    }
+    // the arenas of grouped placement and of the sweep lived in the call part
+    delete h->grouped;
+    h->grouped = nullptr;
+    delete h->sweep;
+    h->sweep = nullptr;
+    h->ws = ws;
+    h->ws_bytes = bytes;
+    return ALD_OK;
+}
+
+int ald_workspace_needed(ald_handle_t h, size_t* bytes)
+{
+    if (!h || !bytes) return ALD_EINVAL;
+    *bytes = h->need;
     return ALD_OK;
 }
 
@@ -550,10 +616,6 @@ int ald_destroy(ald_handle_t h)
     delete h->grouped;
     delete h->main;
     delete h->sweep;
-    (void)hipFree(h->err_word);
-    if (h->rb_mem) (void)hipFree(h->rb_mem);
-    if (h->hb_dev) (void)hipFree(h->hb_dev);
-    if (h->mv_mem) (void)hipFree(h->mv_mem);
     for (Events& e : h->pool) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
     for (Events& e : h->pending) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
     delete h;
@@ -626,22 +688,31 @@ int load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const int6
     }
     if (total * 24 > ((int64_t)64 << 30)) return fail(h, ALD_EINVAL, "worker state would exceed 64 GiB");
 
-    HIPCHK(h, hipStreamSynchronize(h->stream));
+    Arena* a = new Arena();
+    std::vector<Scen> sc(1, make_scen(*model));
+    sc[0].use_d = (res_t_dec != nullptr && model->ttft_slo != INFINITY) ? 1 : 0;
+    // the state at the start of the workspace, then the load's error word and
+    // a first tile layout
+    size_t sb = 0, lb = 0;
+    int rc = make_arena(h, a, sc, std::vector<int32_t>(1, W), caps, Ms, nullptr, &sb);
+    if (rc == ALD_OK) rc = layout_scratch(h, a, 256, 4096, nullptr, &lb);
+    if (rc != ALD_OK) { delete a; return rc; }
+    if (sb + 256 + lb > h->ws_bytes) { delete a; return need_space(h, sb + 256 + lb); }
+    // from here the previous workers are gone
     delete h->grouped;
     h->grouped = nullptr;
     delete h->main;
     h->main = nullptr;
-    Arena* a = new Arena();
-    std::vector<Scen> sc(1, make_scen(*model));
-    sc[0].use_d = (res_t_dec != nullptr && model->ttft_slo != INFINITY) ? 1 : 0;
-    int rc = make_arena(h, a, sc, std::vector<int32_t>(1, W), caps, Ms);
-    if (rc == ALD_OK) rc = layout_scratch(h, a, 256, 4096);
+    h->state_bytes = 0;
+    rc = make_arena(h, a, sc, std::vector<int32_t>(1, W), caps, Ms, h->ws, &sb);
+    if (rc == ALD_OK) rc = layout_scratch(h, a, 256, 4096, h->ws + sb + 256, &lb);
     if (rc != ALD_OK) { delete a; return rc; }
-    a->st.err_word = h->err_word;
-    HIPCHK(h, hipMemsetAsync(h->err_word, 0, sizeof(int32_t), h->stream));
+    int32_t* err_word = (int32_t*)(h->ws + sb);
+    a->st.err_word = err_word;
+    HIPCHK(h, hipMemsetAsync(err_word, 0, sizeof(int32_t), h->stream));
     HIPCHK(h, launch_ingest(a->st, W, res_offsets, res_l_in, res_l_pred, res_generated, res_t_dec, h->stream));
     int32_t dev_err = 0;
-    HIPCHK(h, hipMemcpyAsync(&dev_err, h->err_word, sizeof(int32_t), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipMemcpyAsync(&dev_err, err_word, sizeof(int32_t), hipMemcpyDeviceToHost, h->stream));
     HIPCHK(h, hipStreamSynchronize(h->stream));
     if (dev_err) {
         delete a;
@@ -663,6 +734,7 @@ int load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const int6
     HIPCHK(h, hipStreamSynchronize(h->stream));
     if (c.err) { delete a; return map_dev_error(h, c.err); }
     h->main = a;
+    h->state_bytes = sb;
     h->W = W;
     h->model = *model;
     h->max_cap = maxcap;
@@ -701,19 +773,6 @@ struct HbScope {
     Arena* a;
     ~HbScope() { a->hb_host.clear(); }
 };
-
-// Make room for n int32 entries of per-call device tables (heartbeats, query maps).
-int reserve_call_tables(ald_handle* h, size_t n)
-{
-    if (n <= h->hb_dev_n) return ALD_OK;
-    HIPCHK(h, hipStreamSynchronize(h->stream));
-    if (h->hb_dev) HIPCHK(h, hipFree(h->hb_dev));
-    h->hb_dev = nullptr;
-    h->hb_dev_n = 0;
-    HIPCHK(h, hipMalloc(&h->hb_dev, n * sizeof(int32_t)));
-    h->hb_dev_n = n;
-    return ALD_OK;
-}
 
 // One stream call: heartbeats every H processed queries, or hb_before[q]
 // (host array) decode iterations before query q.
@@ -756,20 +815,26 @@ int place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t
     if (tau_final >= ((int64_t)1 << 27) || (int64_t)h->max_cap * tau_final >= ((int64_t)1 << 27))
         return fail(h, ALD_EOVERFLOW, "too many heartbeats for the 32-bit request state");
     Arena* a = h->main;
-    HbScope hb_scope{a};
-    if (hb_before) {
-        int rc0 = reserve_call_tables(h, (size_t)Q);
-        if (rc0 != ALD_OK) return rc0;
-        HIPCHK(h, hipMemcpyAsync(h->hb_dev, hb_before, (size_t)Q * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
-        a->hb_host.assign(1, hb_before);
-    }
     int32_t T = std::min(h->tile, Q);
     if (H > 0) T = std::min(T, H);
     const int32_t wave = h->eval_wave[a->eval_mode][out_diag ? 1 : 0];
-    const int32_t* want_hb = hb_before ? h->hb_dev : nullptr;
-    if (T != a->T || wave != a->target) {
+    // the call part of the workspace: the tile scratch, then the per-query heartbeats
+    char* const call = h->ws + h->state_bytes;
+    size_t scratch_bytes = 0;
+    rc = layout_scratch(h, a, T, wave, nullptr, &scratch_bytes);
+    if (rc != ALD_OK) return rc;
+    const size_t need = h->state_bytes + scratch_bytes + (hb_before ? align256((size_t)Q * sizeof(int32_t)) : 0);
+    if (need > h->ws_bytes) return need_space(h, need);
+    HbScope hb_scope{a};
+    int32_t* hb_dev = (int32_t*)(call + scratch_bytes);
+    if (hb_before) {
+        HIPCHK(h, hipMemcpyAsync(hb_dev, hb_before, (size_t)Q * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
+        a->hb_host.assign(1, hb_before);
+    }
+    const int32_t* want_hb = hb_before ? hb_dev : nullptr;
+    if (T != a->T || wave != a->target || a->scratch != call) {
         a->hscen[0].hb = want_hb;
-        rc = layout_scratch(h, a, T, wave);  // also copies the scenario table
+        rc = layout_scratch(h, a, T, wave, call, &scratch_bytes);  // also copies the scenario table
         if (rc != ALD_OK) return rc;
     } else if (a->hscen[0].hb != want_hb) {
         a->hscen[0].hb = want_hb;
@@ -858,16 +923,11 @@ int ald_move_requests(ald_handle_t h, int32_t K, const int32_t* l_in, const int3
     }
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
     const size_t b_mw = up(mw.size() * sizeof(MoveWorker)), b_q = up(lin.size() * sizeof(int32_t));
-    const size_t need = b_mw + 2 * b_q;
-    HIPCHK(h, hipStreamSynchronize(h->stream));
-    if (need > h->mv_bytes) {
-        if (h->mv_mem) HIPCHK(h, hipFree(h->mv_mem));
-        h->mv_mem = nullptr;
-        h->mv_bytes = 0;
-        HIPCHK(h, hipMalloc(&h->mv_mem, need));
-        h->mv_bytes = need;
-    }
-    char* base = (char*)h->mv_mem;
+    // the call part of the workspace: the error word, then the tables
+    const size_t need = h->state_bytes + 256 + b_mw + 2 * b_q;
+    if (need > h->ws_bytes) return need_space(h, need);
+    int32_t* err_word = (int32_t*)(h->ws + h->state_bytes);
+    char* base = h->ws + h->state_bytes + 256;
     MoveArgs a{};
     a.mw = (const MoveWorker*)base;
     a.nw = (int32_t)mw.size();
@@ -875,18 +935,18 @@ int ald_move_requests(ald_handle_t h, int32_t K, const int32_t* l_in, const int3
     a.hb = h->hb_index;
     a.lin = (const int32_t*)(base + b_mw);
     a.lpred = (const int32_t*)(base + b_mw + b_q);
-    a.err = h->err_word;
+    a.err = err_word;
     HIPCHK(h, hipMemcpyAsync(base, mw.data(), mw.size() * sizeof(MoveWorker), hipMemcpyHostToDevice, h->stream));
     HIPCHK(h, hipMemcpyAsync(base + b_mw, lin.data(), lin.size() * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
     HIPCHK(h, hipMemcpyAsync(base + b_mw + b_q, lp.data(), lp.size() * sizeof(int32_t), hipMemcpyHostToDevice,
                              h->stream));
-    HIPCHK(h, hipMemsetAsync(h->err_word, 0, sizeof(int32_t), h->stream));
+    HIPCHK(h, hipMemsetAsync(err_word, 0, sizeof(int32_t), h->stream));
     a.apply = 0;  // check every worker first: a move that cannot be applied changes nothing
     HIPCHK(h, launch_move(h->main->st, a, h->stream));
     a.apply = 1;
     HIPCHK(h, launch_move(h->main->st, a, h->stream));
     int32_t dev_err = 0;
-    HIPCHK(h, hipMemcpyAsync(&dev_err, h->err_word, sizeof(int32_t), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipMemcpyAsync(&dev_err, err_word, sizeof(int32_t), hipMemcpyDeviceToHost, h->stream));
     HIPCHK(h, hipStreamSynchronize(h->stream));
     if (dev_err == DEV_ESLOTS) return fail(h, ALD_ESLOTS, "a worker has no request slot left for a moved request");
     if (dev_err != 0)
@@ -958,8 +1018,9 @@ void route_groups(const std::vector<int32_t>& N, std::vector<int64_t>& counts, i
 }
 
 // A scenario view of the loaded workers, one scenario per group: the worker
-// arrays are the loaded arena's, the control and scratch arrays its own.
-int grouped_view(ald_handle* h, int32_t G, const int32_t* sizes)
+// arrays are the loaded arena's, the control and scratch arrays its own, laid
+// out at `base` (with base null only the size, *bytes, is computed).
+int grouped_view(ald_handle* h, int32_t G, const int32_t* sizes, char* base, size_t* bytes)
 {
     Arena* m = h->main;
     if (!h->grouped) h->grouped = new Arena();
@@ -989,14 +1050,11 @@ int grouped_view(ald_handle* h, int32_t G, const int32_t* sizes)
         k.take(&ctl, G); k.take(&ti, G); k.take(&dscen, G); k.take(&dlist, (size_t)G * MAX_DIRTY); k.take(&dcount, G);
     };
     carve(c);
-    if (c.off > a.mem_bytes) {
-        if (a.mem) HIPCHK(h, hipFree(a.mem));
-        a.mem = nullptr;
-        a.mem_bytes = 0;
-        HIPCHK(h, hipMalloc(&a.mem, c.off));
-        a.mem_bytes = c.off;
-    }
-    Carver k{(char*)a.mem};
+    *bytes = align256(c.off);
+    if (!base) return ALD_OK;
+    a.mem = base;
+    a.mem_bytes = *bytes;
+    Carver k{base};
     carve(k);
     a.dscen = dscen;
     a.st.scen = dscen;
@@ -1075,22 +1133,33 @@ int ald_place_grouped(ald_handle_t h, int32_t G, const int32_t* group_workers, i
             fill[g] += 1;
         }
     }
-    HIPCHK(h, hipStreamSynchronize(h->stream));
-    int rc = grouped_view(h, G, group_workers);
+    // the call part of the workspace: the groups' control arrays, the query
+    // maps and heartbeat counts, then the tile scratch
+    int32_t qmax = 1;
+    for (int32_t g = 0; g < G; ++g) qmax = std::max(qmax, off[g + 1] - off[g]);
+    const int32_t T = std::min(h->tile, qmax);
+    const int32_t wave = h->eval_wave[h->main->eval_mode][out_diag ? 1 : 0];
+    size_t vb = 0, sbytes = 0;
+    int rc = grouped_view(h, G, group_workers, nullptr, &vb);
+    if (rc == ALD_OK) rc = layout_scratch(h, h->grouped, T, wave, nullptr, &sbytes);
     if (rc != ALD_OK) return rc;
-    rc = reserve_call_tables(h, 2 * (size_t)Q);
+    const size_t tb = align256(2 * (size_t)Q * sizeof(int32_t));
+    const size_t need = h->state_bytes + vb + tb + sbytes;
+    if (need > h->ws_bytes) return need_space(h, need);
+    char* const call = h->ws + h->state_bytes;
+    rc = grouped_view(h, G, group_workers, call, &vb);
     if (rc != ALD_OK) return rc;
+    int32_t* const dtab = (int32_t*)(call + vb);
     Arena& a = *h->grouped;
     HbScope hb_scope{&a};
-    HIPCHK(h, hipMemcpyAsync(h->hb_dev, tab.data(), 2 * (size_t)Q * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
+    HIPCHK(h, hipMemcpyAsync(dtab, tab.data(), 2 * (size_t)Q * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
     std::vector<Ctl> c(G);
-    int32_t qmax = 1;
     if (H > 0) a.hb_host.resize(G);
     for (int32_t g = 0; g < G; ++g) {
         Scen& sc = a.hscen[g];
         const int32_t n = off[g + 1] - off[g];
-        sc.qmap = h->hb_dev + off[g];
-        sc.hb = H > 0 ? h->hb_dev + Q + off[g] : nullptr;
+        sc.qmap = dtab + off[g];
+        sc.hb = H > 0 ? dtab + Q + off[g] : nullptr;
         sc.out_off = 0;
         sc.out_add = sc.wbase;
         Ctl& x = c[g];
@@ -1110,11 +1179,9 @@ int ald_place_grouped(ald_handle_t h, int32_t G, const int32_t* group_workers, i
             }
             x.hb_next = next_hb(hg, 0, n);
         }
-        qmax = std::max(qmax, n);
     }
-    const int32_t T = std::min(h->tile, qmax);
     for (Ctl& x : c) x.T = T;
-    rc = layout_scratch(h, &a, T, h->eval_wave[a.eval_mode][out_diag ? 1 : 0]);  // also copies the scenario table
+    rc = layout_scratch(h, &a, T, wave, call + vb + tb, &sbytes);  // also copies the scenario table
     if (rc != ALD_OK) return rc;
     std::vector<TileInfo> ti(G);
     for (auto& t : ti) { t = TileInfo{}; t.first_pc[0] = t.first_pc[1] = INT32_MAX; }
@@ -1124,7 +1191,7 @@ int ald_place_grouped(ald_handle_t h, int32_t G, const int32_t* group_workers, i
     a.st.q_lpred = q_l_pred;
     a.st.out_worker = out_worker;
     a.st.out_diag = (Diag*)out_diag;
-    a.st.err_word = h->err_word;
+    a.st.err_word = nullptr;
     HIPCHK(h, launch_query_stats(q_l_in, q_l_pred, Q, a.st.ctl, G, h->stream));
     rc = run_rounds(h, &a, H > 0, 0, c);
     if (rc != ALD_OK) return rc;
@@ -1166,8 +1233,8 @@ RbRho rb_rho(double k2, double c2)
 }
 
 // Algorithm 2 over P problems.  noalloc: the tables live in the library's
-// fixed device array (rb_static_ptr) and the caller passes the error arrays,
-// so nothing is allocated; otherwise they live in memory the handle keeps.
+// fixed device array (rb_static_ptr) and the caller passes the error arrays;
+// otherwise they live in the call part of the caller's workspace.
 int rebalance_impl(ald_handle_t h, int32_t P, const int32_t* n_workers, const ald_model_t* models,
                   const int64_t* old_offsets, const int32_t* old_worker, const int32_t* old_l_pred,
                   const int32_t* old_l_out, const int32_t* old_l_real, const int32_t* old_l_repred,
@@ -1216,7 +1283,7 @@ int rebalance_impl(ald_handle_t h, int32_t P, const int32_t* n_workers, const al
     const size_t b_err = own_err ? up(wtot * sizeof(int64_t)) : 0;
     const size_t need = b_prob + b_chunk + 2 * b_err;
     char* base = nullptr;
-    int32_t* err_word = h->err_word;
+    int32_t* err_word = nullptr;
     if (noalloc) {
         if (own_err) return fail(h, ALD_EINVAL, "the allocation-free call needs out_le and out_be");
         if (P > RB_STATIC_P || chunks.size() + 1 > (size_t)RB_STATIC_CHUNKS)
@@ -1229,15 +1296,11 @@ int rebalance_impl(ald_handle_t h, int32_t P, const int32_t* n_workers, const al
         base = mem;
         err_word = (int32_t*)(mem + RB_STATIC_TABLES);
     } else {
-        HIPCHK(h, hipStreamSynchronize(h->stream));  // the tables may be in use by an earlier call
-        if (need > h->rb_bytes) {
-            if (h->rb_mem) HIPCHK(h, hipFree(h->rb_mem));
-            h->rb_mem = nullptr;
-            h->rb_bytes = 0;
-            HIPCHK(h, hipMalloc(&h->rb_mem, need));
-            h->rb_bytes = need;
-        }
-        base = (char*)h->rb_mem;
+        // the call part of the workspace: the error word, then the tables
+        const size_t total = h->state_bytes + 256 + need;
+        if (total > h->ws_bytes) return need_space(h, total);
+        err_word = (int32_t*)(h->ws + h->state_bytes);
+        base = h->ws + h->state_bytes + 256;
     }
     RbArgs a{};
     a.prob = (const RbProblem*)base;
@@ -1284,13 +1347,16 @@ namespace {
 
 // The sweep, with a heartbeat period per scenario (H null: none).
 int sweep(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* H, int32_t Q, const int32_t* q_l_in,
-          const int32_t* q_l_pred, int32_t* out_rejected, int32_t* out_first_reject, int32_t* out_worker)
+          const int32_t* q_l_pred, int32_t* out_rejected, int32_t* out_first_reject, int32_t* out_worker,
+          int64_t* out_min_gpus, size_t* size_only = nullptr)
 {
     if (!h) return ALD_EINVAL;
     HIPCHK(h, hipSetDevice(h->device));
     if (S <= 0 || Q < 0) return fail(h, ALD_EINVAL, "S must be >= 1 and Q >= 0");
-    if (!scen || !out_rejected || !out_first_reject) return fail(h, ALD_EINVAL, "null argument");
-    if (Q > 0 && (!q_l_in || !q_l_pred)) return fail(h, ALD_EINVAL, "null query array");
+    if (S >= (1 << 24)) return fail(h, ALD_EINVAL, "at most 2^24 - 1 scenarios");
+    if (!scen) return fail(h, ALD_EINVAL, "null argument");
+    if (!size_only && (!out_rejected || !out_first_reject)) return fail(h, ALD_EINVAL, "null argument");
+    if (!size_only && Q > 0 && (!q_l_in || !q_l_pred)) return fail(h, ALD_EINVAL, "null query array");
     bool any_hb = false;
     for (int32_t s = 0; s < S && H; ++s) {
         if (H[s] < 0) return fail(h, ALD_EINVAL, "heartbeat_every must be >= 0");
@@ -1301,6 +1367,8 @@ int sweep(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* 
     int64_t NW = 0, slots = 0;
     for (int s = 0; s < S; ++s) {
         if (scen[s].n_workers < 1) return fail(h, ALD_EINVAL, "scenario with no workers");
+        if (scen[s].gpus_per_worker < 1 || scen[s].gpus_per_worker > 256)
+            return fail(h, ALD_EINVAL, "gpus_per_worker must lie in [1, 256]");
         if (scen[s].kv_capacity < 1) return fail(h, ALD_EINVAL, "kv_capacity must be >= 1");
         if (scen[s].kv_capacity > ((int64_t)1 << 30)) return fail(h, ALD_EOVERFLOW, "kv_capacity above 2^30 tokens");
         std::string why = check_model(scen[s].model);
@@ -1323,6 +1391,7 @@ int sweep(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* 
     if (slots * 24 + NW * (int64_t)LB_MAX * 2 > ((int64_t)128 << 30)) return fail(h, ALD_EINVAL, "sweep state would exceed 128 GiB");
     for (int s = 0; s < S; ++s) {
         sc[s] = make_scen(scen[s].model);
+        sc[s].gpw = scen[s].gpus_per_worker;
         W[s] = scen[s].n_workers;
         int64_t b = batch_bound(scen[s].model);
         int32_t cap = (int32_t)((b < 0 ? (int64_t)Q : std::min<int64_t>(Q, b)) + 1);
@@ -1331,13 +1400,23 @@ int sweep(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* 
             Ms.push_back((int32_t)scen[s].kv_capacity);
         }
     }
-    HIPCHK(h, hipStreamSynchronize(h->stream));
+    // the call part of the workspace: every scenario's workers, then the tile scratch
     if (!h->sweep) h->sweep = new Arena();
     Arena& a = *h->sweep;
-    int rc = make_arena(h, &a, sc, W, caps, Ms);
-    if (rc != ALD_OK) return rc;
     const int32_t T = std::max(1, std::min(h->tile, Q));
-    rc = layout_scratch(h, &a, T, 16384);
+    size_t ab = 0, sbytes = 0;
+    int rc = make_arena(h, &a, sc, W, caps, Ms, nullptr, &ab);
+    if (rc == ALD_OK) rc = layout_scratch(h, &a, T, 16384, nullptr, &sbytes);
+    if (rc != ALD_OK) return rc;
+    const size_t need = h->state_bytes + ab + sbytes;
+    if (size_only) {
+        *size_only = ab + sbytes;
+        return ALD_OK;
+    }
+    if (need > h->ws_bytes) return need_space(h, need);
+    char* const call = h->ws + h->state_bytes;
+    rc = make_arena(h, &a, sc, W, caps, Ms, call, &ab);
+    if (rc == ALD_OK) rc = layout_scratch(h, &a, T, 16384, call + ab, &sbytes);
     if (rc != ALD_OK) return rc;
     std::vector<Ctl> c(S);
     for (int s = 0; s < S; ++s) {
@@ -1356,7 +1435,7 @@ int sweep(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* 
     a.st.q_lpred = q_l_pred;
     a.st.out_worker = out_worker;
     a.st.out_diag = nullptr;
-    a.st.err_word = h->err_word;
+    a.st.err_word = nullptr;
     for (int s = 0; s < S; ++s) a.hscen[s].out_off = (int64_t)s * Q;
     HIPCHK(h, hipMemcpyAsync(a.dscen, a.hscen.data(), S * sizeof(Scen), hipMemcpyHostToDevice, h->stream));
     if (Q > 0) {
@@ -1364,7 +1443,7 @@ int sweep(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* 
         rc = run_rounds(h, &a, any_hb, 0, c);
         if (rc != ALD_OK) return rc;
     }
-    HIPCHK(h, launch_sweep_outputs(a.st, out_rejected, out_first_reject, h->stream));
+    HIPCHK(h, launch_sweep_outputs(a.st, out_rejected, out_first_reject, out_min_gpus, h->stream));
     HIPCHK(h, hipStreamSynchronize(h->stream));
     return ALD_OK;
 }
@@ -1375,17 +1454,60 @@ extern "C" {
 
 int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, int32_t Q, const int32_t* q_l_in,
                         const int32_t* q_l_pred, int32_t* out_rejected, int32_t* out_first_reject,
-                        int32_t* out_worker)
+                        int32_t* out_worker, int64_t* out_min_gpus)
 {
-    return sweep(h, S, scen, nullptr, Q, q_l_in, q_l_pred, out_rejected, out_first_reject, out_worker);
+    return sweep(h, S, scen, nullptr, Q, q_l_in, q_l_pred, out_rejected, out_first_reject, out_worker, out_min_gpus);
+}
+
+int ald_sweep_workspace_size(ald_handle_t h, int32_t S, const ald_scenario_t* scen, int32_t Q, size_t* bytes)
+{
+    if (!h || !bytes) return ALD_EINVAL;
+    return sweep(h, S, scen, nullptr, Q, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, bytes);
+}
+
+int ald_workspace_size(ald_handle_t h, int32_t W, int64_t n_resident, const ald_model_t* model,
+                       int32_t slots_per_worker, int32_t with_history, int32_t Q, size_t* bytes)
+{
+    if (!h || !bytes || !model) return ALD_EINVAL;
+    if (W <= 0 || n_resident < 0 || slots_per_worker < 0 || Q < 0) return fail(h, ALD_EINVAL, "bad size");
+    std::string why = check_model(*model);
+    if (!why.empty()) return fail(h, ALD_EINVAL, why);
+    int64_t bound = slots_per_worker > 0 ? slots_per_worker : batch_bound(*model);
+    if (bound < 0) return fail(h, ALD_EINVAL, "c2 == 0 leaves the batch size unbounded: pass slots_per_worker");
+    // the state's size depends on the total of the workers' slot ranges, at
+    // most n_resident + W (bound + 2), which these slot counts add up to
+    std::vector<int32_t> caps(W, (int32_t)std::min<int64_t>(bound + 1, INT32_MAX)), Ms(W, 1);
+    const int64_t extra = std::min<int64_t>(n_resident, INT32_MAX - caps[0]);
+    caps[0] += (int32_t)extra;
+    Arena a;
+    std::vector<Scen> sc(1, make_scen(*model));
+    sc[0].use_d = (with_history && model->ttft_slo != INFINITY) ? 1 : 0;
+    size_t sb = 0, lb = 0, most = 0;
+    int rc = make_arena(h, &a, sc, std::vector<int32_t>(1, W), caps, Ms, nullptr, &sb);
+    if (rc == ALD_OK) rc = layout_scratch(h, &a, 256, 4096, nullptr, &lb);
+    if (rc != ALD_OK) return rc;
+    most = 256 + lb;
+    // a placement call of up to Q queries, for any evaluation variant the
+    // model can take, with per-query heartbeats
+    const int32_t T = std::max(1, std::min(h->tile, Q));
+    for (int m = 0; m < 3; ++m)
+        for (int x = 0; x < 2; ++x) {
+            size_t tb = 0;
+            rc = layout_scratch(h, &a, T, h->eval_wave[m][x], nullptr, &tb);
+            if (rc != ALD_OK) return rc;
+            most = std::max(most, tb + align256((size_t)Q * sizeof(int32_t)));
+        }
+    *bytes = sb + most;
+    return ALD_OK;
 }
 
 int ald_sweep_scenarios_hb(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* heartbeat_every,
                            int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred, int32_t* out_rejected,
-                           int32_t* out_first_reject, int32_t* out_worker)
+                           int32_t* out_first_reject, int32_t* out_worker, int64_t* out_min_gpus)
 {
     if (h && !heartbeat_every) return fail(h, ALD_EINVAL, "null heartbeat_every");
-    return sweep(h, S, scen, heartbeat_every, Q, q_l_in, q_l_pred, out_rejected, out_first_reject, out_worker);
+    return sweep(h, S, scen, heartbeat_every, Q, q_l_in, q_l_pred, out_rejected, out_first_reject, out_worker,
+                 out_min_gpus);
 }
 
 int ald_rebalance(ald_handle_t h, int32_t P, const int32_t* n_workers, const ald_model_t* models,

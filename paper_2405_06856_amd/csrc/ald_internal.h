@@ -83,7 +83,8 @@ struct Scen {
     // the next i > start with hb[i] > 0.
     const int32_t* qmap;
     const int32_t* hb;
-    int32_t out_add, pad;
+    int32_t out_add;
+    int32_t gpw;        // GPUs per worker (a sweep's answer counts n_workers * gpw GPUs)
 };
 
 __host__ __device__ inline int64_t q_at(const Scen& sc, int32_t i) { return sc.qmap ? (int64_t)sc.qmap[i] : (int64_t)i; }
@@ -256,6 +257,9 @@ hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* ti
                         hipStream_t stream);
 hipError_t launch_summary(const State& st, int32_t W, int32_t* B, int64_t* sc, int64_t* sr, int64_t* peak,
                           hipStream_t stream);
-hipError_t launch_sweep_outputs(const State& st, int32_t* rejected, int32_t* first_reject, hipStream_t stream);
+// rejected / first rejected query per scenario, and (min_gpus non-null) the
+// scenario with no rejection and the fewest GPUs: {GPUs, scenario} or {-1, -1}
+hipError_t launch_sweep_outputs(const State& st, int32_t* rejected, int32_t* first_reject, int64_t* min_gpus,
+                                hipStream_t stream);
 
 }  // namespace ald

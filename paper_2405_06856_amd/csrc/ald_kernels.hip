@@ -1053,6 +1053,28 @@ __global__ void k_sweep_outputs(State st, int32_t* rejected, int32_t* first_reje
     first_reject[s] = f == INT32_MAX ? -1 : f;
 }
 
+// The sweep's answer (Sec. 4.4, Sec. 6.4: the fewest GPUs that serve the
+// stream with no violation): among scenarios with no rejection, the smallest
+// n_workers * GPUs per worker, ties to the lowest scenario index.  One block;
+// the (GPUs, index) pairs are ordered as one int64 key.
+__global__ __launch_bounds__(256) void k_sweep_best(State st, int64_t* min_gpus)
+{
+    __shared__ int64_t red[4];
+    int64_t best = INT64_MAX;
+    for (int s = threadIdx.x; s < st.S; s += 256) {
+        const Scen sc = st.scen[s];
+        if (st.ctl[s].n_rej != 0 || st.ctl[s].err != 0) continue;
+        // GPUs < 2^38 and s < 2^24 (checked on the host): the key fits in 62 bits
+        const int64_t key = ((int64_t)sc.W * sc.gpw << 24) + s;
+        best = key < best ? key : best;
+    }
+    best = block_reduce<256>(best, INT64_MAX, OpMin(), red);
+    if (threadIdx.x == 0) {
+        min_gpus[0] = best == INT64_MAX ? -1 : best >> 24;
+        min_gpus[1] = best == INT64_MAX ? -1 : (best & ((1 << 24) - 1));
+    }
+}
+
 // ---------------------------------------------------------------------------------------------
 hipError_t launch_ingest(const State& st, int32_t W, const int64_t* res_off, const int32_t* lin,
                          const int32_t* lpred, const int32_t* gen, const double* tdec, hipStream_t stream)
@@ -1125,10 +1147,14 @@ hipError_t launch_summary(const State& st, int32_t W, int32_t* B, int64_t* sc, i
     return hipGetLastError();
 }
 
-hipError_t launch_sweep_outputs(const State& st, int32_t* rejected, int32_t* first_reject, hipStream_t stream)
+hipError_t launch_sweep_outputs(const State& st, int32_t* rejected, int32_t* first_reject, int64_t* min_gpus,
+                                hipStream_t stream)
 {
     hipLaunchKernelGGL(k_sweep_outputs, dim3((st.S + 255) / 256), dim3(256), 0, stream, st, rejected,
                        first_reject);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || min_gpus == nullptr) return e;
+    hipLaunchKernelGGL(k_sweep_best, dim3(1), dim3(256), 0, stream, st, min_gpus);
     return hipGetLastError();
 }
 

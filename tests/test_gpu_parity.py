@@ -476,12 +476,13 @@ def test_sweep_small_matches_oracle(aladdin):
     s = wl.make_sweep("mini", 9, Q=700, worker_counts=(2, 3, 5, 16), gpu_counts=(1, 2), base_capacity=6000,
                       model=wl.BASE_MODEL, in_dist=wl.MID_IN, out_dist=wl.MID_OUT, rate=None)
     ev = aladdin.Evaluator(0, tile=128)
-    rej, first, workers = ev.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True)
+    rej, first, workers, best = ev.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True, want_answer=True)
     ev.close()
     orej, ofirst, oworkers = ref.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True)
     assert np.array_equal(workers, oworkers)
     assert np.array_equal(rej, orej)
     assert np.array_equal(first, ofirst)
+    assert best == ref.min_gpus(s.scenarios, orej)
 
 
 @pytest.mark.parametrize("tile", [64, 1024])
@@ -567,10 +568,11 @@ def test_sweep_full_size(aladdin):
     say("sweep: 256 scenarios x 16384 queries")
     g = json.load(open(os.path.join(GOLDEN, "sweep_oracle.json")))
     ev = aladdin.Evaluator(0, tile=1024)
-    rej, first, workers = ev.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True)
+    rej, first, workers, best = ev.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True, want_answer=True)
     ev.close()
     assert list(rej) == g["rejected"]
     assert list(first) == g["first_reject"]
     assert _digest(workers.astype(np.int32)) == g["sha256"]["worker"]
-    gpus, idx = aladdin.smallest_feasible_cluster(s.scenarios, rej)
-    assert (gpus, idx) == (g["min_gpus"], g["min_gpus_scenario"])
+    # the answer, computed on the device, equals the oracle's
+    assert best == (g["min_gpus"], g["min_gpus_scenario"])
+    assert aladdin.smallest_feasible_cluster(s.scenarios, rej) == best

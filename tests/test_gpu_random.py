@@ -102,9 +102,10 @@ def test_random_sweep_matches_oracle(aladdin, seed):
     print("random sweep", seed, "S", len(scen), "W", [s.n_workers for s in scen], "Q", q_in.size, "tile", tile,
           flush=True)
     ev = aladdin.Evaluator(0, tile=tile)
-    rej, first, workers = ev.sweep(scen, q_in, q_pred, want_workers=True, heartbeat_every=H)
+    rej, first, workers, best = ev.sweep(scen, q_in, q_pred, want_workers=True, heartbeat_every=H, want_answer=True)
     ev.close()
     orej, ofirst, oworkers = ref.sweep(scen, q_in, q_pred, want_workers=True, heartbeat_every=H)
     assert np.array_equal(workers, oworkers), np.argwhere(workers != oworkers)[:5]
     assert np.array_equal(rej, orej)
     assert np.array_equal(first, ofirst)
+    assert best == ref.min_gpus(scen, orej)

@@ -48,6 +48,8 @@ def test_noalloc_matches_allocating_entry_point():
     from paper_2405_06856_amd import aladdin
     dev = torch.device("cuda", 0)
     h = aladdin.ald_create(0, torch.cuda.current_stream(dev).cuda_stream)
+    ws = torch.empty(64 << 20, dtype=torch.uint8, device=dev)  # ald_rebalance's tables
+    aladdin.ald_set_workspace(h, ws)
     try:
         big = wl.make_rebalance("noalloc big", 91, 24, 48, 20, 600, sigma_err=0.7)
         small = wl.make_rebalance("noalloc small", 92, 3, 9, 6, 40, sigma_err=0.6)
