@@ -4,10 +4,12 @@ A step is one pass of the placement path over the large workload (512 workers
 with 512 resident requests each, 65536 arriving queries): every (query, worker)
 pair is evaluated (KV peak, decode and TTFT checks), each query is resolved by
 Algorithm 1 and committed in arrival order, diagnostics included.  Inputs and
-worker state are resident in HBM before the timed region.  The same line also
-reports the scaling sweep (256 cluster configurations x 16384 queries) as
-sweeps per second, the roofline position of the pair-evaluation kernel, and the
-CPU oracle timed on a bounded sample on this host.
+worker state are resident in HBM before the timed region.  The same JSON line
+reports the roofline position of the pair-evaluation kernel, the tiny, medium
+and long workloads (the long one heartbeats, rebuilds and commits), the scaling
+sweep (256 cluster configurations x 16384 queries, with its answer), Algorithm
+2, the smallest cluster per arrival rate (Eq. 7), and the CPU oracle timed on a
+bounded sample on this host.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -18,19 +20,28 @@ import gc
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+METRIC = "query×worker placement evals/sec + scenario sweeps/sec; % of HBM roofline"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
+# VALU issue: 256 compute units x 4 SIMDs x 16 lanes per clock x 2.4 GHz, in
+# 10^12 32-bit lane operations per second (a wave64 instruction takes 4 clocks)
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+# 32-bit operations the pair evaluator needs per (query, worker) pair, counted
+# from its formula: breakpoint slot 2, KV peak with the query 8, capacity test 1,
+# decode test 4, TTFT test 1, feasibility 2, smallest-excess bookkeeping 4
+OPS_PER_PAIR = 22
 TILE_LARGE = 65536
 
 
-def algorithmic_bytes_per_pair(residents_per_worker: int) -> int:
-    # the two int32 columns the breakpoint rule depends on (remaining length and
-    # context of every resident) plus five int64 worker aggregates
+def scan_equivalent_bytes_per_pair(residents_per_worker: int) -> int:
+    """Bytes an O(R) scan of the worker's state would read per pair: the two
+    int32 columns the breakpoint rule depends on plus five int64 aggregates."""
     return 8 * residents_per_worker + 40
 
 
@@ -61,6 +72,24 @@ def measured_traffic():
     return doc.get("bytes_per_launch")
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def host_cores() -> int:
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
 def cpu_baseline(trace, budget_s: float = 12.0, max_q: int = 8192):
     """The oracle as it stands, one thread, on the first n queries of the stream
     (n doubled until one run takes at least half the budget)."""
@@ -75,9 +104,72 @@ def cpu_baseline(trace, budget_s: float = 12.0, max_q: int = 8192):
         if dt >= budget_s / 2 or n >= max_q:
             break
         n = min(max_q, 2 * n)
+    nc = host_cores()
     return {"value": n * trace.n_workers / dt, "unit": "pair-evals/s", "cores": 1, "kind": "oracle",
-            "sample": "first %d of %d queries x %d workers of the large workload, single thread, "
-                      "%.1f s" % (n, trace.n_queries, trace.n_workers, dt)}
+            "host_cores": nc, "cpu_model": cpu_model(),
+            "sample": "first %d of %d queries x %d workers of the large workload, 1 core of %d (%s), %.1f s"
+                      % (n, trace.n_queries, trace.n_workers, nc, cpu_model(), dt)}
+
+
+def no_gc(fn):
+    """Run fn with the Python garbage collector off (a collector pass over
+    torch's object graph takes tens of ms and is not the library's time)."""
+    gc.collect()
+    gc.disable()
+    try:
+        return fn()
+    finally:
+        gc.enable()
+
+
+def time_workload(name: str, runs: int, tile: int = 4096):
+    """Place a whole workload `runs` times from a fresh load (not timed), one
+    warm-up first: wall time of the placement call (it returns when its stream
+    work is done), and per-kernel device time from the library's events."""
+    import torch
+
+    from paper_2405_06856_amd import aladdin
+    from paper_2405_06856_amd import workloads as wl
+    t = wl.make_config(name)
+    ev = aladdin.Evaluator(0, tile=tile)
+    dev = ev.device
+    ql = torch.as_tensor(t.q_l_in, dtype=torch.int32).to(dev)
+    qp = torch.as_tensor(t.q_l_pred, dtype=torch.int32).to(dev)
+    Q = t.n_queries
+    out = torch.empty(Q, dtype=torch.int32, device=dev)
+    dg = torch.empty(Q * aladdin.DIAG_DTYPE.itemsize, dtype=torch.uint8, device=dev)
+    walls = []
+    kinds = ("build", "eval", "select", "commit")
+    kern = {k: 0.0 for k in kinds}
+    rounds = 0
+    for r in range(runs + 1):
+        ev.load_trace(t)
+        torch.cuda.synchronize()
+        if r > 0:
+            ev.profiling(True, kinds=kinds)
+
+        def one():
+            t0 = time.perf_counter()
+            ev.place_device(ql, qp, t.heartbeat_every, diag=True, out=out, diag_out=dg)
+            return time.perf_counter() - t0
+
+        dt = no_gc(one)
+        if r > 0:
+            walls.append(dt)
+            for k in kinds:
+                kern[k] += ev.kernel_time(k)[0]
+            rounds += ev.kernel_time("commit")[1]
+            ev.profiling(False)
+    placed = int((out >= 0).sum().item())
+    ev.close()
+    med = statistics.median(walls)
+    pairs = Q * t.n_workers
+    T = min(tile, t.heartbeat_every) if t.heartbeat_every else tile
+    return {"workers": t.n_workers, "residents_per_worker": int(t.res_offsets[1] - t.res_offsets[0]),
+            "queries": Q, "heartbeat_every": t.heartbeat_every, "tile": tile, "pairs": pairs, "placed": placed,
+            "runs": runs, "ms_median": med * 1e3, "ms_min": min(walls) * 1e3, "pair_evals_per_s": pairs / med,
+            "kernels_ms_per_run": {k: v / runs for k, v in kern.items()}, "rounds_per_run": rounds / runs,
+            "tiles_per_run": -(-Q // T)}
 
 
 def time_sweep(steps: int):
@@ -87,25 +179,25 @@ def time_sweep(steps: int):
     from paper_2405_06856_amd import workloads as wl
     sw = wl.make_config("sweep")
     sev = aladdin.Evaluator(0, tile=1024)
-    for _ in range(2):  # warm-up
-        rej, first, _ = sev.sweep(sw.scenarios, sw.q_l_in, sw.q_l_pred)
+    for _ in range(2):  # warm-up (and the workspace grows to its size)
+        sev.sweep(sw.scenarios, sw.q_l_in, sw.q_l_pred, want_answer=True)
     torch.cuda.synchronize()
-    # a Python garbage-collection pass inside the loop (tens of ms over torch's
-    # object graph) is not the library's time
-    gc.collect()
-    gc.disable()
-    try:
-        t0 = time.perf_counter()
+    walls = []
+
+    def run():
+        res = None
         for _ in range(steps):
-            rej, first, _ = sev.sweep(sw.scenarios, sw.q_l_in, sw.q_l_pred)
-        torch.cuda.synchronize()
-        sweep_s = (time.perf_counter() - t0) / steps
-    finally:
-        gc.enable()
-    gpus, idx = aladdin.smallest_feasible_cluster(sw.scenarios, rej)
+            t0 = time.perf_counter()
+            res = sev.sweep(sw.scenarios, sw.q_l_in, sw.q_l_pred, want_answer=True)
+            walls.append(time.perf_counter() - t0)
+        return res
+
+    rej, first, _, (gpus, idx) = no_gc(run)
     sev.close()
-    return {"sweeps_per_s": 1.0 / sweep_s, "ms_per_sweep": sweep_s * 1e3, "scenarios": len(sw.scenarios),
-            "queries": sw.n_queries, "min_total_gpus": gpus, "min_gpus_scenario": idx}
+    med = statistics.median(walls)
+    return {"sweeps_per_s": 1.0 / med, "ms_per_sweep": med * 1e3, "ms_min": min(walls) * 1e3, "runs": steps,
+            "scenarios": len(sw.scenarios), "queries": sw.n_queries, "min_total_gpus": gpus,
+            "min_gpus_scenario": idx, "answer_from": "device (ald_sweep_scenarios out_min_gpus)"}
 
 
 def scaling_over_rates(rates=(100.0, 200.0, 300.0, 400.0, 500.0), gpus_per_worker: int = 1):
@@ -155,74 +247,48 @@ def time_rebalance(steps: int, oracle_problems: int = 0):
     def call():
         nw.copy_(nw0)
         ev.call(aladdin.ald_rebalance, b.P, b.n_workers, models, b.old_offsets, *old, b.new_offsets, nl, nw,
-                              le, be, mv, 0, None, obj)
+                le, be, mv, 0, None, obj)
 
     for _ in range(2):
         call()
     ev.profiling(True, kinds=("rebalance",))
     torch.cuda.synchronize()
-    gc.collect()
-    gc.disable()
-    try:
-        t0 = time.perf_counter()
+    walls = []
+
+    def run():
         for _ in range(steps):
+            t0 = time.perf_counter()
             call()
-        torch.cuda.synchronize()
-        dt = (time.perf_counter() - t0) / steps
-    finally:
-        gc.enable()
+            walls.append(time.perf_counter() - t0)
+
+    no_gc(run)
     k_ms, k_n = ev.kernel_time("rebalance")
     moves = int(mv.sum().item())
     ev.close()
-    out = {"problems_per_s": b.P / dt, "ms_per_call": dt * 1e3, "kernel_ms_per_call": k_ms / max(k_n, 1),
-           "problems": b.P, "workers": Wt, "ongoing": int(b.old_offsets[-1]), "new": int(b.new_offsets[-1]),
-           "moves": moves}
+    med = statistics.median(walls)
+    out = {"problems_per_s": b.P / med, "ms_per_call": med * 1e3, "ms_min": min(walls) * 1e3,
+           "kernel_ms_per_call": k_ms / max(k_n, 1), "problems": b.P, "workers": Wt,
+           "ongoing": int(b.old_offsets[-1]), "new": int(b.new_offsets[-1]), "moves": moves}
     if oracle_problems > 0:
         from oracle import ref  # the CPU baseline leg may use the oracle
         t0 = time.perf_counter()
         for p in range(oracle_problems):
             ref.rebalance(*b.problem(p))
         out["oracle_problems_per_s"] = oracle_problems / (time.perf_counter() - t0)
-        out["oracle_sample"] = "first %d problems, one thread" % oracle_problems
+        out["oracle_sample"] = "first %d problems, 1 core of %d" % (oracle_problems, host_cores())
     return out
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--sweep-steps", type=int, default=5)
-    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--no-sweep", action="store_true")
-    ap.add_argument("--sweep-only", action="store_true", help="time only the scaling sweep (for profiling)")
-    ap.add_argument("--no-rebalance", action="store_true")
-    ap.add_argument("--no-scaling", action="store_true", help="skip the smallest cluster per arrival rate")
-    ap.add_argument("--rebalance-only", action="store_true", help="time only Algorithm 2 (for profiling)")
-    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
-                    help="also run a plain device-to-device copy of MIB MiB (a reference kernel of known "
-                         "traffic for scaling memory counters)")
-    args = ap.parse_args()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the evaluator runs on a single device "
-              "(multi-GPU sharding is a design note, not built)", file=sys.stderr)
-        sys.exit(2)
-
+def time_large(steps: int, warmup: int, calibrate_copy: int = 0):
+    """The headline: K steps of the large workload on the library's stream."""
     import numpy as np
     import torch
 
     from paper_2405_06856_amd import aladdin
     from paper_2405_06856_amd import workloads as wl
-
     dev = torch.device("cuda", 0)
-    if args.sweep_only:
-        print(json.dumps({"sweep": time_sweep(args.sweep_steps)}), flush=True)
-        return
-    if args.rebalance_only:
-        print(json.dumps({"rebalance": time_rebalance(args.steps)}), flush=True)
-        return
-    if args.calibrate_copy > 0:
-        n = args.calibrate_copy * (1 << 20) // 4
+    if calibrate_copy > 0:  # a copy of known traffic, for scaling memory counters
+        n = calibrate_copy * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.int32, device=dev)
         dst = torch.empty_like(src)
         for _ in range(3):
@@ -233,7 +299,6 @@ def main():
     R = int(trace.res_offsets[1] - trace.res_offsets[0])
     W, Q = trace.n_workers, trace.n_queries
     pairs = W * Q
-
     ev = aladdin.Evaluator(0, tile=TILE_LARGE)
     t_load0 = time.perf_counter()
     ev.load_trace(trace)
@@ -241,60 +306,101 @@ def main():
     ql = torch.as_tensor(trace.q_l_in, dtype=torch.int32).to(dev)
     qp = torch.as_tensor(trace.q_l_pred, dtype=torch.int32).to(dev)
     before = ev.summary()
-    torch.cuda.synchronize()
-
     out = torch.empty(Q, dtype=torch.int32, device=dev)
     dg = torch.empty(Q * aladdin.DIAG_DTYPE.itemsize, dtype=torch.uint8, device=dev)
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         ev.place_device(ql, qp, 0, diag=True, out=out, diag_out=dg)
     torch.cuda.synchronize()
     # No query of this stream fits anywhere, so the worker state is the same at
-    # the start of every step (checked below).  Only the pair-evaluation kernel
-    # is timed inside the timed region (two events per step).
+    # the start of every step (checked below).  Inside the timed region only
+    # the pair-evaluation kernel is timed (two events per step, without a
+    # system-scope fence); every step returns when its stream work is done, so
+    # the host clock also gives each step's latency.
     ev.profiling(True, kinds=("eval",))
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    gc.collect()
-    gc.disable()  # no collector pass inside the timed region
-    try:
+    walls = []
+
+    def run():
         start.record(ev.stream)
         t0 = time.perf_counter()
-        for _ in range(args.steps):
+        for _ in range(steps):
+            t1 = time.perf_counter()
             ev.place_device(ql, qp, 0, diag=True, out=out, diag_out=dg)
+            walls.append(time.perf_counter() - t1)
         stop.record(ev.stream)
         torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-    finally:
-        gc.enable()
+        return time.perf_counter() - t0
+
+    wall = no_gc(run)
     gpu_ms = start.elapsed_time(stop)
     eval_ms, eval_n = ev.kernel_time("eval")
     # per-kernel breakdown from a separate, untimed pass
     ev.profiling(True)
-    for _ in range(args.steps):
+    for _ in range(steps):
         ev.place_device(ql, qp, 0, diag=True, out=out, diag_out=dg)
     torch.cuda.synchronize()
-    sel_ms, sel_n = ev.kernel_time("select")
-    com_ms, com_n = ev.kernel_time("commit")
-    bld_ms, bld_n = ev.kernel_time("build")
+    kern = {k: ev.kernel_time(k)[0] / steps for k in ("build", "eval", "select", "commit")}
     ev.profiling(False)
     placed = int((out >= 0).sum().item())
     after = ev.summary()
+    ev.close()
     assert placed == 0 and all(np.array_equal(before[k], after[k]) for k in before), \
         "state changed during the large-workload steps"
-
-    ms_per_step = gpu_ms / args.steps
-    value = pairs / (ms_per_step / 1e3)
     eval_avg_ms = eval_ms / max(eval_n, 1)
-    pairs_per_eval_launch = pairs * args.steps / max(eval_n, 1)
-    achieved = algorithmic_bytes_per_pair(R) * pairs_per_eval_launch / (eval_avg_ms / 1e3) / 1e9
-    traffic = measured_traffic() if pairs_per_eval_launch == pairs else None
+    pairs_per_launch = pairs * steps / max(eval_n, 1)
+    return {"R": R, "pairs": pairs, "gpu_ms": gpu_ms, "wall": wall, "walls": walls, "eval_avg_ms": eval_avg_ms,
+            "pairs_per_launch": pairs_per_launch, "kernels": kern, "load_s": load_s, "trace": trace}
 
-    sweep_info = None if args.no_sweep else time_sweep(args.sweep_steps)
-    rb_info = None if args.no_rebalance else time_rebalance(args.steps, 0 if args.no_cpu else 8)
-    scaling_info = None if (args.no_sweep or args.no_scaling) else scaling_over_rates()
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--sweep-steps", type=int, default=5)
+    ap.add_argument("--runs", type=int, default=5, help="timed runs of the long workload (twice as many of the "
+                                                        "tiny and medium ones)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-rebalance", action="store_true")
+    ap.add_argument("--no-scaling", action="store_true", help="skip the smallest cluster per arrival rate")
+    ap.add_argument("--no-workloads", action="store_true", help="skip the tiny, medium and long workloads")
+    ap.add_argument("--only", choices=("large", "sweep", "rebalance", "long", "medium", "tiny"),
+                    help="time one part only (for profiling)")
+    ap.add_argument("--sweep-only", action="store_true", help="same as --only sweep")
+    ap.add_argument("--rebalance-only", action="store_true", help="same as --only rebalance")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="also run a plain device-to-device copy of MIB MiB (a reference kernel of known "
+                         "traffic for scaling memory counters)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the evaluator runs on a single device "
+              "(multi-GPU sharding is a design note, not built)", file=sys.stderr)
+        sys.exit(2)
+    only = args.only or ("sweep" if args.sweep_only else ("rebalance" if args.rebalance_only else None))
+    if only == "sweep":
+        print(json.dumps({"sweep": time_sweep(args.sweep_steps)}), flush=True)
+        return
+    if only == "rebalance":
+        print(json.dumps({"rebalance": time_rebalance(args.steps)}), flush=True)
+        return
+    if only in ("long", "medium", "tiny"):
+        print(json.dumps({only: time_workload(only, args.runs)}), flush=True)
+        return
+    if only == "large":
+        args.no_workloads = args.no_sweep = args.no_rebalance = args.no_scaling = args.no_cpu = True
+
+    L = time_large(args.steps, args.warmup, args.calibrate_copy)
+    ms_per_step = L["gpu_ms"] / args.steps
+    value = L["pairs"] / (ms_per_step / 1e3)
+    eval_s = L["eval_avg_ms"] / 1e3
+    achieved_tops = OPS_PER_PAIR * L["pairs_per_launch"] / eval_s / 1e12
+    traffic = measured_traffic() if L["pairs_per_launch"] == L["pairs"] else None
+    walls = sorted(L["walls"])
     line = {
-        "metric": "query x worker placement evals/sec (+ scenario sweeps/sec; % of HBM roofline)",
+        "metric": METRIC,
         "value": value,
         "unit": "pair-evals/s",
         "n_gpus": 1,
@@ -309,22 +415,29 @@ def main():
         "config": {"workload": "large: 512 workers x 512 resident requests, 65536 queries, KV 262144 tokens, "
                                "lognormal lengths (input mu 6.5 sigma 1.2 [16,8192], output mu 5.5 sigma 1.0 "
                                "[8,2048]), diagnostics on",
-                   "pairs_per_step": pairs, "tile": TILE_LARGE, "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_eval (pair evaluation)", "kernel_avg_ms": eval_avg_ms,
-                     "bytes_per_pair": algorithmic_bytes_per_pair(R)},
-        "kernels_ms_per_step": {"build": bld_ms / args.steps, "eval": eval_ms / args.steps,
-                                "select": sel_ms / args.steps, "commit": com_ms / args.steps},
-        "wall_ms_per_step": wall * 1e3 / args.steps,
-        "load_ms": load_s * 1e3,
-        "sweep": sweep_info,
-        "rebalance": rb_info,
-        "scaling": scaling_info,
+                   "pairs_per_step": L["pairs"], "tile": TILE_LARGE, "parallelism": "single GPU"},
+        "step_ms": {"median": statistics.median(walls) * 1e3, "min": walls[0] * 1e3, "mean_device": ms_per_step,
+                    "clock": "median and min: host clock per step (a step returns when its stream work is "
+                             "done); mean_device: events around the timed region"},
+        "roofline": {"bound": "alu", "achieved": achieved_tops, "peak": VALU_PEAK_TOPS, "unit": "Tops/s",
+                     "frac": achieved_tops / VALU_PEAK_TOPS, "traffic": traffic,
+                     "kernel": "k_eval (pair evaluation)", "kernel_avg_ms": L["eval_avg_ms"],
+                     "ops_per_pair": OPS_PER_PAIR, "pairs_per_launch": L["pairs_per_launch"],
+                     "hbm_frac": (traffic / eval_s / 1e9 / HBM_PEAK_GBS) if traffic else None,
+                     "scan_equivalent_GBps": scan_equivalent_bytes_per_pair(L["R"]) * L["pairs_per_launch"]
+                     / eval_s / 1e9},
+        "kernels_ms_per_step": L["kernels"],
+        "wall_ms_per_step": L["wall"] * 1e3 / args.steps,
+        "load_ms": L["load_s"] * 1e3,
     }
+    if not args.no_workloads:
+        line["workloads"] = {n: time_workload(n, args.runs if n == "long" else 2 * args.runs)
+                             for n in ("tiny", "medium", "long")}
+    line["sweep"] = None if args.no_sweep else time_sweep(args.sweep_steps)
+    line["rebalance"] = None if args.no_rebalance else time_rebalance(args.steps, 0 if args.no_cpu else 8)
+    line["eq7_scaling"] = None if (args.no_sweep or args.no_scaling) else scaling_over_rates()
     if not args.no_cpu:
-        line["cpu_baseline"] = cpu_baseline(trace)
-    ev.close()
+        line["cpu_baseline"] = cpu_baseline(L["trace"])
     print(json.dumps(line), flush=True)
 
 
