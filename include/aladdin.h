@@ -353,6 +353,19 @@ int ald_worker_summary(ald_handle_t handle, int32_t* B, int64_t* sum_c, int64_t*
 int ald_set_profiling(ald_handle_t handle, int32_t kinds);
 int ald_kernel_time(ald_handle_t handle, int32_t kind, double* total_ms, int64_t* launches);
 
+/* Tile statistics of the handle's last successful placement call
+ * (ald_place_stream, ald_place_stream_hb, ald_place_grouped,
+ * ald_sweep_scenarios, ald_sweep_scenarios_hb), summed over scenarios, into the
+ * host array out[4]: [0] commit rounds run, [1] tiles cut before their end
+ * (the candidate lists published at tile start could no longer decide a query
+ * exactly, 64 workers had changed, or the stale-scan budget ran out),
+ * [2] decisions that scanned the tile-start bit words of the untouched workers
+ * instead of cutting, [3] tiles cut on the stale-scan budget.  Placements
+ * never depend on these figures; they describe how the arrival-order commit of
+ * Algorithm 1 (Sec. 4.2) was split into speculative tiles.  After a failed
+ * call the figures are unspecified. */
+int ald_place_stats(ald_handle_t handle, int64_t* out);
+
 /* Message for the last error on this handle, or for a code. */
 const char* ald_last_error(ald_handle_t handle);
 const char* ald_strerror(int code);

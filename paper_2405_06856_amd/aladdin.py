@@ -52,8 +52,9 @@ assert DIAG_DTYPE.itemsize == 40
 SYMBOLS = ("ald_create", "ald_destroy", "ald_set_workspace", "ald_workspace_needed", "ald_workspace_size",
            "ald_sweep_workspace_size", "ald_set_tile", "ald_load_workers", "ald_load_workers_history",
            "ald_place_stream", "ald_place_stream_hb", "ald_place_grouped", "ald_move_requests",
-           "ald_sweep_scenarios", "ald_sweep_scenarios_hb", "ald_rebalance", "ald_rebalance_noalloc", "ald_worker_summary", "ald_set_profiling", "ald_kernel_time",
-           "ald_last_error", "ald_strerror")
+           "ald_sweep_scenarios", "ald_sweep_scenarios_hb", "ald_rebalance", "ald_rebalance_noalloc",
+           "ald_worker_summary", "ald_set_profiling", "ald_kernel_time", "ald_place_stats", "ald_last_error",
+           "ald_strerror")
 
 
 def _load():
@@ -83,6 +84,7 @@ def _load():
         "ald_worker_summary": ([P, P, P, P, P], ctypes.c_int),
         "ald_set_profiling": ([P, i32], ctypes.c_int),
         "ald_kernel_time": ([P, i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)], ctypes.c_int),
+        "ald_place_stats": ([P, ctypes.POINTER(i64)], ctypes.c_int),
         "ald_last_error": ([P], ctypes.c_char_p),
         "ald_strerror": ([ctypes.c_int], ctypes.c_char_p),
     }
@@ -270,6 +272,12 @@ def ald_kernel_time(h, kind: int):
     n = ctypes.c_int64()
     _check(h, _L.ald_kernel_time(h, int(kind), ctypes.byref(ms), ctypes.byref(n)))
     return ms.value, n.value
+
+
+def ald_place_stats(h):
+    out = (ctypes.c_int64 * 4)()
+    _check(h, _L.ald_place_stats(h, out))
+    return {"rounds": out[0], "cuts": out[1], "fallbacks": out[2], "stale_cuts": out[3]}
 
 
 def ald_last_error(h) -> str:
@@ -503,6 +511,10 @@ class Evaluator:
 
     def kernel_time(self, kind: str):
         return ald_kernel_time(self.h, KERNEL_KINDS[kind])
+
+    def tile_stats(self):
+        """How the last placement call split the arrival-order commit into tiles."""
+        return ald_place_stats(self.h)
 
 
 def smallest_feasible_cluster(scenarios, rejected):

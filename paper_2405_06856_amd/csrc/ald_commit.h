@@ -242,7 +242,7 @@ __device__ __forceinline__ QView broadcast_q(const QSum& q, int p)
 // workers).
 __device__ Diag reject_diag(const State& st, const Scen& sc, const QSum& q, int i, int start, int w0, int32_t lin,
                             int32_t lp, int32_t tau, int32_t hb, const CommitLDS& L, int nd, int hot,
-                            const WinBits& wb, int* abort)
+                            const WinBits& wb, int* abort, int* scanned)
 {
     Diag d;
     d.n_feasible = 0;
@@ -252,6 +252,7 @@ __device__ Diag reject_diag(const State& st, const Scen& sc, const QSum& q, int 
     d.kv_excess_min = 0;
     d.near_tie = 0;
     *abort = 0;
+    *scanned = 0;
     const int32_t sq = lin - tau, eq = lp + tau;
     int64_t exmin = q.ex1;
     if (q.w1 >= 0 && dirty_w(L, sc.W, nd, q.w1)) {
@@ -259,6 +260,7 @@ __device__ Diag reject_diag(const State& st, const Scen& sc, const QSum& q, int 
             *abort = 1;
             return d;
         }
+        *scanned = 1;
         int j = 0;
         while (j < nd && L.dw[j] != q.w1) ++j;
         const DAgg& a = L.dag[j];
@@ -287,6 +289,8 @@ struct Decision {
     int32_t w;      // chosen worker, -1 = rejected
     int32_t lane;   // dirty lane holding w, -1 when w was untouched in the tile
     int32_t abort;  // the tile-start lists cannot decide this query exactly
+    int32_t stale;  // exact scans of workers that turned out infeasible
+    int32_t fallback;  // the untouched workers' bit words were scanned
     Diag d;
 };
 
@@ -371,6 +375,55 @@ __device__ __forceinline__ int64_t dirty_kv_peak(const State& st, CommitLDS& L, 
     return wave_kv_peak<true>(st.e + base, st.s + base, cB, sq, eq, p0);
 }
 
+// Algorithm 1's best worker among the workers untouched in this tile whose
+// tile-start bit for query i is set in `words` (feasibility or near tie): for
+// them the tile-start results are still exact.  With `listed`, only workers of
+// the kind the selection lists (with interchangeable empty workers, the
+// non-empty ones).  The whole wave scans the scenario's bit words, eight
+// batches of 64 workers at a time; every lane gets (key, worker), worker -1
+// when there is none.
+struct KeyW {
+    uint64_t k;
+    int32_t w;
+};
+__device__ __forceinline__ KeyW best_untouched(const uint64_t* words, const uint64_t* keys, const CommitLDS* L, int W,
+                                            int nd, int64_t row0, int bit, bool listed, bool uniform_M)
+{
+    const int lane = lane_id();
+    const uint64_t* row = words + row0;
+    uint64_t k = 0;
+    int32_t w = -1;
+    for (int b0 = 0; b0 < W; b0 += 64 * 8) {
+        uint64_t wd[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int ww = b0 + u * 64 + lane;
+            wd[u] = ww < W ? row[ww] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int ww = b0 + u * 64 + lane;
+            bool ok = (wd[u] >> bit) & 1;
+            if (!ballot(ok)) continue;
+            ok = ok && !dirty_w(*L, W, nd, ww);
+            const uint64_t kk = ok ? keys[ww] : 0;
+            ok = ok && !(listed && uniform_M && kk == 0);
+            const bool take = ok && ranks_before(kk, ww, k, w);
+            k = take ? kk : k;
+            w = take ? ww : w;
+        }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint64_t ok2 = __shfl_xor(k, off, 64);
+        const int32_t ow = __shfl_xor(w, off, 64);
+        const bool take = ranks_before(ok2, ow, k, w);
+        k = take ? ok2 : k;
+        w = take ? ow : w;
+    }
+    return KeyW{k, w};
+}
+
 // Decide one query with the whole wave.  `a` is this lane's dirty worker.
 __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int i, int start, int w0, int32_t lin,
                            int32_t lp, int32_t tau, int32_t hb, CommitLDS& L, int nd, int hot, int& hotBs,
@@ -380,6 +433,8 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
     r.w = -1;
     r.lane = -1;
     r.abort = 0;
+    r.stale = 0;
+    r.fallback = 0;
     r.d.n_feasible = 0;
     r.d.near_tie = 0;
     r.d.kv_peak_chosen = 0;
@@ -405,9 +460,14 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
         bw = take ? w : bw;
         have = have | take;
     }
-    if (!have && q.ncand > TOPK) {
-        r.abort = 1;
-        return r;
+    if (!have && q.ncand > TOPK) {  // every listed candidate was committed to: the best untouched one
+        const KeyW c = best_untouched(st.bits_feas, st.key + sc.wbase, &L, sc.W, nd,
+                                      sc.bits_off + (int64_t)((i - start) >> 6) * sc.W, (i - start) & 63, true,
+                                      sc.uniform_M != 0);
+        have = c.w >= 0;
+        bk = have ? c.k : bk;
+        bw = have ? c.w : bw;
+        r.fallback = 1;
     }
     if (!have && sc.uniform_M && q.efeas && next_empty >= 0) {
         have = true;
@@ -454,6 +514,7 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
                 r.lane = bl;
                 return r;
             }
+            r.stale += 1;
         }
         r.w = have ? bw : -1;
         return r;
@@ -468,6 +529,7 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
         int32_t p0;
         const int64_t pk = dirty_kv_peak(st, L, a, bl, hot, hotBs, hotm, sq, eq, &p0);
         const bool ok = pk <= rdlane(a.M, bl);
+        r.stale += ok ? 0 : 1;
         if (lane == bl) {
             cand = false;
             feas_now = ok;
@@ -495,13 +557,14 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
     // smallest KV excess
     int64_t exmin = q.ex1;
     const int j1 = dirty_lane(a, q.w1);
-    if (q.w1 >= 0 && j1 >= 0) {
-        if (q.w2 >= 0 && dirty_lane(a, q.w2) >= 0) {
-            r.abort = 1;
-            return r;
-        }
+    const int j2 = q.w2 >= 0 ? dirty_lane(a, q.w2) : -1;
+    if (q.w1 >= 0 && j1 >= 0 && j2 >= 0) {  // both dirty: the tile-start lists cannot decide
+        r.abort = 1;
+        return r;
+    } else if (q.w1 >= 0 && j1 >= 0) {
         int32_t p0;
         const int64_t pk = dirty_kv_peak(st, L, a, j1, hot, hotBs, hotm, sq, eq, &p0);
+        r.stale += 1;
         const int64_t ex_now = pk - rdlane(a.M, j1);
         exmin = q.w2 < 0 ? ex_now : (ex_now < q.ex2 ? ex_now : (int64_t)q.ex2);
     }
@@ -514,9 +577,12 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
             nt = r.w < 0 || !ranks_before(bk, bw, q.ntkey, q.ntw);
         } else if (r.w < 0) {
             nt = true;
-        } else {
-            r.abort = 1;
-            return r;
+        } else {  // the best near-tie worker was committed to: the best untouched one with a near tie
+            const KeyW c = best_untouched(st.bits_nt, st.key + sc.wbase, &L, sc.W, nd,
+                                          sc.bits_off + (int64_t)((i - start) >> 6) * sc.W, (i - start) & 63, false,
+                                          sc.uniform_M != 0);
+            nt = c.w >= 0 && !ranks_before(bk, bw, c.k, c.w);
+            r.fallback = 1;
         }
     }
     const bool dnt = valid && Lt.nt && (r.w < 0 || !ranks_before(bk, bw, a.key, a.w));
@@ -661,6 +727,11 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
     int firstrej = fpc > start ? start : INT32_MAX;
     WinBits wb;
     wb.f0 = wb.f1 = wb.n0 = wb.n1 = 0;
+    // Exact scans forced by tile-start lists gone stale.  Past a budget a fresh
+    // tile (rebuilt summaries, re-evaluated pairs) is the cheaper way on, and
+    // the tile is cut before the next decision.
+    int stale = 0, fallbacks = 0;
+    bool stale_cut = false;
     while (pos < end && !cut) {
         // one window of 64 queries; `cur` is the first undecided lane
         const int w0 = pos;
@@ -683,9 +754,11 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
             const int p = pm ? __ffsll((unsigned long long)pm) - 1 : NT;
             // lanes cur..p-1: rejected whatever happened earlier in the tile
             Diag dr;
-            int ab = 0;
+            int ab = 0, scn = 0;
             const bool mine = act && lane >= cur && lane < p;
-            if (want_diag && mine) dr = reject_diag(st, sc, q, i, start, w0, lin, lp, tau, hb, L, nd, hot, wb, &ab);
+            if (want_diag && mine)
+                dr = reject_diag(st, sc, q, i, start, w0, lin, lp, tau, hb, L, nd, hot, wb, &ab, &scn);
+            stale += ballot(mine && scn) ? 1 : 0;
             const uint64_t am = ballot(mine && ab);
             const int abl = am ? __ffsll((unsigned long long)am) - 1 : NT;
             const int lim = min(p, abl);
@@ -707,6 +780,12 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
             }
             // the query of lane p, decided by the whole wave
             const int ip = w0 + p;
+            if (stale >= STALE_CUT) {
+                pos = ip;
+                cut = true;
+                stale_cut = true;
+                break;
+            }
             const QView qv = broadcast_q(q, p);
             const int32_t plin = rdlane(lin, p), plp = rdlane(lp, p);
             if (next_empty == -2 && qv.efeas) next_empty = next_empty_worker(st, sc, L, nd, next_from);
@@ -718,6 +797,8 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
                 cut = true;
                 break;
             }
+            stale += dc.stale;
+            fallbacks += dc.fallback;
             if (lane == 0) {
                 if (st.out_worker) st.out_worker[sc.out_off + q_at(sc, ip)] = dc.w < 0 ? dc.w : dc.w + sc.out_add;
                 if (want_diag) st.out_diag[q_at(sc, ip)] = dc.d;
@@ -904,6 +985,8 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
         }
         cp->start = pos;
         cp->aborts = c.aborts + (cut ? 1 : 0);
+        cp->fallbacks = c.fallbacks + fallbacks;
+        cp->stale_cuts = c.stale_cuts + (stale_cut ? 1 : 0);
         cp->commits = c.commits + commits;
         cp->round = c.round + 1;
         st.tinfo[s].first_pc[(c.round + 1) & 1] = INT32_MAX;

@@ -80,6 +80,7 @@ struct ald_handle {
     bool dirty_pending = false;    // the last commit round left workers with stale summaries
     bool check_all = false;        // stale workers are not listed (after grouped placement): check every one
     int64_t qcount = 0;            // queries processed since the load (routes grouped placement)
+    int64_t stats[4] = {0, 0, 0, 0};  // the last placement call: rounds, cuts, fallbacks, stale cuts
     Arena* grouped = nullptr;      // scenario view of the loaded workers for grouped placement
     // App. A's router: the group sizes it routes for and the queries each group
     // received since the load (or since the sizes changed)
@@ -489,6 +490,8 @@ int64_t rounds_needed(const std::vector<Ctl>& c, const std::vector<const int32_t
 // round listed.
 int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, std::vector<Ctl>& hc)
 {
+    std::fill(h->stats, h->stats + 4, 0);
+    std::vector<Ctl> c0(hc);
     if (a->hctl_n < a->S) {
         if (a->hctl) HIPCHK(h, hipHostFree(a->hctl));
         a->hctl = nullptr;
@@ -516,6 +519,12 @@ int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, 
         prof_collect(h);
         for (const Ctl& x : hc)
             if (x.err) return map_dev_error(h, x.err);
+    }
+    for (size_t i = 0; i < hc.size(); ++i) {
+        h->stats[0] += hc[i].round - c0[i].round;
+        h->stats[1] += hc[i].aborts - c0[i].aborts;
+        h->stats[2] += hc[i].fallbacks - c0[i].fallbacks;
+        h->stats[3] += hc[i].stale_cuts - c0[i].stale_cuts;
     }
     return ALD_OK;
 }
@@ -638,6 +647,13 @@ int ald_set_profiling(ald_handle_t h, int32_t kinds)
     if (h->prof) {
         for (int k = 0; k < 5; ++k) { h->tot_ms[k] = 0; h->launches[k] = 0; }
     }
+    return ALD_OK;
+}
+
+int ald_place_stats(ald_handle_t h, int64_t* out)
+{
+    if (!h || !out) return ALD_EINVAL;
+    std::copy(h->stats, h->stats + 4, out);
     return ALD_OK;
 }
 

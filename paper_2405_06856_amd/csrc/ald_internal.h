@@ -42,6 +42,12 @@ constexpr int COMMIT_THREADS = 64;  // the arrival-order commit runs as one wave
 constexpr int HOT = 8192;          // most request slots per worker (commit keeps one worker in LDS)
 constexpr int BUILD_THREADS = 256;
 constexpr int MAX_DIRTY = 64;      // workers changed within one tile before the tile is cut
+#ifndef ALD_STALE_CUT
+#define ALD_STALE_CUT 24
+#endif
+// exact re-scans of changed workers (infeasible ones, or for diagnostics) after
+// which the commit cuts its tile; a build-time option
+constexpr int STALE_CUT = ALD_STALE_CUT;
 constexpr int32_t NEG = INT32_MIN;
 // pme with no slot before it: far below every demand, yet pme + sq cannot wrap
 // in 32 bits (|sq| < 2^28)
@@ -109,6 +115,8 @@ struct Ctl {
     int32_t ndirty;     // workers the last commit round changed (their summaries are stale)
     int32_t hb_next;    // with per-query heartbeats: the next query (> start) that heartbeats
                         // precede, Q if none; 0 otherwise
+    int32_t fallbacks;  // decisions that scanned the untouched workers' bit words (statistics)
+    int32_t stale_cuts; // tiles cut on the stale-scan budget (statistics)
 };
 
 // Tile description published by the selection kernel for the commit kernel.
