@@ -1235,6 +1235,14 @@ RbRho rb_rho(double k2, double c2)
     RbRho r{};
     r.k2 = k2;
     r.c2 = c2;
+    r.rho_d = c2 / k2;
+    // rho <= 1e9: R fits easily; c2 - R k2 is a multiple of the smaller of the
+    // two significands' units, so the single rounding of the fma keeps its sign
+    r.R = (int64_t)std::nearbyint(r.rho_d);
+    const double rem = std::fma(-(double)r.R, k2, c2);
+    r.fs = rem > 0.0 ? 1 : (rem < 0.0 ? -1 : 0);
+    // |rho - R| <= |rho_d - R| + |rho - rho_d|, the latter at most 2^-53 rho_d
+    r.f_up = (std::fabs(r.rho_d - (double)r.R) + std::ldexp(r.rho_d, -52)) * (1.0 + std::ldexp(1.0, -50));
     int ek = 0, ec = 0;
     const double fk = std::frexp(k2, &ek);
     r.mk = (uint64_t)std::ldexp(fk, 53);
@@ -1267,6 +1275,7 @@ int rebalance_impl(ald_handle_t h, int32_t P, const int32_t* n_workers, const al
     std::vector<RbProblem> prob(P);
     std::vector<RbChunk> chunks;
     int64_t wtot = 0;
+    int32_t wmax = 1, jmax = 0;
     for (int32_t p = 0; p < P; ++p) {
         const std::string tag = "problem " + std::to_string(p) + ": ";
         if (n_workers[p] < 1 || n_workers[p] > RB_WMAX)
@@ -1283,6 +1292,8 @@ int rebalance_impl(ald_handle_t h, int32_t P, const int32_t* n_workers, const al
         prob[p] = RbProblem{o0, o1, n0, wtot, rb_rho(m.k2, m.c2), n_workers[p], (int32_t)(n1 - n0)};
         for (int64_t b = o0; b < o1; b += RB_CHUNK) chunks.push_back(RbChunk{b, std::min(o1, b + RB_CHUNK), p, 0});
         wtot += n_workers[p];
+        wmax = std::max(wmax, n_workers[p]);
+        jmax = std::max(jmax, (int32_t)(n1 - n0));
     }
     const int64_t n_old = old_offsets[P], n_new = new_offsets[P];
     if (n_old >= ((int64_t)1 << 30) || n_new >= ((int64_t)1 << 30)) return fail(h, ALD_EINVAL, "too many requests");
@@ -1337,6 +1348,16 @@ int rebalance_impl(ald_handle_t h, int32_t P, const int32_t* n_workers, const al
     a.log_cap = log_cap;
     a.obj = out_obj;
     a.err = err_word;
+    a.wmax = wmax;
+    a.jmax = jmax;
+    {
+        int lds_max = 0;
+        HIPCHK(h, hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device));
+        if (rb_moves_lds(wmax, jmax) + 512 > (size_t)lds_max)  // and the kernel's own small arrays
+            return fail(h, ALD_EINVAL, "the largest problem's workers and new requests need " +
+                                           std::to_string(rb_moves_lds(wmax, jmax)) + " bytes of LDS, more than the " +
+                                           std::to_string(lds_max) + " of a workgroup");
+    }
     HIPCHK(h, hipMemcpyAsync(base, prob.data(), P * sizeof(RbProblem), hipMemcpyHostToDevice, h->stream));
     if (!chunks.empty())
         HIPCHK(h, hipMemcpyAsync(base + b_prob, chunks.data(), chunks.size() * sizeof(RbChunk),

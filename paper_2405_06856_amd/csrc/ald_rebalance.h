@@ -6,20 +6,25 @@
 
 namespace ald {
 
-constexpr int RB_THREADS = 1024;
 constexpr int RB_WMAX = 4096;     // workers per problem (the error accumulators live in LDS)
 constexpr int RB_JMAX = 8192;     // new requests per problem
 constexpr int RB_ETHREADS = 256;  // threads per error-accumulation block
 constexpr int RB_CHUNK = 2048;    // ongoing requests per error-accumulation block
 constexpr int32_t RB_LEN_MAX = 1 << 24;
+constexpr int RB_LIST = 1024;     // requests near the top gain taken exactly per chunk and wave
+constexpr int RB_WAVES = 4;       // waves per problem in the moves kernel
 
 // rho = c2 / k2 of one problem, held so that the sign of a + rho * b (integer
 // a, b) is exact: k2 = mk * 2^ek and c2 = mc * 2^ec with 53-bit integer
-// significands (mc = 0 when c2 = 0), sh = ek - ec.
+// significands (mc = 0 when c2 = 0), sh = ek - ec; rho_d = fl(c2 / k2) for
+// the fp64 stand-ins; R the integer nearest rho, fs the exact sign of rho - R
+// and f_up >= |rho - R| (so that a + R b = 0 decides the sign of a + rho b as
+// fs * sign(b), and a small |b| f_up lets a + R b decide it alone).
 struct RbRho {
-    double k2, c2;
+    double k2, c2, rho_d, f_up;
     uint64_t mk, mc;
-    int32_t sh, pad;
+    int64_t R;
+    int32_t sh, fs;
 };
 
 struct RbProblem {
@@ -51,9 +56,12 @@ struct RbArgs {
     int32_t log_cap;
     int64_t* obj;         // per problem: sum |c| before and after as pairs (a, b) = a + rho * b (nullable)
     int32_t* err;
+    int32_t wmax, jmax;   // the largest W and n_new over the problems (size the moves kernel's LDS)
 };
-// error accumulation (nchunk + P blocks), then the greedy moves (P blocks)
+// error accumulation (nchunk + P blocks), then the greedy moves (P blocks of RB_WAVES waves)
 hipError_t launch_rebalance(const RbArgs& a, hipStream_t stream);
+// LDS bytes of the moves kernel for problems of at most wmax workers and jmax new requests
+size_t rb_moves_lds(int32_t wmax, int32_t jmax);
 
 // Fixed device array of the allocation-free entry point: the problem and chunk
 // tables of at most RB_STATIC_P problems and RB_STATIC_CHUNKS chunks, then the

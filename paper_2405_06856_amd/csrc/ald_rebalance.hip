@@ -12,9 +12,10 @@
 //              every (placed request j, other worker y) pair, the one that
 //              lowers sum |c| most (ties to the lowest j, then y) while that
 //              decrease is positive -- found per step from the smallest c and
-//              one gain per request.  Every comparison is the sign of
-//              a + rho * b for integer a, b, taken exactly (rb_sign), so the
-//              choices are exact.
+//              one gain per request.  Gains are ranked with fp64 stand-ins of
+//              proven error; whatever lies within that error of the top is
+//              compared exactly as the sign of a + rho * b for integer a, b
+//              (rb_sign), so the choices are exact.
 #include "ald_device.h"
 #include "ald_rebalance.h"
 
@@ -151,6 +152,10 @@ __device__ __noinline__ int rb_sign_exact(int64_t a, int64_t b, const RbRho& r)
     return cmp > 0 ? sa : (cmp < 0 ? sb : 0);
 }
 
+// When fp64 cannot decide, a + rho b = (a + R b) + (rho - R) b: a zero first
+// term leaves the sign of (rho - R) b, and a first term of at least 1 in size
+// decides alone while |(rho - R) b| < 1/2.  Only what is left takes the
+// 128-bit comparison.
 __device__ __forceinline__ int rb_sign(int64_t a, int64_t b, const RbRho& r)
 {
     const int sa = (a > 0) - (a < 0), sb = (b > 0) - (b < 0);
@@ -159,6 +164,9 @@ __device__ __forceinline__ int rb_sign(int64_t a, int64_t b, const RbRho& r)
     const double x = (double)a * r.k2, y = (double)b * r.c2;
     const double v = x + y, t = fabs(x) + fabs(y);
     if (fabs(v) > 0x1p-50 * t) return v > 0.0 ? 1 : -1;
+    const __int128 A = (__int128)a + (__int128)r.R * b;
+    if (A == 0) return r.fs * sb;
+    if (fabs((double)b) * r.f_up < 0.5) return A > 0 ? 1 : -1;
     return rb_sign_exact(a, b, r);
 }
 __device__ __forceinline__ int rp_sign(RbPair u, const RbRho& r) { return rb_sign(u.a, u.b, r); }
@@ -191,61 +199,204 @@ __device__ __forceinline__ RbPair shfl_pair(RbPair v, int off)
     return RbPair{__shfl_xor(v.a, off, 64), __shfl_xor(v.b, off, 64)};
 }
 
-// sum |c| over the problem's workers (block-wide; every thread gets it)
-__device__ RbPair rb_objective(const int64_t* cle, const int32_t* cbe, int W, const RbRho& rho, int64_t* red)
+// ---------------------------------------------------------------------------------------------
+// fp64 stand-ins.  For integers a, b (|a| < 2^56, |b| < 2^31) and rho_d =
+// fl(c2 / k2), fl(fl(a) + fl(rho_d * b)) lies within 3.1 u T of a + rho * b,
+// with T = |a| + rho |b| and u = 2^-53 (the conversion of a, the rounding of
+// rho_d and of the product, and the sum).  S below bounds T over every value
+// the kernel compares, and each decision taken in fp64 keeps a margin of
+// tol = 2^-46 S (128 u S) against that error; whatever falls inside the margin
+// is decided with exact pairs.
+__device__ __forceinline__ double rb_approx(int64_t a, int64_t b, double rho_d)
+{
+    return (double)a + rho_d * (double)b;
+}
+__device__ __forceinline__ double rb_mag(int64_t a, int64_t b, double rho_d)
+{
+    return fabs((double)a) + rho_d * fabs((double)b);
+}
+// Wave-wide max / min of a double and min of an int: an inclusive scan with
+// DPP row shifts and row broadcasts (as wave_incl_scan), read from lane 63.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_f64(double ident, double x)
+{
+    const uint64_t ui = __builtin_bit_cast(uint64_t, ident), ux = __builtin_bit_cast(uint64_t, x);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)ui, (int)(uint32_t)ux, CTRL, ROW_MASK,
+                                                              0xf, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)(ui >> 32), (int)(uint32_t)(ux >> 32),
+                                                              CTRL, ROW_MASK, 0xf, false);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+template <bool MAX>
+__device__ __forceinline__ double wave_ext_f64(double x)
+{
+    constexpr double id = MAX ? -INFINITY : INFINITY;
+    auto op = [](double u, double v) { return MAX ? fmax(u, v) : fmin(u, v); };
+    x = op(x, dpp_f64<0x111, 0xf>(id, x));  // row_shr:1
+    x = op(x, dpp_f64<0x112, 0xf>(id, x));  // row_shr:2
+    x = op(x, dpp_f64<0x114, 0xf>(id, x));  // row_shr:4
+    x = op(x, dpp_f64<0x118, 0xf>(id, x));  // row_shr:8
+    x = op(x, dpp_f64<0x142, 0xa>(id, x));  // row_bcast:15
+    x = op(x, dpp_f64<0x143, 0xc>(id, x));  // row_bcast:31
+    return rdlane_f64(x, 63);
+}
+__device__ __forceinline__ double wave_max_f64(double v) { return wave_ext_f64<true>(v); }
+__device__ __forceinline__ double wave_min_f64(double v) { return wave_ext_f64<false>(v); }
+struct Min32 {
+    __device__ int32_t operator()(int32_t a, int32_t b) const { return a < b ? a : b; }
+};
+__device__ __forceinline__ int32_t wave_min_i32(int32_t v) { return rdlane(wave_incl_scan(v, INT32_MAX, Min32()), 63); }
+
+// sum |c| over the problem's workers (whole wave; every lane gets it)
+__device__ RbPair rb_objective(const int64_t* cle, const int32_t* cbe, int W, const RbRho& rho)
 {
     RbPair s{0, 0};
-    for (int y = threadIdx.x; y < W; y += RB_THREADS) s = rp_add(s, rp_abs(RbPair{cle[y], cbe[y]}, rho));
-    const int64_t oa = block_reduce<RB_THREADS>(s.a, 0, OpAdd(), red);
-    const int64_t ob = block_reduce<RB_THREADS>(s.b, 0, OpAdd(), red);
-    return RbPair{oa, ob};
+    for (int y = lane_id(); y < W; y += 64) s = rp_add(s, rp_abs(RbPair{cle[y], cbe[y]}, rho));
+    return RbPair{wave_sum64(s.a), wave_sum64(s.b)};
 }
 
-__global__ __launch_bounds__(RB_THREADS) void k_rb_moves(RbArgs a)
+// Half the decrease of sum |c| when a request of d = (l, 1) moves from a worker
+// with c_x > 0 to one with c_min < 0:
+// (|c_x| - |c_x - d| + |c_min| - |c_min + d|) / 2 = min(d, c_x) - max(0, d + c_min).
+__device__ __forceinline__ double rb_half_gain(double dd, double cxd, double cmd)
 {
-    constexpr int NWAVE = RB_THREADS / 64;
-    constexpr int JPT = RB_JMAX / RB_THREADS;  // new requests per thread
-    __shared__ int64_t cle[RB_WMAX];   // c_y = (cle[y], cbe[y])
-    __shared__ int32_t cbe[RB_WMAX];
-    __shared__ int32_t jl[RB_JMAX];    // predicted length of new request j
-    __shared__ int16_t jx[RB_JMAX];    // current worker of new request j (-1: unplaced)
-    __shared__ int16_t neg[RB_WMAX];   // the workers with c < 0, in no particular order
-    __shared__ int16_t pos[RB_WMAX];   // index of a worker in neg (-1: not there)
-    __shared__ uint8_t cpos[RB_WMAX];  // c_y > 0
-    __shared__ int64_t wga[NWAVE], wgb[NWAVE];
-    __shared__ int32_t wo[NWAVE];
-    __shared__ int64_t red[NWAVE];
-    __shared__ int32_t s_nneg;
-    if (*a.err != 0) return;  // invalid input somewhere: nothing changes
+    return fmin(dd, cxd) - fmax(0.0, dd + cmd);
+}
+// The same half decrease as an exact pair; the two signs it branches on are
+// read off the stand-ins when they clear the margin (their error is below
+// 9 u S), else taken exactly.
+__device__ __forceinline__ RbPair rb_half_gain_exact(RbPair cx, double cxd, RbPair cm, double cmd, int64_t l,
+                                                     double dd, double tol, const RbRho& rho)
+{
+    const RbPair d{l, 1};
+    const double t1 = dd - cxd, t2 = dd + cmd;
+    const bool d_le_cx = t1 < -tol || (t1 <= tol && rp_sign(rp_sub(d, cx), rho) <= 0);
+    const bool spill = t2 > tol || (t2 >= -tol && rp_sign(rp_add(d, cm), rho) > 0);
+    const RbPair mn = d_le_cx ? d : cx;
+    return spill ? rp_sub(mn, rp_add(d, cm)) : mn;
+}
+
+// Wave-wide choice among lanes that hold an exact candidate (o != INT32_MAX):
+// with one such lane its value is read, otherwise a butterfly with `better`.
+template <typename Better>
+__device__ __forceinline__ void rb_pick(RbPair& v, int32_t& o, Better better)
+{
+    uint64_t m = ballot(o != INT32_MAX);
+    if (m == 0) return;
+    if (__popcll(m) <= 6) {  // a few: in turn, with uniform operands
+        int l = __ffsll((unsigned long long)m) - 1;
+        RbPair bv{rdlane64s(v.a, l), rdlane64s(v.b, l)};
+        int32_t bo = rdlane(o, l);
+        m &= m - 1;
+        while (m) {
+            l = __ffsll((unsigned long long)m) - 1;
+            const RbPair cv{rdlane64s(v.a, l), rdlane64s(v.b, l)};
+            const int32_t co = rdlane(o, l);
+            if (better(cv, co, bv, bo)) {
+                bv = cv;
+                bo = co;
+            }
+            m &= m - 1;
+        }
+        v = bv;
+        o = bo;
+        return;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const RbPair ov = shfl_pair(v, off);
+        const int32_t oo = __shfl_xor(o, off, 64);
+        if (better(ov, oo, v, o)) {
+            v = ov;
+            o = oo;
+        }
+    }
+    v = RbPair{rdlane64s(v.a, 0), rdlane64s(v.b, 0)};
+    o = rdlane(o, 0);
+}
+
+// One block of RB_WAVES waves per problem.  LDS (sized by the launch for its
+// largest problem): c_y as the exact pair (cle, cbe), the fp64 stand-in of
+// every positive c_y, the receivers list, each new request's length and
+// current worker, and per wave a list of requests near the top gain.  A step:
+// every wave finds c_min (the same result in each), takes the gains of its
+// share of the requests and its best candidate; the waves' results meet in
+// LDS; wave 0 finds the receiver and applies the move.  Three block barriers
+// per step.
+__global__ __launch_bounds__(64 * RB_WAVES) void k_rb_moves(RbArgs a)
+{
+    extern __shared__ __align__(16) unsigned char rb_lds[];
+    __shared__ double x_g[RB_WAVES];              // each wave's largest stand-in gain
+    __shared__ int64_t x_a[RB_WAVES], x_b[RB_WAVES];  // each wave's best exact gain
+    __shared__ int32_t x_j[RB_WAVES];             // and its request
+    __shared__ double s_S;                        // bound on |a| + rho |b| over the values compared
+    __shared__ int32_t s_nneg;                    // receivers listed
+    __shared__ int32_t s_err;
+    // invalid input somewhere: nothing changes (one read for the whole block,
+    // as another block may raise the word meanwhile)
+    if (threadIdx.x == 0) s_err = *a.err;
+    __syncthreads();
+    if (s_err != 0) return;
     const int p = blockIdx.x;
     const RbProblem pr = a.prob[p];
     const RbRho rho = pr.rho;
-    const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
+    const double rho_d = rho.rho_d;
+    const int lane = lane_id(), wv = wave_id();
     const int W = pr.W, n = pr.n_new;
+    const int Wm = a.wmax, Jm = a.jmax;
+    int64_t* cle = (int64_t*)rb_lds;
+    double* cdp = (double*)(cle + Wm);  // [Wm + 1] stand-in of c where c > 0 (the sources), else -inf;
+                                        // slot W: unplaced
+    int32_t* cbe = (int32_t*)(cdp + Wm + 1);
+    int32_t* jl = cbe + Wm;
+    int16_t* jx = (int16_t*)(jl + Jm);  // current worker of each new request (W: unplaced)
+    int16_t* neg = jx + Jm;    // the workers with c < 0, in no particular order
+    int16_t* pos = neg + Wm;   // index of a worker in neg (-1: not there)
+    int16_t* lst = pos + Wm + wv * RB_LIST;  // this wave's requests near the top gain, a chunk at a time
     const int64_t max_moves = 4 * (int64_t)n + W;  // a guard; every move lowers sum |c| strictly
+    const uint64_t below = (1ull << lane) - 1;
+    auto lower = [&](RbPair u, int32_t uy, RbPair v, int32_t vy) { return rb_lower(u, uy, v, vy, rho); };
+    auto better = [&](RbPair u, int32_t uj, RbPair v, int32_t vj) { return rb_better(u, uj, v, vj, rho); };
 
-    if (tid == 0) s_nneg = 0;
-    __syncthreads();
-    for (int y = tid; y < W; y += RB_THREADS) {
-        const int64_t le = a.le[pr.wbase + y];
-        const int32_t be = (int32_t)a.be[pr.wbase + y];
-        cle[y] = le;
-        cbe[y] = be;
-        const int sg = rb_sign(le, be, rho);
-        int32_t at = -1;
-        if (sg < 0) {
-            at = atomicAdd(&s_nneg, 1);
-            neg[at] = (int16_t)y;
+    RbPair obj0{0, 0};
+    if (wv == 0) {
+        double S = 0.0;
+        int nneg = 0;
+        for (int y0 = 0; y0 < W; y0 += 64) {
+            const int y = y0 + lane;
+            const bool in = y < W;
+            const int64_t le = in ? a.le[pr.wbase + y] : 0;
+            const int32_t be = in ? (int32_t)a.be[pr.wbase + y] : 0;
+            const int sg = in ? rb_sign(le, be, rho) : 0;
+            const uint64_t nm = ballot(in && sg < 0);
+            const int at = nneg + __popcll(nm & below);
+            if (in) {
+                cle[y] = le;
+                cbe[y] = be;
+                cdp[y] = sg > 0 ? rb_approx(le, be, rho_d) : -INFINITY;
+                pos[y] = (int16_t)(sg < 0 ? at : -1);
+                if (sg < 0) neg[at] = (int16_t)y;
+                S = fmax(S, rb_mag(le, be, rho_d));
+            }
+            nneg += __popcll(nm);
         }
-        pos[y] = (int16_t)at;
-        cpos[y] = sg > 0 ? 1 : 0;
-    }
-    for (int j = tid; j < n; j += RB_THREADS) {
-        jx[j] = (int16_t)a.new_worker[pr.new0 + j];
-        jl[j] = a.new_lpred[pr.new0 + j];
+        if (lane == 0) cdp[W] = -INFINITY;
+        for (int j = lane; j < n; j += 64) {
+            const int32_t w = a.new_worker[pr.new0 + j];
+            jx[j] = (int16_t)(w < 0 ? W : w);
+            const int32_t l = a.new_lpred[pr.new0 + j];
+            jl[j] = l;
+            S = fmax(S, (double)l + rho_d);
+        }
+        S = wave_max_f64(S) * (1.0 + 0x1p-40);
+        __builtin_amdgcn_wave_barrier();
+        obj0 = rb_objective(cle, cbe, W, rho);
+        if (lane == 0) {
+            s_S = S;
+            s_nneg = nneg;
+        }
     }
     __syncthreads();
-    const RbPair obj0 = rb_objective(cle, cbe, W, rho, red);  // ends with a barrier
 
     // A move of j from x to y lowers sum |c| by A + G with A = |c_x| - |c_x - d|
     // and G = |c_y| - |c_y + d| (d = l_pred_j + rho > 0).  G = -d when c_y >= 0
@@ -261,136 +412,208 @@ __global__ __launch_bounds__(RB_THREADS) void k_rb_moves(RbArgs a)
     int32_t moves = 0;
     for (;;) {
         const int nneg = s_nneg;
+        const double S = s_S;
         if (nneg == 0) break;  // no move gains
-        // c_min and the lowest worker index at it, in every wave
-        RbPair cm{0, 0};
-        int32_t ci = INT32_MAX;
+        const double tol = S * 0x1p-46;
+        // ---- c_min and the lowest worker index at it (every wave alike)
+        double m1 = INFINITY, m2 = INFINITY;
+        int32_t y1 = INT32_MAX;
         for (int k = lane; k < nneg; k += 64) {
             const int32_t y = neg[k];
-            const RbPair v{cle[y], cbe[y]};
-            if (rb_lower(v, y, cm, ci, rho)) {
-                cm = v;
-                ci = y;
+            const double v = rb_approx(cle[y], cbe[y], rho_d);
+            if (v < m1) {
+                m2 = m1;
+                m1 = v;
+                y1 = y;
+            } else {
+                m2 = fmin(m2, v);
             }
         }
+        const double cthr = wave_min_f64(m1) + 2.0 * tol;
+        RbPair cm{0, 0};
+        int32_t ci = INT32_MAX;
+        if (m2 <= cthr) {  // several near the minimum in this lane: all of them exactly
+            for (int k = lane; k < nneg; k += 64) {
+                const int32_t y = neg[k];
+                const RbPair v{cle[y], cbe[y]};
+                if (rb_approx(v.a, v.b, rho_d) > cthr) continue;
+                if (lower(v, y, cm, ci)) {
+                    cm = v;
+                    ci = y;
+                }
+            }
+        } else if (m1 <= cthr) {
+            cm = RbPair{cle[y1], cbe[y1]};
+            ci = y1;
+        }
+        rb_pick(cm, ci, lower);
+        const double cmd = rb_approx(cm.a, cm.b, rho_d);
+
+        // ---- this wave's share of the requests: per lane the two best
+        // stand-in gains (lower index first on equal values) and the third; a
+        // request that cannot move has gain -inf
+        const int jw = wv * 64 + lane;
+        double g1 = -INFINITY, g2 = -INFINITY, g3 = -INFINITY;
+        int32_t j1 = INT32_MAX, j2 = INT32_MAX;
+#pragma unroll 4
+        for (int j = jw; j < n; j += 64 * RB_WAVES) {
+            const double g = rb_half_gain((double)jl[j] + rho_d, cdp[jx[j]], cmd);
+            const bool t1 = g > g1, t2 = g > g2;
+            g3 = t2 ? g2 : fmax(g3, g);
+            g2 = t1 ? g1 : (t2 ? g : g2);
+            j2 = t1 ? j1 : (t2 ? j : j2);
+            g1 = t1 ? g : g1;
+            j1 = t1 ? j : j1;
+        }
+        {
+            const double gw = wave_max_f64(g1);
+            if (lane == 0) x_g[wv] = gw;
+        }
+        __syncthreads();
+        double gmax = x_g[0];
 #pragma unroll
-        for (int off = 32; off > 0; off >>= 1) {
-            const RbPair ov = shfl_pair(cm, off);
-            const int32_t oy = __shfl_xor(ci, off, 64);
-            if (rb_lower(ov, oy, cm, ci, rho)) {
-                cm = ov;
-                ci = oy;
-            }
-        }
-        // each thread's requests, in increasing j: the first largest gain
+        for (int w = 1; w < RB_WAVES; ++w) gmax = fmax(gmax, x_g[w]);
+        if (!(gmax + tol > 0.0)) break;  // every exact gain is <= 0 (or nothing can move)
+        const double gthr = gmax - 2.0 * tol;
         RbPair bg{0, 0};
         int32_t bj = INT32_MAX;
-#pragma unroll
-        for (int u = 0; u < JPT; ++u) {
-            const int j = tid + u * RB_THREADS;
-            if (j >= n) break;
+        auto exact = [&](int j) {
             const int x = jx[j];
-            if (x < 0 || !cpos[x]) continue;
-            const RbPair cx{cle[x], cbe[x]};
-            const RbPair d{(int64_t)jl[j], 1};
-            // (|c_x| - |c_x - d|) + (|c_min| - |c_min + d|), c_x > 0 > c_min
-            const RbPair g = rp_add(rp_sub(cx, rp_abs(rp_sub(cx, d), rho)),
-                                    rp_sub(RbPair{-cm.a, -cm.b}, rp_abs(rp_add(cm, d), rho)));
-            if (rp_sign(rp_sub(g, bg), rho) > 0) {  // strictly: only positive gains, earlier j on ties
+            const int32_t l = jl[j];
+            return rb_half_gain_exact(RbPair{cle[x], cbe[x]}, cdp[x], cm, cmd, l, (double)l + rho_d, tol, rho);
+        };
+        if (ballot(g3 >= gthr)) {
+            // three or more near the top in some lane (ties are common: equal
+            // lengths give equal gains): list this wave's requests near the
+            // top, a chunk at a time, and take them exactly one per lane
+            constexpr int STRIDE = 64 * RB_WAVES;
+            for (int c0 = wv * 64; c0 < n; c0 += STRIDE * (RB_LIST / 64)) {
+                int cnt = 0;
+                for (int t = 0; t < RB_LIST / 64; ++t) {
+                    const int j = c0 + t * STRIDE + lane;
+                    const bool near = j < n && rb_half_gain((double)jl[j] + rho_d, cdp[jx[j]], cmd) >= gthr;
+                    const uint64_t m = ballot(near);
+                    if (near) lst[cnt + __popcll(m & below)] = (int16_t)j;
+                    cnt += __popcll(m);
+                }
+                __builtin_amdgcn_wave_barrier();
+                for (int k = lane; k < cnt; k += 64) {
+                    const int j = lst[k];
+                    const RbPair g = exact(j);
+                    if (better(g, j, bg, bj)) {
+                        bg = g;
+                        bj = j;
+                    }
+                }
+                __builtin_amdgcn_wave_barrier();
+            }
+        } else {
+            if (g1 >= gthr) {
+                bg = exact(j1);
+                bj = j1;
+            }
+            if (g2 >= gthr) {
+                const RbPair g = exact(j2);
+                if (better(g, j2, bg, bj)) {
+                    bg = g;
+                    bj = j2;
+                }
+            }
+        }
+        rb_pick(bg, bj, better);
+        if (lane == 0) {
+            x_a[wv] = bg.a;
+            x_b[wv] = bg.b;
+            x_j[wv] = bj;
+        }
+        __syncthreads();
+        bg = RbPair{x_a[0], x_b[0]};
+        bj = x_j[0];
+#pragma unroll
+        for (int w = 1; w < RB_WAVES; ++w) {
+            const RbPair g{x_a[w], x_b[w]};
+            const int32_t j = x_j[w];
+            if (better(g, j, bg, bj)) {
                 bg = g;
                 bj = j;
             }
         }
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) {
-            const RbPair og = shfl_pair(bg, off);
-            const int32_t oj = __shfl_xor(bj, off, 64);
-            if (rb_better(og, oj, bg, bj, rho)) {
-                bg = og;
-                bj = oj;
-            }
-        }
-        if (lane == 0) {
-            wga[wv] = bg.a;
-            wgb[wv] = bg.b;
-            wo[wv] = bj;
-        }
-        __syncthreads();
-        // every wave finds the block's best from the per-wave ones
-        RbPair g = lane < NWAVE ? RbPair{wga[lane], wgb[lane]} : RbPair{0, 0};
-        int32_t jb = lane < NWAVE ? wo[lane] : INT32_MAX;
-#pragma unroll
-        for (int off = NWAVE / 2; off > 0; off >>= 1) {
-            const RbPair og = shfl_pair(g, off);
-            const int32_t oj = __shfl_xor(jb, off, 64);
-            if (rb_better(og, oj, g, jb, rho)) {
-                g = og;
-                jb = oj;
-            }
-        }
-        jb = rdlane(jb, 0);
-        if (jb == INT32_MAX) break;  // no move lowers the objective
+        if (bj == INT32_MAX || rp_sign(bg, rho) <= 0) break;  // no move lowers the objective
         if (moves >= max_moves) {
-            if (tid == 0) raise_error(a.err, DEV_EOVERFLOW);
+            if (threadIdx.x == 0) raise_error(a.err, DEV_EOVERFLOW);
             break;
         }
+
         if (wv == 0) {
-            const RbPair d{(int64_t)jl[jb], 1};
+            // ---- the receiver: the workers at c_min, or the lowest-index one with c <= -d
+            const RbPair d{(int64_t)jl[bj], 1};
+            const double dd = (double)d.a + rho_d;
             int32_t y = ci;
-            if (rp_sign(rp_add(cm, d), rho) <= 0) {  // the lowest-index receiver at or below -d
+            if (rp_sign(rp_add(cm, d), rho) <= 0) {
                 int32_t lo = INT32_MAX;
                 for (int k = lane; k < nneg; k += 64) {
                     const int32_t w = neg[k];
-                    if (w < lo && rp_sign(rp_add(RbPair{cle[w], cbe[w]}, d), rho) <= 0) lo = w;
+                    if (w >= lo) continue;
+                    const double sd = rb_approx(cle[w], cbe[w], rho_d) + dd;
+                    const bool takes = sd <= -tol ||
+                                       (sd < tol && rp_sign(rp_add(RbPair{cle[w], cbe[w]}, d), rho) <= 0);
+                    if (takes) lo = w;
                 }
-#pragma unroll
-                for (int off = 32; off > 0; off >>= 1) {
-                    const int32_t o = __shfl_xor(lo, off, 64);
-                    lo = o < lo ? o : lo;
-                }
-                y = rdlane(lo, 0);
+                y = wave_min_i32(lo);
             }
+            // ---- apply (every lane computes the same values; lane 0 writes them)
+            const int x = jx[bj];
+            const RbPair cx = rp_sub(RbPair{cle[x], cbe[x]}, d);
+            const RbPair cy = rp_add(RbPair{cle[y], cbe[y]}, d);
+            const int sx = rp_sign(cx, rho), sy = rp_sign(cy, rho);
+            const double S1 = fmax(S, fmax(rb_mag(cx.a, cx.b, rho_d), rb_mag(cy.a, cy.b, rho_d)) * (1.0 + 0x1p-40));
+            const int at_y = pos[y], last = nneg - 1, wl = neg[last];
+            __builtin_amdgcn_wave_barrier();
             if (lane == 0) {
-                const int x = jx[jb];
-                const RbPair cx = rp_sub(RbPair{cle[x], cbe[x]}, d);
-                const RbPair cy = rp_add(RbPair{cle[y], cbe[y]}, d);
                 cle[x] = cx.a;
                 cbe[x] = (int32_t)cx.b;
+                cdp[x] = sx > 0 ? rb_approx(cx.a, cx.b, rho_d) : -INFINITY;
                 cle[y] = cy.a;
                 cbe[y] = (int32_t)cy.b;
-                const int sx = rp_sign(cx, rho), sy = rp_sign(cy, rho);
-                cpos[x] = sx > 0 ? 1 : 0;
-                cpos[y] = sy > 0 ? 1 : 0;
-                if (sx < 0) {  // x (c_x was > 0) joins the receivers
-                    pos[x] = (int16_t)s_nneg;
-                    neg[s_nneg] = (int16_t)x;
-                    s_nneg += 1;
-                }
-                if (sy >= 0) {  // y (c_y was < 0, listed) leaves: the last entry takes its place
-                    const int at = pos[y], last = s_nneg - 1, wl = neg[last];
-                    neg[at] = (int16_t)wl;
-                    pos[wl] = (int16_t)at;
-                    pos[y] = -1;
-                    s_nneg = last;
-                }
-                jx[jb] = (int16_t)y;
+                cdp[y] = sy > 0 ? rb_approx(cy.a, cy.b, rho_d) : -INFINITY;
+                jx[bj] = (int16_t)y;
                 if (a.log != nullptr && moves < a.log_cap) {
-                    a.log[2 * ((int64_t)p * a.log_cap + moves)] = jb;
+                    a.log[2 * ((int64_t)p * a.log_cap + moves)] = bj;
                     a.log[2 * ((int64_t)p * a.log_cap + moves) + 1] = y;
                 }
+                // y (c_y was < 0, listed) leaves when c_y >= 0: the last entry
+                // takes its place; x (c_x was > 0) joins when c_x < 0, appended
+                int nn = nneg;
+                if (sy >= 0) {
+                    neg[at_y] = (int16_t)wl;
+                    pos[wl] = (int16_t)at_y;
+                    pos[y] = -1;
+                    nn -= 1;
+                }
+                if (sx < 0) {
+                    pos[x] = (int16_t)nn;
+                    neg[nn] = (int16_t)x;
+                    nn += 1;
+                }
+                s_nneg = nn;
+                s_S = S1;
             }
         }
         moves += 1;
-        __syncthreads();  // the move is applied before the next step reads the lists
+        __syncthreads();  // the move is applied before the next step reads the state
     }
+    if (wv != 0) return;
     // final errors and workers
-    for (int y = tid; y < W; y += RB_THREADS) {
+    for (int y = lane; y < W; y += 64) {
         a.le[pr.wbase + y] = cle[y];
         a.be[pr.wbase + y] = cbe[y];
     }
-    for (int j = tid; j < n; j += RB_THREADS) a.new_worker[pr.new0 + j] = jx[j];
-    const RbPair obj1 = rb_objective(cle, cbe, W, rho, red);
-    if (tid == 0) {
+    for (int j = lane; j < n; j += 64) {
+        const int x = jx[j];
+        a.new_worker[pr.new0 + j] = x == W ? -1 : x;
+    }
+    const RbPair obj1 = rb_objective(cle, cbe, W, rho);
+    if (lane == 0) {
         if (a.moves != nullptr) a.moves[p] = moves;
         if (a.obj != nullptr) {
             a.obj[4 * p] = obj0.a;
@@ -401,12 +624,17 @@ __global__ __launch_bounds__(RB_THREADS) void k_rb_moves(RbArgs a)
     }
 }
 
+size_t rb_moves_lds(int32_t wmax, int32_t jmax)
+{
+    return (size_t)wmax * (8 + 8 + 4 + 2 + 2) + 8 + (size_t)jmax * (4 + 2) + RB_WAVES * RB_LIST * 2;
+}
+
 hipError_t launch_rebalance(const RbArgs& a, hipStream_t stream)
 {
     hipLaunchKernelGGL(k_rb_errors, dim3(a.nchunk + a.P), dim3(RB_ETHREADS), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_rb_moves, dim3(a.P), dim3(RB_THREADS), 0, stream, a);
+    hipLaunchKernelGGL(k_rb_moves, dim3(a.P), dim3(64 * RB_WAVES), rb_moves_lds(a.wmax, a.jmax), stream, a);
     return hipGetLastError();
 }
 

@@ -55,6 +55,9 @@ SMALL = [
     ("many workers", 1, 4096, 2, 64, 0.9),
     ("most new requests", 1, 40, 8, 8192, 0.7),
     ("no prediction error", 2, 16, 30, 100, 0.0),
+    # the largest problem the library takes (4096 workers, 8192 new requests):
+    # the moves kernel's LDS at its maximum
+    ("largest problem", 2, [4096, 8], [1, 3], [8192, 10], 0.02),
 ]
 
 
