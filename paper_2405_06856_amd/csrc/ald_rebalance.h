@@ -11,7 +11,6 @@ constexpr int RB_JMAX = 8192;     // new requests per problem
 constexpr int RB_ETHREADS = 256;  // threads per error-accumulation block
 constexpr int RB_CHUNK = 2048;    // ongoing requests per error-accumulation block
 constexpr int32_t RB_LEN_MAX = 1 << 24;
-constexpr int RB_LIST = 1024;     // requests near the top gain taken exactly per chunk and wave
 constexpr int RB_WAVES = 4;       // waves per problem in the moves kernel
 
 // rho = c2 / k2 of one problem, held so that the sign of a + rho * b (integer

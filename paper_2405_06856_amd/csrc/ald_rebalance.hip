@@ -265,25 +265,37 @@ __device__ __forceinline__ double rb_half_gain(double dd, double cxd, double cmd
 // The same half decrease as an exact pair; the two signs it branches on are
 // read off the stand-ins when they clear the margin (their error is below
 // 9 u S), else taken exactly.
-__device__ __forceinline__ RbPair rb_half_gain_exact(RbPair cx, double cxd, RbPair cm, double cmd, int64_t l,
-                                                     double dd, double tol, const RbRho& rho)
+// With M = -c_min, the half decrease is min(d, c_x) - max(0, d - M) <= M,
+// with equality exactly when M <= d <= c_x: such a request (`plateau`) holds
+// the largest decrease of all.
+struct RbHalfGain {
+    RbPair g;
+    bool plateau;
+};
+__device__ __forceinline__ RbHalfGain rb_half_gain_exact(RbPair cx, double cxd, RbPair cm, double cmd, int64_t l,
+                                                         double dd, double tol, const RbRho& rho)
 {
     const RbPair d{l, 1};
     const double t1 = dd - cxd, t2 = dd + cmd;
-    const bool d_le_cx = t1 < -tol || (t1 <= tol && rp_sign(rp_sub(d, cx), rho) <= 0);
-    const bool spill = t2 > tol || (t2 >= -tol && rp_sign(rp_add(d, cm), rho) > 0);
-    const RbPair mn = d_le_cx ? d : cx;
-    return spill ? rp_sub(mn, rp_add(d, cm)) : mn;
+    const int s1 = t1 < -tol ? -1 : (t1 > tol ? 1 : rp_sign(rp_sub(d, cx), rho));  // sign of d - c_x
+    const int s2 = t2 < -tol ? -1 : (t2 > tol ? 1 : rp_sign(rp_add(d, cm), rho));  // sign of d - M
+    const RbPair mn = s1 <= 0 ? d : cx;
+    return RbHalfGain{s2 > 0 ? rp_sub(mn, rp_add(d, cm)) : mn, s1 <= 0 && s2 >= 0};
 }
 
-// Wave-wide choice among lanes that hold an exact candidate (o != INT32_MAX):
-// with one such lane its value is read, otherwise a butterfly with `better`.
+// Wave-wide choice among lanes that hold an exact candidate (o != INT32_MAX),
+// by the strict order `better`; `key` is the candidate's fp64 stand-in,
+// larger for better ones.  A few candidates are taken in turn with uniform
+// operands.  Otherwise the lane with the largest key (lowest index on equal
+// keys) is the champion, every lane compares itself with it exactly, and the
+// search goes on among those that beat it: the champion improves every round,
+// and ties (equal pairs) and near ties settle in one or two.
 template <typename Better>
-__device__ __forceinline__ void rb_pick(RbPair& v, int32_t& o, Better better)
+__device__ __forceinline__ void rb_pick(RbPair& v, int32_t& o, double key, Better better)
 {
     uint64_t m = ballot(o != INT32_MAX);
     if (m == 0) return;
-    if (__popcll(m) <= 6) {  // a few: in turn, with uniform operands
+    if (__popcll(m) <= 4) {
         int l = __ffsll((unsigned long long)m) - 1;
         RbPair bv{rdlane64s(v.a, l), rdlane64s(v.b, l)};
         int32_t bo = rdlane(o, l);
@@ -302,33 +314,38 @@ __device__ __forceinline__ void rb_pick(RbPair& v, int32_t& o, Better better)
         o = bo;
         return;
     }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const RbPair ov = shfl_pair(v, off);
-        const int32_t oo = __shfl_xor(o, off, 64);
-        if (better(ov, oo, v, o)) {
-            v = ov;
-            o = oo;
+    bool in = o != INT32_MAX;
+    for (;;) {
+        const double kmax = wave_max_f64(in ? key : -INFINITY);
+        const int32_t omin = wave_min_i32(in && key == kmax ? o : INT32_MAX);
+        const int l = __ffsll((unsigned long long)ballot(in && key == kmax && o == omin)) - 1;
+        const RbPair cv{rdlane64s(v.a, l), rdlane64s(v.b, l)};
+        const int32_t co = rdlane(o, l);
+        in = in && better(v, o, cv, co);
+        if (!ballot(in)) {
+            v = cv;
+            o = co;
+            return;
         }
     }
-    v = RbPair{rdlane64s(v.a, 0), rdlane64s(v.b, 0)};
-    o = rdlane(o, 0);
 }
 
 // One block of RB_WAVES waves per problem.  LDS (sized by the launch for its
 // largest problem): c_y as the exact pair (cle, cbe), the fp64 stand-in of
-// every positive c_y, the receivers list, each new request's length and
-// current worker, and per wave a list of requests near the top gain.  A step:
+// every positive c_y, the receivers list, and each new request's length and
+// current worker.  A step:
 // every wave finds c_min (the same result in each), takes the gains of its
 // share of the requests and its best candidate; the waves' results meet in
 // LDS; wave 0 finds the receiver and applies the move.  Three block barriers
 // per step.
+template <int JT>  // new requests per lane: at least jmax / (64 RB_WAVES)
 __global__ __launch_bounds__(64 * RB_WAVES) void k_rb_moves(RbArgs a)
 {
     extern __shared__ __align__(16) unsigned char rb_lds[];
     __shared__ double x_g[RB_WAVES];              // each wave's largest stand-in gain
     __shared__ int64_t x_a[RB_WAVES], x_b[RB_WAVES];  // each wave's best exact gain
     __shared__ int32_t x_j[RB_WAVES];             // and its request
+    __shared__ int32_t x_p[RB_WAVES];             // each wave's lowest request on the plateau
     __shared__ double s_S;                        // bound on |a| + rho |b| over the values compared
     __shared__ int32_t s_nneg;                    // receivers listed
     __shared__ int32_t s_err;
@@ -352,7 +369,6 @@ __global__ __launch_bounds__(64 * RB_WAVES) void k_rb_moves(RbArgs a)
     int16_t* jx = (int16_t*)(jl + Jm);  // current worker of each new request (W: unplaced)
     int16_t* neg = jx + Jm;    // the workers with c < 0, in no particular order
     int16_t* pos = neg + Wm;   // index of a worker in neg (-1: not there)
-    int16_t* lst = pos + Wm + wv * RB_LIST;  // this wave's requests near the top gain, a chunk at a time
     const int64_t max_moves = 4 * (int64_t)n + W;  // a guard; every move lowers sum |c| strictly
     const uint64_t below = (1ull << lane) - 1;
     auto lower = [&](RbPair u, int32_t uy, RbPair v, int32_t vy) { return rb_lower(u, uy, v, vy, rho); };
@@ -418,15 +434,18 @@ __global__ __launch_bounds__(64 * RB_WAVES) void k_rb_moves(RbArgs a)
         // ---- c_min and the lowest worker index at it (every wave alike)
         double m1 = INFINITY, m2 = INFINITY;
         int32_t y1 = INT32_MAX;
+        RbPair p1{0, 0};
         for (int k = lane; k < nneg; k += 64) {
             const int32_t y = neg[k];
-            const double v = rb_approx(cle[y], cbe[y], rho_d);
-            if (v < m1) {
+            const RbPair v{cle[y], cbe[y]};
+            const double vd = rb_approx(v.a, v.b, rho_d);
+            if (vd < m1) {
                 m2 = m1;
-                m1 = v;
+                m1 = vd;
                 y1 = y;
+                p1 = v;
             } else {
-                m2 = fmin(m2, v);
+                m2 = fmin(m2, vd);
             }
         }
         const double cthr = wave_min_f64(m1) + 2.0 * tol;
@@ -443,30 +462,35 @@ __global__ __launch_bounds__(64 * RB_WAVES) void k_rb_moves(RbArgs a)
                 }
             }
         } else if (m1 <= cthr) {
-            cm = RbPair{cle[y1], cbe[y1]};
+            cm = p1;
             ci = y1;
         }
-        rb_pick(cm, ci, lower);
+        rb_pick(cm, ci, -rb_approx(cm.a, cm.b, rho_d), lower);
         const double cmd = rb_approx(cm.a, cm.b, rho_d);
 
-        // ---- this wave's share of the requests: per lane the two best
-        // stand-in gains (lower index first on equal values) and the third; a
-        // request that cannot move has gain -inf
+        // ---- this wave's share of the requests, j = jw + t * 64 * RB_WAVES:
+        // their stand-in gains stay in registers (a request that cannot move
+        // has gain -inf)
         const int jw = wv * 64 + lane;
-        double g1 = -INFINITY, g2 = -INFINITY, g3 = -INFINITY;
-        int32_t j1 = INT32_MAX, j2 = INT32_MAX;
-#pragma unroll 4
-        for (int j = jw; j < n; j += 64 * RB_WAVES) {
-            const double g = rb_half_gain((double)jl[j] + rho_d, cdp[jx[j]], cmd);
-            const bool t1 = g > g1, t2 = g > g2;
-            g3 = t2 ? g2 : fmax(g3, g);
-            g2 = t1 ? g1 : (t2 ? g : g2);
-            j2 = t1 ? j1 : (t2 ? j : j2);
-            g1 = t1 ? g : g1;
-            j1 = t1 ? j : j1;
+        const int tn = n > wv * 64 ? (n - wv * 64 + 64 * RB_WAVES - 1) / (64 * RB_WAVES) : 0;  // wave-uniform
+        double gq[JT], cq[JT];  // stand-in gain and c_x of each request
+        int32_t xq[JT], lq[JT];  // its worker and length
+        double gl = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < JT; ++t) {
+            const int j = jw + t * 64 * RB_WAVES;
+            const bool in = t < tn && j < n;
+            xq[t] = in ? jx[j] : W;
+            lq[t] = in ? jl[j] : 1;
+        }
+#pragma unroll
+        for (int t = 0; t < JT; ++t) {
+            cq[t] = cdp[xq[t]];
+            gq[t] = rb_half_gain((double)lq[t] + rho_d, cq[t], cmd);
+            gl = fmax(gl, gq[t]);
         }
         {
-            const double gw = wave_max_f64(g1);
+            const double gw = wave_max_f64(gl);
             if (lane == 0) x_g[wv] = gw;
         }
         __syncthreads();
@@ -474,68 +498,62 @@ __global__ __launch_bounds__(64 * RB_WAVES) void k_rb_moves(RbArgs a)
 #pragma unroll
         for (int w = 1; w < RB_WAVES; ++w) gmax = fmax(gmax, x_g[w]);
         if (!(gmax + tol > 0.0)) break;  // every exact gain is <= 0 (or nothing can move)
+        // every request whose stand-in lies within twice the margin of the top
+        // may hold the largest exact gain: those of this lane, exactly, in
+        // increasing j (ties are common: equal lengths give equal gains)
         const double gthr = gmax - 2.0 * tol;
         RbPair bg{0, 0};
-        int32_t bj = INT32_MAX;
-        auto exact = [&](int j) {
-            const int x = jx[j];
-            const int32_t l = jl[j];
-            return rb_half_gain_exact(RbPair{cle[x], cbe[x]}, cdp[x], cm, cmd, l, (double)l + rho_d, tol, rho);
-        };
-        if (ballot(g3 >= gthr)) {
-            // three or more near the top in some lane (ties are common: equal
-            // lengths give equal gains): list this wave's requests near the
-            // top, a chunk at a time, and take them exactly one per lane
-            constexpr int STRIDE = 64 * RB_WAVES;
-            for (int c0 = wv * 64; c0 < n; c0 += STRIDE * (RB_LIST / 64)) {
-                int cnt = 0;
-                for (int t = 0; t < RB_LIST / 64; ++t) {
-                    const int j = c0 + t * STRIDE + lane;
-                    const bool near = j < n && rb_half_gain((double)jl[j] + rho_d, cdp[jx[j]], cmd) >= gthr;
-                    const uint64_t m = ballot(near);
-                    if (near) lst[cnt + __popcll(m & below)] = (int16_t)j;
-                    cnt += __popcll(m);
-                }
-                __builtin_amdgcn_wave_barrier();
-                for (int k = lane; k < cnt; k += 64) {
-                    const int j = lst[k];
-                    const RbPair g = exact(j);
-                    if (better(g, j, bg, bj)) {
-                        bg = g;
-                        bj = j;
-                    }
-                }
-                __builtin_amdgcn_wave_barrier();
-            }
-        } else {
-            if (g1 >= gthr) {
-                bg = exact(j1);
-                bj = j1;
-            }
-            if (g2 >= gthr) {
-                const RbPair g = exact(j2);
-                if (better(g, j2, bg, bj)) {
-                    bg = g;
-                    bj = j2;
+        int32_t bj = INT32_MAX, pj = INT32_MAX;  // best candidate; lowest request on the plateau
+        int64_t ca[JT];
+        int32_t cb[JT];
+#pragma unroll
+        for (int t = 0; t < JT; ++t) {  // the exact c_x of every candidate, loads issued together
+            const bool nr = gq[t] >= gthr;
+            ca[t] = nr ? cle[xq[t]] : 0;
+            cb[t] = nr ? cbe[xq[t]] : 0;
+        }
+#pragma unroll
+        for (int t = 0; t < JT; ++t) {
+            if (gq[t] >= gthr) {
+                const int j = jw + t * 64 * RB_WAVES;
+                const int32_t l = lq[t];
+                const RbHalfGain h =
+                    rb_half_gain_exact(RbPair{ca[t], cb[t]}, cq[t], cm, cmd, l, (double)l + rho_d, tol, rho);
+                pj = (h.plateau && j < pj) ? j : pj;
+                if (!h.plateau && better(h.g, j, bg, bj)) {
+                    bg = h.g;
+                    bj = j;
                 }
             }
         }
-        rb_pick(bg, bj, better);
+        // a plateau request anywhere settles the step (the lowest such index);
+        // otherwise the best candidate of each wave, then of the block
+        const int32_t pw = wave_min_i32(pj);
+        if (pw == INT32_MAX) rb_pick(bg, bj, rb_approx(bg.a, bg.b, rho_d), better);
         if (lane == 0) {
             x_a[wv] = bg.a;
             x_b[wv] = bg.b;
             x_j[wv] = bj;
+            x_p[wv] = pw;
         }
         __syncthreads();
-        bg = RbPair{x_a[0], x_b[0]};
-        bj = x_j[0];
+        int32_t pb = x_p[0];
 #pragma unroll
-        for (int w = 1; w < RB_WAVES; ++w) {
-            const RbPair g{x_a[w], x_b[w]};
-            const int32_t j = x_j[w];
-            if (better(g, j, bg, bj)) {
-                bg = g;
-                bj = j;
+        for (int w = 1; w < RB_WAVES; ++w) pb = min(pb, x_p[w]);
+        if (pb != INT32_MAX) {
+            bg = RbPair{-cm.a, -cm.b};
+            bj = pb;
+        } else {
+            bg = RbPair{x_a[0], x_b[0]};
+            bj = x_j[0];
+#pragma unroll
+            for (int w = 1; w < RB_WAVES; ++w) {
+                const RbPair g{x_a[w], x_b[w]};
+                const int32_t j = x_j[w];
+                if (better(g, j, bg, bj)) {
+                    bg = g;
+                    bj = j;
+                }
             }
         }
         if (bj == INT32_MAX || rp_sign(bg, rho) <= 0) break;  // no move lowers the objective
@@ -626,7 +644,7 @@ __global__ __launch_bounds__(64 * RB_WAVES) void k_rb_moves(RbArgs a)
 
 size_t rb_moves_lds(int32_t wmax, int32_t jmax)
 {
-    return (size_t)wmax * (8 + 8 + 4 + 2 + 2) + 8 + (size_t)jmax * (4 + 2) + RB_WAVES * RB_LIST * 2;
+    return (size_t)wmax * (8 + 8 + 4 + 2 + 2) + 8 + (size_t)jmax * (4 + 2);
 }
 
 hipError_t launch_rebalance(const RbArgs& a, hipStream_t stream)
@@ -634,7 +652,17 @@ hipError_t launch_rebalance(const RbArgs& a, hipStream_t stream)
     hipLaunchKernelGGL(k_rb_errors, dim3(a.nchunk + a.P), dim3(RB_ETHREADS), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_rb_moves, dim3(a.P), dim3(64 * RB_WAVES), rb_moves_lds(a.wmax, a.jmax), stream, a);
+    const size_t lds = rb_moves_lds(a.wmax, a.jmax);
+    const int per_lane = (a.jmax + 64 * RB_WAVES - 1) / (64 * RB_WAVES);
+    static_assert(RB_JMAX <= 32 * 64 * RB_WAVES, "the widest variant covers RB_JMAX");
+    if (per_lane <= 4)
+        hipLaunchKernelGGL(k_rb_moves<4>, dim3(a.P), dim3(64 * RB_WAVES), lds, stream, a);
+    else if (per_lane <= 8)
+        hipLaunchKernelGGL(k_rb_moves<8>, dim3(a.P), dim3(64 * RB_WAVES), lds, stream, a);
+    else if (per_lane <= 16)
+        hipLaunchKernelGGL(k_rb_moves<16>, dim3(a.P), dim3(64 * RB_WAVES), lds, stream, a);
+    else
+        hipLaunchKernelGGL(k_rb_moves<32>, dim3(a.P), dim3(64 * RB_WAVES), lds, stream, a);
     return hipGetLastError();
 }
 

@@ -53,6 +53,7 @@ SMALL = [
     ("mixed sizes", 4, [3, 64, 17, 1], [0, 9, 40, 3], [50, 0, 300, 7], 0.6),
     ("several waves of requests", 2, 33, 20, 2000, 0.7),
     ("many workers", 1, 4096, 2, 64, 0.9),
+    ("3000 new requests", 2, 24, 6, [3000, 40], 0.7),
     ("most new requests", 1, 40, 8, 8192, 0.7),
     ("no prediction error", 2, 16, 30, 100, 0.0),
     # the largest problem the library takes (4096 workers, 8192 new requests):
