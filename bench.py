@@ -90,7 +90,7 @@ def host_cores() -> int:
         return os.cpu_count() or 1
 
 
-def cpu_baseline(trace, budget_s: float = 12.0, max_q: int = 8192):
+def cpu_baseline(trace, budget_s: float = 20.0, max_q: int = 16384):
     """The oracle as it stands, one thread, on the first n queries of the stream
     (n doubled until one run takes at least half the budget)."""
     from oracle import ref
