@@ -5,12 +5,14 @@ from __future__ import annotations
 
 import os
 import subprocess
+import sys
 
 import pytest
 
 from oracle import ref
 from tests import test_oracle as pins
 
+HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = open(ref.SRC).read()
 
 # (name, original text, planted mistake)
@@ -134,21 +136,52 @@ def test_mutant_table_applies():
         assert SRC.count(old) >= 1, name
 
 
-@pytest.mark.parametrize("idx", range(len(MUTANTS)), ids=[m[0] for m in MUTANTS])
-def test_pins_catch_planted_mistake(idx, tmp_path, monkeypatch):
+def first_catch(idx: int, workdir: str) -> str:
+    """Build the oracle with mutant idx planted and run the pins until one
+    fails; the failing pin's name, or "" when none does."""
     name, old, new = MUTANTS[idx]
-    src = tmp_path / "mutant.c"
-    src.write_text(SRC.replace(old, new, 1))
-    lib = tmp_path / "libmutant.so"
+    src = os.path.join(workdir, "mutant.c")
+    with open(src, "w") as f:
+        f.write(SRC.replace(old, new, 1))
+    lib = os.path.join(workdir, "libmutant.so")
     subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-fPIC",
-                           "-shared", "-o", str(lib), str(src), "-lm"])
-    monkeypatch.setattr(ref, "SRC", str(src))
-    monkeypatch.setattr(ref, "LIB", str(lib))
-    monkeypatch.setattr(ref, "_lib", None)
-    caught = []
-    for pin in PINS:
+                           "-shared", "-o", lib, src, "-lm"])
+    ref.SRC, ref.LIB, ref._lib = src, lib, None
+    for pin in PINS:  # the first pin that fails is enough
         try:
             pin()
         except Exception as e:  # AssertionError, or an oracle error code
-            caught.append(getattr(pin, "__name__", "bruteforce") + ": " + type(e).__name__)
-    assert caught, "no pin caught the planted mistake: " + name
+            return getattr(pin, "__name__", "bruteforce") + ": " + type(e).__name__
+    return ""
+
+
+@pytest.fixture(scope="module")
+def catches(tmp_path_factory):
+    """Every mutant, each in a process of its own (a few at a time)."""
+    from concurrent.futures import ThreadPoolExecutor
+    root = os.path.dirname(HERE)
+    env = dict(os.environ, PYTHONPATH=root + os.pathsep + os.environ.get("PYTHONPATH", ""), OMP_NUM_THREADS="1")
+    env.pop("ORACLE_LIB", None)
+
+    def run(idx):
+        d = tmp_path_factory.mktemp("mutant%d" % idx)
+        out = subprocess.run([sys.executable, __file__, str(idx), str(d)], cwd=root, env=env, capture_output=True,
+                             text=True, timeout=600)
+        if out.returncode != 0:
+            return "runner failed: " + out.stderr[-400:]
+        return out.stdout.strip().splitlines()[-1] if out.stdout.strip() else ""
+
+    workers = max(1, min(8, len(os.sched_getaffinity(0))))
+    with ThreadPoolExecutor(workers) as ex:
+        return list(ex.map(run, range(len(MUTANTS))))
+
+
+@pytest.mark.parametrize("idx", range(len(MUTANTS)), ids=[m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(idx, catches):
+    name = MUTANTS[idx][0]
+    assert catches[idx] and not catches[idx].startswith("runner failed"), \
+        "no pin caught the planted mistake: %s (%s)" % (name, catches[idx])
+
+
+if __name__ == "__main__":  # one mutant: python tests/test_oracle_mutants.py IDX WORKDIR
+    print(first_catch(int(sys.argv[1]), sys.argv[2]))
