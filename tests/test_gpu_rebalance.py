@@ -86,6 +86,23 @@ def test_rebalance_models_per_problem(ev):
     check_against_oracle(b, got)
 
 
+def test_rebalance_extreme_rho(ev):
+    """rho exactly 500 (pairs such as (1000, 0) and (500, 1) then tie exactly,
+    and the lowest index decides), about 10^9 (the largest ratio taken) and
+    10^-12 (the batch term only breaks ties of lengths)."""
+    from fractions import Fraction
+    b = wl.make_rebalance("extreme rho", 61, 3, [40, 40, 40], [12, 12, 12], [300, 300, 300], sigma_err=0.7)
+    base = b.models[0]
+    b.models = [dataclasses.replace(base, k2=2.0 ** -22, c2=500 * 2.0 ** -22),
+                dataclasses.replace(base, k2=1e-12, c2=999999999.5e-12),
+                dataclasses.replace(base, k2=1.0, c2=1e-12)]
+    rhos = [Fraction(m.c2) / Fraction(m.k2) for m in b.models]
+    assert rhos[0] == 500 and abs(rhos[1] - 10 ** 9) < 1 and rhos[2] < Fraction(1, 10 ** 11)
+    got = ev.rebalance(b, want_log=True)
+    assert int(got["moves"].sum()) > 0
+    check_against_oracle(b, got)
+
+
 def test_rebalance_full_size(ev):
     """The 256-problem workload in the launch the benchmark times: every 16th
     problem against the oracle (the exhaustive oracle takes about half a second
