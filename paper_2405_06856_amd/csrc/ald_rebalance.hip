@@ -567,7 +567,8 @@ __global__ __launch_bounds__(64 * RB_WAVES) void k_rb_moves(RbArgs a)
             const RbPair d{(int64_t)jl[bj], 1};
             const double dd = (double)d.a + rho_d;
             int32_t y = ci;
-            if (rp_sign(rp_add(cm, d), rho) <= 0) {
+            // on the plateau d >= M, so no worker but those at c_min has c <= -d
+            if (pb == INT32_MAX && rp_sign(rp_add(cm, d), rho) <= 0) {
                 int32_t lo = INT32_MAX;
                 for (int k = lane; k < nneg; k += 64) {
                     const int32_t w = neg[k];
