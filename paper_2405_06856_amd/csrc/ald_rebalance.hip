@@ -566,6 +566,8 @@ __global__ __launch_bounds__(64 * RB_WAVES) void k_rb_moves(RbArgs a)
             // ---- the receiver: the workers at c_min, or the lowest-index one with c <= -d
             const RbPair d{(int64_t)jl[bj], 1};
             const double dd = (double)d.a + rho_d;
+            const int x = jx[bj];  // (its loads go out before the receiver's)
+            const RbPair cx = rp_sub(RbPair{cle[x], cbe[x]}, d);
             int32_t y = ci;
             // on the plateau d >= M, so no worker but those at c_min has c <= -d
             if (pb == INT32_MAX && rp_sign(rp_add(cm, d), rho) <= 0) {
@@ -581,20 +583,21 @@ __global__ __launch_bounds__(64 * RB_WAVES) void k_rb_moves(RbArgs a)
                 y = wave_min_i32(lo);
             }
             // ---- apply (every lane computes the same values; lane 0 writes them)
-            const int x = jx[bj];
-            const RbPair cx = rp_sub(RbPair{cle[x], cbe[x]}, d);
             const RbPair cy = rp_add(RbPair{cle[y], cbe[y]}, d);
-            const int sx = rp_sign(cx, rho), sy = rp_sign(cy, rho);
+            // signs from the stand-ins where they clear the margin
+            const double vx = rb_approx(cx.a, cx.b, rho_d), vy = rb_approx(cy.a, cy.b, rho_d);
+            const int sx = vx > tol ? 1 : (vx < -tol ? -1 : rp_sign(cx, rho));
+            const int sy = vy > tol ? 1 : (vy < -tol ? -1 : rp_sign(cy, rho));
             const double S1 = fmax(S, fmax(rb_mag(cx.a, cx.b, rho_d), rb_mag(cy.a, cy.b, rho_d)) * (1.0 + 0x1p-40));
             const int at_y = pos[y], last = nneg - 1, wl = neg[last];
             __builtin_amdgcn_wave_barrier();
             if (lane == 0) {
                 cle[x] = cx.a;
                 cbe[x] = (int32_t)cx.b;
-                cdp[x] = sx > 0 ? rb_approx(cx.a, cx.b, rho_d) : -INFINITY;
+                cdp[x] = sx > 0 ? vx : -INFINITY;
                 cle[y] = cy.a;
                 cbe[y] = (int32_t)cy.b;
-                cdp[y] = sy > 0 ? rb_approx(cy.a, cy.b, rho_d) : -INFINITY;
+                cdp[y] = sy > 0 ? vy : -INFINITY;
                 jx[bj] = (int16_t)y;
                 if (a.log != nullptr && moves < a.log_cap) {
                     a.log[2 * ((int64_t)p * a.log_cap + moves)] = bj;
