@@ -379,9 +379,9 @@ __device__ __forceinline__ int64_t dirty_kv_peak(const State& st, CommitLDS& L, 
 // tile-start bit for query i is set in `words` (feasibility or near tie): for
 // them the tile-start results are still exact.  With `listed`, only workers of
 // the kind the selection lists (with interchangeable empty workers, the
-// non-empty ones).  The whole wave scans the scenario's bit words, eight
-// batches of 64 workers at a time; every lane gets (key, worker), worker -1
-// when there is none.
+// non-empty ones).  The whole wave scans the scenario's bit words and rank
+// keys, sixteen batches of 64 workers at a time; every lane gets (key, worker),
+// worker -1 when there is none.
 struct KeyW {
     uint64_t k;
     int32_t w;
@@ -393,20 +393,22 @@ __device__ __forceinline__ KeyW best_untouched(const uint64_t* words, const uint
     const uint64_t* row = words + row0;
     uint64_t k = 0;
     int32_t w = -1;
-    for (int b0 = 0; b0 < W; b0 += 64 * 8) {
-        uint64_t wd[8];
+    for (int b0 = 0; b0 < W; b0 += 64 * 16) {
+        // the words and the rank keys of the batch in one round trip
+        uint64_t wd[16], kd[16];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < 16; ++u) {
             const int ww = b0 + u * 64 + lane;
             wd[u] = ww < W ? row[ww] : 0;
+            kd[u] = ww < W ? keys[ww] : 0;
         }
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < 16; ++u) {
             const int ww = b0 + u * 64 + lane;
             bool ok = (wd[u] >> bit) & 1;
             if (!ballot(ok)) continue;
             ok = ok && !dirty_w(*L, W, nd, ww);
-            const uint64_t kk = ok ? keys[ww] : 0;
+            const uint64_t kk = ok ? kd[u] : 0;
             ok = ok && !(listed && uniform_M && kk == 0);
             const bool take = ok && ranks_before(kk, ww, k, w);
             k = take ? kk : k;
