@@ -522,9 +522,11 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
         return r;
     }
 
-    // ---- with diagnostics: every dirty candidate is scanned
-    bool cand = unknown;
-    bool feas_now = false;
+    // ---- with diagnostics: the feasibility of every dirty candidate; a worker
+    // whose peak bound plus the query's own demand fits needs no scan
+    const bool sure = unknown && (int64_t)a.pub + lin + lp <= (int64_t)a.M;
+    bool cand = unknown && !sure;
+    bool feas_now = sure;
     for (;;) {
         const int bl = wave_best_lane(a.key, a.w, cand);
         if (bl < 0) break;
@@ -593,6 +595,15 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
     // the chosen worker's figures
     if (r.w >= 0) {
         if (r.lane >= 0) {
+            if (!((ballot(sn.done) >> r.lane) & 1)) {  // chosen on its bound: its exact peak now
+                int32_t p0;
+                const int64_t pk = dirty_kv_peak(st, L, a, r.lane, hot, hotBs, hotm, sq, eq, &p0);
+                if (lane == r.lane) {
+                    sn.done = true;
+                    sn.pk = (int32_t)pk;
+                    sn.p0 = p0;
+                }
+            }
             r.d.kv_peak_chosen = rdlane(sn.pk, r.lane);
             r.d.ttft_chosen = rdlane_f64(Lt.ttft, r.lane);
             r.d.tdec_chosen = rdlane_f64(Lt.tdec, r.lane);
