@@ -387,7 +387,7 @@ struct KeyW {
     int32_t w;
 };
 __device__ __forceinline__ KeyW best_untouched(const uint64_t* words, const uint64_t* keys, const CommitLDS* L, int W,
-                                            int nd, int64_t row0, int bit, bool listed, bool uniform_M)
+                                            int nd, int64_t row0, int bit, bool listed, bool uniform_M, bool dpp)
 {
     const int lane = lane_id();
     const uint64_t* row = words + row0;
@@ -414,6 +414,16 @@ __device__ __forceinline__ KeyW best_untouched(const uint64_t* words, const uint
             k = take ? kk : k;
             w = take ? ww : w;
         }
+    }
+    // the best over the lanes (the largest key, then the lowest index), by
+    // DPP scans or by a shuffle butterfly: the same result; which form leaves
+    // the caller more scalar registers depends on the kernel variant (`dpp`)
+    if (dpp) {
+        const bool valid = w >= 0;
+        const uint64_t kmax = wave_max_u64(valid ? k : 0);
+        const bool top = valid && k == kmax;
+        const int32_t wmin = wave_min32(top ? w : INT32_MAX);
+        return ballot(top) ? KeyW{kmax, wmin} : KeyW{0, -1};
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
@@ -465,7 +475,7 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
     if (!have && q.ncand > TOPK) {  // every listed candidate was committed to: the best untouched one
         const KeyW c = best_untouched(st.bits_feas, st.key + sc.wbase, &L, sc.W, nd,
                                       sc.bits_off + (int64_t)((i - start) >> 6) * sc.W, (i - start) & 63, true,
-                                      sc.uniform_M != 0);
+                                      sc.uniform_M != 0, !want_diag);
         have = c.w >= 0;
         bk = have ? c.k : bk;
         bw = have ? c.w : bw;
@@ -584,7 +594,7 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
         } else {  // the best near-tie worker was committed to: the best untouched one with a near tie
             const KeyW c = best_untouched(st.bits_nt, st.key + sc.wbase, &L, sc.W, nd,
                                           sc.bits_off + (int64_t)((i - start) >> 6) * sc.W, (i - start) & 63, false,
-                                          sc.uniform_M != 0);
+                                          sc.uniform_M != 0, !want_diag);
             nt = c.w >= 0 && !ranks_before(bk, bw, c.k, c.w);
             r.fallback = 1;
         }

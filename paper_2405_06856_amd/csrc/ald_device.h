@@ -317,7 +317,33 @@ struct Or32 {
 struct Max32 {
     __device__ int32_t operator()(int32_t a, int32_t b) const { return a > b ? a : b; }
 };
+struct Min32 {
+    __device__ int32_t operator()(int32_t a, int32_t b) const { return a < b ? a : b; }
+};
 __device__ __forceinline__ int32_t wave_sum32(int32_t v) { return rdlane(wave_incl_scan(v, 0, Add32()), 63); }
+__device__ __forceinline__ int32_t wave_min32(int32_t v) { return rdlane(wave_incl_scan(v, INT32_MAX, Min32()), 63); }
+// Largest 64-bit unsigned value over the 64 lanes: the same scan on both
+// halves of the word, the comparison on the whole word.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t ident, uint64_t x)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)ident, (int)(uint32_t)x, CTRL, ROW_MASK,
+                                                              0xf, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)(ident >> 32), (int)(uint32_t)(x >> 32),
+                                                              CTRL, ROW_MASK, 0xf, false);
+    return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x)
+{
+    auto mx = [](uint64_t a, uint64_t b) { return a > b ? a : b; };
+    x = mx(x, dpp_u64<0x111, 0xf>(0, x));  // row_shr:1
+    x = mx(x, dpp_u64<0x112, 0xf>(0, x));  // row_shr:2
+    x = mx(x, dpp_u64<0x114, 0xf>(0, x));  // row_shr:4
+    x = mx(x, dpp_u64<0x118, 0xf>(0, x));  // row_shr:8
+    x = mx(x, dpp_u64<0x142, 0xa>(0, x));  // row_bcast:15
+    x = mx(x, dpp_u64<0x143, 0xc>(0, x));  // row_bcast:31
+    return rdlane64(x, 63);
+}
 __device__ __forceinline__ int32_t wave_max32(int32_t v) { return rdlane(wave_incl_scan(v, INT32_MIN, Max32()), 63); }
 __device__ __forceinline__ uint64_t wave_or64(uint64_t v)
 {

@@ -242,10 +242,7 @@ __device__ __forceinline__ double wave_ext_f64(double x)
 }
 __device__ __forceinline__ double wave_max_f64(double v) { return wave_ext_f64<true>(v); }
 __device__ __forceinline__ double wave_min_f64(double v) { return wave_ext_f64<false>(v); }
-struct Min32 {
-    __device__ int32_t operator()(int32_t a, int32_t b) const { return a < b ? a : b; }
-};
-__device__ __forceinline__ int32_t wave_min_i32(int32_t v) { return rdlane(wave_incl_scan(v, INT32_MAX, Min32()), 63); }
+__device__ __forceinline__ int32_t wave_min_i32(int32_t v) { return wave_min32(v); }
 
 // sum |c| over the problem's workers (whole wave; every lane gets it)
 __device__ RbPair rb_objective(const int64_t* cle, const int32_t* cbe, int W, const RbRho& rho)
