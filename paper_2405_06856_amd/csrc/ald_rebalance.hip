@@ -101,7 +101,8 @@ __global__ __launch_bounds__(RB_ETHREADS) void k_rb_errors(RbArgs a)
             const int lead = __ffsll((unsigned long long)act) - 1;
             const int32_t xk = rdlane(x, lead);
             const bool mine = x == xk;
-            const int64_t sl = wave_sum64(mine ? dl : 0), sb = wave_sum64(mine ? db : 0);
+            // |dl| <= 2^24 and |db| <= 1 per lane: the wave's sums fit 32 bits
+            const int64_t sl = wave_sum32(mine ? (int32_t)dl : 0), sb = wave_sum32(mine ? (int32_t)db : 0);
             if (lane == lead) {
                 atomicAdd((unsigned long long*)&a.le[pr.wbase + xk], (unsigned long long)sl);
                 atomicAdd((unsigned long long*)&a.be[pr.wbase + xk], (unsigned long long)sb);
