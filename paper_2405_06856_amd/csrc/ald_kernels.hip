@@ -916,12 +916,28 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
             }
         }
     }
+    // the two smallest KV excesses feed only the diagnostics: each wave of
+    // the group merges its share of the worker blocks' two smallest keys (new
+    // first = smaller first; new second = min(larger first, smaller second))
+    uint64_t a1 = ~0ull, a2 = ~0ull;
+    if (act && st.out_diag) {
+        const ulonglong2* prow = st.part + sc.part_off + (qi - start);
+#pragma unroll 8
+        for (int b = slice; b < sc.nblk; b += G) {
+            const ulonglong2 p = prow[(int64_t)b * sc.pstride];
+            const uint64_t lo = p.x < a1 ? p.x : a1;
+            const uint64_t hi = p.x < a1 ? a1 : p.x;
+            const uint64_t s2 = p.y < a2 ? p.y : a2;
+            a1 = lo;
+            a2 = hi < s2 ? hi : s2;
+        }
+    }
     // merge the group's partial results into its first wave (lists by rank,
-    // counts summed)
+    // counts summed, excess keys as above)
     struct Part {
         uint64_t tkey[TOPK];
         int32_t tw[TOPK];
-        uint64_t ntkey;
+        uint64_t ntkey, a1, a2;
         int32_t ntw, nfeas, ncand, ntcnt, efeas, pad;
     };
     __shared__ Part parts[NWV][64];
@@ -936,6 +952,8 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
             pt.ncand = ncand;
             pt.ntcnt = ntcnt;
             pt.efeas = efeas ? 1 : 0;
+            pt.a1 = a1;
+            pt.a2 = a2;
         }
         __syncthreads();
         if (slice > 0) return;
@@ -950,25 +968,16 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
             ncand += pt.ncand;
             ntcnt += pt.ntcnt;
             efeas = efeas | (pt.efeas != 0);
+            const uint64_t lo = pt.a1 < a1 ? pt.a1 : a1;
+            const uint64_t hi = pt.a1 < a1 ? a1 : pt.a1;
+            const uint64_t s2 = pt.a2 < a2 ? pt.a2 : a2;
+            a1 = lo;
+            a2 = hi < s2 ? hi : s2;
         }
     }
     if (!live) return;
     int32_t ex1 = INT32_MAX, w1 = -1, ex2 = INT32_MAX, w2 = -1;
-    // the two smallest KV excesses feed only the diagnostics: merge the worker
-    // blocks' two smallest keys (new first = smaller first; new second =
-    // min(larger first, smaller second))
     if (act && st.out_diag) {
-        const ulonglong2* prow = st.part + sc.part_off + (qi - start);
-        uint64_t a1 = ~0ull, a2 = ~0ull;
-#pragma unroll 8
-        for (int b = 0; b < sc.nblk; ++b) {
-            const ulonglong2 p = prow[(int64_t)b * sc.pstride];
-            const uint64_t lo = p.x < a1 ? p.x : a1;
-            const uint64_t hi = p.x < a1 ? a1 : p.x;
-            const uint64_t s2 = p.y < a2 ? p.y : a2;
-            a1 = lo;
-            a2 = hi < s2 ? hi : s2;
-        }
         ex_unpack(a1, ex1, w1);
         ex_unpack(a2, ex2, w2);
     }
