@@ -51,10 +51,10 @@
  *     tables after it.  A call that does not fit returns ALD_ESPACE before
  *     doing any work, and ald_workspace_needed gives the size it needed.  The
  *     only memory the library allocates is one pinned host buffer per handle
- *     (64 bytes per scenario) into which the kernels copy their control blocks.
- *   - All work runs on the stream given to ald_create.  Every call below returns
- *     after that stream has finished the call's work, so errors are synchronous
- *     and outputs are ready on return.
+ *     (76 bytes per scenario) into which the kernels copy their control blocks.
+ *   - All work runs on the stream given to ald_create.  Every call below but
+ *     ald_place_stream_async returns after that stream has finished the call's
+ *     work, so errors are synchronous and outputs are ready on return.
  *   - Return value: ALD_OK (0) or a negative ALD_E* code; ald_last_error() gives
  *     a message.  On a validation error nothing is written to the outputs and
  *     the handle's worker state is unchanged.
@@ -82,6 +82,8 @@ extern "C" {
 #define ALD_ESTATE (-4)    /* call order: no workers loaded */
 #define ALD_EOVERFLOW (-5) /* a value would leave the exactly representable range */
 #define ALD_ESPACE (-6)    /* the attached workspace is too small for the call (see ald_workspace_needed) */
+#define ALD_EINCOMPLETE (-7) /* an asynchronous placement ran out of rounds (see ald_place_resume) */
+#define ALD_EBLOCKED (-8)  /* an asynchronous placement did not run: an earlier one is unfinished */
 
 typedef struct ald_handle* ald_handle_t;
 
@@ -195,6 +197,45 @@ int ald_load_workers_history(ald_handle_t handle, int32_t W, const ald_model_t* 
  * outside [1, 2^24]; ALD_ESLOTS when a worker runs out of request slots. */
 int ald_place_stream(ald_handle_t handle, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
                      int32_t heartbeat_every, int32_t* out_worker, ald_query_diag_t* out_diag);
+
+/* ald_place_stream (Algorithm 1 and the constraints of Sec. 4.2, placed in
+ * arrival order), stream-asynchronous: the call validates its arguments,
+ * enqueues its work on the handle's stream and returns without waiting, so a
+ * serving loop can keep placing batches back to back.  Outputs, and *status
+ * (a DEVICE int32), are valid once the stream has reached the call.
+ *
+ * How many tile rounds a call takes depends on the data (a tile is cut where
+ * its start-of-tile candidate lists cannot decide a query exactly), and a
+ * stream cannot branch on it, so the call enqueues the rounds it needs when no
+ * tile is cut plus spare_rounds (>= 0) more; rounds left over after the last
+ * query do nothing.  *status is then
+ *   ALD_OK           every query was decided (out_worker, out_diag complete);
+ *   ALD_EINCOMPLETE  tiles were cut more often than spare_rounds allowed: the
+ *                    queries before the stopping point are placed, the rest
+ *                    are not yet (their out_worker entries are unwritten);
+ *                    ald_place_resume finishes the call;
+ *   ALD_EBLOCKED     an earlier asynchronous call on this handle was
+ *                    unfinished or failed, so this call did nothing (issue it
+ *                    again after ald_place_resume: arrival order is kept);
+ *   ALD_EINVAL, ALD_ESLOTS, ALD_EOVERFLOW  as ald_place_stream returns them.
+ * Query arrays and outputs must stay valid until the stream has reached the
+ * call, or until ald_place_resume has returned if it stopped short.  Every
+ * other call on the handle that uses the loaded workers (ald_place_stream,
+ * ald_place_stream_hb, ald_place_grouped, ald_move_requests,
+ * ald_worker_summary, ald_set_workspace) first waits for the stream and
+ * returns ALD_EINCOMPLETE (changing nothing) while an asynchronous call is
+ * unfinished, or the error of one that failed.  ald_place_stats is not updated by asynchronous calls.  Returns
+ * ALD_EINVAL for a null status or spare_rounds outside [0, 2^20]. */
+int ald_place_stream_async(ald_handle_t handle, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
+                           int32_t heartbeat_every, int32_t spare_rounds, int32_t* out_worker,
+                           ald_query_diag_t* out_diag, int32_t* status);
+
+/* Wait for the handle's stream and finish the asynchronous placement call
+ * that stopped short (ALD_EINCOMPLETE), synchronously, with its own
+ * arguments; the calls issued after it (ALD_EBLOCKED) are dropped and must be
+ * issued again.  ALD_OK when nothing was unfinished; a device error of the
+ * asynchronous calls (ALD_ESLOTS, ...) is returned here as well. */
+int ald_place_resume(ald_handle_t handle);
 
 /* As ald_place_stream, with heartbeats driven by the caller's clock instead
  * of a period: hb_before[q] >= 0 (host array [Q]) decode iterations run

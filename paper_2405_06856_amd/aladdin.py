@@ -22,6 +22,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libaladdin.so")
 
 ALD_OK, ALD_EINVAL, ALD_EHIP, ALD_ESLOTS, ALD_ESTATE, ALD_EOVERFLOW, ALD_ESPACE = 0, -1, -2, -3, -4, -5, -6
+ALD_EINCOMPLETE, ALD_EBLOCKED = -7, -8
 
 KERNEL_KINDS = {"build": 0, "eval": 1, "select": 2, "commit": 3, "rebalance": 4}
 
@@ -51,7 +52,8 @@ assert DIAG_DTYPE.itemsize == 40
 
 SYMBOLS = ("ald_create", "ald_destroy", "ald_set_workspace", "ald_workspace_needed", "ald_workspace_size",
            "ald_sweep_workspace_size", "ald_set_tile", "ald_load_workers", "ald_load_workers_history",
-           "ald_place_stream", "ald_place_stream_hb", "ald_place_grouped", "ald_move_requests",
+           "ald_place_stream", "ald_place_stream_async", "ald_place_resume", "ald_place_stream_hb",
+           "ald_place_grouped", "ald_move_requests",
            "ald_sweep_scenarios", "ald_sweep_scenarios_hb", "ald_rebalance", "ald_rebalance_noalloc",
            "ald_worker_summary", "ald_set_profiling", "ald_kernel_time", "ald_place_stats", "ald_last_error",
            "ald_strerror")
@@ -74,6 +76,8 @@ def _load():
         "ald_load_workers": ([P, i32, ctypes.POINTER(Model), P, P, P, P, P, i32], ctypes.c_int),
         "ald_load_workers_history": ([P, i32, ctypes.POINTER(Model), P, P, P, P, P, P, i32], ctypes.c_int),
         "ald_place_stream": ([P, i32, P, P, i32, P, P], ctypes.c_int),
+        "ald_place_stream_async": ([P, i32, P, P, i32, i32, P, P, P], ctypes.c_int),
+        "ald_place_resume": ([P], ctypes.c_int),
         "ald_place_grouped": ([P, i32, P, i32, P, P, i32, P, P], ctypes.c_int),
         "ald_place_stream_hb": ([P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_move_requests": ([P, i32, P, P, P, P], ctypes.c_int),
@@ -177,6 +181,17 @@ def ald_load_workers_history(h, W: int, model: Model, kv_capacity, res_offsets, 
 def ald_place_stream(h, Q: int, q_l_in, q_l_pred, heartbeat_every: int, out_worker, out_diag=None) -> None:
     _check(h, _L.ald_place_stream(h, int(Q), _dptr(q_l_in), _dptr(q_l_pred), int(heartbeat_every),
                                   _dptr(out_worker), _dptr(out_diag)))
+
+
+def ald_place_stream_async(h, Q: int, q_l_in, q_l_pred, heartbeat_every: int, spare_rounds: int, out_worker,
+                           out_diag, status) -> None:
+    """status: device int32 [1], written when the stream reaches the call."""
+    _check(h, _L.ald_place_stream_async(h, int(Q), _dptr(q_l_in), _dptr(q_l_pred), int(heartbeat_every),
+                                        int(spare_rounds), _dptr(out_worker), _dptr(out_diag), _dptr(status)))
+
+
+def ald_place_resume(h) -> None:
+    _check(h, _L.ald_place_resume(h))
 
 
 def ald_place_stream_hb(h, Q: int, q_l_in, q_l_pred, hb_before, out_worker, out_diag=None) -> None:
@@ -393,6 +408,37 @@ class Evaluator:
                 raise ValueError("diag_out must be a uint8 tensor of at least Q * %d bytes" % DIAG_DTYPE.itemsize)
         self.call(ald_place_stream, Q, q_l_in, q_l_pred, heartbeat_every, out, d)
         return out, d
+
+    def place_async(self, q_l_in, q_l_pred, heartbeat_every=0, diag=True, out=None, diag_out=None, status=None,
+                    spare_rounds=0):
+        """As place_device, returning once the work is enqueued: (out, diag,
+        status), where status (int32 [1] on the device) reads ALD_OK once the
+        stream has placed every query, ALD_EINCOMPLETE if the rounds ran out
+        (resume() finishes the call) or ALD_EBLOCKED if an earlier call was
+        unfinished (issue it again after resume())."""
+        t = self.torch
+        Q = int(q_l_in.numel())
+        if out is None:
+            out = t.empty(max(Q, 1), dtype=t.int32, device=self.device)
+        elif out.dtype != t.int32 or out.numel() < Q:
+            raise ValueError("out must be an int32 tensor of at least Q elements")
+        d = None
+        if diag:
+            d = diag_out
+            if d is None:
+                d = t.empty(max(Q, 1) * DIAG_DTYPE.itemsize, dtype=t.uint8, device=self.device)
+            elif d.dtype != t.uint8 or d.numel() < Q * DIAG_DTYPE.itemsize:
+                raise ValueError("diag_out must be a uint8 tensor of at least Q * %d bytes" % DIAG_DTYPE.itemsize)
+        if status is None:
+            status = t.empty(1, dtype=t.int32, device=self.device)
+        elif status.dtype != t.int32 or status.numel() < 1:
+            raise ValueError("status must be an int32 tensor of at least one element")
+        self.call(ald_place_stream_async, Q, q_l_in, q_l_pred, heartbeat_every, spare_rounds, out, d, status)
+        return out, d, status
+
+    def resume(self) -> None:
+        """Finish an asynchronous placement that ran out of rounds (synchronously)."""
+        ald_place_resume(self.h)
 
     def place(self, q_l_in, q_l_pred, heartbeat_every=0, diag=True, hb_before=None) -> Placement:
         """hb_before: decode iterations before each query (instead of a period)."""

@@ -698,6 +698,7 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
     auto publish = [&]() {
         if (st.ctl_host != nullptr && part == 0 && lane == 0) st.ctl_host[s] = *cp;
     };
+    if (cp->call != st.call) return;  // another call's control block
     if (st.qbad != nullptr && *st.qbad) {  // an invalid query length: nothing is written
         if (part == 0 && lane == 0) cp->err = DEV_EINVAL;
         publish();

@@ -1,7 +1,7 @@
 // Host side of libaladdin: argument validation, the layout of the caller's
 // workspace, and the round loop that drives the tile pipeline (build -> eval ->
-// select -> commit) on the caller's HIP stream.  Every entry point returns
-// after its stream work is done.
+// select -> commit) on the caller's HIP stream.  Every entry point but
+// ald_place_stream_async returns after its stream work is done.
 //
 // Device memory: the library allocates none.  The caller attaches a workspace
 // (ald_set_workspace); the loaded workers' state occupies its start
@@ -57,6 +57,25 @@ struct Events {
     int kind;
 };
 
+// Where the stream of the loaded workers stands (what the next call starts from).
+struct Pos {
+    int32_t tau, hb_index, since_hb;
+    bool rebuild;
+    int64_t qcount;
+};
+
+// An asynchronous placement call, kept until the host has seen how it ended:
+// the arguments a resumption needs, and the stream position before the call
+// and after it (heartbeats fall at the same queries whatever tiles are cut,
+// so the position after a finished call is known when it is issued).
+struct AsyncCall {
+    int32_t call;
+    State st;         // its kernels' arguments (queries, outputs)
+    int32_t T, wave;  // its tile and evaluation grid target
+    bool moves;       // heartbeats move tau within the call
+    Pos before, after;
+};
+
 }  // namespace
 
 struct ald_handle {
@@ -80,6 +99,8 @@ struct ald_handle {
     bool dirty_pending = false;    // the last commit round left workers with stale summaries
     bool check_all = false;        // stale workers are not listed (after grouped placement): check every one
     int64_t qcount = 0;            // queries processed since the load (routes grouped placement)
+    int32_t call_seq = 0;          // placement calls issued (the id in their control blocks)
+    std::vector<AsyncCall> issued; // asynchronous calls whose end the host has not seen yet
     int64_t stats[4] = {0, 0, 0, 0};  // the last placement call: rounds, cuts, fallbacks, stale cuts
     Arena* grouped = nullptr;      // scenario view of the loaded workers for grouped placement
     // App. A's router: the group sizes it routes for and the queries each group
@@ -488,10 +509,9 @@ int64_t rounds_needed(const std::vector<Ctl>& c, const std::vector<const int32_t
 // `first_mode` (-1: skipped, nothing is stale); later rounds check every worker
 // when a heartbeat can have moved tau, else only the ones the previous commit
 // round listed.
-int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, std::vector<Ctl>& hc)
+// The pinned host mirror the commit kernel copies the control blocks into.
+int ensure_hctl(ald_handle* h, Arena* a)
 {
-    std::fill(h->stats, h->stats + 4, 0);
-    std::vector<Ctl> c0(hc);
     if (a->hctl_n < a->S) {
         if (a->hctl) HIPCHK(h, hipHostFree(a->hctl));
         a->hctl = nullptr;
@@ -500,18 +520,34 @@ int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, 
         a->hctl_n = a->S;
     }
     HIPCHK(h, hipHostGetDevicePointer((void**)&a->st.ctl_host, a->hctl, 0));
+    return ALD_OK;
+}
+
+// One round of the tile pipeline on every scenario of the arena.
+int launch_round(ald_handle* h, Arena* a, int mode)
+{
+    if (mode >= 0) LAUNCH(h, 0, launch_build(a->st, h->stream, mode));
+    LAUNCH(h, 1, launch_eval(a->st, a->eval_blocks, a->eval_mode, h->stream));
+    LAUNCH(h, 2, launch_select(a->st, a->sel_blocks, h->stream));
+    LAUNCH(h, 3, launch_commit(a->st, a->commit_blocks, a->use_d, h->stream));
+    return ALD_OK;
+}
+
+int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, std::vector<Ctl>& hc)
+{
+    std::fill(h->stats, h->stats + 4, 0);
+    std::vector<Ctl> c0(hc);
+    int rc = ensure_hctl(h, a);
+    if (rc != ALD_OK) return rc;
     bool first = true;
     for (;;) {
         int64_t need = rounds_needed(hc, a->hb_host);
         if (need < 0) return fail(h, ALD_EHIP, "internal error: a tile of no queries");
         if (need == 0) break;
         for (int64_t r = 0; r < need; ++r) {
-            const int mode = first ? first_mode : (build_every_round ? 0 : 1);
+            rc = launch_round(h, a, first ? first_mode : (build_every_round ? 0 : 1));
+            if (rc != ALD_OK) return rc;
             first = false;
-            if (mode >= 0) LAUNCH(h, 0, launch_build(a->st, h->stream, mode));
-            LAUNCH(h, 1, launch_eval(a->st, a->eval_blocks, a->eval_mode, h->stream));
-            LAUNCH(h, 2, launch_select(a->st, a->sel_blocks, h->stream));
-            LAUNCH(h, 3, launch_commit(a->st, a->commit_blocks, a->use_d, h->stream));
         }
         // every commit launch wrote its scenarios' control blocks to the pinned mirror
         HIPCHK(h, hipStreamSynchronize(h->stream));
@@ -529,6 +565,113 @@ int run_rounds(ald_handle* h, Arena* a, bool build_every_round, int first_mode, 
     return ALD_OK;
 }
 
+// The stream position after a call that starts from control block `c` and
+// finishes: tiles end at heartbeats whatever tiles are cut, so the position
+// follows from the tile sequence without cuts (as the commit kernel updates it).
+Pos project(Ctl c, const int32_t* hb, int64_t qcount)
+{
+    while (c.start < c.Q) {
+        const int32_t end = tile_end(c.start, c.Q, c.T, c.H, c.since_hb, c.hb_next);
+        const int32_t since = c.since_hb + (end - c.start);
+        c.rebuild = 0;
+        if (c.H > 0 && since >= c.H) {
+            c.tau += 1;
+            c.hb_index += 1;
+            c.since_hb = 0;
+            c.rebuild = 1;
+        } else if (hb && end == c.hb_next && end < c.Q) {
+            c.tau += hb[end];
+            c.hb_index += hb[end];
+            c.since_hb = 0;
+            c.rebuild = 1;
+            c.hb_next = next_hb(hb, end, c.Q);
+        } else {
+            c.since_hb = since;
+        }
+        c.start = end;
+    }
+    return Pos{c.tau, c.hb_index, c.since_hb, c.rebuild != 0, qcount + c.Q};
+}
+
+void set_pos(ald_handle* h, const Pos& p)
+{
+    h->tau = p.tau;
+    h->hb_index = p.hb_index;
+    h->since_hb = p.since_hb;
+    h->rebuild_pending = p.rebuild;
+    h->qcount = p.qcount;
+}
+
+bool same_pos(const Ctl& c, const Pos& p)
+{
+    return c.tau == p.tau && c.hb_index == p.hb_index && c.since_hb == p.since_hb && (c.rebuild != 0) == p.rebuild;
+}
+
+// Read how the asynchronous placement calls issued since the host last looked
+// have ended.  All finished: the position they projected is confirmed.  One
+// stopped short of its queries (every later one was blocked on the device and
+// did nothing): with `resume` its remaining rounds run now and the blocked
+// calls are forgotten (their callers issue them again), else ALD_EINCOMPLETE.
+// A device error is returned as the synchronous call would have returned it.
+int settle(ald_handle* h, bool resume)
+{
+    if (h->issued.empty()) return ALD_OK;
+    Arena* a = h->main;
+    Ctl c{};
+    HIPCHK(h, hipMemcpyAsync(&c, a->st.ctl, sizeof(Ctl), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    prof_collect(h);
+    size_t k = 0;
+    while (k < h->issued.size() && h->issued[k].call != c.call) ++k;
+    if (k == h->issued.size()) {
+        h->issued.clear();
+        return fail(h, ALD_EHIP, "internal error: the control block belongs to no issued call");
+    }
+    const AsyncCall x = h->issued[k];
+    const bool last = k + 1 == h->issued.size();
+    if (c.err) {
+        h->issued.clear();
+        set_pos(h, x.before);
+        return map_dev_error(h, c.err);
+    }
+    if (c.start < c.Q && !resume)
+        return fail(h, ALD_EINCOMPLETE, "an asynchronous placement stopped at query " + std::to_string(c.start) +
+                                            " of " + std::to_string(c.Q) + ": ald_place_resume finishes it");
+    h->issued.clear();
+    if (c.start < c.Q) {
+        // lay the tile scratch out for the call again (a blocked call may have
+        // changed it), then run its remaining rounds with its own arguments
+        a->hscen[0].hb = nullptr;
+        size_t sb = 0;
+        int rc = layout_scratch(h, a, x.T, x.wave, h->ws + h->state_bytes, &sb);
+        if (rc != ALD_OK) return rc;
+        a->st.q_lin = x.st.q_lin;
+        a->st.q_lpred = x.st.q_lpred;
+        a->st.out_worker = x.st.out_worker;
+        a->st.out_diag = x.st.out_diag;
+        a->st.call = x.call;
+        std::vector<Ctl> hc(1, c);
+        rc = run_rounds(h, a, x.moves, x.moves ? 0 : 1, hc);
+        if (rc != ALD_OK) {
+            set_pos(h, x.before);
+            return rc;
+        }
+        c = hc[0];
+    } else if (!last) {
+        set_pos(h, x.before);
+        return fail(h, ALD_EHIP, "internal error: a call after a finished one did not start");
+    }
+    if (c.start < c.Q || !same_pos(c, x.after)) {
+        set_pos(h, x.before);
+        return fail(h, ALD_EHIP, "internal error: the stream position differs from the one projected");
+    }
+    set_pos(h, x.after);
+    h->round = c.round;
+    h->dirty_pending = c.ndirty > 0;
+    h->check_all = false;
+    return ALD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -542,6 +685,9 @@ const char* ald_strerror(int code)
     case ALD_ESLOTS: return "worker request slots exhausted";
     case ALD_ESTATE: return "no workers loaded";
     case ALD_EOVERFLOW: return "value outside the exactly representable range";
+    case ALD_ESPACE: return "workspace too small";
+    case ALD_EINCOMPLETE: return "asynchronous placement unfinished";
+    case ALD_EBLOCKED: return "asynchronous placement blocked by an unfinished one";
     default: return "unknown error";
     }
 }
@@ -581,6 +727,9 @@ int ald_set_workspace(ald_handle_t h, void* workspace, size_t bytes)
     if (!h) return ALD_EINVAL;
     HIPCHK(h, hipSetDevice(h->device));
     if (bytes > 0 && !workspace) return fail(h, ALD_EINVAL, "null workspace");
+    if (h->main) {
+        if (int rc0 = settle(h, false)) return rc0;
+    }
     if (((uintptr_t)workspace & 255) != 0) return fail(h, ALD_EINVAL, "the workspace must be 256-byte aligned");
     char* ws = bytes > 0 ? (char*)workspace : nullptr;
     if (h->main) {
@@ -660,6 +809,11 @@ int ald_place_stats(ald_handle_t h, int64_t* out)
 int ald_kernel_time(ald_handle_t h, int32_t kind, double* total_ms, int64_t* launches)
 {
     if (!h || kind < 0 || kind > 4) return ALD_EINVAL;
+    if (!h->pending.empty()) {  // launches of asynchronous calls
+        HIPCHK(h, hipSetDevice(h->device));
+        HIPCHK(h, hipStreamSynchronize(h->stream));
+        prof_collect(h);
+    }
     if (total_ms) *total_ms = h->tot_ms[kind];
     if (launches) *launches = h->launches[kind];
     return ALD_OK;
@@ -714,7 +868,9 @@ int load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const int6
     if (rc == ALD_OK) rc = layout_scratch(h, a, 256, 4096, nullptr, &lb);
     if (rc != ALD_OK) { delete a; return rc; }
     if (sb + 256 + lb > h->ws_bytes) { delete a; return need_space(h, sb + 256 + lb); }
-    // from here the previous workers are gone
+    // from here the previous workers are gone (with any asynchronous call on them)
+    prof_collect(h);
+    h->issued.clear();
     delete h->grouped;
     h->grouped = nullptr;
     delete h->main;
@@ -791,17 +947,26 @@ struct HbScope {
 };
 
 // One stream call: heartbeats every H processed queries, or hb_before[q]
-// (host array) decode iterations before query q.
+// (host array) decode iterations before query q.  With `status` (a device
+// word) the call is asynchronous: it enqueues the rounds the call needs if no
+// tile is cut, plus `spare` more, and the status kernel writes its outcome.
 int place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred, int32_t heartbeat_every,
-                 const int32_t* hb_before, int32_t* out_worker, ald_query_diag_t* out_diag)
+                 const int32_t* hb_before, int32_t* out_worker, ald_query_diag_t* out_diag,
+                 int32_t* status = nullptr, int32_t spare = 0)
 {
     if (!h) return ALD_EINVAL;
     HIPCHK(h, hipSetDevice(h->device));
     if (!h->main) return fail(h, ALD_ESTATE, "ald_load_workers has not been called");
     if (Q < 0 || heartbeat_every < 0) return fail(h, ALD_EINVAL, "Q and heartbeat_every must be >= 0");
-    if (Q == 0) return ALD_OK;
+    const bool async = status != nullptr;
+    if (async && (spare < 0 || spare > (1 << 20))) return fail(h, ALD_EINVAL, "spare_rounds must lie in [0, 2^20]");
+    int rc = async ? ALD_OK : settle(h, false);
+    if (rc != ALD_OK) return rc;
+    if (Q == 0) {
+        if (async) HIPCHK(h, launch_status(nullptr, 0, status, h->stream));
+        return ALD_OK;
+    }
     if (!q_l_in || !q_l_pred || !out_worker) return fail(h, ALD_EINVAL, "null argument");
-    int rc = ALD_OK;
     const int32_t H = heartbeat_every;
     int32_t tau = h->tau, hb = h->hb_index, since = h->since_hb;
     bool rebuild = h->rebuild_pending;
@@ -868,18 +1033,47 @@ int place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t
     c.first_rej = INT32_MAX;
     c.round = h->round;
     c.hb_next = hb_before ? next_hb(hb_before, 0, Q) : 0;
+    h->call_seq = h->call_seq == INT32_MAX ? 1 : h->call_seq + 1;
+    c.call = h->call_seq;
+    // an asynchronous call after another one starts only if that one finished
+    const int32_t gate = (async && !h->issued.empty()) ? h->issued.back().call : -1;
     TileInfo ti{};
     ti.first_pc[0] = ti.first_pc[1] = INT32_MAX;
-    HIPCHK(h, launch_begin(c, ti, a->st.ctl, a->st.tinfo, a->st.qbad, h->stream));
+    HIPCHK(h, launch_begin(c, ti, a->st.ctl, a->st.tinfo, a->st.qbad, gate, h->stream));
     a->st.q_lin = q_l_in;
     a->st.q_lpred = q_l_pred;
     a->st.out_worker = out_worker;
     a->st.out_diag = (Diag*)out_diag;
+    a->st.call = c.call;
     std::vector<Ctl> hc(1, c);
     // first build: every worker after a heartbeat, the last commit round's
-    // workers if it changed any, else nothing
+    // workers if it changed any (unknown after an asynchronous call), else nothing
     const bool moves = H > 0 || hb_before != nullptr;  // heartbeats can move tau within the call
-    const int first_mode = (rebuild || moves || h->check_all) ? 0 : (h->dirty_pending ? 1 : -1);
+    const bool dirty = h->dirty_pending || !h->issued.empty();
+    const int first_mode = (rebuild || moves || h->check_all) ? 0 : (dirty ? 1 : -1);
+    if (async) {
+        rc = ensure_hctl(h, a);
+        if (rc != ALD_OK) return rc;
+        const int64_t need = rounds_needed(hc, a->hb_host);
+        if (need < 1) return fail(h, ALD_EHIP, "internal error: a tile of no queries");
+        for (int64_t r = 0; r < need + spare; ++r) {
+            rc = launch_round(h, a, r == 0 ? first_mode : (moves ? 0 : 1));
+            if (rc != ALD_OK) return rc;
+        }
+        HIPCHK(h, launch_status(a->st.ctl, c.call, status, h->stream));
+        AsyncCall x;
+        x.call = c.call;
+        x.st = a->st;
+        x.T = T;
+        x.wave = wave;
+        x.moves = moves;
+        x.before = Pos{h->tau, h->hb_index, h->since_hb, h->rebuild_pending, h->qcount};
+        x.after = project(c, nullptr, h->qcount);
+        h->issued.push_back(x);
+        set_pos(h, x.after);
+        h->check_all = false;
+        return ALD_OK;
+    }
     rc = run_rounds(h, a, moves, first_mode, hc);
     if (rc != ALD_OK) return rc;
     c = hc[0];
@@ -904,12 +1098,30 @@ int ald_place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int
     return place_stream(h, Q, q_l_in, q_l_pred, heartbeat_every, nullptr, out_worker, out_diag);
 }
 
+int ald_place_stream_async(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred,
+                           int32_t heartbeat_every, int32_t spare_rounds, int32_t* out_worker,
+                           ald_query_diag_t* out_diag, int32_t* status)
+{
+    if (h && !status) return fail(h, ALD_EINVAL, "null status");
+    return place_stream(h, Q, q_l_in, q_l_pred, heartbeat_every, nullptr, out_worker, out_diag, status,
+                        spare_rounds);
+}
+
+int ald_place_resume(ald_handle_t h)
+{
+    if (!h) return ALD_EINVAL;
+    HIPCHK(h, hipSetDevice(h->device));
+    if (!h->main) return fail(h, ALD_ESTATE, "ald_load_workers has not been called");
+    return settle(h, true);
+}
+
 int ald_move_requests(ald_handle_t h, int32_t K, const int32_t* l_in, const int32_t* l_pred, const int32_t* from,
                       const int32_t* to)
 {
     if (!h) return ALD_EINVAL;
     HIPCHK(h, hipSetDevice(h->device));
     if (!h->main) return fail(h, ALD_ESTATE, "ald_load_workers has not been called");
+    if (int rc0 = settle(h, false)) return rc0;
     if (K < 0) return fail(h, ALD_EINVAL, "K must be >= 0");
     if (K == 0) return ALD_OK;
     if (!l_in || !l_pred || !from || !to) return fail(h, ALD_EINVAL, "null argument");
@@ -1056,6 +1268,7 @@ int grouped_view(ald_handle* h, int32_t G, const int32_t* sizes, char* base, siz
     a.eval_mode = m->eval_mode;
     a.use_d = m->use_d;
     a.st = m->st;  // worker and slot arrays
+    a.st.call = 0;  // as in its own control blocks
     Carver c{nullptr};
     Ctl* ctl = nullptr;
     TileInfo* ti = nullptr;
@@ -1096,6 +1309,7 @@ int ald_place_grouped(ald_handle_t h, int32_t G, const int32_t* group_workers, i
     if (!h) return ALD_EINVAL;
     HIPCHK(h, hipSetDevice(h->device));
     if (!h->main) return fail(h, ALD_ESTATE, "ald_load_workers has not been called");
+    if (int rc0 = settle(h, false)) return rc0;
     if (G < 1 || !group_workers) return fail(h, ALD_EINVAL, "G must be >= 1 with a size per group");
     int64_t wsum = 0;
     for (int32_t g = 0; g < G; ++g) {
@@ -1576,6 +1790,7 @@ int ald_worker_summary(ald_handle_t h, int32_t* B, int64_t* sum_c, int64_t* sum_
     if (!h) return ALD_EINVAL;
     HIPCHK(h, hipSetDevice(h->device));
     if (!h->main) return fail(h, ALD_ESTATE, "ald_load_workers has not been called");
+    if (int rc0 = settle(h, false)) return rc0;
     if (!B || !sum_c || !sum_r || !peak) return fail(h, ALD_EINVAL, "null argument");
     // bring every worker's summaries to the current decode iteration first
     HIPCHK(h, launch_build(h->main->st, h->stream, 2));

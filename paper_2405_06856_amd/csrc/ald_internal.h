@@ -117,6 +117,8 @@ struct Ctl {
                         // precede, Q if none; 0 otherwise
     int32_t fallbacks;  // decisions that scanned the untouched workers' bit words (statistics)
     int32_t stale_cuts; // tiles cut on the stale-scan budget (statistics)
+    int32_t call;       // the placement call the block belongs to (State::call); kernels
+                        // launched for another call leave it alone
 };
 
 // Tile description published by the selection kernel for the commit kernel.
@@ -218,6 +220,7 @@ struct State {
     int32_t* dcount;   // [S]
     int32_t S;
     int32_t NW;
+    int32_t call;      // this launch's placement call: control blocks of another call are not touched
     // tile scratch
     uint64_t* bits_feas;
     uint64_t* bits_nt;
@@ -261,8 +264,11 @@ hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream);
 hipError_t launch_commit(const State& st, int32_t blocks, bool use_d, hipStream_t stream);
 hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q, Ctl* ctl, int32_t S,
                               hipStream_t stream);
-hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* tinfo, int32_t* qbad,
+// gate: -1, or the asynchronous call that must have finished for this one to start
+hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* tinfo, int32_t* qbad, int32_t gate,
                         hipStream_t stream);
+// status = the outcome of asynchronous call `call` (ctl null: ALD_OK)
+hipError_t launch_status(const Ctl* ctl, int32_t call, int32_t* status, hipStream_t stream);
 hipError_t launch_summary(const State& st, int32_t W, int32_t* B, int64_t* sc, int64_t* sr, int64_t* peak,
                           hipStream_t stream);
 // rejected / first rejected query per scenario, and (min_gpus non-null) the

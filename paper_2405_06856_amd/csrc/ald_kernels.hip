@@ -14,6 +14,7 @@
 //             extra blocks finalize the rejected prefix in parallel
 //             (ald_commit.h; launched from ald_commit.hip and ald_commit_d.hip).
 #include "ald_device.h"
+#include "../../include/aladdin.h"
 
 #include <type_traits>
 
@@ -368,6 +369,7 @@ __global__ __launch_bounds__(BUILD_THREADS) void k_ingest(State st, const int64_
 __device__ __forceinline__ void build_one(const State& st, int mode, int gw, int s)
 {
     const Ctl* c = st.ctl + s;
+    if (mode != 2 && c->call != st.call) return;  // another call's control block
     if (mode == 0) {
         if (c->err || c->start >= c->Q) return;
         if (st.built[gw]) {
@@ -689,7 +691,8 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
     const Scen sc = st.scen[s];
     const Ctl* cp = st.ctl + s;
     const int32_t start = cp->start, Q = cp->Q;
-    if (st.qbad != nullptr && start == 0) {
+    const bool mine = cp->call == st.call;
+    if (st.qbad != nullptr && start == 0 && mine) {
         // first round of a one-scenario call: check every query length of the
         // call before the first commit can run (grid-stride over all queries)
         bool bad = false;
@@ -699,7 +702,7 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
         }
         if (ballot(bad) != 0 && lane_id() == 0) atomicOr(st.qbad, 1);
     }
-    if (cp->err || start >= Q) return;
+    if (cp->err || start >= Q || !mine) return;
     const int32_t end = tile_end(start, Q, cp->T, cp->H, cp->since_hb, cp->hb_next);
     const int local = blockIdx.x - sc.eval_blk0;
     const int wb = local % sc.nblk;
@@ -825,6 +828,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     Ctl* cp = st.ctl + s;
     const int32_t start = cp->start, Q = cp->Q;
     const int local = blockIdx.x - sc.sel_blk0;
+    if (cp->call != st.call) return;  // another call's control block (its tile record too)
     const bool done = cp->err || start >= Q;
     const int32_t end = done ? start : tile_end(start, Q, cp->T, cp->H, cp->since_hb, cp->hb_next);
     const int parity = cp->round & 1;
@@ -1035,12 +1039,36 @@ __global__ __launch_bounds__(256) void k_query_stats(const int32_t* lin, const i
 
 // Start of an ald_place_stream call (one scenario): the control block, the
 // tile record and a cleared query-error word (the first round's pair
-// evaluation checks the query lengths).
-__global__ void k_begin(Ctl c, TileInfo ti, Ctl* ctl, TileInfo* tinfo, int32_t* qbad)
+// evaluation checks the query lengths).  With gate >= 0 the call follows
+// asynchronous call `gate` and starts only if that call finished without an
+// error; otherwise the control block stays that call's, and every kernel of
+// this call finds it foreign and does nothing.
+__global__ void k_begin(Ctl c, TileInfo ti, Ctl* ctl, TileInfo* tinfo, int32_t* qbad, int32_t gate)
 {
+    if (gate >= 0) {
+        const Ctl o = *ctl;
+        if (o.call != gate || o.err || o.start < o.Q) return;
+    }
     *ctl = c;
     *tinfo = ti;
     *qbad = 0;
+}
+
+// Outcome of asynchronous call `call` (ctl null: a call with no queries),
+// as the ALD_* code the synchronous call would have returned.
+__global__ void k_status(const Ctl* ctl, int32_t call, int32_t* status)
+{
+    int32_t r = ALD_OK;
+    if (ctl != nullptr) {
+        const Ctl c = *ctl;
+        if (c.call != call) r = ALD_EBLOCKED;
+        else if (c.err == DEV_ESLOTS) r = ALD_ESLOTS;
+        else if (c.err == DEV_EOVERFLOW) r = ALD_EOVERFLOW;
+        else if (c.err == DEV_EINVAL) r = ALD_EINVAL;
+        else if (c.err != 0) r = ALD_EHIP;
+        else if (c.start < c.Q) r = ALD_EINCOMPLETE;
+    }
+    *status = r;
 }
 
 __global__ void k_summary(State st, int32_t W, int32_t* B, int64_t* sc, int64_t* sr, int64_t* peak)
@@ -1142,10 +1170,16 @@ hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t 
     return hipGetLastError();
 }
 
-hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* tinfo, int32_t* qbad,
+hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* tinfo, int32_t* qbad, int32_t gate,
                         hipStream_t stream)
 {
-    hipLaunchKernelGGL(k_begin, dim3(1), dim3(1), 0, stream, c, ti, ctl, tinfo, qbad);
+    hipLaunchKernelGGL(k_begin, dim3(1), dim3(1), 0, stream, c, ti, ctl, tinfo, qbad, gate);
+    return hipGetLastError();
+}
+
+hipError_t launch_status(const Ctl* ctl, int32_t call, int32_t* status, hipStream_t stream)
+{
+    hipLaunchKernelGGL(k_status, dim3(1), dim3(1), 0, stream, ctl, call, status);
     return hipGetLastError();
 }
 

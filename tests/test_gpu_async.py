@@ -1,0 +1,207 @@
+"""Stream-asynchronous placement (needs an MI355X).
+
+ald_place_stream_async enqueues the tile rounds a call needs when no tile is
+cut (plus spare rounds) and returns; a status word on the device tells how the
+call ended.  A chain of such calls must place exactly what the oracle's one
+arrival-order pass places (Algorithm 1, Sec. 4.2), also when rounds run out
+(the call stops short, later calls are blocked, ald_place_resume finishes it
+and the blocked calls are issued again), when heartbeats fall inside and
+between calls, and when synchronous calls are mixed in."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from oracle import ref
+from paper_2405_06856_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+INT_FIELDS = ("n_feasible", "near_tie", "kv_peak_chosen", "kv_excess_min")
+SENTINEL = 12345
+
+
+@pytest.fixture(scope="module")
+def aladdin():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2405_06856_amd import aladdin as mod
+    return mod
+
+
+def trace(W, R, Q, cap, seed):
+    return wl.make_trace("async", seed, W=W, R=R, Q=Q, kv_capacity=cap, model=wl.BASE_MODEL,
+                         in_dist=wl.SHORT_IN, out_dist=wl.SHORT_OUT, rate=200.0)
+
+
+def chunks(Q, n):
+    edges = np.linspace(0, Q, n + 1).astype(int)
+    return [(int(a), int(b)) for a, b in zip(edges[:-1], edges[1:])]
+
+
+def run_async_chain(aladdin, ev, t, H, parts, spare, diag=True):
+    """Issue every part asynchronously; on a short call resume it and issue the
+    blocked parts again.  Returns the concatenated placement and diagnostics,
+    and how many calls stopped short."""
+    import torch
+    dev = ev.device
+    ql = torch.as_tensor(t.q_l_in, dtype=torch.int32, device=dev)
+    qp = torch.as_tensor(t.q_l_pred, dtype=torch.int32, device=dev)
+    Q = int(ql.numel())
+    out = torch.full((Q,), -7, dtype=torch.int32, device=dev)
+    dg = torch.zeros(Q * aladdin.DIAG_DTYPE.itemsize, dtype=torch.uint8, device=dev) if diag else None
+    status = torch.full((len(parts),), SENTINEL, dtype=torch.int32, device=dev)
+    short = 0
+    todo = list(range(len(parts)))
+    while todo:
+        for k in todo:
+            a, b = parts[k]
+            ev.place_async(ql[a:b], qp[a:b], heartbeat_every=H, diag=diag, out=out[a:b],
+                           diag_out=None if dg is None else dg[a * 40:b * 40], status=status[k:k + 1],
+                           spare_rounds=spare)
+        torch.cuda.synchronize()
+        st = status.cpu().numpy()
+        codes = st[todo]
+        assert SENTINEL not in codes, codes
+        bad = [i for i, c in enumerate(codes) if c != aladdin.ALD_OK]
+        if not bad:
+            break
+        first = bad[0]
+        # the first call that did not finish stopped short; every later one was blocked
+        assert codes[first] == aladdin.ALD_EINCOMPLETE, codes
+        assert all(c == aladdin.ALD_EBLOCKED for c in codes[first + 1:]), codes
+        short += 1
+        ev.resume()
+        todo = todo[first + 1:]
+        status[todo] = SENTINEL
+    torch.cuda.synchronize()
+    got_w = out.cpu().numpy()
+    got_d = None if dg is None else dg.cpu().numpy().view(aladdin.DIAG_DTYPE)
+    return got_w, got_d, short
+
+
+def compare(got_w, got_d, summ, want, H, Q):
+    assert np.array_equal(got_w, want.worker), np.flatnonzero(got_w != want.worker)[:10]
+    if got_d is not None:
+        for f in INT_FIELDS:
+            assert np.array_equal(got_d[f].astype(np.int64), getattr(want, f).astype(np.int64)), f
+        for f in ("ttft_chosen", "tdec_chosen"):
+            assert np.allclose(got_d[f], getattr(want, f), rtol=1e-9, atol=0.0), f
+    if H == 0 or Q % H:
+        for f in ("B", "sum_c", "sum_r", "peak"):
+            assert np.array_equal(summ[f].astype(np.int64), getattr(want, f)), f
+
+
+CASES = [
+    # W, residents per worker, Q, KV capacity, heartbeat period, parts, spare rounds
+    (12, 5, 3000, 30000, 0, 6, 0),
+    (12, 5, 3000, 30000, 50, 7, 0),
+    (40, 3, 4000, 8000, 0, 5, 2),
+    (64, 1, 4096, 8000, 100, 9, 0),
+    (64, 1, 4096, 8000, 37, 4, 64),
+]
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_async_chain_matches_oracle(aladdin, case):
+    W, R, Q, cap, H, n, spare = CASES[case]
+    print("async chain case", case, "W", W, "R", R, "Q", Q, "cap", cap, "H", H, "parts", n, "spare", spare,
+          flush=True)
+    t = trace(W, R, Q, cap, 9100 + case)
+    want = ref.place_trace(t, heartbeat_every=H)
+    ev = aladdin.Evaluator(0, tile=4096)
+    ev.load_trace(t)
+    got_w, got_d, short = run_async_chain(aladdin, ev, t, H, chunks(Q, n), spare)
+    summ = ev.summary()
+    ev.close()
+    print("calls that stopped short", short, flush=True)
+    if case == 0:
+        assert short > 0  # long tiles on a filling cluster: the resumption path was taken
+    compare(got_w, got_d, summ, want, H, Q)
+
+
+def test_async_without_cuts_needs_no_resume(aladdin):
+    # a full cluster (capacity 1 token): every query is rejected, no worker
+    # changes, so no tile is cut and the rounds enqueued are exactly enough,
+    # heartbeats inside and between calls included
+    t = trace(64, 2, 3000, 1, 9200)
+    want = ref.place_trace(t, heartbeat_every=25)
+    assert (want.worker < 0).all()
+    ev = aladdin.Evaluator(0, tile=4096)
+    ev.load_trace(t)
+    got_w, got_d, short = run_async_chain(aladdin, ev, t, 25, chunks(3000, 8), 0)
+    summ = ev.summary()
+    ev.close()
+    assert short == 0
+    compare(got_w, got_d, summ, want, 25, 3000)
+
+
+def test_sync_calls_after_async_ones(aladdin):
+    import torch
+    t = trace(12, 0, 3000, 8000, 9300)
+    H = 0
+    want = ref.place_trace(t, heartbeat_every=H)
+    ev = aladdin.Evaluator(0, tile=4096)
+    ev.load_trace(t)
+    dev = ev.device
+    ql = torch.as_tensor(t.q_l_in, dtype=torch.int32, device=dev)
+    qp = torch.as_tensor(t.q_l_pred, dtype=torch.int32, device=dev)
+    out = torch.full((3000,), -7, dtype=torch.int32, device=dev)
+    dg = torch.zeros(3000 * 40, dtype=torch.uint8, device=dev)
+    s = torch.full((2,), SENTINEL, dtype=torch.int32, device=dev)
+    ev.place_async(ql[:1000], qp[:1000], H, True, out[:1000], dg[:40000], s[0:1], spare_rounds=0)
+    ev.place_async(ql[1000:1500], qp[1000:1500], H, True, out[1000:1500], dg[40000:60000], s[1:2], spare_rounds=0)
+    torch.cuda.synchronize()
+    codes = s.cpu().numpy()
+    assert codes[0] == aladdin.ALD_EINCOMPLETE and codes[1] == aladdin.ALD_EBLOCKED, codes
+    # a synchronous call refuses to run over an unfinished asynchronous one and changes nothing
+    with pytest.raises(aladdin.AladdinError) as e:
+        ev.place_device(ql[1000:1500], qp[1000:1500], H, True, out[1000:1500], dg[40000:60000])
+    assert e.value.code == aladdin.ALD_EINCOMPLETE
+    ev.resume()
+    ev.resume()  # nothing left: a no-op
+    ev.place_device(ql[1000:2200], qp[1000:2200], H, True, out[1000:2200], dg[40000:88000])
+    s[0] = SENTINEL
+    ev.place_async(ql[2200:], qp[2200:], H, True, out[2200:], dg[88000:], s[0:1], spare_rounds=4096)
+    torch.cuda.synchronize()
+    assert int(s[0].item()) == aladdin.ALD_OK
+    summ = ev.summary()
+    ev.close()
+    compare(out.cpu().numpy(), dg.cpu().numpy().view(aladdin.DIAG_DTYPE), summ, want, H, 3000)
+
+
+def test_async_errors_and_empty_calls(aladdin):
+    import torch
+    t = trace(12, 5, 600, 30000, 9400)
+    ev = aladdin.Evaluator(0, tile=4096)
+    ev.load_trace(t)
+    dev = ev.device
+    before = ev.summary()
+    s = torch.full((3,), SENTINEL, dtype=torch.int32, device=dev)
+    empty = torch.empty(0, dtype=torch.int32, device=dev)
+    ev.place_async(empty, empty, 0, False, status=s[0:1])
+    bad = torch.as_tensor(t.q_l_in, dtype=torch.int32, device=dev).clone()
+    bad[17] = 0  # a length outside [1, 2^24]
+    qp = torch.as_tensor(t.q_l_pred, dtype=torch.int32, device=dev)
+    out = torch.full((600,), -7, dtype=torch.int32, device=dev)
+    ev.place_async(bad, qp, 0, True, out=out, status=s[1:2])
+    ev.place_async(qp, qp, 0, True, status=s[2:3])
+    torch.cuda.synchronize()
+    codes = s.cpu().numpy()
+    assert codes[0] == aladdin.ALD_OK and codes[1] == aladdin.ALD_EINVAL and codes[2] == aladdin.ALD_EBLOCKED, codes
+    assert (out.cpu().numpy() == -7).all()  # nothing written
+    # the failed call's error is reported once, then the handle works from where it stood
+    with pytest.raises(aladdin.AladdinError) as e:
+        ev.resume()
+    assert e.value.code == aladdin.ALD_EINVAL
+    after = ev.summary()
+    for f in before:
+        assert np.array_equal(before[f], after[f]), f
+    with pytest.raises(aladdin.AladdinError) as e:
+        ev.place_async(qp, qp, 0, True, status=s[0:1], spare_rounds=-1)
+    assert e.value.code == aladdin.ALD_EINVAL
+    got = ev.place(t.q_l_in, t.q_l_pred, heartbeat_every=0, diag=False)
+    ev.close()
+    want = ref.place_trace(t, heartbeat_every=0)
+    assert np.array_equal(got.worker, want.worker)
