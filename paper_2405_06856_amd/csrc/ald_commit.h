@@ -696,9 +696,14 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
     const int lane = threadIdx.x;
     // the control block as the host will read it (after the stream synchronises)
     auto publish = [&]() {
-        if (st.ctl_host != nullptr && part == 0 && lane == 0) st.ctl_host[s] = *cp;
+        if (part != 0 || lane != 0) return;
+        if (st.ctl_host != nullptr) st.ctl_host[s] = *cp;
+        if (st.status != nullptr) *st.status = ctl_status(*cp);
     };
-    if (cp->call != st.call) return;  // another call's control block
+    if (cp->call != st.call) {  // another call's control block: this call was blocked
+        if (st.status != nullptr && part == 0 && lane == 0) *st.status = ALD_EBLOCKED;
+        return;
+    }
     if (st.qbad != nullptr && *st.qbad) {  // an invalid query length: nothing is written
         if (part == 0 && lane == 0) cp->err = DEV_EINVAL;
         publish();

@@ -963,7 +963,7 @@ int place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t
     int rc = async ? ALD_OK : settle(h, false);
     if (rc != ALD_OK) return rc;
     if (Q == 0) {
-        if (async) HIPCHK(h, launch_status(nullptr, 0, status, h->stream));
+        if (async) HIPCHK(h, launch_status_ok(status, h->stream));
         return ALD_OK;
     }
     if (!q_l_in || !q_l_pred || !out_worker) return fail(h, ALD_EINVAL, "null argument");
@@ -1056,11 +1056,13 @@ int place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t
         if (rc != ALD_OK) return rc;
         const int64_t need = rounds_needed(hc, a->hb_host);
         if (need < 1) return fail(h, ALD_EHIP, "internal error: a tile of no queries");
+        // the last round's commit kernel writes the call's outcome
         for (int64_t r = 0; r < need + spare; ++r) {
+            a->st.status = r + 1 == need + spare ? status : nullptr;
             rc = launch_round(h, a, r == 0 ? first_mode : (moves ? 0 : 1));
+            a->st.status = nullptr;
             if (rc != ALD_OK) return rc;
         }
-        HIPCHK(h, launch_status(a->st.ctl, c.call, status, h->stream));
         AsyncCall x;
         x.call = c.call;
         x.st = a->st;

@@ -29,6 +29,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/aladdin.h"
+
 namespace ald {
 
 constexpr int TOPK = 4;            // feasible candidates kept per query
@@ -120,6 +122,17 @@ struct Ctl {
     int32_t call;       // the placement call the block belongs to (State::call); kernels
                         // launched for another call leave it alone
 };
+
+// The outcome of a one-scenario placement call as the ALD_* code its
+// synchronous form returns (control block `c`, after the call's rounds).
+__host__ __device__ inline int32_t ctl_status(const Ctl& c)
+{
+    if (c.err == DEV_ESLOTS) return ALD_ESLOTS;
+    if (c.err == DEV_EOVERFLOW) return ALD_EOVERFLOW;
+    if (c.err == DEV_EINVAL) return ALD_EINVAL;
+    if (c.err != 0) return ALD_EHIP;
+    return c.start < c.Q ? ALD_EINCOMPLETE : ALD_OK;
+}
 
 // Tile description published by the selection kernel for the commit kernel.
 struct TileInfo {
@@ -221,6 +234,8 @@ struct State {
     int32_t S;
     int32_t NW;
     int32_t call;      // this launch's placement call: control blocks of another call are not touched
+    int32_t* status;   // the last round of an asynchronous call: where the commit kernel writes
+                       // the call's outcome (one scenario; null otherwise)
     // tile scratch
     uint64_t* bits_feas;
     uint64_t* bits_nt;
@@ -267,8 +282,8 @@ hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t 
 // gate: -1, or the asynchronous call that must have finished for this one to start
 hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* tinfo, int32_t* qbad, int32_t gate,
                         hipStream_t stream);
-// status = the outcome of asynchronous call `call` (ctl null: ALD_OK)
-hipError_t launch_status(const Ctl* ctl, int32_t call, int32_t* status, hipStream_t stream);
+// status = ALD_OK (an asynchronous call with no queries)
+hipError_t launch_status_ok(int32_t* status, hipStream_t stream);
 hipError_t launch_summary(const State& st, int32_t W, int32_t* B, int64_t* sc, int64_t* sr, int64_t* peak,
                           hipStream_t stream);
 // rejected / first rejected query per scenario, and (min_gpus non-null) the

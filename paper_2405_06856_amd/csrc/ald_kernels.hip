@@ -14,7 +14,6 @@
 //             extra blocks finalize the rejected prefix in parallel
 //             (ald_commit.h; launched from ald_commit.hip and ald_commit_d.hip).
 #include "ald_device.h"
-#include "../../include/aladdin.h"
 
 #include <type_traits>
 
@@ -1054,22 +1053,8 @@ __global__ void k_begin(Ctl c, TileInfo ti, Ctl* ctl, TileInfo* tinfo, int32_t* 
     *qbad = 0;
 }
 
-// Outcome of asynchronous call `call` (ctl null: a call with no queries),
-// as the ALD_* code the synchronous call would have returned.
-__global__ void k_status(const Ctl* ctl, int32_t call, int32_t* status)
-{
-    int32_t r = ALD_OK;
-    if (ctl != nullptr) {
-        const Ctl c = *ctl;
-        if (c.call != call) r = ALD_EBLOCKED;
-        else if (c.err == DEV_ESLOTS) r = ALD_ESLOTS;
-        else if (c.err == DEV_EOVERFLOW) r = ALD_EOVERFLOW;
-        else if (c.err == DEV_EINVAL) r = ALD_EINVAL;
-        else if (c.err != 0) r = ALD_EHIP;
-        else if (c.start < c.Q) r = ALD_EINCOMPLETE;
-    }
-    *status = r;
-}
+// The outcome of an asynchronous call with no queries.
+__global__ void k_status_ok(int32_t* status) { *status = ALD_OK; }
 
 __global__ void k_summary(State st, int32_t W, int32_t* B, int64_t* sc, int64_t* sr, int64_t* peak)
 {
@@ -1177,9 +1162,9 @@ hipError_t launch_begin(const Ctl& c, const TileInfo& ti, Ctl* ctl, TileInfo* ti
     return hipGetLastError();
 }
 
-hipError_t launch_status(const Ctl* ctl, int32_t call, int32_t* status, hipStream_t stream)
+hipError_t launch_status_ok(int32_t* status, hipStream_t stream)
 {
-    hipLaunchKernelGGL(k_status, dim3(1), dim3(1), 0, stream, ctl, call, status);
+    hipLaunchKernelGGL(k_status_ok, dim3(1), dim3(1), 0, stream, status);
     return hipGetLastError();
 }
 
