@@ -53,8 +53,10 @@
  *     only memory the library allocates is one pinned host buffer per handle
  *     (76 bytes per scenario) into which the kernels copy their control blocks.
  *   - All work runs on the stream given to ald_create.  Every call below but
- *     ald_place_stream_async returns after that stream has finished the call's
- *     work, so errors are synchronous and outputs are ready on return.
+ *     ald_place_stream_async and ald_sweep_scenarios_async returns after that
+ *     stream has finished the call's work, so errors are synchronous and
+ *     outputs are ready on return; those two validate their arguments, enqueue
+ *     their work and return, and report the outcome in a device status word.
  *   - Return value: ALD_OK (0) or a negative ALD_E* code; ald_last_error() gives
  *     a message.  On a validation error nothing is written to the outputs and
  *     the handle's worker state is unchanged.
@@ -312,6 +314,26 @@ int ald_sweep_scenarios_hb(ald_handle_t handle, int32_t S, const ald_scenario_t*
                            const int32_t* heartbeat_every, int32_t Q, const int32_t* q_l_in,
                            const int32_t* q_l_pred, int32_t* out_rejected, int32_t* out_first_reject,
                            int32_t* out_worker, int64_t* out_min_gpus);
+
+/* The scaling sweep of Sec. 4.4 (ald_sweep_scenarios, or with heartbeat_every
+ * non-NULL ald_sweep_scenarios_hb), stream-asynchronous: the call validates
+ * its arguments, enqueues its work and returns without waiting; the host
+ * arrays scen and heartbeat_every are read before it returns.  It enqueues
+ * the rounds every scenario needs when no tile is cut, plus spare_rounds
+ * (>= 0) more.  *status (a DEVICE int32), valid with the outputs once the
+ * stream has reached the call, is ALD_OK; ALD_EINCOMPLETE when tiles were cut
+ * more often than spare_rounds allowed (the outputs are not valid: run the
+ * sweep again, synchronously or with more spare rounds; a sweep changes no
+ * handle state, so nothing needs finishing); or the code the synchronous
+ * sweep returns for a device error (ALD_EINVAL for a query length outside
+ * [1, 2^24]).  The query arrays and outputs must stay valid until the stream
+ * has reached the call, and the sweep's tables in the workspace stay in use
+ * until then (a later call on the handle is ordered after it on the stream). */
+int ald_sweep_scenarios_async(ald_handle_t handle, int32_t S, const ald_scenario_t* scen,
+                              const int32_t* heartbeat_every, int32_t Q, const int32_t* q_l_in,
+                              const int32_t* q_l_pred, int32_t spare_rounds, int32_t* out_rejected,
+                              int32_t* out_first_reject, int32_t* out_worker, int64_t* out_min_gpus,
+                              int32_t* status);
 
 /* Algorithm 2 (Sec. 4.3): re-balance the new requests of a heartbeat against
  * the output-length prediction errors of the ongoing ones, for P independent

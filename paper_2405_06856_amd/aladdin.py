@@ -54,7 +54,8 @@ SYMBOLS = ("ald_create", "ald_destroy", "ald_set_workspace", "ald_workspace_need
            "ald_sweep_workspace_size", "ald_set_tile", "ald_load_workers", "ald_load_workers_history",
            "ald_place_stream", "ald_place_stream_async", "ald_place_resume", "ald_place_stream_hb",
            "ald_place_grouped", "ald_move_requests",
-           "ald_sweep_scenarios", "ald_sweep_scenarios_hb", "ald_rebalance", "ald_rebalance_noalloc",
+           "ald_sweep_scenarios", "ald_sweep_scenarios_hb", "ald_sweep_scenarios_async", "ald_rebalance",
+           "ald_rebalance_noalloc",
            "ald_worker_summary", "ald_set_profiling", "ald_kernel_time", "ald_place_stats", "ald_last_error",
            "ald_strerror")
 
@@ -83,6 +84,7 @@ def _load():
         "ald_move_requests": ([P, i32, P, P, P, P], ctypes.c_int),
         "ald_sweep_scenarios": ([P, i32, P, i32, P, P, P, P, P, P], ctypes.c_int),
         "ald_sweep_scenarios_hb": ([P, i32, P, P, i32, P, P, P, P, P, P], ctypes.c_int),
+        "ald_sweep_scenarios_async": ([P, i32, P, P, i32, P, P, i32, P, P, P, P, P], ctypes.c_int),
         "ald_rebalance": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, i32, P, P], ctypes.c_int),
         "ald_rebalance_noalloc": ([P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, i32, P, P], ctypes.c_int),
         "ald_worker_summary": ([P, P, P, P, P], ctypes.c_int),
@@ -226,6 +228,21 @@ def ald_sweep_scenarios(h, S: int, scen, Q: int, q_l_in, q_l_pred, out_rejected,
     _check(h, _L.ald_sweep_scenarios(h, int(S), ctypes.cast(scen, ctypes.c_void_p), int(Q), _dptr(q_l_in),
                                      _dptr(q_l_pred), _dptr(out_rejected), _dptr(out_first_reject),
                                      _dptr(out_worker), _dptr(out_min_gpus)))
+
+
+def ald_sweep_scenarios_async(h, S: int, scen, heartbeat_every, Q: int, q_l_in, q_l_pred, spare_rounds: int,
+                              out_rejected, out_first_reject, out_worker, out_min_gpus, status) -> None:
+    """heartbeat_every: None or a host array of S periods; status: device int32 [1]."""
+    hb = None
+    if heartbeat_every is not None:
+        hb = np.ascontiguousarray(heartbeat_every, dtype=np.int32)
+        if hb.shape != (int(S),):
+            raise ValueError("heartbeat_every must hold one period per scenario")
+    _check(h, _L.ald_sweep_scenarios_async(h, int(S), ctypes.cast(scen, ctypes.c_void_p),
+                                           None if hb is None else hb.ctypes.data_as(ctypes.c_void_p), int(Q),
+                                           _dptr(q_l_in), _dptr(q_l_pred), int(spare_rounds), _dptr(out_rejected),
+                                           _dptr(out_first_reject), _dptr(out_worker), _dptr(out_min_gpus),
+                                           _dptr(status)))
 
 
 def ald_sweep_scenarios_hb(h, S: int, scen, heartbeat_every, Q: int, q_l_in, q_l_pred, out_rejected,
@@ -514,6 +531,27 @@ class Evaluator:
             b = best.cpu().numpy()
             out = out + ((None, -1) if b[0] < 0 else (int(b[0]), int(b[1])),)
         return out
+
+    def sweep_async(self, scenarios, q_l_in, q_l_pred, want_workers=False, heartbeat_every=None, spare_rounds=0):
+        """As sweep, with device query tensors, returning once the work is
+        enqueued: device tensors (rejected, first rejected, workers or None,
+        answer int64 [2], status int32 [1]); status reads ALD_OK once the
+        stream has run the sweep, ALD_EINCOMPLETE if its rounds ran out."""
+        t = self.torch
+        S = len(scenarios)
+        arr = (Scenario * S)()
+        for i, s in enumerate(scenarios):
+            arr[i] = Scenario(s.n_workers, s.gpus_per_worker, s.kv_capacity, to_model(s.model))
+        Q = int(q_l_in.numel())
+        rej = t.empty(S, dtype=t.int32, device=self.device)
+        first = t.empty(S, dtype=t.int32, device=self.device)
+        ow = t.empty(max(S * Q, 1), dtype=t.int32, device=self.device) if want_workers else None
+        best = t.empty(2, dtype=t.int64, device=self.device)
+        status = t.empty(1, dtype=t.int32, device=self.device)
+        hb = None if heartbeat_every is None else np.broadcast_to(np.asarray(heartbeat_every, dtype=np.int32), (S,))
+        self.call(ald_sweep_scenarios_async, S, arr, hb, Q, q_l_in, q_l_pred, spare_rounds, rej, first, ow, best,
+                  status)
+        return rej, first, ow, best, status
 
     def rebalance(self, batch, want_log=False):
         """Algorithm 2 on a workloads.RebalanceBatch; returns the new workers and

@@ -1599,13 +1599,17 @@ int rebalance_impl(ald_handle_t h, int32_t P, const int32_t* n_workers, const al
 namespace {
 
 // The sweep, with a heartbeat period per scenario (H null: none).
+// With `status` (a device word) the sweep is asynchronous: it enqueues the
+// rounds every scenario needs if no tile is cut, plus `spare` more, and a
+// status kernel writes the outcome.
 int sweep(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* H, int32_t Q, const int32_t* q_l_in,
           const int32_t* q_l_pred, int32_t* out_rejected, int32_t* out_first_reject, int32_t* out_worker,
-          int64_t* out_min_gpus, size_t* size_only = nullptr)
+          int64_t* out_min_gpus, size_t* size_only = nullptr, int32_t* status = nullptr, int32_t spare = 0)
 {
     if (!h) return ALD_EINVAL;
     HIPCHK(h, hipSetDevice(h->device));
     if (S <= 0 || Q < 0) return fail(h, ALD_EINVAL, "S must be >= 1 and Q >= 0");
+    if (status && (spare < 0 || spare > (1 << 20))) return fail(h, ALD_EINVAL, "spare_rounds must lie in [0, 2^20]");
     if (S >= (1 << 24)) return fail(h, ALD_EINVAL, "at most 2^24 - 1 scenarios");
     if (!scen) return fail(h, ALD_EINVAL, "null argument");
     if (!size_only && (!out_rejected || !out_first_reject)) return fail(h, ALD_EINVAL, "null argument");
@@ -1693,10 +1697,25 @@ int sweep(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* 
     HIPCHK(h, hipMemcpyAsync(a.dscen, a.hscen.data(), S * sizeof(Scen), hipMemcpyHostToDevice, h->stream));
     if (Q > 0) {
         HIPCHK(h, launch_query_stats(q_l_in, q_l_pred, Q, a.st.ctl, S, h->stream));
-        rc = run_rounds(h, &a, any_hb, 0, c);
-        if (rc != ALD_OK) return rc;
+        if (status) {
+            rc = ensure_hctl(h, &a);
+            if (rc != ALD_OK) return rc;
+            const int64_t need = rounds_needed(c, a.hb_host);
+            if (need < 1) return fail(h, ALD_EHIP, "internal error: a tile of no queries");
+            for (int64_t r = 0; r < need + spare; ++r) {
+                rc = launch_round(h, &a, r == 0 ? 0 : (any_hb ? 0 : 1));
+                if (rc != ALD_OK) return rc;
+            }
+        } else {
+            rc = run_rounds(h, &a, any_hb, 0, c);
+            if (rc != ALD_OK) return rc;
+        }
     }
     HIPCHK(h, launch_sweep_outputs(a.st, out_rejected, out_first_reject, out_min_gpus, h->stream));
+    if (status) {
+        HIPCHK(h, launch_sweep_status(a.st, status, h->stream));
+        return ALD_OK;
+    }
     HIPCHK(h, hipStreamSynchronize(h->stream));
     return ALD_OK;
 }
@@ -1710,6 +1729,16 @@ int ald_sweep_scenarios(ald_handle_t h, int32_t S, const ald_scenario_t* scen, i
                         int32_t* out_worker, int64_t* out_min_gpus)
 {
     return sweep(h, S, scen, nullptr, Q, q_l_in, q_l_pred, out_rejected, out_first_reject, out_worker, out_min_gpus);
+}
+
+int ald_sweep_scenarios_async(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* heartbeat_every,
+                              int32_t Q, const int32_t* q_l_in, const int32_t* q_l_pred, int32_t spare_rounds,
+                              int32_t* out_rejected, int32_t* out_first_reject, int32_t* out_worker,
+                              int64_t* out_min_gpus, int32_t* status)
+{
+    if (h && !status) return fail(h, ALD_EINVAL, "null status");
+    return sweep(h, S, scen, heartbeat_every, Q, q_l_in, q_l_pred, out_rejected, out_first_reject, out_worker,
+                 out_min_gpus, nullptr, status, spare_rounds);
 }
 
 int ald_sweep_workspace_size(ald_handle_t h, int32_t S, const ald_scenario_t* scen, int32_t Q, size_t* bytes)

@@ -290,5 +290,7 @@ hipError_t launch_summary(const State& st, int32_t W, int32_t* B, int64_t* sc, i
 // scenario with no rejection and the fewest GPUs: {GPUs, scenario} or {-1, -1}
 hipError_t launch_sweep_outputs(const State& st, int32_t* rejected, int32_t* first_reject, int64_t* min_gpus,
                                 hipStream_t stream);
+// status = the outcome of an asynchronous sweep (after its rounds)
+hipError_t launch_sweep_status(const State& st, int32_t* status, hipStream_t stream);
 
 }  // namespace ald

@@ -1097,6 +1097,24 @@ __global__ __launch_bounds__(256) void k_sweep_best(State st, int64_t* min_gpus)
     }
 }
 
+// The outcome of an asynchronous sweep: the first scenario (by index) with a
+// device error gives the code, as the synchronous sweep returns it; else
+// ALD_EINCOMPLETE if a scenario has queries left, else ALD_OK.  One block.
+__global__ __launch_bounds__(256) void k_sweep_status(State st, int32_t* status)
+{
+    __shared__ int64_t red[4];
+    int64_t first_err = INT32_MAX, left = 0;
+    for (int s = threadIdx.x; s < st.S; s += 256) {
+        const Ctl c = st.ctl[s];
+        if (c.err != 0 && s < first_err) first_err = s;
+        left |= c.start < c.Q ? 1 : 0;
+    }
+    first_err = block_reduce<256>(first_err, (int64_t)INT32_MAX, OpMin(), red);
+    left = block_reduce<256>(left, (int64_t)0, OpMax(), red);
+    if (threadIdx.x == 0)
+        *status = first_err != INT32_MAX ? ctl_status(st.ctl[first_err]) : (left ? ALD_EINCOMPLETE : ALD_OK);
+}
+
 // ---------------------------------------------------------------------------------------------
 hipError_t launch_ingest(const State& st, int32_t W, const int64_t* res_off, const int32_t* lin,
                          const int32_t* lpred, const int32_t* gen, const double* tdec, hipStream_t stream)
@@ -1183,6 +1201,12 @@ hipError_t launch_sweep_outputs(const State& st, int32_t* rejected, int32_t* fir
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || min_gpus == nullptr) return e;
     hipLaunchKernelGGL(k_sweep_best, dim3(1), dim3(256), 0, stream, st, min_gpus);
+    return hipGetLastError();
+}
+
+hipError_t launch_sweep_status(const State& st, int32_t* status, hipStream_t stream)
+{
+    hipLaunchKernelGGL(k_sweep_status, dim3(1), dim3(256), 0, stream, st, status);
     return hipGetLastError();
 }
 

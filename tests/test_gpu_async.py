@@ -205,3 +205,65 @@ def test_async_errors_and_empty_calls(aladdin):
     ev.close()
     want = ref.place_trace(t, heartbeat_every=0)
     assert np.array_equal(got.worker, want.worker)
+
+
+def mini_sweep(seed, Q):
+    return wl.make_sweep("mini-hb", seed, Q=Q, worker_counts=(1, 2, 3, 5, 16, 40), gpu_counts=(1, 2),
+                         base_capacity=65536, model=wl.BASE_MODEL, in_dist=wl.MID_IN, out_dist=wl.MID_OUT, rate=None)
+
+
+def check_sweep(aladdin, s, got, H):
+    rej, first, ow, best, status = got
+    assert int(status.item()) == aladdin.ALD_OK
+    S, Q = len(s.scenarios), len(s.q_l_in)
+    orej, ofirst, oworkers = ref.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True, heartbeat_every=H,
+                                       n_threads=4)
+    assert np.array_equal(ow.cpu().numpy()[:S * Q].reshape(S, Q), oworkers)
+    assert np.array_equal(rej.cpu().numpy(), orej)
+    assert np.array_equal(first.cpu().numpy(), ofirst)
+    b = best.cpu().numpy()
+    assert ((None, -1) if b[0] < 0 else (int(b[0]), int(b[1]))) == ref.min_gpus(s.scenarios, orej)
+
+
+def test_async_sweeps_back_to_back_match_oracle(aladdin):
+    import torch
+    s1, s2 = mini_sweep(21, 2500), mini_sweep(22, 1800)
+    H2 = np.array([0, 1, 2, 7, 25, 64, 100, 333, 1000, 1799, 1800, 5000], np.int32)
+    ev = aladdin.Evaluator(0, tile=1024)
+    dev = ev.device
+    q1 = [torch.as_tensor(x, dtype=torch.int32, device=dev) for x in (s1.q_l_in, s1.q_l_pred)]
+    q2 = [torch.as_tensor(x, dtype=torch.int32, device=dev) for x in (s2.q_l_in, s2.q_l_pred)]
+    # two sweeps in flight: the second lays its tables over the first's, after it on the stream
+    g1 = ev.sweep_async(s1.scenarios, *q1, want_workers=True, spare_rounds=256)
+    g2 = ev.sweep_async(s2.scenarios, *q2, want_workers=True, heartbeat_every=H2, spare_rounds=256)
+    torch.cuda.synchronize()
+    check_sweep(aladdin, s1, g1, None)
+    check_sweep(aladdin, s2, g2, H2)
+    # Long tiles on small clusters that fill up: the synchronous sweep cuts
+    # tiles (its tile statistics say so), and without heartbeats every
+    # scenario has the same tiles, so a sweep with no spare round cannot finish
+    s3 = wl.make_sweep("async-cuts", 23, Q=3000, worker_counts=(6, 12, 40), gpu_counts=(1,), base_capacity=8000,
+                       model=wl.BASE_MODEL, in_dist=wl.SHORT_IN, out_dist=wl.SHORT_OUT, rate=None)
+    ev3 = aladdin.Evaluator(0, tile=4096)
+    ev3.sweep(s3.scenarios, s3.q_l_in, s3.q_l_pred)
+    st = ev3.tile_stats()
+    print("sweep tile statistics", st, flush=True)
+    assert st["cuts"] > 0
+    q3 = [torch.as_tensor(x, dtype=torch.int32, device=dev) for x in (s3.q_l_in, s3.q_l_pred)]
+    g = ev3.sweep_async(s3.scenarios, *q3, want_workers=True, spare_rounds=0)
+    torch.cuda.synchronize()
+    assert int(g[4].item()) == aladdin.ALD_EINCOMPLETE
+    g = ev3.sweep_async(s3.scenarios, *q3, want_workers=True, spare_rounds=int(st["cuts"]))
+    torch.cuda.synchronize()
+    check_sweep(aladdin, s3, g, None)
+    ev3.close()
+    # a query length outside [1, 2^24]
+    bad = q1[0].clone()
+    bad[5] = 0
+    g = ev.sweep_async(s1.scenarios, bad, q1[1], spare_rounds=4)
+    torch.cuda.synchronize()
+    assert int(g[4].item()) == aladdin.ALD_EINVAL
+    with pytest.raises(aladdin.AladdinError) as e:
+        ev.sweep_async(s1.scenarios, *q1, spare_rounds=-1)
+    assert e.value.code == aladdin.ALD_EINVAL
+    ev.close()
