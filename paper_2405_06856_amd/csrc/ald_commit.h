@@ -143,6 +143,40 @@ __device__ __forceinline__ WinBits load_win_bits(const State& st, const Scen& sc
     return b;
 }
 
+// Sorted tile layout: the window cache of the dirty workers dw[0 .. cnt)
+// (lane jb + k gets worker dw[k]'s words), in the arrival order that
+// load_win_bits gives in the arrival layout.  The wave gathers them: lane i
+// reads, for each worker, the word holding query w0 + i at its sorted tile
+// position tp, and the two ballots are that worker's bits for the window.
+// Eight workers' loads go out together.
+__device__ __forceinline__ void gather_win_bits(const State& st, const Scen& sc, const int32_t* dw, int jb, int cnt,
+                                                int start, int w0, bool act, int tp, WinBits& wb)
+{
+    const int lane = lane_id();
+    const int64_t row = sc.bits_off + (int64_t)(tp >> 6) * sc.W;
+    const int bit = tp & 63, s = (w0 - start) & 63;
+    for (int j0 = 0; j0 < cnt; j0 += 8) {
+        uint64_t f[8], n[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const bool ok = act && j0 + u < cnt;
+            const int w = dw[min(j0 + u, cnt - 1)];
+            f[u] = ok ? st.bits_feas[row + w] : 0;
+            n[u] = ok ? st.bits_nt[row + w] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const uint64_t fb = ballot((f[u] >> bit) & 1), nb = ballot((n[u] >> bit) & 1);
+            if (j0 + u < cnt && lane == jb + j0 + u) {
+                wb.f0 = fb << s;
+                wb.n0 = nb << s;
+                wb.f1 = s ? fb >> (64 - s) : 0;
+                wb.n1 = s ? nb >> (64 - s) : 0;
+            }
+        }
+    }
+}
+
 // bit of query i (tile offset) in a cached window
 __device__ __forceinline__ bool win_bit(uint64_t lo, uint64_t hi, int start, int w0, int i)
 {
@@ -473,8 +507,9 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
         have = have | take;
     }
     if (!have && q.ncand > TOPK) {  // every listed candidate was committed to: the best untouched one
+        const int tp = st.qpos != nullptr ? st.qpos[i - start] : i - start;  // the query's bit position
         const KeyW c = best_untouched(st.bits_feas, st.key + sc.wbase, &L, sc.W, nd,
-                                      sc.bits_off + (int64_t)((i - start) >> 6) * sc.W, (i - start) & 63, true,
+                                      sc.bits_off + (int64_t)(tp >> 6) * sc.W, tp & 63, true,
                                       sc.uniform_M != 0, !want_diag);
         have = c.w >= 0;
         bk = have ? c.k : bk;
@@ -592,8 +627,9 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
         } else if (r.w < 0) {
             nt = true;
         } else {  // the best near-tie worker was committed to: the best untouched one with a near tie
+            const int tp = st.qpos != nullptr ? st.qpos[i - start] : i - start;
             const KeyW c = best_untouched(st.bits_nt, st.key + sc.wbase, &L, sc.W, nd,
-                                          sc.bits_off + (int64_t)((i - start) >> 6) * sc.W, (i - start) & 63, false,
+                                          sc.bits_off + (int64_t)(tp >> 6) * sc.W, tp & 63, false,
                                           sc.uniform_M != 0, !want_diag);
             nt = c.w >= 0 && !ranks_before(bk, bw, c.k, c.w);
             r.fallback = 1;
@@ -766,16 +802,24 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
         const int w0 = pos;
         const int i = w0 + lane;
         const bool act = i < end;
+        // the tile position of this lane's query: its own offset, or in the
+        // sorted layout where the pair evaluation put it (the selection's
+        // summaries and the bit words are kept by position)
+        const int tp = (st.qpos != nullptr && act) ? st.qpos[i - start] : i - start;
         QSum q;
         int32_t lin = 1, lp = 1;
         if (act) {
-            q = st.qsum[sc.qsum_off + (i - start)];
+            q = st.qsum[sc.qsum_off + tp];
             lin = st.q_lin[q_at(sc, i)];
             lp = st.q_lpred[q_at(sc, i)];
         } else {
             q.nfeas = 0;
         }
-        if (lane < nd) wb = load_win_bits(st, sc, a.w, start, w0, end);
+        // the window's bit words of the dirty workers
+        if (st.qpos != nullptr)
+            gather_win_bits(st, sc, L.dw, 0, nd, start, w0, act, tp, wb);
+        else if (lane < nd)
+            wb = load_win_bits(st, sc, a.w, start, w0, end);
         const uint64_t potm = ballot(act && q.nfeas > 0);
         int cur = 0;
         while (cur < NT && w0 + cur < end) {
@@ -870,11 +914,15 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
                     a.SR = st.SR[gw];
                     a.key = st.key[gw];
                     a.rhs = st.rhs[gw];
-                    wb = load_win_bits(st, sc, w, start, w0, end);
+                    if (st.qpos == nullptr) wb = load_win_bits(st, sc, w, start, w0, end);
                 }
                 if (lane == 0) {
                     L.dw[j] = w;
                     if (sc.W <= DBITS_W * 32) L.dbits[w >> 5] |= 1u << (w & 31);
+                }
+                if (st.qpos != nullptr) {
+                    wave_sync();  // L.dw[j] written
+                    gather_win_bits(st, sc, L.dw + j, j, 1, start, w0, act, tp, wb);
                 }
                 nd += 1;
             }

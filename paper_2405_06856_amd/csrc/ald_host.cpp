@@ -360,7 +360,12 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks, ch
         sc.qsum_off = qs;
         qs += (int64_t)schunks * SEL_THREADS;
     }
-    *bytes = align256((size_t)bits * 16 + (size_t)part * sizeof(ulonglong2) + (size_t)qs * sizeof(QSum) + 1024);
+    // one-scenario tiles this long are evaluated in l_pred order: the tile's
+    // permutation and its inverse
+    const bool sorted = a->S == 1 && T >= SORT_MIN_TILE;
+    const size_t perm_bytes = sorted ? align256((size_t)echunks * EVAL_Q * sizeof(int32_t)) : 0;
+    *bytes = align256((size_t)bits * 16 + (size_t)part * sizeof(ulonglong2) + (size_t)qs * sizeof(QSum) + 1024) +
+             2 * perm_bytes;
     if (!base) return ALD_OK;
     a->hscen = hs;
     a->eval_blocks = eb;
@@ -379,6 +384,11 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks, ch
     p += (size_t)part * sizeof(ulonglong2);
     p = (char*)(((uintptr_t)p + 255) & ~(uintptr_t)255);
     a->st.qsum = (QSum*)p;
+    p += (size_t)qs * sizeof(QSum);
+    p = (char*)(((uintptr_t)p + 255) & ~(uintptr_t)255);
+    a->st.qorig = sorted ? (int32_t*)p : nullptr;
+    a->st.qpos = sorted ? (int32_t*)(p + perm_bytes) : nullptr;
+
     HIPCHK(h, hipMemcpyAsync(a->dscen, a->hscen.data(), a->S * sizeof(Scen), hipMemcpyHostToDevice, h->stream));
     return ALD_OK;
 }

@@ -39,6 +39,7 @@ constexpr int EVAL_QPT = 4;        // queries per pair-evaluation thread
 constexpr int EVAL_Q = EVAL_THREADS * EVAL_QPT;  // queries per pair-evaluation block
 constexpr int EVAL_WPB_MAX = 64;  // workers per pair-evaluation block at most
 constexpr int STAGE_MAX = 768;     // live requests of a worker the evaluation stages in LDS (fewer than)
+constexpr int SORT_MIN_TILE = 16384;  // one-scenario tiles at least this long are evaluated in l_pred order
 constexpr int SEL_THREADS = 256;   // queries per selection block
 constexpr int COMMIT_THREADS = 64;  // the arrival-order commit runs as one wave
 constexpr int HOT = 8192;          // most request slots per worker (commit keeps one worker in LDS)
@@ -140,7 +141,8 @@ struct TileInfo {
     int32_t first_pc[2];  // first query of the tile with a feasible worker (by round parity)
 };
 
-// Per-query result of the selection kernel (tile-start state).  With
+// Per-query result of the selection kernel (tile-start state), kept by tile
+// position (the query's offset, or its place in the sorted layout).  With
 // interchangeable empty workers (uniform capacity), empty workers are not listed
 // one by one: `efeas` says whether an empty worker is feasible (all are alike).
 struct QSum {
@@ -239,6 +241,13 @@ struct State {
     // tile scratch
     uint64_t* bits_feas;
     uint64_t* bits_nt;
+    // Sorted tile layout (one-scenario tiles of at least SORT_MIN_TILE queries;
+    // null otherwise): the pair evaluation takes each chunk of EVAL_Q queries in
+    // order of l_pred, and the bit words and excess keys are kept by that order.
+    // qorig[p] = tile offset of the query at sorted tile position p; qpos is the
+    // inverse (both per tile offset, pstride entries).
+    int32_t* qorig;
+    int32_t* qpos;
     ulonglong2* part;  // per (worker block, query): the two smallest KV-excess keys
     QSum* qsum;
     // queries and outputs

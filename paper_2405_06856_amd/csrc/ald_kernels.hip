@@ -665,6 +665,84 @@ __device__ __forceinline__ void near_tie_words(const State& st, const Scen& sc, 
     if (lane >= EVAL_QPT && lane < 2 * EVAL_QPT) bdst[w] = bits;
 }
 
+// Sorted layout (a one-scenario tile with State::qorig): the order in which
+// the block evaluates its chunk of EVAL_Q queries, by l_pred in buckets of 8
+// (the last bucket also takes every l_pred above 2032), ties by arrival, the
+// chunk's missing queries (offsets >= nact) last, so that the lanes of a wave
+// read neighbouring breakpoint entries and summaries.  Every worker block of
+// the chunk computes the same order.  A stable counting sort: the lanes of a
+// wave with the same bucket find each other by eight ballots (one per key
+// bit); a histogram per (segment of 64 offsets, bucket) and one scan over the
+// buckets give each query its position.  On return o[m] is the chunk offset
+// of the query at position m * NT + tid (its lengths are then read again:
+// passing them through LDS, or holding them through the sort, measured
+// slower); the chunk's first worker block writes the tile's permutation
+// (qorig, qpos).  `sh`: 10 KB of scratch (histogram, then the permutation);
+// `red` that of block_scan_excl.
+template <int QPT>
+__device__ __forceinline__ void sort_chunk(const State& st, const Scen& sc, int start, int q0, int nact, bool writer,
+                                           int (&o)[QPT], uint16_t* sh, int64_t* red)
+{
+    constexpr int NT = EVAL_THREADS;
+    constexpr int NB = 256;                 // buckets (one per thread for the scan)
+    constexpr int NS = QPT * (NT / 64);     // segments of 64 offsets: segment m * 4 + wave
+    static_assert(NT == NB, "one bucket per thread");
+    uint16_t* H = sh;                       // [NS][NB] counts, then positions
+    uint16_t* perm = sh + NS * NB;          // sorted position -> chunk offset
+    const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
+    const uint64_t below = (1ull << lane) - 1;
+    for (int k = tid; k < NS * NB / 4; k += NT) reinterpret_cast<uint64_t*>(H)[k] = 0;
+    int key[QPT];
+#pragma unroll
+    for (int m = 0; m < QPT; ++m) {
+        const int off = m * NT + tid;
+        const bool in = off < nact;
+        const int32_t l = in ? st.q_lpred[q_at(sc, q0 + off)] : 1;
+        // (an invalid length, which fails the call, still gets a bucket)
+        key[m] = in ? min(max(l - 1, 0) >> 3, NB - 2) : NB - 1;
+    }
+    __syncthreads();
+    int rank[QPT];
+#pragma unroll
+    for (int m = 0; m < QPT; ++m) {
+        uint64_t peers = ~0ull;
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            const bool kb = (key[m] >> b) & 1;
+            const uint64_t bb = ballot(kb);
+            peers &= kb ? bb : ~bb;
+        }
+        rank[m] = __popcll(peers & below);
+        if (rank[m] == 0) H[(m * (NT / 64) + wv) * NB + key[m]] = (uint16_t)__popcll(peers);
+    }
+    __syncthreads();
+    int64_t cnt = 0;
+    for (int sg = 0; sg < NS; ++sg) cnt += H[sg * NB + tid];
+    int64_t all;
+    int64_t at = block_scan_excl<NT, false>(cnt, 0, OpAdd(), &all, red);
+    for (int sg = 0; sg < NS; ++sg) {
+        const int n = H[sg * NB + tid];
+        H[sg * NB + tid] = (uint16_t)at;
+        at += n;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int m = 0; m < QPT; ++m) perm[H[(m * (NT / 64) + wv) * NB + key[m]] + rank[m]] = (uint16_t)(m * NT + tid);
+    __syncthreads();
+    const int t0 = q0 - start;  // the chunk's first tile offset
+#pragma unroll
+    for (int m = 0; m < QPT; ++m) {
+        const int p = m * NT + tid;
+        const int off = perm[p];
+        o[m] = off;
+        if (writer && p < nact) {
+            st.qorig[t0 + p] = t0 + off;
+            st.qpos[t0 + off] = t0 + p;
+        }
+    }
+    __syncthreads();  // the scratch is the staging area of the evaluation
+}
+
 // Pair evaluation: block = (scenario, worker block, chunk of EVAL_Q queries).
 // Thread t holds queries t, t + 256, t + 512, t + 768 of the chunk.  For each
 // worker of the block, its summaries and breakpoint table (built with the
@@ -685,6 +763,7 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
     __shared__ int4 Ss[PF_N * NT];                 // pms of live slot k, k = 0..B
     __shared__ WInfo Wi[EVAL_WPB_MAX];
     __shared__ int64_t red[NT / 64];
+    static_assert(sizeof(Ss) >= 10 * 1024, "the sort's scratch");
 
     const int s = find_scen<&Scen::eval_blk0>(st, blockIdx.x);
     const Scen sc = st.scen[s];
@@ -712,16 +791,25 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
     const int tid = threadIdx.x;
     const int lane = lane_id();
 
+    // Thread tid evaluates chunk positions m * NT + tid: the chunk's queries in
+    // arrival order, or (sorted layout) in order of l_pred.  o[m] = the chunk
+    // offset of the query at position m * NT + tid.
+    // Thread tid evaluates chunk positions m * NT + tid: the queries in
+    // arrival order, or (sorted layout) in order of l_pred
+    int o[QPT];  // chunk offset of the query at position m * NT + tid
+#pragma unroll
+    for (int m = 0; m < QPT; ++m) o[m] = m * NT + tid;
+    if (st.qorig != nullptr)
+        sort_chunk<QPT>(st, sc, start, q0, min(EVAL_Q, end - q0), wb == 0, o, reinterpret_cast<uint16_t*>(Ss), red);
     int32_t lin[QPT], lp[QPT];
     bool act[QPT];
     int32_t e1[QPT], w1[QPT], e2[QPT], w2[QPT];  // two smallest KV excesses per query
     int64_t lpmax = 0, qdmin = INT64_MAX, qdmax = INT64_MIN, lnmin = INT64_MAX, lnmax = INT64_MIN;
 #pragma unroll
     for (int m = 0; m < QPT; ++m) {
-        const int qi = q0 + m * NT + tid;
-        act[m] = qi < end;
-        lin[m] = act[m] ? st.q_lin[q_at(sc, qi)] : 1;
-        lp[m] = act[m] ? st.q_lpred[q_at(sc, qi)] : 1;
+        act[m] = q0 + m * NT + tid < end;
+        lin[m] = act[m] ? st.q_lin[q_at(sc, q0 + o[m])] : 1;
+        lp[m] = act[m] ? st.q_lpred[q_at(sc, q0 + o[m])] : 1;
         e1[m] = e2[m] = INT32_MAX;
         w1[m] = w2[m] = -1;
         const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
@@ -848,8 +936,11 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     const int q0 = start + group * 64;
     const bool live = q0 < end;                     // wave-uniform
     const int lane = lane_id();
-    const int qi = q0 + lane;
-    const bool act = live && qi < end;
+    // the group's words hold tile positions q0 - start + lane: the queries in
+    // arrival order, or (sorted layout) the query qorig of each position
+    const int slot = q0 - start + lane;
+    const bool act = live && q0 + lane < end;
+    const int qi = (act && st.qorig != nullptr) ? start + st.qorig[slot] : q0 + lane;
 
     uint64_t tkey[TOPK];
     int32_t tw[TOPK];
@@ -924,7 +1015,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     // first = smaller first; new second = min(larger first, smaller second))
     uint64_t a1 = ~0ull, a2 = ~0ull;
     if (act && st.out_diag) {
-        const ulonglong2* prow = st.part + sc.part_off + (qi - start);
+        const ulonglong2* prow = st.part + sc.part_off + slot;
 #pragma unroll 8
         for (int b = slice; b < sc.nblk; b += G) {
             const ulonglong2 p = prow[(int64_t)b * sc.pstride];
@@ -997,7 +1088,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     q.ex1 = ex1; q.w1 = w1;
     q.ex2 = ex2; q.w2 = w2;
     q.pad = 0;
-    st.qsum[sc.qsum_off + (qi - start)] = q;
+    st.qsum[sc.qsum_off + slot] = q;  // by tile position, as the bit words
     if (q.nfeas > 0) {
         atomicMin(&st.tinfo[s].first_pc[parity], qi);
     } else if (st.qbad == nullptr || *st.qbad == 0) {

@@ -267,3 +267,17 @@ def test_async_sweeps_back_to_back_match_oracle(aladdin):
         ev.sweep_async(s1.scenarios, *q1, spare_rounds=-1)
     assert e.value.code == aladdin.ALD_EINVAL
     ev.close()
+
+
+def test_async_chain_in_sorted_layout_matches_oracle(aladdin):
+    # calls of at least 16,384 queries evaluate in l_pred order; rounds run
+    # out (no spare rounds) and the stopped call is resumed
+    t = trace(40, 3, 54000, 8000, 9500)
+    want = ref.place_trace(t, heartbeat_every=0)
+    ev = aladdin.Evaluator(0, tile=65536)
+    ev.load_trace(t)
+    got_w, got_d, short = run_async_chain(aladdin, ev, t, 0, chunks(54000, 3), 0)
+    summ = ev.summary()
+    ev.close()
+    assert short > 0
+    compare(got_w, got_d, summ, want, 0, 54000)

@@ -102,3 +102,54 @@ def test_near_ties_on_changed_workers_match_oracle(aladdin, W, Q, H):
     ev.close()
     assert st["fallbacks"] > 0
     compare(got, summ, want, Q, H, True)
+
+
+# Tiles of at least 16,384 queries take the sorted layout: the pair evaluation
+# takes each chunk of 1,024 queries in order of l_pred, and the commit gathers
+# its dirty workers' bits through the tile's permutation.  The same filling
+# clusters, the same oracle.
+SORTED_CASES = [
+    # W, residents per worker, Q, KV capacity, heartbeat period, diagnostics
+    (12, 5, 17000, 30000, 0, True),
+    (40, 3, 18000, 8000, 0, True),
+    (40, 3, 18000, 8000, 0, False),
+    (64, 1, 20000, 8000, 17000, True),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SORTED_CASES)))
+def test_sorted_layout_matches_oracle(aladdin, case):
+    W, R, Q, cap, H, diag = SORTED_CASES[case]
+    print("sorted layout case", case, "W", W, "R", R, "Q", Q, "cap", cap, "H", H, "diag", diag, flush=True)
+    t = wl.make_trace("sorted%d" % case, 7800 + case, W=W, R=R, Q=Q, kv_capacity=cap, model=wl.BASE_MODEL,
+                      in_dist=wl.SHORT_IN, out_dist=wl.SHORT_OUT, rate=200.0)
+    ev = aladdin.Evaluator(0, tile=65536)
+    ev.load_trace(t)
+    got = ev.place(t.q_l_in, t.q_l_pred, heartbeat_every=H, diag=diag)
+    st = ev.tile_stats()
+    print("tile statistics", st, flush=True)
+    summ = ev.summary()
+    ev.close()
+    want = ref.place_trace(t, heartbeat_every=H)
+    assert st["cuts"] > 0
+    placed = int((want.worker >= 0).sum())
+    assert 0 < placed < Q
+    compare(got, summ, want, Q, H, diag)
+
+
+def test_sorted_layout_near_ties_match_oracle(aladdin):
+    W, Q = 30, 17000
+    rng = np.random.default_rng(W + Q)
+    off = np.arange(W + 1, dtype=np.int64)
+    t = wl.Trace(name="nt-sorted", seed=0, model=NT_MODEL, kv_capacity=np.full(W, 10 ** 6, np.int64),
+                 res_offsets=off, res_l_in=rng.integers(1, 4, W).astype(np.int32),
+                 res_l_pred=rng.integers(1, 4, W).astype(np.int32), res_generated=np.zeros(W, np.int32),
+                 q_l_in=rng.integers(1, 12, Q).astype(np.int32), q_l_pred=rng.integers(1, 6, Q).astype(np.int32),
+                 arrivals=None, heartbeat_every=0)
+    want = ref.place_trace(t, heartbeat_every=0)
+    ev = aladdin.Evaluator(0, tile=65536)
+    ev.load_trace(t, slots_per_worker=256)
+    got = ev.place(t.q_l_in, t.q_l_pred, heartbeat_every=0, diag=True)
+    summ = ev.summary()
+    ev.close()
+    compare(got, summ, want, Q, 0, True)
