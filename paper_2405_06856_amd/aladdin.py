@@ -451,7 +451,7 @@ class Evaluator:
         elif status.dtype != t.int32 or status.numel() < 1:
             raise ValueError("status must be an int32 tensor of at least one element")
         self.call(ald_place_stream_async, Q, q_l_in, q_l_pred, heartbeat_every, spare_rounds, out, d, status)
-        return out, d, status
+        return out[:Q], (None if d is None else d[:Q * DIAG_DTYPE.itemsize]), status
 
     def resume(self) -> None:
         """Finish an asynchronous placement that ran out of rounds (synchronously)."""
