@@ -481,7 +481,9 @@ class Evaluator:
         self.call(ald_move_requests, len(l_in), l_in, l_pred, from_worker, to_worker)
 
     def place_grouped(self, group_workers, q_l_in, q_l_pred, heartbeat_every=0, diag=True) -> Placement:
-        """Grouped placement (App. A): query x of the stream goes to group x mod G."""
+        """Grouped placement (App. A): the router gives group i the share
+        N_i / N_w of the stream (every count within one query of its share) and
+        each group places its queries on its own workers."""
         t = self.torch
         ql = self._dev(q_l_in, t.int32)
         qp = self._dev(q_l_pred, t.int32)

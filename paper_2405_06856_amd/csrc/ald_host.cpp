@@ -290,6 +290,7 @@ int make_arena(ald_handle* h, Arena* a, const std::vector<Scen>& scen, const std
     HIPCHK(h, hipMemcpyAsync(st.cap, caps.data(), NW * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
     HIPCHK(h, hipMemcpyAsync(st.M, Ms.data(), NW * sizeof(int32_t), hipMemcpyHostToDevice, h->stream));
     HIPCHK(h, hipMemsetAsync(st.dcount, 0, a->S * sizeof(int32_t), h->stream));
+    HIPCHK(h, hipMemsetAsync(qbad, 0, sizeof(int32_t), h->stream));
     bool mono = true, ntint = true;
     int64_t wfirst = 0;
     for (int s = 0; s < a->S; ++s) {
@@ -1703,6 +1704,7 @@ int sweep(ald_handle_t h, int32_t S, const ald_scenario_t* scen, const int32_t* 
     a.st.out_worker = out_worker;
     a.st.out_diag = nullptr;
     a.st.err_word = nullptr;
+    a.st.qbad = nullptr;  // (also with one scenario) the queries are checked below, before the rounds
     for (int s = 0; s < S; ++s) a.hscen[s].out_off = (int64_t)s * Q;
     HIPCHK(h, hipMemcpyAsync(a.dscen, a.hscen.data(), S * sizeof(Scen), hipMemcpyHostToDevice, h->stream));
     if (Q > 0) {

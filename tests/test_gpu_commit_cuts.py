@@ -153,3 +153,32 @@ def test_sorted_layout_near_ties_match_oracle(aladdin):
     summ = ev.summary()
     ev.close()
     compare(got, summ, want, Q, 0, True)
+
+
+def test_sorted_layout_single_group_matches_oracle(aladdin):
+    # grouped placement with one group reads its queries through a query map
+    W, R, Q, cap = 24, 3, 17000, 8000
+    t = wl.make_trace("sorted-g1", 7900, W=W, R=R, Q=Q, kv_capacity=cap, model=wl.BASE_MODEL,
+                      in_dist=wl.SHORT_IN, out_dist=wl.SHORT_OUT, rate=200.0)
+    ev = aladdin.Evaluator(0, tile=65536)
+    ev.load_trace(t)
+    got = ev.place_grouped([W], t.q_l_in, t.q_l_pred, heartbeat_every=0, diag=True)
+    summ = ev.summary()
+    ev.close()
+    want = ref.place_grouped(W, t.kv_capacity, t.res_offsets, t.res_l_in, t.res_l_pred, t.res_generated, t.model,
+                             [W], t.q_l_in, t.q_l_pred, heartbeat_every=0)
+    assert 0 < int((want.worker >= 0).sum()) < Q
+    compare(got, summ, want, Q, 0, True)
+
+
+def test_sorted_layout_single_scenario_sweep_matches_oracle(aladdin):
+    s = wl.make_sweep("sorted-sweep", 7901, Q=17000, worker_counts=(12,), gpu_counts=(1,), base_capacity=8000,
+                      model=wl.BASE_MODEL, in_dist=wl.SHORT_IN, out_dist=wl.SHORT_OUT, rate=None)
+    ev = aladdin.Evaluator(0, tile=65536)
+    rej, first, workers = ev.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True)
+    ev.close()
+    orej, ofirst, oworkers = ref.sweep(s.scenarios, s.q_l_in, s.q_l_pred, want_workers=True)
+    assert 0 < orej[0] < 17000
+    assert np.array_equal(workers, oworkers)
+    assert np.array_equal(rej, orej)
+    assert np.array_equal(first, ofirst)
