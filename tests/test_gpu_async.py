@@ -281,3 +281,38 @@ def test_async_chain_in_sorted_layout_matches_oracle(aladdin):
     ev.close()
     assert short > 0
     compare(got_w, got_d, summ, want, 0, 54000)
+
+
+def test_async_calls_with_changing_heartbeat_periods_match_sync(aladdin):
+    # the host projects the stream position of every asynchronous call
+    # (heartbeats inside the call, and one already due when a call with a
+    # shorter period starts); the first synchronous call afterwards checks the
+    # projection against the device and fails on a difference
+    import torch
+    t = trace(16, 4, 2400, 30000, 9600)
+    parts = [(0, 500, 50), (500, 900, 20), (900, 1300, 0), (1300, 1800, 37), (1800, 2400, 64)]
+    res = []
+    for mode in ("sync", "async"):
+        ev = aladdin.Evaluator(0, tile=4096)
+        ev.load_trace(t)
+        dev = ev.device
+        ql = torch.as_tensor(t.q_l_in, dtype=torch.int32, device=dev)
+        qp = torch.as_tensor(t.q_l_pred, dtype=torch.int32, device=dev)
+        out = torch.full((2400,), -7, dtype=torch.int32, device=dev)
+        dg = torch.zeros(2400 * 40, dtype=torch.uint8, device=dev)
+        s = torch.full((len(parts),), SENTINEL, dtype=torch.int32, device=dev)
+        for k, (a, b, H) in enumerate(parts):
+            if mode == "sync":
+                ev.place_device(ql[a:b], qp[a:b], H, True, out[a:b], dg[a * 40:b * 40])
+            else:
+                ev.place_async(ql[a:b], qp[a:b], H, True, out[a:b], dg[a * 40:b * 40], s[k:k + 1],
+                               spare_rounds=4096)
+        summ = ev.summary()  # settles the asynchronous calls
+        if mode == "async":
+            assert (s.cpu().numpy() == aladdin.ALD_OK).all(), s
+        res.append((out.cpu().numpy(), dg.cpu().numpy(), summ))
+        ev.close()
+    assert np.array_equal(res[0][0], res[1][0])
+    assert np.array_equal(res[0][1], res[1][1])
+    for f in res[0][2]:
+        assert np.array_equal(res[0][2][f], res[1][2][f]), f
