@@ -163,8 +163,12 @@ def catches(tmp_path_factory):
     env = dict(os.environ, PYTHONPATH=root + os.pathsep + os.environ.get("PYTHONPATH", ""), OMP_NUM_THREADS="1")
     env.pop("ORACLE_LIB", None)
 
+    # the directories first, in this thread: pytest's temp factory is not
+    # safe to initialise from several threads at once
+    dirs = [tmp_path_factory.mktemp("mutant%d" % i) for i in range(len(MUTANTS))]
+
     def run(idx):
-        d = tmp_path_factory.mktemp("mutant%d" % idx)
+        d = dirs[idx]
         out = subprocess.run([sys.executable, __file__, str(idx), str(d)], cwd=root, env=env, capture_output=True,
                              text=True, timeout=600)
         if out.returncode != 0:
