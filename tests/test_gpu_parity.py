@@ -576,3 +576,28 @@ def test_sweep_full_size(aladdin):
     # the answer, computed on the device, equals the oracle's
     assert best == (g["min_gpus"], g["min_gpus_scenario"])
     assert aladdin.smallest_feasible_cluster(s.scenarios, rej) == best
+
+
+def test_sorted_layout_arrival_time_heartbeats_match_oracle(aladdin):
+    # one-scenario tiles of 16,384+ queries evaluate in l_pred order; per-query
+    # heartbeats end tiles at arbitrary queries, so chunks come out partial
+    t = wl.make_trace("arrivals-sorted", 29, W=12, R=16, Q=20000, kv_capacity=20000, model=wl.BASE_MODEL, rate=60.0)
+    hb = wl.heartbeats_from_arrivals(t.arrivals, t.model.decode_slo)
+    say("sorted layout, arrival-time heartbeats, iterations", int(hb.sum()))
+    ev = aladdin.Evaluator(0, tile=65536)
+    ev.load_trace(t)
+    r = ev.place(t.q_l_in, t.q_l_pred, hb_before=hb)
+    summ = ev.summary()
+    ev.close()
+    compare(r.worker, r.diag, summ, oracle_hb(t, hb), "arrivals sorted")
+
+
+def test_sorted_layout_decode_history_matches_oracle(aladdin):
+    # constraint (d) takes the commit variants with the decode history
+    t = wl.with_decode_history(wl.make_trace("hist-sorted", 30, W=24, R=24, Q=18000, kv_capacity=20000,
+                                             model=wl.BASE_MODEL), 11)
+    want = ref.place_trace(t)
+    placed = int((want.worker >= 0).sum())
+    say("sorted layout with a decode history, placed", placed)
+    assert 0 < placed < 18000
+    compare(*gpu_place(aladdin, t, tile=65536), want, "history sorted")
