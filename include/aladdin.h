@@ -412,7 +412,10 @@ int ald_worker_summary(ald_handle_t handle, int32_t* B, int64_t* sum_c, int64_t*
  * of the kinds to time (bit k = kind k, 31 = all, 0 = off; anything else
  * outside 0..31 is ALD_EINVAL).  Each timed
  * launch records two events, so time only what is needed.  Totals accumulate
- * over calls while enabled; a nonzero mask resets them. */
+ * over calls while enabled; a nonzero mask resets them.  ald_kernel_time
+ * gives the total and the launches of one kind so far; with launches of
+ * asynchronous calls still timed on the stream it first waits for the stream.
+ * A sweep's kernels are timed the same way (the kinds above). */
 int ald_set_profiling(ald_handle_t handle, int32_t kinds);
 int ald_kernel_time(ald_handle_t handle, int32_t kind, double* total_ms, int64_t* launches);
 
