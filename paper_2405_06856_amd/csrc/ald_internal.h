@@ -15,7 +15,7 @@
 //   request k counted over the requests at or after slot k; it equals the
 //   demand at iteration r_k whenever k is the first of its tie group, and is
 //   below it otherwise), the summaries, kept together in one int4 per slot
-//   (pms = {pme, sm, ss, unused}), are
+//   (pms = {pme, sm, ss, n - k}), are
 //       ss[k]  = sum_{j >= k} s_j                     (ss[n] = 0)
 //       pme[k] = max_{head <= j < k} (P_j + e_j)       (pme[head] = PME_NONE)
 //       sm[k]  = max_{j >= k} P_j                     (sm[n] = NEG)

@@ -106,6 +106,7 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
     int64_t runpm = pmoff;
     for (int k = k0; k < k1; ++k) {
         pms[k].x = runpm == INT64_MIN ? PME_NONE : (int32_t)runpm;
+        pms[k].w = n - k;
         const int64_t P = (int64_t)pms[k].z + (int64_t)(n - k) * e[k];
         const int64_t Pe = P + e[k];
         runpm = Pe > runpm ? Pe : runpm;
@@ -163,10 +164,12 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
         st.peak[gw] = B > 0 ? (int32_t)totP : 0;
         st.rhs[gw] = rhs;
     }
-    // Breakpoint table: a histogram of the remaining lengths r = e - tau of the
-    // live requests (those below LB_MAX), then an exclusive scan, so that entry
-    // v - 1 = number of live requests with r < v.
-    if (B > 0) {
+    // Breakpoint table (only workers the evaluation stages, 0 < B < STAGE_MAX):
+    // a histogram of the remaining lengths r = e - tau of the live requests
+    // (those below LB_MAX), then an exclusive scan, so that entry v - 1 = the
+    // byte offset, within the staged summaries, of the first live slot with
+    // r >= v (16 bytes per slot before it).
+    if (B > 0 && B < STAGE_MAX) {
         __shared__ int32_t hist[LB_MAX];
         for (int v = tid; v < LB_MAX; v += NT) hist[v] = 0;
         __syncthreads();
@@ -175,6 +178,7 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
             if ((uint32_t)r < (uint32_t)LB_MAX) atomicAdd(&hist[r], 1);
         }
         __syncthreads();
+        static_assert((STAGE_MAX - 1) * sizeof(int4) <= 0xFFFF, "byte offsets of staged slots fit 16 bits");
         constexpr int CHV = LB_MAX / NT;  // entries per thread
         int32_t loc = 0;
 #pragma unroll
@@ -185,7 +189,7 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
 #pragma unroll
         for (int j = 0; j < CHV; ++j) {
             run += hist[tid * CHV + j];  // now: requests with r <= tid * CHV + j
-            out[tid * CHV + j] = (uint16_t)run;  // entry v - 1 with v = tid * CHV + j + 1
+            out[tid * CHV + j] = (uint16_t)(run * (int32_t)sizeof(int4));  // entry v - 1, v = tid * CHV + j + 1
         }
     }
     // Integer forms of the latency checks.  Both left sides are rounded fp64
@@ -468,6 +472,8 @@ __device__ __forceinline__ void ex_unpack(uint64_t k, int32_t& ex, int32_t& w)
 // `old` replaced by the wave-uniform `v`.  Through the intrinsic the compiler
 // sees the instruction and inserts whatever wait states its operands need.
 __device__ int ald_writelane(int v, int lane, int old) __asm("llvm.amdgcn.writelane.i32");
+// v_mul_u32_u24: the product of the low 24 bits of each operand (full rate)
+__device__ uint32_t ald_mul_u24(uint32_t a, uint32_t b) __asm("llvm.amdgcn.mul.u24");
 
 // Word `acc` with lane J's value replaced by the wave-uniform `v` (one
 // v_writelane_b32 per half, the lane an inline constant, J < 16).
@@ -563,7 +569,8 @@ struct QRange {
 // Evaluate this thread's queries against one worker and store the wave's bit
 // words (lane j < 2 EVAL_QPT stores word j).  STAGED: breakpoint slot from the block's
 // table and summaries in LDS; else binary search over global memory.  MODE as
-// for launch_eval.
+// for launch_eval.  STAGED requires every l_pred + tau of the block below 2^24
+// (the count-times-end product takes the full-rate 24-bit multiply).
 template <int MODE, bool EX, bool STAGED>
 __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, const WInfo& wi, int w, int32_t tau,
                                             const int32_t (&lin)[EVAL_QPT], const int32_t (&lp)[EVAL_QPT],
@@ -581,20 +588,22 @@ __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, con
     // so that the LDS latencies overlap
     int32_t peak[EVAL_QPT];
     if (STAGED) {
-        int l[EVAL_QPT];
+        int ofs[EVAL_QPT];
         int4 t[EVAL_QPT];
 #pragma unroll
-        for (int m = 0; m < EVAL_QPT; ++m) l[m] = LBs[lp[m] - 1];  // live requests ending before the query
+        for (int m = 0; m < EVAL_QPT; ++m) ofs[m] = LBs[lp[m] - 1];  // byte offset of the first slot ending at or after the query
 #pragma unroll
-        for (int m = 0; m < EVAL_QPT; ++m) t[m] = Ss[l[m]];
+        for (int m = 0; m < EVAL_QPT; ++m) t[m] = *reinterpret_cast<const int4*>(reinterpret_cast<const char*>(Ss) + ofs[m]);
 #pragma unroll
         for (int m = 0; m < EVAL_QPT; ++m) {
             // every candidate below is a KV demand with the query added, so it
             // lies under the worker's peak (<= 2^30) plus l_in + l_pred: 32-bit
-            // wrap-around arithmetic gives it exactly
+            // wrap-around arithmetic gives it exactly (t.w = live slots from
+            // the breakpoint on, below STAGE_MAX)
             const uint32_t sq = (uint32_t)(lin[m] - tau), eq = (uint32_t)(lp[m] + tau);
+            const uint32_t ne = ald_mul_u24((uint32_t)t[m].w, eq);
             const int32_t a = (int32_t)((uint32_t)t[m].x + sq);
-            const int32_t c = (int32_t)((uint32_t)t[m].z + (uint32_t)(B - l[m]) * eq + sq + eq);
+            const int32_t c = (int32_t)((uint32_t)t[m].z + ne + sq + eq);
             const int32_t p = a > t[m].y ? a : t[m].y;
             peak[m] = p > c ? p : c;
         }
@@ -831,7 +840,9 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
     qr.lnmin = block_all<NT>(lnmin, INT64_MAX, OpMin(), red);
     qr.lnmax = block_all<NT>(lnmax, INT64_MIN, OpMax(), red);
     const int L = (int)lpmax;  // table covers v = 0 .. L
-    const bool use_lb = L <= LB_MAX;
+    // staging needs the table to cover every l_pred of the block, and every
+    // eq = l_pred + tau (idle lanes: 1 + tau) below 2^24 for the 24-bit multiply
+    const bool use_lb = L <= LB_MAX && (int64_t)max(L, 1) + tau < ((int64_t)1 << 24);
 
     const int wbeg = wb * sc.wpb;
     const int nw = min(sc.W, wbeg + sc.wpb) - wbeg;
