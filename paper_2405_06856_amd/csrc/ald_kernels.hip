@@ -417,8 +417,10 @@ struct WInfo {
     double rhs;
     int64_t dq_max, ntd_lo, ntd_hi;
     uint64_t ntd_mask, ntt_mask;
-    int32_t head, n, M, lthr, ntt_lo, ntt_hi, ntp_lo, ntp_hi;  // (head, n, M, lthr: one 16-byte read)
+    int32_t head, n, M, lthr;  // (one 16-byte read)
+    int32_t dq32;    // dq_max - the block's smallest qD, clamped to [-1, 2^31 - 1]
     int32_t nt_any;  // some query of the block's chunk may have a near-tie margin with this worker
+    int32_t ntt_lo, ntt_hi, ntp_lo, ntp_hi;
     double dlim;
 };
 
@@ -575,7 +577,7 @@ template <int MODE, bool EX, bool STAGED>
 __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, const WInfo& wi, int w, int32_t tau,
                                             const int32_t (&lin)[EVAL_QPT], const int32_t (&lp)[EVAL_QPT],
                                             const bool (&act)[EVAL_QPT], const uint64_t (&am)[EVAL_QPT],
-                                            int32_t (&e1)[EVAL_QPT],
+                                            const int32_t (&qd)[EVAL_QPT], int32_t (&e1)[EVAL_QPT],
                                             int32_t (&w1)[EVAL_QPT], int32_t (&e2)[EVAL_QPT],
                                             int32_t (&w2)[EVAL_QPT], const uint16_t* LBs, const int4* Ss,
                                             uint64_t* bdst)
@@ -616,12 +618,14 @@ __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, con
         // feasibility from the integer thresholds (the worker's figures read
         // once; no short-circuit, so no branch per query)
         const int32_t M = wi.M, lthr = wi.lthr;
-        const int64_t dq_max = wi.dq_max;
 #pragma unroll
         for (int m = 0; m < EVAL_QPT; ++m) {
-            const int64_t qD = ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m];
+            // constraint (b) as qD <= dq_max: staged, relative to the block's
+            // smallest qD in 32 bits (the block's qD span is below 2^31)
+            const bool bok = STAGED ? qd[m] <= wi.dq32
+                                    : ((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m] <= wi.dq_max;
             // one ballot per compare: each compare's lane mask is its ballot
-            const uint64_t bf = am[m] & ballot(peak[m] <= M) & ballot(qD <= dq_max) & ballot(lin[m] <= lthr);
+            const uint64_t bf = am[m] & ballot(peak[m] <= M) & ballot(bok) & ballot(lin[m] <= lthr);
             bits = put_lane(bits, bf, m);
             if (EX) keep_two<STAGED>(peak[m] - M, w, e1[m], w1[m], e2[m], w2[m]);
         }
@@ -840,9 +844,15 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
     qr.lnmin = block_all<NT>(lnmin, INT64_MAX, OpMin(), red);
     qr.lnmax = block_all<NT>(lnmax, INT64_MIN, OpMax(), red);
     const int L = (int)lpmax;  // table covers v = 0 .. L
-    // staging needs the table to cover every l_pred of the block, and every
-    // eq = l_pred + tau (idle lanes: 1 + tau) below 2^24 for the 24-bit multiply
-    const bool use_lb = L <= LB_MAX && (int64_t)max(L, 1) + tau < ((int64_t)1 << 24);
+    // staging needs the table to cover every l_pred of the block, every
+    // eq = l_pred + tau (idle lanes: 1 + tau) below 2^24 for the 24-bit
+    // multiply, and the block's qD within a 2^31 span
+    const bool use_lb = L <= LB_MAX && (int64_t)max(L, 1) + tau < ((int64_t)1 << 24) &&
+                        qr.qdmax - qr.qdmin < ((int64_t)1 << 31);
+    int32_t qd[QPT];  // qD - the block's smallest (idle lanes: anything; masked)
+#pragma unroll
+    for (int m = 0; m < QPT; ++m)
+        qd[m] = (int32_t)(((int64_t)lin[m] << sc.gs) + (int64_t)sc.gn * lp[m] - qr.qdmin);
 
     const int wbeg = wb * sc.wpb;
     const int nw = min(sc.W, wbeg + sc.wpb) - wbeg;
@@ -859,6 +869,8 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
         x.S2 = cur ? st.S2[gw] : 0;
         x.rhs = st.rhs[gw];
         x.dq_max = st.dq_max[gw];
+        const int64_t dqr = x.dq_max - qr.qdmin;
+        x.dq32 = dqr < 0 ? -1 : (dqr > INT32_MAX ? INT32_MAX : (int32_t)dqr);
         x.ntd_lo = st.ntd_lo[gw];
         x.ntd_hi = st.ntd_hi[gw];
         x.lthr = st.lthr[gw];
@@ -894,14 +906,14 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
         __syncthreads();
         const int nxt = next_staged(Wi, nw, use_lb, cur + 1);
         if (nxt < nw) pf = prefetch_worker(st, Wi[nxt], sc.wbase + wbeg + nxt, tid);
-        eval_worker<MODE, EX, true>(st, sc, Wi[cur], wbeg + cur, tau, lin, lp, act, am, e1, w1, e2, w2, LBs, Ss, bdst);
+        eval_worker<MODE, EX, true>(st, sc, Wi[cur], wbeg + cur, tau, lin, lp, act, am, qd, e1, w1, e2, w2, LBs, Ss, bdst);
         cur = nxt;
     }
     // workers too large to stage: binary search over global memory
     for (int j0 = 0; j0 < nw; ++j0) {
         const WInfo wi = Wi[j0];
         if (use_lb && wi.n - wi.head < STAGE_MAX) continue;
-        eval_worker<MODE, EX, false>(st, sc, wi, wbeg + j0, tau, lin, lp, act, am, e1, w1, e2, w2, LBs, Ss, bdst);
+        eval_worker<MODE, EX, false>(st, sc, wi, wbeg + j0, tau, lin, lp, act, am, qd, e1, w1, e2, w2, LBs, Ss, bdst);
     }
     if (MODE >= 1 && EX) {  // near-tie margins feed only the diagnostics
         for (int j0 = 0; j0 < nw; ++j0)
