@@ -9,7 +9,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libaladdin.so")
-SOURCES = [os.path.join(CSRC, f) for f in ("ald_host.cpp", "ald_kernels.hip", "ald_commit.hip", "ald_commit_d.hip",
+SOURCES = [os.path.join(CSRC, f) for f in ("ald_host.cpp", "ald_kernels.hip", "ald_commit.hip", "ald_commit_c.hip", "ald_commit_d.hip",
+                                                  "ald_commit_dc.hip",
                                                   "ald_rebalance.hip", "ald_move.hip")]
 HEADERS = [os.path.join(CSRC, f) for f in ("ald_internal.h", "ald_device.h", "ald_commit.h", "ald_rebalance.h", "ald_move.h")] + [
     os.path.join(ROOT, "include", "aladdin.h")]

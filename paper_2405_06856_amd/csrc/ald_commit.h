@@ -206,12 +206,21 @@ __device__ __forceinline__ View dagg_view(const DAgg& a, int32_t hb)
 // Per-launch commit state held in LDS.  dag[] mirrors the lanes' DAgg for the
 // per-lane diagnostics of rejected queries (diagnostics only); dw[] and dbits
 // say which workers are dirty.
+// The kernel variant with the LDS copies (CACHE), for scenarios of up to CW
+// workers, also keeps for the untouched-worker scan the tile-start rank keys
+// (read at the tile's first scan) and the last bit row of each kind that a
+// scan read: a later scan of the same 64-query window reads LDS only.
+constexpr int CW = COMMIT_CACHE_W;
 struct CommitLDS {
     DAgg dag[MAX_DIRTY];
     int32_t dw[MAX_DIRTY];
     uint32_t dbits[DBITS_W];
     int32_t he[HOT];
     int32_t hs[HOT];
+    uint64_t ckey[CW];     // tile-start rank keys (valid once kok)
+    uint64_t crow[2][CW];  // bit rows: [0] feasibility, [1] near tie
+    int64_t ctag[2];       // offset of the row held in crow[k] (-1: none)
+    int32_t kok;
 };
 
 // Is worker w (scenario-local) dirty in this tile?  (any lane, any w)
@@ -232,7 +241,7 @@ __device__ __forceinline__ int dirty_lane(const DAgg& a, int w)
 
 // Lowest-index worker at or after `from` that is empty and untouched in this
 // tile (wave-cooperative; -1 if none).  Empty workers have rank key 0.
-__device__ int next_empty_worker(const State& st, const Scen& sc, const CommitLDS& L, int nd, int from)
+__device__ __forceinline__ int next_empty_worker(const State& st, const Scen& sc, const CommitLDS& L, int nd, int from)
 {
     for (int base = from; base < sc.W; base += 64) {
         const int w = base + lane_id();
@@ -274,7 +283,7 @@ __device__ __forceinline__ QView broadcast_q(const QSum& q, int p)
 // Diagnostics of a query with no feasible worker at tile start (so none now),
 // decided by its own lane (diagnostics only: reads the LDS mirror of the dirty
 // workers).
-__device__ Diag reject_diag(const State& st, const Scen& sc, const QSum& q, int i, int start, int w0, int32_t lin,
+__device__ __forceinline__ Diag reject_diag(const State& st, const Scen& sc, const QSum& q, int i, int start, int w0, int32_t lin,
                             int32_t lp, int32_t tau, int32_t hb, const CommitLDS& L, int nd, int hot,
                             const WinBits& wb, int* abort, int* scanned)
 {
@@ -414,39 +423,100 @@ __device__ __forceinline__ int64_t dirty_kv_peak(const State& st, CommitLDS& L, 
 // them the tile-start results are still exact.  With `listed`, only workers of
 // the kind the selection lists (with interchangeable empty workers, the
 // non-empty ones).  The whole wave scans the scenario's bit words and rank
-// keys, sixteen batches of 64 workers at a time; every lane gets (key, worker),
-// worker -1 when there is none.
+// keys, from the LDS copies (kind 0: feasibility, 1: near tie) in the CACHE
+// variant, else from global memory sixteen batches of 64 workers per round
+// trip; every lane gets (key, worker), worker -1 when there is none.
 struct KeyW {
     uint64_t k;
     int32_t w;
 };
-__device__ __forceinline__ KeyW best_untouched(const uint64_t* words, const uint64_t* keys, const CommitLDS* L, int W,
-                                            int nd, int64_t row0, int bit, bool listed, bool uniform_M, bool dpp)
+template <bool CACHE>
+__device__ __forceinline__ KeyW best_untouched(const uint64_t* words, const uint64_t* keys, CommitLDS* L, int W,
+                                            int nd, int64_t row0, int bit, bool listed, bool uniform_M, bool dpp,
+                                            int kind)
 {
     const int lane = lane_id();
-    const uint64_t* row = words + row0;
     uint64_t k = 0;
     int32_t w = -1;
-    for (int b0 = 0; b0 < W; b0 += 64 * 16) {
-        // the words and the rank keys of the batch in one round trip
-        uint64_t wd[16], kd[16];
+    static_assert(CW <= DBITS_W * 32, "the LDS scan reads the dirty bitmap");
+    if (CACHE) {  // (the launch checked W <= CW)
+        // the row (and, at the tile's first scan, the keys) into LDS, sixteen
+        // batches per round trip
+        const bool need_row = L->ctag[kind] != row0, need_keys = L->kok == 0;  // wave-uniform
+        if (need_row || need_keys) {
+            const uint64_t* row = words + row0;
+            for (int b0 = 0; b0 < W; b0 += 64 * 16) {
+                uint64_t wd[16], kd[16];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
-            const int ww = b0 + u * 64 + lane;
-            wd[u] = ww < W ? row[ww] : 0;
-            kd[u] = ww < W ? keys[ww] : 0;
+                for (int u = 0; u < 16; ++u) {
+                    const int ww = b0 + u * 64 + lane;
+                    wd[u] = (need_row && ww < W) ? row[ww] : 0;
+                    kd[u] = (need_keys && ww < W) ? keys[ww] : 0;
+                }
+#pragma unroll
+                for (int u = 0; u < 16; ++u) {
+                    const int ww = b0 + u * 64 + lane;
+                    if (ww < W) {
+                        if (need_row) L->crow[kind][ww] = wd[u];
+                        if (need_keys) L->ckey[ww] = kd[u];
+                    }
+                }
+            }
+            wave_sync();
+            if (lane == 0) {
+                L->ctag[kind] = row0;
+                L->kok = 1;
+            }
+            wave_sync();
         }
+        // each lane its own workers lane + 64 j in increasing index (a later
+        // one replaces only with a larger key), eight per round of LDS reads
+        // (slots up to CW exist; those at or past W are masked)
+        const bool skip_empty = listed && uniform_M;
+        const int nb = (W + 63) / 64;
+        for (int j0 = 0; j0 < nb; j0 += 8) {
+            uint64_t wd[8], kd[8];
+            uint32_t db[8];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
-            const int ww = b0 + u * 64 + lane;
-            bool ok = (wd[u] >> bit) & 1;
-            if (!ballot(ok)) continue;
-            ok = ok && !dirty_w(*L, W, nd, ww);
-            const uint64_t kk = ok ? kd[u] : 0;
-            ok = ok && !(listed && uniform_M && kk == 0);
-            const bool take = ok && ranks_before(kk, ww, k, w);
-            k = take ? kk : k;
-            w = take ? ww : w;
+            for (int u = 0; u < 8; ++u) {
+                const int ww = min((j0 + u) * 64 + lane, CW - 1);
+                wd[u] = L->crow[kind][ww];
+                kd[u] = L->ckey[ww];
+                db[u] = L->dbits[ww >> 5];
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int ww = (j0 + u) * 64 + lane;
+                const bool ok = ww < W && ((wd[u] >> bit) & 1) && !((db[u] >> (ww & 31)) & 1u) &&
+                                !(skip_empty && kd[u] == 0);
+                const bool take = ok && (w < 0 || kd[u] > k);
+                k = take ? kd[u] : k;
+                w = take ? ww : w;
+            }
+        }
+    } else {
+        const uint64_t* row = words + row0;
+        for (int b0 = 0; b0 < W; b0 += 64 * 16) {
+            // the words and the rank keys of the batch in one round trip
+            uint64_t wd[16], kd[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                const int ww = b0 + u * 64 + lane;
+                wd[u] = ww < W ? row[ww] : 0;
+                kd[u] = ww < W ? keys[ww] : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                const int ww = b0 + u * 64 + lane;
+                bool ok = (wd[u] >> bit) & 1;
+                if (!ballot(ok)) continue;
+                ok = ok && !dirty_w(*L, W, nd, ww);
+                const uint64_t kk = ok ? kd[u] : 0;
+                ok = ok && !(listed && uniform_M && kk == 0);
+                const bool take = ok && ranks_before(kk, ww, k, w);
+                k = take ? kk : k;
+                w = take ? ww : w;
+            }
         }
     }
     // the best over the lanes (the largest key, then the lowest index), by
@@ -471,7 +541,8 @@ __device__ __forceinline__ KeyW best_untouched(const uint64_t* words, const uint
 }
 
 // Decide one query with the whole wave.  `a` is this lane's dirty worker.
-__device__ Decision decide(const State& st, const Scen& sc, const QView& q, int i, int start, int w0, int32_t lin,
+template <bool CACHE>
+__device__ __forceinline__ Decision decide(const State& st, const Scen& sc, const QView& q, int i, int start, int w0, int32_t lin,
                            int32_t lp, int32_t tau, int32_t hb, CommitLDS& L, int nd, int hot, int& hotBs,
                            int& hotm, int next_empty, bool want_diag, const WinBits& wb, const DAgg& a, Scan& sn)
 {
@@ -508,9 +579,9 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
     }
     if (!have && q.ncand > TOPK) {  // every listed candidate was committed to: the best untouched one
         const int tp = st.qpos != nullptr ? st.qpos[i - start] : i - start;  // the query's bit position
-        const KeyW c = best_untouched(st.bits_feas, st.key + sc.wbase, &L, sc.W, nd,
+        const KeyW c = best_untouched<CACHE>(st.bits_feas, st.key + sc.wbase, &L, sc.W, nd,
                                       sc.bits_off + (int64_t)(tp >> 6) * sc.W, tp & 63, true,
-                                      sc.uniform_M != 0, !want_diag);
+                                      sc.uniform_M != 0, !want_diag, 0);
         have = c.w >= 0;
         bk = have ? c.k : bk;
         bw = have ? c.w : bw;
@@ -628,9 +699,9 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
             nt = true;
         } else {  // the best near-tie worker was committed to: the best untouched one with a near tie
             const int tp = st.qpos != nullptr ? st.qpos[i - start] : i - start;
-            const KeyW c = best_untouched(st.bits_nt, st.key + sc.wbase, &L, sc.W, nd,
+            const KeyW c = best_untouched<CACHE>(st.bits_nt, st.key + sc.wbase, &L, sc.W, nd,
                                           sc.bits_off + (int64_t)(tp >> 6) * sc.W, tp & 63, false,
-                                          sc.uniform_M != 0, !want_diag);
+                                          sc.uniform_M != 0, !want_diag, 1);
             nt = c.w >= 0 && !ranks_before(bk, bw, c.k, c.w);
             r.fallback = 1;
         }
@@ -671,7 +742,7 @@ __device__ Decision decide(const State& st, const Scen& sc, const QView& q, int 
 // entries ending strictly before it; a tail entry lands after every prefix
 // entry ending no later and after earlier tail entries ending no later.  Whole
 // wave.
-__device__ void writeback_hot(const State& st, CommitLDS& L, DAgg& a, int hot, int Bs, int m, bool mirror)
+__device__ __forceinline__ void writeback_hot(const State& st, CommitLDS& L, DAgg& a, int hot, int Bs, int m, bool mirror)
 {
     const int lane = lane_id();
     const int B = Bs + m;
@@ -720,7 +791,7 @@ __device__ void writeback_hot(const State& st, CommitLDS& L, DAgg& a, int hot, i
     }
 }
 
-template <bool DIAG, bool USE_D>
+template <bool DIAG, bool USE_D, bool CACHE>
 __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
 {
     constexpr int NT = COMMIT_THREADS;
@@ -749,6 +820,11 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
         publish();
         return;
     }
+    if (CACHE && sc.W > CW) {  // the LDS copies hold CW workers (the host never launches this)
+        if (part == 0 && lane == 0) cp->err = DEV_EINVAL;
+        publish();
+        return;
+    }
     const int32_t start = ti.start, end = ti.end;
     const int32_t fpc = min(st.tinfo[s].first_pc[ti.parity & 1], end);  // (no local copy indexed at run time)
 
@@ -762,7 +838,13 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
     __shared__ CommitLDS L;
     if (sc.W <= DBITS_W * 32)
         for (int k = lane; k < (sc.W + 31) / 32; k += NT) L.dbits[k] = 0u;
-    if (lane == 0) cp->rebuild = 0;
+    if (lane == 0) {
+        cp->rebuild = 0;
+        if (CACHE) {
+            L.ctag[0] = L.ctag[1] = -1;
+            L.kok = 0;
+        }
+    }
     wave_sync();
     constexpr bool want_diag = DIAG;  // st.out_diag != nullptr
     int nd = 0;    // dirty workers (wave-uniform); lane j < nd holds the j-th in `a`
@@ -863,7 +945,7 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
             const int32_t plin = rdlane(lin, p), plp = rdlane(lp, p);
             if (next_empty == -2 && qv.efeas) next_empty = next_empty_worker(st, sc, L, nd, next_from);
             Scan sn;
-            const Decision dc = decide(st, sc, qv, ip, start, w0, plin, plp, tau, hb, L, nd, hot, hotBs, hotm,
+            const Decision dc = decide<CACHE>(st, sc, qv, ip, start, w0, plin, plp, tau, hb, L, nd, hot, hotBs, hotm,
                                        next_empty, want_diag, wb, a, sn);
             if (dc.abort) {
                 pos = ip;
@@ -1071,7 +1153,11 @@ __global__ __launch_bounds__(COMMIT_THREADS) void k_commit(State st)
     publish();
 }
 
-// The variants that check constraint (d) (defined in their own unit).
-hipError_t launch_commit_d(const State& st, int32_t blocks, hipStream_t stream);
+// The other variants, each pair in a unit of its own (so that the register
+// allocation of one does not depend on the others): with the LDS copies of
+// the scan; checking constraint (d); both.
+hipError_t launch_commit_c(const State& st, int32_t blocks, hipStream_t stream);
+hipError_t launch_commit_d(const State& st, int32_t blocks, bool cache, hipStream_t stream);
+hipError_t launch_commit_dc(const State& st, int32_t blocks, hipStream_t stream);
 
 }  // namespace ald

@@ -3,11 +3,12 @@
 
 namespace ald {
 
-hipError_t launch_commit_d(const State& st, int32_t blocks, hipStream_t stream)
+hipError_t launch_commit_d(const State& st, int32_t blocks, bool cache, hipStream_t stream)
 {
+    if (cache) return launch_commit_dc(st, blocks, stream);
     const dim3 g(blocks), b(COMMIT_THREADS);
-    if (st.out_diag != nullptr) hipLaunchKernelGGL((k_commit<true, true>), g, b, 0, stream, st);
-    else hipLaunchKernelGGL((k_commit<false, true>), g, b, 0, stream, st);
+    if (st.out_diag != nullptr) hipLaunchKernelGGL((k_commit<true, true, false>), g, b, 0, stream, st);
+    else hipLaunchKernelGGL((k_commit<false, true, false>), g, b, 0, stream, st);
     return hipGetLastError();
 }
 

@@ -40,6 +40,10 @@ struct Arena {
     Scen* dscen = nullptr;
     int eval_mode = 2;    // how the pair evaluation takes the latency checks (launch_eval)
     bool use_d = false;   // some scenario checks constraint (d)
+    // the commit keeps its untouched-worker scan's rows and keys in LDS: one
+    // scenario of at most COMMIT_CACHE_W workers whose tiles heartbeats cut
+    // (short tiles whose queries commit, so that scans repeat within a window)
+    bool commit_cache = false;
     Ctl* hctl = nullptr;  // pinned host copy of the control blocks
     int32_t hctl_n = 0;
     // per scenario: the host copy of its per-query heartbeats during a call
@@ -540,7 +544,7 @@ int launch_round(ald_handle* h, Arena* a, int mode)
     if (mode >= 0) LAUNCH(h, 0, launch_build(a->st, h->stream, mode));
     LAUNCH(h, 1, launch_eval(a->st, a->eval_blocks, a->eval_mode, h->stream));
     LAUNCH(h, 2, launch_select(a->st, a->sel_blocks, h->stream));
-    LAUNCH(h, 3, launch_commit(a->st, a->commit_blocks, a->use_d, h->stream));
+    LAUNCH(h, 3, launch_commit(a->st, a->commit_blocks, a->use_d, a->commit_cache, h->stream));
     return ALD_OK;
 }
 
@@ -661,6 +665,7 @@ int settle(ald_handle* h, bool resume)
         a->st.out_worker = x.st.out_worker;
         a->st.out_diag = x.st.out_diag;
         a->st.call = x.call;
+        a->commit_cache = x.moves && a->S == 1 && a->hW[0] <= COMMIT_CACHE_W;
         std::vector<Ctl> hc(1, c);
         rc = run_rounds(h, a, x.moves, x.moves ? 0 : 1, hc);
         if (rc != ALD_OK) {
@@ -1060,6 +1065,7 @@ int place_stream(ald_handle_t h, int32_t Q, const int32_t* q_l_in, const int32_t
     // first build: every worker after a heartbeat, the last commit round's
     // workers if it changed any (unknown after an asynchronous call), else nothing
     const bool moves = H > 0 || hb_before != nullptr;  // heartbeats can move tau within the call
+    a->commit_cache = moves && a->S == 1 && a->hW[0] <= COMMIT_CACHE_W;
     const bool dirty = h->dirty_pending || !h->issued.empty();
     const int first_mode = (rebuild || moves || h->check_all) ? 0 : (dirty ? 1 : -1);
     if (async) {

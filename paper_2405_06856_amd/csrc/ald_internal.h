@@ -45,6 +45,7 @@ constexpr int COMMIT_THREADS = 64;  // the arrival-order commit runs as one wave
 constexpr int HOT = 8192;          // most request slots per worker (commit keeps one worker in LDS)
 constexpr int BUILD_THREADS = 256;
 constexpr int MAX_DIRTY = 64;      // workers changed within one tile before the tile is cut
+constexpr int COMMIT_CACHE_W = 2048;  // workers of a scenario whose scan rows the commit can keep in LDS
 #ifndef ALD_STALE_CUT
 #define ALD_STALE_CUT 24
 #endif
@@ -285,7 +286,9 @@ hipError_t launch_eval(const State& st, int32_t blocks, int mode, hipStream_t st
 int eval_blocks_per_cu(int mode, bool ex);
 hipError_t launch_select(const State& st, int32_t blocks, hipStream_t stream);
 // use_d: some scenario checks constraint (d)
-hipError_t launch_commit(const State& st, int32_t blocks, bool use_d, hipStream_t stream);
+// cache: the variant that keeps the untouched-worker scan's bit rows and rank
+// keys in LDS (scenarios of at most COMMIT_CACHE_W workers)
+hipError_t launch_commit(const State& st, int32_t blocks, bool use_d, bool cache, hipStream_t stream);
 hipError_t launch_query_stats(const int32_t* lin, const int32_t* lpred, int32_t Q, Ctl* ctl, int32_t S,
                               hipStream_t stream);
 // gate: -1, or the asynchronous call that must have finished for this one to start

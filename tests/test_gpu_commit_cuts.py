@@ -28,6 +28,10 @@ CASES = [
     (40, 3, 4000, 8000, 0, False),
     (64, 1, 4096, 8000, 0, False),
     (64, 1, 4096, 8000, 100, True),
+    # heartbeats cut the tiles: one scenario of at most 2,048 workers takes the
+    # commit variant that keeps the untouched-worker scan's rows in LDS
+    (40, 3, 4000, 8000, 50, False),
+    (130, 2, 4000, 8000, 100, True),
 ]
 
 
@@ -73,6 +77,25 @@ def test_long_tiles_match_oracle(aladdin, case):
     placed = int((want.worker >= 0).sum())
     assert 0 < placed < Q  # the cluster fills up part way through
     compare(got, summ, want, Q, H, diag)
+
+
+@pytest.mark.parametrize("W", [2048, 2049])
+def test_heartbeat_tiles_around_the_lds_copy_limit_match_oracle(aladdin, W):
+    # 2,048 workers: the commit keeps its scan rows in LDS; 2,049: it reads them
+    # from global memory; both must place as the oracle does
+    Q, H = 3000, 100
+    print("heartbeat tiles W", W, "Q", Q, "H", H, flush=True)
+    t = wl.make_trace("lim%d" % W, 8800 + W, W=W, R=1, Q=Q, kv_capacity=1200, model=wl.BASE_MODEL,
+                      in_dist=wl.SHORT_IN, out_dist=wl.SHORT_OUT, rate=200.0)
+    ev = aladdin.Evaluator(0, tile=4096)
+    ev.load_trace(t)
+    got = ev.place(t.q_l_in, t.q_l_pred, heartbeat_every=H, diag=True)
+    st = ev.tile_stats()
+    print("tile statistics", st, flush=True)
+    summ = ev.summary()
+    ev.close()
+    want = ref.place_trace(t, heartbeat_every=H)
+    compare(got, summ, want, Q, H, True)
 
 
 # Integer latency model with narrow bands (k1 > 0, TTFT margin zero where
