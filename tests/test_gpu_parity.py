@@ -197,6 +197,49 @@ def test_arrival_time_heartbeats_match_oracle(aladdin, history):
     compare(np.concatenate(ws), np.concatenate(ds), summ, oracle_hb(t, hb), "arrivals/%s" % history)
 
 
+def test_decode_clock_past_2_24(aladdin):
+    """Once l_pred + tau reaches 2^24 a block leaves the staged evaluation (its
+    24-bit count-times-end product) for the exact path.  One heartbeat entry
+    runs 2^24 - 3,000 decode iterations, then 1,000 run before each query, so
+    the first queries are evaluated staged and the later ones are not."""
+    W, Q = 8, 1500
+    rng = np.random.default_rng(31)
+    t = wl.Trace(name="tau24", seed=0, model=wl.BASE_MODEL, kv_capacity=np.full(W, 4000, np.int64),
+                 res_offsets=np.arange(W + 1, dtype=np.int64), res_l_in=rng.integers(1, 50, W).astype(np.int32),
+                 res_l_pred=rng.integers(1, 50, W).astype(np.int32), res_generated=np.zeros(W, np.int32),
+                 q_l_in=rng.integers(1, 500, Q).astype(np.int32), q_l_pred=rng.integers(1, 900, Q).astype(np.int32),
+                 arrivals=None, heartbeat_every=0)
+    hb = np.full(Q, 1000, np.int32)
+    hb[0] = (1 << 24) - 3000
+    say("decode clock past 2^24: final tau", int(hb.astype(np.int64).sum()))
+    ev = aladdin.Evaluator(0, tile=256)
+    ev.load_trace(t, slots_per_worker=6)  # (slots + 1 times the final tau must stay below 2^27)
+    r = ev.place(t.q_l_in, t.q_l_pred, hb_before=hb)
+    summ = ev.summary()
+    ev.close()
+    want = oracle_hb(t, hb)
+    assert (want.worker >= 0).sum() > Q // 2
+    compare(r.worker, r.diag, summ, want, "tau past 2^24")
+
+
+def test_block_qd_span_past_2_31(aladdin):
+    """gamma = 256 / 2^8: qD = 256 (l_in + l_pred).  A query of l_in = 2^23 among
+    short ones gives its block of 1,024 queries a qD span of at least 2^31, so
+    that block leaves the staged evaluation (32-bit compares relative to the
+    block's smallest qD) for the exact path; the tile's other blocks stay."""
+    model = dataclasses.replace(wl.BASE_MODEL, gamma_num=256, gamma_log2den=8)
+    t = wl.make_trace("qdspan", 41, W=40, R=4, Q=4096, kv_capacity=30000, model=model)
+    ql, qp = t.q_l_in.copy(), t.q_l_pred.copy()
+    ql[100], qp[100] = 1 << 23, 500
+    ql[3000], qp[3000] = (1 << 23) + 5, 700
+    assert 256 * (int(ql[100]) + int(qp[100])) - 256 * int((ql[:1024] + qp[:1024]).min()) >= 1 << 31
+    t = dataclasses.replace(t, q_l_in=ql, q_l_pred=qp)
+    say("qD span past 2^31 in blocks 0 and 2 of 4")
+    want = ref.place_trace(t)
+    assert (want.worker >= 0).sum() > 0 and want.worker[100] == -1 and want.worker[3000] == -1
+    compare(*gpu_place(aladdin, t, tile=4096), want, "qD span")
+
+
 def test_heartbeats_per_query_checked(aladdin):
     t = wl.make_trace("hbbad", 28, W=4, R=2, Q=10, kv_capacity=30000, model=wl.BASE_MODEL)
     ev = aladdin.Evaluator(0)
