@@ -385,11 +385,11 @@ int ald_rebalance(ald_handle_t handle, int32_t P, const int32_t* n_workers, cons
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): the same
  * computation and arguments as ald_rebalance, with every table in a fixed
- * device array of the library (about 600 KB per device, set up by
- * ald_create and held until the process ends) instead of handle memory.  It
- * calls no hipMalloc or hipFree.  out_le and out_be must be given (ALD_EINVAL
- * otherwise); at most 4096 problems and 16383 chunks of ongoing requests (a
- * problem's ongoing requests fill chunks of 2048; ALD_EINVAL beyond).  Every
+ * device array of the library (about 1 MB per device, set up by ald_create
+ * and held until the process ends) instead of handle memory.  It calls no
+ * hipMalloc or hipFree.  out_le and out_be must be given (ALD_EINVAL
+ * otherwise); at most 4096 problems and 32767 chunks of ongoing requests (a
+ * problem's ongoing requests fill chunks of 1024; ALD_EINVAL beyond).  Every
  * call on one device shares that device's array and leaves its contents
  * behind; calls that overlap on one device (other streams or threads) race. */
 int ald_rebalance_noalloc(ald_handle_t handle, int32_t P, const int32_t* n_workers, const ald_model_t* models,

@@ -9,7 +9,7 @@ namespace ald {
 constexpr int RB_WMAX = 4096;     // workers per problem (the error accumulators live in LDS)
 constexpr int RB_JMAX = 8192;     // new requests per problem
 constexpr int RB_ETHREADS = 256;  // threads per error-accumulation block
-constexpr int RB_CHUNK = 2048;    // ongoing requests per error-accumulation block
+constexpr int RB_CHUNK = 1024;    // ongoing requests per error-accumulation block
 constexpr int32_t RB_LEN_MAX = 1 << 24;
 constexpr int RB_WAVES = 4;       // waves per problem in the moves kernel
 
@@ -66,7 +66,7 @@ size_t rb_moves_lds(int32_t wmax, int32_t jmax);
 // tables of at most RB_STATIC_P problems and RB_STATIC_CHUNKS chunks, then the
 // error word.  One copy per device, held until the process ends.
 constexpr int RB_STATIC_P = 4096;
-constexpr int RB_STATIC_CHUNKS = 16384;
+constexpr int RB_STATIC_CHUNKS = 32768;
 constexpr size_t RB_STATIC_TABLES = ((RB_STATIC_P * sizeof(RbProblem) + 255) & ~(size_t)255) +
                                     ((RB_STATIC_CHUNKS * sizeof(RbChunk) + 255) & ~(size_t)255);
 constexpr size_t RB_STATIC_BYTES = RB_STATIC_TABLES + 256;
