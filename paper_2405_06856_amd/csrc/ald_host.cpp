@@ -91,7 +91,7 @@ struct ald_handle {
     // [mode][diagnostics] (compute units x blocks per unit): a placement's
     // evaluation grid is sized to one such wave of blocks, since a partial
     // second wave leaves most of the chip idle
-    int32_t eval_wave[3][2] = {};
+    int32_t eval_wave[EVAL_MODES][2] = {};
     Arena* main = nullptr;
     Arena* sweep = nullptr;  // the arena of the last sweep (in the call part of the workspace)
     int32_t W = 0;
@@ -721,8 +721,8 @@ int ald_create(ald_handle_t* out, int device, void* hip_stream)
     int cus = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess || cus <= 0)
         return ALD_EHIP;
-    int32_t wave[3][2];
-    for (int m = 0; m < 3; ++m)
+    int32_t wave[EVAL_MODES][2];
+    for (int m = 0; m < EVAL_MODES; ++m)
         for (int x = 0; x < 2; ++x) {
             const int per_cu = eval_blocks_per_cu(m, x == 1);
             if (per_cu <= 0) return ALD_EHIP;
@@ -733,7 +733,7 @@ int ald_create(ald_handle_t* out, int device, void* hip_stream)
     ald_handle* h = new ald_handle();
     h->device = device;
     h->stream = (hipStream_t)hip_stream;
-    std::copy(&wave[0][0], &wave[0][0] + 6, &h->eval_wave[0][0]);
+    std::copy(&wave[0][0], &wave[0][0] + 2 * EVAL_MODES, &h->eval_wave[0][0]);
     *out = h;
     return ALD_OK;
 }
@@ -893,6 +893,11 @@ int load_workers(ald_handle_t h, int32_t W, const ald_model_t* model, const int6
     h->main = nullptr;
     h->state_bytes = 0;
     rc = make_arena(h, a, sc, std::vector<int32_t>(1, W), caps, Ms, h->ws, &sb);
+    // workers loaded with more requests than the evaluation stages: the variant
+    // that reads them through their tables (any choice gives the same results)
+    int64_t maxres = 0;
+    for (int i = 0; i < W; ++i) maxres = std::max<int64_t>(maxres, off[i + 1] - off[i]);
+    if (rc == ALD_OK && a->eval_mode == 2 && maxres >= STAGE_MAX) a->eval_mode = 3;
     if (rc == ALD_OK) rc = layout_scratch(h, a, 256, 4096, h->ws + sb + 256, &lb);
     if (rc != ALD_OK) { delete a; return rc; }
     int32_t* err_word = (int32_t*)(h->ws + sb);
@@ -1790,7 +1795,7 @@ int ald_workspace_size(ald_handle_t h, int32_t W, int64_t n_resident, const ald_
     // a placement call of up to Q queries, for any evaluation variant the
     // model can take, with per-query heartbeats
     const int32_t T = std::max(1, std::min(h->tile, Q));
-    for (int m = 0; m < 3; ++m)
+    for (int m = 0; m < EVAL_MODES; ++m)
         for (int x = 0; x < 2; ++x) {
             size_t tb = 0;
             rc = layout_scratch(h, &a, T, h->eval_wave[m][x], nullptr, &tb);

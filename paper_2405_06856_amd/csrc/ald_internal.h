@@ -57,6 +57,7 @@ constexpr int32_t NEG = INT32_MIN;
 // in 32 bits (|sq| < 2^28)
 constexpr int32_t PME_NONE = -(1 << 30);
 constexpr int LB_MAX = 2048;       // l_pred range of a worker's breakpoint table
+constexpr int LB_SLOTS = 4096;     // workers with fewer live requests have a breakpoint table
 
 // error codes raised on the device (mirrors ALD_E* in aladdin.h)
 constexpr int32_t DEV_EINVAL = -1;
@@ -279,7 +280,10 @@ hipError_t launch_ingest(const State& st, int32_t W, const int64_t* res_off, con
 // the last commit; 2: every worker unconditionally
 hipError_t launch_build(const State& st, hipStream_t stream, int mode);
 // mode 0: latency checks in fp64; 1: integer thresholds, near-tie margins in
-// fp64; 2: integer thresholds and near-tie sets
+// fp64; 2: integer thresholds and near-tie sets; 3: as 2, with the workers too
+// large to stage read through their breakpoint tables in global memory (a
+// variant of its own: it holds more registers)
+constexpr int EVAL_MODES = 4;
 hipError_t launch_eval(const State& st, int32_t blocks, int mode, hipStream_t stream);
 // pair-evaluation blocks of the variant launch_eval takes for (mode, ex) that
 // one compute unit holds at once, or 0 if the runtime cannot say

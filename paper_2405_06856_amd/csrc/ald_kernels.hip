@@ -164,12 +164,12 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
         st.peak[gw] = B > 0 ? (int32_t)totP : 0;
         st.rhs[gw] = rhs;
     }
-    // Breakpoint table (only workers the evaluation stages, 0 < B < STAGE_MAX):
-    // a histogram of the remaining lengths r = e - tau of the live requests
-    // (those below LB_MAX), then an exclusive scan, so that entry v - 1 = the
-    // byte offset, within the staged summaries, of the first live slot with
-    // r >= v (16 bytes per slot before it).
-    if (B > 0 && B < STAGE_MAX) {
+    // Breakpoint table (workers with 0 < B < LB_SLOTS): a histogram of the
+    // remaining lengths r = e - tau of the live requests (those below LB_MAX),
+    // then an exclusive scan, so that entry v - 1 = the byte offset, from the
+    // first live slot's summaries, of the first live slot with r >= v (16
+    // bytes per slot before it).
+    if (B > 0 && B < LB_SLOTS) {
         __shared__ int32_t hist[LB_MAX];
         for (int v = tid; v < LB_MAX; v += NT) hist[v] = 0;
         __syncthreads();
@@ -178,7 +178,8 @@ __device__ void build_worker(const State& st, const Scen& sc, int gw, int32_t ta
             if ((uint32_t)r < (uint32_t)LB_MAX) atomicAdd(&hist[r], 1);
         }
         __syncthreads();
-        static_assert((STAGE_MAX - 1) * sizeof(int4) <= 0xFFFF, "byte offsets of staged slots fit 16 bits");
+        static_assert((LB_SLOTS - 1) * sizeof(int4) <= 0xFFFF && STAGE_MAX <= LB_SLOTS,
+                      "byte offsets of the slots fit 16 bits; every staged worker has a table");
         constexpr int CHV = LB_MAX / NT;  // entries per thread
         int32_t loc = 0;
 #pragma unroll
@@ -572,8 +573,10 @@ struct QRange {
 // words (lane j < 2 EVAL_QPT stores word j).  STAGED: breakpoint slot from the block's
 // table and summaries in LDS; else binary search over global memory.  MODE as
 // for launch_eval.  STAGED requires every l_pred + tau of the block below 2^24
-// (the count-times-end product takes the full-rate 24-bit multiply).
-template <int MODE, bool EX, bool STAGED>
+// (the count-times-end product takes the full-rate 24-bit multiply).  TAB: an
+// unstaged worker with a table is read through it from global memory for the
+// queries the table covers (l_pred <= LB_MAX), by a binary search for the rest.
+template <int MODE, bool EX, bool STAGED, bool TAB>
 __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, const WInfo& wi, int w, int32_t tau,
                                             const int32_t (&lin)[EVAL_QPT], const int32_t (&lp)[EVAL_QPT],
                                             const bool (&act)[EVAL_QPT], const uint64_t (&am)[EVAL_QPT],
@@ -608,6 +611,26 @@ __device__ __forceinline__ void eval_worker(const State& st, const Scen& sc, con
             const int32_t c = (int32_t)((uint32_t)t[m].z + ne + sq + eq);
             const int32_t p = a > t[m].y ? a : t[m].y;
             peak[m] = p > c ? p : c;
+        }
+    } else if (TAB && B < LB_SLOTS) {
+        // two dependent reads per query, table entry then summaries (32-bit
+        // wrap-around arithmetic as above, with a full 32-bit multiply); a
+        // query past the table's range searches
+        const uint16_t* tb = st.lbt + (int64_t)(sc.wbase + w) * LB_MAX;
+        int kq[EVAL_QPT];
+#pragma unroll
+        for (int m = 0; m < EVAL_QPT; ++m) kq[m] = (B > 0 && lp[m] <= LB_MAX) ? tb[lp[m] - 1] / (int)sizeof(int4) : 0;
+        int4 t[EVAL_QPT];
+#pragma unroll
+        for (int m = 0; m < EVAL_QPT; ++m) t[m] = v.pms[v.head + kq[m]];
+#pragma unroll
+        for (int m = 0; m < EVAL_QPT; ++m) {
+            const uint32_t sq = (uint32_t)(lin[m] - tau), eq = (uint32_t)(lp[m] + tau);
+            const int32_t a = (int32_t)((uint32_t)t[m].x + sq);
+            const int32_t c = (int32_t)((uint32_t)t[m].z + (uint32_t)t[m].w * eq + sq + eq);
+            const int32_t p = a > t[m].y ? a : t[m].y;
+            peak[m] = p > c ? p : c;
+            if (lp[m] > LB_MAX) peak[m] = (int32_t)kv_peak_with(v, lin[m] - tau, lp[m] + tau);
         }
     } else {
 #pragma unroll
@@ -765,8 +788,8 @@ __device__ __forceinline__ void sort_chunk(const State& st, const Scen& sc, int 
 // one is evaluated.  Workers with B >= STAGE_MAX, or chunks with an l_pred above
 // LB_MAX, take the binary search over global memory instead.  MODE: how the
 // latency checks are taken (launch_eval); EX: the two smallest KV excesses are
-// tracked (diagnostics).
-template <int MODE, bool EX>
+// tracked (diagnostics); TAB: unstaged workers are read through their tables.
+template <int MODE, bool EX, bool TAB = false>
 __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4))) void k_eval(State st)
 {
     constexpr int NT = EVAL_THREADS;
@@ -906,14 +929,16 @@ __global__ __launch_bounds__(EVAL_THREADS) __attribute__((amdgpu_waves_per_eu(4)
         __syncthreads();
         const int nxt = next_staged(Wi, nw, use_lb, cur + 1);
         if (nxt < nw) pf = prefetch_worker(st, Wi[nxt], sc.wbase + wbeg + nxt, tid);
-        eval_worker<MODE, EX, true>(st, sc, Wi[cur], wbeg + cur, tau, lin, lp, act, am, qd, e1, w1, e2, w2, LBs, Ss, bdst);
+        eval_worker<MODE, EX, true, false>(st, sc, Wi[cur], wbeg + cur, tau, lin, lp, act, am, qd, e1, w1, e2, w2,
+                                           LBs, Ss, bdst);
         cur = nxt;
     }
     // workers too large to stage: binary search over global memory
     for (int j0 = 0; j0 < nw; ++j0) {
         const WInfo wi = Wi[j0];
         if (use_lb && wi.n - wi.head < STAGE_MAX) continue;
-        eval_worker<MODE, EX, false>(st, sc, wi, wbeg + j0, tau, lin, lp, act, am, qd, e1, w1, e2, w2, LBs, Ss, bdst);
+        eval_worker<MODE, EX, false, TAB>(st, sc, wi, wbeg + j0, tau, lin, lp, act, am, qd, e1, w1, e2, w2, LBs, Ss,
+                                          bdst);
     }
     if (MODE >= 1 && EX) {  // near-tie margins feed only the diagnostics
         for (int j0 = 0; j0 < nw; ++j0)
@@ -1248,7 +1273,10 @@ hipError_t launch_eval(const State& st, int32_t blocks, int mode, hipStream_t st
 {
     const bool ex = st.out_diag != nullptr;
     const dim3 g(blocks), b(EVAL_THREADS);
-    if (mode == 2) {
+    if (mode == 3) {
+        if (ex) hipLaunchKernelGGL((k_eval<2, true, true>), g, b, 0, stream, st);
+        else hipLaunchKernelGGL((k_eval<2, false, true>), g, b, 0, stream, st);
+    } else if (mode == 2) {
         if (ex) hipLaunchKernelGGL((k_eval<2, true>), g, b, 0, stream, st);
         else hipLaunchKernelGGL((k_eval<2, false>), g, b, 0, stream, st);
     } else if (mode == 1) {
@@ -1263,7 +1291,8 @@ hipError_t launch_eval(const State& st, int32_t blocks, int mode, hipStream_t st
 
 int eval_blocks_per_cu(int mode, bool ex)
 {
-    const void* f = mode == 2 ? (ex ? (const void*)k_eval<2, true> : (const void*)k_eval<2, false>)
+    const void* f = mode == 3 ? (ex ? (const void*)k_eval<2, true, true> : (const void*)k_eval<2, false, true>)
+                  : mode == 2 ? (ex ? (const void*)k_eval<2, true> : (const void*)k_eval<2, false>)
                   : mode == 1 ? (ex ? (const void*)k_eval<1, true> : (const void*)k_eval<1, false>)
                               : (ex ? (const void*)k_eval<0, true> : (const void*)k_eval<0, false>);
     int n = 0;

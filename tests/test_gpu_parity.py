@@ -240,6 +240,23 @@ def test_block_qd_span_past_2_31(aladdin):
     compare(*gpu_place(aladdin, t, tile=4096), want, "qD span")
 
 
+@pytest.mark.parametrize("W,R,cap,dslo,slots", [(12, 900, 850_000, 1.0, 2000), (3, 4100, 3_800_000, 2.0, 5000)])
+def test_workers_too_large_to_stage_match_oracle(aladdin, W, R, cap, dslo, slots):
+    """Workers loaded with at least 768 requests take the evaluation variant
+    that reads unstaged workers through their breakpoint tables in global
+    memory: below 4,096 live requests by table (queries with l_pred past the
+    table's 2,048 by search), from 4,096 on by search; heartbeats retire
+    requests between tiles."""
+    m = dataclasses.replace(wl.BASE_MODEL, ttft_slo=10.0, decode_slo=dslo)
+    t = wl.make_trace("big%d" % R, 90 + R, W=W, R=R, Q=1500, kv_capacity=cap, model=m,
+                      in_dist=(6.0, 1.0, 16, 4096), out_dist=(6.0, 1.0, 16, 4096))
+    assert (t.q_l_pred > 2048).any() and (t.q_l_pred <= 2048).mean() > 0.8
+    say("workers of", R, "requests, largest l_pred", int(t.q_l_pred.max()))
+    want = ref.place_trace(t, heartbeat_every=50)
+    assert 0 < (want.worker >= 0).sum() < t.n_queries
+    compare(*gpu_place(aladdin, t, tile=4096, H=50, slots=slots), want, "big workers %d" % R)
+
+
 def test_heartbeats_per_query_checked(aladdin):
     t = wl.make_trace("hbbad", 28, W=4, R=2, Q=10, kv_capacity=30000, model=wl.BASE_MODEL)
     ev = aladdin.Evaluator(0)
