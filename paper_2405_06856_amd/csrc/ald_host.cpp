@@ -335,9 +335,10 @@ int layout_scratch(ald_handle* h, Arena* a, int32_t T, int32_t target_blocks, ch
     int32_t Wmax = 1;
     for (int s = 0; s < a->S; ++s) Wmax = std::max(Wmax, a->hW[s]);
     int32_t wpb = (int32_t)std::max<int64_t>(1, (NWtot * echunks + target_blocks - 1) / target_blocks);
-    // at most 256 worker blocks per scenario: the selection merges one excess
-    // entry per worker block and query
-    wpb = std::max(wpb, (Wmax + 255) / 256);
+    // at most 512 worker blocks per scenario: the selection merges one excess
+    // entry per worker block and query (for short tiles over many workers the
+    // evaluation's extra blocks outweigh the longer merge up to about there)
+    wpb = std::max(wpb, (Wmax + 511) / 512);
     wpb = std::min(wpb, EVAL_WPB_MAX);
     int64_t bits = 0, part = 0, qs = 0;
     int32_t eb = 0, sb = 0, cb = 0;
