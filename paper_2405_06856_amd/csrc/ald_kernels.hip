@@ -1062,16 +1062,21 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(State st)
     // the group merges its share of the worker blocks' two smallest keys (new
     // first = smaller first; new second = min(larger first, smaller second))
     uint64_t a1 = ~0ull, a2 = ~0ull;
+    auto merge = [&](ulonglong2 p) {
+        const uint64_t lo = p.x < a1 ? p.x : a1;
+        const uint64_t hi = p.x < a1 ? a1 : p.x;
+        const uint64_t s2 = p.y < a2 ? p.y : a2;
+        a1 = lo;
+        a2 = hi < s2 ? hi : s2;
+    };
     if (act && st.out_diag) {
         const ulonglong2* prow = st.part + sc.part_off + slot;
+        if (sc.nblk > 64 * G) {  // many worker blocks (short tiles over many workers): more reads in flight
+#pragma unroll 16
+            for (int b = slice; b < sc.nblk; b += G) merge(prow[(int64_t)b * sc.pstride]);
+        } else {
 #pragma unroll 8
-        for (int b = slice; b < sc.nblk; b += G) {
-            const ulonglong2 p = prow[(int64_t)b * sc.pstride];
-            const uint64_t lo = p.x < a1 ? p.x : a1;
-            const uint64_t hi = p.x < a1 ? a1 : p.x;
-            const uint64_t s2 = p.y < a2 ? p.y : a2;
-            a1 = lo;
-            a2 = hi < s2 ? hi : s2;
+            for (int b = slice; b < sc.nblk; b += G) merge(prow[(int64_t)b * sc.pstride]);
         }
     }
     // merge the group's partial results into its first wave (lists by rank,
